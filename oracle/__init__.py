@@ -1,0 +1,234 @@
+"""fp64 CPU oracle for the seven credit-assignment estimators.
+
+TEST INFRASTRUCTURE ONLY. Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline
+leg of ``bench.py`` may import this package. The GPU library never loads it, and it shares no
+code with the GPU library.
+
+The arithmetic lives in ``rlcs_oracle.c`` (sequential recurrences, one step at a time, in
+fp64). This module only widens the inputs to fp64 and marshals them through ctypes:
+float32 arrays are widened exactly, and uint16 arrays are read as bfloat16 bit patterns and
+widened exactly. Scalar parameters are taken as float32 first (the precision the GPU entry
+points receive) and then widened.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from typing import Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "rlcs_oracle.c")
+_HDR = os.path.join(_HERE, "rlcs_oracle.h")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+__all__ = [
+    "build", "gae", "td_lambda", "discounted", "vtrace", "retrace", "elig_trace",
+    "episodic_prefix", "affine_scan", "widen", "param",
+]
+
+
+def build(force: bool = False) -> str:
+    """Compile ``liboracle.so`` with gcc (plain -O2, no FMA contraction, no fast-math)."""
+    stale = (not os.path.exists(_LIB)
+             or os.path.getmtime(_LIB) < max(os.path.getmtime(_SRC), os.path.getmtime(_HDR)))
+    if force or stale:
+        tmp = _LIB + f".tmp{os.getpid()}"
+        subprocess.check_call(["gcc", "-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math",
+                               "-shared", "-fPIC", "-Wall", "-Werror", "-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        lib = ctypes.CDLL(build())
+        D = ctypes.POINTER(ctypes.c_double)
+        U8 = ctypes.POINTER(ctypes.c_uint8)
+        I64, F64, INT = ctypes.c_int64, ctypes.c_double, ctypes.c_int
+        sigs = {
+            "oracle_gae": [D, D, U8, U8, D, D, D, D, I64, I64, F64, F64],
+            "oracle_td_lambda": [D, D, U8, U8, D, D, D, I64, I64, F64, F64],
+            "oracle_discounted": [D, U8, U8, D, D, D, I64, I64, F64],
+            "oracle_vtrace": [D, D, D, U8, U8, D, D, D, D, I64, I64, F64, F64, F64],
+            "oracle_retrace": [D, D, D, D, U8, U8, D, D, D, D, I64, I64, F64, F64, F64],
+            "oracle_elig_trace": [D, U8, U8, D, I64, I64, F64, F64],
+            "oracle_episodic_prefix": [D, U8, U8, D, I64, I64, INT],
+            "oracle_affine_scan": [D, D, D, D, I64, I64, INT],
+        }
+        for name, argtypes in sigs.items():
+            fn = getattr(lib, name)
+            fn.argtypes = argtypes
+            fn.restype = None
+        _lib = lib
+    return _lib
+
+
+def widen(a) -> Optional[np.ndarray]:
+    """Exact widening to fp64: float32/float64 as is, uint16 as bfloat16 bit patterns."""
+    if a is None:
+        return None
+    a = np.asarray(a)
+    if a.dtype == np.uint16:
+        a = (a.astype(np.uint32) << 16).view(np.float32)
+    if a.dtype not in (np.float32, np.float64):
+        raise TypeError(f"oracle data arrays must be float32, float64 or bf16 bits, got {a.dtype}")
+    return np.ascontiguousarray(a, dtype=np.float64)
+
+
+def param(x: float) -> float:
+    """A scalar parameter as the GPU receives it: rounded to float32, then widened."""
+    return float(np.float32(x))
+
+
+def _flags(f) -> Optional[np.ndarray]:
+    if f is None:
+        return None
+    f = np.asarray(f)
+    if f.dtype == np.bool_:
+        f = f.view(np.uint8)
+    if f.dtype != np.uint8:
+        raise TypeError(f"flag arrays must be uint8 or bool, got {f.dtype}")
+    return np.ascontiguousarray(f)
+
+
+def _ptr(a, ctype):
+    if a is None:
+        return None
+    return a.ctypes.data_as(ctypes.POINTER(ctype))
+
+
+def _shape(a):
+    a = np.asarray(a)
+    if a.ndim != 2:
+        raise ValueError(f"expected a 2-D [N, T] array, got shape {a.shape}")
+    return a.shape
+
+
+def _check(N, T, *arrays):
+    for a in arrays:
+        if a is not None and a.size != N * T:
+            raise ValueError(f"array of size {a.size} does not match [N={N}, T={T}]")
+
+
+def gae(r, v, term=None, trunc=None, bv=None, boot=None, *, gamma, lam):
+    """Returns (advantages, returns), both fp64 [N, T]."""
+    N, T = _shape(r)
+    r, v, bv, boot = widen(r), widen(v), widen(bv), widen(boot)
+    term, trunc = _flags(term), _flags(trunc)
+    _check(N, T, v, term, trunc, bv)
+    if trunc is not None and bv is None:
+        raise ValueError("bv is required when trunc is given")
+    adv = np.empty((N, T)); ret = np.empty((N, T))
+    D, U = ctypes.c_double, ctypes.c_uint8
+    _load().oracle_gae(_ptr(r, D), _ptr(v, D), _ptr(term, U), _ptr(trunc, U), _ptr(bv, D),
+                       _ptr(boot, D), _ptr(adv, D), _ptr(ret, D), N, T,
+                       param(gamma), param(lam))
+    return adv, ret
+
+
+def td_lambda(r, v, term=None, trunc=None, bv=None, boot=None, *, gamma, lam):
+    N, T = _shape(r)
+    r, v, bv, boot = widen(r), widen(v), widen(bv), widen(boot)
+    term, trunc = _flags(term), _flags(trunc)
+    _check(N, T, v, term, trunc, bv)
+    if trunc is not None and bv is None:
+        raise ValueError("bv is required when trunc is given")
+    out = np.empty((N, T))
+    D, U = ctypes.c_double, ctypes.c_uint8
+    _load().oracle_td_lambda(_ptr(r, D), _ptr(v, D), _ptr(term, U), _ptr(trunc, U), _ptr(bv, D),
+                             _ptr(boot, D), _ptr(out, D), N, T, param(gamma), param(lam))
+    return out
+
+
+def discounted(r, term=None, trunc=None, bv=None, boot=None, *, gamma):
+    N, T = _shape(r)
+    r, bv, boot = widen(r), widen(bv), widen(boot)
+    term, trunc = _flags(term), _flags(trunc)
+    _check(N, T, term, trunc, bv)
+    if trunc is not None and bv is None:
+        raise ValueError("bv is required when trunc is given")
+    out = np.empty((N, T))
+    D, U = ctypes.c_double, ctypes.c_uint8
+    _load().oracle_discounted(_ptr(r, D), _ptr(term, U), _ptr(trunc, U), _ptr(bv, D),
+                              _ptr(boot, D), _ptr(out, D), N, T, param(gamma))
+    return out
+
+
+def vtrace(r, v, log_rho, term=None, trunc=None, bv=None, boot=None, *, gamma,
+           rho_bar=1.0, c_bar=1.0):
+    """Returns (vs, pg), both fp64 [N, T]."""
+    N, T = _shape(r)
+    r, v, log_rho, bv, boot = widen(r), widen(v), widen(log_rho), widen(bv), widen(boot)
+    term, trunc = _flags(term), _flags(trunc)
+    _check(N, T, v, log_rho, term, trunc, bv)
+    if trunc is not None and bv is None:
+        raise ValueError("bv is required when trunc is given")
+    vs = np.empty((N, T)); pg = np.empty((N, T))
+    D, U = ctypes.c_double, ctypes.c_uint8
+    _load().oracle_vtrace(_ptr(r, D), _ptr(v, D), _ptr(log_rho, D), _ptr(term, U),
+                          _ptr(trunc, U), _ptr(bv, D), _ptr(boot, D), _ptr(vs, D), _ptr(pg, D),
+                          N, T, param(gamma), param(rho_bar), param(c_bar))
+    return vs, pg
+
+
+def retrace(r, q, eq, log_rho, term=None, trunc=None, bv=None, boot=None, *, gamma, lam,
+            c_bar=1.0):
+    """Returns (delta, q_ret), both fp64 [N, T]."""
+    N, T = _shape(r)
+    r, q, eq, log_rho = widen(r), widen(q), widen(eq), widen(log_rho)
+    bv, boot = widen(bv), widen(boot)
+    term, trunc = _flags(term), _flags(trunc)
+    _check(N, T, q, eq, log_rho, term, trunc, bv)
+    if trunc is not None and bv is None:
+        raise ValueError("bv is required when trunc is given")
+    delta = np.empty((N, T)); q_ret = np.empty((N, T))
+    D, U = ctypes.c_double, ctypes.c_uint8
+    _load().oracle_retrace(_ptr(r, D), _ptr(q, D), _ptr(eq, D), _ptr(log_rho, D),
+                           _ptr(term, U), _ptr(trunc, U), _ptr(bv, D), _ptr(boot, D),
+                           _ptr(delta, D), _ptr(q_ret, D), N, T,
+                           param(gamma), param(lam), param(c_bar))
+    return delta, q_ret
+
+
+def elig_trace(x, term=None, trunc=None, *, gamma, lam):
+    N, T = _shape(x)
+    x = widen(x)
+    term, trunc = _flags(term), _flags(trunc)
+    _check(N, T, term, trunc)
+    out = np.empty((N, T))
+    D, U = ctypes.c_double, ctypes.c_uint8
+    _load().oracle_elig_trace(_ptr(x, D), _ptr(term, U), _ptr(trunc, U), _ptr(out, D), N, T,
+                              param(gamma), param(lam))
+    return out
+
+
+def episodic_prefix(x, term=None, trunc=None, *, boundary="ends_at"):
+    if boundary not in ("ends_at", "starts_at"):
+        raise ValueError(f"boundary must be 'ends_at' or 'starts_at', got {boundary!r}")
+    N, T = _shape(x)
+    x = widen(x)
+    term, trunc = _flags(term), _flags(trunc)
+    _check(N, T, term, trunc)
+    out = np.empty((N, T))
+    D, U = ctypes.c_double, ctypes.c_uint8
+    _load().oracle_episodic_prefix(_ptr(x, D), _ptr(term, U), _ptr(trunc, U), _ptr(out, D),
+                                   N, T, 1 if boundary == "starts_at" else 0)
+    return out
+
+
+def affine_scan(alpha, beta, carry=None, *, reverse=True):
+    N, T = _shape(alpha)
+    alpha, beta, carry = widen(alpha), widen(beta), widen(carry)
+    _check(N, T, beta)
+    out = np.empty((N, T))
+    D = ctypes.c_double
+    _load().oracle_affine_scan(_ptr(alpha, D), _ptr(beta, D), _ptr(carry, D), _ptr(out, D),
+                               N, T, 1 if reverse else 0)
+    return out
