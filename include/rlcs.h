@@ -1,0 +1,183 @@
+/*
+ * rlcs: RL credit-assignment scans for AMD Instinct MI355X (gfx950).
+ *
+ * Seven estimators share one first-order linear recurrence, evaluated independently over every
+ * row of a [N, T] rollout buffer (Section 1, Eq. 1):
+ *     backward:  A_t = alpha_t + beta_t * A_{t+1}      (GAE, V-Trace, Retrace, TD(lambda),
+ *                                                       discounted returns)
+ *     forward:   A_t = alpha_t + beta_t * A_{t-1}      (eligibility traces, episodic prefix sums)
+ * Each entry point builds the per-step coefficients of Table 1 on chip from the raw rollout
+ * tensors, scans them with the associative combine of Eq. 2, and writes its outputs once.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Pointers   All array pointers are DEVICE pointers. Arrays are [N, T] row-major and
+ *            contiguous (element (n, t) at n*T + t) unless stated otherwise; per-row arrays
+ *            are [N]. Data inputs are `const void*` holding `dtype` elements (RLCS_F32: float,
+ *            RLCS_BF16: bfloat16 bit patterns). Outputs are always float32.
+ * Flags      `term` / `trunc` are uint8 [N, T]: nonzero = the episode terminated / was
+ *            truncated after step t (Table 1 caption; d = term OR trunc). A step with both
+ *            set counts as terminated. NULL means no step carries that flag.
+ * bv         Continuation value V(s_{t+1}) of a truncated step (Section 3.2), [N, T], read
+ *            only where trunc is set. Required (non-NULL) exactly when trunc is non-NULL.
+ * boot       Value of the state just past the window, V(s_T) (Section 3.2, window edge), [N];
+ *            NULL means 0 (no bootstrap).
+ * Outputs    Must not overlap any input or each other. An output documented as optional may
+ *            be NULL, in which case it is not written.
+ * Alignment  Every pointer must be aligned to its element size. 16-byte aligned data pointers
+ *            (and 4-byte aligned flag pointers) take the vectorised path; others a slower one.
+ * Sizes      N, T >= 0. N == 0 or T == 0 is a no-op returning RLCS_OK.
+ * Params     Discount gamma and trace parameter lambda must lie in [0, 1]; clipping
+ *            thresholds rho_bar, c_bar must be > 0 (+infinity allowed). NaN is rejected.
+ * Numerics   Arithmetic is float32 (bfloat16 inputs are widened exactly); the scan may
+ *            associate differently from a sequential loop (Proposition 1), so results differ
+ *            from one only by rounding. Results are bitwise reproducible run to run for a
+ *            given shape and variant. Inputs must be finite.
+ * Stream     `stream` is a hipStream_t (NULL = the default stream). Every call only enqueues
+ *            work and returns; outputs are valid once the stream has reached that point.
+ * Workspace  `ws` (optional) is device memory of at least rlcs_workspace_size(N, T) bytes.
+ *            With it, rows much longer than a workgroup's tile are split over several
+ *            workgroups that pass carries to each other through `ws`, which fills the GPU
+ *            when N is small. `ws` must be zero-filled once before its first use; every call
+ *            leaves it ready for the next one. Calls sharing one `ws` must be ordered on one
+ *            stream. With ws == NULL (or ws_bytes too small) the library processes each row
+ *            within one workgroup: same results up to rounding, less parallel.
+ * Memory     The library allocates nothing and keeps no state between calls apart from the
+ *            process-wide variant override below; it is safe to call from several threads.
+ * Errors     Every argument is checked on the host before any HIP call; an error returns a
+ *            status and enqueues nothing. RLCS_ERR_LAUNCH reports a failed kernel launch.
+ */
+#ifndef RLCS_H
+#define RLCS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    RLCS_OK = 0,
+    RLCS_ERR_INVALID_ARG = 1, /* bad size, NULL required pointer, bad parameter or enum */
+    RLCS_ERR_DTYPE = 2,       /* unknown dtype */
+    RLCS_ERR_WORKSPACE = 3,   /* workspace required by the forced variant is missing/too small */
+    RLCS_ERR_LAUNCH = 4       /* the HIP kernel launch failed */
+} rlcs_status;
+
+typedef enum { RLCS_F32 = 0, RLCS_BF16 = 1 } rlcs_dtype;
+
+/* Episodic prefix sum boundary convention (Section 3.3.6). */
+typedef enum {
+    RLCS_ENDS_AT = 0,  /* a flag at t-1 ends the running sum: beta_t = 1 - d_{t-1} */
+    RLCS_STARTS_AT = 1 /* a flag at t starts a new running sum: beta_t = 1 - d_t */
+} rlcs_boundary;
+
+typedef enum { RLCS_BACKWARD = 0, RLCS_FORWARD = 1 } rlcs_direction;
+
+/* hipStream_t, passed as an opaque pointer so that this header needs no HIP headers. */
+typedef void* rlcs_stream_t;
+
+/* Generalized Advantage Estimation (Table 1; Section 3.3.1):
+ *   alpha_t = r_t + gamma * succ(V)_t - V_t,   beta_t = gamma * lambda * (1 - d_t),   A_T = 0,
+ * where succ(V)_t is V_{t+1} inside an episode, bv_t after a truncation, 0 after a termination
+ * and boot[n] at the last step (Section 3.2).
+ *   r, v     [N, T] rewards and values V(s_t), dtype
+ *   adv      [N, T] float32 out: advantages A_t
+ *   ret      [N, T] float32 out, optional: value targets A_t + V_t                            */
+rlcs_status rlcs_gae(const void* r, const void* v, const uint8_t* term, const uint8_t* trunc,
+                     const void* bv, const void* boot, float* adv, float* ret,
+                     int64_t N, int64_t T, float gamma, float lambda, rlcs_dtype dtype,
+                     void* ws, size_t ws_bytes, rlcs_stream_t stream);
+
+/* V-Trace (Table 1; Section 3.3.2), with rho_t = min(rho_bar, exp(log_rho_t)),
+ * c_t = min(c_bar, exp(log_rho_t)):
+ *   alpha_t = rho_t (r_t + gamma succ(V)_t - V_t),  beta_t = gamma c_t (1 - d_t),  Delta_T = 0.
+ *   log_rho  [N, T] log(pi(a_t|s_t) / mu(a_t|s_t)), dtype
+ *   vs       [N, T] float32 out: value targets vs_t = V_t + Delta_t
+ *   pg       [N, T] float32 out, optional: policy-gradient advantages
+ *            rho_t (r_t + gamma succ(vs)_t - V_t), where succ(vs) is vs_{t+1} inside an
+ *            episode and otherwise follows the succ(V) rule above.                            */
+rlcs_status rlcs_vtrace(const void* r, const void* v, const void* log_rho, const uint8_t* term,
+                        const uint8_t* trunc, const void* bv, const void* boot, float* vs,
+                        float* pg, int64_t N, int64_t T, float gamma, float rho_bar, float c_bar,
+                        rlcs_dtype dtype, void* ws, size_t ws_bytes, rlcs_stream_t stream);
+
+/* Retrace(lambda) (Table 1; Section 3.3.3), with c_t = lambda * min(c_bar, exp(log_rho_t)) and
+ * c_T = 0:
+ *   alpha_t = r_t + gamma succ(E_pi Q)_t - Q(s_t, a_t),  beta_t = gamma c_{t+1} (1 - d_t),
+ *   Delta_T = 0.
+ *   q        [N, T] Q(s_t, a_t) of the taken action, dtype
+ *   eq       [N, T] E_{a ~ pi} Q(s_t, a), dtype; boot[n] is E_pi Q(s_T, .) and bv_t is
+ *            E_pi Q of the true successor of a truncated step
+ *   log_rho  [N, T] log(pi(a_t|s_t) / mu(a_t|s_t)), dtype
+ *   delta    [N, T] float32 out: corrections Delta_t
+ *   q_ret    [N, T] float32 out, optional: Retrace targets Q(s_t, a_t) + Delta_t              */
+rlcs_status rlcs_retrace(const void* r, const void* q, const void* eq, const void* log_rho,
+                         const uint8_t* term, const uint8_t* trunc, const void* bv,
+                         const void* boot, float* delta, float* q_ret, int64_t N, int64_t T,
+                         float gamma, float lambda, float c_bar, rlcs_dtype dtype, void* ws,
+                         size_t ws_bytes, rlcs_stream_t stream);
+
+/* TD(lambda) returns (Table 1; Section 3.3.4):
+ *   alpha_t = r_t + gamma (1 - lambda) succ(V)_t,  beta_t = gamma lambda (1 - d_t),  G_T = boot,
+ * except that a truncated step continues with the full discount: alpha_t = r_t + gamma bv_t.
+ *   ret      [N, T] float32 out: lambda-returns G_t                                         */
+rlcs_status rlcs_td_lambda(const void* r, const void* v, const uint8_t* term,
+                           const uint8_t* trunc, const void* bv, const void* boot, float* ret,
+                           int64_t N, int64_t T, float gamma, float lambda, rlcs_dtype dtype,
+                           void* ws, size_t ws_bytes, rlcs_stream_t stream);
+
+/* Discounted returns (Table 1; Section 3.3.4):
+ *   alpha_t = r_t (+ gamma bv_t at a truncated step),  beta_t = gamma (1 - d_t),  G_T = boot.
+ *   ret      [N, T] float32 out: returns G_t                                                */
+rlcs_status rlcs_discounted(const void* r, const uint8_t* term, const uint8_t* trunc,
+                            const void* bv, const void* boot, float* ret, int64_t N, int64_t T,
+                            float gamma, rlcs_dtype dtype, void* ws, size_t ws_bytes,
+                            rlcs_stream_t stream);
+
+/* Eligibility traces, forward (Table 1; Section 3.3.5), one scalar per step:
+ *   z_t = gamma lambda (1 - d_{t-1}) z_{t-1} + x_t,  d_{-1} = 0,  z_{-1} = 0.
+ *   x        [N, T] per-step gradient / feature values, dtype
+ *   z        [N, T] float32 out: traces z_t                                                 */
+rlcs_status rlcs_elig_trace(const void* x, const uint8_t* term, const uint8_t* trunc, float* z,
+                            int64_t N, int64_t T, float gamma, float lambda, rlcs_dtype dtype,
+                            void* ws, size_t ws_bytes, rlcs_stream_t stream);
+
+/* Episodic prefix sum, forward (Table 1; Section 3.3.6):
+ *   RLCS_ENDS_AT:   C_t = x_t + (1 - d_{t-1}) C_{t-1};  RLCS_STARTS_AT: C_t = x_t + (1 - d_t) C_{t-1};
+ *   C_{-1} = 0.
+ *   c        [N, T] float32 out: running sums C_t                                            */
+rlcs_status rlcs_episodic_prefix(const void* x, const uint8_t* term, const uint8_t* trunc,
+                                 float* c, int64_t N, int64_t T, rlcs_boundary boundary,
+                                 rlcs_dtype dtype, void* ws, size_t ws_bytes,
+                                 rlcs_stream_t stream);
+
+/* The bare recurrence with caller-supplied coefficients (the generic scan of Section 4.1):
+ *   RLCS_BACKWARD: out_t = alpha_t + beta_t out_{t+1}, out_T = carry[n];
+ *   RLCS_FORWARD:  out_t = alpha_t + beta_t out_{t-1}, out_{-1} = carry[n].
+ *   alpha, beta [N, T] dtype; carry [N] dtype, optional (NULL = 0); out [N, T] float32.     */
+rlcs_status rlcs_affine_scan(const void* alpha, const void* beta, const void* carry, float* out,
+                             int64_t N, int64_t T, rlcs_direction direction, rlcs_dtype dtype,
+                             void* ws, size_t ws_bytes, rlcs_stream_t stream);
+
+/* Bytes of workspace that let any entry point above split rows of an [N, T] call over
+ * several workgroups (0 if no split can be needed). */
+size_t rlcs_workspace_size(int64_t N, int64_t T);
+
+/* Static description of a status code. Never NULL. */
+const char* rlcs_status_string(rlcs_status status);
+
+/* Library version as major * 10000 + minor * 100 + patch. */
+int rlcs_version(void);
+
+/* Kernel-variant override, process-wide, for tests and benchmarks: 0 = automatic choice,
+ * 1 = whole rows per workgroup, 2 = rows split across workgroups (needs the workspace).
+ * Not thread-safe with concurrent calls. Returns RLCS_ERR_INVALID_ARG for other values. */
+rlcs_status rlcs_set_variant_override(int variant);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RLCS_H */

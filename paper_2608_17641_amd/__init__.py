@@ -1,0 +1,238 @@
+"""rlcs: RL credit-assignment scans for AMD MI355X (gfx950).
+
+Thin PyTorch binding over the C ABI of ``include/rlcs.h``: every function below checks its
+tensors, passes their device pointers, sizes and the current HIP stream to the function of the
+same name in ``librlcs.so``, and returns the output tensors. All arithmetic runs in the HIP
+kernels; there is no other code path.
+
+Tensors: data inputs are ``[N, T]`` contiguous float32 or bfloat16 (all of one call share the
+dtype), flags are ``[N, T]`` uint8 or bool, ``boot`` / ``carry`` are ``[N]`` of the data dtype,
+outputs are float32 ``[N, T]`` (allocated when not given). All tensors must live on the same
+GPU. ``ws`` is an optional zero-initialised uint8 workspace (see ``make_workspace``).
+"""
+from __future__ import annotations
+
+from typing import Optional, Tuple
+
+import torch
+
+from . import _native
+from ._native import RlcsError
+
+__all__ = [
+    "rlcs_gae", "rlcs_vtrace", "rlcs_retrace", "rlcs_td_lambda", "rlcs_discounted",
+    "rlcs_elig_trace", "rlcs_episodic_prefix", "rlcs_affine_scan", "rlcs_workspace_size",
+    "rlcs_version", "rlcs_set_variant_override", "make_workspace", "RlcsError",
+]
+
+_DTYPES = {torch.float32: _native.RLCS_F32, torch.bfloat16: _native.RLCS_BF16}
+
+
+def _dev(t: torch.Tensor) -> torch.device:
+    return t.device
+
+
+def _check_data(name, t, N, T, dtype, device, shape=None):
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    exp = shape if shape is not None else (N, T)
+    if tuple(t.shape) != tuple(exp):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(exp)}")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} has dtype {t.dtype}, expected {dtype} like the other data inputs")
+    if t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t
+
+
+def _check_flags(name, t, N, T, device):
+    if t is None:
+        return None
+    if t.dtype not in (torch.uint8, torch.bool):
+        raise TypeError(f"{name} must be uint8 or bool, got {t.dtype}")
+    if tuple(t.shape) != (N, T):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {(N, T)}")
+    if t.device != device or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous tensor on {device}")
+    return t
+
+
+def _out(name, t, N, T, device):
+    if t is None:
+        return torch.empty((N, T), dtype=torch.float32, device=device)
+    if t.dtype != torch.float32 or tuple(t.shape) != (N, T) or t.device != device \
+            or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous float32 [N, T] tensor on {device}")
+    return t
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else t.data_ptr()
+
+
+def _ws(ws: Optional[torch.Tensor], device):
+    if ws is None:
+        return None, 0
+    if ws.device != device or not ws.is_contiguous():
+        raise ValueError(f"ws must be a contiguous tensor on {device}")
+    return ws.data_ptr(), ws.numel() * ws.element_size()
+
+
+def _prep(x: torch.Tensor):
+    if not isinstance(x, torch.Tensor) or x.dim() != 2:
+        raise ValueError("data inputs must be 2-D [N, T] tensors")
+    if x.dtype not in _DTYPES:
+        raise TypeError(f"data inputs must be float32 or bfloat16, got {x.dtype}")
+    if x.device.type != "cuda":
+        raise ValueError("tensors must be on a GPU")
+    N, T = x.shape
+    return int(N), int(T), x.dtype, x.device
+
+
+def _stream(device):
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def _call(fn: str, *args):
+    code = getattr(_native.load(), fn)(*args)
+    if code != _native.RLCS_OK:
+        raise RlcsError(fn, code)
+
+
+def make_workspace(N: int, T: int, device) -> torch.Tensor:
+    """Zero-filled workspace for calls of shape [N, T] (lets long rows span workgroups)."""
+    n = int(_native.load().rlcs_workspace_size(int(N), int(T)))
+    return torch.zeros(max(n, 64), dtype=torch.uint8, device=device)
+
+
+def rlcs_workspace_size(N: int, T: int) -> int:
+    return int(_native.load().rlcs_workspace_size(int(N), int(T)))
+
+
+def rlcs_version() -> int:
+    return int(_native.load().rlcs_version())
+
+
+def rlcs_set_variant_override(variant: int) -> None:
+    _call("rlcs_set_variant_override", int(variant))
+
+
+def rlcs_gae(r, v, term=None, trunc=None, bv=None, boot=None, adv=None, ret=None, *,
+             gamma: float, lam: float, ws=None, want_ret: bool = True) -> Tuple[torch.Tensor, Optional[torch.Tensor]]:
+    N, T, dt, dev = _prep(r)
+    _check_data("v", v, N, T, dt, dev); _check_data("bv", bv, N, T, dt, dev)
+    _check_data("boot", boot, N, T, dt, dev, shape=(N,))
+    _check_flags("term", term, N, T, dev); _check_flags("trunc", trunc, N, T, dev)
+    adv = _out("adv", adv, N, T, dev)
+    ret = _out("ret", ret, N, T, dev) if (want_ret or ret is not None) else None
+    wp, wb = _ws(ws, dev)
+    with torch.cuda.device(dev):
+        _call("rlcs_gae", _ptr(r), _ptr(v), _ptr(term), _ptr(trunc), _ptr(bv), _ptr(boot),
+              _ptr(adv), _ptr(ret), N, T, gamma, lam, _DTYPES[dt], wp, wb, _stream(dev))
+    return adv, ret
+
+
+def rlcs_vtrace(r, v, log_rho, term=None, trunc=None, bv=None, boot=None, vs=None, pg=None, *,
+                gamma: float, rho_bar: float = 1.0, c_bar: float = 1.0, ws=None,
+                want_pg: bool = True):
+    N, T, dt, dev = _prep(r)
+    _check_data("v", v, N, T, dt, dev); _check_data("log_rho", log_rho, N, T, dt, dev)
+    _check_data("bv", bv, N, T, dt, dev); _check_data("boot", boot, N, T, dt, dev, shape=(N,))
+    _check_flags("term", term, N, T, dev); _check_flags("trunc", trunc, N, T, dev)
+    vs = _out("vs", vs, N, T, dev)
+    pg = _out("pg", pg, N, T, dev) if (want_pg or pg is not None) else None
+    wp, wb = _ws(ws, dev)
+    with torch.cuda.device(dev):
+        _call("rlcs_vtrace", _ptr(r), _ptr(v), _ptr(log_rho), _ptr(term), _ptr(trunc), _ptr(bv),
+              _ptr(boot), _ptr(vs), _ptr(pg), N, T, gamma, rho_bar, c_bar, _DTYPES[dt], wp, wb,
+              _stream(dev))
+    return vs, pg
+
+
+def rlcs_retrace(r, q, eq, log_rho, term=None, trunc=None, bv=None, boot=None, delta=None,
+                 q_ret=None, *, gamma: float, lam: float, c_bar: float = 1.0, ws=None,
+                 want_q_ret: bool = True):
+    N, T, dt, dev = _prep(r)
+    for name, t in (("q", q), ("eq", eq), ("log_rho", log_rho), ("bv", bv)):
+        _check_data(name, t, N, T, dt, dev)
+    _check_data("boot", boot, N, T, dt, dev, shape=(N,))
+    _check_flags("term", term, N, T, dev); _check_flags("trunc", trunc, N, T, dev)
+    delta = _out("delta", delta, N, T, dev)
+    q_ret = _out("q_ret", q_ret, N, T, dev) if (want_q_ret or q_ret is not None) else None
+    wp, wb = _ws(ws, dev)
+    with torch.cuda.device(dev):
+        _call("rlcs_retrace", _ptr(r), _ptr(q), _ptr(eq), _ptr(log_rho), _ptr(term), _ptr(trunc),
+              _ptr(bv), _ptr(boot), _ptr(delta), _ptr(q_ret), N, T, gamma, lam, c_bar,
+              _DTYPES[dt], wp, wb, _stream(dev))
+    return delta, q_ret
+
+
+def rlcs_td_lambda(r, v, term=None, trunc=None, bv=None, boot=None, ret=None, *, gamma: float,
+                   lam: float, ws=None) -> torch.Tensor:
+    N, T, dt, dev = _prep(r)
+    _check_data("v", v, N, T, dt, dev); _check_data("bv", bv, N, T, dt, dev)
+    _check_data("boot", boot, N, T, dt, dev, shape=(N,))
+    _check_flags("term", term, N, T, dev); _check_flags("trunc", trunc, N, T, dev)
+    ret = _out("ret", ret, N, T, dev)
+    wp, wb = _ws(ws, dev)
+    with torch.cuda.device(dev):
+        _call("rlcs_td_lambda", _ptr(r), _ptr(v), _ptr(term), _ptr(trunc), _ptr(bv), _ptr(boot),
+              _ptr(ret), N, T, gamma, lam, _DTYPES[dt], wp, wb, _stream(dev))
+    return ret
+
+
+def rlcs_discounted(r, term=None, trunc=None, bv=None, boot=None, ret=None, *, gamma: float,
+                    ws=None) -> torch.Tensor:
+    N, T, dt, dev = _prep(r)
+    _check_data("bv", bv, N, T, dt, dev); _check_data("boot", boot, N, T, dt, dev, shape=(N,))
+    _check_flags("term", term, N, T, dev); _check_flags("trunc", trunc, N, T, dev)
+    ret = _out("ret", ret, N, T, dev)
+    wp, wb = _ws(ws, dev)
+    with torch.cuda.device(dev):
+        _call("rlcs_discounted", _ptr(r), _ptr(term), _ptr(trunc), _ptr(bv), _ptr(boot), _ptr(ret),
+              N, T, gamma, _DTYPES[dt], wp, wb, _stream(dev))
+    return ret
+
+
+def rlcs_elig_trace(x, term=None, trunc=None, z=None, *, gamma: float, lam: float,
+                    ws=None) -> torch.Tensor:
+    N, T, dt, dev = _prep(x)
+    _check_flags("term", term, N, T, dev); _check_flags("trunc", trunc, N, T, dev)
+    z = _out("z", z, N, T, dev)
+    wp, wb = _ws(ws, dev)
+    with torch.cuda.device(dev):
+        _call("rlcs_elig_trace", _ptr(x), _ptr(term), _ptr(trunc), _ptr(z), N, T, gamma, lam,
+              _DTYPES[dt], wp, wb, _stream(dev))
+    return z
+
+
+def rlcs_episodic_prefix(x, term=None, trunc=None, c=None, *, boundary: str = "ends_at",
+                         ws=None) -> torch.Tensor:
+    N, T, dt, dev = _prep(x)
+    if boundary not in ("ends_at", "starts_at"):
+        raise ValueError(f"boundary must be 'ends_at' or 'starts_at', got {boundary!r}")
+    _check_flags("term", term, N, T, dev); _check_flags("trunc", trunc, N, T, dev)
+    c = _out("c", c, N, T, dev)
+    wp, wb = _ws(ws, dev)
+    b = _native.RLCS_STARTS_AT if boundary == "starts_at" else _native.RLCS_ENDS_AT
+    with torch.cuda.device(dev):
+        _call("rlcs_episodic_prefix", _ptr(x), _ptr(term), _ptr(trunc), _ptr(c), N, T, b,
+              _DTYPES[dt], wp, wb, _stream(dev))
+    return c
+
+
+def rlcs_affine_scan(alpha, beta, carry=None, out=None, *, reverse: bool = True,
+                     ws=None) -> torch.Tensor:
+    N, T, dt, dev = _prep(alpha)
+    _check_data("beta", beta, N, T, dt, dev); _check_data("carry", carry, N, T, dt, dev, shape=(N,))
+    out = _out("out", out, N, T, dev)
+    wp, wb = _ws(ws, dev)
+    d = _native.RLCS_BACKWARD if reverse else _native.RLCS_FORWARD
+    with torch.cuda.device(dev):
+        _call("rlcs_affine_scan", _ptr(alpha), _ptr(beta), _ptr(carry), _ptr(out), N, T, d,
+              _DTYPES[dt], wp, wb, _stream(dev))
+    return out

@@ -1,0 +1,78 @@
+"""ctypes view of the C ABI declared in include/rlcs.h (librlcs.so, built in-tree).
+
+Loading fails loudly when the library has not been built: there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+from .build import LIB
+
+RLCS_OK = 0
+RLCS_ERR_INVALID_ARG = 1
+RLCS_ERR_DTYPE = 2
+RLCS_ERR_WORKSPACE = 3
+RLCS_ERR_LAUNCH = 4
+
+RLCS_F32 = 0
+RLCS_BF16 = 1
+
+RLCS_ENDS_AT = 0
+RLCS_STARTS_AT = 1
+
+RLCS_BACKWARD = 0
+RLCS_FORWARD = 1
+
+_P = ctypes.c_void_p
+_I64 = ctypes.c_int64
+_F = ctypes.c_float
+_INT = ctypes.c_int
+_SZ = ctypes.c_size_t
+
+# name -> argtypes, in the order of include/rlcs.h
+PROTOTYPES = {
+    "rlcs_gae": [_P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _F, _F, _INT, _P, _SZ, _P],
+    "rlcs_vtrace": [_P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _F, _F, _F, _INT, _P, _SZ, _P],
+    "rlcs_retrace": [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _F, _F, _F, _INT, _P, _SZ,
+                     _P],
+    "rlcs_td_lambda": [_P, _P, _P, _P, _P, _P, _P, _I64, _I64, _F, _F, _INT, _P, _SZ, _P],
+    "rlcs_discounted": [_P, _P, _P, _P, _P, _P, _I64, _I64, _F, _INT, _P, _SZ, _P],
+    "rlcs_elig_trace": [_P, _P, _P, _P, _I64, _I64, _F, _F, _INT, _P, _SZ, _P],
+    "rlcs_episodic_prefix": [_P, _P, _P, _P, _I64, _I64, _INT, _INT, _P, _SZ, _P],
+    "rlcs_affine_scan": [_P, _P, _P, _P, _I64, _I64, _INT, _INT, _P, _SZ, _P],
+    "rlcs_workspace_size": [_I64, _I64],
+    "rlcs_status_string": [_INT],
+    "rlcs_version": [],
+    "rlcs_set_variant_override": [_INT],
+}
+RESTYPES = {"rlcs_workspace_size": _SZ, "rlcs_status_string": ctypes.c_char_p}
+
+_lib = None
+
+
+def load() -> ctypes.CDLL:
+    """The loaded librlcs.so with prototypes set. Raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB):
+            raise RuntimeError(
+                f"{LIB} is missing: build it first (python -m paper_2608_17641_amd.build "
+                "or __graft_entry__.build())")
+        lib = ctypes.CDLL(LIB)
+        for name, argtypes in PROTOTYPES.items():
+            fn = getattr(lib, name)
+            fn.argtypes = argtypes
+            fn.restype = RESTYPES.get(name, _INT)
+        _lib = lib
+    return _lib
+
+
+def status_string(code: int) -> str:
+    return load().rlcs_status_string(code).decode()
+
+
+class RlcsError(RuntimeError):
+    def __init__(self, fn: str, code: int):
+        super().__init__(f"{fn} returned {code}: {status_string(code)}")
+        self.code = code

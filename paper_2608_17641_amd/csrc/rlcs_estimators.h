@@ -1,0 +1,349 @@
+// Per-estimator coefficient builders (Table 1 with the boundary rules of Section 3.2) and
+// epilogues. Each policy describes:
+//   kBackward   direction of its recurrence (Section 1, Eq. 1);
+//   kSlots      number of [N, T] data inputs it reads (Args::in[0 .. kSlots-1]);
+//   slot_used   whether slot s is read (the truncation continuation only with truncation);
+//   kFlags      whether it reads term / trunc;
+//   kRowValue   whether it reads the per-row value (bootstrap or carry) at the row edge;
+//   kNbr        number of values it needs from the neighbouring step on the carry-source side
+//               (exported by that step's lane, or loaded from memory at a lane edge);
+//   build       alpha_k, beta_k of the lane's K steps;
+//   finish      the outputs of the K steps given the scanned values A_k and X, the scanned
+//               value just past the lane on the carry-source side.
+//
+// Row edges are folded into the coefficients so that one segmented scan runs over the flat
+// [N*T] array: at the last step of a row (backward) or the first (forward) beta is 0, and a
+// nonzero carry A_T (or z_{-1}) enters alpha as beta * carry, which equals adding
+// decay_product * carry after the scan (Section 4.1, step 4).
+#pragma once
+
+#include "rlcs_device.h"
+
+namespace rlcs {
+
+struct Params {
+    float gamma, lambda, rho_bar, c_bar;
+};
+
+struct Args {
+    const void* in[5];     // data inputs, meaning fixed by the policy
+    const uint8_t* term;   // [N, T] or null
+    const uint8_t* trunc;  // [N, T] or null
+    const void* row_value; // [N] bootstrap / carry, or null (= 0)
+    float* out0;
+    float* out1;           // may be null
+    Params p;
+    int64_t N, T;
+    void* ws;              // cross-workgroup carry records (split-row variant only)
+};
+
+// Bit helpers over K-bit masks.
+__device__ __forceinline__ bool bit(uint32_t m, int k) { return (m >> k) & 1u; }
+
+// Successor value of step k as Section 3.2 defines it: 0 after a termination, the supplied
+// continuation after a truncation, the row bootstrap at the window edge, else the next
+// step's value.
+__device__ __forceinline__ float successor(bool term, bool trunc, bool edge, float bv, float B,
+                                           float next) {
+    return term ? 0.f : (trunc ? bv : (edge ? B : next));
+}
+
+// ---------------------------------------------------------------- GAE (Section 3.3.1)
+// in: r, v, bv
+struct GaeOp {
+    static constexpr bool kBackward = true;
+    static constexpr int kSlots = 3;
+    static constexpr bool kFlags = true, kRowValue = true;
+    static constexpr int kNbr = 1;  // V of the next step
+    static constexpr bool slot_used(int s, bool trunc) { return s < 2 || trunc; }
+
+    template <int K>
+    __device__ static void nbr_export(const Params&, const float (&d)[kSlots][K], uint32_t, float (&nb)[kNbr]) {
+        nb[0] = d[1][0];
+    }
+    template <typename DT>
+    __device__ static void nbr_load(const Args& a, int64_t p, float (&nb)[kNbr]) {
+        nb[0] = load_one<DT>(a.in[1], p);
+    }
+    template <int K, bool TR>
+    __device__ static void build(const Params& P, const float (&d)[kSlots][K], uint32_t term,
+                                 uint32_t trunc, uint32_t edge, const float (&B)[K],
+                                 const float (&nb)[kNbr], float (&al)[K], float (&be)[K]) {
+        const float gl = P.gamma * P.lambda;
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+            const bool te = bit(term, k), tr = TR && bit(trunc, k), ed = bit(edge, k);
+            const float next = (k + 1 < K) ? d[1][k + 1] : nb[0];
+            const float s = successor(te, tr, ed, TR ? d[2][k] : 0.f, B[k], next);
+            al[k] = fmaf(P.gamma, s, d[0][k]) - d[1][k];
+            be[k] = (te || tr || ed) ? 0.f : gl;
+        }
+    }
+    template <int K, bool TR>
+    __device__ static void finish(const Params&, const float (&d)[kSlots][K], uint32_t, uint32_t,
+                                  uint32_t, const float (&)[K], const float (&)[kNbr],
+                                  const float (&A)[K], float, float (&o0)[K], float (&o1)[K]) {
+#pragma unroll
+        for (int k = 0; k < K; ++k) { o0[k] = A[k]; o1[k] = A[k] + d[1][k]; }
+    }
+};
+
+// ---------------------------------------------------------------- V-Trace (Section 3.3.2)
+// in: r, v, log_rho, bv
+struct VtraceOp {
+    static constexpr bool kBackward = true;
+    static constexpr int kSlots = 4;
+    static constexpr bool kFlags = true, kRowValue = true;
+    static constexpr int kNbr = 1;  // V of the next step
+    static constexpr bool slot_used(int s, bool trunc) { return s < 3 || trunc; }
+
+    template <int K>
+    __device__ static void nbr_export(const Params&, const float (&d)[kSlots][K], uint32_t, float (&nb)[kNbr]) {
+        nb[0] = d[1][0];
+    }
+    template <typename DT>
+    __device__ static void nbr_load(const Args& a, int64_t p, float (&nb)[kNbr]) {
+        nb[0] = load_one<DT>(a.in[1], p);
+    }
+    template <int K, bool TR>
+    __device__ static void build(const Params& P, const float (&d)[kSlots][K], uint32_t term,
+                                 uint32_t trunc, uint32_t edge, const float (&B)[K],
+                                 const float (&nb)[kNbr], float (&al)[K], float (&be)[K]) {
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+            const bool te = bit(term, k), tr = TR && bit(trunc, k), ed = bit(edge, k);
+            const float ratio = __expf(d[2][k]);
+            const float rho = fminf(P.rho_bar, ratio);
+            const float c = fminf(P.c_bar, ratio);
+            const float next = (k + 1 < K) ? d[1][k + 1] : nb[0];
+            const float s = successor(te, tr, ed, TR ? d[3][k] : 0.f, B[k], next);
+            al[k] = rho * (fmaf(P.gamma, s, d[0][k]) - d[1][k]);
+            be[k] = (te || tr || ed) ? 0.f : P.gamma * c;
+        }
+    }
+    template <int K, bool TR>
+    __device__ static void finish(const Params& P, const float (&d)[kSlots][K], uint32_t term,
+                                  uint32_t trunc, uint32_t edge, const float (&B)[K],
+                                  const float (&nb)[kNbr], const float (&A)[K], float X,
+                                  float (&o0)[K], float (&o1)[K]) {
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+            const bool te = bit(term, k), tr = TR && bit(trunc, k), ed = bit(edge, k);
+            const float rho = fminf(P.rho_bar, __expf(d[2][k]));
+            // vs of the next step: V_{t+1} + Delta_{t+1}
+            const float vs_next = (k + 1 < K) ? d[1][k + 1] + A[k + 1] : nb[0] + X;
+            const float s = successor(te, tr, ed, TR ? d[3][k] : 0.f, B[k], vs_next);
+            o0[k] = d[1][k] + A[k];
+            o1[k] = rho * (fmaf(P.gamma, s, d[0][k]) - d[1][k]);
+        }
+    }
+};
+
+// ---------------------------------------------------------------- Retrace (Section 3.3.3)
+// in: r, q, eq, log_rho, bv
+struct RetraceOp {
+    static constexpr bool kBackward = true;
+    static constexpr int kSlots = 5;
+    static constexpr bool kFlags = true, kRowValue = true;
+    static constexpr int kNbr = 2;  // E_pi Q and c of the next step
+    static constexpr bool slot_used(int s, bool trunc) { return s < 4 || trunc; }
+
+    __device__ static float trace(const Params& P, float log_rho) {
+        return P.lambda * fminf(P.c_bar, __expf(log_rho));
+    }
+    template <int K>
+    __device__ static void nbr_export(const Params& P, const float (&d)[kSlots][K], uint32_t, float (&nb)[kNbr]) {
+        nb[0] = d[2][0];
+        nb[1] = trace(P, d[3][0]);
+    }
+    template <typename DT>
+    __device__ static void nbr_load(const Args& a, int64_t p, float (&nb)[kNbr]) {
+        nb[0] = load_one<DT>(a.in[2], p);
+        nb[1] = trace(a.p, load_one<DT>(a.in[3], p));
+    }
+    template <int K, bool TR>
+    __device__ static void build(const Params& P, const float (&d)[kSlots][K], uint32_t term,
+                                 uint32_t trunc, uint32_t edge, const float (&B)[K],
+                                 const float (&nb)[kNbr], float (&al)[K], float (&be)[K]) {
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+            const bool te = bit(term, k), tr = TR && bit(trunc, k), ed = bit(edge, k);
+            const float eq_next = (k + 1 < K) ? d[2][k + 1] : nb[0];
+            const float c_next = (k + 1 < K) ? trace(P, d[3][k + 1]) : nb[1];
+            const float s = successor(te, tr, ed, TR ? d[4][k] : 0.f, B[k], eq_next);
+            al[k] = fmaf(P.gamma, s, d[0][k]) - d[1][k];
+            // c_T = 0: the last step of a row never carries (edge)
+            be[k] = (te || tr || ed) ? 0.f : P.gamma * c_next;
+        }
+    }
+    template <int K, bool TR>
+    __device__ static void finish(const Params&, const float (&d)[kSlots][K], uint32_t, uint32_t,
+                                  uint32_t, const float (&)[K], const float (&)[kNbr],
+                                  const float (&A)[K], float, float (&o0)[K], float (&o1)[K]) {
+#pragma unroll
+        for (int k = 0; k < K; ++k) { o0[k] = A[k]; o1[k] = d[1][k] + A[k]; }
+    }
+};
+
+// ---------------------------------------------------------------- TD(lambda) (Section 3.3.4)
+// in: r, v, bv
+struct TdLambdaOp {
+    static constexpr bool kBackward = true;
+    static constexpr int kSlots = 3;
+    static constexpr bool kFlags = true, kRowValue = true;
+    static constexpr int kNbr = 1;
+    static constexpr bool slot_used(int s, bool trunc) { return s < 2 || trunc; }
+
+    template <int K>
+    __device__ static void nbr_export(const Params&, const float (&d)[kSlots][K], uint32_t, float (&nb)[kNbr]) {
+        nb[0] = d[1][0];
+    }
+    template <typename DT>
+    __device__ static void nbr_load(const Args& a, int64_t p, float (&nb)[kNbr]) {
+        nb[0] = load_one<DT>(a.in[1], p);
+    }
+    template <int K, bool TR>
+    __device__ static void build(const Params& P, const float (&d)[kSlots][K], uint32_t term,
+                                 uint32_t trunc, uint32_t edge, const float (&B)[K],
+                                 const float (&nb)[kNbr], float (&al)[K], float (&be)[K]) {
+        const float gl = P.gamma * P.lambda;
+        const float g1l = P.gamma * (1.f - P.lambda);
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+            const bool te = bit(term, k), tr = TR && bit(trunc, k), ed = bit(edge, k);
+            const bool done = te || tr;
+            const float next = (k + 1 < K) ? d[1][k + 1] : nb[0];
+            float a;
+            if (te)       a = d[0][k];                          // no successor value
+            else if (tr)  a = fmaf(P.gamma, d[2][k], d[0][k]);  // full-gamma continuation
+            else if (ed)  a = fmaf(P.gamma, B[k], d[0][k]);     // gamma(1-l) B + carry gamma l B
+            else          a = fmaf(g1l, next, d[0][k]);
+            al[k] = a;
+            be[k] = (done || ed) ? 0.f : gl;
+        }
+    }
+    template <int K, bool TR>
+    __device__ static void finish(const Params&, const float (&)[kSlots][K], uint32_t, uint32_t,
+                                  uint32_t, const float (&)[K], const float (&)[kNbr],
+                                  const float (&A)[K], float, float (&o0)[K], float (&)[K]) {
+#pragma unroll
+        for (int k = 0; k < K; ++k) o0[k] = A[k];
+    }
+};
+
+// ---------------------------------------------------------------- discounted returns (Section 3.3.4)
+// in: r, bv
+struct DiscountedOp {
+    static constexpr bool kBackward = true;
+    static constexpr int kSlots = 2;
+    static constexpr bool kFlags = true, kRowValue = true;
+    static constexpr int kNbr = 0;
+    static constexpr bool slot_used(int s, bool trunc) { return s < 1 || trunc; }
+
+    template <int K>
+    __device__ static void nbr_export(const Params&, const float (&)[kSlots][K], uint32_t, float (&)[1]) {}
+    template <typename DT>
+    __device__ static void nbr_load(const Args&, int64_t, float (&)[1]) {}
+    template <int K, bool TR>
+    __device__ static void build(const Params& P, const float (&d)[kSlots][K], uint32_t term,
+                                 uint32_t trunc, uint32_t edge, const float (&B)[K],
+                                 const float (&)[1], float (&al)[K], float (&be)[K]) {
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+            const bool te = bit(term, k), tr = TR && bit(trunc, k), ed = bit(edge, k);
+            const bool done = te || tr;
+            const float cont = te ? 0.f : (tr ? d[1][k] : (ed ? B[k] : 0.f));
+            al[k] = fmaf(P.gamma, cont, d[0][k]);
+            be[k] = (done || ed) ? 0.f : P.gamma;
+        }
+    }
+    template <int K, bool TR>
+    __device__ static void finish(const Params&, const float (&)[kSlots][K], uint32_t, uint32_t,
+                                  uint32_t, const float (&)[K], const float (&)[1],
+                                  const float (&A)[K], float, float (&o0)[K], float (&)[K]) {
+#pragma unroll
+        for (int k = 0; k < K; ++k) o0[k] = A[k];
+    }
+};
+
+// ---------------------------------------------------------------- forward scans (Sections 3.3.5-3.3.6)
+// in: x. kDecay: eligibility traces (gamma lambda) vs. prefix sum (1). kStartsAt: a flag at t
+// cuts the carry into t instead of into t+1.
+template <bool kDecay, bool kStartsAt>
+struct ForwardOp {
+    static constexpr bool kBackward = false;
+    static constexpr int kSlots = 1;
+    static constexpr bool kFlags = true, kRowValue = false;
+    static constexpr int kNbr = kStartsAt ? 0 : 1;  // done flag of the previous step
+    static constexpr bool slot_used(int s, bool) { return s < 1; }
+
+    template <int K>
+    __device__ static void nbr_export(const Params&, const float (&)[kSlots][K], uint32_t done,
+                                      float (&nb)[kNbr > 0 ? kNbr : 1]) {
+        nb[0] = bit(done, K - 1) ? 1.f : 0.f;
+    }
+    template <typename DT>
+    __device__ static void nbr_load(const Args& a, int64_t p, float (&nb)[kNbr > 0 ? kNbr : 1]) {
+        const bool d = (a.term && a.term[p] != 0) || (a.trunc && a.trunc[p] != 0);
+        nb[0] = d ? 1.f : 0.f;
+    }
+    template <int K, bool TR>
+    __device__ static void build(const Params& P, const float (&d)[kSlots][K], uint32_t term,
+                                 uint32_t trunc, uint32_t edge, const float (&)[K],
+                                 const float (&nb)[kNbr > 0 ? kNbr : 1], float (&al)[K],
+                                 float (&be)[K]) {
+        const float decay = kDecay ? P.gamma * P.lambda : 1.f;
+        const uint32_t done = term | (TR ? trunc : 0u);
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+            bool cut;
+            if (kStartsAt) cut = bit(done, k);
+            else cut = (k > 0) ? bit(done, k - 1) : (nb[0] != 0.f);
+            al[k] = d[0][k];
+            be[k] = (cut || bit(edge, k)) ? 0.f : decay;
+        }
+    }
+    template <int K, bool TR>
+    __device__ static void finish(const Params&, const float (&)[kSlots][K], uint32_t, uint32_t,
+                                  uint32_t, const float (&)[K], const float (&)[kNbr > 0 ? kNbr : 1],
+                                  const float (&A)[K], float, float (&o0)[K], float (&)[K]) {
+#pragma unroll
+        for (int k = 0; k < K; ++k) o0[k] = A[k];
+    }
+};
+
+// ---------------------------------------------------------------- bare recurrence (Section 4.1)
+// in: alpha, beta; the per-row carry enters at the row edge.
+template <bool kBack>
+struct AffineOp {
+    static constexpr bool kBackward = kBack;
+    static constexpr int kSlots = 2;
+    static constexpr bool kFlags = false, kRowValue = true;
+    static constexpr int kNbr = 0;
+    static constexpr bool slot_used(int s, bool) { return s < 2; }
+
+    template <int K>
+    __device__ static void nbr_export(const Params&, const float (&)[kSlots][K], uint32_t, float (&)[1]) {}
+    template <typename DT>
+    __device__ static void nbr_load(const Args&, int64_t, float (&)[1]) {}
+    template <int K, bool TR>
+    __device__ static void build(const Params&, const float (&d)[kSlots][K], uint32_t, uint32_t,
+                                 uint32_t edge, const float (&B)[K], const float (&)[1],
+                                 float (&al)[K], float (&be)[K]) {
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+            const bool ed = bit(edge, k);
+            al[k] = ed ? fmaf(d[1][k], B[k], d[0][k]) : d[0][k];
+            be[k] = ed ? 0.f : d[1][k];
+        }
+    }
+    template <int K, bool TR>
+    __device__ static void finish(const Params&, const float (&)[kSlots][K], uint32_t, uint32_t,
+                                  uint32_t, const float (&)[K], const float (&)[1],
+                                  const float (&A)[K], float, float (&o0)[K], float (&)[K]) {
+#pragma unroll
+        for (int k = 0; k < K; ++k) o0[k] = A[k];
+    }
+};
+
+}  // namespace rlcs

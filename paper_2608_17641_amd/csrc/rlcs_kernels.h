@@ -1,0 +1,373 @@
+// The two kernel shapes that run every estimator.
+//
+// Both treat the [N, T] buffer as one flat array of N*T steps and run a segmented scan over it:
+// each lane owns K consecutive steps (one 16-byte vector per input), a wave owns 64*K steps and
+// a workgroup of W waves a chunk of E = W*64*K steps. Per chunk:
+//   1. load every input once (coalesced vector loads), with the carry-source neighbour of the
+//      lane's edge step taken from the adjacent lane by shuffle, or from memory at a wave edge;
+//   2. build alpha, beta in registers (the policy's `build`);
+//   3. compose the lane's K steps serially into one affine map;
+//   4. scan those maps across the wave with shuffles (6 steps);
+//   5. compose the waves' maps through LDS;
+//   6. apply the carry entering the chunk and run the recurrence serially inside each lane;
+//   7. the policy's epilogue and one vector store per output.
+//
+// rows kernel  : each workgroup owns whole rows and walks them chunk by chunk from the carry
+//                source, passing the carry between chunks in LDS. Needs no workspace.
+// tiles kernel : each workgroup owns one chunk ("tile") of the flat array, wherever rows start
+//                or end. A tile whose edge step is not a row edge needs the carry from the
+//                tiles after it (backward) or before it (forward) in the same row: every tile
+//                publishes its composed map to the workspace as soon as step 5 is done, and a
+//                waiting tile composes its neighbours' maps, nearest first, until it meets a
+//                map with beta = 0 (an episode or row edge). Only maps are exchanged, never
+//                partial results, so the association order is fixed and results are
+//                reproducible bit for bit. Tile order comes from an atomic ticket, so a tile
+//                only ever waits for tiles that started before it.
+#pragma once
+
+#include "rlcs_estimators.h"
+
+namespace rlcs {
+
+// Workspace layout of the tiles kernel (zero-filled once by the caller):
+//   header: ticket counter, finished-workgroup counter, call epoch;
+//   then two 64-bit words per tile: (tag << 32 | bits(a)) and (tag << 32 | bits(b)).
+// A record is valid for the current call when its tag equals 2*epoch+1. The last workgroup to
+// finish resets the counters and advances the epoch, so stale records never match.
+struct WsHeader {
+    uint32_t ticket;
+    uint32_t done;
+    uint32_t epoch;
+    uint32_t error;  // set to 1 if a call found the workspace in an inconsistent state
+    uint32_t pad[12];
+};
+static_assert(sizeof(WsHeader) == 64, "workspace header is 64 bytes");
+constexpr size_t kWsRecordBytes = 16;
+
+template <typename T>
+__device__ __forceinline__ T ld_relaxed(const T* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+template <typename T>
+__device__ __forceinline__ void st_relaxed(T* p, T v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Per-thread state of one chunk between the local scan and the carry application.
+template <class Op, typename DT, int K, int W, bool VEC, bool TR>
+struct Chunk {
+    static constexpr bool kBack = Op::kBackward;
+    static constexpr int NS = Op::kSlots;
+    static constexpr int NB = Op::kNbr > 0 ? Op::kNbr : 1;
+    static constexpr uint32_t kAll = (K == 32) ? 0xffffffffu : ((1u << K) - 1u);
+
+    float d[NS][K];
+    float B[K];
+    float nb[NB];
+    float al[K], be[K];
+    uint32_t term, trunc, edge, valid;
+    int64_t p0;
+    bool full;
+    Pair excl;     // lanes between this lane and the wave's carry-source edge
+    Pair wave_in;  // waves between this wave and the chunk's carry-source edge
+
+    // Steps 1-4. Writes the wave's map to s_a/s_b[wave]; the caller synchronises.
+    __device__ void local_scan(const Args& a, int64_t chunk_lo, int64_t lo, int64_t hi,
+                               float* s_a, float* s_b, int lane, int wave) {
+        const int64_t T = a.T;
+        p0 = chunk_lo + int64_t(wave * kWave + lane) * K;
+        valid = 0;
+#pragma unroll
+        for (int k = 0; k < K; ++k)
+            if (p0 + k >= lo && p0 + k < hi) valid |= 1u << k;
+        full = VEC && valid == kAll;
+
+        // Row edges and the per-row value at each edge.
+        edge = 0;
+#pragma unroll
+        for (int k = 0; k < K; ++k) B[k] = 0.f;
+        if (valid) {
+            const int64_t first = p0 + __builtin_ctz(valid);
+            int64_t row = first / T;
+            int64_t t = first - row * T;
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+                if (p0 + k < first || !bit(valid, k)) continue;
+                const bool e = kBack ? (t == T - 1) : (t == 0);
+                if (e) {
+                    edge |= 1u << k;
+                    if (Op::kRowValue && a.row_value) B[k] = load_one<DT>(a.row_value, row);
+                }
+                if (++t == T) { t = 0; ++row; }
+            }
+        }
+
+        // Loads.
+#pragma unroll
+        for (int s = 0; s < NS; ++s) {
+            if (Op::slot_used(s, TR)) load_k<DT, K>(a.in[s], p0, valid, full, d[s]);
+            else {
+#pragma unroll
+                for (int k = 0; k < K; ++k) d[s][k] = 0.f;
+            }
+        }
+        term = 0; trunc = 0;
+        if (Op::kFlags) {
+            if (a.term) term = load_flags_k<K>(a.term, p0, valid, full);
+            if (TR) trunc = load_flags_k<K>(a.trunc, p0, valid, full);
+        }
+
+        // Neighbour on the carry-source side of the lane's edge step.
+        if (Op::kNbr > 0) {
+            float own[NB];
+            Op::template nbr_export<K>(a.p, d, term | trunc, own);
+#pragma unroll
+            for (int i = 0; i < NB; ++i) nb[i] = kBack ? __shfl_down(own[i], 1) : __shfl_up(own[i], 1);
+            const bool wave_edge = kBack ? (lane == kWave - 1) : (lane == 0);
+            const int ke = kBack ? K - 1 : 0;
+            // Needed only if the edge step is in range and not a row edge; then the neighbour
+            // is in the same row, hence inside the array.
+            if (wave_edge && bit(valid, ke) && !bit(edge, ke))
+                Op::template nbr_load<DT>(a, kBack ? p0 + K : p0 - 1, nb);
+        } else {
+#pragma unroll
+            for (int i = 0; i < NB; ++i) nb[i] = 0.f;
+        }
+
+        Op::template build<K, TR>(a.p, d, term, trunc, edge, B, nb, al, be);
+#pragma unroll
+        for (int k = 0; k < K; ++k)
+            if (!bit(valid, k)) { al[k] = 0.f; be[k] = 1.f; }
+
+        // Serial composition of the lane's K steps, nearest-to-output outermost.
+        Pair agg;
+        if (kBack) {
+            agg = Pair{al[K - 1], be[K - 1]};
+#pragma unroll
+            for (int k = K - 2; k >= 0; --k) agg = compose(Pair{al[k], be[k]}, agg);
+        } else {
+            agg = Pair{al[0], be[0]};
+#pragma unroll
+            for (int k = 1; k < K; ++k) agg = compose(Pair{al[k], be[k]}, agg);
+        }
+        const Pair incl = wave_scan_inclusive<kBack>(agg, lane);
+        excl = wave_exclusive_from_inclusive<kBack>(incl, lane);
+        if (lane == (kBack ? 0 : kWave - 1)) { s_a[wave] = incl.a; s_b[wave] = incl.b; }
+    }
+
+    // Step 5 (after the barrier): maps of the waves on this wave's carry-source side.
+    __device__ void wave_prefix(const float* s_a, const float* s_b, int wave) {
+        Pair acc = identity_pair();
+        if (kBack) {
+            for (int j = W - 1; j > wave; --j) acc = compose(Pair{s_a[j], s_b[j]}, acc);
+        } else {
+            for (int j = 0; j < wave; ++j) acc = compose(Pair{s_a[j], s_b[j]}, acc);
+        }
+        wave_in = acc;
+    }
+
+    // The whole chunk's map (all waves), for publishing.
+    __device__ static Pair chunk_map(const float* s_a, const float* s_b) {
+        Pair acc = identity_pair();
+        if (kBack) {
+            for (int j = W - 1; j >= 0; --j) acc = compose(Pair{s_a[j], s_b[j]}, acc);
+        } else {
+            for (int j = 0; j < W; ++j) acc = compose(Pair{s_a[j], s_b[j]}, acc);
+        }
+        return acc;
+    }
+
+    // Steps 6-7 given the value C just past the chunk on its carry-source side. Returns the
+    // value of the lane's step nearest the chunk's output side (A[0] backward, A[K-1] forward).
+    __device__ float finish(const Args& a, float C) {
+        const float X = apply(excl, apply(wave_in, C));
+        float A[K];
+        if (kBack) {
+            float nxt = X;
+#pragma unroll
+            for (int k = K - 1; k >= 0; --k) { A[k] = fmaf(be[k], nxt, al[k]); nxt = A[k]; }
+        } else {
+            float prv = X;
+#pragma unroll
+            for (int k = 0; k < K; ++k) { A[k] = fmaf(be[k], prv, al[k]); prv = A[k]; }
+        }
+        float o0[K], o1[K];
+        Op::template finish<K, TR>(a.p, d, term, trunc, edge, B, nb, A, X, o0, o1);
+        const bool vec_out = full;
+        store_k<K>(a.out0, p0, valid, vec_out, o0);
+        if (a.out1) store_k<K>(a.out1, p0, valid, vec_out, o1);
+        return kBack ? A[0] : A[K - 1];
+    }
+};
+
+// Rows kernel: workgroup g owns rows [g*R, g*R + R) and walks them in chunks of E steps
+// aligned to multiples of K, starting from the carry source (the end for backward scans).
+template <class Op, typename DT, int K, int W, bool VEC, bool TR>
+__global__ void __launch_bounds__(W * kWave) rows_kernel(Args a, int64_t rows_per_wg) {
+    using C = Chunk<Op, DT, K, W, VEC, TR>;
+    constexpr int64_t E = int64_t(W) * kWave * K;
+    __shared__ float s_a[W], s_b[W];
+    __shared__ float s_carry;
+    const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+    const int64_t row_lo = int64_t(blockIdx.x) * rows_per_wg;
+    const int64_t row_hi = min(row_lo + rows_per_wg, a.N);
+    const int64_t lo = row_lo * a.T, hi = row_hi * a.T;
+    float carry = 0.f;
+    if (Op::kBackward) {
+        int64_t chunk_hi = (hi + K - 1) / K * K;
+        for (;;) {
+            const int64_t chunk_lo = chunk_hi - E;
+            C c;
+            c.local_scan(a, chunk_lo, lo, hi, s_a, s_b, lane, wave);
+            __syncthreads();
+            c.wave_prefix(s_a, s_b, wave);
+            const float first = c.finish(a, carry);
+            if (chunk_lo <= lo) break;
+            // the next chunk (earlier in time) continues from A at chunk_lo
+            if (threadIdx.x == 0) s_carry = first;
+            __syncthreads();
+            carry = s_carry;
+            chunk_hi = chunk_lo;
+        }
+    } else {
+        int64_t chunk_lo = lo / K * K;
+        for (;;) {
+            C c;
+            c.local_scan(a, chunk_lo, lo, hi, s_a, s_b, lane, wave);
+            __syncthreads();
+            c.wave_prefix(s_a, s_b, wave);
+            const float last = c.finish(a, carry);
+            if (chunk_lo + E >= hi) break;
+            if (threadIdx.x == W * kWave - 1) s_carry = last;
+            __syncthreads();
+            carry = s_carry;
+            chunk_lo += E;
+        }
+    }
+}
+
+// Polls of one record before a waiting tile gives up (about a second). Reached only when the
+// workspace was not zero-filled before first use; the tile then continues with a NaN carry
+// and flags the workspace header instead of waiting forever.
+constexpr uint32_t kMaxPolls = 1u << 20;
+
+// Value entering tile `tile` from its carry-source side, composed from the published maps of
+// the neighbouring tiles of the same row, nearest outermost; run by one full wave.
+template <bool kBack>
+__device__ float gather_carry(const uint64_t* rec, int64_t tile, int64_t first_tile,
+                              int64_t last_tile, uint32_t tag, int lane, WsHeader* hdr) {
+    // Tiles to visit: tile+1 .. last_tile (backward) or tile-1 down to first_tile (forward).
+    Pair acc = identity_pair();
+    int64_t step = 1;
+    for (;;) {
+        const int64_t j = kBack ? tile + step + lane : tile - step - lane;
+        const bool inside = kBack ? (j <= last_tile) : (j >= first_tile);
+        Pair v = Pair{0.f, 0.f};  // past the row edge: nothing flows in
+        bool ready = !inside;
+        uint64_t prefix_mask, sever_mask;
+        for (uint32_t polls = 0;; ++polls) {
+            if (!ready) {
+                const uint64_t w0 = ld_relaxed(rec + 2 * j);
+                const uint64_t w1 = ld_relaxed(rec + 2 * j + 1);
+                if (uint32_t(w0 >> 32) == tag && uint32_t(w1 >> 32) == tag) {
+                    ready = true;
+                    v = Pair{__uint_as_float(uint32_t(w0)), __uint_as_float(uint32_t(w1))};
+                }
+            }
+            const uint64_t rmask = __ballot(ready);
+            sever_mask = __ballot(ready && v.b == 0.f);
+            const int first_missing = (rmask == ~0ull) ? 64 : __builtin_ctzll(~rmask);
+            prefix_mask = (first_missing == 64) ? ~0ull : ((1ull << first_missing) - 1ull);
+            if ((sever_mask & prefix_mask) != 0ull || first_missing == 64) break;
+            if (polls >= kMaxPolls) {
+                if (lane == 0) st_relaxed(&hdr->error, 1u);
+                return __builtin_nanf("");
+            }
+            __builtin_amdgcn_s_sleep(1);
+        }
+        const uint64_t sev = sever_mask & prefix_mask;
+        const int stop = sev ? __builtin_ctzll(sev) : 64;
+        const Pair mine = (lane <= stop) ? v : identity_pair();
+        const Pair all = wave_scan_inclusive<true>(mine, lane);  // lane 0: lanes 0..63 composed
+        const Pair batch = Pair{__shfl(all.a, 0), __shfl(all.b, 0)};
+        acc = compose(acc, batch);
+        if (stop < 64) return acc.a;
+        step += kWave;
+    }
+}
+
+// Tiles kernel: one workgroup per E-step tile of the flat array, split rows carried through
+// the workspace. Grid = number of tiles.
+template <class Op, typename DT, int K, int W, bool VEC, bool TR>
+__global__ void __launch_bounds__(W * kWave) tiles_kernel(Args a, int64_t num_tiles) {
+    using C = Chunk<Op, DT, K, W, VEC, TR>;
+    constexpr bool kBack = Op::kBackward;
+    constexpr int64_t E = int64_t(W) * kWave * K;
+    __shared__ float s_a[W], s_b[W];
+    __shared__ float s_carry;
+    __shared__ uint32_t s_ticket, s_epoch;
+    WsHeader* hdr = reinterpret_cast<WsHeader*>(a.ws);
+    uint64_t* rec = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(a.ws) + sizeof(WsHeader));
+    const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+
+    if (threadIdx.x == 0) {
+        s_epoch = ld_relaxed(&hdr->epoch);
+        s_ticket = __hip_atomic_fetch_add(&hdr->ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    __syncthreads();
+    const uint32_t epoch = s_epoch;
+    const uint32_t tag = 2u * epoch + 1u;
+    const int64_t ticket = s_ticket;
+    if (ticket >= num_tiles) {
+        // Only possible if the workspace was not zero-filled before first use.
+        if (threadIdx.x == 0) st_relaxed(&hdr->error, 1u);
+        return;
+    }
+    const int64_t tile = kBack ? num_tiles - 1 - ticket : ticket;
+    const int64_t total = a.N * a.T;
+    const int64_t lo = tile * E, hi = min(lo + E, total);
+
+    C c;
+    c.local_scan(a, lo, lo, hi, s_a, s_b, lane, wave);
+    __syncthreads();
+    c.wave_prefix(s_a, s_b, wave);
+
+    // A tile is read by its neighbour on the output side iff the boundary between them is not
+    // a row edge; it needs its own carry iff its carry-source boundary is not a row edge.
+    const int64_t T = a.T;
+    const bool publish = kBack ? (lo % T != 0) : (hi % T != 0 && hi < total);
+    const bool need = kBack ? (hi % T != 0) : (lo % T != 0);
+    if (publish && threadIdx.x == 0) {
+        const Pair m = C::chunk_map(s_a, s_b);
+        const uint64_t hi_tag = uint64_t(tag) << 32;
+        st_relaxed(rec + 2 * tile, hi_tag | __float_as_uint(m.a));
+        st_relaxed(rec + 2 * tile + 1, hi_tag | __float_as_uint(m.b));
+    }
+    if (need && wave == 0) {
+        // Tiles of the same row on the carry-source side.
+        int64_t first_tile = 0, last_tile = 0;
+        if (kBack) {
+            const int64_t row_end = (hi / T) * T + T - 1;  // hi is inside the row (need)
+            last_tile = row_end / E;
+        } else {
+            const int64_t row_start = (lo / T) * T;
+            first_tile = row_start / E;
+        }
+        const float v = gather_carry<kBack>(rec, tile, first_tile, last_tile, tag, lane, hdr);
+        if (lane == 0) s_carry = v;
+    }
+    __syncthreads();
+    const float carry = need ? s_carry : 0.f;
+    c.finish(a, carry);
+
+    if (threadIdx.x == 0) {
+        const uint32_t done = __hip_atomic_fetch_add(&hdr->done, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+        if (done == uint32_t(num_tiles - 1)) {
+            st_relaxed(&hdr->ticket, 0u);
+            st_relaxed(&hdr->done, 0u);
+            st_relaxed(&hdr->epoch, (epoch + 1u) & 0x7fffffffu);
+        }
+    }
+}
+
+}  // namespace rlcs

@@ -1,0 +1,126 @@
+"""CPU checks of the C ABI boundary: the library loads, exports every function the public
+header declares, and rejects bad arguments with the documented status codes before making
+any HIP call (so none of these touch a GPU)."""
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "rlcs.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_2608_17641_amd import _native
+    from paper_2608_17641_amd.build import build
+    build(force=False)
+    return _native.load()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(rlcs_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_expected_entry_points():
+    names = declared_functions()
+    for n in ("rlcs_gae", "rlcs_vtrace", "rlcs_retrace", "rlcs_td_lambda", "rlcs_discounted",
+              "rlcs_elig_trace", "rlcs_episodic_prefix", "rlcs_affine_scan",
+              "rlcs_workspace_size", "rlcs_status_string", "rlcs_version"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    from paper_2608_17641_amd import _native
+    for name in declared_functions():
+        assert hasattr(lib, name), f"librlcs.so does not export {name}"
+        assert name in _native.PROTOTYPES, f"binding has no prototype for {name}"
+
+
+def test_status_strings_and_version(lib):
+    for code in range(5):
+        assert lib.rlcs_status_string(code)
+    assert b"unknown" in lib.rlcs_status_string(99)
+    assert lib.rlcs_version() >= 100
+
+
+def test_workspace_size(lib):
+    assert lib.rlcs_workspace_size(0, 5) == 64
+    assert lib.rlcs_workspace_size(64, 4096) == 64 + 16 * (64 * 4096 // 1024)
+    assert lib.rlcs_workspace_size(1, 1025) == 64 + 16 * 2
+    assert lib.rlcs_workspace_size(-1, 5) == 64
+
+
+FAKE = ctypes.c_void_p(0x10000)       # never dereferenced: every call below fails validation
+FAKE2 = ctypes.c_void_p(0x20000)
+MISALIGNED = ctypes.c_void_p(0x10001)
+
+
+def gae(lib, **kw):
+    a = dict(r=FAKE, v=FAKE, term=None, trunc=None, bv=None, boot=None, adv=FAKE2, ret=None,
+             N=4, T=8, gamma=0.99, lam=0.95, dtype=0, ws=None, ws_bytes=0, stream=None)
+    a.update(kw)
+    return lib.rlcs_gae(*a.values())
+
+
+def test_gae_validation(lib):
+    from paper_2608_17641_amd import _native as n
+    assert gae(lib, N=-1) == n.RLCS_ERR_INVALID_ARG
+    assert gae(lib, T=-3) == n.RLCS_ERR_INVALID_ARG
+    assert gae(lib, dtype=7) == n.RLCS_ERR_DTYPE
+    assert gae(lib, r=None) == n.RLCS_ERR_INVALID_ARG
+    assert gae(lib, adv=None) == n.RLCS_ERR_INVALID_ARG
+    assert gae(lib, trunc=FAKE) == n.RLCS_ERR_INVALID_ARG  # trunc without bv
+    for bad in (-0.1, 1.5, math.nan):
+        assert gae(lib, gamma=bad) == n.RLCS_ERR_INVALID_ARG
+        assert gae(lib, lam=bad) == n.RLCS_ERR_INVALID_ARG
+    assert gae(lib, r=MISALIGNED) == n.RLCS_ERR_INVALID_ARG
+    assert gae(lib, N=2**40, T=2**40) == n.RLCS_ERR_INVALID_ARG  # N*T overflows
+    # empty problems are no-ops, even with null pointers
+    assert gae(lib, N=0, r=None, v=None, adv=None) == n.RLCS_OK
+    assert gae(lib, T=0, r=None, v=None, adv=None) == n.RLCS_OK
+
+
+def test_other_entry_points_validation(lib):
+    from paper_2608_17641_amd import _native as n
+    P = None
+    # vtrace: clip thresholds must be > 0 (inf allowed), NaN rejected
+    def vt(**kw):
+        a = dict(r=FAKE, v=FAKE, lr=FAKE, term=P, trunc=P, bv=P, boot=P, vs=FAKE2, pg=P, N=2,
+                 T=3, gamma=0.9, rho_bar=1.0, c_bar=1.0, dtype=0, ws=P, wsb=0, s=P)
+        a.update(kw)
+        return lib.rlcs_vtrace(*a.values())
+    assert vt(rho_bar=0.0) == n.RLCS_ERR_INVALID_ARG
+    assert vt(c_bar=-1.0) == n.RLCS_ERR_INVALID_ARG
+    assert vt(c_bar=math.nan) == n.RLCS_ERR_INVALID_ARG
+    assert vt(lr=None) == n.RLCS_ERR_INVALID_ARG
+    assert vt(N=0, rho_bar=math.inf, c_bar=math.inf) == n.RLCS_OK
+    assert lib.rlcs_retrace(FAKE, FAKE, None, FAKE, P, P, P, P, FAKE2, P, 2, 3, 0.9, 0.9, 1.0,
+                            0, P, 0, P) == n.RLCS_ERR_INVALID_ARG  # eq missing
+    assert lib.rlcs_td_lambda(FAKE, FAKE, P, FAKE, P, P, FAKE2, 2, 3, 0.9, 0.9, 0, P, 0, P) \
+        == n.RLCS_ERR_INVALID_ARG  # trunc without bv
+    assert lib.rlcs_discounted(FAKE, P, P, P, P, FAKE2, 2, 3, 1.01, 0, P, 0, P) \
+        == n.RLCS_ERR_INVALID_ARG
+    assert lib.rlcs_elig_trace(FAKE, P, P, None, 2, 3, 0.9, 0.9, 0, P, 0, P) \
+        == n.RLCS_ERR_INVALID_ARG
+    assert lib.rlcs_episodic_prefix(FAKE, P, P, FAKE2, 2, 3, 5, 0, P, 0, P) \
+        == n.RLCS_ERR_INVALID_ARG  # bad boundary enum
+    assert lib.rlcs_episodic_prefix(FAKE, P, P, FAKE2, 2, 3, 0, 9, P, 0, P) == n.RLCS_ERR_DTYPE
+    assert lib.rlcs_affine_scan(FAKE, FAKE, P, FAKE2, 2, 3, 2, 0, P, 0, P) \
+        == n.RLCS_ERR_INVALID_ARG  # bad direction
+    assert lib.rlcs_affine_scan(FAKE, None, P, FAKE2, 2, 3, 0, 0, P, 0, P) \
+        == n.RLCS_ERR_INVALID_ARG
+    # bf16 data needs only 2-byte alignment; an odd address is still rejected
+    assert lib.rlcs_affine_scan(MISALIGNED, FAKE, P, FAKE2, 2, 3, 0, 1, P, 0, P) \
+        == n.RLCS_ERR_INVALID_ARG
+
+
+def test_variant_override_range(lib):
+    from paper_2608_17641_amd import _native as n
+    assert lib.rlcs_set_variant_override(3) == n.RLCS_ERR_INVALID_ARG
+    assert lib.rlcs_set_variant_override(-1) == n.RLCS_ERR_INVALID_ARG
+    assert lib.rlcs_set_variant_override(0) == n.RLCS_OK

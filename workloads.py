@@ -26,6 +26,7 @@ __all__ = [
     "Rollout",
     "make_rollout",
     "make_rlhf_rollout",
+    "make_affine",
     "bf16_bits_from_f32",
     "f32_from_bf16_bits",
     "CONFIGS",
@@ -114,6 +115,21 @@ def make_rlhf_rollout(N: int, T: int, seed: int = 0, *, dtype: str = "f32",
         log_rho=_finish(zeros, dtype), q=_finish(values, dtype), eq=_finish(values, dtype),
         x=_finish(rewards, dtype), term=term, trunc=trunc,
     )
+
+
+def make_affine(N: int, T: int, seed: int = 0, *, dtype: str = "f32",
+                p_zero: float = 0.02) -> Rollout:
+    """Coefficients for the bare recurrence: alpha ~ N(0, 1), beta ~ U(0, 1) with a fraction
+    p_zero of exact zeros (episode cuts), one carry per row ~ N(0, 1)."""
+    if dtype not in ("f32", "bf16"):
+        raise ValueError(f"dtype must be 'f32' or 'bf16', got {dtype!r}")
+    rng = np.random.default_rng(seed)
+    alpha = rng.standard_normal((N, T), dtype=np.float32)
+    beta = rng.random((N, T), dtype=np.float32)
+    beta[rng.random((N, T)) < p_zero] = 0.0
+    carry = rng.standard_normal((N,), dtype=np.float32)
+    return Rollout(N, T, dtype, alpha=_finish(alpha, dtype), beta=_finish(beta, dtype),
+                   carry=_finish(carry, dtype))
 
 
 # The five synthetic workloads (shapes, dtypes, flag rates and parameters).
