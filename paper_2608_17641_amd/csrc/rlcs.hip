@@ -13,17 +13,21 @@ using namespace rlcs;
 
 namespace {
 
-constexpr int kWavesPerGroup = 4;
+// Waves per workgroup: 4 for rows of up to 4*64*K steps (several rows per workgroup), 16 for
+// longer rows (one row, or a 16*64*K-step tile of one, per workgroup).
+constexpr int kSmallWaves = 4;
+constexpr int kLargeWaves = 16;
 
 // Steps per lane: one 16-byte vector of each input.
 template <typename DT> struct Width;
 template <> struct Width<float> { static constexpr int K = 4; };
 template <> struct Width<bf16_t> { static constexpr int K = 8; };
 
-constexpr int64_t kMinChunk = int64_t(kWavesPerGroup) * kWave * Width<float>::K;
+// Smallest tile of the split-row variant (float32), which sizes the workspace.
+constexpr int64_t kMinTile = int64_t(kLargeWaves) * kWave * Width<float>::K;
 
-// Rows longer than one chunk are split across workgroups (when a workspace is given) only if
-// there are too few rows for whole-row workgroups to fill the GPU.
+// Rows longer than one large workgroup's chunk are split across workgroups (when a workspace
+// is given) only if there are too few rows for whole-row workgroups to fill the GPU.
 constexpr int64_t kSplitBelowRows = 1024;
 
 std::atomic<int> g_variant{0};
@@ -48,26 +52,42 @@ rlcs_status check_common(int64_t N, int64_t T, rlcs_dtype dtype,
     return RLCS_OK;
 }
 
-template <class Op, typename DT, bool VEC, bool TR>
-rlcs_status launch(const Args& a, bool split, int64_t num_tiles, int64_t rows_per_wg,
-                   hipStream_t stream) {
+// How one call is run.
+struct Plan {
+    bool split;           // tiles kernel (rows split across workgroups) vs rows kernel
+    int waves;            // waves per workgroup
+    int64_t num_tiles;    // tiles kernel: grid size
+    int64_t rows_per_wg;  // rows kernel: rows per workgroup
+    int wave_local;       // rows kernel: no carry crosses waves
+};
+
+template <class Op, typename DT, bool VEC, bool TR, int W>
+void launch_w(const Args& a, const Plan& p, hipStream_t stream) {
     constexpr int K = Width<DT>::K;
-    const dim3 block(kWavesPerGroup * kWave);
-    if (split) {
-        hipLaunchKernelGGL((tiles_kernel<Op, DT, K, kWavesPerGroup, VEC, TR>), dim3(unsigned(num_tiles)),
-                           block, 0, stream, a, num_tiles);
+    const dim3 block(W * kWave);
+    if (p.split) {
+        hipLaunchKernelGGL((tiles_kernel<Op, DT, K, W, VEC, TR>), dim3(unsigned(p.num_tiles)),
+                           block, 0, stream, a, p.num_tiles);
     } else {
-        const int64_t groups = (a.N + rows_per_wg - 1) / rows_per_wg;
-        hipLaunchKernelGGL((rows_kernel<Op, DT, K, kWavesPerGroup, VEC, TR>), dim3(unsigned(groups)),
-                           block, 0, stream, a, rows_per_wg);
+        const int64_t groups = (a.N + p.rows_per_wg - 1) / p.rows_per_wg;
+        hipLaunchKernelGGL((rows_kernel<Op, DT, K, W, VEC, TR>), dim3(unsigned(groups)),
+                           block, 0, stream, a, p.rows_per_wg, p.wave_local);
     }
+}
+
+template <class Op, typename DT, bool VEC, bool TR>
+rlcs_status launch(const Args& a, const Plan& p, hipStream_t stream) {
+    if (p.split) launch_w<Op, DT, VEC, TR, kLargeWaves>(a, p, stream);
+    else if (p.waves == kSmallWaves) launch_w<Op, DT, VEC, TR, kSmallWaves>(a, p, stream);
+    else launch_w<Op, DT, VEC, TR, kLargeWaves>(a, p, stream);
     return hipGetLastError() == hipSuccess ? RLCS_OK : RLCS_ERR_LAUNCH;
 }
 
 template <class Op, typename DT>
 rlcs_status dispatch_dt(Args& a, bool has_trunc, void* ws, size_t ws_bytes, hipStream_t stream) {
     constexpr int K = Width<DT>::K;
-    constexpr int64_t E = int64_t(kWavesPerGroup) * kWave * K;
+    constexpr int64_t E_small = int64_t(kSmallWaves) * kWave * K;
+    constexpr int64_t E_large = int64_t(kLargeWaves) * kWave * K;
     const int64_t N = a.N, T = a.T, total = N * T;
 
     // Vector path: 16-byte data and output vectors, K-byte flag vectors.
@@ -77,39 +97,43 @@ rlcs_status dispatch_dt(Args& a, bool has_trunc, void* ws, size_t ws_bytes, hipS
     if (!aligned(a.out0, 16) || (a.out1 && !aligned(a.out1, 16))) vec = false;
     if (Op::kFlags && ((a.term && !aligned(a.term, K)) || (has_trunc && !aligned(a.trunc, K)))) vec = false;
 
-    // Variant.
-    const int64_t num_tiles = (total + E - 1) / E;
-    const size_t ws_need = sizeof(WsHeader) + size_t(num_tiles) * kWsRecordBytes;
-    const bool ws_ok = ws && ws_bytes >= ws_need && aligned(ws, 64) && num_tiles < int64_t(UINT32_MAX);
+    Plan p{};
+    p.num_tiles = (total + E_large - 1) / E_large;
+    const size_t ws_need = sizeof(WsHeader) + size_t(p.num_tiles) * kWsRecordBytes;
+    const bool ws_ok = ws && ws_bytes >= ws_need && aligned(ws, 64) && p.num_tiles < int64_t(UINT32_MAX);
     const int forced = g_variant.load(std::memory_order_relaxed);
-    bool split;
     if (forced == 2) {
         if (!ws_ok) return RLCS_ERR_WORKSPACE;
-        split = true;
+        p.split = true;
     } else if (forced == 1) {
-        split = false;
+        p.split = false;
     } else {
-        split = T > E && ws_ok && N < kSplitBelowRows;
+        p.split = T > E_large && ws_ok && N < kSplitBelowRows;
     }
-    // Whole rows per workgroup: as many as fit in one chunk (at least one). When T is not a
-    // multiple of K a row range may start mid-vector, costing up to K-1 extra slots.
-    const int64_t slack = (T % K == 0) ? 0 : K - 1;
-    const int64_t rows_per_wg = (T <= E - slack) ? (E - slack) / T : 1;
-    if (split) {
-        if (num_tiles > INT32_MAX) return RLCS_ERR_INVALID_ARG;
+    if (p.split) {
+        if (p.num_tiles > INT32_MAX) return RLCS_ERR_INVALID_ARG;
+        p.waves = kLargeWaves;
         a.ws = ws;
-    } else if ((N + rows_per_wg - 1) / rows_per_wg > INT32_MAX) {
-        return RLCS_ERR_INVALID_ARG;
+    } else {
+        p.waves = (T <= E_small) ? kSmallWaves : kLargeWaves;
+        const int64_t E = int64_t(p.waves) * kWave * K;
+        // Whole rows per workgroup: as many as fit in one chunk (at least one). When T is not
+        // a multiple of K a row range may start mid-vector, costing up to K-1 extra slots.
+        const int64_t slack = (T % K == 0) ? 0 : K - 1;
+        p.rows_per_wg = (T <= E - slack) ? (E - slack) / T : 1;
+        if ((N + p.rows_per_wg - 1) / p.rows_per_wg > INT32_MAX) return RLCS_ERR_INVALID_ARG;
+        // Rows never straddle waves when T divides a wave's span (and is a multiple of K).
+        p.wave_local = (T % K == 0 && (int64_t(kWave) * K) % T == 0) ? 1 : 0;
     }
 
     if constexpr (Op::kFlags) {
         if (has_trunc) {
-            return vec ? launch<Op, DT, true, true>(a, split, num_tiles, rows_per_wg, stream)
-                       : launch<Op, DT, false, true>(a, split, num_tiles, rows_per_wg, stream);
+            return vec ? launch<Op, DT, true, true>(a, p, stream)
+                       : launch<Op, DT, false, true>(a, p, stream);
         }
     }
-    return vec ? launch<Op, DT, true, false>(a, split, num_tiles, rows_per_wg, stream)
-               : launch<Op, DT, false, false>(a, split, num_tiles, rows_per_wg, stream);
+    return vec ? launch<Op, DT, true, false>(a, p, stream)
+               : launch<Op, DT, false, false>(a, p, stream);
 }
 
 template <class Op>
@@ -267,7 +291,7 @@ rlcs_status rlcs_affine_scan(const void* alpha, const void* beta, const void* ca
 size_t rlcs_workspace_size(int64_t N, int64_t T) {
     if (N <= 0 || T <= 0) return sizeof(WsHeader);
     if (N > INT64_MAX / T) return 0;
-    const int64_t tiles = (N * T + kMinChunk - 1) / kMinChunk;
+    const int64_t tiles = (N * T + kMinTile - 1) / kMinTile;
     return sizeof(WsHeader) + size_t(tiles) * kWsRecordBytes;
 }
 

@@ -25,29 +25,51 @@ __device__ __forceinline__ Pair compose(Pair outer, Pair inner) {
 // Value of the map at X.
 __device__ __forceinline__ float apply(Pair m, float x) { return fmaf(m.b, x, m.a); }
 
-// Inclusive scan of lane aggregates across the wave, towards the carry source: for a backward
-// scan lane l ends with lanes l..63 composed (suffix), for a forward scan lanes 0..l (prefix).
-// log2(64) = 6 shuffle steps (Hillis-Steele, as traced in Appendix A).
-template <bool kBackward>
-__device__ __forceinline__ Pair wave_scan_inclusive(Pair v, int lane) {
-#pragma unroll
-    for (int s = 1; s < kWave; s <<= 1) {
-        const float a = kBackward ? __shfl_down(v.a, s) : __shfl_up(v.a, s);
-        const float b = kBackward ? __shfl_down(v.b, s) : __shfl_up(v.b, s);
-        const bool has = kBackward ? (lane + s < kWave) : (lane >= s);
-        if (has) v = compose(v, Pair{a, b});
-    }
-    return v;
+// DPP lane moves (GFX9 data-parallel primitives). A lane whose source lane does not exist
+// keeps `fill`.
+constexpr int kDppRowShr = 0x110;  // row_shr:n = 0x110 + n (within rows of 16 lanes)
+constexpr int kDppWaveShr1 = 0x138;  // wave_shr:1 (lane i reads lane i-1 across the wave)
+
+template <int kCtrl>
+__device__ __forceinline__ float dpp_move(float fill, float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(fill), __float_as_int(v), kCtrl,
+                                                      0xf, 0xf, false));
 }
 
-// The inclusive value of the neighbouring lane on the carry-source side (identity at the wave
-// edge): the composition of every lane strictly between this lane and the wave's edge.
-template <bool kBackward>
-__device__ __forceinline__ Pair wave_exclusive_from_inclusive(Pair incl, int lane) {
-    const float a = kBackward ? __shfl_down(incl.a, 1) : __shfl_up(incl.a, 1);
-    const float b = kBackward ? __shfl_down(incl.b, 1) : __shfl_up(incl.b, 1);
-    const bool edge = kBackward ? (lane == kWave - 1) : (lane == 0);
-    return edge ? identity_pair() : Pair{a, b};
+// Value of lane i-1 (lane 0 receives `fill`).
+__device__ __forceinline__ float shift_up1(float v, float fill) { return dpp_move<kDppWaveShr1>(fill, v); }
+
+__device__ __forceinline__ Pair read_lane(Pair v, int lane) {
+    return Pair{__int_as_float(__builtin_amdgcn_readlane(__float_as_int(v.a), lane)),
+                __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v.b), lane))};
+}
+
+// Inclusive prefix scan of per-lane maps over the 64 lanes (lane l ends with lanes 0..l
+// composed, lane 0 innermost). Kogge-Stone inside each row of 16 lanes with DPP row shifts
+// (4 steps), then the three row totals are read into scalars and composed onto the rows
+// after them. No LDS traffic; the same tree as the Hillis-Steele trace of Appendix A inside a
+// row.
+__device__ __forceinline__ Pair wave_scan_inclusive(Pair v, int lane) {
+#define RLCS_ROW_STEP(S)                                                                 \
+    {                                                                                    \
+        const Pair o{dpp_move<kDppRowShr + S>(0.f, v.a), dpp_move<kDppRowShr + S>(1.f, v.b)}; \
+        v = compose(v, o);                                                               \
+    }
+    RLCS_ROW_STEP(1)
+    RLCS_ROW_STEP(2)
+    RLCS_ROW_STEP(4)
+    RLCS_ROW_STEP(8)
+#undef RLCS_ROW_STEP
+    const Pair t0 = read_lane(v, 15), t1 = read_lane(v, 31), t2 = read_lane(v, 47);
+    const Pair p1 = t0;
+    const Pair p2 = compose(t1, p1);
+    const Pair p3 = compose(t2, p2);
+    const int row = lane >> 4;
+    if (row > 0) {
+        const Pair p = (row == 1) ? p1 : ((row == 2) ? p2 : p3);
+        v = compose(v, p);
+    }
+    return v;
 }
 
 // ------------------------------------------------------------------ element loads / stores
@@ -109,40 +131,76 @@ __device__ __forceinline__ void load_k(const void* base, int64_t p0, uint32_t va
     }
 }
 
-// Flags of K consecutive steps as a K-bit mask (bit k set: byte k nonzero).
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+
+// Flags of K consecutive steps: raw 32-bit words (vector path) and their K-bit mask (bit k
+// set: byte k nonzero). Loading and converting are separate so that every load of a chunk can
+// be issued before the first use of any of them. Non-temporal: each flag is read once.
 template <int K>
-__device__ __forceinline__ uint32_t load_flags_k(const uint8_t* base, int64_t p0, uint32_t valid,
-                                                 bool full) {
-    uint32_t m = 0;
-    if (full) {
-        uint32_t w[(K + 3) / 4];
-        if constexpr (K == 4) {
-            w[0] = *reinterpret_cast<const uint32_t*>(base + p0);
-        } else if constexpr (K == 8) {
-            const uint2 u = *reinterpret_cast<const uint2*>(base + p0);
-            w[0] = u.x; w[1] = u.y;
-        } else {
-            static_assert(K == 16, "flag vector width");
-            const uint4 u = *reinterpret_cast<const uint4*>(base + p0);
-            w[0] = u.x; w[1] = u.y; w[2] = u.z; w[3] = u.w;
-        }
-#pragma unroll
-        for (int k = 0; k < K; ++k) m |= (((w[k >> 2] >> (8 * (k & 3))) & 0xffu) != 0u) ? (1u << k) : 0u;
+__device__ __forceinline__ void load_flag_words(const uint8_t* base, int64_t p0, uint32_t (&w)[(K + 3) / 4]) {
+    if constexpr (K == 4) {
+        w[0] = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(base + p0));
+    } else if constexpr (K == 8) {
+        const u32x2 u = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(base + p0));
+        w[0] = u.x; w[1] = u.y;
     } else {
-#pragma unroll
-        for (int k = 0; k < K; ++k)
-            if ((valid >> k) & 1u) m |= (base[p0 + k] != 0) ? (1u << k) : 0u;
+        static_assert(K == 16, "flag vector width");
+        const u32x4 u = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(base + p0));
+        w[0] = u.x; w[1] = u.y; w[2] = u.z; w[3] = u.w;
     }
+}
+
+template <int K>
+__device__ __forceinline__ uint32_t flag_mask(const uint32_t (&w)[(K + 3) / 4]) {
+    uint32_t m = 0;
+#pragma unroll
+    for (int k = 0; k < K; ++k) m |= (((w[k >> 2] >> (8 * (k & 3))) & 0xffu) != 0u) ? (1u << k) : 0u;
     return m;
 }
 
+// Masked element-wise flag load (ragged chunks).
+template <int K>
+__device__ __forceinline__ uint32_t load_flags_masked(const uint8_t* base, int64_t p0, uint32_t valid) {
+    uint32_t m = 0;
+#pragma unroll
+    for (int k = 0; k < K; ++k)
+        if ((valid >> k) & 1u) m |= (base[p0 + k] != 0) ? (1u << k) : 0u;
+    return m;
+}
+
+// Raw words of K consecutive data elements: 16-byte vector loads, non-temporal because every
+// input is read exactly once.
+template <typename DT, int K>
+__device__ __forceinline__ void load_words(const void* base, int64_t p0, uint32_t (&w)[K * sizeof(DT) / 4]) {
+    constexpr int kBytes = K * int(sizeof(DT));
+    static_assert(kBytes % 16 == 0 || kBytes == 8, "vector width");
+    const char* p = reinterpret_cast<const char*>(base) + p0 * int64_t(sizeof(DT));
+    if constexpr (kBytes % 16 == 0) {
+#pragma unroll
+        for (int i = 0; i < kBytes / 16; ++i) {
+            const u32x4 u = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p) + i);
+            w[4 * i + 0] = u.x; w[4 * i + 1] = u.y; w[4 * i + 2] = u.z; w[4 * i + 3] = u.w;
+        }
+    } else {
+        const u32x2 u = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(p));
+        w[0] = u.x; w[1] = u.y;
+    }
+}
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// Outputs are written once and not read again by the kernel: non-temporal 16-byte stores.
 template <int K>
 __device__ __forceinline__ void store_k(float* base, int64_t p0, uint32_t valid, bool full,
                                         const float (&v)[K]) {
     if (full) {
-        float4* p = reinterpret_cast<float4*>(base + p0);
+        f32x4* p = reinterpret_cast<f32x4*>(base + p0);
 #pragma unroll
-        for (int i = 0; i < K / 4; ++i) p[i] = make_float4(v[4 * i], v[4 * i + 1], v[4 * i + 2], v[4 * i + 3]);
+        for (int i = 0; i < K / 4; ++i) {
+            const f32x4 q = {v[4 * i], v[4 * i + 1], v[4 * i + 2], v[4 * i + 3]};
+            __builtin_nontemporal_store(q, p + i);
+        }
     } else {
 #pragma unroll
         for (int k = 0; k < K; ++k)

@@ -6,7 +6,8 @@
 //   kFlags      whether it reads term / trunc;
 //   kRowValue   whether it reads the per-row value (bootstrap or carry) at the row edge;
 //   kNbr        number of values it needs from the neighbouring step on the carry-source side
-//               (exported by that step's lane, or loaded from memory at a lane edge);
+//               (exported by that step's lane, or at a wave edge loaded raw from memory by
+//               nbr_load_raw and converted by nbr_fix once every load has been issued);
 //   build       alpha_k, beta_k of the lane's K steps;
 //   finish      the outputs of the K steps given the scanned values A_k and X, the scanned
 //               value just past the lane on the carry-source side.
@@ -61,9 +62,13 @@ struct GaeOp {
     __device__ static void nbr_export(const Params&, const float (&d)[kSlots][K], uint32_t, float (&nb)[kNbr]) {
         nb[0] = d[1][0];
     }
+    static constexpr int kNbrRaw = kNbr;
     template <typename DT>
-    __device__ static void nbr_load(const Args& a, int64_t p, float (&nb)[kNbr]) {
-        nb[0] = load_one<DT>(a.in[1], p);
+    __device__ static void nbr_load_raw(const Args& a, int64_t p, float (&raw)[kNbrRaw]) {
+        raw[0] = load_one<DT>(a.in[1], p);
+    }
+    __device__ static void nbr_fix(const Args&, const float (&raw)[kNbrRaw], float (&nb)[kNbr]) {
+        nb[0] = raw[0];
     }
     template <int K, bool TR>
     __device__ static void build(const Params& P, const float (&d)[kSlots][K], uint32_t term,
@@ -101,9 +106,13 @@ struct VtraceOp {
     __device__ static void nbr_export(const Params&, const float (&d)[kSlots][K], uint32_t, float (&nb)[kNbr]) {
         nb[0] = d[1][0];
     }
+    static constexpr int kNbrRaw = kNbr;
     template <typename DT>
-    __device__ static void nbr_load(const Args& a, int64_t p, float (&nb)[kNbr]) {
-        nb[0] = load_one<DT>(a.in[1], p);
+    __device__ static void nbr_load_raw(const Args& a, int64_t p, float (&raw)[kNbrRaw]) {
+        raw[0] = load_one<DT>(a.in[1], p);
+    }
+    __device__ static void nbr_fix(const Args&, const float (&raw)[kNbrRaw], float (&nb)[kNbr]) {
+        nb[0] = raw[0];
     }
     template <int K, bool TR>
     __device__ static void build(const Params& P, const float (&d)[kSlots][K], uint32_t term,
@@ -156,10 +165,15 @@ struct RetraceOp {
         nb[0] = d[2][0];
         nb[1] = trace(P, d[3][0]);
     }
+    static constexpr int kNbrRaw = kNbr;
     template <typename DT>
-    __device__ static void nbr_load(const Args& a, int64_t p, float (&nb)[kNbr]) {
-        nb[0] = load_one<DT>(a.in[2], p);
-        nb[1] = trace(a.p, load_one<DT>(a.in[3], p));
+    __device__ static void nbr_load_raw(const Args& a, int64_t p, float (&raw)[kNbrRaw]) {
+        raw[0] = load_one<DT>(a.in[2], p);
+        raw[1] = load_one<DT>(a.in[3], p);
+    }
+    __device__ static void nbr_fix(const Args& a, const float (&raw)[kNbrRaw], float (&nb)[kNbr]) {
+        nb[0] = raw[0];
+        nb[1] = trace(a.p, raw[1]);
     }
     template <int K, bool TR>
     __device__ static void build(const Params& P, const float (&d)[kSlots][K], uint32_t term,
@@ -198,9 +212,13 @@ struct TdLambdaOp {
     __device__ static void nbr_export(const Params&, const float (&d)[kSlots][K], uint32_t, float (&nb)[kNbr]) {
         nb[0] = d[1][0];
     }
+    static constexpr int kNbrRaw = kNbr;
     template <typename DT>
-    __device__ static void nbr_load(const Args& a, int64_t p, float (&nb)[kNbr]) {
-        nb[0] = load_one<DT>(a.in[1], p);
+    __device__ static void nbr_load_raw(const Args& a, int64_t p, float (&raw)[kNbrRaw]) {
+        raw[0] = load_one<DT>(a.in[1], p);
+    }
+    __device__ static void nbr_fix(const Args&, const float (&raw)[kNbrRaw], float (&nb)[kNbr]) {
+        nb[0] = raw[0];
     }
     template <int K, bool TR>
     __device__ static void build(const Params& P, const float (&d)[kSlots][K], uint32_t term,
@@ -242,8 +260,10 @@ struct DiscountedOp {
 
     template <int K>
     __device__ static void nbr_export(const Params&, const float (&)[kSlots][K], uint32_t, float (&)[1]) {}
+    static constexpr int kNbrRaw = 1;
     template <typename DT>
-    __device__ static void nbr_load(const Args&, int64_t, float (&)[1]) {}
+    __device__ static void nbr_load_raw(const Args&, int64_t, float (&)[1]) {}
+    __device__ static void nbr_fix(const Args&, const float (&)[1], float (&)[1]) {}
     template <int K, bool TR>
     __device__ static void build(const Params& P, const float (&d)[kSlots][K], uint32_t term,
                                  uint32_t trunc, uint32_t edge, const float (&B)[K],
@@ -282,10 +302,20 @@ struct ForwardOp {
                                       float (&nb)[kNbr > 0 ? kNbr : 1]) {
         nb[0] = bit(done, K - 1) ? 1.f : 0.f;
     }
+    // Raw flag bytes of the previous step (as 32-bit patterns); a missing flag array is read
+    // from the data input instead (always in bounds) and ignored.
+    static constexpr int kNbrRaw = 2;
     template <typename DT>
-    __device__ static void nbr_load(const Args& a, int64_t p, float (&nb)[kNbr > 0 ? kNbr : 1]) {
-        const bool d = (a.term && a.term[p] != 0) || (a.trunc && a.trunc[p] != 0);
-        nb[0] = d ? 1.f : 0.f;
+    __device__ static void nbr_load_raw(const Args& a, int64_t p, float (&raw)[kNbrRaw]) {
+        const uint8_t* fallback = reinterpret_cast<const uint8_t*>(a.in[0]);
+        raw[0] = __uint_as_float(uint32_t((a.term ? a.term : fallback)[p]));
+        raw[1] = __uint_as_float(uint32_t((a.trunc ? a.trunc : fallback)[p]));
+    }
+    __device__ static void nbr_fix(const Args& a, const float (&raw)[kNbrRaw],
+                                   float (&nb)[kNbr > 0 ? kNbr : 1]) {
+        const bool t = a.term && __float_as_uint(raw[0]) != 0u;
+        const bool r = a.trunc && __float_as_uint(raw[1]) != 0u;
+        nb[0] = (t || r) ? 1.f : 0.f;
     }
     template <int K, bool TR>
     __device__ static void build(const Params& P, const float (&d)[kSlots][K], uint32_t term,
@@ -324,8 +354,10 @@ struct AffineOp {
 
     template <int K>
     __device__ static void nbr_export(const Params&, const float (&)[kSlots][K], uint32_t, float (&)[1]) {}
+    static constexpr int kNbrRaw = 1;
     template <typename DT>
-    __device__ static void nbr_load(const Args&, int64_t, float (&)[1]) {}
+    __device__ static void nbr_load_raw(const Args&, int64_t, float (&)[1]) {}
+    __device__ static void nbr_fix(const Args&, const float (&)[1], float (&)[1]) {}
     template <int K, bool TR>
     __device__ static void build(const Params&, const float (&d)[kSlots][K], uint32_t, uint32_t,
                                  uint32_t edge, const float (&B)[K], const float (&)[1],

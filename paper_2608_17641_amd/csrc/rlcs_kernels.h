@@ -30,16 +30,17 @@
 namespace rlcs {
 
 // Workspace layout of the tiles kernel (zero-filled once by the caller):
-//   header: ticket counter, finished-workgroup counter, call epoch;
+//   header: ticket counter, call epoch, error flag;
 //   then two 64-bit words per tile: (tag << 32 | bits(a)) and (tag << 32 | bits(b)).
-// A record is valid for the current call when its tag equals 2*epoch+1. The last workgroup to
-// finish resets the counters and advances the epoch, so stale records never match.
+// A record is valid for the current call when its tag equals 2*epoch+1. The workgroup that
+// draws the last ticket of a call resets the counter and advances the epoch (every other
+// workgroup of the call read the epoch before drawing its ticket), so stale records never
+// match and the next call on the same stream finds the header ready.
 struct WsHeader {
     uint32_t ticket;
-    uint32_t done;
     uint32_t epoch;
     uint32_t error;  // set to 1 if a call found the workspace in an inconsistent state
-    uint32_t pad[12];
+    uint32_t pad[13];
 };
 static_assert(sizeof(WsHeader) == 64, "workspace header is 64 bytes");
 constexpr size_t kWsRecordBytes = 16;
@@ -53,7 +54,30 @@ __device__ __forceinline__ void st_relaxed(T* p, T v) {
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// Lane l of a wave owns the l-th group of K steps of the wave's span for forward scans and the
+// (63-l)-th for backward scans, so that in both directions the carry flows from lane l-1 to
+// lane l and the wave scan is a prefix scan over lanes.
+template <bool kBack>
+__device__ __forceinline__ int lane_group(int lane) { return kBack ? (kWave - 1 - lane) : lane; }
+
+// Row and step index of flat position p (32-bit division when the array allows it).
+__device__ __forceinline__ void row_and_step(int64_t p, int64_t T, bool small, int64_t& row, int64_t& t) {
+    if (small) {
+        const uint32_t r = uint32_t(p) / uint32_t(T);
+        row = r;
+        t = int64_t(uint32_t(p) - r * uint32_t(T));
+    } else {
+        row = p / T;
+        t = p - row * T;
+    }
+}
+
 // Per-thread state of one chunk between the local scan and the carry application.
+//
+// FULL chunks (every step of the chunk in range, 16-byte aligned data, T >= K) take a
+// branch-free path: one vector load per input, issued back to back, and at most one row edge
+// per lane, whose per-row value is loaded unconditionally from a clamped row index. Other
+// chunks (the ragged ends of a range) take the masked element-wise path.
 template <class Op, typename DT, int K, int W, bool VEC, bool TR>
 struct Chunk {
     static constexpr bool kBack = Op::kBackward;
@@ -67,29 +91,79 @@ struct Chunk {
     float al[K], be[K];
     uint32_t term, trunc, edge, valid;
     int64_t p0;
-    bool full;
-    Pair excl;     // lanes between this lane and the wave's carry-source edge
+    Pair incl;     // lanes 0..lane of this wave composed (lane 0 innermost)
     Pair wave_in;  // waves between this wave and the chunk's carry-source edge
 
-    // Steps 1-4. Writes the wave's map to s_a/s_b[wave]; the caller synchronises.
-    __device__ void local_scan(const Args& a, int64_t chunk_lo, int64_t lo, int64_t hi,
-                               float* s_a, float* s_b, int lane, int wave) {
+    // Whether lane 0 must read the carry-source neighbour of its edge step from memory: only
+    // if that step is in range and not a row edge (then the neighbour is in the same row,
+    // hence inside the array).
+    __device__ bool needs_nbr(int lane) const {
+        const int ke = kBack ? K - 1 : 0;
+        return Op::kNbr > 0 && lane == 0 && bit(valid, ke) && !bit(edge, ke);
+    }
+
+    // Step 1 for a chunk whose steps are all in range: every load is issued before any loaded
+    // value is used.
+    __device__ void load_full(const Args& a, bool small, int lane, float (&nraw)[Op::kNbrRaw]) {
         const int64_t T = a.T;
-        p0 = chunk_lo + int64_t(wave * kWave + lane) * K;
+        valid = kAll;
+        int64_t row, t;
+        row_and_step(p0, T, small, row, t);
+        // at most one row edge among the K steps (T >= K)
+        int ke = -1;
+        int64_t row_e = row;
+        if (kBack) {
+            if (t + K - 1 >= T - 1) ke = int(T - 1 - t);
+        } else {
+            if (t == 0) ke = 0;
+            else if (t + K - 1 >= T) { ke = int(T - t); row_e = row + 1; }
+        }
+        edge = ke >= 0 ? (1u << ke) : 0u;
+        // A missing optional array is read from in[0] instead (in bounds) and the value dropped.
+        const bool has_rv = Op::kRowValue && a.row_value;
+        const float rv_raw = load_one<DT>(has_rv ? a.row_value : a.in[0], min(row_e, a.N - 1));
+        constexpr int kWords = K * int(sizeof(DT)) / 4;
+        uint32_t w[NS][kWords];
+#pragma unroll
+        for (int s = 0; s < NS; ++s)
+            if (Op::slot_used(s, TR)) load_words<DT, K>(a.in[s], p0, w[s]);
+        uint32_t tw[(K + 3) / 4], rw[(K + 3) / 4];
+        const uint8_t* fallback = reinterpret_cast<const uint8_t*>(a.in[0]);
+        if (Op::kFlags) load_flag_words<K>(a.term ? a.term : fallback, p0, tw);
+        if (Op::kFlags && TR) load_flag_words<K>(a.trunc, p0, rw);
+        if (needs_nbr(lane)) Op::template nbr_load_raw<DT>(a, kBack ? p0 + K : p0 - 1, nraw);
+
+        // conversions
+#pragma unroll
+        for (int s = 0; s < NS; ++s) {
+            if (Op::slot_used(s, TR)) unpack_words<DT, K>(w[s], d[s]);
+            else {
+#pragma unroll
+                for (int k = 0; k < K; ++k) d[s][k] = 0.f;
+            }
+        }
+        term = (Op::kFlags && a.term) ? flag_mask<K>(tw) : 0u;
+        trunc = (Op::kFlags && TR) ? flag_mask<K>(rw) : 0u;
+        const float rv = has_rv ? rv_raw : 0.f;
+#pragma unroll
+        for (int k = 0; k < K; ++k) B[k] = (k == ke) ? rv : 0.f;
+    }
+
+    // Step 1 for a chunk with steps outside [lo, hi): element-wise, masked.
+    __device__ void load_masked(const Args& a, int64_t lo, int64_t hi, bool small, int lane,
+                                float (&nraw)[Op::kNbrRaw]) {
+        const int64_t T = a.T;
         valid = 0;
 #pragma unroll
         for (int k = 0; k < K; ++k)
             if (p0 + k >= lo && p0 + k < hi) valid |= 1u << k;
-        full = VEC && valid == kAll;
-
-        // Row edges and the per-row value at each edge.
         edge = 0;
 #pragma unroll
         for (int k = 0; k < K; ++k) B[k] = 0.f;
         if (valid) {
             const int64_t first = p0 + __builtin_ctz(valid);
-            int64_t row = first / T;
-            int64_t t = first - row * T;
+            int64_t row, t;
+            row_and_step(first, T, small, row, t);
 #pragma unroll
             for (int k = 0; k < K; ++k) {
                 if (p0 + k < first || !bit(valid, k)) continue;
@@ -101,11 +175,9 @@ struct Chunk {
                 if (++t == T) { t = 0; ++row; }
             }
         }
-
-        // Loads.
 #pragma unroll
         for (int s = 0; s < NS; ++s) {
-            if (Op::slot_used(s, TR)) load_k<DT, K>(a.in[s], p0, valid, full, d[s]);
+            if (Op::slot_used(s, TR)) load_k<DT, K>(a.in[s], p0, valid, false, d[s]);
             else {
 #pragma unroll
                 for (int k = 0; k < K; ++k) d[s][k] = 0.f;
@@ -113,31 +185,42 @@ struct Chunk {
         }
         term = 0; trunc = 0;
         if (Op::kFlags) {
-            if (a.term) term = load_flags_k<K>(a.term, p0, valid, full);
-            if (TR) trunc = load_flags_k<K>(a.trunc, p0, valid, full);
+            if (a.term) term = load_flags_masked<K>(a.term, p0, valid);
+            if (TR) trunc = load_flags_masked<K>(a.trunc, p0, valid);
         }
+        if (needs_nbr(lane)) Op::template nbr_load_raw<DT>(a, kBack ? p0 + K : p0 - 1, nraw);
+    }
 
-        // Neighbour on the carry-source side of the lane's edge step.
+    // Steps 1-4. Writes the wave's map to s_a/s_b[wave] unless `wave_local`; the caller
+    // synchronises.
+    template <bool FULL>
+    __device__ void local_scan(const Args& a, int64_t chunk_lo, int64_t lo, int64_t hi,
+                               float* s_a, float* s_b, int lane, int wave, bool wave_local,
+                               bool small) {
+        p0 = chunk_lo + int64_t(wave * kWave + lane_group<kBack>(lane)) * K;
+        float nraw[Op::kNbrRaw];
+        if (FULL) load_full(a, small, lane, nraw);
+        else load_masked(a, lo, hi, small, lane, nraw);
+
+        // Neighbour on the carry-source side of the lane's edge step: lane l-1 holds it, lane 0
+        // read it from memory.
         if (Op::kNbr > 0) {
             float own[NB];
             Op::template nbr_export<K>(a.p, d, term | trunc, own);
 #pragma unroll
-            for (int i = 0; i < NB; ++i) nb[i] = kBack ? __shfl_down(own[i], 1) : __shfl_up(own[i], 1);
-            const bool wave_edge = kBack ? (lane == kWave - 1) : (lane == 0);
-            const int ke = kBack ? K - 1 : 0;
-            // Needed only if the edge step is in range and not a row edge; then the neighbour
-            // is in the same row, hence inside the array.
-            if (wave_edge && bit(valid, ke) && !bit(edge, ke))
-                Op::template nbr_load<DT>(a, kBack ? p0 + K : p0 - 1, nb);
+            for (int i = 0; i < NB; ++i) nb[i] = shift_up1(own[i], 0.f);
+            if (needs_nbr(lane)) Op::nbr_fix(a, nraw, nb);
         } else {
 #pragma unroll
             for (int i = 0; i < NB; ++i) nb[i] = 0.f;
         }
 
         Op::template build<K, TR>(a.p, d, term, trunc, edge, B, nb, al, be);
+        if (!FULL) {
 #pragma unroll
-        for (int k = 0; k < K; ++k)
-            if (!bit(valid, k)) { al[k] = 0.f; be[k] = 1.f; }
+            for (int k = 0; k < K; ++k)
+                if (!bit(valid, k)) { al[k] = 0.f; be[k] = 1.f; }
+        }
 
         // Serial composition of the lane's K steps, nearest-to-output outermost.
         Pair agg;
@@ -150,9 +233,8 @@ struct Chunk {
 #pragma unroll
             for (int k = 1; k < K; ++k) agg = compose(Pair{al[k], be[k]}, agg);
         }
-        const Pair incl = wave_scan_inclusive<kBack>(agg, lane);
-        excl = wave_exclusive_from_inclusive<kBack>(incl, lane);
-        if (lane == (kBack ? 0 : kWave - 1)) { s_a[wave] = incl.a; s_b[wave] = incl.b; }
+        incl = wave_scan_inclusive(agg, lane);
+        if (!wave_local && lane == kWave - 1) { s_a[wave] = incl.a; s_b[wave] = incl.b; }
     }
 
     // Step 5 (after the barrier): maps of the waves on this wave's carry-source side.
@@ -179,8 +261,11 @@ struct Chunk {
 
     // Steps 6-7 given the value C just past the chunk on its carry-source side. Returns the
     // value of the lane's step nearest the chunk's output side (A[0] backward, A[K-1] forward).
+    template <bool FULL>
     __device__ float finish(const Args& a, float C) {
-        const float X = apply(excl, apply(wave_in, C));
+        const float Xw = apply(wave_in, C);
+        // value entering this lane = value leaving lane l-1 on its output side
+        const float X = shift_up1(apply(incl, Xw), Xw);
         float A[K];
         if (kBack) {
             float nxt = X;
@@ -193,17 +278,35 @@ struct Chunk {
         }
         float o0[K], o1[K];
         Op::template finish<K, TR>(a.p, d, term, trunc, edge, B, nb, A, X, o0, o1);
-        const bool vec_out = full;
-        store_k<K>(a.out0, p0, valid, vec_out, o0);
-        if (a.out1) store_k<K>(a.out1, p0, valid, vec_out, o1);
+        store_k<K>(a.out0, p0, valid, FULL, o0);
+        if (a.out1) store_k<K>(a.out1, p0, valid, FULL, o1);
         return kBack ? A[0] : A[K - 1];
     }
 };
 
+// One chunk: local scan, the wave composition (unless rows are wave-local) and, through
+// `carry_of`, the value entering the chunk; then the carry application and stores.
+template <bool FULL, class C, class CarryFn>
+__device__ __forceinline__ float run_chunk(C& c, const Args& a, int64_t chunk_lo, int64_t lo,
+                                           int64_t hi, float* s_a, float* s_b, int lane,
+                                           int wave, bool wave_local, bool small,
+                                           CarryFn&& carry_of) {
+    c.template local_scan<FULL>(a, chunk_lo, lo, hi, s_a, s_b, lane, wave, wave_local, small);
+    if (wave_local) {
+        c.wave_in = identity_pair();
+    } else {
+        __syncthreads();
+        c.wave_prefix(s_a, s_b, wave);
+    }
+    return c.template finish<FULL>(a, carry_of());
+}
+
 // Rows kernel: workgroup g owns rows [g*R, g*R + R) and walks them in chunks of E steps
 // aligned to multiples of K, starting from the carry source (the end for backward scans).
+// `wave_local`: every wave's span starts and ends on row edges (T divides 64*K and the chunk
+// is row aligned), so no carry crosses waves and step 5 is skipped.
 template <class Op, typename DT, int K, int W, bool VEC, bool TR>
-__global__ void __launch_bounds__(W * kWave) rows_kernel(Args a, int64_t rows_per_wg) {
+__global__ void __launch_bounds__(W * kWave) rows_kernel(Args a, int64_t rows_per_wg, int wave_local) {
     using C = Chunk<Op, DT, K, W, VEC, TR>;
     constexpr int64_t E = int64_t(W) * kWave * K;
     __shared__ float s_a[W], s_b[W];
@@ -212,19 +315,22 @@ __global__ void __launch_bounds__(W * kWave) rows_kernel(Args a, int64_t rows_pe
     const int64_t row_lo = int64_t(blockIdx.x) * rows_per_wg;
     const int64_t row_hi = min(row_lo + rows_per_wg, a.N);
     const int64_t lo = row_lo * a.T, hi = row_hi * a.T;
+    const bool small = a.N * a.T < (int64_t(1) << 31);
+    const bool can_full = VEC && a.T >= K;
     float carry = 0.f;
+    auto carry_of = [&]() { return carry; };
     if (Op::kBackward) {
         int64_t chunk_hi = (hi + K - 1) / K * K;
         for (;;) {
             const int64_t chunk_lo = chunk_hi - E;
             C c;
-            c.local_scan(a, chunk_lo, lo, hi, s_a, s_b, lane, wave);
-            __syncthreads();
-            c.wave_prefix(s_a, s_b, wave);
-            const float first = c.finish(a, carry);
+            const float first = (can_full && chunk_lo >= lo && chunk_hi <= hi)
+                ? run_chunk<true>(c, a, chunk_lo, lo, hi, s_a, s_b, lane, wave, wave_local, small, carry_of)
+                : run_chunk<false>(c, a, chunk_lo, lo, hi, s_a, s_b, lane, wave, wave_local, small, carry_of);
             if (chunk_lo <= lo) break;
-            // the next chunk (earlier in time) continues from A at chunk_lo
-            if (threadIdx.x == 0) s_carry = first;
+            // the next chunk (earlier in time) continues from A at chunk_lo, held by lane 63 of
+            // wave 0
+            if (threadIdx.x == kWave - 1) s_carry = first;
             __syncthreads();
             carry = s_carry;
             chunk_hi = chunk_lo;
@@ -233,10 +339,9 @@ __global__ void __launch_bounds__(W * kWave) rows_kernel(Args a, int64_t rows_pe
         int64_t chunk_lo = lo / K * K;
         for (;;) {
             C c;
-            c.local_scan(a, chunk_lo, lo, hi, s_a, s_b, lane, wave);
-            __syncthreads();
-            c.wave_prefix(s_a, s_b, wave);
-            const float last = c.finish(a, carry);
+            const float last = (can_full && chunk_lo >= lo && chunk_lo + E <= hi)
+                ? run_chunk<true>(c, a, chunk_lo, lo, hi, s_a, s_b, lane, wave, wave_local, small, carry_of)
+                : run_chunk<false>(c, a, chunk_lo, lo, hi, s_a, s_b, lane, wave, wave_local, small, carry_of);
             if (chunk_lo + E >= hi) break;
             if (threadIdx.x == W * kWave - 1) s_carry = last;
             __syncthreads();
@@ -252,15 +357,17 @@ __global__ void __launch_bounds__(W * kWave) rows_kernel(Args a, int64_t rows_pe
 constexpr uint32_t kMaxPolls = 1u << 20;
 
 // Value entering tile `tile` from its carry-source side, composed from the published maps of
-// the neighbouring tiles of the same row, nearest outermost; run by one full wave.
+// the neighbouring tiles of the same row, nearest outermost; run by one full wave. Lane l looks
+// at the tile 63-l places further (so the nearest tile sits in lane 63, outermost in the
+// prefix scan).
 template <bool kBack>
 __device__ float gather_carry(const uint64_t* rec, int64_t tile, int64_t first_tile,
                               int64_t last_tile, uint32_t tag, int lane, WsHeader* hdr) {
-    // Tiles to visit: tile+1 .. last_tile (backward) or tile-1 down to first_tile (forward).
+    const int dist = kWave - 1 - lane;
     Pair acc = identity_pair();
     int64_t step = 1;
     for (;;) {
-        const int64_t j = kBack ? tile + step + lane : tile - step - lane;
+        const int64_t j = kBack ? tile + step + dist : tile - step - dist;
         const bool inside = kBack ? (j <= last_tile) : (j >= first_tile);
         Pair v = Pair{0.f, 0.f};  // past the row edge: nothing flows in
         bool ready = !inside;
@@ -276,9 +383,10 @@ __device__ float gather_carry(const uint64_t* rec, int64_t tile, int64_t first_t
             }
             const uint64_t rmask = __ballot(ready);
             sever_mask = __ballot(ready && v.b == 0.f);
-            const int first_missing = (rmask == ~0ull) ? 64 : __builtin_ctzll(~rmask);
-            prefix_mask = (first_missing == 64) ? ~0ull : ((1ull << first_missing) - 1ull);
-            if ((sever_mask & prefix_mask) != 0ull || first_missing == 64) break;
+            // ready tiles counted from the nearest (lane 63) down
+            const int run = (rmask == ~0ull) ? 64 : __builtin_clzll(~rmask);
+            prefix_mask = (run == 64) ? ~0ull : ~((~0ull) >> run);
+            if ((sever_mask & prefix_mask) != 0ull || run == 64) break;
             if (polls >= kMaxPolls) {
                 if (lane == 0) st_relaxed(&hdr->error, 1u);
                 return __builtin_nanf("");
@@ -286,10 +394,9 @@ __device__ float gather_carry(const uint64_t* rec, int64_t tile, int64_t first_t
             __builtin_amdgcn_s_sleep(1);
         }
         const uint64_t sev = sever_mask & prefix_mask;
-        const int stop = sev ? __builtin_ctzll(sev) : 64;
-        const Pair mine = (lane <= stop) ? v : identity_pair();
-        const Pair all = wave_scan_inclusive<true>(mine, lane);  // lane 0: lanes 0..63 composed
-        const Pair batch = Pair{__shfl(all.a, 0), __shfl(all.b, 0)};
+        const int stop = sev ? __builtin_clzll(sev) : 64;  // distance of the nearest sever
+        const Pair mine = (dist <= stop) ? v : identity_pair();
+        const Pair batch = read_lane(wave_scan_inclusive(mine, lane), kWave - 1);
         acc = compose(acc, batch);
         if (stop < 64) return acc.a;
         step += kWave;
@@ -311,8 +418,17 @@ __global__ void __launch_bounds__(W * kWave) tiles_kernel(Args a, int64_t num_ti
     const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
 
     if (threadIdx.x == 0) {
-        s_epoch = ld_relaxed(&hdr->epoch);
-        s_ticket = __hip_atomic_fetch_add(&hdr->ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const uint32_t epoch = ld_relaxed(&hdr->epoch);
+        // release: the epoch read above is ordered before the ticket draw; acquire: the last
+        // drawer sees every earlier draw (and so every earlier epoch read) before resetting.
+        const uint32_t ticket = __hip_atomic_fetch_add(&hdr->ticket, 1u, __ATOMIC_ACQ_REL,
+                                                       __HIP_MEMORY_SCOPE_AGENT);
+        if (ticket == uint32_t(num_tiles - 1)) {
+            st_relaxed(&hdr->ticket, 0u);
+            st_relaxed(&hdr->epoch, (epoch + 1u) & 0x7fffffffu);
+        }
+        s_epoch = epoch;
+        s_ticket = ticket;
     }
     __syncthreads();
     const uint32_t epoch = s_epoch;
@@ -328,7 +444,10 @@ __global__ void __launch_bounds__(W * kWave) tiles_kernel(Args a, int64_t num_ti
     const int64_t lo = tile * E, hi = min(lo + E, total);
 
     C c;
-    c.local_scan(a, lo, lo, hi, s_a, s_b, lane, wave);
+    const bool small = total < (int64_t(1) << 31);
+    const bool full = VEC && a.T >= K && hi - lo == E;
+    if (full) c.template local_scan<true>(a, lo, lo, hi, s_a, s_b, lane, wave, false, small);
+    else c.template local_scan<false>(a, lo, lo, hi, s_a, s_b, lane, wave, false, small);
     __syncthreads();
     c.wave_prefix(s_a, s_b, wave);
 
@@ -358,16 +477,9 @@ __global__ void __launch_bounds__(W * kWave) tiles_kernel(Args a, int64_t num_ti
     }
     __syncthreads();
     const float carry = need ? s_carry : 0.f;
-    c.finish(a, carry);
+    if (full) c.template finish<true>(a, carry);
+    else c.template finish<false>(a, carry);
 
-    if (threadIdx.x == 0) {
-        const uint32_t done = __hip_atomic_fetch_add(&hdr->done, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-        if (done == uint32_t(num_tiles - 1)) {
-            st_relaxed(&hdr->ticket, 0u);
-            st_relaxed(&hdr->done, 0u);
-            st_relaxed(&hdr->epoch, (epoch + 1u) & 0x7fffffffu);
-        }
-    }
 }
 
 }  // namespace rlcs

@@ -50,8 +50,8 @@ def test_status_strings_and_version(lib):
 
 def test_workspace_size(lib):
     assert lib.rlcs_workspace_size(0, 5) == 64
-    assert lib.rlcs_workspace_size(64, 4096) == 64 + 16 * (64 * 4096 // 1024)
-    assert lib.rlcs_workspace_size(1, 1025) == 64 + 16 * 2
+    assert lib.rlcs_workspace_size(64, 4096) == 64 + 16 * (64 * 4096 // 4096)
+    assert lib.rlcs_workspace_size(1, 4097) == 64 + 16 * 2
     assert lib.rlcs_workspace_size(-1, 5) == 64
 
 

@@ -65,7 +65,7 @@ def test_rlhf_64x4096(name, var):
     ws = rl.make_workspace(64, 4096, DEV)
     with variant(var):
         check(name, ro, trunc=False, boot=False, ws=ws, gamma=1.0, lam=0.95, label=f"variant {var}")
-    assert int(ws[12:16].view(torch.int32).item()) == 0  # workspace error flag
+    assert int(ws[8:12].view(torch.int32).item()) == 0  # workspace error flag
 
 
 # ------------------------------------------------------------------ shapes and variants
@@ -242,4 +242,4 @@ def test_workspace_reused_across_shapes():
             for name in ("gae", "elig_trace"):
                 ro = make_inputs(name, N, T, seed=N * T)
                 check(name, ro, ws=ws, label=f"{N}x{T}")
-    assert int(ws[12:16].view(torch.int32).item()) == 0
+    assert int(ws[8:12].view(torch.int32).item()) == 0
