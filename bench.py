@@ -18,8 +18,12 @@ Prints one JSON line on stdout:
 from __future__ import annotations
 
 import argparse
+import glob
+import hashlib
 import json
 import os
+import sqlite3
+import statistics
 import sys
 import time
 
@@ -50,6 +54,13 @@ def parse():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--extra", action="store_true", help="also time the other workloads (stderr)")
+    ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="print the counter summary of two rocprofv3 --pmc runs and exit")
+    ap.add_argument("--summarize-trace", metavar="TRACE_DIR",
+                    help="print per-kernel durations of a rocprofv3 --kernel-trace run and exit")
+    ap.add_argument("--profile-pass", action="store_true",
+                    help="eager launches of the timed kernel plus a plain copy of known size, "
+                         "for rocprofv3 runs (no JSON line)")
     return ap.parse_args()
 
 
@@ -77,8 +88,124 @@ def cpu_baseline(ro, seconds):
     }
 
 
+COPY_BYTES = 64 << 20
+KERNEL_TAG = "rows_kernel<rlcs::GaeOp, float, 4, 4, true, true>"
+COUNTERS_FILE = os.path.join(ROOT, "profiles", "gae_4096x256_f32_counters.md")
+
+
+def kernel_source_hash():
+    """sha256 over the HIP sources of the library (kernels and launch code)."""
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2608_17641_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        if name.endswith((".h", ".hip")):
+            with open(os.path.join(csrc, name), "rb") as f:
+                h.update(name.encode() + b"\0" + f.read())
+    return h.hexdigest()
+
+
+def recorded_traffic():
+    """HBM bytes per launch from the committed counter summary, if it was taken on the
+    current kernel sources; otherwise None."""
+    try:
+        text = open(COUNTERS_FILE).read()
+    except OSError:
+        return None
+    fields = dict(l.split(":", 1) for l in text.splitlines() if ":" in l and not l.startswith(" "))
+    if fields.get("source_sha256", "").strip() != kernel_source_hash():
+        return None
+    try:
+        return int(fields["traffic_bytes_per_launch"].strip())
+    except (KeyError, ValueError):
+        return None
+
+
+def _rocpd(path):
+    dbs = sorted(glob.glob(os.path.join(path, "**", "*.db"), recursive=True)) if os.path.isdir(path) else [path]
+    if not dbs:
+        raise SystemExit(f"no rocprofv3 database under {path}")
+    return sqlite3.connect(dbs[0])
+
+
+def summarize_counters(fetch_dir, write_dir):
+    """Counter summary (FETCH_SIZE, WRITE_SIZE per dispatch of the timed kernel, each scaled by
+    the same counter on a plain device copy of COPY_BYTES) in the committed format."""
+    out = {}
+    for counter, path in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
+        cur = _rocpd(path).cursor()
+        rows = cur.execute("select kernel_name, value, grid_size from counters_collection "
+                           "where counter_name = ?", (counter,)).fetchall()
+        mine = [v for n, v, g in rows if KERNEL_TAG in n]
+        # the copy of COPY_BYTES is the largest copy dispatch in the run
+        copies = [(g, v) for n, v, g in rows if "copyBuffer" in n or "copy_kernel" in n]
+        if not mine or not copies:
+            raise SystemExit(f"{counter}: kernel or calibration copy not found in {path}")
+        copy_kib = max(copies)[1]
+        out[counter] = (statistics.mean(mine), len(mine), copy_kib, (COPY_BYTES / 1024) / copy_kib)
+    fetch, write = out["FETCH_SIZE"], out["WRITE_SIZE"]
+    traffic = int(round((fetch[0] * fetch[3] + write[0] * write[3]) * 1024))
+    alg = algorithmic_bytes(N, T)
+    lines = [
+        f"# HBM traffic of {KERNEL_TAG}",
+        f"# workload: GAE {N}x{T} fp32, term+trunc, bootstrap (bench.py --profile-pass)",
+        "commands (repo root, GPU box):",
+        "  rocprofv3 --pmc FETCH_SIZE -d gpurun_out/pmc_fetch -o run -- python bench.py --profile-pass --steps 200 --warmup 20",
+        "  rocprofv3 --pmc WRITE_SIZE -d gpurun_out/pmc_write -o run -- python bench.py --profile-pass --steps 200 --warmup 20",
+        "  python bench.py --summarize-counters gpurun_out/pmc_fetch gpurun_out/pmc_write",
+        f"FETCH_SIZE_KiB_per_dispatch: {fetch[0]:.1f}",
+        f"FETCH_SIZE_dispatches: {fetch[1]}",
+        f"FETCH_SIZE_copy_KiB: {fetch[2]:.1f}",
+        f"FETCH_SIZE_scale: {fetch[3]:.4f}",
+        f"WRITE_SIZE_KiB_per_dispatch: {write[0]:.1f}",
+        f"WRITE_SIZE_dispatches: {write[1]}",
+        f"WRITE_SIZE_copy_KiB: {write[2]:.1f}",
+        f"WRITE_SIZE_scale: {write[3]:.4f}",
+        f"traffic_bytes_per_launch: {traffic}",
+        f"algorithmic_bytes_per_launch: {alg}",
+        f"traffic_over_algorithmic: {traffic / alg:.4f}",
+        f"source_sha256: {kernel_source_hash()}",
+    ]
+    print("\n".join(lines))
+
+
+def summarize_trace(trace_dir):
+    """Per-kernel duration statistics from a rocprofv3 --kernel-trace run."""
+    cur = _rocpd(trace_dir).cursor()
+    rows = cur.execute("select name, start, end from kernels").fetchall()
+    by = {}
+    for n, a, b in rows:
+        by.setdefault(n, []).append((b - a) / 1e3)
+    print(f"{'kernel':<70} {'calls':>6} {'avg_us':>8} {'median_us':>9} {'min_us':>7} {'max_us':>8}")
+    for n, v in sorted(by.items(), key=lambda kv: -sum(kv[1])):
+        v.sort()
+        print(f"{n[:70]:<70} {len(v):>6} {statistics.mean(v):>8.3f} {v[len(v) // 2]:>9.3f} "
+              f"{v[0]:>7.3f} {v[-1]:>8.3f}")
+
+
+def profile_pass(step, args, dev):
+    """Eager launches for kernel-trace / counter runs, then a plain device copy of COPY_BYTES
+    (read COPY_BYTES, write COPY_BYTES) that calibrates the HBM byte counters."""
+    import torch
+    for i in range(args.warmup):
+        step(i)
+    for i in range(args.steps):
+        step(i)
+    src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(f"profile pass: {args.warmup + args.steps} launches, 3 copies of {COPY_BYTES} B", flush=True)
+
+
 def main():
     args = parse()
+    if args.summarize_counters:
+        summarize_counters(*args.summarize_counters)
+        return
+    if args.summarize_trace:
+        summarize_trace(args.summarize_trace)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); rows are independent, so "
               "a multi-GPU run would shard rows with no exchange and is not part of this build.",
@@ -110,6 +237,10 @@ def main():
         s = sets[i % S]
         rl.rlcs_gae(s["r"], s["v"], s["term"], s["trunc"], s["bv"], s["boot"], s["adv"], s["ret"],
                     gamma=GAMMA, lam=LAM)
+
+    if args.profile_pass:
+        profile_pass(step, args, dev)
+        return
 
     # parity of the timed configuration before timing
     import oracle
@@ -181,7 +312,8 @@ def main():
                    "gsteps_per_s": round(N * T / per_step_s / 1e9, 2),
                    "pct_of_peak": round(100 * gbs / PEAK_HBM_GBS, 2)},
         "roofline": {"bound": "hbm", "achieved": round(gbs, 2), "peak": PEAK_HBM_GBS,
-                     "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": None},
+                     "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
+                     "traffic": recorded_traffic()},
     }
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(ro, args.cpu_seconds)
