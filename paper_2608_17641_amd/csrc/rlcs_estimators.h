@@ -3,6 +3,8 @@
 //   kBackward   direction of its recurrence (Section 1, Eq. 1);
 //   kSlots      number of [N, T] data inputs it reads (Args::in[0 .. kSlots-1]);
 //   slot_used   whether slot s is read (the truncation continuation only with truncation);
+//   kTruncSlot  the slot read only at truncated steps (-1: none); a lane loads it only when
+//               one of its steps is truncated;
 //   kFlags      whether it reads term / trunc;
 //   kRowValue   whether it reads the per-row value (bootstrap or carry) at the row edge;
 //   kNbr        number of values it needs from the neighbouring step on the carry-source side
@@ -54,6 +56,7 @@ __device__ __forceinline__ float successor(bool term, bool trunc, bool edge, flo
 struct GaeOp {
     static constexpr bool kBackward = true;
     static constexpr int kSlots = 3;
+    static constexpr int kTruncSlot = 2;  // read only at truncated steps
     static constexpr bool kFlags = true, kRowValue = true;
     static constexpr int kNbr = 1;  // V of the next step
     static constexpr bool slot_used(int s, bool trunc) { return s < 2 || trunc; }
@@ -98,6 +101,7 @@ struct GaeOp {
 struct VtraceOp {
     static constexpr bool kBackward = true;
     static constexpr int kSlots = 4;
+    static constexpr int kTruncSlot = 3;  // read only at truncated steps
     static constexpr bool kFlags = true, kRowValue = true;
     static constexpr int kNbr = 1;  // V of the next step
     static constexpr bool slot_used(int s, bool trunc) { return s < 3 || trunc; }
@@ -153,6 +157,7 @@ struct VtraceOp {
 struct RetraceOp {
     static constexpr bool kBackward = true;
     static constexpr int kSlots = 5;
+    static constexpr int kTruncSlot = 4;  // read only at truncated steps
     static constexpr bool kFlags = true, kRowValue = true;
     static constexpr int kNbr = 2;  // E_pi Q and c of the next step
     static constexpr bool slot_used(int s, bool trunc) { return s < 4 || trunc; }
@@ -204,6 +209,7 @@ struct RetraceOp {
 struct TdLambdaOp {
     static constexpr bool kBackward = true;
     static constexpr int kSlots = 3;
+    static constexpr int kTruncSlot = 2;  // read only at truncated steps
     static constexpr bool kFlags = true, kRowValue = true;
     static constexpr int kNbr = 1;
     static constexpr bool slot_used(int s, bool trunc) { return s < 2 || trunc; }
@@ -254,6 +260,7 @@ struct TdLambdaOp {
 struct DiscountedOp {
     static constexpr bool kBackward = true;
     static constexpr int kSlots = 2;
+    static constexpr int kTruncSlot = 1;  // read only at truncated steps
     static constexpr bool kFlags = true, kRowValue = true;
     static constexpr int kNbr = 0;
     static constexpr bool slot_used(int s, bool trunc) { return s < 1 || trunc; }
@@ -293,6 +300,7 @@ template <bool kDecay, bool kStartsAt>
 struct ForwardOp {
     static constexpr bool kBackward = false;
     static constexpr int kSlots = 1;
+    static constexpr int kTruncSlot = -1;
     static constexpr bool kFlags = true, kRowValue = false;
     static constexpr int kNbr = kStartsAt ? 0 : 1;  // done flag of the previous step
     static constexpr bool slot_used(int s, bool) { return s < 1; }
@@ -348,6 +356,7 @@ template <bool kBack>
 struct AffineOp {
     static constexpr bool kBackward = kBack;
     static constexpr int kSlots = 2;
+    static constexpr int kTruncSlot = -1;
     static constexpr bool kFlags = false, kRowValue = true;
     static constexpr int kNbr = 0;
     static constexpr bool slot_used(int s, bool) { return s < 2; }

@@ -119,19 +119,30 @@ struct Chunk {
             else if (t + K - 1 >= T) { ke = int(T - t); row_e = row + 1; }
         }
         edge = ke >= 0 ? (1u << ke) : 0u;
+        // Flags first: the truncation mask decides whether this lane reads its truncation
+        // continuations, so that dependent load is issued while the data loads are in flight.
         // A missing optional array is read from in[0] instead (in bounds) and the value dropped.
+        uint32_t tw[(K + 3) / 4], rw[(K + 3) / 4];
+        const uint8_t* fallback = reinterpret_cast<const uint8_t*>(a.in[0]);
+        if (Op::kFlags && TR) load_flag_words<K>(a.trunc, p0, rw);
+        if (Op::kFlags) load_flag_words<K>(a.term ? a.term : fallback, p0, tw);
         const bool has_rv = Op::kRowValue && a.row_value;
         const float rv_raw = load_one<DT>(has_rv ? a.row_value : a.in[0], min(row_e, a.N - 1));
         constexpr int kWords = K * int(sizeof(DT)) / 4;
+        constexpr int kTS = TR ? Op::kTruncSlot : -1;
         uint32_t w[NS][kWords];
 #pragma unroll
         for (int s = 0; s < NS; ++s)
-            if (Op::slot_used(s, TR)) load_words<DT, K>(a.in[s], p0, w[s]);
-        uint32_t tw[(K + 3) / 4], rw[(K + 3) / 4];
-        const uint8_t* fallback = reinterpret_cast<const uint8_t*>(a.in[0]);
-        if (Op::kFlags) load_flag_words<K>(a.term ? a.term : fallback, p0, tw);
-        if (Op::kFlags && TR) load_flag_words<K>(a.trunc, p0, rw);
+            if (Op::slot_used(s, TR) && s != kTS) load_words<DT, K>(a.in[s], p0, w[s]);
         if (needs_nbr(lane)) Op::template nbr_load_raw<DT>(a, kBack ? p0 + K : p0 - 1, nraw);
+        trunc = (Op::kFlags && TR) ? flag_mask<K>(rw) : 0u;
+        if constexpr (kTS >= 0) {
+            if (trunc) load_words<DT, K>(a.in[kTS], p0, w[kTS]);
+            else {
+#pragma unroll
+                for (int i = 0; i < kWords; ++i) w[kTS][i] = 0u;
+            }
+        }
 
         // conversions
 #pragma unroll
@@ -143,7 +154,6 @@ struct Chunk {
             }
         }
         term = (Op::kFlags && a.term) ? flag_mask<K>(tw) : 0u;
-        trunc = (Op::kFlags && TR) ? flag_mask<K>(rw) : 0u;
         const float rv = has_rv ? rv_raw : 0.f;
 #pragma unroll
         for (int k = 0; k < K; ++k) B[k] = (k == ke) ? rv : 0.f;
@@ -175,18 +185,19 @@ struct Chunk {
                 if (++t == T) { t = 0; ++row; }
             }
         }
-#pragma unroll
-        for (int s = 0; s < NS; ++s) {
-            if (Op::slot_used(s, TR)) load_k<DT, K>(a.in[s], p0, valid, false, d[s]);
-            else {
-#pragma unroll
-                for (int k = 0; k < K; ++k) d[s][k] = 0.f;
-            }
-        }
         term = 0; trunc = 0;
         if (Op::kFlags) {
             if (a.term) term = load_flags_masked<K>(a.term, p0, valid);
             if (TR) trunc = load_flags_masked<K>(a.trunc, p0, valid);
+        }
+        constexpr int kTS = TR ? Op::kTruncSlot : -1;
+#pragma unroll
+        for (int s = 0; s < NS; ++s) {
+            if (Op::slot_used(s, TR)) load_k<DT, K>(a.in[s], p0, s == kTS ? (valid & trunc) : valid, false, d[s]);
+            else {
+#pragma unroll
+                for (int k = 0; k < K; ++k) d[s][k] = 0.f;
+            }
         }
         if (needs_nbr(lane)) Op::template nbr_load_raw<DT>(a, kBack ? p0 + K : p0 - 1, nraw);
     }
