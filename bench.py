@@ -215,10 +215,9 @@ def main():
     import torch
     import workloads
     import paper_2608_17641_amd as rl
-    from paper_2608_17641_amd.build import is_stale, build
+    from paper_2608_17641_amd.build import build
 
-    if is_stale():
-        build(force=False)
+    build(force=False)  # only if nothing is built yet
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
 

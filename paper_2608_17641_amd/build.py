@@ -50,8 +50,8 @@ def is_stale() -> bool:
 
 
 def build(force: bool = True, verbose: bool = False) -> str:
-    """Compile librlcs.so (always when force, else only if missing or older than a source)."""
-    if not force and not is_stale():
+    """Compile librlcs.so: always when force, else only if it does not exist yet."""
+    if not force and os.path.exists(LIB):
         return LIB
     tmp = LIB + f".tmp{os.getpid()}"
     cmd = command(tmp)
