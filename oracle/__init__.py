@@ -31,10 +31,9 @@ __all__ = [
 
 
 def build(force: bool = False) -> str:
-    """Compile ``liboracle.so`` with gcc (plain -O2, no FMA contraction, no fast-math)."""
-    stale = (not os.path.exists(_LIB)
-             or os.path.getmtime(_LIB) < max(os.path.getmtime(_SRC), os.path.getmtime(_HDR)))
-    if force or stale:
+    """Compile ``liboracle.so`` with gcc (plain -O2, no FMA contraction, no fast-math): always
+    when force, else only if it does not exist yet."""
+    if force or not os.path.exists(_LIB):
         tmp = _LIB + f".tmp{os.getpid()}"
         subprocess.check_call(["gcc", "-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math",
                                "-shared", "-fPIC", "-Wall", "-Werror", "-o", tmp, _SRC, "-lm"])
