@@ -1,6 +1,7 @@
 """Throughput of the credit-assignment hot path on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu] [--extra]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu]
+    python bench.py --extra                      # every workload, table on stderr
 
 Workload: GAE over a 4096 x 256 float32 rollout buffer with termination and truncation flags,
 truncation continuations and per-row bootstraps (seeded synthetic data). One step is one call
@@ -53,7 +54,8 @@ def parse():
     ap.add_argument("--sets", type=int, default=32, help="rotated input/output sets (cold HBM)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
-    ap.add_argument("--extra", action="store_true", help="also time the other workloads (stderr)")
+    ap.add_argument("--extra", action="store_true",
+                    help="time every estimator of every workload (table on stderr, no JSON line)")
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="print the counter summary of two rocprofv3 --pmc runs and exit")
     ap.add_argument("--summarize-trace", metavar="TRACE_DIR",
@@ -198,6 +200,134 @@ def profile_pass(step, args, dev):
     print(f"profile pass: {args.warmup + args.steps} launches, 3 copies of {COPY_BYTES} B", flush=True)
 
 
+# Dense algorithmic bytes per step (data elements of `eb` bytes, 1-byte flags, 4-byte outputs)
+# and the data inputs each estimator reads, for the --extra workloads.
+EXTRA_EST = {
+    "gae": (("r", "v"), 2), "vtrace": (("r", "v", "log_rho"), 2),
+    "retrace": (("r", "q", "eq", "log_rho"), 2), "td_lambda": (("r", "v"), 1),
+    "discounted": (("r",), 1), "elig_trace": (("x",), 1), "episodic_prefix": (("x",), 1),
+}
+
+
+def extra_bytes(name, N, T, eb, trunc, boot):
+    data, outs = EXTRA_EST[name]
+    backward = name not in ("elig_trace", "episodic_prefix")
+    per = len(data) * eb + 1 + (1 + (eb if backward else 0) if trunc else 0) + 4 * outs
+    return N * T * per + (N * eb if (boot and backward) else 0)
+
+
+def run_extra(dev):
+    """Time every estimator of every workload (cold where the data exceeds the Infinity Cache,
+    otherwise over rotated sets), after a parity check of sampled rows against the oracle.
+    Prints a table on stderr."""
+    import torch
+    import oracle
+    import workloads
+    import paper_2608_17641_amd as rl
+
+    def to_dev(a):
+        if a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16)).to(dev).view(torch.bfloat16)
+        return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+
+    def call(name, d, ws, gamma, lam, trunc, boot):
+        tr = d["trunc"] if trunc else None
+        bv = d["bv"] if trunc else None
+        bt = d["boot"] if boot else None
+        if name == "gae":
+            return rl.rlcs_gae(d["r"], d["v"], d["term"], tr, bv, bt, d["o0"], d["o1"], gamma=gamma, lam=lam, ws=ws)
+        if name == "vtrace":
+            return rl.rlcs_vtrace(d["r"], d["v"], d["log_rho"], d["term"], tr, bv, bt, d["o0"], d["o1"], gamma=gamma, ws=ws)
+        if name == "retrace":
+            return rl.rlcs_retrace(d["r"], d["q"], d["eq"], d["log_rho"], d["term"], tr, bv, bt, d["o0"], d["o1"],
+                                   gamma=gamma, lam=lam, ws=ws)
+        if name == "td_lambda":
+            return (rl.rlcs_td_lambda(d["r"], d["v"], d["term"], tr, bv, bt, d["o0"], gamma=gamma, lam=lam, ws=ws),)
+        if name == "discounted":
+            return (rl.rlcs_discounted(d["r"], d["term"], tr, bv, bt, d["o0"], gamma=gamma, ws=ws),)
+        if name == "elig_trace":
+            return (rl.rlcs_elig_trace(d["x"], d["term"], tr, d["o0"], gamma=gamma, lam=lam, ws=ws),)
+        return (rl.rlcs_episodic_prefix(d["x"], d["term"], tr, d["o0"], ws=ws),)
+
+    def ref(name, ro, rows, gamma, lam, trunc, boot):
+        g = lambda k: ro[k][rows]
+        tr = g("trunc") if trunc else None
+        bv = g("bv") if trunc else None
+        bt = g("boot") if boot else None
+        if name == "gae":
+            return oracle.gae(g("r"), g("v"), g("term"), tr, bv, bt, gamma=gamma, lam=lam)
+        if name == "vtrace":
+            return oracle.vtrace(g("r"), g("v"), g("log_rho"), g("term"), tr, bv, bt, gamma=gamma)
+        if name == "retrace":
+            return oracle.retrace(g("r"), g("q"), g("eq"), g("log_rho"), g("term"), tr, bv, bt, gamma=gamma, lam=lam)
+        if name == "td_lambda":
+            return (oracle.td_lambda(g("r"), g("v"), g("term"), tr, bv, bt, gamma=gamma, lam=lam),)
+        if name == "discounted":
+            return (oracle.discounted(g("r"), g("term"), tr, bv, bt, gamma=gamma),)
+        if name == "elig_trace":
+            return (oracle.elig_trace(g("x"), g("term"), tr, gamma=gamma, lam=lam),)
+        return (oracle.episodic_prefix(g("x"), g("term"), tr),)
+
+    plan = [("gae_8x128", 8, 128, "f32", dict(p_term=0.01, p_trunc=0.0), False, True, 0.99, 0.95, ("gae",))]
+    seven = tuple(EXTRA_EST)
+    plan.append(("all7_4096x32", 4096, 32, "f32", dict(p_term=0.02, p_trunc=0.01), True, True, 0.99, 0.95, seven))
+    plan.append(("4096x256", 4096, 256, "f32", dict(p_term=0.02, p_trunc=0.01), True, True, 0.99, 0.95, ("gae", "vtrace")))
+    plan.append(("rlhf_64x4096", 64, 4096, "f32", None, False, False, 1.0, 0.95, ("gae", "td_lambda")))
+    for n_ in (16384, 65536):
+        for t_ in (64, 512, 2048):
+            plan.append((f"bf16_{n_}x{t_}", n_, t_, "bf16", dict(p_term=0.005, p_trunc=0.005), True, True, 0.99, 0.95, seven))
+    print(f"{'workload':<18} {'estimator':<16} {'us/step':>9} {'GB/s':>8} {'%peak':>6} {'Gsteps/s':>9} {'sets':>5} {'max_rel_err':>11}",
+          file=sys.stderr, flush=True)
+    for label, n_, t_, dt, kw, trunc, boot, gamma, lam, ests in plan:
+        ro = (workloads.make_rlhf_rollout(n_, t_, 0) if kw is None
+              else workloads.make_rollout(n_, t_, 0, dtype=dt, **kw))
+        eb = 2 if dt == "bf16" else 4
+        base = {k: to_dev(v) for k, v in ro.items()}
+        set_bytes = sum(v.numel() * v.element_size() for v in base.values()) + 8 * n_ * t_
+        S = max(1, min(32, -(-600_000_000 // set_bytes)))
+        sets = []
+        for i in range(S):
+            d = base if i == 0 else {k: v.clone() for k, v in base.items()}
+            d = dict(d)
+            d["o0"] = torch.empty((n_, t_), dtype=torch.float32, device=dev)
+            d["o1"] = torch.empty((n_, t_), dtype=torch.float32, device=dev)
+            sets.append(d)
+        ws = rl.make_workspace(n_, t_, dev)
+        rows = np.unique(np.concatenate([[0, n_ - 1], np.random.default_rng(1).integers(0, n_, 32)]))
+        for name in ests:
+            outs = call(name, sets[0], ws, gamma, lam, trunc, boot)
+            torch.cuda.synchronize()
+            refs = ref(name, ro, rows, gamma, lam, trunc, boot)
+            rel = 0.0
+            for o, r_ in zip(outs, refs):
+                got = o.index_select(0, torch.from_numpy(rows).to(dev)).double().cpu().numpy()
+                rel = max(rel, float(np.max(np.abs(got - r_))) / (1 + float(np.max(np.abs(r_)))))
+            if rel > (1e-3 if dt == "bf16" else 1e-5):
+                raise SystemExit(f"parity failure in {label} {name}: {rel}")
+            nbytes = extra_bytes(name, n_, t_, eb, trunc, boot)
+            est_us = max(2.0, nbytes / 5e3)
+            K = int(max(20, min(2000, 20000 / est_us)))
+            for i in range(3):
+                call(name, sets[i % S], ws, gamma, lam, trunc, boot)
+            torch.cuda.synchronize()
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(graph):
+                for i in range(K):
+                    call(name, sets[i % S], ws, gamma, lam, trunc, boot)
+            graph.replay()
+            torch.cuda.synchronize()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(); graph.replay(); b.record()
+            torch.cuda.synchronize()
+            us = a.elapsed_time(b) * 1e3 / K
+            gbs = nbytes / (us * 1e-6) / 1e9
+            print(f"{label:<18} {name:<16} {us:>9.3f} {gbs:>8.1f} {100 * gbs / PEAK_HBM_GBS:>5.1f}% "
+                  f"{n_ * t_ / (us * 1e-6) / 1e9:>9.1f} {S:>5} {rel:>11.2e}", file=sys.stderr, flush=True)
+            del graph
+        del sets, base, ws
+        torch.cuda.empty_cache()
+
+
 def main():
     args = parse()
     if args.summarize_counters:
@@ -220,6 +350,9 @@ def main():
     build(force=False)  # only if nothing is built yet
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.extra:
+        run_extra(dev)
+        return
 
     ro = workloads.make_rollout(N, T, seed=0, p_term=0.02, p_trunc=0.01)
     names = ("r", "v", "term", "trunc", "bv", "boot")
