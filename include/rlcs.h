@@ -26,7 +26,8 @@
  *            be NULL, in which case it is not written.
  * Alignment  Every pointer must be aligned to its element size. 16-byte aligned data pointers
  *            (and 4-byte aligned flag pointers) take the vectorised path; others a slower one.
- * Sizes      N, T >= 0. N == 0 or T == 0 is a no-op returning RLCS_OK.
+ * Sizes      N >= 0, 0 <= T <= 2^30, N*T representable. N == 0 or T == 0 is a no-op returning
+ *            RLCS_OK.
  * Params     Discount gamma and trace parameter lambda must lie in [0, 1]; clipping
  *            thresholds rho_bar, c_bar must be > 0 (+infinity allowed). NaN is rejected.
  * Numerics   Arithmetic is float32 (bfloat16 inputs are widened exactly); the scan may

@@ -30,6 +30,9 @@ constexpr int64_t kMinTile = int64_t(kLargeWaves) * kWave * Width<float>::K;
 // is given) only if there are too few rows for whole-row workgroups to fill the GPU.
 constexpr int64_t kSplitBelowRows = 1024;
 
+// Longest supported row (the kernels keep offsets within a row range in 32 bits).
+constexpr int64_t kMaxT = int64_t(1) << 30;
+
 std::atomic<int> g_variant{0};
 
 bool aligned(const void* p, size_t a) { return reinterpret_cast<uintptr_t>(p) % a == 0; }
@@ -43,7 +46,7 @@ rlcs_status check_common(int64_t N, int64_t T, rlcs_dtype dtype,
                          std::initializer_list<const void*> data, std::initializer_list<const void*> outs) {
     if (N < 0 || T < 0) return RLCS_ERR_INVALID_ARG;
     if (dtype != RLCS_F32 && dtype != RLCS_BF16) return RLCS_ERR_DTYPE;
-    if (T > 0 && N > INT64_MAX / T) return RLCS_ERR_INVALID_ARG;
+    if (T > kMaxT || (T > 0 && N > INT64_MAX / T)) return RLCS_ERR_INVALID_ARG;
     const size_t es = dtype_size(dtype);
     for (const void* p : data)
         if (p && !aligned(p, es)) return RLCS_ERR_INVALID_ARG;
@@ -149,6 +152,7 @@ Args make_args(int64_t N, int64_t T, float gamma, float lambda, float rho_bar, f
     Args a{};
     a.N = N;
     a.T = T;
+    a.inv_T = T > 0 ? 1.f / float(T) : 0.f;
     a.p = Params{gamma, lambda, rho_bar, c_bar};
     return a;
 }

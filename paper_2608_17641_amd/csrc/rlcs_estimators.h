@@ -37,6 +37,7 @@ struct Args {
     float* out1;           // may be null
     Params p;
     int64_t N, T;
+    float inv_T;           // 1 / T in fp32 (row bookkeeping)
     void* ws;              // cross-workgroup carry records (split-row variant only)
 };
 

@@ -60,16 +60,25 @@ __device__ __forceinline__ void st_relaxed(T* p, T v) {
 template <bool kBack>
 __device__ __forceinline__ int lane_group(int lane) { return kBack ? (kWave - 1 - lane) : lane; }
 
-// Row and step index of flat position p (32-bit division when the array allows it).
-__device__ __forceinline__ void row_and_step(int64_t p, int64_t T, bool small, int64_t& row, int64_t& t) {
-    if (small) {
-        const uint32_t r = uint32_t(p) / uint32_t(T);
-        row = r;
-        t = int64_t(uint32_t(p) - r * uint32_t(T));
-    } else {
-        row = p / T;
-        t = p - row * T;
-    }
+// Row and step of flat positions relative to a base position whose row and step are known:
+// position base.pos + d (0 <= d, base.t + d < 2^31) is in row base.row + q at step r, where
+// (q, r) = divmod(base.t + d, T). The quotient comes from an fp32 reciprocal (inv_T = 1/T) and
+// is corrected by at most one in either direction, which makes it exact for the offsets that
+// occur here (base.t + d < T + 16*64*K, or < 2^31 with a quotient below 2).
+struct RowBase {
+    int64_t pos, row, t;
+};
+
+__device__ __forceinline__ void row_and_step(const RowBase& b, int64_t p, int64_t T, float inv_T,
+                                             int64_t& row, int64_t& t) {
+    const uint32_t u = uint32_t(b.t + (p - b.pos));
+    const uint32_t Tu = uint32_t(T);
+    uint32_t q = uint32_t(float(u) * inv_T);
+    int64_t r = int64_t(u) - int64_t(q) * int64_t(Tu);
+    if (r < 0) { --q; r += Tu; }
+    else if (r >= int64_t(Tu)) { ++q; r -= Tu; }
+    row = b.row + q;
+    t = r;
 }
 
 // Per-thread state of one chunk between the local scan and the carry application.
@@ -102,14 +111,30 @@ struct Chunk {
         return Op::kNbr > 0 && lane == 0 && bit(valid, ke) && !bit(edge, ke);
     }
 
-    // Step 1 for a chunk whose steps are all in range: every load is issued before any loaded
-    // value is used.
-    __device__ void load_full(const Args& a, bool small, int lane, float (&nraw)[Op::kNbrRaw]) {
+    // Step 1 for a chunk whose steps are all in range. The flag and data loads go out first
+    // (their addresses need nothing but p0); the row bookkeeping, the per-row value and the
+    // neighbour load follow while they are in flight; a lane reads its truncation
+    // continuations only if one of its steps is truncated. No loaded value is used before every
+    // load of the lane has been issued.
+    template <class BaseFn>
+    __device__ void load_full(const Args& a, BaseFn&& base_of, int lane, float (&nraw)[Op::kNbrRaw]) {
         const int64_t T = a.T;
         valid = kAll;
-        int64_t row, t;
-        row_and_step(p0, T, small, row, t);
+        // A missing optional array is read from in[0] instead (in bounds) and the value dropped.
+        uint32_t tw[(K + 3) / 4], rw[(K + 3) / 4];
+        const uint8_t* fallback = reinterpret_cast<const uint8_t*>(a.in[0]);
+        if (Op::kFlags && TR) load_flag_words<K>(a.trunc, p0, rw);
+        if (Op::kFlags) load_flag_words<K>(a.term ? a.term : fallback, p0, tw);
+        constexpr int kWords = K * int(sizeof(DT)) / 4;
+        constexpr int kTS = TR ? Op::kTruncSlot : -1;
+        uint32_t w[NS][kWords];
+#pragma unroll
+        for (int s = 0; s < NS; ++s)
+            if (Op::slot_used(s, TR) && s != kTS) load_words<DT, K>(a.in[s], p0, w[s]);
+
         // at most one row edge among the K steps (T >= K)
+        int64_t row, t;
+        row_and_step(base_of(), p0, T, a.inv_T, row, t);
         int ke = -1;
         int64_t row_e = row;
         if (kBack) {
@@ -119,21 +144,8 @@ struct Chunk {
             else if (t + K - 1 >= T) { ke = int(T - t); row_e = row + 1; }
         }
         edge = ke >= 0 ? (1u << ke) : 0u;
-        // Flags first: the truncation mask decides whether this lane reads its truncation
-        // continuations, so that dependent load is issued while the data loads are in flight.
-        // A missing optional array is read from in[0] instead (in bounds) and the value dropped.
-        uint32_t tw[(K + 3) / 4], rw[(K + 3) / 4];
-        const uint8_t* fallback = reinterpret_cast<const uint8_t*>(a.in[0]);
-        if (Op::kFlags && TR) load_flag_words<K>(a.trunc, p0, rw);
-        if (Op::kFlags) load_flag_words<K>(a.term ? a.term : fallback, p0, tw);
         const bool has_rv = Op::kRowValue && a.row_value;
         const float rv_raw = load_one<DT>(has_rv ? a.row_value : a.in[0], min(row_e, a.N - 1));
-        constexpr int kWords = K * int(sizeof(DT)) / 4;
-        constexpr int kTS = TR ? Op::kTruncSlot : -1;
-        uint32_t w[NS][kWords];
-#pragma unroll
-        for (int s = 0; s < NS; ++s)
-            if (Op::slot_used(s, TR) && s != kTS) load_words<DT, K>(a.in[s], p0, w[s]);
         if (needs_nbr(lane)) Op::template nbr_load_raw<DT>(a, kBack ? p0 + K : p0 - 1, nraw);
         trunc = (Op::kFlags && TR) ? flag_mask<K>(rw) : 0u;
         if constexpr (kTS >= 0) {
@@ -160,7 +172,8 @@ struct Chunk {
     }
 
     // Step 1 for a chunk with steps outside [lo, hi): element-wise, masked.
-    __device__ void load_masked(const Args& a, int64_t lo, int64_t hi, bool small, int lane,
+    template <class BaseFn>
+    __device__ void load_masked(const Args& a, int64_t lo, int64_t hi, BaseFn&& base_of, int lane,
                                 float (&nraw)[Op::kNbrRaw]) {
         const int64_t T = a.T;
         valid = 0;
@@ -173,7 +186,7 @@ struct Chunk {
         if (valid) {
             const int64_t first = p0 + __builtin_ctz(valid);
             int64_t row, t;
-            row_and_step(first, T, small, row, t);
+            row_and_step(base_of(), first, T, a.inv_T, row, t);
 #pragma unroll
             for (int k = 0; k < K; ++k) {
                 if (p0 + k < first || !bit(valid, k)) continue;
@@ -204,14 +217,14 @@ struct Chunk {
 
     // Steps 1-4. Writes the wave's map to s_a/s_b[wave] unless `wave_local`; the caller
     // synchronises.
-    template <bool FULL>
+    template <bool FULL, class BaseFn>
     __device__ void local_scan(const Args& a, int64_t chunk_lo, int64_t lo, int64_t hi,
                                float* s_a, float* s_b, int lane, int wave, bool wave_local,
-                               bool small) {
+                               BaseFn&& base_of) {
         p0 = chunk_lo + int64_t(wave * kWave + lane_group<kBack>(lane)) * K;
         float nraw[Op::kNbrRaw];
-        if (FULL) load_full(a, small, lane, nraw);
-        else load_masked(a, lo, hi, small, lane, nraw);
+        if (FULL) load_full(a, base_of, lane, nraw);
+        else load_masked(a, lo, hi, base_of, lane, nraw);
 
         // Neighbour on the carry-source side of the lane's edge step: lane l-1 holds it, lane 0
         // read it from memory.
@@ -297,12 +310,12 @@ struct Chunk {
 
 // One chunk: local scan, the wave composition (unless rows are wave-local) and, through
 // `carry_of`, the value entering the chunk; then the carry application and stores.
-template <bool FULL, class C, class CarryFn>
+template <bool FULL, class C, class BaseFn, class CarryFn>
 __device__ __forceinline__ float run_chunk(C& c, const Args& a, int64_t chunk_lo, int64_t lo,
                                            int64_t hi, float* s_a, float* s_b, int lane,
-                                           int wave, bool wave_local, bool small,
+                                           int wave, bool wave_local, BaseFn&& base_of,
                                            CarryFn&& carry_of) {
-    c.template local_scan<FULL>(a, chunk_lo, lo, hi, s_a, s_b, lane, wave, wave_local, small);
+    c.template local_scan<FULL>(a, chunk_lo, lo, hi, s_a, s_b, lane, wave, wave_local, base_of);
     if (wave_local) {
         c.wave_in = identity_pair();
     } else {
@@ -326,18 +339,19 @@ __global__ void __launch_bounds__(W * kWave) rows_kernel(Args a, int64_t rows_pe
     const int64_t row_lo = int64_t(blockIdx.x) * rows_per_wg;
     const int64_t row_hi = min(row_lo + rows_per_wg, a.N);
     const int64_t lo = row_lo * a.T, hi = row_hi * a.T;
-    const bool small = a.N * a.T < (int64_t(1) << 31);
     const bool can_full = VEC && a.T >= K;
     float carry = 0.f;
     auto carry_of = [&]() { return carry; };
+    // the workgroup's first step is the start of row row_lo
+    auto base_of = [&]() { return RowBase{lo, row_lo, 0}; };
     if (Op::kBackward) {
         int64_t chunk_hi = (hi + K - 1) / K * K;
         for (;;) {
             const int64_t chunk_lo = chunk_hi - E;
             C c;
             const float first = (can_full && chunk_lo >= lo && chunk_hi <= hi)
-                ? run_chunk<true>(c, a, chunk_lo, lo, hi, s_a, s_b, lane, wave, wave_local, small, carry_of)
-                : run_chunk<false>(c, a, chunk_lo, lo, hi, s_a, s_b, lane, wave, wave_local, small, carry_of);
+                ? run_chunk<true>(c, a, chunk_lo, lo, hi, s_a, s_b, lane, wave, wave_local, base_of, carry_of)
+                : run_chunk<false>(c, a, chunk_lo, lo, hi, s_a, s_b, lane, wave, wave_local, base_of, carry_of);
             if (chunk_lo <= lo) break;
             // the next chunk (earlier in time) continues from A at chunk_lo, held by lane 63 of
             // wave 0
@@ -351,8 +365,8 @@ __global__ void __launch_bounds__(W * kWave) rows_kernel(Args a, int64_t rows_pe
         for (;;) {
             C c;
             const float last = (can_full && chunk_lo >= lo && chunk_lo + E <= hi)
-                ? run_chunk<true>(c, a, chunk_lo, lo, hi, s_a, s_b, lane, wave, wave_local, small, carry_of)
-                : run_chunk<false>(c, a, chunk_lo, lo, hi, s_a, s_b, lane, wave, wave_local, small, carry_of);
+                ? run_chunk<true>(c, a, chunk_lo, lo, hi, s_a, s_b, lane, wave, wave_local, base_of, carry_of)
+                : run_chunk<false>(c, a, chunk_lo, lo, hi, s_a, s_b, lane, wave, wave_local, base_of, carry_of);
             if (chunk_lo + E >= hi) break;
             if (threadIdx.x == W * kWave - 1) s_carry = last;
             __syncthreads();
@@ -455,10 +469,14 @@ __global__ void __launch_bounds__(W * kWave) tiles_kernel(Args a, int64_t num_ti
     const int64_t lo = tile * E, hi = min(lo + E, total);
 
     C c;
-    const bool small = total < (int64_t(1) << 31);
     const bool full = VEC && a.T >= K && hi - lo == E;
-    if (full) c.template local_scan<true>(a, lo, lo, hi, s_a, s_b, lane, wave, false, small);
-    else c.template local_scan<false>(a, lo, lo, hi, s_a, s_b, lane, wave, false, small);
+    // row and step of the tile's first position (uniform; evaluated after the loads are issued)
+    auto base_of = [&]() {
+        const int64_t r = lo / a.T;
+        return RowBase{lo, r, lo - r * a.T};
+    };
+    if (full) c.template local_scan<true>(a, lo, lo, hi, s_a, s_b, lane, wave, false, base_of);
+    else c.template local_scan<false>(a, lo, lo, hi, s_a, s_b, lane, wave, false, base_of);
     __syncthreads();
     c.wave_prefix(s_a, s_b, wave);
 

@@ -79,7 +79,8 @@ def test_gae_validation(lib):
         assert gae(lib, gamma=bad) == n.RLCS_ERR_INVALID_ARG
         assert gae(lib, lam=bad) == n.RLCS_ERR_INVALID_ARG
     assert gae(lib, r=MISALIGNED) == n.RLCS_ERR_INVALID_ARG
-    assert gae(lib, N=2**40, T=2**40) == n.RLCS_ERR_INVALID_ARG  # N*T overflows
+    assert gae(lib, N=2**40, T=2**30) == n.RLCS_ERR_INVALID_ARG  # N*T overflows
+    assert gae(lib, N=1, T=2**30 + 1) == n.RLCS_ERR_INVALID_ARG  # row longer than supported
     # empty problems are no-ops, even with null pointers
     assert gae(lib, N=0, r=None, v=None, adv=None) == n.RLCS_OK
     assert gae(lib, T=0, r=None, v=None, adv=None) == n.RLCS_OK
