@@ -25,7 +25,7 @@ _HDR = os.path.join(_HERE, "rlcs_oracle.h")
 _LIB = os.path.join(_HERE, "liboracle.so")
 
 __all__ = [
-    "build", "gae", "td_lambda", "discounted", "vtrace", "retrace", "elig_trace",
+    "build", "gae", "td_lambda", "discounted", "vtrace", "retrace", "retrace_full", "elig_trace",
     "episodic_prefix", "affine_scan", "widen", "param",
 ]
 
@@ -57,6 +57,8 @@ def _load():
             "oracle_discounted": [D, U8, U8, D, D, D, I64, I64, F64],
             "oracle_vtrace": [D, D, D, U8, U8, D, D, D, D, I64, I64, F64, F64, F64],
             "oracle_retrace": [D, D, D, D, U8, U8, D, D, D, D, I64, I64, F64, F64, F64],
+            "oracle_retrace_full": [D, D, D, ctypes.POINTER(ctypes.c_int32), D, U8, U8, D, D, D,
+                                    D, I64, I64, I64, F64, F64, F64],
             "oracle_elig_trace": [D, U8, U8, D, I64, I64, F64, F64],
             "oracle_episodic_prefix": [D, U8, U8, D, I64, I64, INT],
             "oracle_affine_scan": [D, D, D, D, I64, I64, INT],
@@ -193,6 +195,30 @@ def retrace(r, q, eq, log_rho, term=None, trunc=None, bv=None, boot=None, *, gam
                            _ptr(term, U), _ptr(trunc, U), _ptr(bv, D), _ptr(boot, D),
                            _ptr(delta, D), _ptr(q_ret, D), N, T,
                            param(gamma), param(lam), param(c_bar))
+    return delta, q_ret
+
+
+def retrace_full(r, q, pi, actions, mu, term=None, trunc=None, bv=None, boot=None, *, gamma,
+                 lam, c_bar=1.0):
+    """Full-form Retrace: q and pi are [N, T, A], actions int32 [N, T], mu [N, T] (behaviour
+    probability of the taken action). Returns (delta, q_ret), both fp64 [N, T]."""
+    N, T = _shape(r)
+    q3 = np.asarray(q)
+    if q3.ndim != 3 or q3.shape[:2] != (N, T) or np.asarray(pi).shape != q3.shape:
+        raise ValueError("q and pi must be [N, T, A] arrays matching r")
+    A = q3.shape[2]
+    r, q3, pi3, mu, bv, boot = widen(r), widen(q3), widen(pi), widen(mu), widen(bv), widen(boot)
+    act = np.ascontiguousarray(actions, dtype=np.int32)
+    term, trunc = _flags(term), _flags(trunc)
+    _check(N, T, mu, act, term, trunc, bv)
+    if trunc is not None and bv is None:
+        raise ValueError("bv is required when trunc is given")
+    delta = np.empty((N, T)); q_ret = np.empty((N, T))
+    D, U = ctypes.c_double, ctypes.c_uint8
+    _load().oracle_retrace_full(_ptr(r, D), _ptr(q3, D), _ptr(pi3, D), _ptr(act, ctypes.c_int32),
+                                _ptr(mu, D), _ptr(term, U), _ptr(trunc, U), _ptr(bv, D),
+                                _ptr(boot, D), _ptr(delta, D), _ptr(q_ret, D), N, T, A,
+                                param(gamma), param(lam), param(c_bar))
     return delta, q_ret
 
 

@@ -26,6 +26,7 @@
 
 #include <math.h>
 #include <stddef.h>
+#include <stdlib.h>
 
 /* Flag helpers: a NULL flag array means every flag is clear. */
 static int flag_at(const uint8_t* f, int64_t i) { return f != NULL && f[i] != 0; }
@@ -167,37 +168,78 @@ void oracle_vtrace(const double* r, const double* v, const double* log_rho,
     }
 }
 
-/* Retrace(lambda), Table 1 and Section 3.3.3:
- *   c_t = lambda * min(c_bar, exp(log_rho_t)) for t < T, c_T = 0,
+/* The Retrace(lambda) recurrence of one row given its per-step terms (Table 1 and
+ * Section 3.3.3): with c_T = 0,
  *   delta_t = r_t + gamma succ(E_pi Q)_t - Q(s_t, a_t),
  *   Delta_t = delta_t + gamma c_{t+1} (1 - d_t) Delta_{t+1},  Delta_T = 0,
- *   Q_ret_t = Q(s_t, a_t) + Delta_t.
+ *   Q_ret_t = Q(s_t, a_t) + Delta_t.                                                          */
+static void retrace_row(const double* rr, const double* qq, const double* ee, const double* cc,
+                        const uint8_t* te, const uint8_t* tr, const double* bb, double B,
+                        double* delta, double* q_ret, int64_t T, double gamma) {
+    double Delta_next = 0.0;
+    double c_next = 0.0; /* c_T = 0 */
+    for (int64_t t = T - 1; t >= 0; --t) {
+        const double d = (flag_at(te, t) || flag_at(tr, t)) ? 1.0 : 0.0;
+        const double td = rr[t] + gamma * successor(ee, te, tr, bb, B, t, T) - qq[t];
+        const double Delta = td + gamma * c_next * (1.0 - d) * Delta_next;
+        delta[t] = Delta;
+        q_ret[t] = qq[t] + Delta;
+        Delta_next = Delta;
+        c_next = cc[t];
+    }
+}
+
+/* Retrace(lambda), Table 1 and Section 3.3.3, with c_t = lambda * min(c_bar, exp(log_rho_t)).
  * The row bootstrap is E_pi Q(s_T, .).                                                      */
 void oracle_retrace(const double* r, const double* q, const double* eq, const double* log_rho,
                     const uint8_t* term, const uint8_t* trunc, const double* bv,
                     const double* boot, double* delta, double* q_ret,
                     int64_t N, int64_t T, double gamma, double lambda, double c_bar) {
+    double* c = (double*)malloc(sizeof(double) * (size_t)(T > 0 ? T : 1));
+    if (!c) return;
     for (int64_t n = 0; n < N; ++n) {
-        const double* rr = r + n * T;
-        const double* qq = q + n * T;
-        const double* ee = eq + n * T;
-        const double* lr = log_rho + n * T;
-        const uint8_t* te = row_of_flags(term, n, T);
-        const uint8_t* tr = row_of_flags(trunc, n, T);
-        const double* bb = row_of(bv, n, T);
-        const double B = boot ? boot[n] : 0.0;
-        double Delta_next = 0.0;
-        double c_next = 0.0; /* c_T = 0 */
-        for (int64_t t = T - 1; t >= 0; --t) {
-            const double d = (flag_at(te, t) || flag_at(tr, t)) ? 1.0 : 0.0;
-            const double td = rr[t] + gamma * successor(ee, te, tr, bb, B, t, T) - qq[t];
-            const double Delta = td + gamma * c_next * (1.0 - d) * Delta_next;
-            delta[n * T + t] = Delta;
-            q_ret[n * T + t] = qq[t] + Delta;
-            Delta_next = Delta;
-            c_next = lambda * fmin(c_bar, exp(lr[t]));
-        }
+        for (int64_t t = 0; t < T; ++t) c[t] = lambda * fmin(c_bar, exp(log_rho[n * T + t]));
+        retrace_row(r + n * T, q + n * T, eq + n * T, c, row_of_flags(term, n, T),
+                    row_of_flags(trunc, n, T), row_of(bv, n, T), boot ? boot[n] : 0.0,
+                    delta + n * T, q_ret + n * T, T, gamma);
     }
+    free(c);
+}
+
+/* Full-form Retrace (Sections 3.3.3 and 7.3): the per-step terms come from the [N, T, A]
+ * Q-values and target-policy probabilities, the taken actions and the behaviour
+ * probabilities of the taken actions:
+ *   E_pi Q(s_t) = sum_a pi(a|s_t) Q(s_t, a),  Q(s_t, a_t),
+ *   rho_t = pi(a_t|s_t) / mu(a_t|s_t),  c_t = lambda * min(c_bar, rho_t).                    */
+void oracle_retrace_full(const double* r, const double* q, const double* pi,
+                         const int32_t* actions, const double* mu, const uint8_t* term,
+                         const uint8_t* trunc, const double* bv, const double* boot,
+                         double* delta, double* q_ret, int64_t N, int64_t T, int64_t A,
+                         double gamma, double lambda, double c_bar) {
+    const size_t n_t = (size_t)(T > 0 ? T : 1);
+    double* c = (double*)malloc(sizeof(double) * n_t);
+    double* qa = (double*)malloc(sizeof(double) * n_t);
+    double* eq = (double*)malloc(sizeof(double) * n_t);
+    if (!c || !qa || !eq) { free(c); free(qa); free(eq); return; }
+    for (int64_t n = 0; n < N; ++n) {
+        for (int64_t t = 0; t < T; ++t) {
+            const double* qs = q + (n * T + t) * A;
+            const double* ps = pi + (n * T + t) * A;
+            const int32_t a = actions[n * T + t];
+            double e = 0.0;
+            for (int64_t k = 0; k < A; ++k) e += ps[k] * qs[k];
+            const int in_range = a >= 0 && a < A;
+            const double q_taken = in_range ? qs[a] : 0.0;
+            const double pi_taken = in_range ? ps[a] : 0.0;
+            eq[t] = e;
+            qa[t] = q_taken;
+            c[t] = lambda * fmin(c_bar, pi_taken / mu[n * T + t]);
+        }
+        retrace_row(r + n * T, qa, eq, c, row_of_flags(term, n, T), row_of_flags(trunc, n, T),
+                    row_of(bv, n, T), boot ? boot[n] : 0.0, delta + n * T, q_ret + n * T, T,
+                    gamma);
+    }
+    free(c); free(qa); free(eq);
 }
 
 /* Eligibility traces (forward), Table 1 and Section 3.3.5:

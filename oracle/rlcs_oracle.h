@@ -47,6 +47,17 @@ void oracle_retrace(const double* r, const double* q, const double* eq, const do
                     const double* boot, double* delta, double* q_ret,
                     int64_t N, int64_t T, double gamma, double lambda, double c_bar);
 
+/* Full-form Retrace: Q(s_t, .) and pi(.|s_t) as [N, T, A], the taken actions (int32, [N, T])
+ * and the behaviour probability mu(a_t|s_t) ([N, T]) replace the per-step inputs above:
+ * E_pi Q(s_t) = sum_a pi(a|s_t) Q(s_t, a), Q(s_t, a_t) and rho_t = pi(a_t|s_t) / mu(a_t|s_t).
+ * An action outside [0, A) selects nothing (its Q and pi are taken as 0). bv and boot are
+ * expected values E_pi Q of the true successor / of s_T, as above. */
+void oracle_retrace_full(const double* r, const double* q, const double* pi,
+                         const int32_t* actions, const double* mu, const uint8_t* term,
+                         const uint8_t* trunc, const double* bv, const double* boot,
+                         double* delta, double* q_ret, int64_t N, int64_t T, int64_t A,
+                         double gamma, double lambda, double c_bar);
+
 void oracle_elig_trace(const double* x, const uint8_t* term, const uint8_t* trunc, double* z,
                        int64_t N, int64_t T, double gamma, double lambda);
 

@@ -202,3 +202,43 @@ def prefix_sum(x, term, trunc, starts_at=False):
     return [sum(x[k] for k in range(segment_start(d, t, starts_at), t + 1))
             for t in range(len(x))]
 
+
+
+def retrace_full_sum(r, q3, pi3, actions, mu, term, trunc, bv, B, gamma, lam, c_bar):
+    """Munos et al.'s sum form with the per-step terms taken from the [T, A] tensors:
+    E_pi Q(s_t) = sum_a pi(a|s_t) Q(s_t, a), Q(s_t, a_t), c_t = lambda min(c_bar, pi(a_t)/mu_t);
+    an action outside [0, A) selects nothing."""
+    T = len(r)
+    A = len(q3[0]) if T else 0
+    eq, qt, lr_c = [], [], []
+    for t in range(T):
+        eq.append(sum(float(pi3[t][k]) * float(q3[t][k]) for k in range(A)))
+        a = int(actions[t])
+        ok = 0 <= a < A
+        qt.append(float(q3[t][a]) if ok else 0.0)
+        p = float(pi3[t][a]) if ok else 0.0
+        lr_c.append(lam * min(c_bar, p / float(mu[t])))
+    r, bv = _f(r), _f(bv)
+    d = done_flags(term, trunc)
+
+    def nxt(k):
+        if term[k]:
+            return 0.0
+        if trunc[k]:
+            return bv[k]
+        if k == T - 1:
+            return float(B)
+        return eq[k + 1]
+
+    td = [r[k] + gamma * nxt(k) - qt[k] for k in range(T)]
+    Delta = []
+    for s in range(T):
+        e = segment_end(d, s)
+        acc = 0.0
+        for k in range(s, e + 1):
+            prod = 1.0
+            for i in range(s + 1, k + 1):
+                prod *= lr_c[i]
+            acc += gamma ** (k - s) * prod * td[k]
+        Delta.append(acc)
+    return Delta, [qt[k] + Delta[k] for k in range(T)]

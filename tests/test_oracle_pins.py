@@ -510,3 +510,39 @@ def test_bf16_widening_is_exact():
     assert w.dtype == np.float64
     back = workloads.bf16_bits_from_f32(w.astype(np.float32))
     assert np.array_equal(back, ro["r"])
+
+
+# ---------------------------------------------------------------- full-form Retrace (Section 7.3)
+
+@pytest.mark.parametrize("A", [1, 3, 4, 7])
+def test_retrace_full_brute_force(A):
+    """Full-form Retrace against the Munos sum with the per-step terms computed from the
+    [T, A] tensors in the test, including out-of-range actions and every flag pattern mix."""
+    import workloads
+    N, T = 120, 11
+    ro = workloads.make_retrace_full(N, T, A, seed=40 + A, p_term=0.15, p_trunc=0.15)
+    act = ro["actions"].copy()
+    act[::7, ::3] = A + 2      # out of range: selects nothing
+    act[1::9, 1::4] = -1
+    c_bar = 0.8
+    dl, qr = oracle.retrace_full(ro["r"], ro["q3"], ro["pi3"], act, ro["mu"], ro["term"],
+                                 ro["trunc"], ro["bv"], ro["boot"], gamma=G, lam=L, c_bar=c_bar)
+    res = [brute.retrace_full_sum(ro["r"][n], ro["q3"][n], ro["pi3"][n], act[n], ro["mu"][n],
+                                  ro["term"][n], ro["trunc"][n], ro["bv"][n], ro["boot"][n],
+                                  g32, l32, oracle.param(c_bar)) for n in range(N)]
+    rtol_close(dl, [a for a, _ in res])
+    rtol_close(qr, [b for _, b in res])
+
+
+def test_retrace_full_single_action_is_gae():
+    """A = 1 with pi = mu = 1: E_pi Q = Q, rho = 1, c = lambda, so the correction is the GAE
+    advantage with V = Q (Section 3.3.3 with Table 1's GAE row)."""
+    N, T = 40, 30
+    x = random_inputs(N, T, 41)
+    term, trunc = _flags(N, T, 41)
+    q3 = x["q"][:, :, None]
+    ones = np.ones((N, T))
+    dl, _ = oracle.retrace_full(x["r"], q3, ones[:, :, None], np.zeros((N, T), np.int32), ones,
+                                term, trunc, x["bv"], x["boot"], gamma=G, lam=L)
+    adv, _ = oracle.gae(x["r"], x["q"], term, trunc, x["bv"], x["boot"], gamma=G, lam=L)
+    rtol_close(dl, adv)

@@ -27,6 +27,7 @@ __all__ = [
     "make_rollout",
     "make_rlhf_rollout",
     "make_affine",
+    "make_retrace_full",
     "bf16_bits_from_f32",
     "f32_from_bf16_bits",
     "CONFIGS",
@@ -130,6 +131,41 @@ def make_affine(N: int, T: int, seed: int = 0, *, dtype: str = "f32",
     carry = rng.standard_normal((N,), dtype=np.float32)
     return Rollout(N, T, dtype, alpha=_finish(alpha, dtype), beta=_finish(beta, dtype),
                    carry=_finish(carry, dtype))
+
+
+def _softmax(z: np.ndarray) -> np.ndarray:
+    e = np.exp(z - z.max(axis=-1, keepdims=True))
+    return e / e.sum(axis=-1, keepdims=True)
+
+
+def make_retrace_full(N: int, T: int, A: int, seed: int = 0, *, dtype: str = "f32",
+                      p_term: float = 0.02, p_trunc: float = 0.01,
+                      logit_sigma: float = 1.0) -> Rollout:
+    """Rollout for Retrace in its full form: Q(s_t, .) ~ N(0, 1) over A actions, target and
+    behaviour policies as softmaxes of independent N(0, logit_sigma) logits, actions drawn from
+    the behaviour policy, mu = the behaviour probability of the drawn action (all [N, T] or
+    [N, T, A]); rewards, truncation continuations (E_pi Q of the true successor) and
+    bootstraps ~ N(0, 1); Bernoulli flags. Actions are int32."""
+    if dtype not in ("f32", "bf16"):
+        raise ValueError(f"dtype must be 'f32' or 'bf16', got {dtype!r}")
+    rng = np.random.default_rng(seed)
+    rewards = rng.standard_normal((N, T), dtype=np.float32)
+    q = rng.standard_normal((N, T, A), dtype=np.float32)
+    pi = _softmax(logit_sigma * rng.standard_normal((N, T, A))).astype(np.float32)
+    mu_all = _softmax(logit_sigma * rng.standard_normal((N, T, A)))
+    u = rng.random((N, T, 1))
+    actions = np.minimum((np.cumsum(mu_all, axis=-1) < u).sum(axis=-1), A - 1).astype(np.int32)
+    mu = np.take_along_axis(mu_all, actions[..., None].astype(np.int64), axis=-1)[..., 0]
+    boot = rng.standard_normal((N,), dtype=np.float32)
+    bv = rng.standard_normal((N, T), dtype=np.float32)
+    term = (rng.random((N, T)) < p_term).astype(np.uint8)
+    trunc = (rng.random((N, T)) < p_trunc).astype(np.uint8)
+    ro = Rollout(N, T, dtype, r=_finish(rewards, dtype), q3=_finish(q, dtype),
+                 pi3=_finish(pi, dtype), mu=_finish(mu.astype(np.float32), dtype),
+                 actions=np.ascontiguousarray(actions), bv=_finish(bv, dtype),
+                 boot=_finish(boot, dtype), term=term, trunc=trunc)
+    ro.A = A
+    return ro
 
 
 # The five synthetic workloads (shapes, dtypes, flag rates and parameters).
