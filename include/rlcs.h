@@ -120,6 +120,27 @@ rlcs_status rlcs_retrace(const void* r, const void* q, const void* eq, const voi
                          float gamma, float lambda, float c_bar, rlcs_dtype dtype, void* ws,
                          size_t ws_bytes, rlcs_stream_t stream);
 
+/* Retrace(lambda) in its full form (Section 3.3.3; the [N, T, A] inputs of Section 7.3): the
+ * per-step terms are computed in the kernel from the action axis,
+ *   E_pi Q(s_t) = sum_a pi(a|s_t) Q(s_t, a),  Q(s_t, a_t),  rho_t = pi(a_t|s_t) / mu_t,
+ *   c_t = lambda * min(c_bar, rho_t),  c_T = 0,
+ * and then scanned exactly as rlcs_retrace does.
+ *   q, pi    [N, T, A] Q-values and target-policy probabilities, dtype, contiguous
+ *   actions  [N, T] int32 taken actions; an action outside [0, A) selects nothing (its Q and
+ *            pi are taken as 0)
+ *   mu       [N, T] behaviour-policy probability of the taken action, dtype (nonzero)
+ *   bv, boot E_pi Q of the true successor of a truncated step / of s_T, as for rlcs_retrace
+ *   delta, q_ret  as for rlcs_retrace
+ *   A        number of actions, 1 <= A <= 28 (each workgroup stages its rows' [steps, A]
+ *            slices in LDS)
+ * Rows are never split across workgroups for this entry point; ws is unused.               */
+rlcs_status rlcs_retrace_full(const void* r, const void* q, const void* pi,
+                              const int32_t* actions, const void* mu, const uint8_t* term,
+                              const uint8_t* trunc, const void* bv, const void* boot,
+                              float* delta, float* q_ret, int64_t N, int64_t T, int64_t A,
+                              float gamma, float lambda, float c_bar, rlcs_dtype dtype,
+                              void* ws, size_t ws_bytes, rlcs_stream_t stream);
+
 /* TD(lambda) returns (Table 1; Section 3.3.4):
  *   alpha_t = r_t + gamma (1 - lambda) succ(V)_t,  beta_t = gamma lambda (1 - d_t),  G_T = boot,
  * except that a truncated step continues with the full discount: alpha_t = r_t + gamma bv_t.

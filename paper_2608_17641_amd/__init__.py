@@ -20,7 +20,7 @@ from . import _native
 from ._native import RlcsError
 
 __all__ = [
-    "rlcs_gae", "rlcs_vtrace", "rlcs_retrace", "rlcs_td_lambda", "rlcs_discounted",
+    "rlcs_gae", "rlcs_vtrace", "rlcs_retrace", "rlcs_retrace_full", "rlcs_td_lambda", "rlcs_discounted",
     "rlcs_elig_trace", "rlcs_episodic_prefix", "rlcs_affine_scan", "rlcs_workspace_size",
     "rlcs_version", "rlcs_set_variant_override", "make_workspace", "RlcsError",
 ]
@@ -168,6 +168,31 @@ def rlcs_retrace(r, q, eq, log_rho, term=None, trunc=None, bv=None, boot=None, d
         _call("rlcs_retrace", _ptr(r), _ptr(q), _ptr(eq), _ptr(log_rho), _ptr(term), _ptr(trunc),
               _ptr(bv), _ptr(boot), _ptr(delta), _ptr(q_ret), N, T, gamma, lam, c_bar,
               _DTYPES[dt], wp, wb, _stream(dev))
+    return delta, q_ret
+
+
+def rlcs_retrace_full(r, q, pi, actions, mu, term=None, trunc=None, bv=None, boot=None,
+                      delta=None, q_ret=None, *, gamma: float, lam: float, c_bar: float = 1.0,
+                      want_q_ret: bool = True):
+    """Full-form Retrace: q, pi [N, T, A] (data dtype), actions int32 [N, T], mu [N, T]."""
+    N, T, dt, dev = _prep(r)
+    if not isinstance(q, torch.Tensor) or q.dim() != 3 or tuple(q.shape[:2]) != (N, T):
+        raise ValueError("q must be a [N, T, A] tensor")
+    A = int(q.shape[2])
+    _check_data("q", q, N, T, dt, dev, shape=(N, T, A))
+    _check_data("pi", pi, N, T, dt, dev, shape=(N, T, A))
+    _check_data("mu", mu, N, T, dt, dev); _check_data("bv", bv, N, T, dt, dev)
+    _check_data("boot", boot, N, T, dt, dev, shape=(N,))
+    if not isinstance(actions, torch.Tensor) or actions.dtype != torch.int32 \
+            or tuple(actions.shape) != (N, T) or actions.device != dev or not actions.is_contiguous():
+        raise ValueError(f"actions must be a contiguous int32 [N, T] tensor on {dev}")
+    _check_flags("term", term, N, T, dev); _check_flags("trunc", trunc, N, T, dev)
+    delta = _out("delta", delta, N, T, dev)
+    q_ret = _out("q_ret", q_ret, N, T, dev) if (want_q_ret or q_ret is not None) else None
+    with torch.cuda.device(dev):
+        _call("rlcs_retrace_full", _ptr(r), _ptr(q), _ptr(pi), _ptr(actions), _ptr(mu),
+              _ptr(term), _ptr(trunc), _ptr(bv), _ptr(boot), _ptr(delta), _ptr(q_ret), N, T, A,
+              gamma, lam, c_bar, _DTYPES[dt], None, 0, _stream(dev))
     return delta, q_ret
 
 

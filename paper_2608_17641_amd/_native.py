@@ -36,6 +36,8 @@ PROTOTYPES = {
     "rlcs_vtrace": [_P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _F, _F, _F, _INT, _P, _SZ, _P],
     "rlcs_retrace": [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _F, _F, _F, _INT, _P, _SZ,
                      _P],
+    "rlcs_retrace_full": [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _F, _F, _F,
+                          _INT, _P, _SZ, _P],
     "rlcs_td_lambda": [_P, _P, _P, _P, _P, _P, _P, _I64, _I64, _F, _F, _INT, _P, _SZ, _P],
     "rlcs_discounted": [_P, _P, _P, _P, _P, _P, _I64, _I64, _F, _INT, _P, _SZ, _P],
     "rlcs_elig_trace": [_P, _P, _P, _P, _I64, _I64, _F, _F, _INT, _P, _SZ, _P],

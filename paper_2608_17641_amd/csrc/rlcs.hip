@@ -17,6 +17,10 @@ namespace {
 // longer rows (one row, or a 16*64*K-step tile of one, per workgroup).
 constexpr int kSmallWaves = 4;
 constexpr int kLargeWaves = 16;
+// Staged policies (full-form Retrace) use 4 waves, or 1 when the action axis is too long for
+// a 4-wave chunk's slices to fit the LDS budget.
+constexpr int kStagedWaves = 1;
+constexpr int64_t kStagedLdsBudget = 64 * 1024;
 
 // Steps per lane: one 16-byte vector of each input.
 template <typename DT> struct Width;
@@ -29,6 +33,9 @@ constexpr int64_t kMinTile = int64_t(kLargeWaves) * kWave * Width<float>::K;
 // Rows longer than one large workgroup's chunk are split across workgroups (when a workspace
 // is given) only if there are too few rows for whole-row workgroups to fill the GPU.
 constexpr int64_t kSplitBelowRows = 1024;
+
+// Largest action axis of full-form Retrace (its [steps, A] slices are staged in LDS).
+constexpr int64_t kMaxActions = 28;
 
 // Longest supported row (the kernels keep offsets within a row range in 32 bits).
 constexpr int64_t kMaxT = int64_t(1) << 30;
@@ -62,28 +69,44 @@ struct Plan {
     int64_t num_tiles;    // tiles kernel: grid size
     int64_t rows_per_wg;  // rows kernel: rows per workgroup
     int wave_local;       // rows kernel: no carry crosses waves
+    size_t lds_bytes;     // dynamic LDS (staged policies)
 };
 
 template <class Op, typename DT, bool VEC, bool TR, int W>
 void launch_w(const Args& a, const Plan& p, hipStream_t stream) {
     constexpr int K = Width<DT>::K;
     const dim3 block(W * kWave);
-    if (p.split) {
-        hipLaunchKernelGGL((tiles_kernel<Op, DT, K, W, VEC, TR>), dim3(unsigned(p.num_tiles)),
-                           block, 0, stream, a, p.num_tiles);
-    } else {
-        const int64_t groups = (a.N + p.rows_per_wg - 1) / p.rows_per_wg;
-        hipLaunchKernelGGL((rows_kernel<Op, DT, K, W, VEC, TR>), dim3(unsigned(groups)),
-                           block, 0, stream, a, p.rows_per_wg, p.wave_local);
+    if constexpr (Op::kStaged == 0) {
+        if (p.split) {
+            hipLaunchKernelGGL((tiles_kernel<Op, DT, K, W, VEC, TR>), dim3(unsigned(p.num_tiles)),
+                               block, 0, stream, a, p.num_tiles);
+            return;
+        }
     }
+    const int64_t groups = (a.N + p.rows_per_wg - 1) / p.rows_per_wg;
+    hipLaunchKernelGGL((rows_kernel<Op, DT, K, W, VEC, TR>), dim3(unsigned(groups)), block,
+                       p.lds_bytes, stream, a, p.rows_per_wg, p.wave_local);
 }
 
 template <class Op, typename DT, bool VEC, bool TR>
 rlcs_status launch(const Args& a, const Plan& p, hipStream_t stream) {
-    if (p.split) launch_w<Op, DT, VEC, TR, kLargeWaves>(a, p, stream);
-    else if (p.waves == kSmallWaves) launch_w<Op, DT, VEC, TR, kSmallWaves>(a, p, stream);
-    else launch_w<Op, DT, VEC, TR, kLargeWaves>(a, p, stream);
+    if constexpr (Op::kStaged > 0) {
+        if (p.waves == kStagedWaves) launch_w<Op, DT, VEC, TR, kStagedWaves>(a, p, stream);
+        else launch_w<Op, DT, VEC, TR, kSmallWaves>(a, p, stream);
+    } else {
+        if (p.split) launch_w<Op, DT, VEC, TR, kLargeWaves>(a, p, stream);
+        else if (p.waves == kSmallWaves) launch_w<Op, DT, VEC, TR, kSmallWaves>(a, p, stream);
+        else launch_w<Op, DT, VEC, TR, kLargeWaves>(a, p, stream);
+    }
     return hipGetLastError() == hipSuccess ? RLCS_OK : RLCS_ERR_LAUNCH;
+}
+
+// LDS bytes of a staged policy's chunk with W waves: the staged slots plus the two
+// [steps, A] slices.
+template <class Op, typename DT>
+constexpr int64_t staged_lds_bytes(int W, int64_t A) {
+    const int64_t E = int64_t(W) * kWave * Width<DT>::K;
+    return int64_t(sizeof(float)) * Op::kStaged * (E + 4) + 2 * (E + 1) * A * int64_t(sizeof(DT));
 }
 
 template <class Op, typename DT>
@@ -105,20 +128,29 @@ rlcs_status dispatch_dt(Args& a, bool has_trunc, void* ws, size_t ws_bytes, hipS
     const size_t ws_need = sizeof(WsHeader) + size_t(p.num_tiles) * kWsRecordBytes;
     const bool ws_ok = ws && ws_bytes >= ws_need && aligned(ws, 64) && p.num_tiles < int64_t(UINT32_MAX);
     const int forced = g_variant.load(std::memory_order_relaxed);
-    if (forced == 2) {
-        if (!ws_ok) return RLCS_ERR_WORKSPACE;
-        p.split = true;
-    } else if (forced == 1) {
+    if constexpr (Op::kStaged > 0) {
+        // Staged policies keep whole rows in one workgroup (chunk loop for long rows).
         p.split = false;
+        if (staged_lds_bytes<Op, DT>(kSmallWaves, a.A) <= kStagedLdsBudget) p.waves = kSmallWaves;
+        else if (staged_lds_bytes<Op, DT>(kStagedWaves, a.A) <= kStagedLdsBudget) p.waves = kStagedWaves;
+        else return RLCS_ERR_INVALID_ARG;
+        p.lds_bytes = size_t(staged_lds_bytes<Op, DT>(p.waves, a.A));
     } else {
-        p.split = T > E_large && ws_ok && N < kSplitBelowRows;
+        if (forced == 2) {
+            if (!ws_ok) return RLCS_ERR_WORKSPACE;
+            p.split = true;
+        } else if (forced == 1) {
+            p.split = false;
+        } else {
+            p.split = T > E_large && ws_ok && N < kSplitBelowRows;
+        }
+        p.waves = p.split ? kLargeWaves : ((T <= E_small) ? kSmallWaves : kLargeWaves);
+        p.lds_bytes = 0;
     }
     if (p.split) {
         if (p.num_tiles > INT32_MAX) return RLCS_ERR_INVALID_ARG;
-        p.waves = kLargeWaves;
         a.ws = ws;
     } else {
-        p.waves = (T <= E_small) ? kSmallWaves : kLargeWaves;
         const int64_t E = int64_t(p.waves) * kWave * K;
         // Whole rows per workgroup: as many as fit in one chunk (at least one). When T is not
         // a multiple of K a row range may start mid-vector, costing up to K-1 extra slots.
@@ -208,6 +240,28 @@ rlcs_status rlcs_retrace(const void* r, const void* q, const void* eq, const voi
     a.term = term; a.trunc = trunc; a.row_value = boot;
     a.out0 = delta; a.out1 = q_ret;
     return dispatch<RetraceOp>(a, dtype, trunc != nullptr, ws, ws_bytes, stream);
+}
+
+rlcs_status rlcs_retrace_full(const void* r, const void* q, const void* pi,
+                              const int32_t* actions, const void* mu, const uint8_t* term,
+                              const uint8_t* trunc, const void* bv, const void* boot,
+                              float* delta, float* q_ret, int64_t N, int64_t T, int64_t A,
+                              float gamma, float lambda, float c_bar, rlcs_dtype dtype,
+                              void* ws, size_t ws_bytes, rlcs_stream_t stream) {
+    rlcs_status st = check_common(N, T, dtype, {r, q, pi, mu, bv, boot}, {delta, q_ret});
+    if (st != RLCS_OK) return st;
+    if (!unit_interval(gamma) || !unit_interval(lambda) || !positive(c_bar)) return RLCS_ERR_INVALID_ARG;
+    if (A < 1 || A > kMaxActions) return RLCS_ERR_INVALID_ARG;
+    if (N == 0 || T == 0) return RLCS_OK;
+    if (N * T > INT64_MAX / A) return RLCS_ERR_INVALID_ARG;
+    if (!r || !q || !pi || !actions || !mu || !delta || (trunc && !bv)) return RLCS_ERR_INVALID_ARG;
+    if (!aligned(actions, 4)) return RLCS_ERR_INVALID_ARG;
+    Args a = make_args(N, T, gamma, lambda, 1.f, c_bar);
+    a.in[0] = r; a.in[1] = q; a.in[2] = pi; a.in[3] = mu; a.in[4] = bv;
+    a.actions = actions; a.A = A;
+    a.term = term; a.trunc = trunc; a.row_value = boot;
+    a.out0 = delta; a.out1 = q_ret;
+    return dispatch<RetraceFullOp>(a, dtype, trunc != nullptr, ws, ws_bytes, stream);
 }
 
 rlcs_status rlcs_td_lambda(const void* r, const void* v, const uint8_t* term,

@@ -30,6 +30,8 @@ struct Params {
 
 struct Args {
     const void* in[5];     // data inputs, meaning fixed by the policy
+    const int32_t* actions;  // full-form Retrace: taken actions [N, T]
+    int64_t A;             // full-form Retrace: number of actions
     const uint8_t* term;   // [N, T] or null
     const uint8_t* trunc;  // [N, T] or null
     const void* row_value; // [N] bootstrap / carry, or null (= 0)
@@ -39,6 +41,12 @@ struct Args {
     int64_t N, T;
     float inv_T;           // 1 / T in fp32 (row bookkeeping)
     void* ws;              // cross-workgroup carry records (split-row variant only)
+};
+
+// Defaults shared by the policies: no inputs staged through LDS.
+struct OpBase {
+    static constexpr int kStaged = 0;
+    static constexpr int staged_index(int) { return -1; }
 };
 
 // Bit helpers over K-bit masks.
@@ -54,7 +62,7 @@ __device__ __forceinline__ float successor(bool term, bool trunc, bool edge, flo
 
 // ---------------------------------------------------------------- GAE (Section 3.3.1)
 // in: r, v, bv
-struct GaeOp {
+struct GaeOp : OpBase {
     static constexpr bool kBackward = true;
     static constexpr int kSlots = 3;
     static constexpr int kTruncSlot = 2;  // read only at truncated steps
@@ -99,7 +107,7 @@ struct GaeOp {
 
 // ---------------------------------------------------------------- V-Trace (Section 3.3.2)
 // in: r, v, log_rho, bv
-struct VtraceOp {
+struct VtraceOp : OpBase {
     static constexpr bool kBackward = true;
     static constexpr int kSlots = 4;
     static constexpr int kTruncSlot = 3;  // read only at truncated steps
@@ -155,7 +163,7 @@ struct VtraceOp {
 
 // ---------------------------------------------------------------- Retrace (Section 3.3.3)
 // in: r, q, eq, log_rho, bv
-struct RetraceOp {
+struct RetraceOp : OpBase {
     static constexpr bool kBackward = true;
     static constexpr int kSlots = 5;
     static constexpr int kTruncSlot = 4;  // read only at truncated steps
@@ -205,9 +213,79 @@ struct RetraceOp {
     }
 };
 
+// ---------------------------------------------------------------- full-form Retrace (Section 7.3)
+// Global inputs: in[0] r, in[4] bv (truncated steps only); the [N, T, A] Q-values in[1] and
+// target probabilities in[2], the taken actions and the behaviour probabilities in[3] are
+// reduced per step while the chunk is staged, into three LDS slots:
+//   slot 1: Q(s_t, a_t),  slot 2: E_pi Q(s_t) = sum_a pi(a|s_t) Q(s_t, a),
+//   slot 3: rho_t = pi(a_t|s_t) / mu(a_t|s_t).
+// An action outside [0, A) selects nothing (Q and pi taken as 0). The recurrence is
+// RetraceOp's with c_t = lambda * min(c_bar, rho_t).
+struct RetraceFullOp : OpBase {
+    static constexpr bool kBackward = true;
+    static constexpr int kSlots = 5;
+    static constexpr int kTruncSlot = 4;  // read only at truncated steps
+    static constexpr bool kFlags = true, kRowValue = true;
+    static constexpr int kNbr = 2;  // E_pi Q and c of the next step, read from the stage
+    static constexpr int kNbrRaw = 1;
+    static constexpr int kStaged = 3;
+    static constexpr int staged_index(int s) { return (s >= 1 && s <= 3) ? s - 1 : -1; }
+    static constexpr bool slot_used(int s, bool trunc) { return s == 0 || (s == 4 && trunc); }
+
+    __device__ static float trace(const Params& P, float rho) { return P.lambda * fminf(P.c_bar, rho); }
+
+    // Per-step terms of step s from the staged Q / pi values of that step (LDS) and its action
+    // and behaviour probability.
+    __device__ static void reduce_step(const float* q_row, const float* pi_row, int64_t A,
+                                       int32_t act, float mu, float& q_taken, float& eq,
+                                       float& rho) {
+        float e = 0.f, qa = 0.f, pa = 0.f;
+        for (int64_t k = 0; k < A; ++k) {
+            const float qk = q_row[k], pk = pi_row[k];
+            e = fmaf(pk, qk, e);
+            if (k == act) { qa = qk; pa = pk; }
+        }
+        q_taken = qa;
+        eq = e;
+        rho = pa / mu;
+    }
+    __device__ static void nbr_from_stage(const Params& P, const float* stage, int stride, int i,
+                                          float (&nb)[kNbr]) {
+        nb[0] = stage[1 * stride + i];
+        nb[1] = trace(P, stage[2 * stride + i]);
+    }
+    template <int K>
+    __device__ static void nbr_export(const Params&, const float (&)[kSlots][K], uint32_t, float (&)[kNbr]) {}
+    template <typename DT>
+    __device__ static void nbr_load_raw(const Args&, int64_t, float (&)[kNbrRaw]) {}
+    __device__ static void nbr_fix(const Args&, const float (&)[kNbrRaw], float (&)[kNbr]) {}
+
+    template <int K, bool TR>
+    __device__ static void build(const Params& P, const float (&d)[kSlots][K], uint32_t term,
+                                 uint32_t trunc, uint32_t edge, const float (&B)[K],
+                                 const float (&nb)[kNbr], float (&al)[K], float (&be)[K]) {
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+            const bool te = bit(term, k), tr = TR && bit(trunc, k), ed = bit(edge, k);
+            const float eq_next = (k + 1 < K) ? d[2][k + 1] : nb[0];
+            const float c_next = (k + 1 < K) ? trace(P, d[3][k + 1]) : nb[1];
+            const float s = successor(te, tr, ed, TR ? d[4][k] : 0.f, B[k], eq_next);
+            al[k] = fmaf(P.gamma, s, d[0][k]) - d[1][k];
+            be[k] = (te || tr || ed) ? 0.f : P.gamma * c_next;
+        }
+    }
+    template <int K, bool TR>
+    __device__ static void finish(const Params&, const float (&d)[kSlots][K], uint32_t, uint32_t,
+                                  uint32_t, const float (&)[K], const float (&)[kNbr],
+                                  const float (&A)[K], float, float (&o0)[K], float (&o1)[K]) {
+#pragma unroll
+        for (int k = 0; k < K; ++k) { o0[k] = A[k]; o1[k] = d[1][k] + A[k]; }
+    }
+};
+
 // ---------------------------------------------------------------- TD(lambda) (Section 3.3.4)
 // in: r, v, bv
-struct TdLambdaOp {
+struct TdLambdaOp : OpBase {
     static constexpr bool kBackward = true;
     static constexpr int kSlots = 3;
     static constexpr int kTruncSlot = 2;  // read only at truncated steps
@@ -258,7 +336,7 @@ struct TdLambdaOp {
 
 // ---------------------------------------------------------------- discounted returns (Section 3.3.4)
 // in: r, bv
-struct DiscountedOp {
+struct DiscountedOp : OpBase {
     static constexpr bool kBackward = true;
     static constexpr int kSlots = 2;
     static constexpr int kTruncSlot = 1;  // read only at truncated steps
@@ -298,7 +376,7 @@ struct DiscountedOp {
 // in: x. kDecay: eligibility traces (gamma lambda) vs. prefix sum (1). kStartsAt: a flag at t
 // cuts the carry into t instead of into t+1.
 template <bool kDecay, bool kStartsAt>
-struct ForwardOp {
+struct ForwardOp : OpBase {
     static constexpr bool kBackward = false;
     static constexpr int kSlots = 1;
     static constexpr int kTruncSlot = -1;
@@ -354,7 +432,7 @@ struct ForwardOp {
 // ---------------------------------------------------------------- bare recurrence (Section 4.1)
 // in: alpha, beta; the per-row carry enters at the row edge.
 template <bool kBack>
-struct AffineOp {
+struct AffineOp : OpBase {
     static constexpr bool kBackward = kBack;
     static constexpr int kSlots = 2;
     static constexpr int kTruncSlot = -1;

@@ -93,6 +93,7 @@ struct Chunk {
     static constexpr int NS = Op::kSlots;
     static constexpr int NB = Op::kNbr > 0 ? Op::kNbr : 1;
     static constexpr uint32_t kAll = (K == 32) ? 0xffffffffu : ((1u << K) - 1u);
+    static constexpr int kStride = W * kWave * K + 4;  // staged slot stride (floats)
 
     float d[NS][K];
     float B[K];
@@ -100,6 +101,8 @@ struct Chunk {
     float al[K], be[K];
     uint32_t term, trunc, edge, valid;
     int64_t p0;
+    int sidx;            // p0 - chunk_lo: the lane's first step within the chunk
+    const float* stage;  // staged slots (policies with kStaged > 0)
     Pair incl;     // lanes 0..lane of this wave composed (lane 0 innermost)
     Pair wave_in;  // waves between this wave and the chunk's carry-source edge
 
@@ -108,7 +111,14 @@ struct Chunk {
     // hence inside the array).
     __device__ bool needs_nbr(int lane) const {
         const int ke = kBack ? K - 1 : 0;
-        return Op::kNbr > 0 && lane == 0 && bit(valid, ke) && !bit(edge, ke);
+        return Op::kNbr > 0 && Op::kStaged == 0 && lane == 0 && bit(valid, ke) && !bit(edge, ke);
+    }
+
+    // Staged slot s (Op::staged_index(s) >= 0) of the lane's K steps, from LDS.
+    __device__ void read_staged(int s, uint32_t mask, bool full) {
+        const float* src = stage + Op::staged_index(s) * kStride + sidx;
+#pragma unroll
+        for (int k = 0; k < K; ++k) d[s][k] = (full || bit(mask, k)) ? src[k] : 0.f;
     }
 
     // Step 1 for a chunk whose steps are all in range. The flag and data loads go out first
@@ -159,7 +169,8 @@ struct Chunk {
         // conversions
 #pragma unroll
         for (int s = 0; s < NS; ++s) {
-            if (Op::slot_used(s, TR)) unpack_words<DT, K>(w[s], d[s]);
+            if (Op::staged_index(s) >= 0) read_staged(s, kAll, true);
+            else if (Op::slot_used(s, TR)) unpack_words<DT, K>(w[s], d[s]);
             else {
 #pragma unroll
                 for (int k = 0; k < K; ++k) d[s][k] = 0.f;
@@ -206,7 +217,8 @@ struct Chunk {
         constexpr int kTS = TR ? Op::kTruncSlot : -1;
 #pragma unroll
         for (int s = 0; s < NS; ++s) {
-            if (Op::slot_used(s, TR)) load_k<DT, K>(a.in[s], p0, s == kTS ? (valid & trunc) : valid, false, d[s]);
+            if (Op::staged_index(s) >= 0) read_staged(s, valid, false);
+            else if (Op::slot_used(s, TR)) load_k<DT, K>(a.in[s], p0, s == kTS ? (valid & trunc) : valid, false, d[s]);
             else {
 #pragma unroll
                 for (int k = 0; k < K; ++k) d[s][k] = 0.f;
@@ -220,15 +232,20 @@ struct Chunk {
     template <bool FULL, class BaseFn>
     __device__ void local_scan(const Args& a, int64_t chunk_lo, int64_t lo, int64_t hi,
                                float* s_a, float* s_b, int lane, int wave, bool wave_local,
-                               BaseFn&& base_of) {
-        p0 = chunk_lo + int64_t(wave * kWave + lane_group<kBack>(lane)) * K;
+                               BaseFn&& base_of, const float* staged) {
+        sidx = (wave * kWave + lane_group<kBack>(lane)) * K;
+        p0 = chunk_lo + sidx;
+        stage = staged;
         float nraw[Op::kNbrRaw];
         if (FULL) load_full(a, base_of, lane, nraw);
         else load_masked(a, lo, hi, base_of, lane, nraw);
 
         // Neighbour on the carry-source side of the lane's edge step: lane l-1 holds it, lane 0
-        // read it from memory.
-        if (Op::kNbr > 0) {
+        // read it from memory; staged policies read it from the stage (which covers one step
+        // past the chunk).
+        if constexpr (Op::kStaged > 0) {
+            Op::nbr_from_stage(a.p, stage, kStride, kBack ? sidx + K : sidx - 1, nb);
+        } else if (Op::kNbr > 0) {
             float own[NB];
             Op::template nbr_export<K>(a.p, d, term | trunc, own);
 #pragma unroll
@@ -314,8 +331,9 @@ template <bool FULL, class C, class BaseFn, class CarryFn>
 __device__ __forceinline__ float run_chunk(C& c, const Args& a, int64_t chunk_lo, int64_t lo,
                                            int64_t hi, float* s_a, float* s_b, int lane,
                                            int wave, bool wave_local, BaseFn&& base_of,
-                                           CarryFn&& carry_of) {
-    c.template local_scan<FULL>(a, chunk_lo, lo, hi, s_a, s_b, lane, wave, wave_local, base_of);
+                                           CarryFn&& carry_of, const float* staged) {
+    c.template local_scan<FULL>(a, chunk_lo, lo, hi, s_a, s_b, lane, wave, wave_local, base_of,
+                                staged);
     if (wave_local) {
         c.wave_in = identity_pair();
     } else {
@@ -323,6 +341,78 @@ __device__ __forceinline__ float run_chunk(C& c, const Args& a, int64_t chunk_lo
         c.wave_prefix(s_a, s_b, wave);
     }
     return c.template finish<FULL>(a, carry_of());
+}
+
+// Staging for policies whose per-step terms are reductions over an action axis (full-form
+// Retrace). Steps [chunk_lo, chunk_lo + E] (one past the chunk, for the neighbour) that lie in
+// [lo, N*T) are staged. The chunk's [steps, A] slices of Q (in[1]) and pi (in[2]) are copied to
+// LDS with coalesced element loads, issued eight at a time per thread; after a barrier the
+// owner thread of each step (steps tid, tid + blockDim, ...) reduces its slice into the
+// staged slots. Layout of `dyn`: kStaged slots of E + 4 floats, then the two slices as DT.
+template <class Op, typename DT, int E, int J>
+__device__ void stage_chunk(const Args& a, int64_t chunk_lo, int64_t lo, float* dyn) {
+    constexpr int kStride = E + 4;
+    const int64_t total = a.N * a.T;
+    const int64_t A = a.A;
+    const int64_t s_lo = max(chunk_lo, lo);
+    const int64_t s_hi = min(chunk_lo + E + 1, total);
+    const int64_t n_steps = s_hi > s_lo ? s_hi - s_lo : 0;
+    const int64_t off = s_lo - chunk_lo;
+    DT* sq = reinterpret_cast<DT*>(dyn + Op::kStaged * kStride);
+    DT* sp = sq + int64_t(E + 1) * A;
+    const int nt = blockDim.x, tid = threadIdx.x;
+
+    // actions and behaviour probabilities of this thread's steps
+    int32_t act[J];
+    float mu[J];
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+        const int64_t i = tid + int64_t(j) * nt;  // stage index
+        const int64_t st = chunk_lo + i;
+        const bool ok = i <= E && st >= s_lo && st < s_hi;
+        act[j] = ok ? a.actions[st] : -1;
+        mu[j] = ok ? load_one<DT>(a.in[3], st) : 1.f;
+    }
+    // slices of Q and pi
+    const DT* gq = reinterpret_cast<const DT*>(a.in[1]) + s_lo * A;
+    const DT* gp = reinterpret_cast<const DT*>(a.in[2]) + s_lo * A;
+    const int64_t n_el = n_steps * A;
+    for (int64_t base = tid; base < n_el; base += 8 * int64_t(nt)) {
+        DT vq[8], vp[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int64_t m = base + int64_t(u) * nt;
+            if (m < n_el) { vq[u] = gq[m]; vp[u] = gp[m]; }
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int64_t m = base + int64_t(u) * nt;
+            if (m < n_el) { sq[off * A + m] = vq[u]; sp[off * A + m] = vp[u]; }
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+        const int64_t i = tid + int64_t(j) * nt;
+        if (i > E) continue;
+        const int64_t st = chunk_lo + i;
+        float qa = 0.f, eq = 0.f, rho = 0.f;
+        if (st >= s_lo && st < s_hi) {
+            float e = 0.f;
+            const DT* qr = sq + i * A;
+            const DT* pr = sp + i * A;
+            for (int64_t k = 0; k < A; ++k) {
+                const float qk = widen(qr[k]), pk = widen(pr[k]);
+                e = fmaf(pk, qk, e);
+                if (k == act[j]) { qa = qk; rho = pk; }
+            }
+            eq = e;
+            rho = rho / mu[j];
+        }
+        dyn[0 * kStride + i] = qa;
+        dyn[1 * kStride + i] = eq;
+        dyn[2 * kStride + i] = rho;
+    }
 }
 
 // Rows kernel: workgroup g owns rows [g*R, g*R + R) and walks them in chunks of E steps
@@ -342,16 +432,22 @@ __global__ void __launch_bounds__(W * kWave) rows_kernel(Args a, int64_t rows_pe
     const bool can_full = VEC && a.T >= K;
     float carry = 0.f;
     auto carry_of = [&]() { return carry; };
+    extern __shared__ float s_dyn[];  // staged policies only (sized at launch)
+    const float* stage = Op::kStaged > 0 ? s_dyn : nullptr;
     // the workgroup's first step is the start of row row_lo
     auto base_of = [&]() { return RowBase{lo, row_lo, 0}; };
     if (Op::kBackward) {
         int64_t chunk_hi = (hi + K - 1) / K * K;
         for (;;) {
             const int64_t chunk_lo = chunk_hi - E;
+            if constexpr (Op::kStaged > 0) {
+                stage_chunk<Op, DT, int(E), K + 1>(a, chunk_lo, lo, s_dyn);
+                __syncthreads();
+            }
             C c;
             const float first = (can_full && chunk_lo >= lo && chunk_hi <= hi)
-                ? run_chunk<true>(c, a, chunk_lo, lo, hi, s_a, s_b, lane, wave, wave_local, base_of, carry_of)
-                : run_chunk<false>(c, a, chunk_lo, lo, hi, s_a, s_b, lane, wave, wave_local, base_of, carry_of);
+                ? run_chunk<true>(c, a, chunk_lo, lo, hi, s_a, s_b, lane, wave, wave_local, base_of, carry_of, stage)
+                : run_chunk<false>(c, a, chunk_lo, lo, hi, s_a, s_b, lane, wave, wave_local, base_of, carry_of, stage);
             if (chunk_lo <= lo) break;
             // the next chunk (earlier in time) continues from A at chunk_lo, held by lane 63 of
             // wave 0
@@ -363,10 +459,14 @@ __global__ void __launch_bounds__(W * kWave) rows_kernel(Args a, int64_t rows_pe
     } else {
         int64_t chunk_lo = lo / K * K;
         for (;;) {
+            if constexpr (Op::kStaged > 0) {
+                stage_chunk<Op, DT, int(E), K + 1>(a, chunk_lo, lo, s_dyn);
+                __syncthreads();
+            }
             C c;
             const float last = (can_full && chunk_lo >= lo && chunk_lo + E <= hi)
-                ? run_chunk<true>(c, a, chunk_lo, lo, hi, s_a, s_b, lane, wave, wave_local, base_of, carry_of)
-                : run_chunk<false>(c, a, chunk_lo, lo, hi, s_a, s_b, lane, wave, wave_local, base_of, carry_of);
+                ? run_chunk<true>(c, a, chunk_lo, lo, hi, s_a, s_b, lane, wave, wave_local, base_of, carry_of, stage)
+                : run_chunk<false>(c, a, chunk_lo, lo, hi, s_a, s_b, lane, wave, wave_local, base_of, carry_of, stage);
             if (chunk_lo + E >= hi) break;
             if (threadIdx.x == W * kWave - 1) s_carry = last;
             __syncthreads();
@@ -475,8 +575,9 @@ __global__ void __launch_bounds__(W * kWave) tiles_kernel(Args a, int64_t num_ti
         const int64_t r = lo / a.T;
         return RowBase{lo, r, lo - r * a.T};
     };
-    if (full) c.template local_scan<true>(a, lo, lo, hi, s_a, s_b, lane, wave, false, base_of);
-    else c.template local_scan<false>(a, lo, lo, hi, s_a, s_b, lane, wave, false, base_of);
+    static_assert(Op::kStaged == 0, "staged policies run on the rows kernel only");
+    if (full) c.template local_scan<true>(a, lo, lo, hi, s_a, s_b, lane, wave, false, base_of, nullptr);
+    else c.template local_scan<false>(a, lo, lo, hi, s_a, s_b, lane, wave, false, base_of, nullptr);
     __syncthreads();
     c.wave_prefix(s_a, s_b, wave);
 

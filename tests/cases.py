@@ -36,6 +36,8 @@ def to_device(arr, device):
     import torch
     if arr is None:
         return None
+    if arr.dtype == np.int32:
+        return torch.from_numpy(np.ascontiguousarray(arr)).to(device)
     if arr.dtype == np.uint16:
         return torch.from_numpy(arr.view(np.int16)).to(device).view(torch.bfloat16)
     return torch.from_numpy(np.ascontiguousarray(arr)).to(device)

@@ -120,6 +120,26 @@ def test_other_entry_points_validation(lib):
         == n.RLCS_ERR_INVALID_ARG
 
 
+def test_retrace_full_validation(lib):
+    from paper_2608_17641_amd import _native as n
+    P = None
+
+    def rf(**kw):
+        a = dict(r=FAKE, q=FAKE, pi=FAKE, act=FAKE, mu=FAKE, term=P, trunc=P, bv=P, boot=P,
+                 delta=FAKE2, q_ret=P, N=2, T=3, A=4, gamma=0.9, lam=0.9, c_bar=1.0, dtype=0,
+                 ws=P, wsb=0, s=P)
+        a.update(kw)
+        return lib.rlcs_retrace_full(*a.values())
+    assert rf(A=0) == n.RLCS_ERR_INVALID_ARG
+    assert rf(A=29) == n.RLCS_ERR_INVALID_ARG
+    assert rf(act=None) == n.RLCS_ERR_INVALID_ARG
+    assert rf(mu=None) == n.RLCS_ERR_INVALID_ARG
+    assert rf(pi=None) == n.RLCS_ERR_INVALID_ARG
+    assert rf(act=ctypes.c_void_p(0x10002)) == n.RLCS_ERR_INVALID_ARG  # int32 alignment
+    assert rf(trunc=FAKE) == n.RLCS_ERR_INVALID_ARG
+    assert rf(N=0, q=None) == n.RLCS_OK
+
+
 def test_variant_override_range(lib):
     from paper_2608_17641_amd import _native as n
     assert lib.rlcs_set_variant_override(3) == n.RLCS_ERR_INVALID_ARG

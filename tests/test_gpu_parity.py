@@ -243,3 +243,56 @@ def test_workspace_reused_across_shapes():
                 ro = make_inputs(name, N, T, seed=N * T)
                 check(name, ro, ws=ws, label=f"{N}x{T}")
     assert int(ws[8:12].view(torch.int32).item()) == 0
+
+
+# ------------------------------------------------------------------ full-form Retrace
+
+def _retrace_full_run(ro, *, trunc=True, boot=True, gamma=0.99, lam=0.95, c_bar=1.0, act=None):
+    d = device_inputs(ro, DEV)
+    if act is not None:
+        d["actions"] = torch.from_numpy(act).to(DEV)
+    dl, qr = rl.rlcs_retrace_full(d["r"], d["q3"], d["pi3"], d["actions"], d["mu"], d["term"],
+                                  d["trunc"] if trunc else None, d["bv"] if trunc else None,
+                                  d["boot"] if boot else None, gamma=gamma, lam=lam, c_bar=c_bar)
+    torch.cuda.synchronize()
+    import oracle
+    a = ro["actions"] if act is None else act
+    rd, rq = oracle.retrace_full(ro["r"], ro["q3"], ro["pi3"], a, ro["mu"], ro["term"],
+                                 ro["trunc"] if trunc else None, ro["bv"] if trunc else None,
+                                 ro["boot"] if boot else None, gamma=gamma, lam=lam, c_bar=c_bar)
+    return {"delta": dl, "q_ret": qr}, {"delta": rd, "q_ret": rq}
+
+
+@pytest.mark.parametrize("A", [1, 3, 4, 6, 7, 18, 28])
+@pytest.mark.parametrize("T", [1, 7, 33, 256, 1000, 4097])
+def test_retrace_full_shapes(A, T):
+    N = 23
+    ro = workloads.make_retrace_full(N, T, A, seed=A * 1000 + T, p_term=0.05, p_trunc=0.05)
+    out, ref = _retrace_full_run(ro, c_bar=0.9)
+    assert_parity(out, ref, 1e-5, label=f"retrace_full A={A} T={T}")
+
+
+@pytest.mark.parametrize("A", [4, 18])
+def test_retrace_full_bf16_and_plain(A):
+    ro = workloads.make_retrace_full(300, 129, A, seed=A, dtype="bf16", p_term=0.05, p_trunc=0.05)
+    out, ref = _retrace_full_run(ro)
+    assert_parity(out, ref, 1e-3, label=f"retrace_full bf16 A={A}")
+    ro = workloads.make_retrace_full(300, 256, A, seed=A + 1, p_term=0.05, p_trunc=0.0)
+    out, ref = _retrace_full_run(ro, trunc=False, boot=False)
+    assert_parity(out, ref, 1e-5, label=f"retrace_full plain A={A}")
+
+
+def test_retrace_full_out_of_range_actions():
+    A = 5
+    ro = workloads.make_retrace_full(64, 100, A, seed=77, p_term=0.05, p_trunc=0.05)
+    act = ro["actions"].copy()
+    act[::3, ::7] = A
+    act[1::5, 2::9] = -3
+    out, ref = _retrace_full_run(ro, act=act)
+    assert_parity(out, ref, 1e-5, label="retrace_full out-of-range actions")
+
+
+def test_retrace_full_4096x256():
+    ro = workloads.make_retrace_full(4096, 256, 4, seed=0, p_term=0.02, p_trunc=0.01)
+    out, ref = _retrace_full_run(ro)
+    assert_parity(out, ref, 1e-5, label="retrace_full 4096x256x4")
