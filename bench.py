@@ -56,6 +56,7 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--extra", action="store_true",
                     help="time every estimator of every workload (table on stderr, no JSON line)")
+    ap.add_argument("--only", default="", help="with --extra: only workloads whose label starts so")
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="print the counter summary of two rocprofv3 --pmc runs and exit")
     ap.add_argument("--summarize-trace", metavar="TRACE_DIR",
@@ -216,7 +217,7 @@ def extra_bytes(name, N, T, eb, trunc, boot):
     return N * T * per + (N * eb if (boot and backward) else 0)
 
 
-def run_extra(dev):
+def run_extra(dev, only=""):
     """Time every estimator of every workload (cold where the data exceeds the Infinity Cache,
     otherwise over rotated sets), after a parity check of sampled rows against the oracle.
     Prints a table on stderr."""
@@ -279,6 +280,8 @@ def run_extra(dev):
     print(f"{'workload':<18} {'estimator':<16} {'us/step':>9} {'GB/s':>8} {'%peak':>6} {'Gsteps/s':>9} {'sets':>5} {'max_rel_err':>11}",
           file=sys.stderr, flush=True)
     for label, n_, t_, dt, kw, trunc, boot, gamma, lam, ests in plan:
+        if not label.startswith(only):
+            continue
         ro = (workloads.make_rlhf_rollout(n_, t_, 0) if kw is None
               else workloads.make_rollout(n_, t_, 0, dtype=dt, **kw))
         eb = 2 if dt == "bf16" else 4
@@ -326,6 +329,64 @@ def run_extra(dev):
             del graph
         del sets, base, ws
         torch.cuda.empty_cache()
+    for label, n_, t_, a_ in (("rf_4096x256x4", 4096, 256, 4), ("rf_512x4096x4", 512, 4096, 4),
+                              ("rf_4096x256x18", 4096, 256, 18)):
+        if label.startswith(only):
+            run_retrace_full(label, n_, t_, a_, dev)
+
+
+def run_retrace_full(label, n_, t_, a_, dev):
+    """Full-form Retrace (fp32, truncation), parity on sampled rows, then graph-timed."""
+    import torch
+    import oracle
+    import workloads
+    import paper_2608_17641_amd as rl
+    ro = workloads.make_retrace_full(n_, t_, a_, 0)
+    base = {k: torch.from_numpy(np.ascontiguousarray(v)).to(dev) for k, v in ro.items()}
+    set_bytes = sum(v.numel() * v.element_size() for v in base.values()) + 8 * n_ * t_
+    S = max(1, min(32, -(-600_000_000 // set_bytes)))
+    sets = []
+    for i in range(S):
+        d = dict(base if i == 0 else {k: v.clone() for k, v in base.items()})
+        d["o0"] = torch.empty((n_, t_), dtype=torch.float32, device=dev)
+        d["o1"] = torch.empty((n_, t_), dtype=torch.float32, device=dev)
+        sets.append(d)
+
+    def call(d):
+        rl.rlcs_retrace_full(d["r"], d["q3"], d["pi3"], d["actions"], d["mu"], d["term"], d["trunc"],
+                             d["bv"], d["boot"], d["o0"], d["o1"], gamma=0.99, lam=0.95)
+
+    call(sets[0])
+    torch.cuda.synchronize()
+    rows = np.unique(np.concatenate([[0, n_ - 1], np.random.default_rng(1).integers(0, n_, 32)]))
+    g = lambda k: ro[k][rows]
+    rd, rq = oracle.retrace_full(g("r"), g("q3"), g("pi3"), g("actions"), g("mu"), g("term"),
+                                 g("trunc"), g("bv"), g("boot"), gamma=0.99, lam=0.95)
+    rel = 0.0
+    for o, r_ in ((sets[0]["o0"], rd), (sets[0]["o1"], rq)):
+        got = o.index_select(0, torch.from_numpy(rows).to(dev)).double().cpu().numpy()
+        rel = max(rel, float(np.max(np.abs(got - r_))) / (1 + float(np.max(np.abs(r_)))))
+    if rel > 1e-5:
+        raise SystemExit(f"parity failure in {label}: {rel}")
+    # r, Q and pi [A], action (4 B), mu, term, trunc, bv, two outputs; bootstrap per row
+    nbytes = n_ * t_ * (4 + 8 * a_ + 4 + 4 + 1 + 1 + 4 + 8) + 4 * n_
+    K = int(max(20, min(2000, 20000 / max(2.0, nbytes / 5e3))))
+    for i in range(3):
+        call(sets[i % S])
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for i in range(K):
+            call(sets[i % S])
+    graph.replay()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(); graph.replay(); b.record()
+    torch.cuda.synchronize()
+    us = a.elapsed_time(b) * 1e3 / K
+    gbs = nbytes / (us * 1e-6) / 1e9
+    print(f"{label:<18} {'retrace_full':<16} {us:>9.3f} {gbs:>8.1f} {100 * gbs / PEAK_HBM_GBS:>5.1f}% "
+          f"{n_ * t_ / (us * 1e-6) / 1e9:>9.1f} {S:>5} {rel:>11.2e}", file=sys.stderr, flush=True)
 
 
 def main():
@@ -351,7 +412,7 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     if args.extra:
-        run_extra(dev)
+        run_extra(dev, args.only)
         return
 
     ro = workloads.make_rollout(N, T, seed=0, p_term=0.02, p_trunc=0.01)

@@ -2,24 +2,27 @@
 
     python -m paper_2608_17641_amd.build
 
-produces ``paper_2608_17641_amd/librlcs.so`` from ``csrc/rlcs.hip`` (kernels in
-``csrc/rlcs_*.h``) against the public header ``include/rlcs.h``.
+produces ``paper_2608_17641_amd/librlcs.so`` from the translation units ``csrc/rlcs_*.hip``
+(one per group of entry points, compiled in parallel; kernels in ``csrc/rlcs_*.h``) against
+the public header ``include/rlcs.h``.
 """
 from __future__ import annotations
 
+import glob
 import os
 import shutil
 import subprocess
 import sys
+import tempfile
+from concurrent.futures import ThreadPoolExecutor
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "librlcs.so")
-SOURCES = [os.path.join(CSRC, "rlcs.hip")]
-HEADERS = [os.path.join(CSRC, f) for f in ("rlcs_device.h", "rlcs_estimators.h", "rlcs_kernels.h")]
-HEADERS.append(os.path.join(INCLUDE, "rlcs.h"))
+SOURCES = sorted(glob.glob(os.path.join(CSRC, "rlcs_*.hip")))
+HEADERS = sorted(glob.glob(os.path.join(CSRC, "rlcs_*.h"))) + [os.path.join(INCLUDE, "rlcs.h")]
 
 ARCH = "gfx950"
 
@@ -31,15 +34,20 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found (ROCm is required to build the rlcs library)")
 
 
-def command(out: str = LIB):
-    return [
-        hipcc(), "-O3", f"--offload-arch={ARCH}", "-std=c++17", "-fPIC", "-shared",
-        # packed fp32 instructions are kept out of the generated code
-        "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-        "-Wall", "-Wno-unused-function",
-        f"-I{INCLUDE}", f"-I{CSRC}",
-        "-o", out, *SOURCES,
-    ]
+FLAGS = [
+    "-O3", f"--offload-arch={ARCH}", "-std=c++17", "-fPIC",
+    # packed fp32 instructions are kept out of the generated code
+    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-Wall", "-Wno-unused-function",
+]
+
+
+def compile_command(src: str, obj: str):
+    return [hipcc(), *FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c", "-o", obj, src]
+
+
+def link_command(objs, out: str = LIB):
+    return [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", out, *objs]
 
 
 def is_stale() -> bool:
@@ -49,22 +57,37 @@ def is_stale() -> bool:
     return any(os.path.getmtime(p) > t for p in SOURCES + HEADERS)
 
 
+_NOISE = ("is not a recognized feature for this target", "(ignoring feature)")
+
+
+def _run(cmd):
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    err = "\n".join(l for l in res.stderr.splitlines() if not any(n in l for n in _NOISE))
+    return res.returncode, err
+
+
 def build(force: bool = True, verbose: bool = False) -> str:
     """Compile librlcs.so: always when force, else only if it does not exist yet."""
     if not force and os.path.exists(LIB):
         return LIB
-    tmp = LIB + f".tmp{os.getpid()}"
-    cmd = command(tmp)
-    res = subprocess.run(cmd, capture_output=True, text=True)
-    noise = "is not a recognized feature for this target"
-    err = "\n".join(l for l in res.stderr.splitlines() if noise not in l and "(ignoring feature)" not in l)
-    if res.returncode != 0:
-        if os.path.exists(tmp):
-            os.remove(tmp)
-        raise RuntimeError(f"hipcc failed ({res.returncode}):\n{' '.join(cmd)}\n{err}")
-    if verbose and err.strip():
-        print(err, file=sys.stderr)
-    os.replace(tmp, LIB)
+    with tempfile.TemporaryDirectory(prefix="rlcs_build_") as tmpdir:
+        objs = [os.path.join(tmpdir, os.path.basename(src) + ".o") for src in SOURCES]
+        jobs = min(len(SOURCES), max(1, min(8, os.cpu_count() or 1)))
+        with ThreadPoolExecutor(max_workers=jobs) as pool:
+            results = list(pool.map(lambda so: (so[0], _run(compile_command(*so))),
+                                    zip(SOURCES, objs)))
+        for src, (rc, err) in results:
+            if rc != 0:
+                raise RuntimeError(f"hipcc failed on {src} ({rc}):\n{err}")
+            if verbose and err.strip():
+                print(err, file=sys.stderr)
+        tmp = LIB + f".tmp{os.getpid()}"
+        rc, err = _run(link_command(objs, tmp))
+        if rc != 0:
+            if os.path.exists(tmp):
+                os.remove(tmp)
+            raise RuntimeError(f"link failed ({rc}):\n{err}")
+        os.replace(tmp, LIB)
     return LIB
 
 

@@ -1,0 +1,41 @@
+// Entry points that launch nothing: workspace size, status strings, version, variant override.
+#include "rlcs_dispatch.h"
+
+using namespace rlcs;
+using namespace rlcs::host;
+
+namespace rlcs {
+namespace host {
+std::atomic<int> g_variant{0};
+}  // namespace host
+}  // namespace rlcs
+
+extern "C" {
+
+size_t rlcs_workspace_size(int64_t N, int64_t T) {
+    if (N <= 0 || T <= 0) return sizeof(WsHeader);
+    if (N > INT64_MAX / T) return 0;
+    const int64_t tiles = (N * T + kMinTile - 1) / kMinTile;
+    return sizeof(WsHeader) + size_t(tiles) * kWsRecordBytes;
+}
+
+const char* rlcs_status_string(rlcs_status status) {
+    switch (status) {
+        case RLCS_OK: return "RLCS_OK";
+        case RLCS_ERR_INVALID_ARG: return "RLCS_ERR_INVALID_ARG: invalid size, pointer, parameter or enum";
+        case RLCS_ERR_DTYPE: return "RLCS_ERR_DTYPE: unsupported dtype";
+        case RLCS_ERR_WORKSPACE: return "RLCS_ERR_WORKSPACE: workspace missing or too small";
+        case RLCS_ERR_LAUNCH: return "RLCS_ERR_LAUNCH: kernel launch failed";
+    }
+    return "unknown rlcs_status";
+}
+
+int rlcs_version(void) { return 100; }
+
+rlcs_status rlcs_set_variant_override(int variant) {
+    if (variant < 0 || variant > 2) return RLCS_ERR_INVALID_ARG;
+    g_variant.store(variant, std::memory_order_relaxed);
+    return RLCS_OK;
+}
+
+}  // extern "C"

@@ -102,6 +102,14 @@ __device__ __forceinline__ void unpack_words(const uint32_t* w, float (&out)[K])
     }
 }
 
+// Element k of the DT values packed in a 32-bit word holding element `k` of a block (fp32: the
+// word itself; bf16: the low half for even k, the high half for odd k).
+template <typename DT>
+__device__ __forceinline__ float word_elem(uint32_t word, int k) {
+    if constexpr (sizeof(DT) == 4) return __uint_as_float(word);
+    else return __uint_as_float((k & 1) ? (word & 0xffff0000u) : (word << 16));
+}
+
 // K consecutive elements starting at p0 (a multiple of K). `full`: all K are in range and the
 // pointer is 16-byte aligned, so the load is one or more 16-byte vector loads. Otherwise only
 // elements whose bit is set in `valid` are read; the rest are 0.

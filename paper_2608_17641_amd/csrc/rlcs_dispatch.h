@@ -1,0 +1,200 @@
+// Host-side pieces shared by the entry points: argument checks (all before any HIP call),
+// the choice of kernel variant, and the launches. Each entry point lives in its own
+// translation unit so that the library's kernels compile in parallel.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <atomic>
+#include <climits>
+#include <cstdint>
+#include <initializer_list>
+
+#include "rlcs.h"
+#include "rlcs_kernels.h"
+
+namespace rlcs {
+namespace host {
+
+// Waves per workgroup: 4 for rows of up to 4*64*K steps (several rows per workgroup), 16 for
+// longer rows (one row, or a 16*64*K-step tile of one, per workgroup).
+constexpr int kSmallWaves = 4;
+constexpr int kLargeWaves = 16;
+// Staged policies (full-form Retrace) use 4 waves, or 1 when the action axis is too long for
+// a 4-wave chunk's slices to fit the LDS budget.
+constexpr int kStagedWaves = 1;
+constexpr int64_t kStagedLdsBudget = 64 * 1024;
+
+// Steps per lane: one 16-byte vector of each input.
+template <typename DT> struct Width;
+template <> struct Width<float> { static constexpr int K = 4; };
+template <> struct Width<bf16_t> { static constexpr int K = 8; };
+
+// Smallest tile of the split-row variant (float32), which sizes the workspace.
+constexpr int64_t kMinTile = int64_t(kLargeWaves) * kWave * Width<float>::K;
+
+// Rows longer than one large workgroup's chunk are split across workgroups (when a workspace
+// is given) only if there are too few rows for whole-row workgroups to fill the GPU.
+constexpr int64_t kSplitBelowRows = 1024;
+
+// Largest action axis of full-form Retrace (its [steps, A] slices are staged in LDS).
+constexpr int64_t kMaxActions = 28;
+
+// Longest supported row (the kernels keep offsets within a row range in 32 bits).
+constexpr int64_t kMaxT = int64_t(1) << 30;
+
+// Process-wide kernel-variant override (rlcs_set_variant_override); defined in rlcs_common.hip.
+extern std::atomic<int> g_variant;
+
+inline bool aligned(const void* p, size_t a) { return reinterpret_cast<uintptr_t>(p) % a == 0; }
+inline bool unit_interval(float x) { return x >= 0.f && x <= 1.f; }  // false for NaN
+inline bool positive(float x) { return x > 0.f; }                     // false for NaN, true for +inf
+
+inline size_t dtype_size(rlcs_dtype d) { return d == RLCS_BF16 ? 2 : 4; }
+
+// Common checks of sizes, dtype and the element alignment of every given pointer.
+inline rlcs_status check_common(int64_t N, int64_t T, rlcs_dtype dtype,
+                         std::initializer_list<const void*> data, std::initializer_list<const void*> outs) {
+    if (N < 0 || T < 0) return RLCS_ERR_INVALID_ARG;
+    if (dtype != RLCS_F32 && dtype != RLCS_BF16) return RLCS_ERR_DTYPE;
+    if (T > kMaxT || (T > 0 && N > INT64_MAX / T)) return RLCS_ERR_INVALID_ARG;
+    const size_t es = dtype_size(dtype);
+    for (const void* p : data)
+        if (p && !aligned(p, es)) return RLCS_ERR_INVALID_ARG;
+    for (const void* p : outs)
+        if (p && !aligned(p, 4)) return RLCS_ERR_INVALID_ARG;
+    return RLCS_OK;
+}
+
+// How one call is run.
+struct Plan {
+    bool split;           // tiles kernel (rows split across workgroups) vs rows kernel
+    int waves;            // waves per workgroup
+    int64_t num_tiles;    // tiles kernel: grid size
+    int64_t rows_per_wg;  // rows kernel: rows per workgroup
+    int wave_local;       // rows kernel: no carry crosses waves
+    size_t lds_bytes;     // dynamic LDS (staged policies)
+};
+
+template <class Op, typename DT, bool VEC, bool TR, int W>
+void launch_w(const Args& a, const Plan& p, hipStream_t stream) {
+    constexpr int K = Width<DT>::K;
+    const dim3 block(W * kWave);
+    if constexpr (Op::kStaged == 0) {
+        if (p.split) {
+            hipLaunchKernelGGL((tiles_kernel<Op, DT, K, W, VEC, TR>), dim3(unsigned(p.num_tiles)),
+                               block, 0, stream, a, p.num_tiles);
+            return;
+        }
+    }
+    const int64_t groups = (a.N + p.rows_per_wg - 1) / p.rows_per_wg;
+    hipLaunchKernelGGL((rows_kernel<Op, DT, K, W, VEC, TR>), dim3(unsigned(groups)), block,
+                       p.lds_bytes, stream, a, p.rows_per_wg, p.wave_local);
+}
+
+template <class Op, typename DT, bool VEC, bool TR>
+rlcs_status launch(const Args& a, const Plan& p, hipStream_t stream) {
+    if constexpr (Op::kStaged > 0) {
+        if (p.waves == kStagedWaves) launch_w<Op, DT, VEC, TR, kStagedWaves>(a, p, stream);
+        else launch_w<Op, DT, VEC, TR, kSmallWaves>(a, p, stream);
+    } else {
+        if (p.split) launch_w<Op, DT, VEC, TR, kLargeWaves>(a, p, stream);
+        else if (p.waves == kSmallWaves) launch_w<Op, DT, VEC, TR, kSmallWaves>(a, p, stream);
+        else launch_w<Op, DT, VEC, TR, kLargeWaves>(a, p, stream);
+    }
+    return hipGetLastError() == hipSuccess ? RLCS_OK : RLCS_ERR_LAUNCH;
+}
+
+// LDS bytes of a staged policy's chunk with W waves: the staged slots plus the two
+// [steps, A] slices.
+template <class Op, typename DT>
+constexpr int64_t staged_lds_bytes(int W, int64_t A) {
+    const int64_t E = int64_t(W) * kWave * Width<DT>::K;
+    const int64_t per_block = 16 / int64_t(sizeof(DT));
+    const int64_t cap = ((E + 1) * A + 3 * per_block) / per_block * per_block;  // see stage_chunk
+    return int64_t(sizeof(float)) * Op::kStaged * (E + 4) + 2 * cap * int64_t(sizeof(DT));
+}
+
+template <class Op, typename DT>
+rlcs_status dispatch_dt(Args& a, bool has_trunc, void* ws, size_t ws_bytes, hipStream_t stream) {
+    constexpr int K = Width<DT>::K;
+    constexpr int64_t E_small = int64_t(kSmallWaves) * kWave * K;
+    constexpr int64_t E_large = int64_t(kLargeWaves) * kWave * K;
+    const int64_t N = a.N, T = a.T, total = N * T;
+
+    // Vector path: 16-byte data and output vectors, K-byte flag vectors.
+    bool vec = true;
+    for (int s = 0; s < Op::kSlots; ++s)
+        if (Op::slot_used(s, has_trunc) && !aligned(a.in[s], 16)) vec = false;
+    if (!aligned(a.out0, 16) || (a.out1 && !aligned(a.out1, 16))) vec = false;
+    if (Op::kFlags && ((a.term && !aligned(a.term, K)) || (has_trunc && !aligned(a.trunc, K)))) vec = false;
+
+    Plan p{};
+    p.num_tiles = (total + E_large - 1) / E_large;
+    const size_t ws_need = sizeof(WsHeader) + size_t(p.num_tiles) * kWsRecordBytes;
+    const bool ws_ok = ws && ws_bytes >= ws_need && aligned(ws, 64) && p.num_tiles < int64_t(UINT32_MAX);
+    const int forced = g_variant.load(std::memory_order_relaxed);
+    if constexpr (Op::kStaged > 0) {
+        // Staged policies keep whole rows in one workgroup (chunk loop for long rows).
+        p.split = false;
+        if (staged_lds_bytes<Op, DT>(kSmallWaves, a.A) <= kStagedLdsBudget) p.waves = kSmallWaves;
+        else if (staged_lds_bytes<Op, DT>(kStagedWaves, a.A) <= kStagedLdsBudget) p.waves = kStagedWaves;
+        else return RLCS_ERR_INVALID_ARG;
+        p.lds_bytes = size_t(staged_lds_bytes<Op, DT>(p.waves, a.A));
+    } else {
+        if (forced == 2) {
+            if (!ws_ok) return RLCS_ERR_WORKSPACE;
+            p.split = true;
+        } else if (forced == 1) {
+            p.split = false;
+        } else {
+            p.split = T > E_large && ws_ok && N < kSplitBelowRows;
+        }
+        p.waves = p.split ? kLargeWaves : ((T <= E_small) ? kSmallWaves : kLargeWaves);
+        p.lds_bytes = 0;
+    }
+    if (p.split) {
+        if (p.num_tiles > INT32_MAX) return RLCS_ERR_INVALID_ARG;
+        a.ws = ws;
+    } else {
+        const int64_t E = int64_t(p.waves) * kWave * K;
+        // Whole rows per workgroup: as many as fit in one chunk (at least one). When T is not
+        // a multiple of K a row range may start mid-vector, costing up to K-1 extra slots.
+        const int64_t slack = (T % K == 0) ? 0 : K - 1;
+        p.rows_per_wg = (T <= E - slack) ? (E - slack) / T : 1;
+        if ((N + p.rows_per_wg - 1) / p.rows_per_wg > INT32_MAX) return RLCS_ERR_INVALID_ARG;
+        // Rows never straddle waves when T divides a wave's span (and is a multiple of K).
+        p.wave_local = (T % K == 0 && (int64_t(kWave) * K) % T == 0) ? 1 : 0;
+    }
+
+    if constexpr (Op::kFlags) {
+        if (has_trunc) {
+            return vec ? launch<Op, DT, true, true>(a, p, stream)
+                       : launch<Op, DT, false, true>(a, p, stream);
+        }
+    }
+    return vec ? launch<Op, DT, true, false>(a, p, stream)
+               : launch<Op, DT, false, false>(a, p, stream);
+}
+
+template <class Op>
+rlcs_status dispatch(Args& a, rlcs_dtype dtype, bool has_trunc, void* ws, size_t ws_bytes,
+                     rlcs_stream_t stream) {
+    if (a.N == 0 || a.T == 0) return RLCS_OK;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    if (dtype == RLCS_BF16) return dispatch_dt<Op, bf16_t>(a, has_trunc, ws, ws_bytes, s);
+    return dispatch_dt<Op, float>(a, has_trunc, ws, ws_bytes, s);
+}
+
+inline Args make_args(int64_t N, int64_t T, float gamma, float lambda, float rho_bar, float c_bar) {
+    Args a{};
+    a.N = N;
+    a.T = T;
+    a.inv_T = T > 0 ? 1.f / float(T) : 0.f;
+    a.p = Params{gamma, lambda, rho_bar, c_bar};
+    return a;
+}
+
+
+}  // namespace host
+}  // namespace rlcs

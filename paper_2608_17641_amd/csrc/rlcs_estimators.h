@@ -32,6 +32,7 @@ struct Args {
     const void* in[5];     // data inputs, meaning fixed by the policy
     const int32_t* actions;  // full-form Retrace: taken actions [N, T]
     int64_t A;             // full-form Retrace: number of actions
+    int stage_vec;         // full-form Retrace: Q and pi are 16-byte aligned
     const uint8_t* term;   // [N, T] or null
     const uint8_t* trunc;  // [N, T] or null
     const void* row_value; // [N] bootstrap / carry, or null (= 0)
@@ -234,20 +235,37 @@ struct RetraceFullOp : OpBase {
 
     __device__ static float trace(const Params& P, float rho) { return P.lambda * fminf(P.c_bar, rho); }
 
-    // Per-step terms of step s from the staged Q / pi values of that step (LDS) and its action
-    // and behaviour probability.
-    __device__ static void reduce_step(const float* q_row, const float* pi_row, int64_t A,
-                                       int32_t act, float mu, float& q_taken, float& eq,
-                                       float& rho) {
+    // Staged terms of one step from its rows Q(s_t, .) and pi(.|s_t) (in LDS), its action and
+    // its behaviour probability: v = {Q(s_t, a_t), E_pi Q(s_t), rho_t}. The expectation sums
+    // the actions in order. `rows16`: both rows start on 16-byte boundaries and hold whole
+    // 16-byte blocks, read one block at a time. An action outside [0, A) selects nothing.
+    template <typename DT>
+    __device__ __forceinline__ static void reduce_step(const DT* q_row, const DT* pi_row, int64_t A, bool rows16,
+                                       int32_t act, float mu, float (&v)[kStaged]) {
+        constexpr int kPer = 16 / int(sizeof(DT));
         float e = 0.f, qa = 0.f, pa = 0.f;
-        for (int64_t k = 0; k < A; ++k) {
-            const float qk = q_row[k], pk = pi_row[k];
-            e = fmaf(pk, qk, e);
-            if (k == act) { qa = qk; pa = pk; }
+        if (rows16) {
+            for (int64_t b = 0; b < A / kPer; ++b) {
+                const u32x4 bq = *reinterpret_cast<const u32x4*>(q_row + b * kPer);
+                const u32x4 bp = *reinterpret_cast<const u32x4*>(pi_row + b * kPer);
+#pragma unroll
+                for (int u = 0; u < kPer; ++u) {
+                    const float qk = word_elem<DT>(bq[u * 4 / kPer], u);
+                    const float pk = word_elem<DT>(bp[u * 4 / kPer], u);
+                    e = fmaf(pk, qk, e);
+                    if (b * kPer + u == act) { qa = qk; pa = pk; }
+                }
+            }
+        } else {
+            for (int64_t k = 0; k < A; ++k) {
+                const float qk = widen(q_row[k]), pk = widen(pi_row[k]);
+                e = fmaf(pk, qk, e);
+                if (k == act) { qa = qk; pa = pk; }
+            }
         }
-        q_taken = qa;
-        eq = e;
-        rho = pa / mu;
+        v[0] = qa;
+        v[1] = e;
+        v[2] = pa / mu;
     }
     __device__ static void nbr_from_stage(const Params& P, const float* stage, int stride, int i,
                                           float (&nb)[kNbr]) {

@@ -25,6 +25,8 @@
 //                only ever waits for tiles that started before it.
 #pragma once
 
+#include <type_traits>
+
 #include "rlcs_estimators.h"
 
 namespace rlcs {
@@ -59,6 +61,11 @@ __device__ __forceinline__ void st_relaxed(T* p, T v) {
 // lane l and the wave scan is a prefix scan over lanes.
 template <bool kBack>
 __device__ __forceinline__ int lane_group(int lane) { return kBack ? (kWave - 1 - lane) : lane; }
+
+// A hook that does nothing.
+struct Nop {
+    __device__ void operator()() const {}
+};
 
 // Row and step of flat positions relative to a base position whose row and step are known:
 // position base.pos + d (0 <= d, base.t + d < 2^31) is in row base.row + q at step r, where
@@ -121,72 +128,90 @@ struct Chunk {
         for (int k = 0; k < K; ++k) d[s][k] = (full || bit(mask, k)) ? src[k] : 0.f;
     }
 
+    // Raw words of a FULL chunk's loads, between load_full and convert_full.
+    static constexpr int kWords = K * int(sizeof(DT)) / 4;
+    static constexpr int kTS = TR ? Op::kTruncSlot : -1;
+    uint32_t w_[NS][kWords];
+    uint32_t tw_[(K + 3) / 4], rw_[(K + 3) / 4];
+    float rv_raw_;
+    int ke_;
+
     // Step 1 for a chunk whose steps are all in range. The flag and data loads go out first
     // (their addresses need nothing but p0); the row bookkeeping, the per-row value and the
     // neighbour load follow while they are in flight; a lane reads its truncation
     // continuations only if one of its steps is truncated. No loaded value is used before every
-    // load of the lane has been issued.
-    template <class BaseFn>
-    __device__ void load_full(const Args& a, BaseFn&& base_of, int lane, float (&nraw)[Op::kNbrRaw]) {
+    // load of the lane has been issued. Staged policies convert later (convert_full after the
+    // stage is complete), so that nothing waits for a load while the staging copies, issued
+    // after the flags, are in flight; they read the continuations unconditionally, since
+    // choosing by the flags would wait for the copies.
+    template <class BaseFn, class PreFn>
+    __device__ void load_full(const Args& a, BaseFn&& base_of, int lane, float (&nraw)[Op::kNbrRaw],
+                              PreFn&& pre) {
         const int64_t T = a.T;
         valid = kAll;
         // A missing optional array is read from in[0] instead (in bounds) and the value dropped.
-        uint32_t tw[(K + 3) / 4], rw[(K + 3) / 4];
         const uint8_t* fallback = reinterpret_cast<const uint8_t*>(a.in[0]);
-        if (Op::kFlags && TR) load_flag_words<K>(a.trunc, p0, rw);
-        if (Op::kFlags) load_flag_words<K>(a.term ? a.term : fallback, p0, tw);
-        constexpr int kWords = K * int(sizeof(DT)) / 4;
-        constexpr int kTS = TR ? Op::kTruncSlot : -1;
-        uint32_t w[NS][kWords];
+        if (Op::kFlags && TR) load_flag_words<K>(a.trunc, p0, rw_);
+        if (Op::kFlags) load_flag_words<K>(a.term ? a.term : fallback, p0, tw_);
+        pre();
 #pragma unroll
         for (int s = 0; s < NS; ++s)
-            if (Op::slot_used(s, TR) && s != kTS) load_words<DT, K>(a.in[s], p0, w[s]);
+            if (Op::slot_used(s, TR) && s != kTS) load_words<DT, K>(a.in[s], p0, w_[s]);
 
         // at most one row edge among the K steps (T >= K)
         int64_t row, t;
         row_and_step(base_of(), p0, T, a.inv_T, row, t);
-        int ke = -1;
+        ke_ = -1;
         int64_t row_e = row;
         if (kBack) {
-            if (t + K - 1 >= T - 1) ke = int(T - 1 - t);
+            if (t + K - 1 >= T - 1) ke_ = int(T - 1 - t);
         } else {
-            if (t == 0) ke = 0;
-            else if (t + K - 1 >= T) { ke = int(T - t); row_e = row + 1; }
+            if (t == 0) ke_ = 0;
+            else if (t + K - 1 >= T) { ke_ = int(T - t); row_e = row + 1; }
         }
-        edge = ke >= 0 ? (1u << ke) : 0u;
+        edge = ke_ >= 0 ? (1u << ke_) : 0u;
         const bool has_rv = Op::kRowValue && a.row_value;
-        const float rv_raw = load_one<DT>(has_rv ? a.row_value : a.in[0], min(row_e, a.N - 1));
+        rv_raw_ = load_one<DT>(has_rv ? a.row_value : a.in[0], min(row_e, a.N - 1));
         if (needs_nbr(lane)) Op::template nbr_load_raw<DT>(a, kBack ? p0 + K : p0 - 1, nraw);
-        trunc = (Op::kFlags && TR) ? flag_mask<K>(rw) : 0u;
-        if constexpr (kTS >= 0) {
-            if (trunc) load_words<DT, K>(a.in[kTS], p0, w[kTS]);
-            else {
+        if constexpr (Op::kStaged > 0) {
+            if constexpr (kTS >= 0) load_words<DT, K>(a.in[kTS], p0, w_[kTS]);
+        } else {
+            trunc = (Op::kFlags && TR) ? flag_mask<K>(rw_) : 0u;
+            if constexpr (kTS >= 0) {
+                if (trunc) load_words<DT, K>(a.in[kTS], p0, w_[kTS]);
+                else {
 #pragma unroll
-                for (int i = 0; i < kWords; ++i) w[kTS][i] = 0u;
+                    for (int i = 0; i < kWords; ++i) w_[kTS][i] = 0u;
+                }
             }
+            convert_full(a);
         }
+    }
 
-        // conversions
+    // The conversions of load_full.
+    __device__ void convert_full(const Args& a) {
+        if constexpr (Op::kStaged > 0) trunc = (Op::kFlags && TR) ? flag_mask<K>(rw_) : 0u;
 #pragma unroll
         for (int s = 0; s < NS; ++s) {
-            if (Op::staged_index(s) >= 0) read_staged(s, kAll, true);
-            else if (Op::slot_used(s, TR)) unpack_words<DT, K>(w[s], d[s]);
+            if (Op::staged_index(s) >= 0) continue;  // read from LDS in the scan
+            if (Op::slot_used(s, TR)) unpack_words<DT, K>(w_[s], d[s]);
             else {
 #pragma unroll
                 for (int k = 0; k < K; ++k) d[s][k] = 0.f;
             }
         }
-        term = (Op::kFlags && a.term) ? flag_mask<K>(tw) : 0u;
-        const float rv = has_rv ? rv_raw : 0.f;
+        term = (Op::kFlags && a.term) ? flag_mask<K>(tw_) : 0u;
+        const float rv = (Op::kRowValue && a.row_value) ? rv_raw_ : 0.f;
 #pragma unroll
-        for (int k = 0; k < K; ++k) B[k] = (k == ke) ? rv : 0.f;
+        for (int k = 0; k < K; ++k) B[k] = (k == ke_) ? rv : 0.f;
     }
 
     // Step 1 for a chunk with steps outside [lo, hi): element-wise, masked.
-    template <class BaseFn>
+    template <class BaseFn, class PreFn>
     __device__ void load_masked(const Args& a, int64_t lo, int64_t hi, BaseFn&& base_of, int lane,
-                                float (&nraw)[Op::kNbrRaw]) {
+                                float (&nraw)[Op::kNbrRaw], PreFn&& pre) {
         const int64_t T = a.T;
+        pre();
         valid = 0;
 #pragma unroll
         for (int k = 0; k < K; ++k)
@@ -214,11 +239,10 @@ struct Chunk {
             if (a.term) term = load_flags_masked<K>(a.term, p0, valid);
             if (TR) trunc = load_flags_masked<K>(a.trunc, p0, valid);
         }
-        constexpr int kTS = TR ? Op::kTruncSlot : -1;
 #pragma unroll
         for (int s = 0; s < NS; ++s) {
-            if (Op::staged_index(s) >= 0) read_staged(s, valid, false);
-            else if (Op::slot_used(s, TR)) load_k<DT, K>(a.in[s], p0, s == kTS ? (valid & trunc) : valid, false, d[s]);
+            if (Op::staged_index(s) >= 0) continue;  // read from LDS in the scan
+            if (Op::slot_used(s, TR)) load_k<DT, K>(a.in[s], p0, s == kTS ? (valid & trunc) : valid, false, d[s]);
             else {
 #pragma unroll
                 for (int k = 0; k < K; ++k) d[s][k] = 0.f;
@@ -228,17 +252,27 @@ struct Chunk {
     }
 
     // Steps 1-4. Writes the wave's map to s_a/s_b[wave] unless `wave_local`; the caller
-    // synchronises.
-    template <bool FULL, class BaseFn>
+    // synchronises. Staged policies: `pre` issues the chunk's staging copies (called once the
+    // flag loads are out, so that waiting for the flags does not wait for the copies) and `mid`
+    // completes the stage (called after every load of the lane is issued, before the staged
+    // slots are read).
+    template <bool FULL, class BaseFn, class PreFn, class MidFn>
     __device__ void local_scan(const Args& a, int64_t chunk_lo, int64_t lo, int64_t hi,
                                float* s_a, float* s_b, int lane, int wave, bool wave_local,
-                               BaseFn&& base_of, const float* staged) {
+                               BaseFn&& base_of, const float* staged, PreFn&& pre, MidFn&& mid) {
         sidx = (wave * kWave + lane_group<kBack>(lane)) * K;
         p0 = chunk_lo + sidx;
         stage = staged;
         float nraw[Op::kNbrRaw];
-        if (FULL) load_full(a, base_of, lane, nraw);
-        else load_masked(a, lo, hi, base_of, lane, nraw);
+        if (FULL) load_full(a, base_of, lane, nraw, pre);
+        else load_masked(a, lo, hi, base_of, lane, nraw, pre);
+        mid();
+        if constexpr (Op::kStaged > 0) {
+            if (FULL) convert_full(a);
+#pragma unroll
+            for (int s = 0; s < NS; ++s)
+                if (Op::staged_index(s) >= 0) read_staged(s, valid, FULL);
+        }
 
         // Neighbour on the carry-source side of the lane's edge step: lane l-1 holds it, lane 0
         // read it from memory; staged policies read it from the stage (which covers one step
@@ -327,13 +361,14 @@ struct Chunk {
 
 // One chunk: local scan, the wave composition (unless rows are wave-local) and, through
 // `carry_of`, the value entering the chunk; then the carry application and stores.
-template <bool FULL, class C, class BaseFn, class CarryFn>
+template <bool FULL, class C, class BaseFn, class CarryFn, class PreFn, class MidFn>
 __device__ __forceinline__ float run_chunk(C& c, const Args& a, int64_t chunk_lo, int64_t lo,
                                            int64_t hi, float* s_a, float* s_b, int lane,
                                            int wave, bool wave_local, BaseFn&& base_of,
-                                           CarryFn&& carry_of, const float* staged) {
+                                           CarryFn&& carry_of, const float* staged, PreFn&& pre,
+                                           MidFn&& mid) {
     c.template local_scan<FULL>(a, chunk_lo, lo, hi, s_a, s_b, lane, wave, wave_local, base_of,
-                                staged);
+                                staged, pre, mid);
     if (wave_local) {
         c.wave_in = identity_pair();
     } else {
@@ -344,76 +379,127 @@ __device__ __forceinline__ float run_chunk(C& c, const Args& a, int64_t chunk_lo
 }
 
 // Staging for policies whose per-step terms are reductions over an action axis (full-form
-// Retrace). Steps [chunk_lo, chunk_lo + E] (one past the chunk, for the neighbour) that lie in
-// [lo, N*T) are staged. The chunk's [steps, A] slices of Q (in[1]) and pi (in[2]) are copied to
-// LDS with coalesced element loads, issued eight at a time per thread; after a barrier the
-// owner thread of each step (steps tid, tid + blockDim, ...) reduces its slice into the
-// staged slots. Layout of `dyn`: kStaged slots of E + 4 floats, then the two slices as DT.
+// Retrace). Steps [chunk_lo, chunk_lo + E] that lie in [lo, N*T) are staged (one step past the
+// chunk, for the neighbour). `issue` starts copying the chunk's [steps, A] slices of Q (in[1])
+// and pi (in[2]) to LDS and loads the steps' actions and behaviour probabilities (in[3]);
+// `commit` completes the copies and, after a barrier, the owner thread of each step (steps
+// tid, tid + blockDim, ...) reduces its slices into the Op::kStaged staged slots. The caller
+// synchronises before the slots are read.
+//
+// Layout of `dyn` (16-byte aligned): kStaged slots of E + 4 floats, then the two slices as DT,
+// `cap` elements each (the size staged_lds_bytes on the host assumes). With 16-byte aligned
+// tensors the 16-byte blocks covering a slice go straight from global memory to LDS
+// (global_load_lds_dwordx4: lane l of a wave fills the 16 bytes at the wave-uniform LDS
+// address plus 16*l), with no register round trip and every block of the chunk in flight at
+// once; LDS element 0 is then the first element of the first block. The one block that can
+// reach past the end of the tensors, and the whole slices of unaligned tensors, are copied
+// element-wise.
 template <class Op, typename DT, int E, int J>
-__device__ void stage_chunk(const Args& a, int64_t chunk_lo, int64_t lo, float* dyn) {
-    constexpr int kStride = E + 4;
-    const int64_t total = a.N * a.T;
-    const int64_t A = a.A;
-    const int64_t s_lo = max(chunk_lo, lo);
-    const int64_t s_hi = min(chunk_lo + E + 1, total);
-    const int64_t n_steps = s_hi > s_lo ? s_hi - s_lo : 0;
-    const int64_t off = s_lo - chunk_lo;
-    DT* sq = reinterpret_cast<DT*>(dyn + Op::kStaged * kStride);
-    DT* sp = sq + int64_t(E + 1) * A;
-    const int nt = blockDim.x, tid = threadIdx.x;
-
-    // actions and behaviour probabilities of this thread's steps
+struct Stager {
+    static constexpr int64_t kPerBlock = 16 / int64_t(sizeof(DT));
+    static constexpr int kStride = E + 4;
+    static_assert((Op::kStaged * kStride * sizeof(float)) % 16 == 0, "slices must be 16-byte aligned");
     int32_t act[J];
     float mu[J];
-#pragma unroll
-    for (int j = 0; j < J; ++j) {
-        const int64_t i = tid + int64_t(j) * nt;  // stage index
-        const int64_t st = chunk_lo + i;
-        const bool ok = i <= E && st >= s_lo && st < s_hi;
-        act[j] = ok ? a.actions[st] : -1;
-        mu[j] = ok ? load_one<DT>(a.in[3], st) : 1.f;
+    int64_t s_lo, s_hi;      // staged steps
+    int64_t el_hi, e0;       // one past the slices' last element; flat element at LDS element 0
+    int64_t el_copy;         // elements [el_copy, el_hi) are copied element-wise
+
+    __device__ static int64_t cap(int64_t A) {
+        return ((int64_t(E + 1) * A + 3 * kPerBlock) / kPerBlock) * kPerBlock;
     }
-    // slices of Q and pi
-    const DT* gq = reinterpret_cast<const DT*>(a.in[1]) + s_lo * A;
-    const DT* gp = reinterpret_cast<const DT*>(a.in[2]) + s_lo * A;
-    const int64_t n_el = n_steps * A;
-    for (int64_t base = tid; base < n_el; base += 8 * int64_t(nt)) {
-        DT vq[8], vp[8];
+
+    __device__ __forceinline__ void issue(const Args& a, int64_t chunk_lo, int64_t lo, float* dyn) {
+        const int64_t total = a.N * a.T, A = a.A;
+        const int nt = blockDim.x, tid = threadIdx.x;
+        s_lo = max(chunk_lo, lo);
+        s_hi = max(min(chunk_lo + E + 1, total), s_lo);
+        // unconditional loads from a clamped step (s_lo is in range), so that no branch waits
+        // for them
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            const int64_t m = base + int64_t(u) * nt;
-            if (m < n_el) { vq[u] = gq[m]; vp[u] = gp[m]; }
+        for (int j = 0; j < J; ++j) {
+            const int64_t i = tid + int64_t(j) * nt;  // stage index
+            const int64_t st = chunk_lo + i;
+            const bool ok = i <= E && st >= s_lo && st < s_hi;
+            const int64_t sc = ok ? st : s_lo;
+            const int32_t act_raw = a.actions[sc];
+            const float mu_raw = load_one<DT>(a.in[3], sc);
+            act[j] = ok ? act_raw : -1;
+            mu[j] = ok ? mu_raw : 1.f;
         }
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            const int64_t m = base + int64_t(u) * nt;
-            if (m < n_el) { sq[off * A + m] = vq[u]; sp[off * A + m] = vp[u]; }
+        const int64_t el_lo = s_lo * A;
+        el_hi = s_hi * A;
+        if (!a.stage_vec) {
+            e0 = el_lo;
+            el_copy = el_lo;
+            return;
         }
-    }
-    __syncthreads();
-#pragma unroll
-    for (int j = 0; j < J; ++j) {
-        const int64_t i = tid + int64_t(j) * nt;
-        if (i > E) continue;
-        const int64_t st = chunk_lo + i;
-        float qa = 0.f, eq = 0.f, rho = 0.f;
-        if (st >= s_lo && st < s_hi) {
-            float e = 0.f;
-            const DT* qr = sq + i * A;
-            const DT* pr = sp + i * A;
-            for (int64_t k = 0; k < A; ++k) {
-                const float qk = widen(qr[k]), pk = widen(pr[k]);
-                e = fmaf(pk, qk, e);
-                if (k == act[j]) { qa = qk; rho = pk; }
+        const int64_t blk_lo = el_lo / kPerBlock;
+        const int64_t nblk = el_hi > el_lo ? (el_hi + kPerBlock - 1) / kPerBlock - blk_lo : 0;
+        const int64_t nfull = min(nblk, max(total * A / kPerBlock - blk_lo, int64_t(0)));
+        e0 = blk_lo * kPerBlock;
+        el_copy = max(el_lo, (blk_lo + nfull) * kPerBlock);
+        const u32x4* gq = reinterpret_cast<const u32x4*>(a.in[1]) + blk_lo;
+        const u32x4* gp = reinterpret_cast<const u32x4*>(a.in[2]) + blk_lo;
+        u32x4* lq = reinterpret_cast<u32x4*>(dyn + Op::kStaged * kStride);
+        u32x4* lp = lq + cap(A) / kPerBlock;
+        const int lane = tid & (kWave - 1);
+        for (int64_t b0 = tid - lane; b0 < nfull; b0 += nt) {
+            if (b0 + lane < nfull) {
+                __builtin_amdgcn_global_load_lds(gq + b0 + lane, (__attribute__((address_space(3))) void*)(lq + b0), 16, 0, 0);
+                __builtin_amdgcn_global_load_lds(gp + b0 + lane, (__attribute__((address_space(3))) void*)(lp + b0), 16, 0, 0);
             }
-            eq = e;
-            rho = rho / mu[j];
         }
-        dyn[0 * kStride + i] = qa;
-        dyn[1 * kStride + i] = eq;
-        dyn[2 * kStride + i] = rho;
     }
-}
+
+    __device__ __forceinline__ void commit(const Args& a, int64_t chunk_lo, float* dyn) {
+        const int64_t A = a.A;
+        const int nt = blockDim.x, tid = threadIdx.x;
+        DT* sq = reinterpret_cast<DT*>(dyn + Op::kStaged * kStride);
+        DT* sp = sq + cap(A);
+        const DT* gq = reinterpret_cast<const DT*>(a.in[1]);
+        const DT* gp = reinterpret_cast<const DT*>(a.in[2]);
+        const int64_t n_el = el_hi - el_copy;
+        for (int64_t base = tid; base < n_el; base += 8 * int64_t(nt)) {
+            DT vq[8], vp[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const int64_t m = base + int64_t(u) * nt;
+                if (m < n_el) { vq[u] = gq[el_copy + m]; vp[u] = gp[el_copy + m]; }
+            }
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const int64_t m = base + int64_t(u) * nt;
+                if (m < n_el) { sq[el_copy - e0 + m] = vq[u]; sp[el_copy - e0 + m] = vp[u]; }
+            }
+        }
+        // the LDS copies of this wave have landed; then every wave's have
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+        // rows are 16-byte aligned whole blocks in LDS when A is a multiple of a block
+        const bool rows16 = a.stage_vec && A % kPerBlock == 0;
+#pragma unroll
+        for (int j = 0; j < J; ++j) {
+            const int64_t i = tid + int64_t(j) * nt;
+            if (i > E) continue;
+            const int64_t st = chunk_lo + i;
+            float v[Op::kStaged];
+#pragma unroll
+            for (int q = 0; q < Op::kStaged; ++q) v[q] = 0.f;
+            if (st >= s_lo && st < s_hi)
+                Op::template reduce_step<DT>(sq + (st * A - e0), sp + (st * A - e0), A, rows16, act[j], mu[j], v);
+#pragma unroll
+            for (int q = 0; q < Op::kStaged; ++q) dyn[q * kStride + i] = v[q];
+        }
+    }
+};
+
+// Policies without staging.
+template <class Op, typename DT, int E, int J>
+struct NoStager {
+    __device__ void issue(const Args&, int64_t, int64_t, float*) {}
+    __device__ void commit(const Args&, int64_t, float*) {}
+};
 
 // Rows kernel: workgroup g owns rows [g*R, g*R + R) and walks them in chunks of E steps
 // aligned to multiples of K, starting from the carry source (the end for backward scans).
@@ -423,6 +509,8 @@ template <class Op, typename DT, int K, int W, bool VEC, bool TR>
 __global__ void __launch_bounds__(W * kWave) rows_kernel(Args a, int64_t rows_per_wg, int wave_local) {
     using C = Chunk<Op, DT, K, W, VEC, TR>;
     constexpr int64_t E = int64_t(W) * kWave * K;
+    using S = std::conditional_t<(Op::kStaged > 0), Stager<Op, DT, int(E), K + 1>,
+                                 NoStager<Op, DT, int(E), K + 1>>;
     __shared__ float s_a[W], s_b[W];
     __shared__ float s_carry;
     const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
@@ -432,7 +520,7 @@ __global__ void __launch_bounds__(W * kWave) rows_kernel(Args a, int64_t rows_pe
     const bool can_full = VEC && a.T >= K;
     float carry = 0.f;
     auto carry_of = [&]() { return carry; };
-    extern __shared__ float s_dyn[];  // staged policies only (sized at launch)
+    extern __shared__ __align__(16) float s_dyn[];  // staged policies only (sized at launch)
     const float* stage = Op::kStaged > 0 ? s_dyn : nullptr;
     // the workgroup's first step is the start of row row_lo
     auto base_of = [&]() { return RowBase{lo, row_lo, 0}; };
@@ -440,14 +528,13 @@ __global__ void __launch_bounds__(W * kWave) rows_kernel(Args a, int64_t rows_pe
         int64_t chunk_hi = (hi + K - 1) / K * K;
         for (;;) {
             const int64_t chunk_lo = chunk_hi - E;
-            if constexpr (Op::kStaged > 0) {
-                stage_chunk<Op, DT, int(E), K + 1>(a, chunk_lo, lo, s_dyn);
-                __syncthreads();
-            }
+            S sg;
+            auto pre = [&]() { sg.issue(a, chunk_lo, lo, s_dyn); };
+            auto mid = [&]() { if constexpr (Op::kStaged > 0) { sg.commit(a, chunk_lo, s_dyn); __syncthreads(); } };
             C c;
             const float first = (can_full && chunk_lo >= lo && chunk_hi <= hi)
-                ? run_chunk<true>(c, a, chunk_lo, lo, hi, s_a, s_b, lane, wave, wave_local, base_of, carry_of, stage)
-                : run_chunk<false>(c, a, chunk_lo, lo, hi, s_a, s_b, lane, wave, wave_local, base_of, carry_of, stage);
+                ? run_chunk<true>(c, a, chunk_lo, lo, hi, s_a, s_b, lane, wave, wave_local, base_of, carry_of, stage, pre, mid)
+                : run_chunk<false>(c, a, chunk_lo, lo, hi, s_a, s_b, lane, wave, wave_local, base_of, carry_of, stage, pre, mid);
             if (chunk_lo <= lo) break;
             // the next chunk (earlier in time) continues from A at chunk_lo, held by lane 63 of
             // wave 0
@@ -459,14 +546,13 @@ __global__ void __launch_bounds__(W * kWave) rows_kernel(Args a, int64_t rows_pe
     } else {
         int64_t chunk_lo = lo / K * K;
         for (;;) {
-            if constexpr (Op::kStaged > 0) {
-                stage_chunk<Op, DT, int(E), K + 1>(a, chunk_lo, lo, s_dyn);
-                __syncthreads();
-            }
+            S sg;
+            auto pre = [&]() { sg.issue(a, chunk_lo, lo, s_dyn); };
+            auto mid = [&]() { if constexpr (Op::kStaged > 0) { sg.commit(a, chunk_lo, s_dyn); __syncthreads(); } };
             C c;
             const float last = (can_full && chunk_lo >= lo && chunk_lo + E <= hi)
-                ? run_chunk<true>(c, a, chunk_lo, lo, hi, s_a, s_b, lane, wave, wave_local, base_of, carry_of, stage)
-                : run_chunk<false>(c, a, chunk_lo, lo, hi, s_a, s_b, lane, wave, wave_local, base_of, carry_of, stage);
+                ? run_chunk<true>(c, a, chunk_lo, lo, hi, s_a, s_b, lane, wave, wave_local, base_of, carry_of, stage, pre, mid)
+                : run_chunk<false>(c, a, chunk_lo, lo, hi, s_a, s_b, lane, wave, wave_local, base_of, carry_of, stage, pre, mid);
             if (chunk_lo + E >= hi) break;
             if (threadIdx.x == W * kWave - 1) s_carry = last;
             __syncthreads();
@@ -576,8 +662,8 @@ __global__ void __launch_bounds__(W * kWave) tiles_kernel(Args a, int64_t num_ti
         return RowBase{lo, r, lo - r * a.T};
     };
     static_assert(Op::kStaged == 0, "staged policies run on the rows kernel only");
-    if (full) c.template local_scan<true>(a, lo, lo, hi, s_a, s_b, lane, wave, false, base_of, nullptr);
-    else c.template local_scan<false>(a, lo, lo, hi, s_a, s_b, lane, wave, false, base_of, nullptr);
+    if (full) c.template local_scan<true>(a, lo, lo, hi, s_a, s_b, lane, wave, false, base_of, nullptr, Nop{}, Nop{});
+    else c.template local_scan<false>(a, lo, lo, hi, s_a, s_b, lane, wave, false, base_of, nullptr, Nop{}, Nop{});
     __syncthreads();
     c.wave_prefix(s_a, s_b, wave);
 
