@@ -272,7 +272,7 @@ def test_retrace_full_shapes(A, T):
     assert_parity(out, ref, 1e-5, label=f"retrace_full A={A} T={T}")
 
 
-@pytest.mark.parametrize("A", [4, 18])
+@pytest.mark.parametrize("A", [4, 8, 18, 24])
 def test_retrace_full_bf16_and_plain(A):
     ro = workloads.make_retrace_full(300, 129, A, seed=A, dtype="bf16", p_term=0.05, p_trunc=0.05)
     out, ref = _retrace_full_run(ro)
@@ -280,6 +280,31 @@ def test_retrace_full_bf16_and_plain(A):
     ro = workloads.make_retrace_full(300, 256, A, seed=A + 1, p_term=0.05, p_trunc=0.0)
     out, ref = _retrace_full_run(ro, trunc=False, boot=False)
     assert_parity(out, ref, 1e-5, label=f"retrace_full plain A={A}")
+
+
+def _misaligned(t):
+    """A copy of `t` whose storage starts one element past a 16-byte boundary."""
+    buf = torch.empty(t.numel() + 1, dtype=t.dtype, device=t.device)
+    buf[1:].copy_(t.reshape(-1))
+    return buf[1:].view(t.shape)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("A", [3, 4, 18])
+def test_retrace_full_unaligned_slices(A, dtype):
+    """Q and pi not 16-byte aligned: the slices are staged element-wise."""
+    ro = workloads.make_retrace_full(37, 301, A, seed=5 + A, dtype=dtype, p_term=0.05, p_trunc=0.05)
+    d = device_inputs(ro, DEV)
+    q, pi = _misaligned(d["q3"]), _misaligned(d["pi3"])
+    assert q.data_ptr() % 16 != 0 and pi.data_ptr() % 16 != 0
+    dl, qr = rl.rlcs_retrace_full(d["r"], q, pi, d["actions"], d["mu"], d["term"], d["trunc"],
+                                  d["bv"], d["boot"], gamma=0.97, lam=0.9, c_bar=1.0)
+    torch.cuda.synchronize()
+    import oracle
+    rd, rq = oracle.retrace_full(ro["r"], ro["q3"], ro["pi3"], ro["actions"], ro["mu"], ro["term"],
+                                 ro["trunc"], ro["bv"], ro["boot"], gamma=0.97, lam=0.9, c_bar=1.0)
+    assert_parity({"delta": dl, "q_ret": qr}, {"delta": rd, "q_ret": rq}, TOL[dtype],
+                  label=f"retrace_full unaligned A={A} {dtype}")
 
 
 def test_retrace_full_out_of_range_actions():
