@@ -26,7 +26,7 @@ _LIB = os.path.join(_HERE, "liboracle.so")
 
 __all__ = [
     "build", "gae", "td_lambda", "discounted", "vtrace", "retrace", "retrace_full", "elig_trace",
-    "episodic_prefix", "affine_scan", "widen", "param",
+    "elig_trace_vec", "episodic_prefix", "affine_scan", "time_major", "widen", "param",
 ]
 
 
@@ -60,6 +60,7 @@ def _load():
             "oracle_retrace_full": [D, D, D, ctypes.POINTER(ctypes.c_int32), D, U8, U8, D, D, D,
                                     D, I64, I64, I64, F64, F64, F64],
             "oracle_elig_trace": [D, U8, U8, D, I64, I64, F64, F64],
+            "oracle_elig_trace_vec": [D, U8, U8, D, I64, I64, I64, F64, F64],
             "oracle_episodic_prefix": [D, U8, U8, D, I64, I64, INT],
             "oracle_affine_scan": [D, D, D, D, I64, I64, INT],
         }
@@ -232,6 +233,37 @@ def elig_trace(x, term=None, trunc=None, *, gamma, lam):
     _load().oracle_elig_trace(_ptr(x, D), _ptr(term, U), _ptr(trunc, U), _ptr(out, D), N, T,
                               param(gamma), param(lam))
     return out
+
+
+def elig_trace_vec(x, term=None, trunc=None, *, gamma, lam):
+    """Eligibility traces of F-vectors: x is [N, T, F], the flags [N, T]. Returns fp64 z
+    [N, T, F]."""
+    x3 = np.asarray(x)
+    if x3.ndim != 3:
+        raise ValueError(f"expected a 3-D [N, T, F] array, got shape {x3.shape}")
+    N, T, F = x3.shape
+    x3 = widen(x3)
+    term, trunc = _flags(term), _flags(trunc)
+    _check(N, T, term, trunc)
+    out = np.empty((N, T, F))
+    D, U = ctypes.c_double, ctypes.c_uint8
+    _load().oracle_elig_trace_vec(_ptr(x3, D), _ptr(term, U), _ptr(trunc, U), _ptr(out, D), N, T,
+                                  F, param(gamma), param(lam))
+    return out
+
+
+def time_major(fn, *args, **kw):
+    """Estimator `fn` (one of the functions above) on time-major inputs: every 2-D argument is
+    [T, N] (step t of environment n at [t, n]); 1-D arguments (bootstraps) are [N]. The oracle
+    is the row-major one applied to the transposed arrays; the outputs come back as [T, N]."""
+    def tr(a):
+        if isinstance(a, np.ndarray) and a.ndim == 2:
+            return np.ascontiguousarray(a.T)
+        return a
+    out = fn(*(tr(a) for a in args), **{k: tr(v) for k, v in kw.items()})
+    if isinstance(out, tuple):
+        return tuple(np.ascontiguousarray(o.T) for o in out)
+    return np.ascontiguousarray(out.T)
 
 
 def episodic_prefix(x, term=None, trunc=None, *, boundary="ends_at"):

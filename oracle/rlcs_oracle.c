@@ -261,6 +261,29 @@ void oracle_elig_trace(const double* x, const uint8_t* term, const uint8_t* trun
     }
 }
 
+/* Vector eligibility traces (forward), Section 3.3.5 with a feature vector per step:
+ *   z_t = gamma * lambda * (1 - d_{t-1}) * z_{t-1} + x_t,  z_{-1} = 0,  d_{-1} = 0,
+ * where x_t and z_t are F-vectors ([N, T, F], features innermost) and the scalar coefficient
+ * of a step (flags [N, T]) multiplies every feature alike. Features are walked one at a time. */
+void oracle_elig_trace_vec(const double* x, const uint8_t* term, const uint8_t* trunc, double* z,
+                           int64_t N, int64_t T, int64_t F, double gamma, double lambda) {
+    for (int64_t n = 0; n < N; ++n) {
+        const uint8_t* te = row_of_flags(term, n, T);
+        const uint8_t* tr = row_of_flags(trunc, n, T);
+        for (int64_t f = 0; f < F; ++f) {
+            double z_prev = 0.0;
+            double d_prev = 0.0;
+            for (int64_t t = 0; t < T; ++t) {
+                const int64_t i = (n * T + t) * F + f;
+                const double zt = gamma * lambda * (1.0 - d_prev) * z_prev + x[i];
+                z[i] = zt;
+                z_prev = zt;
+                d_prev = (flag_at(te, t) || flag_at(tr, t)) ? 1.0 : 0.0;
+            }
+        }
+    }
+}
+
 /* Episodic prefix sum (forward), Table 1 and Section 3.3.6:
  *   ends_at:   C_t = x_t + (1 - d_{t-1}) C_{t-1},  d_{-1} = 0,
  *   starts_at: C_t = x_t + (1 - d_t) C_{t-1},

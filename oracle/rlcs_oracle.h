@@ -61,6 +61,12 @@ void oracle_retrace_full(const double* r, const double* q, const double* pi,
 void oracle_elig_trace(const double* x, const uint8_t* term, const uint8_t* trunc, double* z,
                        int64_t N, int64_t T, double gamma, double lambda);
 
+/* Eligibility traces of F-vectors: x and z are double [N, T, F] (features innermost), the
+ * flags [N, T]; the scalar coefficient gamma * lambda * (1 - d_{t-1}) of a step applies to
+ * every feature. */
+void oracle_elig_trace_vec(const double* x, const uint8_t* term, const uint8_t* trunc, double* z,
+                           int64_t N, int64_t T, int64_t F, double gamma, double lambda);
+
 /* starts_at = 0: a set flag at t-1 ends the running sum before t ("ends_at");
  * starts_at = 1: a set flag at t starts a new running sum at t. */
 void oracle_episodic_prefix(const double* x, const uint8_t* term, const uint8_t* trunc,

@@ -546,3 +546,111 @@ def test_retrace_full_single_action_is_gae():
                                 term, trunc, x["bv"], x["boot"], gamma=G, lam=L)
     adv, _ = oracle.gae(x["r"], x["q"], term, trunc, x["bv"], x["boot"], gamma=G, lam=L)
     rtol_close(dl, adv)
+
+
+# ---------------------------------------------------------------- vector eligibility traces (Section 3.3.5)
+
+@pytest.mark.parametrize("F", [1, 3, 8])
+def test_elig_trace_vec_brute_force(F):
+    """Every feature of z_t against the past-weighted sum over the episode segment, with the
+    step's flags shared by all features."""
+    N, T = 60, 13
+    rng = np.random.default_rng(90 + F)
+    term = (rng.random((N, T)) < 0.15).astype(np.uint8)
+    trunc = (rng.random((N, T)) < 0.15).astype(np.uint8)
+    x = rng.standard_normal((N, T, F))
+    z = oracle.elig_trace_vec(x, term, trunc, gamma=G, lam=L)
+    ref = np.array([[brute.elig_sum(x[n, :, f], term[n], trunc[n], g32, l32) for f in range(F)]
+                    for n in range(N)])  # [N, F, T]
+    rtol_close(z, ref.transpose(0, 2, 1))
+
+
+def test_elig_trace_vec_exhaustive_flags():
+    """All 4**5 flag patterns of a 5-step row, two features."""
+    T = 5
+    term, trunc = all_flag_patterns(T)
+    N = term.shape[0]
+    rng = np.random.default_rng(3)
+    x = rng.standard_normal((N, T, 2))
+    z = oracle.elig_trace_vec(x, term, trunc, gamma=G, lam=L)
+    for f in range(2):
+        rtol_close(z[:, :, f], [brute.elig_sum(x[n, :, f], term[n], trunc[n], g32, l32)
+                                for n in range(N)])
+
+
+def test_elig_trace_vec_one_feature_is_scalar_trace():
+    """F = 1 is the scalar eligibility trace, bit for bit (same fp64 steps)."""
+    N, T = 30, 40
+    term, trunc = _flags(N, T, 11)
+    x = np.random.default_rng(12).standard_normal((N, T))
+    zv = oracle.elig_trace_vec(x[:, :, None], term, trunc, gamma=G, lam=L)[:, :, 0]
+    assert np.array_equal(zv, oracle.elig_trace(x, term, trunc, gamma=G, lam=L))
+
+
+def test_elig_trace_vec_feature_permutation_and_linearity():
+    """Features are independent scans with a shared coefficient: permuting features permutes
+    the traces bit for bit, and the map x -> z is linear."""
+    N, T, F = 20, 50, 6
+    term, trunc = _flags(N, T, 13)
+    rng = np.random.default_rng(14)
+    x1, x2 = rng.standard_normal((N, T, F)), rng.standard_normal((N, T, F))
+    perm = rng.permutation(F)
+    z1 = oracle.elig_trace_vec(x1, term, trunc, gamma=G, lam=L)
+    assert np.array_equal(oracle.elig_trace_vec(x1[:, :, perm], term, trunc, gamma=G, lam=L),
+                          z1[:, :, perm])
+    z2 = oracle.elig_trace_vec(x2, term, trunc, gamma=G, lam=L)
+    z12 = oracle.elig_trace_vec(2.0 * x1 - x2, term, trunc, gamma=G, lam=L)
+    rtol_close(z12, 2.0 * z1 - z2)
+
+
+def test_elig_trace_vec_closed_form():
+    """x = 1 in every feature, no flags: (1 - (gamma lambda)^(t+1)) / (1 - gamma lambda)."""
+    T, F = 200, 4
+    z = oracle.elig_trace_vec(np.ones((1, T, F)), gamma=G, lam=L)
+    gl = g32 * l32
+    ref = (1 - gl ** (np.arange(T) + 1)) / (1 - gl)
+    for f in range(F):
+        rtol_close(z[0, :, f], ref)
+
+
+# ---------------------------------------------------------------- time-major [T, N] layout
+
+def test_time_major_oracle_brute_force():
+    """Each environment's column of the time-major arrays against the sum forms."""
+    T, N = 14, 40
+    rng = np.random.default_rng(21)
+    term = (rng.random((T, N)) < 0.15).astype(np.uint8)
+    trunc = (rng.random((T, N)) < 0.15).astype(np.uint8)
+    r, v, bv, lr = (rng.standard_normal((T, N)) for _ in range(4))
+    q, eq = rng.standard_normal((T, N)), rng.standard_normal((T, N))
+    boot = rng.standard_normal(N)
+    col = lambda a, n: a[:, n]
+    adv, ret = oracle.time_major(oracle.gae, r, v, term, trunc, bv, boot, gamma=G, lam=L)
+    assert adv.shape == (T, N)
+    rtol_close(adv, np.array([brute.gae_sum(col(r, n), col(v, n), col(term, n), col(trunc, n),
+                                            col(bv, n), boot[n], g32, l32) for n in range(N)]).T)
+    rtol_close(ret, adv + v)
+    vs, pg = oracle.time_major(oracle.vtrace, r, v, lr, term, trunc, bv, boot, gamma=G)
+    res = [brute.vtrace_sum(col(r, n), col(v, n), col(lr, n), col(term, n), col(trunc, n),
+                            col(bv, n), boot[n], g32, 1.0, 1.0) for n in range(N)]
+    rtol_close(vs, np.array([a for a, _ in res]).T)
+    rtol_close(pg, np.array([b for _, b in res]).T)
+    dl, _ = oracle.time_major(oracle.retrace, r, q, eq, lr, term, trunc, bv, boot, gamma=G, lam=L)
+    rtol_close(dl, np.array([brute.retrace_sum(col(r, n), col(q, n), col(eq, n), col(lr, n),
+                                               col(term, n), col(trunc, n), col(bv, n), boot[n],
+                                               g32, l32, 1.0)[0] for n in range(N)]).T)
+    td = oracle.time_major(oracle.td_lambda, r, v, term, trunc, bv, boot, gamma=G, lam=L)
+    rtol_close(td, np.array([brute.lambda_return(col(r, n), col(v, n), col(term, n),
+                                                 col(trunc, n), col(bv, n), boot[n], g32, l32)
+                             for n in range(N)]).T)
+    dr = oracle.time_major(oracle.discounted, r, term, trunc, bv, boot, gamma=G)
+    rtol_close(dr, np.array([brute.discounted_sum(col(r, n), col(term, n), col(trunc, n),
+                                                  col(bv, n), boot[n], g32) for n in range(N)]).T)
+    z = oracle.time_major(oracle.elig_trace, r, term, trunc, gamma=G, lam=L)
+    rtol_close(z, np.array([brute.elig_sum(col(r, n), col(term, n), col(trunc, n), g32, l32)
+                            for n in range(N)]).T)
+    for starts in (False, True):
+        c = oracle.time_major(oracle.episodic_prefix, r, term, trunc,
+                              boundary="starts_at" if starts else "ends_at")
+        rtol_close(c, np.array([brute.prefix_sum(col(r, n), col(term, n), col(trunc, n), starts)
+                                for n in range(N)]).T)
