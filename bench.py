@@ -333,6 +333,14 @@ def run_extra(dev, only=""):
                               ("rf_4096x256x18", 4096, 256, 18)):
         if label.startswith(only):
             run_retrace_full(label, n_, t_, a_, dev)
+    for label, t_, n_ in (("tm_256x4096", 256, 4096), ("tm_4096x64", 4096, 64),
+                          ("tm_64x65536", 64, 65536)):
+        if label.startswith(only):
+            run_time_major(label, t_, n_, dev)
+    for label, n_, t_, f_ in (("vec_4096x256x16", 4096, 256, 16), ("vec_64x1024x256", 64, 1024, 256),
+                              ("vec_1x128x1M", 1, 128, 1 << 20)):
+        if label.startswith(only):
+            run_vector_trace(label, n_, t_, f_, dev)
 
 
 def run_retrace_full(label, n_, t_, a_, dev):
@@ -387,6 +395,113 @@ def run_retrace_full(label, n_, t_, a_, dev):
     gbs = nbytes / (us * 1e-6) / 1e9
     print(f"{label:<18} {'retrace_full':<16} {us:>9.3f} {gbs:>8.1f} {100 * gbs / PEAK_HBM_GBS:>5.1f}% "
           f"{n_ * t_ / (us * 1e-6) / 1e9:>9.1f} {S:>5} {rel:>11.2e}", file=sys.stderr, flush=True)
+
+
+def _rotated_sets(base, S, outs):
+    """S input/output sets: set 0 is `base`, the others copies; fresh float32 outputs."""
+    import torch
+    sets = []
+    for i in range(S):
+        d = dict(base if i == 0 else {k: v.clone() for k, v in base.items()})
+        for name, like in outs.items():
+            d[name] = torch.empty_like(like, dtype=torch.float32)
+        sets.append(d)
+    return sets
+
+
+def _graph_time(call, sets, nbytes):
+    """Mean microseconds per call over K graph-replayed calls cycling through `sets`."""
+    import torch
+    S = len(sets)
+    K = int(max(20, min(2000, 20000 / max(2.0, nbytes / 5e3))))
+    for i in range(3):
+        call(sets[i % S])
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for i in range(K):
+            call(sets[i % S])
+    graph.replay()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(); graph.replay(); b.record()
+    torch.cuda.synchronize()
+    del graph
+    return a.elapsed_time(b) * 1e3 / K
+
+
+def _report(label, name, us, nbytes, steps, S, rel):
+    gbs = nbytes / (us * 1e-6) / 1e9
+    print(f"{label:<18} {name:<16} {us:>9.3f} {gbs:>8.1f} {100 * gbs / PEAK_HBM_GBS:>5.1f}% "
+          f"{steps / (us * 1e-6) / 1e9:>9.1f} {S:>5} {rel:>11.2e}", file=sys.stderr, flush=True)
+
+
+def run_time_major(label, t_, n_, dev):
+    """GAE and V-Trace on a time-major [T, N] fp32 buffer with truncation: parity on sampled
+    environments, then graph-timed. Same dense byte count as the row-major form."""
+    import torch
+    import oracle
+    import workloads
+    import paper_2608_17641_amd as rl
+    ro = workloads.make_rollout_time_major(t_, n_, 0, p_term=0.02, p_trunc=0.01)
+    base = {k: torch.from_numpy(np.ascontiguousarray(v)).to(dev) for k, v in ro.items()}
+    set_bytes = sum(v.numel() * v.element_size() for v in base.values()) + 8 * n_ * t_
+    S = max(1, min(32, -(-600_000_000 // set_bytes)))
+    sets = _rotated_sets(base, S, {"o0": base["r"], "o1": base["r"]})
+    ws = rl.make_workspace_columns(n_, t_, dev)
+    cols = np.unique(np.concatenate([[0, n_ - 1], np.random.default_rng(1).integers(0, n_, 32)]))
+    g = lambda k: np.ascontiguousarray(ro[k][:, cols]) if ro[k].ndim == 2 else ro[k][cols]
+    for name in ("gae", "vtrace"):
+        if name == "gae":
+            call = lambda d: rl.rlcs_gae_tm(d["r"], d["v"], d["term"], d["trunc"], d["bv"], d["boot"],
+                                            d["o0"], d["o1"], gamma=0.99, lam=0.95, ws=ws)
+            refs = oracle.time_major(oracle.gae, g("r"), g("v"), g("term"), g("trunc"), g("bv"),
+                                     g("boot"), gamma=0.99, lam=0.95)
+        else:
+            call = lambda d: rl.rlcs_vtrace_tm(d["r"], d["v"], d["log_rho"], d["term"], d["trunc"],
+                                               d["bv"], d["boot"], d["o0"], d["o1"], gamma=0.99, ws=ws)
+            refs = oracle.time_major(oracle.vtrace, g("r"), g("v"), g("log_rho"), g("term"),
+                                     g("trunc"), g("bv"), g("boot"), gamma=0.99)
+        call(sets[0])
+        torch.cuda.synchronize()
+        rel = 0.0
+        for o, r_ in zip((sets[0]["o0"], sets[0]["o1"]), refs):
+            got = o.index_select(1, torch.from_numpy(cols).to(dev)).double().cpu().numpy()
+            rel = max(rel, float(np.max(np.abs(got - r_))) / (1 + float(np.max(np.abs(r_)))))
+        if rel > 1e-5:
+            raise SystemExit(f"parity failure in {label} {name}: {rel}")
+        nbytes = extra_bytes(name, n_, t_, 4, True, True)
+        _report(label, name + "_tm", _graph_time(call, sets, nbytes), nbytes, n_ * t_, S, rel)
+
+
+def run_vector_trace(label, n_, t_, f_, dev):
+    """Eligibility traces of F-vectors (fp32, both flags): parity on sampled rows, then
+    graph-timed. Dense bytes: x and z (4 B each per feature) and two flag bytes per step."""
+    import torch
+    import oracle
+    import workloads
+    import paper_2608_17641_amd as rl
+    ro = workloads.make_vector_trace(n_, t_, f_, 0)
+    base = {k: torch.from_numpy(np.ascontiguousarray(v)).to(dev) for k, v in ro.items()}
+    set_bytes = sum(v.numel() * v.element_size() for v in base.values()) + 4 * n_ * t_ * f_
+    S = max(1, min(32, -(-600_000_000 // set_bytes)))
+    sets = _rotated_sets(base, S, {"z": base["x"]})
+    ws = rl.make_workspace_columns(n_ * f_, t_, dev)
+    call = lambda d: rl.rlcs_elig_trace_vec(d["x"], d["term"], d["trunc"], d["z"], gamma=0.99,
+                                            lam=0.95, ws=ws)
+    call(sets[0])
+    torch.cuda.synchronize()
+    rows = np.unique(np.concatenate([[0, n_ - 1], np.random.default_rng(1).integers(0, n_, 8)]))
+    feats = np.unique(np.concatenate([[0, f_ - 1], np.random.default_rng(2).integers(0, f_, 64)]))
+    xs = np.ascontiguousarray(ro["x"][rows][:, :, feats])
+    ref = oracle.elig_trace_vec(xs, ro["term"][rows], ro["trunc"][rows], gamma=0.99, lam=0.95)
+    got = sets[0]["z"][torch.from_numpy(rows).to(dev)][:, :, torch.from_numpy(feats).to(dev)]
+    got = got.double().cpu().numpy()
+    rel = float(np.max(np.abs(got - ref))) / (1 + float(np.max(np.abs(ref))))
+    if rel > 1e-5:
+        raise SystemExit(f"parity failure in {label}: {rel}")
+    nbytes = n_ * t_ * (8 * f_ + 2)
+    _report(label, "elig_trace_vec", _graph_time(call, sets, nbytes), nbytes, n_ * t_ * f_, S, rel)
 
 
 def main():

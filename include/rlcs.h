@@ -184,8 +184,73 @@ rlcs_status rlcs_affine_scan(const void* alpha, const void* beta, const void* ca
                              void* ws, size_t ws_bytes, rlcs_stream_t stream);
 
 /* Bytes of workspace that let any entry point above split rows of an [N, T] call over
- * several workgroups (0 if no split can be needed). */
+ * several workgroups: a fixed 65600-byte part plus 16 bytes per 4096-step tile (0 if the size
+ * overflows). Every entry point of this header lays the workspace out the same way, so one
+ * workspace at least as large as each call needs serves calls of every kind and shape,
+ * row-major and time-major alike, as long as they are ordered on one stream. */
 size_t rlcs_workspace_size(int64_t N, int64_t T);
+
+/* ---------------------------------------------------------------------------------------
+ * Time-major layouts. The entry points below compute exactly what their row-major namesakes
+ * compute, for buffers stored time-major: every [N, T] array of the row-major form becomes a
+ * [T, ld] array with step t of environment n at element t*ld + n (ld >= N; ld == 0 means
+ * N), e.g. a [T, B] rollout buffer or a strided view of a wider one. All [T, ld] arrays of a
+ * call (data, flags, bv and outputs) share ld; boot stays [N], contiguous. Elements n >= N
+ * of a step are neither read nor written. Sizes: N >= 0, 0 <= T <= 2^30, T*ld representable.
+ * Workspace: at least rlcs_workspace_size_columns(N, T) bytes, zero-filled once, lets few
+ * environments (N below about 64K) be split along T over several workgroups; without it
+ * each group of 64 environments is scanned by one workgroup. Every other convention is the
+ * row-major one.                                                                          */
+rlcs_status rlcs_gae_tm(const void* r, const void* v, const uint8_t* term, const uint8_t* trunc,
+                        const void* bv, const void* boot, float* adv, float* ret, int64_t N,
+                        int64_t T, int64_t ld, float gamma, float lambda, rlcs_dtype dtype,
+                        void* ws, size_t ws_bytes, rlcs_stream_t stream);
+rlcs_status rlcs_vtrace_tm(const void* r, const void* v, const void* log_rho, const uint8_t* term,
+                           const uint8_t* trunc, const void* bv, const void* boot, float* vs,
+                           float* pg, int64_t N, int64_t T, int64_t ld, float gamma,
+                           float rho_bar, float c_bar, rlcs_dtype dtype, void* ws,
+                           size_t ws_bytes, rlcs_stream_t stream);
+rlcs_status rlcs_retrace_tm(const void* r, const void* q, const void* eq, const void* log_rho,
+                            const uint8_t* term, const uint8_t* trunc, const void* bv,
+                            const void* boot, float* delta, float* q_ret, int64_t N, int64_t T,
+                            int64_t ld, float gamma, float lambda, float c_bar, rlcs_dtype dtype,
+                            void* ws, size_t ws_bytes, rlcs_stream_t stream);
+rlcs_status rlcs_td_lambda_tm(const void* r, const void* v, const uint8_t* term,
+                              const uint8_t* trunc, const void* bv, const void* boot, float* ret,
+                              int64_t N, int64_t T, int64_t ld, float gamma, float lambda,
+                              rlcs_dtype dtype, void* ws, size_t ws_bytes, rlcs_stream_t stream);
+rlcs_status rlcs_discounted_tm(const void* r, const uint8_t* term, const uint8_t* trunc,
+                               const void* bv, const void* boot, float* ret, int64_t N, int64_t T,
+                               int64_t ld, float gamma, rlcs_dtype dtype, void* ws,
+                               size_t ws_bytes, rlcs_stream_t stream);
+rlcs_status rlcs_elig_trace_tm(const void* x, const uint8_t* term, const uint8_t* trunc, float* z,
+                               int64_t N, int64_t T, int64_t ld, float gamma, float lambda,
+                               rlcs_dtype dtype, void* ws, size_t ws_bytes, rlcs_stream_t stream);
+rlcs_status rlcs_episodic_prefix_tm(const void* x, const uint8_t* term, const uint8_t* trunc,
+                                    float* c, int64_t N, int64_t T, int64_t ld,
+                                    rlcs_boundary boundary, rlcs_dtype dtype, void* ws,
+                                    size_t ws_bytes, rlcs_stream_t stream);
+
+/* Eligibility traces of feature vectors (Section 3.3.5: the trace of the gradient, or of the
+ * feature vector under linear function approximation), forward:
+ *   z_t = gamma lambda (1 - d_{t-1}) z_{t-1} + x_t,  d_{-1} = 0,  z_{-1} = 0,
+ * with x_t, z_t in R^F and one scalar coefficient per step shared by all F features (the
+ * paper's scalar-beta restriction; per-feature beta is not supported).
+ *   x        [N, T, F] feature values, dtype, row-major (features innermost)
+ *   term, trunc  [N, T] as above (one flag per step, for every feature)
+ *   z        [N, T, F] float32 out: traces
+ * Sizes: N, F >= 0, 0 <= T <= 2^30, N*T*F representable; any of them 0 is a no-op.
+ * Workspace: rlcs_workspace_size_columns(N * F, T) bytes, as for the time-major calls (used
+ * when N*F is below about 64K).                                                           */
+rlcs_status rlcs_elig_trace_vec(const void* x, const uint8_t* term, const uint8_t* trunc,
+                                float* z, int64_t N, int64_t T, int64_t F, float gamma,
+                                float lambda, rlcs_dtype dtype, void* ws, size_t ws_bytes,
+                                rlcs_stream_t stream);
+
+/* Workspace bytes for the time-major calls (columns = N) and rlcs_elig_trace_vec
+ * (columns = N * F) over T steps: the fixed 65600-byte part plus 16 bytes per column per
+ * 32-step tile; 0 for negative sizes or a size that overflows. */
+size_t rlcs_workspace_size_columns(int64_t columns, int64_t T);
 
 /* Static description of a status code. Never NULL. */
 const char* rlcs_status_string(rlcs_status status);

@@ -23,6 +23,9 @@ __all__ = [
     "rlcs_gae", "rlcs_vtrace", "rlcs_retrace", "rlcs_retrace_full", "rlcs_td_lambda", "rlcs_discounted",
     "rlcs_elig_trace", "rlcs_episodic_prefix", "rlcs_affine_scan", "rlcs_workspace_size",
     "rlcs_version", "rlcs_set_variant_override", "make_workspace", "RlcsError",
+    "rlcs_gae_tm", "rlcs_vtrace_tm", "rlcs_retrace_tm", "rlcs_td_lambda_tm", "rlcs_discounted_tm",
+    "rlcs_elig_trace_tm", "rlcs_episodic_prefix_tm", "rlcs_elig_trace_vec",
+    "rlcs_workspace_size_columns", "make_workspace_columns",
 ]
 
 _DTYPES = {torch.float32: _native.RLCS_F32, torch.bfloat16: _native.RLCS_BF16}
@@ -261,3 +264,196 @@ def rlcs_affine_scan(alpha, beta, carry=None, out=None, *, reverse: bool = True,
         _call("rlcs_affine_scan", _ptr(alpha), _ptr(beta), _ptr(carry), _ptr(out), N, T, d,
               _DTYPES[dt], wp, wb, _stream(dev))
     return out
+
+
+# ---------------------------------------------------------------- time-major layouts
+# Every [N, T] tensor of the row-major functions becomes a [T, N] tensor (step t of
+# environment n at [t, n]) whose rows may be strided: stride (ld, 1) with ld >= N, the same
+# for every [T, N] tensor of the call. Outputs not given are allocated with that stride.
+
+def _prep_tm(x: torch.Tensor):
+    if not isinstance(x, torch.Tensor) or x.dim() != 2:
+        raise ValueError("data inputs must be 2-D [T, N] tensors")
+    if x.dtype not in _DTYPES:
+        raise TypeError(f"data inputs must be float32 or bfloat16, got {x.dtype}")
+    if x.device.type != "cuda":
+        raise ValueError("tensors must be on a GPU")
+    T, N = int(x.shape[0]), int(x.shape[1])
+    ld = int(x.stride(0)) if T > 1 else N
+    if (N > 1 and x.stride(1) != 1) or ld < N:
+        raise ValueError("time-major tensors must have stride (ld, 1) with ld >= N")
+    return T, N, ld, x.dtype, x.device
+
+
+def _check_tm(name, t, T, N, ld, device, dtype=None, flags=False):
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if tuple(t.shape) != (T, N):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {(T, N)}")
+    if flags:
+        if t.dtype not in (torch.uint8, torch.bool):
+            raise TypeError(f"{name} must be uint8 or bool, got {t.dtype}")
+    elif dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} has dtype {t.dtype}, expected {dtype}")
+    if t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
+    if (N > 1 and t.stride(1) != 1) or (T > 1 and t.stride(0) != ld):
+        raise ValueError(f"{name} has strides {t.stride()}, expected ({ld}, 1) like the first input")
+    return t
+
+
+def _out_tm(name, t, T, N, ld, device):
+    if t is None:
+        return torch.empty((T, ld), dtype=torch.float32, device=device)[:, :N]
+    if t.dtype != torch.float32:
+        raise ValueError(f"{name} must be float32")
+    return _check_tm(name, t, T, N, ld, device)
+
+
+def _boot_tm(boot, N, dtype, device):
+    return _check_data("boot", boot, 1, N, dtype, device, shape=(N,))
+
+
+def make_workspace_columns(columns: int, T: int, device) -> torch.Tensor:
+    """Zero-filled workspace for time-major calls (columns = N) and rlcs_elig_trace_vec
+    (columns = N * F) over T steps."""
+    n = int(_native.load().rlcs_workspace_size_columns(int(columns), int(T)))
+    return torch.zeros(max(n, 64), dtype=torch.uint8, device=device)
+
+
+def rlcs_workspace_size_columns(columns: int, T: int) -> int:
+    return int(_native.load().rlcs_workspace_size_columns(int(columns), int(T)))
+
+
+def rlcs_gae_tm(r, v, term=None, trunc=None, bv=None, boot=None, adv=None, ret=None, *,
+                gamma: float, lam: float, ws=None, want_ret: bool = True):
+    T, N, ld, dt, dev = _prep_tm(r)
+    _check_tm("v", v, T, N, ld, dev, dt); _check_tm("bv", bv, T, N, ld, dev, dt)
+    _check_tm("term", term, T, N, ld, dev, flags=True); _check_tm("trunc", trunc, T, N, ld, dev, flags=True)
+    _boot_tm(boot, N, dt, dev)
+    adv = _out_tm("adv", adv, T, N, ld, dev)
+    ret = _out_tm("ret", ret, T, N, ld, dev) if (want_ret or ret is not None) else None
+    wp, wb = _ws(ws, dev)
+    with torch.cuda.device(dev):
+        _call("rlcs_gae_tm", _ptr(r), _ptr(v), _ptr(term), _ptr(trunc), _ptr(bv), _ptr(boot),
+              _ptr(adv), _ptr(ret), N, T, ld, gamma, lam, _DTYPES[dt], wp, wb, _stream(dev))
+    return adv, ret
+
+
+def rlcs_vtrace_tm(r, v, log_rho, term=None, trunc=None, bv=None, boot=None, vs=None, pg=None, *,
+                   gamma: float, rho_bar: float = 1.0, c_bar: float = 1.0, ws=None,
+                   want_pg: bool = True):
+    T, N, ld, dt, dev = _prep_tm(r)
+    for name, t in (("v", v), ("log_rho", log_rho), ("bv", bv)):
+        _check_tm(name, t, T, N, ld, dev, dt)
+    _check_tm("term", term, T, N, ld, dev, flags=True); _check_tm("trunc", trunc, T, N, ld, dev, flags=True)
+    _boot_tm(boot, N, dt, dev)
+    vs = _out_tm("vs", vs, T, N, ld, dev)
+    pg = _out_tm("pg", pg, T, N, ld, dev) if (want_pg or pg is not None) else None
+    wp, wb = _ws(ws, dev)
+    with torch.cuda.device(dev):
+        _call("rlcs_vtrace_tm", _ptr(r), _ptr(v), _ptr(log_rho), _ptr(term), _ptr(trunc),
+              _ptr(bv), _ptr(boot), _ptr(vs), _ptr(pg), N, T, ld, gamma, rho_bar, c_bar,
+              _DTYPES[dt], wp, wb, _stream(dev))
+    return vs, pg
+
+
+def rlcs_retrace_tm(r, q, eq, log_rho, term=None, trunc=None, bv=None, boot=None, delta=None,
+                    q_ret=None, *, gamma: float, lam: float, c_bar: float = 1.0, ws=None,
+                    want_q_ret: bool = True):
+    T, N, ld, dt, dev = _prep_tm(r)
+    for name, t in (("q", q), ("eq", eq), ("log_rho", log_rho), ("bv", bv)):
+        _check_tm(name, t, T, N, ld, dev, dt)
+    _check_tm("term", term, T, N, ld, dev, flags=True); _check_tm("trunc", trunc, T, N, ld, dev, flags=True)
+    _boot_tm(boot, N, dt, dev)
+    delta = _out_tm("delta", delta, T, N, ld, dev)
+    q_ret = _out_tm("q_ret", q_ret, T, N, ld, dev) if (want_q_ret or q_ret is not None) else None
+    wp, wb = _ws(ws, dev)
+    with torch.cuda.device(dev):
+        _call("rlcs_retrace_tm", _ptr(r), _ptr(q), _ptr(eq), _ptr(log_rho), _ptr(term),
+              _ptr(trunc), _ptr(bv), _ptr(boot), _ptr(delta), _ptr(q_ret), N, T, ld, gamma, lam,
+              c_bar, _DTYPES[dt], wp, wb, _stream(dev))
+    return delta, q_ret
+
+
+def rlcs_td_lambda_tm(r, v, term=None, trunc=None, bv=None, boot=None, ret=None, *, gamma: float,
+                      lam: float, ws=None) -> torch.Tensor:
+    T, N, ld, dt, dev = _prep_tm(r)
+    _check_tm("v", v, T, N, ld, dev, dt); _check_tm("bv", bv, T, N, ld, dev, dt)
+    _check_tm("term", term, T, N, ld, dev, flags=True); _check_tm("trunc", trunc, T, N, ld, dev, flags=True)
+    _boot_tm(boot, N, dt, dev)
+    ret = _out_tm("ret", ret, T, N, ld, dev)
+    wp, wb = _ws(ws, dev)
+    with torch.cuda.device(dev):
+        _call("rlcs_td_lambda_tm", _ptr(r), _ptr(v), _ptr(term), _ptr(trunc), _ptr(bv),
+              _ptr(boot), _ptr(ret), N, T, ld, gamma, lam, _DTYPES[dt], wp, wb, _stream(dev))
+    return ret
+
+
+def rlcs_discounted_tm(r, term=None, trunc=None, bv=None, boot=None, ret=None, *, gamma: float,
+                       ws=None) -> torch.Tensor:
+    T, N, ld, dt, dev = _prep_tm(r)
+    _check_tm("bv", bv, T, N, ld, dev, dt)
+    _check_tm("term", term, T, N, ld, dev, flags=True); _check_tm("trunc", trunc, T, N, ld, dev, flags=True)
+    _boot_tm(boot, N, dt, dev)
+    ret = _out_tm("ret", ret, T, N, ld, dev)
+    wp, wb = _ws(ws, dev)
+    with torch.cuda.device(dev):
+        _call("rlcs_discounted_tm", _ptr(r), _ptr(term), _ptr(trunc), _ptr(bv), _ptr(boot),
+              _ptr(ret), N, T, ld, gamma, _DTYPES[dt], wp, wb, _stream(dev))
+    return ret
+
+
+def rlcs_elig_trace_tm(x, term=None, trunc=None, z=None, *, gamma: float, lam: float,
+                       ws=None) -> torch.Tensor:
+    T, N, ld, dt, dev = _prep_tm(x)
+    _check_tm("term", term, T, N, ld, dev, flags=True); _check_tm("trunc", trunc, T, N, ld, dev, flags=True)
+    z = _out_tm("z", z, T, N, ld, dev)
+    wp, wb = _ws(ws, dev)
+    with torch.cuda.device(dev):
+        _call("rlcs_elig_trace_tm", _ptr(x), _ptr(term), _ptr(trunc), _ptr(z), N, T, ld, gamma,
+              lam, _DTYPES[dt], wp, wb, _stream(dev))
+    return z
+
+
+def rlcs_episodic_prefix_tm(x, term=None, trunc=None, c=None, *, boundary: str = "ends_at",
+                            ws=None) -> torch.Tensor:
+    T, N, ld, dt, dev = _prep_tm(x)
+    if boundary not in ("ends_at", "starts_at"):
+        raise ValueError(f"boundary must be 'ends_at' or 'starts_at', got {boundary!r}")
+    _check_tm("term", term, T, N, ld, dev, flags=True); _check_tm("trunc", trunc, T, N, ld, dev, flags=True)
+    c = _out_tm("c", c, T, N, ld, dev)
+    wp, wb = _ws(ws, dev)
+    b = _native.RLCS_STARTS_AT if boundary == "starts_at" else _native.RLCS_ENDS_AT
+    with torch.cuda.device(dev):
+        _call("rlcs_episodic_prefix_tm", _ptr(x), _ptr(term), _ptr(trunc), _ptr(c), N, T, ld, b,
+              _DTYPES[dt], wp, wb, _stream(dev))
+    return c
+
+
+# ---------------------------------------------------------------- vector eligibility traces
+
+def rlcs_elig_trace_vec(x, term=None, trunc=None, z=None, *, gamma: float, lam: float,
+                        ws=None) -> torch.Tensor:
+    """x: contiguous [N, T, F] float32 / bfloat16; flags [N, T]; returns float32 z [N, T, F]."""
+    if not isinstance(x, torch.Tensor) or x.dim() != 3:
+        raise ValueError("x must be a 3-D [N, T, F] tensor")
+    if x.dtype not in _DTYPES:
+        raise TypeError(f"x must be float32 or bfloat16, got {x.dtype}")
+    if x.device.type != "cuda" or not x.is_contiguous():
+        raise ValueError("x must be a contiguous tensor on a GPU")
+    N, T, F = (int(s) for s in x.shape)
+    dev = x.device
+    _check_flags("term", term, N, T, dev); _check_flags("trunc", trunc, N, T, dev)
+    if z is None:
+        z = torch.empty((N, T, F), dtype=torch.float32, device=dev)
+    elif z.dtype != torch.float32 or tuple(z.shape) != (N, T, F) or z.device != dev \
+            or not z.is_contiguous():
+        raise ValueError(f"z must be a contiguous float32 [N, T, F] tensor on {dev}")
+    wp, wb = _ws(ws, dev)
+    with torch.cuda.device(dev):
+        _call("rlcs_elig_trace_vec", _ptr(x), _ptr(term), _ptr(trunc), _ptr(z), N, T, F, gamma,
+              lam, _DTYPES[x.dtype], wp, wb, _stream(dev))
+    return z

@@ -1,0 +1,391 @@
+// Column scans: the recurrence of Section 1 (Eq. 1) along T for each of J columns whose
+// steps are strided in memory, for the time-major [T, N] layout (a column is an environment,
+// consecutive environments are adjacent) and for F-vector eligibility traces [N, T, F] (a
+// column is one feature of one row; every feature of a step shares the step's flags and so
+// its coefficient beta_t, Section 3.3.5).
+//
+// Geometry: column j = b * C + c (batch row b, column c within it) holds step t at element
+//   (j / C) * bstride + (j % C) + t * st,
+// and its flags at the same element (`fcol`, time-major) or at (j / C) * fbstride + t * fst
+// (one flag per step of a batch row, vector traces). The per-column row value (bootstrap) is
+// element j of its array.
+//
+// Lanes own columns, so consecutive lanes read consecutive elements of a step (coalesced),
+// and a lane's K steps are consecutive in time. A workgroup of W waves covers 64 columns and
+// W*K consecutive steps (a chunk): wave w owns steps t0 + w*K .. t0 + w*K + K-1. Per lane:
+//   1. load the K steps (flags first, then data, the neighbour step on the carry-source side
+//      and the row value; continuation values only at truncated steps, once the flags are in);
+//   2. build alpha, beta with the estimator's policy (Table 1, Section 3.2);
+//   3. compose the K steps serially into one affine map;
+//   4. compose the maps of the waves on the carry-source side (LDS);
+//   5. take the value entering the chunk (previous chunk of the same workgroup, or the
+//      published maps of other workgroups' tiles) and finish the K steps; store.
+// cols_rows_kernel walks all of T in chunks (carry through LDS); cols_tiles_kernel gives each
+// chunk its own workgroup and carries between them with the workspace protocol of the split-row
+// kernel, per column: a tile publishes its 64 composed maps and composes the maps of the tiles
+// on its carry-source side, nearest first, until it meets beta = 0 (an episode or row edge).
+// Tiles only ever wait for tiles of their own column block, so each block has its own ticket
+// counter: tickets order the block's tiles from the carry source, and no counter is touched by
+// every workgroup of the grid.
+//
+// Workspace of cols_tiles_kernel (the layout of rlcs_kernels.h, zero-filled once):
+//   header: `state` = call epoch << 32 | number of column blocks finished in this call, and the
+//     error flag;
+//   per-block slots: ticket counter (32 bits), finished tiles (32 bits), 64 bytes per block
+//     (at most kWsSlots blocks);
+//   records: two 64-bit words per column per tile, (tag << 32 | bits(a)), (tag << 32 | bits(b)),
+//     valid for the current call when tag = 2*epoch+1.
+// Every workgroup reads the epoch when it starts. The epoch only advances when the last tile of
+// the call finishes (the last tile of a block counts the block finished; the last block advances
+// the epoch and clears the count), so every workgroup of a call reads the same epoch and every
+// call on a workspace has its own, whatever the geometry of the calls before it. The last
+// drawer of a block resets its ticket counter and the last finisher its finished count, so the
+// next call on the same stream finds the workspace ready.
+#pragma once
+
+#include "rlcs_kernels.h"
+
+namespace rlcs {
+
+struct ColGeom {
+    int64_t J;         // columns
+    int64_t C;         // columns per batch row
+    int64_t st;        // elements between consecutive steps of a column
+    int64_t bstride;   // elements between batch rows
+    int64_t fst;       // flags between consecutive steps (flags not per column)
+    int64_t fbstride;  // flags between batch rows (flags not per column)
+    int fcol;          // flags laid out like the data
+};
+
+constexpr int kColK = 8;  // steps per lane
+constexpr int kColW = 4;  // waves per workgroup (time sub-spans of a chunk)
+constexpr int kColL = kColK * kColW;  // steps per chunk
+
+// One lane's K steps of one column.
+template <class Op, typename DT, int K, bool TR>
+struct ColChunk {
+    static constexpr bool kBack = Op::kBackward;
+    static constexpr int NS = Op::kSlots;
+    static constexpr int NB = Op::kNbr > 0 ? Op::kNbr : 1;
+    static constexpr int kTS = TR ? Op::kTruncSlot : -1;
+
+    float d[NS][K];
+    float B[K];
+    float nb[NB];
+    float al[K], be[K];
+    uint32_t term, trunc, edge, valid;
+    int64_t t0;
+
+    // Step 1. `base`: element of step 0 of the column; `fbase`, `fstep`: its flags. Inactive
+    // lanes (columns past J) have no valid step and load nothing.
+    __device__ __forceinline__ void load(const Args& a, bool active, int64_t j, int64_t base, int64_t st,
+                         int64_t fbase, int64_t fstep, int64_t t0_) {
+        t0 = t0_;
+        const int64_t T = a.T;
+        valid = 0;
+        if (active) {
+#pragma unroll
+            for (int k = 0; k < K; ++k)
+                if (t0 + k < T) valid |= 1u << k;
+        }
+        uint8_t tb[K], rb[K];
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+            tb[k] = 0;
+            rb[k] = 0;
+            if (Op::kFlags && bit(valid, k)) {
+                if (a.term) tb[k] = a.term[fbase + (t0 + k) * fstep];
+                if (TR) rb[k] = a.trunc[fbase + (t0 + k) * fstep];
+            }
+        }
+#pragma unroll
+        for (int s = 0; s < NS; ++s) {
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+                d[s][k] = 0.f;
+                if (Op::slot_used(s, TR) && s != kTS && bit(valid, k))
+                    d[s][k] = load_one<DT>(a.in[s], base + (t0 + k) * st);
+            }
+        }
+        // neighbour on the carry-source side and the row value at the row edge
+        float nraw[Op::kNbrRaw];
+        bool have_nbr = false;
+        uint8_t pt = 0, pr = 0;
+        edge = 0;
+#pragma unroll
+        for (int k = 0; k < K; ++k) B[k] = 0.f;
+        if (valid) {
+            if (kBack) {
+                if (Op::kNbr > 0 && t0 + K < T) {
+                    Op::template nbr_load_raw<DT>(a, base + (t0 + K) * st, nraw);
+                    have_nbr = true;
+                }
+                if (t0 + K >= T) {  // the column's last step T-1 is among the lane's steps
+                    const int ke = int(T - 1 - t0);
+                    edge = 1u << ke;
+                    const float rv = (Op::kRowValue && a.row_value) ? load_one<DT>(a.row_value, j) : 0.f;
+#pragma unroll
+                    for (int k = 0; k < K; ++k)
+                        if (k == ke) B[k] = rv;
+                }
+            } else {
+                if (Op::kNbr > 0 && t0 > 0) {
+                    if (a.term) pt = a.term[fbase + (t0 - 1) * fstep];
+                    if (TR) pr = a.trunc[fbase + (t0 - 1) * fstep];
+                }
+                if (t0 == 0) edge = 1u;
+            }
+        }
+        term = 0;
+        trunc = 0;
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+            if (tb[k]) term |= 1u << k;
+            if (rb[k]) trunc |= 1u << k;
+        }
+        if constexpr (kTS >= 0) {
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+                d[kTS][k] = 0.f;
+                if (bit(trunc, k)) d[kTS][k] = load_one<DT>(a.in[kTS], base + (t0 + k) * st);
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < NB; ++i) nb[i] = 0.f;
+        if constexpr (kBack) {
+            if (have_nbr) Op::nbr_fix(a, nraw, nb);
+        } else if constexpr (Op::kNbr > 0) {
+            nb[0] = (pt || (TR && pr)) ? 1.f : 0.f;
+        }
+    }
+
+    // Steps 2-3: the lane's map (nearest-to-output step outermost).
+    __device__ __forceinline__ Pair local(const Params& P) {
+        Op::template build<K, TR>(P, d, term, trunc, edge, B, nb, al, be);
+#pragma unroll
+        for (int k = 0; k < K; ++k)
+            if (!bit(valid, k)) { al[k] = 0.f; be[k] = 1.f; }
+        Pair agg;
+        if (kBack) {
+            agg = Pair{al[K - 1], be[K - 1]};
+#pragma unroll
+            for (int k = K - 2; k >= 0; --k) agg = compose(Pair{al[k], be[k]}, agg);
+        } else {
+            agg = Pair{al[0], be[0]};
+#pragma unroll
+            for (int k = 1; k < K; ++k) agg = compose(Pair{al[k], be[k]}, agg);
+        }
+        return agg;
+    }
+
+    // Step 5 given X, the value entering the lane's steps from the carry-source side. Returns
+    // the value of the lane's step nearest the output side.
+    __device__ __forceinline__ float finish(const Args& a, const Params& P, int64_t base, int64_t st, float X) {
+        float A[K];
+        if (kBack) {
+            float nxt = X;
+#pragma unroll
+            for (int k = K - 1; k >= 0; --k) { A[k] = fmaf(be[k], nxt, al[k]); nxt = A[k]; }
+        } else {
+            float prv = X;
+#pragma unroll
+            for (int k = 0; k < K; ++k) { A[k] = fmaf(be[k], prv, al[k]); prv = A[k]; }
+        }
+        float o0[K], o1[K];
+        Op::template finish<K, TR>(P, d, term, trunc, edge, B, nb, A, X, o0, o1);
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+            if (!bit(valid, k)) continue;
+            const int64_t e = base + (t0 + k) * st;
+            __builtin_nontemporal_store(o0[k], a.out0 + e);
+            if (a.out1) __builtin_nontemporal_store(o1[k], a.out1 + e);
+        }
+        return kBack ? A[0] : A[K - 1];
+    }
+};
+
+// Per-lane column placement.
+struct ColLane {
+    int64_t j, base, fbase, fstep;
+    bool active;
+};
+
+__device__ __forceinline__ ColLane col_lane(const ColGeom& g, int64_t block) {
+    ColLane l;
+    l.j = block * kWave + (threadIdx.x & (kWave - 1));
+    l.active = l.j < g.J;
+    const int64_t jj = l.active ? l.j : 0;
+    const int64_t b = jj / g.C, c = jj - b * g.C;
+    l.base = b * g.bstride + c;
+    l.fbase = g.fcol ? l.base : b * g.fbstride;
+    l.fstep = g.fcol ? g.st : g.fst;
+    return l;
+}
+
+// Composition of the maps of the waves on wave `wave`'s carry-source side (LDS, per lane).
+template <bool kBack, int W>
+__device__ __forceinline__ Pair cols_wave_in(const float (*s_a)[kWave], const float (*s_b)[kWave],
+                                             int wave, int lane) {
+    Pair acc = identity_pair();
+    if (kBack) {
+        for (int w = W - 1; w > wave; --w) acc = compose(Pair{s_a[w][lane], s_b[w][lane]}, acc);
+    } else {
+        for (int w = 0; w < wave; ++w) acc = compose(Pair{s_a[w][lane], s_b[w][lane]}, acc);
+    }
+    return acc;
+}
+
+// Whole columns per workgroup: chunks walked from the carry source, the value at the chunk's
+// output-side edge carried to the next chunk through LDS. Grid: ceil(J / 64) workgroups.
+template <class Op, typename DT, int K, int W, bool TR>
+__global__ void __launch_bounds__(W * kWave) cols_rows_kernel(Args a, ColGeom g) {
+    constexpr bool kBack = Op::kBackward;
+    constexpr int64_t L = int64_t(W) * K;
+    __shared__ float s_a[W][kWave], s_b[W][kWave];
+    __shared__ float s_carry[kWave];
+    const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+    const ColLane cl = col_lane(g, blockIdx.x);
+    const int64_t T = a.T;
+    const int64_t P = (T + L - 1) / L;
+    float carry = 0.f;
+    for (int64_t i = 0; i < P; ++i) {
+        const int64_t p = kBack ? P - 1 - i : i;
+        ColChunk<Op, DT, K, TR> c;
+        c.load(a, cl.active, cl.j, cl.base, g.st, cl.fbase, cl.fstep, p * L + int64_t(wave) * K);
+        const Pair m = c.local(a.p);
+        s_a[wave][lane] = m.a;
+        s_b[wave][lane] = m.b;
+        __syncthreads();
+        const Pair win = cols_wave_in<kBack, W>(s_a, s_b, wave, lane);
+        const float out_edge = c.finish(a, a.p, cl.base, g.st, apply(win, carry));
+        if (wave == (kBack ? 0 : W - 1)) s_carry[lane] = out_edge;
+        __syncthreads();
+        carry = s_carry[lane];
+    }
+}
+
+// Look-back of one lane's column: the value entering tile `tile` from its carry-source side,
+// composed from the published maps of the column's tiles, nearest first, until a map with
+// beta = 0 (the column's edge tile always has one). Up to kColLookAhead records are read per
+// round. Bounded polls: on exhaustion the error flag is set and NaN returned.
+constexpr int kColLookAhead = 4;
+
+template <bool kBack>
+__device__ float cols_gather(const uint64_t* rec, int64_t tile, int64_t P, int64_t J, int64_t j,
+                             uint32_t tag, WsHeader* hdr) {
+    Pair acc = identity_pair();
+    int64_t dist = 1;
+    for (;;) {
+        uint64_t w0[kColLookAhead], w1[kColLookAhead];
+#pragma unroll
+        for (int i = 0; i < kColLookAhead; ++i) {
+            const int64_t q = kBack ? tile + dist + i : tile - dist - i;
+            const bool inside = kBack ? (q < P) : (q >= 0);
+            w0[i] = w1[i] = 0;
+            if (inside) {
+                w0[i] = ld_relaxed(rec + 2 * (q * J + j));
+                w1[i] = ld_relaxed(rec + 2 * (q * J + j) + 1);
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < kColLookAhead; ++i) {
+            const int64_t q = kBack ? tile + dist + i : tile - dist - i;
+            const bool inside = kBack ? (q < P) : (q >= 0);
+            if (!inside) return acc.a;  // past the column's edge tile (not reached in practice)
+            uint32_t polls = 0;
+            while (uint32_t(w0[i] >> 32) != tag || uint32_t(w1[i] >> 32) != tag) {
+                if (++polls > kMaxPolls) {
+                    st_relaxed(&hdr->error, 1u);
+                    return __builtin_nanf("");
+                }
+                __builtin_amdgcn_s_sleep(1);
+                w0[i] = ld_relaxed(rec + 2 * (q * J + j));
+                w1[i] = ld_relaxed(rec + 2 * (q * J + j) + 1);
+            }
+            const Pair m{__uint_as_float(uint32_t(w0[i])), __uint_as_float(uint32_t(w1[i]))};
+            acc = compose(acc, m);
+            if (m.b == 0.f) return acc.a;
+        }
+        dist += kColLookAhead;
+    }
+}
+
+// One chunk per workgroup. Workgroup g serves column block g mod num_blocks; its ticket among
+// that block's P workgroups orders the block's tiles from the carry source, so a tile only waits
+// for tiles of its block that drew earlier tickets. Grid: num_blocks * P workgroups.
+template <class Op, typename DT, int K, int W, bool TR>
+__global__ void __launch_bounds__(W * kWave) cols_tiles_kernel(Args a, ColGeom g, int64_t num_blocks) {
+    constexpr bool kBack = Op::kBackward;
+    constexpr int64_t L = int64_t(W) * K;
+    __shared__ float s_a[W][kWave], s_b[W][kWave];
+    __shared__ float s_carry[kWave];
+    __shared__ uint32_t s_ticket, s_tag;
+    WsHeader* hdr = reinterpret_cast<WsHeader*>(a.ws);
+    char* slots = reinterpret_cast<char*>(a.ws) + sizeof(WsHeader);
+    uint64_t* rec = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(a.ws) + kWsRecordsOffset);
+    const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+    const int64_t T = a.T;
+    const int64_t P = (T + L - 1) / L;
+    const int64_t block = int64_t(blockIdx.x) % num_blocks;
+
+    uint32_t* slot = reinterpret_cast<uint32_t*>(slots + block * 64);
+    if (threadIdx.x == 0) {
+        const uint32_t epoch = uint32_t(ld_relaxed(&hdr->state) >> 32);
+        const uint32_t ticket = __hip_atomic_fetch_add(slot, 1u, __ATOMIC_RELAXED,
+                                                       __HIP_MEMORY_SCOPE_AGENT);
+        if (ticket == uint32_t(P - 1)) st_relaxed(slot, 0u);
+        s_ticket = ticket;
+        s_tag = 2u * epoch + 1u;
+    }
+    __syncthreads();
+    const uint32_t tag = s_tag;
+    const int64_t ticket = s_ticket;
+    if (ticket >= P) {
+        // Only possible if the workspace was not zero-filled before first use.
+        if (threadIdx.x == 0) st_relaxed(&hdr->error, 1u);
+        return;
+    }
+    const int64_t p = kBack ? P - 1 - ticket : ticket;
+    const ColLane cl = col_lane(g, block);
+
+    ColChunk<Op, DT, K, TR> c;
+    c.load(a, cl.active, cl.j, cl.base, g.st, cl.fbase, cl.fstep, p * L + int64_t(wave) * K);
+    const Pair m = c.local(a.p);
+    s_a[wave][lane] = m.a;
+    s_b[wave][lane] = m.b;
+    __syncthreads();
+    const Pair win = cols_wave_in<kBack, W>(s_a, s_b, wave, lane);
+    const bool publish = kBack ? (p > 0) : (p < P - 1);
+    const bool need = kBack ? (p < P - 1) : (p > 0);
+    if (wave == 0) {
+        if (publish && cl.active) {
+            // the whole tile's map of this column
+            Pair tm = identity_pair();
+            if (kBack) {
+                for (int w = W - 1; w >= 0; --w) tm = compose(Pair{s_a[w][lane], s_b[w][lane]}, tm);
+            } else {
+                for (int w = 0; w < W; ++w) tm = compose(Pair{s_a[w][lane], s_b[w][lane]}, tm);
+            }
+            const uint64_t hi_tag = uint64_t(tag) << 32;
+            st_relaxed(rec + 2 * (p * g.J + cl.j), hi_tag | __float_as_uint(tm.a));
+            st_relaxed(rec + 2 * (p * g.J + cl.j) + 1, hi_tag | __float_as_uint(tm.b));
+        }
+        s_carry[lane] = (need && cl.active) ? cols_gather<kBack>(rec, p, P, g.J, cl.j, tag, hdr) : 0.f;
+    }
+    __syncthreads();
+    c.finish(a, a.p, cl.base, g.st, apply(win, s_carry[lane]));
+    if (threadIdx.x == 0) {
+        // this tile is done with the epoch (its records and look-back are behind it)
+        const uint32_t done = __hip_atomic_fetch_add(slot + 1, 1u, __ATOMIC_RELAXED,
+                                                     __HIP_MEMORY_SCOPE_AGENT);
+        if (done == uint32_t(P - 1)) {
+            st_relaxed(slot + 1, 0u);
+            const uint64_t old = __hip_atomic_fetch_add(&hdr->state, uint64_t(1), __ATOMIC_RELAXED,
+                                                        __HIP_MEMORY_SCOPE_AGENT);
+            if (uint32_t(old) == uint32_t(num_blocks - 1))
+                st_relaxed(&hdr->state, uint64_t(((old >> 32) + 1u) & 0x7fffffffu) << 32);
+        }
+    }
+}
+
+}  // namespace rlcs

@@ -1,0 +1,95 @@
+// Host side of the column scans (time-major layouts, vector eligibility traces): checks,
+// the choice between whole columns per workgroup and split columns, and the launches.
+#pragma once
+
+#include "rlcs_columns.h"
+#include "rlcs_dispatch.h"
+
+namespace rlcs {
+namespace host {
+
+// Column blocks (64 columns each) from which whole columns per workgroup already fill the GPU;
+// below it, columns longer than one chunk are split into one-chunk tiles when a workspace is
+// given. Never more than the workspace's per-block slots.
+constexpr int64_t kColSerialBlocks = kWsSlots;
+
+inline int64_t col_tiles(int64_t T) { return (T + kColL - 1) / kColL; }
+
+// Workspace bytes of a split column call: header and block slots, then two records per column
+// per tile (0 if the size does not fit in size_t).
+inline size_t col_ws_need(int64_t J, int64_t T) {
+    const int64_t P = col_tiles(T);
+    if (J <= 0 || P <= 0) return kWsRecordsOffset;
+    if (P > INT64_MAX / J || P * J > int64_t(SIZE_MAX / kWsRecordBytes) / 2) return 0;
+    return kWsRecordsOffset + size_t(P * J) * kWsRecordBytes;
+}
+
+template <class Op, typename DT, bool TR>
+void col_launch(const Args& a, const ColGeom& g, bool split, int64_t blocks, hipStream_t s) {
+    const dim3 block(kColW * kWave);
+    if (split) {
+        hipLaunchKernelGGL((cols_tiles_kernel<Op, DT, kColK, kColW, TR>),
+                           dim3(unsigned(blocks * col_tiles(a.T))), block, 0, s, a, g, blocks);
+    } else {
+        hipLaunchKernelGGL((cols_rows_kernel<Op, DT, kColK, kColW, TR>), dim3(unsigned(blocks)),
+                           block, 0, s, a, g);
+    }
+}
+
+template <class Op>
+rlcs_status col_dispatch(Args& a, const ColGeom& g, rlcs_dtype dtype, bool has_trunc, void* ws,
+                         size_t ws_bytes, rlcs_stream_t stream) {
+    if (g.J == 0 || a.T == 0) return RLCS_OK;
+    const int64_t blocks = (g.J + kWave - 1) / kWave;
+    const int64_t P = col_tiles(a.T);
+    const size_t need = col_ws_need(g.J, a.T);
+    const bool ws_ok = ws && need > 0 && ws_bytes >= need && aligned(ws, 64) &&
+                       blocks <= int64_t(UINT32_MAX) / P;
+    const int forced = g_variant.load(std::memory_order_relaxed);
+    bool split;
+    if (forced == 2) {
+        if (!ws_ok) return RLCS_ERR_WORKSPACE;
+        split = blocks <= kWsSlots;  // more blocks than slots: whole columns
+    } else if (forced == 1) {
+        split = false;
+    } else {
+        split = P > 1 && ws_ok && blocks < kColSerialBlocks;
+    }
+    if (split) {
+        if (blocks * P > INT32_MAX) return RLCS_ERR_INVALID_ARG;
+        a.ws = ws;
+    } else if (blocks > INT32_MAX) {
+        return RLCS_ERR_INVALID_ARG;
+    }
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    const bool tr = Op::kFlags && has_trunc;
+    if (dtype == RLCS_BF16) {
+        if (tr) col_launch<Op, bf16_t, true>(a, g, split, blocks, s);
+        else col_launch<Op, bf16_t, false>(a, g, split, blocks, s);
+    } else {
+        if (tr) col_launch<Op, float, true>(a, g, split, blocks, s);
+        else col_launch<Op, float, false>(a, g, split, blocks, s);
+    }
+    return hipGetLastError() == hipSuccess ? RLCS_OK : RLCS_ERR_LAUNCH;
+}
+
+// Time-major [T, ld] geometry (ld >= N; 0 means N): column n is environment n, flags laid out
+// like the data. Checks sizes, dtype, ld and alignment; fills `g`.
+inline rlcs_status check_time_major(int64_t N, int64_t T, int64_t& ld, rlcs_dtype dtype,
+                                    std::initializer_list<const void*> data,
+                                    std::initializer_list<const void*> outs, ColGeom& g) {
+    if (N < 0 || T < 0) return RLCS_ERR_INVALID_ARG;
+    if (dtype != RLCS_F32 && dtype != RLCS_BF16) return RLCS_ERR_DTYPE;
+    if (ld == 0) ld = N;
+    if (ld < N || T > kMaxT || (T > 0 && ld > INT64_MAX / T)) return RLCS_ERR_INVALID_ARG;
+    const size_t es = dtype_size(dtype);
+    for (const void* p : data)
+        if (p && !aligned(p, es)) return RLCS_ERR_INVALID_ARG;
+    for (const void* p : outs)
+        if (p && !aligned(p, 4)) return RLCS_ERR_INVALID_ARG;
+    g = ColGeom{N, N > 0 ? N : 1, ld, 0, 0, 0, 1};
+    return RLCS_OK;
+}
+
+}  // namespace host
+}  // namespace rlcs

@@ -1,0 +1,72 @@
+// Column-scan entry points of the forward recurrences (Table 1; Sections 3.3.5-3.3.6):
+// time-major eligibility traces and prefix sums, eligibility traces of F-vectors, and the
+// workspace size of the column scans.
+#include "rlcs_columns_dispatch.h"
+
+using namespace rlcs;
+using namespace rlcs::host;
+
+extern "C" {
+
+rlcs_status rlcs_elig_trace_tm(const void* x, const uint8_t* term, const uint8_t* trunc, float* z,
+                               int64_t N, int64_t T, int64_t ld, float gamma, float lambda,
+                               rlcs_dtype dtype, void* ws, size_t ws_bytes, rlcs_stream_t stream) {
+    ColGeom g;
+    rlcs_status st = check_time_major(N, T, ld, dtype, {x}, {z}, g);
+    if (st != RLCS_OK) return st;
+    if (!unit_interval(gamma) || !unit_interval(lambda)) return RLCS_ERR_INVALID_ARG;
+    if (N == 0 || T == 0) return RLCS_OK;
+    if (!x || !z) return RLCS_ERR_INVALID_ARG;
+    Args a = make_args(N, T, gamma, lambda, 1.f, 1.f);
+    a.in[0] = x;
+    a.term = term; a.trunc = trunc;
+    a.out0 = z;
+    return col_dispatch<ForwardOp<true, false>>(a, g, dtype, trunc != nullptr, ws, ws_bytes, stream);
+}
+
+rlcs_status rlcs_episodic_prefix_tm(const void* x, const uint8_t* term, const uint8_t* trunc,
+                                    float* c, int64_t N, int64_t T, int64_t ld,
+                                    rlcs_boundary boundary, rlcs_dtype dtype, void* ws,
+                                    size_t ws_bytes, rlcs_stream_t stream) {
+    ColGeom g;
+    rlcs_status st = check_time_major(N, T, ld, dtype, {x}, {c}, g);
+    if (st != RLCS_OK) return st;
+    if (boundary != RLCS_ENDS_AT && boundary != RLCS_STARTS_AT) return RLCS_ERR_INVALID_ARG;
+    if (N == 0 || T == 0) return RLCS_OK;
+    if (!x || !c) return RLCS_ERR_INVALID_ARG;
+    Args a = make_args(N, T, 1.f, 1.f, 1.f, 1.f);
+    a.in[0] = x;
+    a.term = term; a.trunc = trunc;
+    a.out0 = c;
+    if (boundary == RLCS_STARTS_AT)
+        return col_dispatch<ForwardOp<false, true>>(a, g, dtype, trunc != nullptr, ws, ws_bytes, stream);
+    return col_dispatch<ForwardOp<false, false>>(a, g, dtype, trunc != nullptr, ws, ws_bytes, stream);
+}
+
+rlcs_status rlcs_elig_trace_vec(const void* x, const uint8_t* term, const uint8_t* trunc,
+                                float* z, int64_t N, int64_t T, int64_t F, float gamma,
+                                float lambda, rlcs_dtype dtype, void* ws, size_t ws_bytes,
+                                rlcs_stream_t stream) {
+    if (N < 0 || T < 0 || F < 0) return RLCS_ERR_INVALID_ARG;
+    if (dtype != RLCS_F32 && dtype != RLCS_BF16) return RLCS_ERR_DTYPE;
+    if (T > kMaxT || (T > 0 && F > 0 && N > INT64_MAX / T / F)) return RLCS_ERR_INVALID_ARG;
+    if (x && !aligned(x, dtype_size(dtype))) return RLCS_ERR_INVALID_ARG;
+    if (z && !aligned(z, 4)) return RLCS_ERR_INVALID_ARG;
+    if (!unit_interval(gamma) || !unit_interval(lambda)) return RLCS_ERR_INVALID_ARG;
+    if (N == 0 || T == 0 || F == 0) return RLCS_OK;
+    if (!x || !z) return RLCS_ERR_INVALID_ARG;
+    Args a = make_args(N, T, gamma, lambda, 1.f, 1.f);
+    a.in[0] = x;
+    a.term = term; a.trunc = trunc;
+    a.out0 = z;
+    // column n*F + f: feature f of row n; flags one per step of a row
+    const ColGeom g{N * F, F, F, T * F, 1, T, 0};
+    return col_dispatch<ForwardOp<true, false>>(a, g, dtype, trunc != nullptr, ws, ws_bytes, stream);
+}
+
+size_t rlcs_workspace_size_columns(int64_t columns, int64_t T) {
+    if (columns < 0 || T < 0) return 0;
+    return col_ws_need(columns, T);
+}
+
+}  // extern "C"

@@ -13,10 +13,10 @@ std::atomic<int> g_variant{0};
 extern "C" {
 
 size_t rlcs_workspace_size(int64_t N, int64_t T) {
-    if (N <= 0 || T <= 0) return sizeof(WsHeader);
+    if (N <= 0 || T <= 0) return kWsRecordsOffset;
     if (N > INT64_MAX / T) return 0;
     const int64_t tiles = (N * T + kMinTile - 1) / kMinTile;
-    return sizeof(WsHeader) + size_t(tiles) * kWsRecordBytes;
+    return kWsRecordsOffset + size_t(tiles) * kWsRecordBytes;
 }
 
 const char* rlcs_status_string(rlcs_status status) {

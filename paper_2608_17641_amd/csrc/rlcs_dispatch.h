@@ -131,7 +131,7 @@ rlcs_status dispatch_dt(Args& a, bool has_trunc, void* ws, size_t ws_bytes, hipS
 
     Plan p{};
     p.num_tiles = (total + E_large - 1) / E_large;
-    const size_t ws_need = sizeof(WsHeader) + size_t(p.num_tiles) * kWsRecordBytes;
+    const size_t ws_need = kWsRecordsOffset + size_t(p.num_tiles) * kWsRecordBytes;
     const bool ws_ok = ws && ws_bytes >= ws_need && aligned(ws, 64) && p.num_tiles < int64_t(UINT32_MAX);
     const int forced = g_variant.load(std::memory_order_relaxed);
     if constexpr (Op::kStaged > 0) {

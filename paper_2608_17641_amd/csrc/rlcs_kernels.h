@@ -31,21 +31,29 @@
 
 namespace rlcs {
 
-// Workspace layout of the tiles kernel (zero-filled once by the caller):
-//   header: ticket counter, call epoch, error flag;
-//   then two 64-bit words per tile: (tag << 32 | bits(a)) and (tag << 32 | bits(b)).
-// A record is valid for the current call when its tag equals 2*epoch+1. The workgroup that
-// draws the last ticket of a call resets the counter and advances the epoch (every other
-// workgroup of the call read the epoch before drawing its ticket), so stale records never
-// match and the next call on the same stream finds the header ready.
+// Workspace layout (zero-filled once by the caller), shared by the split kernels of every
+// entry point so that one workspace serves calls of any kind and shape:
+//   header (64 bytes): `state` (call epoch in the high half, a per-call counter in the low
+//   half) and an error flag;
+//   kWsSlotsBytes of per-block counters (column scans only);
+//   from kWsRecordsOffset, the records: two 64-bit words per tile (per column and tile for the
+//   column scans), (tag << 32 | bits(a)) and (tag << 32 | bits(b)).
+// Tiles kernel:
+// A record is valid for the current call when its tag equals 2*epoch+1. Each workgroup draws
+// its ticket and the call's epoch with one atomic add on the draw state; the workgroup that
+// draws the last ticket of a call stores (epoch + 1, 0), so stale records never match and the
+// next call on the same stream finds the state ready. Nothing but the draw touches the state,
+// so no fence is needed (records carry their own tag).
 struct WsHeader {
-    uint32_t ticket;
-    uint32_t epoch;
+    uint64_t state;  // epoch << 32 | ticket
     uint32_t error;  // set to 1 if a call found the workspace in an inconsistent state
     uint32_t pad[13];
 };
 static_assert(sizeof(WsHeader) == 64, "workspace header is 64 bytes");
 constexpr size_t kWsRecordBytes = 16;
+constexpr int64_t kWsSlots = 1024;  // column blocks a split column scan may have
+constexpr size_t kWsSlotsBytes = size_t(kWsSlots) * 64;
+constexpr size_t kWsRecordsOffset = sizeof(WsHeader) + kWsSlotsBytes;
 
 template <typename T>
 __device__ __forceinline__ T ld_relaxed(const T* p) {
@@ -54,6 +62,19 @@ __device__ __forceinline__ T ld_relaxed(const T* p) {
 template <typename T>
 __device__ __forceinline__ void st_relaxed(T* p, T v) {
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Ticket of a workgroup among the n_tiles workgroups of a call that share the draw state
+// `state`, and the call's record tag; drawn by one thread with a single relaxed atomic.
+__device__ __forceinline__ uint32_t draw_ticket(uint64_t* state, int64_t n_tiles, uint32_t& tag) {
+    const uint64_t old = __hip_atomic_fetch_add(state, uint64_t(1), __ATOMIC_RELAXED,
+                                                __HIP_MEMORY_SCOPE_AGENT);
+    const uint32_t ticket = uint32_t(old);
+    const uint32_t epoch = uint32_t(old >> 32);
+    if (ticket == uint32_t(n_tiles - 1))
+        st_relaxed(state, uint64_t((epoch + 1u) & 0x7fffffffu) << 32);
+    tag = 2u * epoch + 1u;
+    return ticket;
 }
 
 // Lane l of a wave owns the l-th group of K steps of the wave's span for forward scans and the
@@ -623,27 +644,18 @@ __global__ void __launch_bounds__(W * kWave) tiles_kernel(Args a, int64_t num_ti
     constexpr int64_t E = int64_t(W) * kWave * K;
     __shared__ float s_a[W], s_b[W];
     __shared__ float s_carry;
-    __shared__ uint32_t s_ticket, s_epoch;
+    __shared__ uint32_t s_ticket, s_tag;
     WsHeader* hdr = reinterpret_cast<WsHeader*>(a.ws);
-    uint64_t* rec = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(a.ws) + sizeof(WsHeader));
+    uint64_t* rec = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(a.ws) + kWsRecordsOffset);
     const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
 
     if (threadIdx.x == 0) {
-        const uint32_t epoch = ld_relaxed(&hdr->epoch);
-        // release: the epoch read above is ordered before the ticket draw; acquire: the last
-        // drawer sees every earlier draw (and so every earlier epoch read) before resetting.
-        const uint32_t ticket = __hip_atomic_fetch_add(&hdr->ticket, 1u, __ATOMIC_ACQ_REL,
-                                                       __HIP_MEMORY_SCOPE_AGENT);
-        if (ticket == uint32_t(num_tiles - 1)) {
-            st_relaxed(&hdr->ticket, 0u);
-            st_relaxed(&hdr->epoch, (epoch + 1u) & 0x7fffffffu);
-        }
-        s_epoch = epoch;
-        s_ticket = ticket;
+        uint32_t tag;
+        s_ticket = draw_ticket(&hdr->state, num_tiles, tag);
+        s_tag = tag;
     }
     __syncthreads();
-    const uint32_t epoch = s_epoch;
-    const uint32_t tag = 2u * epoch + 1u;
+    const uint32_t tag = s_tag;
     const int64_t ticket = s_ticket;
     if (ticket >= num_tiles) {
         // Only possible if the workspace was not zero-filled before first use.

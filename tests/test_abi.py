@@ -49,10 +49,11 @@ def test_status_strings_and_version(lib):
 
 
 def test_workspace_size(lib):
-    assert lib.rlcs_workspace_size(0, 5) == 64
-    assert lib.rlcs_workspace_size(64, 4096) == 64 + 16 * (64 * 4096 // 4096)
-    assert lib.rlcs_workspace_size(1, 4097) == 64 + 16 * 2
-    assert lib.rlcs_workspace_size(-1, 5) == 64
+    fixed = 64 + 1024 * 64  # header, per-block counter slots
+    assert lib.rlcs_workspace_size(0, 5) == fixed
+    assert lib.rlcs_workspace_size(64, 4096) == fixed + 16 * (64 * 4096 // 4096)
+    assert lib.rlcs_workspace_size(1, 4097) == fixed + 16 * 2
+    assert lib.rlcs_workspace_size(-1, 5) == fixed
 
 
 FAKE = ctypes.c_void_p(0x10000)       # never dereferenced: every call below fails validation
@@ -145,3 +146,67 @@ def test_variant_override_range(lib):
     assert lib.rlcs_set_variant_override(3) == n.RLCS_ERR_INVALID_ARG
     assert lib.rlcs_set_variant_override(-1) == n.RLCS_ERR_INVALID_ARG
     assert lib.rlcs_set_variant_override(0) == n.RLCS_OK
+
+
+def test_column_workspace_size(lib):
+    # header and 1024 per-block counter slots, then one 16-byte record per column per
+    # 32-step tile
+    fixed = 64 + 1024 * 64
+    assert lib.rlcs_workspace_size_columns(0, 5) == fixed
+    assert lib.rlcs_workspace_size_columns(4096, 256) == fixed + 16 * 4096 * 8
+    assert lib.rlcs_workspace_size_columns(3, 33) == fixed + 16 * 3 * 2
+    assert lib.rlcs_workspace_size_columns(-1, 5) == 0
+    assert lib.rlcs_workspace_size_columns(2 ** 62, 2 ** 30) == 0  # overflows
+
+
+def gae_tm(lib, **kw):
+    a = dict(r=FAKE, v=FAKE, term=None, trunc=None, bv=None, boot=None, adv=FAKE2, ret=None,
+             N=4, T=8, ld=0, gamma=0.99, lam=0.95, dtype=0, ws=None, ws_bytes=0, stream=None)
+    a.update(kw)
+    return lib.rlcs_gae_tm(*a.values())
+
+
+def test_time_major_validation(lib):
+    from paper_2608_17641_amd import _native as n
+    assert gae_tm(lib, N=-1) == n.RLCS_ERR_INVALID_ARG
+    assert gae_tm(lib, T=-1) == n.RLCS_ERR_INVALID_ARG
+    assert gae_tm(lib, ld=3) == n.RLCS_ERR_INVALID_ARG       # ld < N
+    assert gae_tm(lib, ld=-5) == n.RLCS_ERR_INVALID_ARG
+    assert gae_tm(lib, T=2 ** 30 + 1) == n.RLCS_ERR_INVALID_ARG
+    assert gae_tm(lib, T=2 ** 30, ld=2 ** 40) == n.RLCS_ERR_INVALID_ARG  # T*ld overflows
+    assert gae_tm(lib, dtype=5) == n.RLCS_ERR_DTYPE
+    assert gae_tm(lib, r=None) == n.RLCS_ERR_INVALID_ARG
+    assert gae_tm(lib, trunc=FAKE) == n.RLCS_ERR_INVALID_ARG
+    assert gae_tm(lib, r=MISALIGNED) == n.RLCS_ERR_INVALID_ARG
+    assert gae_tm(lib, gamma=1.5) == n.RLCS_ERR_INVALID_ARG
+    assert gae_tm(lib, N=0) == n.RLCS_OK and gae_tm(lib, T=0) == n.RLCS_OK
+    assert lib.rlcs_vtrace_tm(FAKE, FAKE, FAKE, None, None, None, None, FAKE2, None, 4, 8, 0,
+                              0.99, 0.0, 1.0, 0, None, 0, None) == n.RLCS_ERR_INVALID_ARG
+    assert lib.rlcs_retrace_tm(FAKE, FAKE, None, FAKE, None, None, None, None, FAKE2, None, 4, 8,
+                               0, 0.99, 0.95, 1.0, 0, None, 0, None) == n.RLCS_ERR_INVALID_ARG
+    assert lib.rlcs_td_lambda_tm(FAKE, FAKE, None, None, None, None, FAKE2, 4, 8, 2, 0.99, 0.95,
+                                 0, None, 0, None) == n.RLCS_ERR_INVALID_ARG
+    assert lib.rlcs_discounted_tm(FAKE, None, FAKE, None, None, FAKE2, 4, 8, 0, 0.99, 0, None, 0,
+                                  None) == n.RLCS_ERR_INVALID_ARG
+    assert lib.rlcs_elig_trace_tm(FAKE, None, None, FAKE2, 4, 8, 0, 0.99, math.nan, 0, None, 0,
+                                  None) == n.RLCS_ERR_INVALID_ARG
+    assert lib.rlcs_episodic_prefix_tm(FAKE, None, None, FAKE2, 4, 8, 0, 9, 0, None, 0,
+                                       None) == n.RLCS_ERR_INVALID_ARG
+
+
+def test_elig_trace_vec_validation(lib):
+    from paper_2608_17641_amd import _native as n
+
+    def call(**kw):
+        a = dict(x=FAKE, term=None, trunc=None, z=FAKE2, N=4, T=8, F=3, gamma=0.99, lam=0.95,
+                 dtype=0, ws=None, ws_bytes=0, stream=None)
+        a.update(kw)
+        return lib.rlcs_elig_trace_vec(*a.values())
+    assert call(F=-1) == n.RLCS_ERR_INVALID_ARG
+    assert call(N=-1) == n.RLCS_ERR_INVALID_ARG
+    assert call(N=2 ** 40, T=2 ** 20, F=2 ** 10) == n.RLCS_ERR_INVALID_ARG  # N*T*F overflows
+    assert call(dtype=3) == n.RLCS_ERR_DTYPE
+    assert call(x=None) == n.RLCS_ERR_INVALID_ARG
+    assert call(z=MISALIGNED) == n.RLCS_ERR_INVALID_ARG
+    assert call(lam=-0.5) == n.RLCS_ERR_INVALID_ARG
+    assert call(F=0) == n.RLCS_OK and call(N=0) == n.RLCS_OK

@@ -1,0 +1,276 @@
+"""GPU parity of the column scans through the C ABI: the time-major [T, N] entry points of every
+estimator and the F-vector eligibility traces, against the fp64 oracle on the same seeded
+inputs, with both kernel variants (whole columns per workgroup, columns split over
+workgroups). Bar: max |gpu - oracle| <= tol * (1 + max |oracle|) per output, tol = 1e-5 for
+float32 inputs and 1e-3 for bfloat16 inputs."""
+import contextlib
+
+import numpy as np
+import pytest
+
+from cases import TOL, assert_parity, to_device
+import oracle
+import workloads
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+import paper_2608_17641_amd as rl  # noqa: E402
+
+DEV = torch.device("cuda:0")
+G, L = 0.99, 0.95
+
+
+@contextlib.contextmanager
+def variant(v):
+    rl.rlcs_set_variant_override(v)
+    try:
+        yield
+    finally:
+        rl.rlcs_set_variant_override(0)
+
+
+def strided(t, ld):
+    """`t` [T, N] copied into the first N columns of a [T, ld] buffer (a strided view)."""
+    if ld == t.shape[1]:
+        return t
+    buf = torch.full((t.shape[0], ld), 7, dtype=t.dtype, device=t.device)
+    buf[:, : t.shape[1]] = t
+    return buf[:, : t.shape[1]]
+
+
+TM_ESTIMATORS = ("gae", "vtrace", "retrace", "td_lambda", "discounted", "elig_trace",
+                 "prefix_ends", "prefix_starts")
+
+
+def run_tm(name, d, *, trunc=True, boot=True, ws=None):
+    tr = d["trunc"] if trunc else None
+    bv = d["bv"] if trunc else None
+    bt = d["boot"] if boot else None
+    if name == "gae":
+        a, b = rl.rlcs_gae_tm(d["r"], d["v"], d["term"], tr, bv, bt, gamma=G, lam=L, ws=ws)
+        return {"adv": a, "ret": b}
+    if name == "vtrace":
+        a, b = rl.rlcs_vtrace_tm(d["r"], d["v"], d["log_rho"], d["term"], tr, bv, bt, gamma=G,
+                                 rho_bar=1.0, c_bar=0.9, ws=ws)
+        return {"vs": a, "pg": b}
+    if name == "retrace":
+        a, b = rl.rlcs_retrace_tm(d["r"], d["q"], d["eq"], d["log_rho"], d["term"], tr, bv, bt,
+                                  gamma=G, lam=L, c_bar=1.0, ws=ws)
+        return {"delta": a, "q_ret": b}
+    if name == "td_lambda":
+        return {"ret": rl.rlcs_td_lambda_tm(d["r"], d["v"], d["term"], tr, bv, bt, gamma=G, lam=L,
+                                            ws=ws)}
+    if name == "discounted":
+        return {"ret": rl.rlcs_discounted_tm(d["r"], d["term"], tr, bv, bt, gamma=G, ws=ws)}
+    if name == "elig_trace":
+        return {"z": rl.rlcs_elig_trace_tm(d["x"], d["term"], tr, gamma=G, lam=L, ws=ws)}
+    b = "starts_at" if name == "prefix_starts" else "ends_at"
+    return {"c": rl.rlcs_episodic_prefix_tm(d["x"], d["term"], tr, boundary=b, ws=ws)}
+
+
+def ref_tm(name, ro, *, trunc=True, boot=True):
+    tm = oracle.time_major
+    tr = ro["trunc"] if trunc else None
+    bv = ro["bv"] if trunc else None
+    bt = ro["boot"] if boot else None
+    if name == "gae":
+        a, b = tm(oracle.gae, ro["r"], ro["v"], ro["term"], tr, bv, bt, gamma=G, lam=L)
+        return {"adv": a, "ret": b}
+    if name == "vtrace":
+        a, b = tm(oracle.vtrace, ro["r"], ro["v"], ro["log_rho"], ro["term"], tr, bv, bt,
+                  gamma=G, rho_bar=1.0, c_bar=0.9)
+        return {"vs": a, "pg": b}
+    if name == "retrace":
+        a, b = tm(oracle.retrace, ro["r"], ro["q"], ro["eq"], ro["log_rho"], ro["term"], tr, bv,
+                  bt, gamma=G, lam=L, c_bar=1.0)
+        return {"delta": a, "q_ret": b}
+    if name == "td_lambda":
+        return {"ret": tm(oracle.td_lambda, ro["r"], ro["v"], ro["term"], tr, bv, bt, gamma=G,
+                          lam=L)}
+    if name == "discounted":
+        return {"ret": tm(oracle.discounted, ro["r"], ro["term"], tr, bv, bt, gamma=G)}
+    if name == "elig_trace":
+        return {"z": tm(oracle.elig_trace, ro["x"], ro["term"], tr, gamma=G, lam=L)}
+    b = "starts_at" if name == "prefix_starts" else "ends_at"
+    return {"c": tm(oracle.episodic_prefix, ro["x"], ro["term"], tr, boundary=b)}
+
+
+def device_tm(ro, ld=None):
+    d = {}
+    for k, v in ro.items():
+        t = to_device(v, DEV)
+        d[k] = strided(t, ld) if (ld is not None and t.dim() == 2) else t
+    return d
+
+
+@pytest.mark.parametrize("v", [0, 1, 2])
+@pytest.mark.parametrize("T,N", [(1, 1), (7, 3), (33, 64), (256, 100), (1000, 65), (4097, 5)])
+def test_time_major_every_estimator(T, N, v):
+    ro = workloads.make_rollout_time_major(T, N, seed=T * 7 + N, p_term=0.05, p_trunc=0.05)
+    d = device_tm(ro)
+    ws = rl.make_workspace_columns(N, T, DEV)
+    with variant(v):
+        for name in TM_ESTIMATORS:
+            out = run_tm(name, d, ws=ws)
+            torch.cuda.synchronize()
+            assert_parity(out, ref_tm(name, ro), TOL["f32"], label=f"tm {name} T={T} N={N} v={v}")
+    assert int(ws[8:12].view(torch.int32).item()) == 0
+
+
+@pytest.mark.parametrize("v", [1, 2])
+def test_time_major_bf16_plain_and_strided(v):
+    T, N = 300, 130
+    ro = workloads.make_rollout_time_major(T, N, seed=3, dtype="bf16", p_term=0.03, p_trunc=0.03)
+    ws = rl.make_workspace_columns(N, T, DEV)
+    with variant(v):
+        for ld in (None, 160):
+            d = device_tm(ro, ld)
+            for name in TM_ESTIMATORS:
+                out = run_tm(name, d, ws=ws)
+                torch.cuda.synchronize()
+                assert_parity(out, ref_tm(name, ro), TOL["bf16"], label=f"tm bf16 {name} ld={ld}")
+                if ld is not None:
+                    for o in out.values():
+                        assert o.stride() == (ld, 1)
+            for name in ("gae", "discounted", "elig_trace"):
+                out = run_tm(name, d, trunc=False, boot=False, ws=ws)
+                torch.cuda.synchronize()
+                assert_parity(out, ref_tm(name, ro, trunc=False, boot=False), TOL["bf16"],
+                              label=f"tm bf16 plain {name} ld={ld}")
+
+
+def test_time_major_strided_padding_untouched():
+    """Columns n >= N of a strided [T, ld] output are never written."""
+    T, N, ld = 70, 40, 48
+    ro = workloads.make_rollout_time_major(T, N, seed=9)
+    d = device_tm(ro, ld)
+    adv_buf = torch.full((T, ld), -3.0, device=DEV)
+    ret_buf = torch.full((T, ld), -4.0, device=DEV)
+    rl.rlcs_gae_tm(d["r"], d["v"], d["term"], d["trunc"], d["bv"], d["boot"], adv_buf[:, :N],
+                   ret_buf[:, :N], gamma=G, lam=L)
+    torch.cuda.synchronize()
+    assert torch.all(adv_buf[:, N:] == -3.0) and torch.all(ret_buf[:, N:] == -4.0)
+    assert_parity({"adv": adv_buf[:, :N], "ret": ret_buf[:, :N]}, ref_tm("gae", ro), TOL["f32"],
+                  label="tm strided")
+
+
+@pytest.mark.parametrize("v", [1, 2])
+def test_time_major_headline_shape(v):
+    """GAE on the 4096-environment x 256-step workload stored time-major, whole."""
+    T, N = 256, 4096
+    ro = workloads.make_rollout_time_major(T, N, seed=0, p_term=0.02, p_trunc=0.01)
+    d = device_tm(ro)
+    ws = rl.make_workspace_columns(N, T, DEV)
+    with variant(v):
+        out = run_tm("gae", d, ws=ws)
+        torch.cuda.synchronize()
+    assert_parity(out, ref_tm("gae", ro), TOL["f32"], label=f"tm 256x4096 v={v}")
+
+
+def test_time_major_deterministic_and_workspace_reuse():
+    T, N = 500, 70
+    ro = workloads.make_rollout_time_major(T, N, seed=4)
+    d = device_tm(ro)
+    ws = rl.make_workspace_columns(4 * N, 2 * T, DEV)
+    with variant(2):
+        a1, _ = rl.rlcs_gae_tm(d["r"], d["v"], d["term"], d["trunc"], d["bv"], d["boot"], gamma=G,
+                               lam=L, ws=ws)
+        for T2, N2 in ((37, 3), (999, 200), (64, 64)):
+            ro2 = workloads.make_rollout_time_major(T2, N2, seed=T2)
+            out = run_tm("vtrace", device_tm(ro2), ws=ws)
+            torch.cuda.synchronize()
+            assert_parity(out, ref_tm("vtrace", ro2), TOL["f32"], label=f"reuse {T2}x{N2}")
+        a2, _ = rl.rlcs_gae_tm(d["r"], d["v"], d["term"], d["trunc"], d["bv"], d["boot"], gamma=G,
+                               lam=L, ws=ws)
+        torch.cuda.synchronize()
+    assert torch.equal(a1, a2)
+    assert int(ws[8:12].view(torch.int32).item()) == 0
+
+
+def test_time_major_no_flags_long_lookback():
+    """No flags at all: every split tile composes the maps of all later tiles of its column."""
+    T, N = 3000, 17
+    ro = workloads.make_rollout_time_major(T, N, seed=12, p_term=0.0, p_trunc=0.0)
+    d = device_tm(ro)
+    ws = rl.make_workspace_columns(N, T, DEV)
+    with variant(2):
+        for name in ("discounted", "prefix_ends"):
+            out = run_tm(name, d, trunc=False, ws=ws)
+            torch.cuda.synchronize()
+            assert_parity(out, ref_tm(name, ro, trunc=False), TOL["f32"], label=f"no flags {name}")
+
+
+# ---------------------------------------------------------------- vector eligibility traces
+
+def run_vec(ro, *, trunc=True, ws=None):
+    d = {k: to_device(v, DEV) for k, v in ro.items()}
+    z = rl.rlcs_elig_trace_vec(d["x"], d["term"], d["trunc"] if trunc else None, gamma=G, lam=L,
+                               ws=ws)
+    torch.cuda.synchronize()
+    ref = oracle.elig_trace_vec(ro["x"], ro["term"], ro["trunc"] if trunc else None, gamma=G,
+                                lam=L)
+    return z, ref
+
+
+@pytest.mark.parametrize("v", [0, 1, 2])
+@pytest.mark.parametrize("N,T,F", [(1, 1, 1), (3, 7, 5), (64, 256, 16), (7, 1000, 33),
+                                   (2, 4097, 3), (5, 40, 300), (1, 33, 64)])
+def test_elig_trace_vec_shapes(N, T, F, v):
+    ro = workloads.make_vector_trace(N, T, F, seed=N + T + F, p_term=0.04, p_trunc=0.04)
+    ws = rl.make_workspace_columns(N * F, T, DEV)
+    with variant(v):
+        z, ref = run_vec(ro, ws=ws)
+        assert_parity({"z": z}, {"z": ref}, TOL["f32"], label=f"vec {N}x{T}x{F} v={v}")
+        z, ref = run_vec(ro, trunc=False, ws=ws)
+        assert_parity({"z": z}, {"z": ref}, TOL["f32"], label=f"vec plain {N}x{T}x{F} v={v}")
+
+
+def test_elig_trace_vec_bf16_and_large():
+    ro = workloads.make_vector_trace(200, 129, 24, seed=5, dtype="bf16")
+    z, ref = run_vec(ro)
+    assert_parity({"z": z}, {"z": ref}, TOL["bf16"], label="vec bf16")
+    ro = workloads.make_vector_trace(4096, 64, 16, seed=6)
+    z, ref = run_vec(ro)
+    assert_parity({"z": z}, {"z": ref}, TOL["f32"], label="vec 4096x64x16")
+
+
+def test_elig_trace_vec_one_feature_matches_scalar_entry_point():
+    """F = 1 and the scalar row-major trace compute the same recurrence on the same data."""
+    ro = workloads.make_vector_trace(33, 500, 1, seed=8)
+    d = {k: to_device(v, DEV) for k, v in ro.items()}
+    zv = rl.rlcs_elig_trace_vec(d["x"], d["term"], d["trunc"], gamma=G, lam=L)[:, :, 0]
+    zs = rl.rlcs_elig_trace(d["x"][:, :, 0].contiguous(), d["term"], d["trunc"], gamma=G, lam=L)
+    torch.cuda.synchronize()
+    ref = oracle.elig_trace(ro["x"][:, :, 0], ro["term"], ro["trunc"], gamma=G, lam=L)
+    assert_parity({"z": zv}, {"z": ref}, TOL["f32"], label="vec F=1")
+    assert_parity({"z": zs}, {"z": ref}, TOL["f32"], label="scalar")
+
+
+def test_workspace_shared_by_row_major_and_column_calls():
+    """One workspace serves split row-major calls and split column calls in any order."""
+    from cases import gpu_run, make_inputs, oracle_run, device_inputs
+    n = max(rl.rlcs_workspace_size(64, 8192), rl.rlcs_workspace_size_columns(200, 999),
+            rl.rlcs_workspace_size_columns(16 * 40, 300))
+    ws = torch.zeros(n, dtype=torch.uint8, device=DEV)
+    with variant(2):
+        for rnd in range(2):
+            ro = make_inputs("gae", 64, 8192, seed=rnd)
+            out = gpu_run("gae", device_inputs(ro, DEV), ws=ws)
+            torch.cuda.synchronize()
+            assert_parity(out, oracle_run("gae", ro), TOL["f32"], label=f"row-major {rnd}")
+            ro2 = workloads.make_rollout_time_major(999, 200, seed=rnd)
+            out = run_tm("vtrace", device_tm(ro2), ws=ws)
+            torch.cuda.synchronize()
+            assert_parity(out, ref_tm("vtrace", ro2), TOL["f32"], label=f"time-major {rnd}")
+            ro3 = workloads.make_vector_trace(16, 300, 40, seed=rnd)
+            z, ref = run_vec(ro3, ws=ws)
+            assert_parity({"z": z}, {"z": ref}, TOL["f32"], label=f"vector {rnd}")
+            ro4 = make_inputs("elig_trace", 3, 5000, seed=rnd)
+            out = gpu_run("elig_trace", device_inputs(ro4, DEV), ws=ws)
+            torch.cuda.synchronize()
+            assert_parity(out, oracle_run("elig_trace", ro4), TOL["f32"], label=f"row-major elig {rnd}")
+    assert int(ws[8:12].view(torch.int32).item()) == 0

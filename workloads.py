@@ -28,6 +28,8 @@ __all__ = [
     "make_rlhf_rollout",
     "make_affine",
     "make_retrace_full",
+    "make_rollout_time_major",
+    "make_vector_trace",
     "bf16_bits_from_f32",
     "f32_from_bf16_bits",
     "CONFIGS",
@@ -165,6 +167,31 @@ def make_retrace_full(N: int, T: int, A: int, seed: int = 0, *, dtype: str = "f3
                  actions=np.ascontiguousarray(actions), bv=_finish(bv, dtype),
                  boot=_finish(boot, dtype), term=term, trunc=trunc)
     ro.A = A
+    return ro
+
+
+def make_rollout_time_major(T: int, N: int, seed: int = 0, **kw) -> Rollout:
+    """The rollout of ``make_rollout(N, T, seed, **kw)`` stored time-major: every [N, T] array
+    becomes its [T, N] transpose (step t of environment n at [t, n]); ``boot`` stays [N]."""
+    ro = make_rollout(N, T, seed, **kw)
+    out = Rollout(N, T, ro.dtype)
+    for k, v in ro.items():
+        out[k] = np.ascontiguousarray(v.T) if v.ndim == 2 else v
+    return out
+
+
+def make_vector_trace(N: int, T: int, F: int, seed: int = 0, *, dtype: str = "f32",
+                      p_term: float = 0.02, p_trunc: float = 0.01) -> Rollout:
+    """Inputs of eligibility traces over F-vectors (linear function approximation): feature
+    vectors x [N, T, F] ~ N(0, 1) and Bernoulli flags [N, T]."""
+    if dtype not in ("f32", "bf16"):
+        raise ValueError(f"dtype must be 'f32' or 'bf16', got {dtype!r}")
+    rng = np.random.default_rng(seed)
+    x = rng.standard_normal((N, T, F), dtype=np.float32)
+    term = (rng.random((N, T)) < p_term).astype(np.uint8)
+    trunc = (rng.random((N, T)) < p_trunc).astype(np.uint8)
+    ro = Rollout(N, T, dtype, x=_finish(x, dtype), term=term, trunc=trunc)
+    ro.F = F
     return ro
 
 
