@@ -26,7 +26,8 @@ _LIB = os.path.join(_HERE, "liboracle.so")
 
 __all__ = [
     "build", "gae", "td_lambda", "discounted", "vtrace", "retrace", "retrace_full", "elig_trace",
-    "elig_trace_vec", "episodic_prefix", "affine_scan", "time_major", "widen", "param",
+    "elig_trace_vec", "gae_masked", "normalize_advantages", "episodic_prefix", "affine_scan",
+    "time_major", "widen", "param",
 ]
 
 
@@ -61,6 +62,7 @@ def _load():
                                     D, I64, I64, I64, F64, F64, F64],
             "oracle_elig_trace": [D, U8, U8, D, I64, I64, F64, F64],
             "oracle_elig_trace_vec": [D, U8, U8, D, I64, I64, I64, F64, F64],
+            "oracle_gae_masked": [D, D, U8, U8, U8, D, D, D, D, I64, I64, F64, F64],
             "oracle_episodic_prefix": [D, U8, U8, D, I64, I64, INT],
             "oracle_affine_scan": [D, D, D, D, I64, I64, INT],
         }
@@ -250,6 +252,34 @@ def elig_trace_vec(x, term=None, trunc=None, *, gamma, lam):
     _load().oracle_elig_trace_vec(_ptr(x3, D), _ptr(term, U), _ptr(trunc, U), _ptr(out, D), N, T,
                                   F, param(gamma), param(lam))
     return out
+
+
+def gae_masked(r, v, mask=None, term=None, trunc=None, bv=None, boot=None, *, gamma, lam):
+    """GAE with observation-skip masking (see rlcs_oracle.h). Returns fp64 (adv, ret)."""
+    N, T = _shape(r)
+    r, v, bv, boot = widen(r), widen(v), widen(bv), widen(boot)
+    mask, term, trunc = _flags(mask), _flags(term), _flags(trunc)
+    _check(N, T, v, mask, term, trunc, bv)
+    if trunc is not None and bv is None:
+        raise ValueError("bv is required when trunc is given")
+    adv = np.empty((N, T)); ret = np.empty((N, T))
+    D, U = ctypes.c_double, ctypes.c_uint8
+    _load().oracle_gae_masked(_ptr(r, D), _ptr(v, D), _ptr(mask, U), _ptr(term, U), _ptr(trunc, U),
+                              _ptr(bv, D), _ptr(boot, D), _ptr(adv, D), _ptr(ret, D), N, T,
+                              param(gamma), param(lam))
+    return adv, ret
+
+
+def normalize_advantages(adv, mask=None, *, eps):
+    """Whitening over the steps that take part (mask nonzero; all when mask is None):
+    (adv - mean) / sqrt(var + eps) with the sample mean and the unbiased sample variance of
+    those steps (variance 0 when fewer than two take part), applied to every step. fp64."""
+    a = np.asarray(adv, dtype=np.float64)
+    sel = a.reshape(-1) if mask is None else a[np.asarray(mask) != 0]
+    n = sel.size
+    mean = float(np.sum(sel)) / n if n > 0 else 0.0
+    var = float(np.sum((sel - mean) ** 2)) / (n - 1) if n > 1 else 0.0
+    return (a - mean) / np.sqrt(var + param(eps))
 
 
 def time_major(fn, *args, **kw):

@@ -78,7 +78,53 @@ void oracle_gae(const double* r, const double* v, const uint8_t* term, const uin
     }
 }
 
-/* TD(lambda) returns, Table 1 and Section 3.3.4:
+/* GAE with observation-skip masking (the planned extension of Section 9.3: the recurrence is
+ * carried across masked tokens, beta_t = 1). mask[t] != 0 marks a step that takes part (an
+ * action token); masked steps (observations) are skipped: the advantage passes through them
+ * unchanged, and so does the value a preceding step sees as its successor, which is the value
+ * of the next unmasked step. A flag cuts where it occurs, masked step or not: a terminated
+ * masked step passes on advantage 0 and successor value 0, a truncated one advantage 0 and its
+ * continuation bv_t. Walking backward with the running advantage A and the running successor
+ * value W (A = 0 and W = boot past the window):
+ *   unmasked: A_t = r_t + gamma * s - V_t + gamma * lambda * (cont ? A : 0),  W <- V_t
+ *   masked:   A_t = cont ? A : 0,                                             W <- s
+ * where s = 0 after a termination, bv_t after a truncation, else W, and cont = no flag at t.
+ * Outputs: adv_t = A_t and ret_t = A_t + V_t at every step. mask NULL = every step takes part. */
+void oracle_gae_masked(const double* r, const double* v, const uint8_t* mask,
+                       const uint8_t* term, const uint8_t* trunc, const double* bv,
+                       const double* boot, double* adv, double* ret, int64_t N, int64_t T,
+                       double gamma, double lambda) {
+    for (int64_t n = 0; n < N; ++n) {
+        const double* rr = r + n * T;
+        const double* vv = v + n * T;
+        const uint8_t* mk = row_of_flags(mask, n, T);
+        const uint8_t* te = row_of_flags(term, n, T);
+        const uint8_t* tr = row_of_flags(trunc, n, T);
+        const double* bb = row_of(bv, n, T);
+        double A = 0.0;
+        double W = boot ? boot[n] : 0.0;
+        for (int64_t t = T - 1; t >= 0; --t) {
+            const int is_term = flag_at(te, t);
+            const int is_trunc = !is_term && flag_at(tr, t);
+            const int cont = !is_term && !is_trunc;
+            const double s = is_term ? 0.0 : (is_trunc ? bb[t] : W);
+            const int in = mk == NULL || mk[t] != 0;
+            double At;
+            if (in) {
+                At = rr[t] + gamma * s - vv[t] + gamma * lambda * (cont ? A : 0.0);
+                W = vv[t];
+            } else {
+                At = cont ? A : 0.0;
+                W = s;
+            }
+            adv[n * T + t] = At;
+            ret[n * T + t] = At + vv[t];
+            A = At;
+        }
+    }
+}
+
+/* Vector eligibility traces, Table 1 and Section 3.3.4:
  *   G_t = r_t + gamma * [(1 - lambda) V(s_{t+1}) + lambda G_{t+1}] inside an episode,
  *   with the successor value given by Section 3.2; a truncated step takes the continuation
  *   with the full gamma; a terminated step has no successor; the window carry is G_T = B, so

@@ -61,6 +61,14 @@ void oracle_retrace_full(const double* r, const double* q, const double* pi,
 void oracle_elig_trace(const double* x, const uint8_t* term, const uint8_t* trunc, double* z,
                        int64_t N, int64_t T, double gamma, double lambda);
 
+/* GAE with observation-skip masking: mask uint8 [N, T], nonzero = the step takes part, NULL =
+ * every step does. Masked steps carry the advantage and the successor value through; flags cut
+ * where they occur. adv, ret as oracle_gae (ret = adv + v at every step). */
+void oracle_gae_masked(const double* r, const double* v, const uint8_t* mask,
+                       const uint8_t* term, const uint8_t* trunc, const double* bv,
+                       const double* boot, double* adv, double* ret, int64_t N, int64_t T,
+                       double gamma, double lambda);
+
 /* Eligibility traces of F-vectors: x and z are double [N, T, F] (features innermost), the
  * flags [N, T]; the scalar coefficient gamma * lambda * (1 - d_{t-1}) of a step applies to
  * every feature. */

@@ -654,3 +654,114 @@ def test_time_major_oracle_brute_force():
                               boundary="starts_at" if starts else "ends_at")
         rtol_close(c, np.array([brute.prefix_sum(col(r, n), col(term, n), col(trunc, n), starts)
                                 for n in range(N)]).T)
+
+
+# ---------------------------------------------------------------- observation-skip masking (Section 9.3)
+
+def _compacted_masked_gae(r, v, mask, term, trunc, bv, B):
+    """Masked GAE of one row from its definition by compaction: the unmasked steps form the
+    sequence, a flag anywhere between an unmasked step and the next one (the first one found
+    from the step itself) is that step's flag, with the continuation of the truncated step;
+    the GAE sum form runs on that sequence; a masked step takes the advantage of the first
+    step at or after it that is unmasked, or 0 if a flagged step or the window end comes
+    first."""
+    T = len(r)
+    U = [t for t in range(T) if mask[t]]
+    tc, rc, bc = [], [], []
+    for i, u in enumerate(U):
+        end = U[i + 1] if i + 1 < len(U) else T
+        te = tr = 0
+        b = 0.0
+        for s in range(u, end):
+            if term[s] or trunc[s]:
+                te = 1 if term[s] else 0
+                tr = 0 if term[s] else 1
+                b = bv[s]
+                break
+        tc.append(te); rc.append(tr); bc.append(b)
+    Ac = brute.gae_sum([r[u] for u in U], [v[u] for u in U], tc, rc, bc, B, g32, l32) if U else []
+    pos = {u: i for i, u in enumerate(U)}
+    A = []
+    for t in range(T):
+        if mask[t]:
+            A.append(Ac[pos[t]])
+            continue
+        val = 0.0
+        for s in range(t, T):
+            if mask[s]:
+                val = Ac[pos[s]]
+                break
+            if term[s] or trunc[s]:
+                break
+        A.append(val)
+    return A
+
+
+@pytest.mark.parametrize("p_mask", [0.2, 0.6, 0.9])
+def test_gae_masked_against_compaction(p_mask):
+    N, T = 150, 17
+    rng = np.random.default_rng(int(100 * p_mask))
+    x = random_inputs(N, T, seed=int(1000 * p_mask))
+    term = (rng.random((N, T)) < 0.12).astype(np.uint8)
+    trunc = (rng.random((N, T)) < 0.12).astype(np.uint8)
+    mask = (rng.random((N, T)) >= p_mask).astype(np.uint8)
+    mask[0] = 0  # a row with no unmasked step
+    mask[1] = 1  # a row with every step unmasked
+    adv, ret = oracle.gae_masked(x["r"], x["v"], mask, term, trunc, x["bv"], x["boot"], gamma=G,
+                                 lam=L)
+    ref = [_compacted_masked_gae(x["r"][n], x["v"][n], mask[n], term[n], trunc[n], x["bv"][n],
+                                 x["boot"][n]) for n in range(N)]
+    rtol_close(adv, ref)
+    rtol_close(ret, np.asarray(ref) + x["v"])
+    assert np.all(adv[0] == 0.0)
+
+
+def test_gae_masked_exhaustive_small():
+    """Every mask pattern of a 5-step row under every flag pattern of its steps."""
+    T = 5
+    term, trunc = all_flag_patterns(T)
+    rng = np.random.default_rng(31)
+    for mbits in range(2 ** T):
+        mrow = np.array([(mbits >> k) & 1 for k in range(T)], np.uint8)
+        N = term.shape[0]
+        mask = np.tile(mrow, (N, 1))
+        r, v, bv = (rng.standard_normal((N, T)) for _ in range(3))
+        boot = rng.standard_normal(N)
+        adv, _ = oracle.gae_masked(r, v, mask, term, trunc, bv, boot, gamma=G, lam=L)
+        rtol_close(adv, [_compacted_masked_gae(r[n], v[n], mrow, term[n], trunc[n], bv[n], boot[n])
+                         for n in range(N)])
+
+
+def test_gae_masked_all_unmasked_is_gae():
+    N, T = 40, 60
+    x = random_inputs(N, T, 33)
+    term, trunc = _flags(N, T, 33)
+    ones = np.ones((N, T), np.uint8)
+    a1, r1 = oracle.gae_masked(x["r"], x["v"], ones, term, trunc, x["bv"], x["boot"], gamma=G, lam=L)
+    a0, r0 = oracle.gae_masked(x["r"], x["v"], None, term, trunc, x["bv"], x["boot"], gamma=G, lam=L)
+    a2, r2 = oracle.gae(x["r"], x["v"], term, trunc, x["bv"], x["boot"], gamma=G, lam=L)
+    assert np.array_equal(a1, a0) and np.array_equal(r1, r0)
+    rtol_close(a1, a2)
+    rtol_close(r1, r2)
+
+
+def test_normalize_advantages_exact_moments():
+    """Mean and unbiased variance of the steps that take part, from exactly rounded sums."""
+    import math
+    rng = np.random.default_rng(41)
+    adv = 3.0 + 2.0 * rng.standard_normal((30, 50))
+    mask = (rng.random((30, 50)) < 0.7).astype(np.uint8)
+    eps = 1e-8
+    out = oracle.normalize_advantages(adv, mask, eps=eps)
+    sel = [float(a) for a, m in zip(adv.reshape(-1), mask.reshape(-1)) if m]
+    n = len(sel)
+    mean = math.fsum(sel) / n
+    var = math.fsum((a - mean) ** 2 for a in sel) / (n - 1)
+    rtol_close(out, (adv - mean) / math.sqrt(var + oracle.param(eps)))
+    z = out[mask != 0]
+    assert abs(math.fsum(z.tolist())) < 1e-9
+    rtol_close(math.fsum(((z - z.mean()) ** 2).tolist()) / (n - 1), var / (var + oracle.param(eps)))
+    # one step taking part: variance 0
+    one = np.zeros_like(mask); one[3, 4] = 1
+    out1 = oracle.normalize_advantages(adv, one, eps=eps)
+    rtol_close(out1, (adv - adv[3, 4]) / math.sqrt(oracle.param(eps)))
