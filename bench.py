@@ -341,6 +341,10 @@ def run_extra(dev, only=""):
                               ("vec_1x128x1M", 1, 128, 1 << 20)):
         if label.startswith(only):
             run_vector_trace(label, n_, t_, f_, dev)
+    for label, n_, t_ in (("mt_64x4096", 64, 4096), ("mt_4096x256", 4096, 256),
+                          ("mt_1024x2048", 1024, 2048)):
+        if label.startswith(only):
+            run_masked(label, n_, t_, dev)
 
 
 def run_retrace_full(label, n_, t_, a_, dev):
@@ -502,6 +506,41 @@ def run_vector_trace(label, n_, t_, f_, dev):
         raise SystemExit(f"parity failure in {label}: {rel}")
     nbytes = n_ * t_ * (8 * f_ + 2)
     _report(label, "elig_trace_vec", _graph_time(call, sets, nbytes), nbytes, n_ * t_ * f_, S, rel)
+
+
+def run_masked(label, n_, t_, dev):
+    """Masked GAE on multi-turn rows (fp32, gamma 1), plain and whitened: parity on sampled
+    rows (whitened: the statistics are recomputed by the oracle over the whole batch), then
+    graph-timed. Dense bytes: r, v (4 B each), mask and term (1 B each), adv and ret (4 B
+    each) per step; whitening is counted as fused (no extra bytes)."""
+    import torch
+    import oracle
+    import workloads
+    import paper_2608_17641_amd as rl
+    ro = workloads.make_multiturn(n_, t_, 0)
+    base = {k: torch.from_numpy(np.ascontiguousarray(v)).to(dev) for k, v in ro.items()}
+    set_bytes = sum(v.numel() * v.element_size() for v in base.values()) + 8 * n_ * t_
+    S = max(1, min(32, -(-600_000_000 // set_bytes)))
+    sets = _rotated_sets(base, S, {"o0": base["r"], "o1": base["r"]})
+    ws = torch.empty(rl.rlcs_workspace_size_masked(n_, t_), dtype=torch.uint8, device=dev)
+    adv_ref, _ = oracle.gae_masked(ro["r"], ro["v"], ro["mask"], ro["term"], None, None, ro["boot"],
+                                   gamma=1.0, lam=0.95)
+    nbytes = n_ * t_ * 18
+    rows = np.unique(np.concatenate([[0, n_ - 1], np.random.default_rng(1).integers(0, n_, 32)]))
+    for norm in (False, True):
+        call = lambda d: rl.rlcs_gae_masked(d["r"], d["v"], d["mask"], d["term"], None, None,
+                                            d["boot"], d["o0"], d["o1"], gamma=1.0, lam=0.95,
+                                            normalize=norm, ws=ws)
+        call(sets[0])
+        torch.cuda.synchronize()
+        ref = oracle.normalize_advantages(adv_ref, ro["mask"], eps=1e-8) if norm else adv_ref
+        got = sets[0]["o0"].index_select(0, torch.from_numpy(rows).to(dev)).double().cpu().numpy()
+        r_ = ref[rows]
+        rel = float(np.max(np.abs(got - r_))) / (1 + float(np.max(np.abs(r_))))
+        if rel > 1e-5:
+            raise SystemExit(f"parity failure in {label} norm={norm}: {rel}")
+        _report(label, "gae_masked" + ("_norm" if norm else ""), _graph_time(call, sets, nbytes),
+                nbytes, n_ * t_, S, rel)
 
 
 def main():

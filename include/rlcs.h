@@ -190,6 +190,37 @@ rlcs_status rlcs_affine_scan(const void* alpha, const void* beta, const void* ca
  * row-major and time-major alike, as long as they are ordered on one stream. */
 size_t rlcs_workspace_size(int64_t N, int64_t T);
 
+/* GAE with observation-skip masking, for multi-turn and tool-use trajectories (the extension
+ * planned in Section 9.3: the recurrence is carried across masked tokens, beta_t = 1), with
+ * optional whitening of the advantages.
+ *   mask     [N, T] uint8: nonzero = the step takes part (an action token); zero = it is
+ *            skipped (an observation token). NULL = every step takes part (plain GAE).
+ * A skipped step passes on the advantage of the step after it and the value the step before
+ * it sees as its successor: an unmasked step t has
+ *   A_t = r_t + gamma W_t - V_t + gamma lambda A_{t+1} (the continuation term only without
+ *   a flag at t),
+ * with W_t the value of the next unmasked step, or 0 / bv / boot[n] if a termination /
+ * truncation / the window edge comes first; a skipped step has A_t = A_{t+1}, or 0 if it
+ * carries a flag. Flags cut where they occur, on skipped steps too (a truncated skipped step
+ * hands its bv to the step before it).
+ *   adv      [N, T] float32 out: A_t at every step (skipped steps carry the advantage)
+ *   ret      [N, T] float32 out, optional: A_t + V_t (from the advantage before whitening)
+ *   normalize  0: adv as above; 1: adv is whitened, (A_t - mean) / sqrt(var + eps), mean and
+ *            unbiased variance over the steps that take part (var 0 with fewer than two),
+ *            applied to every step. eps >= 0, finite.
+ *   ws       required when normalize = 1: rlcs_workspace_size_masked(N, T) bytes, 64-byte
+ *            aligned (no zero-fill needed); unused otherwise.
+ * Rows are never split across workgroups for this entry point.                             */
+rlcs_status rlcs_gae_masked(const void* r, const void* v, const uint8_t* mask,
+                            const uint8_t* term, const uint8_t* trunc, const void* bv,
+                            const void* boot, float* adv, float* ret, int64_t N, int64_t T,
+                            float gamma, float lambda, int normalize, float eps,
+                            rlcs_dtype dtype, void* ws, size_t ws_bytes, rlcs_stream_t stream);
+
+/* Workspace bytes that rlcs_gae_masked needs for whitening an [N, T] call (0 for negative
+ * sizes). */
+size_t rlcs_workspace_size_masked(int64_t N, int64_t T);
+
 /* ---------------------------------------------------------------------------------------
  * Time-major layouts. The entry points below compute exactly what their row-major namesakes
  * compute, for buffers stored time-major: every [N, T] array of the row-major form becomes a

@@ -25,7 +25,8 @@ __all__ = [
     "rlcs_version", "rlcs_set_variant_override", "make_workspace", "RlcsError",
     "rlcs_gae_tm", "rlcs_vtrace_tm", "rlcs_retrace_tm", "rlcs_td_lambda_tm", "rlcs_discounted_tm",
     "rlcs_elig_trace_tm", "rlcs_episodic_prefix_tm", "rlcs_elig_trace_vec",
-    "rlcs_workspace_size_columns", "make_workspace_columns",
+    "rlcs_workspace_size_columns", "make_workspace_columns", "rlcs_gae_masked",
+    "rlcs_workspace_size_masked",
 ]
 
 _DTYPES = {torch.float32: _native.RLCS_F32, torch.bfloat16: _native.RLCS_BF16}
@@ -457,3 +458,32 @@ def rlcs_elig_trace_vec(x, term=None, trunc=None, z=None, *, gamma: float, lam: 
         _call("rlcs_elig_trace_vec", _ptr(x), _ptr(term), _ptr(trunc), _ptr(z), N, T, F, gamma,
               lam, _DTYPES[x.dtype], wp, wb, _stream(dev))
     return z
+
+
+# ---------------------------------------------------------------- masked GAE
+
+def rlcs_workspace_size_masked(N: int, T: int) -> int:
+    return int(_native.load().rlcs_workspace_size_masked(int(N), int(T)))
+
+
+def rlcs_gae_masked(r, v, mask=None, term=None, trunc=None, bv=None, boot=None, adv=None,
+                    ret=None, *, gamma: float, lam: float, normalize: bool = False,
+                    eps: float = 1e-8, ws=None, want_ret: bool = True):
+    """GAE with observation-skip masking (mask nonzero = the step takes part), optionally with
+    the advantages whitened over the steps that take part. A workspace for whitening is
+    allocated when none is given."""
+    N, T, dt, dev = _prep(r)
+    _check_data("v", v, N, T, dt, dev); _check_data("bv", bv, N, T, dt, dev)
+    _check_data("boot", boot, N, T, dt, dev, shape=(N,))
+    _check_flags("mask", mask, N, T, dev)
+    _check_flags("term", term, N, T, dev); _check_flags("trunc", trunc, N, T, dev)
+    adv = _out("adv", adv, N, T, dev)
+    ret = _out("ret", ret, N, T, dev) if (want_ret or ret is not None) else None
+    if normalize and ws is None:
+        ws = torch.empty(max(rlcs_workspace_size_masked(N, T), 64), dtype=torch.uint8, device=dev)
+    wp, wb = _ws(ws, dev)
+    with torch.cuda.device(dev):
+        _call("rlcs_gae_masked", _ptr(r), _ptr(v), _ptr(mask), _ptr(term), _ptr(trunc), _ptr(bv),
+              _ptr(boot), _ptr(adv), _ptr(ret), N, T, gamma, lam, 1 if normalize else 0, eps,
+              _DTYPES[dt], wp, wb, _stream(dev))
+    return adv, ret

@@ -55,11 +55,15 @@ PROTOTYPES = {
     "rlcs_episodic_prefix_tm": [_P, _P, _P, _P, _I64, _I64, _I64, _INT, _INT, _P, _SZ, _P],
     "rlcs_elig_trace_vec": [_P, _P, _P, _P, _I64, _I64, _I64, _F, _F, _INT, _P, _SZ, _P],
     "rlcs_workspace_size_columns": [_I64, _I64],
+    "rlcs_gae_masked": [_P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _F, _F, _INT, _F, _INT, _P,
+                        _SZ, _P],
+    "rlcs_workspace_size_masked": [_I64, _I64],
     "rlcs_status_string": [_INT],
     "rlcs_version": [],
     "rlcs_set_variant_override": [_INT],
 }
 RESTYPES = {"rlcs_workspace_size": _SZ, "rlcs_workspace_size_columns": _SZ,
+            "rlcs_workspace_size_masked": _SZ,
             "rlcs_status_string": ctypes.c_char_p}
 
 _lib = None

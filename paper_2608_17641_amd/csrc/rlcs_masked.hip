@@ -1,0 +1,107 @@
+// GAE with observation-skip masking and optional advantage whitening (Section 9.3; Table 1 and
+// Section 3.3.1 for the unmasked steps).
+#include "rlcs_dispatch.h"
+#include "rlcs_masked.h"
+
+using namespace rlcs;
+using namespace rlcs::host;
+
+namespace {
+
+// Bytes of the whitening workspace of an [N, T] call: 64 for the statistics, then one 32-byte
+// partial per workgroup (at most one workgroup per row).
+size_t masked_ws_need(int64_t N) { return 64 + 32 * size_t(N > 0 ? N : 1); }
+
+template <typename DT, bool VEC, bool TR, bool HM, bool STATS>
+void launch_masked(const MaskedArgs& ma, int waves, int64_t groups, int64_t rows_per_wg,
+                   int wave_local, hipStream_t s) {
+    constexpr int K = Width<DT>::K;
+    if (waves == kSmallWaves)
+        hipLaunchKernelGGL((masked_gae_kernel<DT, K, kSmallWaves, VEC, TR, HM, STATS>),
+                           dim3(unsigned(groups)), dim3(kSmallWaves * kWave), 0, s, ma,
+                           rows_per_wg, wave_local);
+    else
+        hipLaunchKernelGGL((masked_gae_kernel<DT, K, kLargeWaves, VEC, TR, HM, STATS>),
+                           dim3(unsigned(groups)), dim3(kLargeWaves * kWave), 0, s, ma,
+                           rows_per_wg, wave_local);
+}
+
+template <typename DT>
+rlcs_status run_masked(MaskedArgs& ma, bool normalize, float eps, void* ws, hipStream_t s) {
+    constexpr int K = Width<DT>::K;
+    const Args& a = ma.a;
+    const int64_t N = a.N, T = a.T;
+    constexpr int64_t E_small = int64_t(kSmallWaves) * kWave * K;
+    const int waves = (T <= E_small) ? kSmallWaves : kLargeWaves;
+    const int64_t E = int64_t(waves) * kWave * K;
+    const int64_t slack = (T % K == 0) ? 0 : K - 1;
+    const int64_t rows_per_wg = (T <= E - slack) ? (E - slack) / T : 1;
+    const int64_t groups = (N + rows_per_wg - 1) / rows_per_wg;
+    if (groups > INT32_MAX) return RLCS_ERR_INVALID_ARG;
+    const int wave_local = (T % K == 0 && (int64_t(kWave) * K) % T == 0) ? 1 : 0;
+    bool vec = aligned(a.in[0], 16) && aligned(a.in[1], 16) && (!a.trunc || aligned(a.in[2], 16)) &&
+               aligned(a.out0, 16) && (!a.out1 || aligned(a.out1, 16)) &&
+               (!a.term || aligned(a.term, K)) && (!a.trunc || aligned(a.trunc, K)) &&
+               (!ma.mask || aligned(ma.mask, K));
+    const bool tr = a.trunc != nullptr, hm = ma.mask != nullptr;
+    double* stats = reinterpret_cast<double*>(ws);
+    ma.partials = normalize ? reinterpret_cast<double*>(reinterpret_cast<char*>(ws) + 64) : nullptr;
+#define RLCS_MASKED(V, TRV, HMV, ST) launch_masked<DT, V, TRV, HMV, ST>(ma, waves, groups, rows_per_wg, wave_local, s)
+#define RLCS_MASKED_ST(V, TRV, HMV) \
+    if (normalize) RLCS_MASKED(V, TRV, HMV, true); else RLCS_MASKED(V, TRV, HMV, false)
+#define RLCS_MASKED_HM(V, TRV) \
+    if (hm) { RLCS_MASKED_ST(V, TRV, true); } else { RLCS_MASKED_ST(V, TRV, false); }
+#define RLCS_MASKED_TR(V) \
+    if (tr) { RLCS_MASKED_HM(V, true); } else { RLCS_MASKED_HM(V, false); }
+    if (vec) { RLCS_MASKED_TR(true); } else { RLCS_MASKED_TR(false); }
+#undef RLCS_MASKED_TR
+#undef RLCS_MASKED_HM
+#undef RLCS_MASKED_ST
+#undef RLCS_MASKED
+    if (normalize) {
+        hipLaunchKernelGGL(masked_stats_kernel, dim3(1), dim3(kReduceThreads), 0, s, ma.partials,
+                           groups, eps, stats);
+        const int64_t total = N * T;
+        const int64_t want = (total + 4 * 256 * 8 - 1) / (4 * 256 * 8);
+        const unsigned grid = unsigned(want < 4096 ? (want > 0 ? want : 1) : 4096);
+        hipLaunchKernelGGL(masked_normalize_kernel, dim3(grid), dim3(256), 0, s, a.out0, total,
+                           stats, aligned(a.out0, 16) ? 1 : 0);
+    }
+    return hipGetLastError() == hipSuccess ? RLCS_OK : RLCS_ERR_LAUNCH;
+}
+
+}  // namespace
+
+extern "C" {
+
+rlcs_status rlcs_gae_masked(const void* r, const void* v, const uint8_t* mask,
+                            const uint8_t* term, const uint8_t* trunc, const void* bv,
+                            const void* boot, float* adv, float* ret, int64_t N, int64_t T,
+                            float gamma, float lambda, int normalize, float eps,
+                            rlcs_dtype dtype, void* ws, size_t ws_bytes, rlcs_stream_t stream) {
+    rlcs_status st = check_common(N, T, dtype, {r, v, bv, boot}, {adv, ret});
+    if (st != RLCS_OK) return st;
+    if (!unit_interval(gamma) || !unit_interval(lambda)) return RLCS_ERR_INVALID_ARG;
+    if (normalize != 0 && normalize != 1) return RLCS_ERR_INVALID_ARG;
+    if (normalize && !(eps >= 0.f && eps < INFINITY)) return RLCS_ERR_INVALID_ARG;
+    if (N == 0 || T == 0) return RLCS_OK;
+    if (!r || !v || !adv || (trunc && !bv)) return RLCS_ERR_INVALID_ARG;
+    if (normalize && (!ws || ws_bytes < masked_ws_need(N) || !aligned(ws, 64)))
+        return RLCS_ERR_WORKSPACE;
+    MaskedArgs ma{};
+    ma.a = make_args(N, T, gamma, lambda, 1.f, 1.f);
+    ma.a.in[0] = r; ma.a.in[1] = v; ma.a.in[2] = bv;
+    ma.a.term = term; ma.a.trunc = trunc; ma.a.row_value = boot;
+    ma.a.out0 = adv; ma.a.out1 = ret;
+    ma.mask = mask;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    if (dtype == RLCS_BF16) return run_masked<bf16_t>(ma, normalize != 0, eps, ws, s);
+    return run_masked<float>(ma, normalize != 0, eps, ws, s);
+}
+
+size_t rlcs_workspace_size_masked(int64_t N, int64_t T) {
+    if (N < 0 || T < 0) return 0;
+    return masked_ws_need(N);
+}
+
+}  // extern "C"

@@ -1,0 +1,96 @@
+"""GPU parity of GAE with observation-skip masking and advantage whitening (rlcs_gae_masked)
+through the C ABI, against the fp64 oracle on the same seeded inputs. Bar: max |gpu - oracle|
+<= tol * (1 + max |oracle|) per output, tol = 1e-5 for float32 inputs and 1e-3 for bfloat16
+inputs (whitened outputs included: the oracle whitens its own fp64 advantages)."""
+import numpy as np
+import pytest
+
+from cases import TOL, assert_parity, to_device
+import oracle
+import workloads
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+import paper_2608_17641_amd as rl  # noqa: E402
+
+DEV = torch.device("cuda:0")
+G, L = 0.99, 0.95
+
+
+def run(ro, mask, *, trunc=True, boot=True, normalize=False, eps=1e-8, gamma=G, lam=L):
+    d = {k: to_device(v, DEV) for k, v in ro.items()}
+    m = None if mask is None else to_device(mask, DEV)
+    tr = d["trunc"] if trunc else None
+    bv = d["bv"] if trunc else None
+    bt = d["boot"] if boot else None
+    adv, ret = rl.rlcs_gae_masked(d["r"], d["v"], m, d["term"], tr, bv, bt, gamma=gamma, lam=lam,
+                                  normalize=normalize, eps=eps)
+    torch.cuda.synchronize()
+    a, r = oracle.gae_masked(ro["r"], ro["v"], mask, ro["term"], ro["trunc"] if trunc else None,
+                             ro["bv"] if trunc else None, ro["boot"] if boot else None, gamma=gamma,
+                             lam=lam)
+    if normalize:
+        a = oracle.normalize_advantages(a, mask, eps=eps)
+    return {"adv": adv, "ret": ret}, {"adv": a, "ret": r}
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("N,T", [(1, 1), (5, 7), (64, 256), (33, 1000), (8, 4097), (3, 9000),
+                                 (300, 33)])
+def test_gae_masked_random_masks(N, T, dtype):
+    ro = workloads.make_rollout(N, T, seed=N * 31 + T, dtype=dtype, p_term=0.03, p_trunc=0.03)
+    mask = (np.random.default_rng(T).random((N, T)) < 0.6).astype(np.uint8)
+    for norm in (False, True):
+        out, ref = run(ro, mask, normalize=norm)
+        assert_parity(out, ref, TOL[dtype], label=f"masked {N}x{T} {dtype} norm={norm}")
+    out, ref = run(ro, None)
+    assert_parity(out, ref, TOL[dtype], label=f"unmasked {N}x{T} {dtype}")
+    out, ref = run(ro, mask, trunc=False, boot=False)
+    assert_parity(out, ref, TOL[dtype], label=f"masked plain {N}x{T} {dtype}")
+
+
+def test_gae_masked_equals_gae_without_mask():
+    ro = workloads.make_rollout(200, 300, seed=5, p_term=0.02, p_trunc=0.01)
+    d = {k: to_device(v, DEV) for k, v in ro.items()}
+    a1, r1 = rl.rlcs_gae_masked(d["r"], d["v"], None, d["term"], d["trunc"], d["bv"], d["boot"],
+                                gamma=G, lam=L)
+    a2, r2 = rl.rlcs_gae(d["r"], d["v"], d["term"], d["trunc"], d["bv"], d["boot"], gamma=G, lam=L)
+    torch.cuda.synchronize()
+    ref, _ = oracle.gae(ro["r"], ro["v"], ro["term"], ro["trunc"], ro["bv"], ro["boot"], gamma=G,
+                        lam=L)
+    assert_parity({"a": a1}, {"a": ref}, TOL["f32"], label="masked entry, no mask")
+    assert_parity({"a": a2}, {"a": ref}, TOL["f32"], label="gae entry")
+
+
+@pytest.mark.parametrize("N,T", [(64, 4096), (16, 8192), (512, 512)])
+def test_gae_masked_multiturn(N, T):
+    ro = workloads.make_multiturn(N, T, seed=N + T)
+    for norm in (False, True):
+        out, ref = run(ro, ro["mask"], normalize=norm, gamma=1.0, lam=0.95)
+        assert_parity(out, ref, TOL["f32"], label=f"multiturn {N}x{T} norm={norm}")
+
+
+def test_gae_masked_edge_cases():
+    ro = workloads.make_rollout(40, 50, seed=9, p_term=0.05, p_trunc=0.05)
+    zeros = np.zeros((40, 50), np.uint8)
+    out, ref = run(ro, zeros)                       # every step skipped
+    assert_parity(out, ref, TOL["f32"], label="all masked")
+    assert float(out["adv"].abs().max()) == 0.0
+    out, ref = run(ro, zeros, normalize=True)       # nothing takes part: mean 0, var 0
+    assert_parity(out, ref, 1e-5, label="all masked, whitened")
+    one = zeros.copy(); one[7, 13] = 1              # one step takes part: var 0
+    out, ref = run(ro, one, normalize=True, eps=1e-2)
+    assert_parity(out, ref, 1e-5, label="one unmasked, whitened")
+
+
+def test_gae_masked_deterministic():
+    ro = workloads.make_multiturn(64, 4096, seed=2)
+    d = {k: to_device(v, DEV) for k, v in ro.items()}
+    outs = [rl.rlcs_gae_masked(d["r"], d["v"], d["mask"], d["term"], None, None, d["boot"],
+                               gamma=1.0, lam=0.95, normalize=True)[0] for _ in range(3)]
+    torch.cuda.synchronize()
+    assert torch.equal(outs[0], outs[1]) and torch.equal(outs[1], outs[2])

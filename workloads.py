@@ -29,6 +29,7 @@ __all__ = [
     "make_affine",
     "make_retrace_full",
     "make_rollout_time_major",
+    "make_multiturn",
     "make_vector_trace",
     "bf16_bits_from_f32",
     "f32_from_bf16_bits",
@@ -178,6 +179,41 @@ def make_rollout_time_major(T: int, N: int, seed: int = 0, **kw) -> Rollout:
     for k, v in ro.items():
         out[k] = np.ascontiguousarray(v.T) if v.ndim == 2 else v
     return out
+
+
+def make_multiturn(N: int, T: int, seed: int = 0, *, dtype: str = "f32", mean_action: float = 48.0,
+                   mean_obs: float = 96.0, kl_sigma: float = 0.01) -> Rollout:
+    """Multi-turn / tool-use rows for masked GAE: each row alternates runs of observation
+    tokens (mask 0; the row starts with one, the prompt) and action tokens (mask 1) with
+    geometric run lengths of the given means; a per-token KL penalty ~ N(0, kl_sigma) on action
+    tokens plus a score ~ N(0, 1) on the row's last action token; values ~ N(0, 1); the row
+    terminates at its last step; no truncation; zero bootstrap."""
+    if dtype not in ("f32", "bf16"):
+        raise ValueError(f"dtype must be 'f32' or 'bf16', got {dtype!r}")
+    rng = np.random.default_rng(seed)
+    mask = np.zeros((N, T), dtype=np.uint8)
+    for n in range(N):
+        t, act = 0, False
+        while t < T:
+            run = int(rng.geometric(1.0 / (mean_action if act else mean_obs)))
+            mask[n, t:t + run] = 1 if act else 0
+            t += run
+            act = not act
+    kl = (kl_sigma * rng.standard_normal((N, T))).astype(np.float32) * mask
+    score = rng.standard_normal((N,), dtype=np.float32)
+    rewards = kl.copy()
+    for n in range(N):
+        idx = np.nonzero(mask[n])[0]
+        if idx.size:
+            rewards[n, idx[-1]] += score[n]
+    values = rng.standard_normal((N, T), dtype=np.float32)
+    term = np.zeros((N, T), dtype=np.uint8)
+    if T > 0:
+        term[:, T - 1] = 1
+    zeros = np.zeros((N, T), dtype=np.float32)
+    return Rollout(N, T, dtype, r=_finish(rewards, dtype), v=_finish(values, dtype),
+                   bv=_finish(zeros, dtype), boot=_finish(np.zeros((N,), np.float32), dtype),
+                   term=term, trunc=np.zeros((N, T), dtype=np.uint8), mask=mask)
 
 
 def make_vector_trace(N: int, T: int, F: int, seed: int = 0, *, dtype: str = "f32",
