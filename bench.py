@@ -522,7 +522,7 @@ def run_masked(label, n_, t_, dev):
     set_bytes = sum(v.numel() * v.element_size() for v in base.values()) + 8 * n_ * t_
     S = max(1, min(32, -(-600_000_000 // set_bytes)))
     sets = _rotated_sets(base, S, {"o0": base["r"], "o1": base["r"]})
-    ws = torch.empty(rl.rlcs_workspace_size_masked(n_, t_), dtype=torch.uint8, device=dev)
+    ws = torch.zeros(rl.rlcs_workspace_size_masked(n_, t_), dtype=torch.uint8, device=dev)
     adv_ref, _ = oracle.gae_masked(ro["r"], ro["v"], ro["mask"], ro["term"], None, None, ro["boot"],
                                    gamma=1.0, lam=0.95)
     nbytes = n_ * t_ * 18

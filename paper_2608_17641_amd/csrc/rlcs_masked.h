@@ -16,10 +16,15 @@
 // steps, a DPP wave scan composes lanes, LDS composes waves and carries chunks.
 //
 // Whitening: the scan kernel also reduces the advantages of the unmasked steps of each
-// workgroup to (count, mean, M2) in fp64; one workgroup merges those partials in a fixed order
-// (Chan et al.'s pairwise update) into the mean and 1/sqrt(var + eps), var the unbiased
-// variance; a last kernel rewrites the advantages. Every order is fixed, so results are
-// reproducible bit for bit.
+// workgroup to (count, mean, M2) in fp64 and publishes them; the workgroup that finishes last
+// (an atomic count of finished workgroups) merges all partials in a fixed order (Chan et al.'s
+// pairwise update) into the mean and 1/sqrt(var + eps), var the unbiased variance; a second
+// kernel rewrites the advantages. Every order is fixed, so results are reproducible bit for
+// bit. A partial is written at device scope and its write completes before its workgroup
+// counts itself finished, so the last workgroup, which reads the partials at device scope
+// after the count, sees every one of them. Finished workgroups are counted in two levels
+// (groups of kMomentGroup workgroups, each with its own counter line; the last of a group
+// counts the group) because atomics on one address serialise.
 #pragma once
 
 #include "rlcs_kernels.h"
@@ -84,8 +89,27 @@ struct MaskedArgs {
     Args a;              // in[0] r, in[1] v, in[2] bv; term, trunc; row_value = boot;
                          // out0 adv, out1 ret (optional)
     const uint8_t* mask; // [N, T], nonzero = the step takes part; null = every step does
-    double* partials;    // per-workgroup (count, mean, M2) of the advantages that take part
+    // whitening only (workspace): stats = {mean, 1/sqrt(var + eps)}; the count of finished
+    // groups; per group, the count of its finished workgroups (one 64-byte line each; all
+    // counts zero between calls); one (count, mean, M2) partial per workgroup
+    double* stats;
+    uint32_t* groups_done;
+    uint32_t* group_counts;
+    double* partials;
+    float eps;
 };
+
+constexpr int kMomentGroup = 32;  // workgroups per first-level finished count
+
+// Chan et al.'s merge of (n, mean, M2) summaries: b into a.
+__device__ __forceinline__ void merge_moments(double& n, double& mean, double& m2, double nb,
+                                              double mb, double m2b) {
+    if (nb == 0.0) return;
+    const double nn = n + nb, d = mb - mean;
+    mean += d * (nb / nn);
+    m2 += m2b + d * d * (n * nb / nn);
+    n = nn;
+}
 
 // Map of one step.
 __device__ __forceinline__ Tri masked_gae_step(const Params& P, bool in, bool te, bool tr, bool ed,
@@ -272,6 +296,7 @@ __global__ void __launch_bounds__(W * kWave) masked_gae_kernel(MaskedArgs ma, in
         chunk_hi = chunk_lo;
     }
     if constexpr (STATS) {
+        __shared__ int s_last;
         n = wave_sum(n);
         s1 = wave_sum(s1);
         s2 = wave_sum(s2);
@@ -282,71 +307,116 @@ __global__ void __launch_bounds__(W * kWave) masked_gae_kernel(MaskedArgs ma, in
             for (int w = 0; w < W; ++w) { tn += s_stat[0][w]; t1 += s_stat[1][w]; t2 += s_stat[2][w]; }
             const double mean = tn > 0.0 ? t1 / tn : 0.0;
             const double m2 = tn > 0.0 ? fmax(t2 - t1 * mean, 0.0) : 0.0;
-            double* out = ma.partials + 4 * int64_t(blockIdx.x);
-            out[0] = tn;
-            out[1] = mean;
-            out[2] = m2;
-        }
-    }
-}
-
-// One workgroup: merges the G partials (count, mean, M2) in a fixed order and writes the mean
-// and 1/sqrt(var + eps) (var unbiased; 0 with fewer than two advantages) to stats[0..1].
-constexpr int kReduceThreads = 1024;
-
-__global__ void __launch_bounds__(kReduceThreads) masked_stats_kernel(const double* partials,
-                                                                      int64_t G, float eps,
-                                                                      double* stats) {
-    __shared__ double s_n[kReduceThreads], s_mean[kReduceThreads], s_m2[kReduceThreads];
-    const int tid = threadIdx.x;
-    double n = 0.0, mean = 0.0, m2 = 0.0;
-    for (int64_t g = tid; g < G; g += kReduceThreads) {
-        const double nb = partials[4 * g], mb = partials[4 * g + 1], m2b = partials[4 * g + 2];
-        if (nb == 0.0) continue;
-        const double nn = n + nb, d = mb - mean;
-        mean += d * (nb / nn);
-        m2 += m2b + d * d * (n * nb / nn);
-        n = nn;
-    }
-    s_n[tid] = n; s_mean[tid] = mean; s_m2[tid] = m2;
-    __syncthreads();
-    for (int half = kReduceThreads / 2; half > 0; half >>= 1) {
-        if (tid < half) {
-            const double na = s_n[tid], nb = s_n[tid + half];
-            if (nb > 0.0) {
-                const double nn = na + nb, d = s_mean[tid + half] - s_mean[tid];
-                s_mean[tid] += d * (nb / nn);
-                s_m2[tid] += s_m2[tid + half] + d * d * (na * nb / nn);
-                s_n[tid] = nn;
+            uint64_t* out = reinterpret_cast<uint64_t*>(ma.partials + 4 * int64_t(blockIdx.x));
+            st_relaxed(out, uint64_t(__double_as_longlong(tn)));
+            st_relaxed(out + 1, uint64_t(__double_as_longlong(mean)));
+            st_relaxed(out + 2, uint64_t(__double_as_longlong(m2)));
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the partial is written
+            const uint32_t G = gridDim.x, g = blockIdx.x / kMomentGroup;
+            const uint32_t n_groups = (G + kMomentGroup - 1) / kMomentGroup;
+            const uint32_t in_group = min(uint32_t(kMomentGroup), G - g * kMomentGroup);
+            uint32_t* gc = ma.group_counts + 16 * g;
+            bool last = false;
+            if (__hip_atomic_fetch_add(gc, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+                in_group - 1) {
+                st_relaxed(gc, 0u);
+                last = __hip_atomic_fetch_add(ma.groups_done, 1u, __ATOMIC_RELAXED,
+                                              __HIP_MEMORY_SCOPE_AGENT) == n_groups - 1;
+                if (last) st_relaxed(ma.groups_done, 0u);
             }
+            s_last = last ? 1 : 0;
         }
         __syncthreads();
-    }
-    if (tid == 0) {
-        const double var = s_n[0] > 1.0 ? s_m2[0] / (s_n[0] - 1.0) : 0.0;
-        stats[0] = s_n[0] > 0.0 ? s_mean[0] : 0.0;
-        stats[1] = 1.0 / sqrt(var + double(eps));
+        if (s_last) {
+            // merge every partial: thread-serial over a fixed stride, then a fixed butterfly
+            // within each wave, then the waves in order
+            double cn = 0.0, cm = 0.0, c2 = 0.0;
+            const uint64_t* part = reinterpret_cast<const uint64_t*>(ma.partials);
+            constexpr int kBatch = 8;  // partials per thread in flight
+            const int64_t G = gridDim.x, step = int64_t(W) * kWave;
+            for (int64_t g0 = threadIdx.x; g0 < G; g0 += kBatch * step) {
+                uint64_t raw[kBatch][3];
+#pragma unroll
+                for (int u = 0; u < kBatch; ++u) {
+                    const int64_t g = g0 + u * step;
+                    if (g < G) {
+                        raw[u][0] = ld_relaxed(part + 4 * g);
+                        raw[u][1] = ld_relaxed(part + 4 * g + 1);
+                        raw[u][2] = ld_relaxed(part + 4 * g + 2);
+                    }
+                }
+#pragma unroll
+                for (int u = 0; u < kBatch; ++u) {
+                    if (g0 + u * step < G)
+                        merge_moments(cn, cm, c2, __longlong_as_double(int64_t(raw[u][0])),
+                                      __longlong_as_double(int64_t(raw[u][1])),
+                                      __longlong_as_double(int64_t(raw[u][2])));
+                }
+            }
+#pragma unroll
+            for (int o = 32; o >= 1; o >>= 1) {
+                const double nb = __shfl_xor(cn, o, kWave), mb = __shfl_xor(cm, o, kWave),
+                             m2b = __shfl_xor(c2, o, kWave);
+                merge_moments(cn, cm, c2, nb, mb, m2b);
+            }
+            __syncthreads();
+            if (lane == 0) { s_stat[0][wave] = cn; s_stat[1][wave] = cm; s_stat[2][wave] = c2; }
+            __syncthreads();
+            if (threadIdx.x == 0) {
+                double tn = 0.0, tm = 0.0, t2 = 0.0;
+                for (int w = 0; w < W; ++w) merge_moments(tn, tm, t2, s_stat[0][w], s_stat[1][w], s_stat[2][w]);
+                const double var = tn > 1.0 ? t2 / (tn - 1.0) : 0.0;
+                ma.stats[0] = tn > 0.0 ? tm : 0.0;
+                ma.stats[1] = 1.0 / sqrt(var + double(ma.eps));
+            }
+        }
     }
 }
 
-// adv <- (adv - mean) * rstd over all `total` elements (grid-stride, 16-byte vectors when
-// aligned).
-__global__ void __launch_bounds__(256) masked_normalize_kernel(float* adv, int64_t total,
-                                                               const double* stats, int vec) {
+// adv <- (adv - mean) * rstd over all `total` elements. Each thread rewrites kNormVec 16-byte
+// vectors (strided by the workgroup size, so that a wave's accesses are contiguous), all loads
+// issued before the first store; workgroup 0 also does the elements past the last vector. The
+// element-wise form is for advantages not 16-byte aligned.
+constexpr int kNormThreads = 256;
+constexpr int kNormVec = 4;
+
+__global__ void __launch_bounds__(kNormThreads) masked_normalize_kernel(float* adv, int64_t total,
+                                                                        const double* stats,
+                                                                        int vec) {
     const float mean = float(stats[0]), rstd = float(stats[1]);
-    const int64_t stride = int64_t(gridDim.x) * blockDim.x;
-    const int64_t tid = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    const int64_t base = int64_t(blockIdx.x) * kNormThreads * kNormVec + threadIdx.x;
     if (vec) {
         f32x4* p = reinterpret_cast<f32x4*>(adv);
         const int64_t nv = total / 4;
-        for (int64_t i = tid; i < nv; i += stride) {
-            f32x4 x = __builtin_nontemporal_load(p + i);
-            x = (x - mean) * rstd;
-            __builtin_nontemporal_store(x, p + i);
+        f32x4 x[kNormVec];
+#pragma unroll
+        for (int u = 0; u < kNormVec; ++u) {
+            const int64_t i = base + int64_t(u) * kNormThreads;
+            if (i < nv) x[u] = __builtin_nontemporal_load(p + i);
         }
-        for (int64_t i = nv * 4 + tid; i < total; i += stride) adv[i] = (adv[i] - mean) * rstd;
+#pragma unroll
+        for (int u = 0; u < kNormVec; ++u) {
+            const int64_t i = base + int64_t(u) * kNormThreads;
+            if (i < nv) __builtin_nontemporal_store((x[u] - mean) * rstd, p + i);
+        }
+        if (blockIdx.x == 0 && threadIdx.x < total - nv * 4) {
+            const int64_t i = nv * 4 + threadIdx.x;
+            adv[i] = (adv[i] - mean) * rstd;
+        }
     } else {
-        for (int64_t i = tid; i < total; i += stride) adv[i] = (adv[i] - mean) * rstd;
+        // the same 4 * kNormVec * kNormThreads elements per workgroup, one at a time
+        const int64_t first = int64_t(blockIdx.x) * kNormThreads * kNormVec * 4 + threadIdx.x;
+        float x[4 * kNormVec];
+#pragma unroll
+        for (int u = 0; u < 4 * kNormVec; ++u) {
+            const int64_t i = first + int64_t(u) * kNormThreads;
+            if (i < total) x[u] = adv[i];
+        }
+#pragma unroll
+        for (int u = 0; u < 4 * kNormVec; ++u) {
+            const int64_t i = first + int64_t(u) * kNormThreads;
+            if (i < total) adv[i] = (x[u] - mean) * rstd;
+        }
     }
 }
 

@@ -8,9 +8,11 @@ using namespace rlcs::host;
 
 namespace {
 
-// Bytes of the whitening workspace of an [N, T] call: 64 for the statistics, then one 32-byte
-// partial per workgroup (at most one workgroup per row).
-size_t masked_ws_need(int64_t N) { return 64 + 32 * size_t(N > 0 ? N : 1); }
+// Bytes of the whitening workspace of an [N, T] call (at most one workgroup per row): 64 for
+// the statistics and the count of finished groups, a 64-byte count line per group of
+// kMomentGroup workgroups, then one 32-byte partial per workgroup.
+size_t masked_groups(int64_t N) { return size_t((N > 0 ? N : 1) + kMomentGroup - 1) / kMomentGroup; }
+size_t masked_ws_need(int64_t N) { return 64 + 64 * masked_groups(N) + 32 * size_t(N > 0 ? N : 1); }
 
 template <typename DT, bool VEC, bool TR, bool HM, bool STATS>
 void launch_masked(const MaskedArgs& ma, int waves, int64_t groups, int64_t rows_per_wg,
@@ -45,7 +47,13 @@ rlcs_status run_masked(MaskedArgs& ma, bool normalize, float eps, void* ws, hipS
                (!ma.mask || aligned(ma.mask, K));
     const bool tr = a.trunc != nullptr, hm = ma.mask != nullptr;
     double* stats = reinterpret_cast<double*>(ws);
-    ma.partials = normalize ? reinterpret_cast<double*>(reinterpret_cast<char*>(ws) + 64) : nullptr;
+    if (normalize) {
+        ma.stats = stats;
+        ma.groups_done = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(ws) + 16);
+        ma.group_counts = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(ws) + 64);
+        ma.partials = reinterpret_cast<double*>(reinterpret_cast<char*>(ws) + 64 + 64 * masked_groups(N));
+        ma.eps = eps;
+    }
 #define RLCS_MASKED(V, TRV, HMV, ST) launch_masked<DT, V, TRV, HMV, ST>(ma, waves, groups, rows_per_wg, wave_local, s)
 #define RLCS_MASKED_ST(V, TRV, HMV) \
     if (normalize) RLCS_MASKED(V, TRV, HMV, true); else RLCS_MASKED(V, TRV, HMV, false)
@@ -59,13 +67,12 @@ rlcs_status run_masked(MaskedArgs& ma, bool normalize, float eps, void* ws, hipS
 #undef RLCS_MASKED_ST
 #undef RLCS_MASKED
     if (normalize) {
-        hipLaunchKernelGGL(masked_stats_kernel, dim3(1), dim3(kReduceThreads), 0, s, ma.partials,
-                           groups, eps, stats);
         const int64_t total = N * T;
-        const int64_t want = (total + 4 * 256 * 8 - 1) / (4 * 256 * 8);
-        const unsigned grid = unsigned(want < 4096 ? (want > 0 ? want : 1) : 4096);
-        hipLaunchKernelGGL(masked_normalize_kernel, dim3(grid), dim3(256), 0, s, a.out0, total,
-                           stats, aligned(a.out0, 16) ? 1 : 0);
+        const int64_t per_wg = int64_t(kNormThreads) * kNormVec * 4;  // elements
+        const int64_t grid = (total + per_wg - 1) / per_wg;
+        if (grid > INT32_MAX) return RLCS_ERR_INVALID_ARG;
+        hipLaunchKernelGGL(masked_normalize_kernel, dim3(unsigned(grid)), dim3(kNormThreads), 0, s,
+                           a.out0, total, stats, aligned(a.out0, 16) ? 1 : 0);
     }
     return hipGetLastError() == hipSuccess ? RLCS_OK : RLCS_ERR_LAUNCH;
 }

@@ -94,3 +94,37 @@ def test_gae_masked_deterministic():
                                gamma=1.0, lam=0.95, normalize=True)[0] for _ in range(3)]
     torch.cuda.synchronize()
     assert torch.equal(outs[0], outs[1]) and torch.equal(outs[1], outs[2])
+
+
+def test_gae_masked_workspace_reuse():
+    """One zero-filled whitening workspace serves calls of several shapes in turn."""
+    ws = torch.zeros(rl.rlcs_workspace_size_masked(600, 1), dtype=torch.uint8, device=DEV)
+    for N, T, seed in ((600, 40, 1), (7, 3000, 2), (600, 40, 1), (64, 1024, 3)):
+        ro = workloads.make_multiturn(N, T, seed=seed, mean_action=20, mean_obs=30)
+        d = {k: to_device(v, DEV) for k, v in ro.items()}
+        adv, _ = rl.rlcs_gae_masked(d["r"], d["v"], d["mask"], d["term"], None, None, d["boot"],
+                                    gamma=1.0, lam=0.95, normalize=True, ws=ws)
+        torch.cuda.synchronize()
+        a, _ = oracle.gae_masked(ro["r"], ro["v"], ro["mask"], ro["term"], None, None, ro["boot"],
+                                 gamma=1.0, lam=0.95)
+        assert_parity({"adv": adv}, {"adv": oracle.normalize_advantages(a, ro["mask"], eps=1e-8)},
+                      TOL["f32"], label=f"reuse {N}x{T}")
+    assert int(ws[16:20].view(torch.int32).item()) == 0
+
+
+def test_gae_masked_unaligned_outputs_whitened():
+    """Advantages not 16-byte aligned: element-wise loads, stores and whitening."""
+    N, T = 37, 301
+    ro = workloads.make_rollout(N, T, seed=21, p_term=0.03, p_trunc=0.03)
+    mask = (np.random.default_rng(21).random((N, T)) < 0.5).astype(np.uint8)
+    d = {k: to_device(v, DEV) for k, v in ro.items()}
+    buf = torch.zeros(N * T + 1, dtype=torch.float32, device=DEV)
+    adv = buf[1:].view(N, T)
+    assert adv.data_ptr() % 16 != 0
+    rl.rlcs_gae_masked(d["r"], d["v"], to_device(mask, DEV), d["term"], d["trunc"], d["bv"],
+                       d["boot"], adv, None, gamma=G, lam=L, normalize=True, want_ret=False)
+    torch.cuda.synchronize()
+    a, _ = oracle.gae_masked(ro["r"], ro["v"], mask, ro["term"], ro["trunc"], ro["bv"], ro["boot"],
+                             gamma=G, lam=L)
+    assert_parity({"adv": adv}, {"adv": oracle.normalize_advantages(a, mask, eps=1e-8)},
+                  TOL["f32"], label="unaligned whitened")
