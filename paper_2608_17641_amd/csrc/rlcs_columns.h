@@ -76,10 +76,22 @@ struct ColChunk {
     uint32_t term, trunc, edge, valid;
     int64_t t0;
 
-    // Step 1. `base`: element of step 0 of the column; `fbase`, `fstep`: its flags. Inactive
-    // lanes (columns past J) have no valid step and load nothing.
-    __device__ __forceinline__ void load(const Args& a, bool active, int64_t j, int64_t base, int64_t st,
-                         int64_t fbase, int64_t fstep, int64_t t0_) {
+    // Raw loads between issue and complete.
+    uint8_t tb[K], rb[K];
+    uint8_t pt, pr;
+    float nraw[Op::kNbrRaw];
+    float rv;
+    bool have_nbr;
+
+    // Step 1, first half. `base`: element of step 0 of the column; `fbase`, `fstep`: its flags.
+    // Every load goes out unconditionally from a clamped, in-range step (the values of steps
+    // past T and of inactive lanes are dropped in `complete`), so no branch waits for a load
+    // and the loads of the next chunk can be in flight while this one is scanned. With
+    // kBvAlways the continuation values are read here too, for every step; otherwise
+    // `complete` reads them only at truncated steps.
+    template <bool kBvAlways>
+    __device__ __forceinline__ void issue(const Args& a, bool active, int64_t j, int64_t base,
+                                          int64_t st, int64_t fbase, int64_t fstep, int64_t t0_) {
         t0 = t0_;
         const int64_t T = a.T;
         valid = 0;
@@ -88,62 +100,72 @@ struct ColChunk {
             for (int k = 0; k < K; ++k)
                 if (t0 + k < T) valid |= 1u << k;
         }
-        uint8_t tb[K], rb[K];
+        const uint8_t* fallback = reinterpret_cast<const uint8_t*>(a.in[0]);
 #pragma unroll
         for (int k = 0; k < K; ++k) {
-            tb[k] = 0;
-            rb[k] = 0;
-            if (Op::kFlags && bit(valid, k)) {
-                if (a.term) tb[k] = a.term[fbase + (t0 + k) * fstep];
-                if (TR) rb[k] = a.trunc[fbase + (t0 + k) * fstep];
-            }
+            const int64_t tc = min(t0 + k, T - 1);
+            tb[k] = (Op::kFlags ? (a.term ? a.term : fallback) : fallback)[fbase + tc * fstep];
+            rb[k] = TR ? a.trunc[fbase + tc * fstep] : uint8_t(0);
         }
 #pragma unroll
         for (int s = 0; s < NS; ++s) {
 #pragma unroll
             for (int k = 0; k < K; ++k) {
+                const int64_t tc = min(t0 + k, T - 1);
                 d[s][k] = 0.f;
-                if (Op::slot_used(s, TR) && s != kTS && bit(valid, k))
-                    d[s][k] = load_one<DT>(a.in[s], base + (t0 + k) * st);
+                if (Op::slot_used(s, TR) && (s != kTS || kBvAlways))
+                    d[s][k] = load_one<DT>(a.in[s], base + tc * st);
             }
         }
-        // neighbour on the carry-source side and the row value at the row edge
-        float nraw[Op::kNbrRaw];
-        bool have_nbr = false;
-        uint8_t pt = 0, pr = 0;
+        have_nbr = false;
+        pt = pr = 0;
+        if constexpr (kBack) {
+            if constexpr (Op::kNbr > 0) {
+                Op::template nbr_load_raw<DT>(a, base + min(t0 + K, T - 1) * st, nraw);
+                have_nbr = t0 + K < T;
+            }
+            rv = (Op::kRowValue && a.row_value) ? load_one<DT>(a.row_value, active ? j : 0) : 0.f;
+        } else {
+            if constexpr (Op::kNbr > 0) {
+                const int64_t tp = max(t0 - 1, int64_t(0));
+                pt = (a.term ? a.term : fallback)[fbase + tp * fstep];
+                pr = TR ? a.trunc[fbase + tp * fstep] : uint8_t(0);
+            }
+            rv = 0.f;
+        }
+    }
+
+    // Step 1, second half: flag masks, edge, row value, neighbour; continuation values at
+    // truncated steps unless `issue` read them all.
+    template <bool kBvAlways>
+    __device__ __forceinline__ void complete(const Args& a, int64_t base, int64_t st) {
+        const int64_t T = a.T;
+        term = 0;
+        trunc = 0;
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+            if (Op::kFlags && a.term && tb[k]) term |= 1u << k;
+            if (TR && rb[k]) trunc |= 1u << k;
+        }
+        term &= valid;
+        trunc &= valid;
         edge = 0;
 #pragma unroll
         for (int k = 0; k < K; ++k) B[k] = 0.f;
         if (valid) {
             if (kBack) {
-                if (Op::kNbr > 0 && t0 + K < T) {
-                    Op::template nbr_load_raw<DT>(a, base + (t0 + K) * st, nraw);
-                    have_nbr = true;
-                }
                 if (t0 + K >= T) {  // the column's last step T-1 is among the lane's steps
                     const int ke = int(T - 1 - t0);
                     edge = 1u << ke;
-                    const float rv = (Op::kRowValue && a.row_value) ? load_one<DT>(a.row_value, j) : 0.f;
 #pragma unroll
                     for (int k = 0; k < K; ++k)
                         if (k == ke) B[k] = rv;
                 }
-            } else {
-                if (Op::kNbr > 0 && t0 > 0) {
-                    if (a.term) pt = a.term[fbase + (t0 - 1) * fstep];
-                    if (TR) pr = a.trunc[fbase + (t0 - 1) * fstep];
-                }
-                if (t0 == 0) edge = 1u;
+            } else if (t0 == 0) {
+                edge = 1u;
             }
         }
-        term = 0;
-        trunc = 0;
-#pragma unroll
-        for (int k = 0; k < K; ++k) {
-            if (tb[k]) term |= 1u << k;
-            if (rb[k]) trunc |= 1u << k;
-        }
-        if constexpr (kTS >= 0) {
+        if constexpr (kTS >= 0 && !kBvAlways) {
 #pragma unroll
             for (int k = 0; k < K; ++k) {
                 d[kTS][k] = 0.f;
@@ -153,10 +175,17 @@ struct ColChunk {
 #pragma unroll
         for (int i = 0; i < NB; ++i) nb[i] = 0.f;
         if constexpr (kBack) {
-            if (have_nbr) Op::nbr_fix(a, nraw, nb);
+            if (have_nbr && valid) Op::nbr_fix(a, nraw, nb);
         } else if constexpr (Op::kNbr > 0) {
-            nb[0] = (pt || (TR && pr)) ? 1.f : 0.f;
+            nb[0] = (t0 > 0 && (pt || (TR && pr))) ? 1.f : 0.f;
         }
+    }
+
+    // Step 1 without overlap: issue, then complete.
+    __device__ __forceinline__ void load(const Args& a, bool active, int64_t j, int64_t base,
+                                         int64_t st, int64_t fbase, int64_t fstep, int64_t t0_) {
+        issue<false>(a, active, j, base, st, fbase, fstep, t0_);
+        complete<false>(a, base, st);
     }
 
     // Steps 2-3: the lane's map (nearest-to-output step outermost).
@@ -236,8 +265,10 @@ __device__ __forceinline__ Pair cols_wave_in(const float (*s_a)[kWave], const fl
 }
 
 // Whole columns per workgroup: chunks walked from the carry source, the value at the chunk's
-// output-side edge carried to the next chunk through LDS. Grid: ceil(J / 64) workgroups.
-template <class Op, typename DT, int K, int W, bool TR>
+// output-side edge carried to the next chunk through LDS. PIPE (columns of several chunks):
+// the next chunk's loads are in flight while a chunk is scanned. Grid: ceil(J / 64)
+// workgroups.
+template <class Op, typename DT, int K, int W, bool TR, bool PIPE>
 __global__ void __launch_bounds__(W * kWave) cols_rows_kernel(Args a, ColGeom g) {
     constexpr bool kBack = Op::kBackward;
     constexpr int64_t L = int64_t(W) * K;
@@ -248,10 +279,10 @@ __global__ void __launch_bounds__(W * kWave) cols_rows_kernel(Args a, ColGeom g)
     const int64_t T = a.T;
     const int64_t P = (T + L - 1) / L;
     float carry = 0.f;
-    for (int64_t i = 0; i < P; ++i) {
-        const int64_t p = kBack ? P - 1 - i : i;
-        ColChunk<Op, DT, K, TR> c;
-        c.load(a, cl.active, cl.j, cl.base, g.st, cl.fbase, cl.fstep, p * L + int64_t(wave) * K);
+    auto t0_of = [&](int64_t i) { return (kBack ? P - 1 - i : i) * L + int64_t(wave) * K; };
+    // steps 1 (second half) to 5 of chunk i, whose loads are issued; the carry moves on
+    auto scan = [&](ColChunk<Op, DT, K, TR>& c) {
+        c.template complete<PIPE>(a, cl.base, g.st);
         const Pair m = c.local(a.p);
         s_a[wave][lane] = m.a;
         s_b[wave][lane] = m.b;
@@ -261,6 +292,26 @@ __global__ void __launch_bounds__(W * kWave) cols_rows_kernel(Args a, ColGeom g)
         if (wave == (kBack ? 0 : W - 1)) s_carry[lane] = out_edge;
         __syncthreads();
         carry = s_carry[lane];
+    };
+    ColChunk<Op, DT, K, TR> c;
+    c.template issue<PIPE>(a, cl.active, cl.j, cl.base, g.st, cl.fbase, cl.fstep, t0_of(0));
+    if constexpr (PIPE) {
+        // software pipeline: chunk i+1's loads (continuation values included, so that nothing
+        // waits for the flags) go out before chunk i is scanned
+        for (int64_t i = 0; i + 1 < P; ++i) {
+            ColChunk<Op, DT, K, TR> nxt;
+            nxt.template issue<true>(a, cl.active, cl.j, cl.base, g.st, cl.fbase, cl.fstep, t0_of(i + 1));
+            __builtin_amdgcn_sched_barrier(0);  // keep those loads ahead of this chunk's first wait
+            scan(c);
+            c = nxt;
+        }
+        scan(c);
+    } else {
+        for (int64_t i = 0;; ++i) {
+            scan(c);
+            if (i + 1 == P) break;
+            c.template issue<false>(a, cl.active, cl.j, cl.base, g.st, cl.fbase, cl.fstep, t0_of(i + 1));
+        }
     }
 }
 

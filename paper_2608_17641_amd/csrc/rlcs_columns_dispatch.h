@@ -15,6 +15,10 @@ constexpr int64_t kColSerialBlocks = kWsSlots;
 
 inline int64_t col_tiles(int64_t T) { return (T + kColL - 1) / kColL; }
 
+// Whole-column walks of at least this many chunks overlap each chunk's loads with the scan of
+// the one before (shorter ones gain less than the unconditional continuation reads cost).
+constexpr int64_t kColPipeChunks = 8;
+
 // Workspace bytes of a split column call: header and block slots, then two records per column
 // per tile (0 if the size does not fit in size_t).
 inline size_t col_ws_need(int64_t J, int64_t T) {
@@ -30,8 +34,11 @@ void col_launch(const Args& a, const ColGeom& g, bool split, int64_t blocks, hip
     if (split) {
         hipLaunchKernelGGL((cols_tiles_kernel<Op, DT, kColK, kColW, TR>),
                            dim3(unsigned(blocks * col_tiles(a.T))), block, 0, s, a, g, blocks);
+    } else if (col_tiles(a.T) >= kColPipeChunks) {
+        hipLaunchKernelGGL((cols_rows_kernel<Op, DT, kColK, kColW, TR, true>), dim3(unsigned(blocks)),
+                           block, 0, s, a, g);
     } else {
-        hipLaunchKernelGGL((cols_rows_kernel<Op, DT, kColK, kColW, TR>), dim3(unsigned(blocks)),
+        hipLaunchKernelGGL((cols_rows_kernel<Op, DT, kColK, kColW, TR, false>), dim3(unsigned(blocks)),
                            block, 0, s, a, g);
     }
 }
