@@ -337,6 +337,9 @@ def run_extra(dev, only=""):
                           ("tm_64x65536", 64, 65536)):
         if label.startswith(only):
             run_time_major(label, t_, n_, dev)
+    for label, n_, t_, ld in (("sr_4096x256_ld320", 4096, 256, 320), ("sr_64x4096_ld4160", 64, 4096, 4160)):
+        if label.startswith(only):
+            run_strided_rows(label, n_, t_, ld, dev)
     for label, n_, t_, f_ in (("vec_4096x256x16", 4096, 256, 16), ("vec_64x1024x256", 64, 1024, 256),
                               ("vec_1x128x1M", 1, 128, 1 << 20)):
         if label.startswith(only):
@@ -457,13 +460,16 @@ def run_time_major(label, t_, n_, dev):
     g = lambda k: np.ascontiguousarray(ro[k][:, cols]) if ro[k].ndim == 2 else ro[k][cols]
     for name in ("gae", "vtrace"):
         if name == "gae":
-            call = lambda d: rl.rlcs_gae_tm(d["r"], d["v"], d["term"], d["trunc"], d["bv"], d["boot"],
-                                            d["o0"], d["o1"], gamma=0.99, lam=0.95, ws=ws)
+            call = lambda d: rl.rlcs_gae_strided(d["r"].t(), d["v"].t(), d["term"].t(), d["trunc"].t(),
+                                                 d["bv"].t(), d["boot"], d["o0"].t(), d["o1"].t(),
+                                                 gamma=0.99, lam=0.95, ws=ws)
             refs = oracle.time_major(oracle.gae, g("r"), g("v"), g("term"), g("trunc"), g("bv"),
                                      g("boot"), gamma=0.99, lam=0.95)
         else:
-            call = lambda d: rl.rlcs_vtrace_tm(d["r"], d["v"], d["log_rho"], d["term"], d["trunc"],
-                                               d["bv"], d["boot"], d["o0"], d["o1"], gamma=0.99, ws=ws)
+            call = lambda d: rl.rlcs_vtrace_strided(d["r"].t(), d["v"].t(), d["log_rho"].t(),
+                                                    d["term"].t(), d["trunc"].t(), d["bv"].t(),
+                                                    d["boot"], d["o0"].t(), d["o1"].t(), gamma=0.99,
+                                                    ws=ws)
             refs = oracle.time_major(oracle.vtrace, g("r"), g("v"), g("log_rho"), g("term"),
                                      g("trunc"), g("bv"), g("boot"), gamma=0.99)
         call(sets[0])
@@ -476,6 +482,48 @@ def run_time_major(label, t_, n_, dev):
             raise SystemExit(f"parity failure in {label} {name}: {rel}")
         nbytes = extra_bytes(name, n_, t_, 4, True, True)
         _report(label, name + "_tm", _graph_time(call, sets, nbytes), nbytes, n_ * t_, S, rel)
+
+
+def run_strided_rows(label, n_, t_, ld, dev):
+    """GAE on [N, T] rows that are the first T steps of [N, ld] rows (fp32, truncation):
+    parity on sampled rows, then graph-timed. Same dense byte count as the row-major form."""
+    import torch
+    import oracle
+    import workloads
+    import paper_2608_17641_amd as rl
+    ro = workloads.make_rollout(n_, t_, 0, p_term=0.02, p_trunc=0.01)
+
+    def wide(a):
+        t = torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+        if t.dim() != 2:
+            return t
+        buf = torch.zeros((n_, ld), dtype=t.dtype, device=dev)
+        buf[:, :t_] = t
+        return buf[:, :t_]
+    base = {k: wide(v) for k, v in ro.items()}
+    S = max(1, min(32, -(-600_000_000 // (n_ * ld * 30))))
+    sets = []
+    for i in range(S):
+        d = dict(base if i == 0 else {k: wide(v) for k, v in ro.items()})
+        d["o0"] = torch.empty((n_, ld), dtype=torch.float32, device=dev)[:, :t_]
+        d["o1"] = torch.empty((n_, ld), dtype=torch.float32, device=dev)[:, :t_]
+        sets.append(d)
+    ws = rl.make_workspace_columns(n_, t_, dev)
+    call = lambda d: rl.rlcs_gae_strided(d["r"], d["v"], d["term"], d["trunc"], d["bv"], d["boot"],
+                                         d["o0"], d["o1"], gamma=0.99, lam=0.95, ws=ws)
+    call(sets[0])
+    torch.cuda.synchronize()
+    rows = np.unique(np.concatenate([[0, n_ - 1], np.random.default_rng(1).integers(0, n_, 32)]))
+    g = lambda k: ro[k][rows]
+    refs = oracle.gae(g("r"), g("v"), g("term"), g("trunc"), g("bv"), g("boot"), gamma=0.99, lam=0.95)
+    rel = 0.0
+    for o, r_ in zip((sets[0]["o0"], sets[0]["o1"]), refs):
+        got = o.index_select(0, torch.from_numpy(rows).to(dev)).double().cpu().numpy()
+        rel = max(rel, float(np.max(np.abs(got - r_))) / (1 + float(np.max(np.abs(r_)))))
+    if rel > 1e-5:
+        raise SystemExit(f"parity failure in {label}: {rel}")
+    nbytes = extra_bytes("gae", n_, t_, 4, True, True)
+    _report(label, "gae_strided", _graph_time(call, sets, nbytes), nbytes, n_ * t_, S, rel)
 
 
 def run_vector_trace(label, n_, t_, f_, dev):

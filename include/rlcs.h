@@ -223,45 +223,58 @@ rlcs_status rlcs_gae_masked(const void* r, const void* v, const uint8_t* mask,
 size_t rlcs_workspace_size_masked(int64_t N, int64_t T);
 
 /* ---------------------------------------------------------------------------------------
- * Time-major layouts. The entry points below compute exactly what their row-major namesakes
- * compute, for buffers stored time-major: every [N, T] array of the row-major form becomes a
- * [T, ld] array with step t of environment n at element t*ld + n (ld >= N; ld == 0 means
- * N), e.g. a [T, B] rollout buffer or a strided view of a wider one. All [T, ld] arrays of a
- * call (data, flags, bv and outputs) share ld; boot stays [N], contiguous. Elements n >= N
- * of a step are neither read nor written. Sizes: N >= 0, 0 <= T <= 2^30, T*ld representable.
+ * Strided layouts. The entry points below compute exactly what their row-major namesakes
+ * compute, for [N, T] arrays laid out with element (n, t) at n * stride_n + t * stride_t:
+ *   - time-major buffers ([T, ld] storage, step t of environment n at t * ld + n):
+ *     stride_n = 1, stride_t = ld (>= N);
+ *   - strided rows ([N, ld] storage, e.g. a view of the first T steps of wider rows):
+ *     stride_n = ld (>= T), stride_t = 1;
+ *   - dense row-major (stride_n = T, stride_t = 1) runs the row-major entry point itself.
+ * Both strides are >= 1, counted in elements, and one dimension must nest inside the other
+ * (stride_n >= T * stride_t or stride_t >= N * stride_n), so that distinct (n, t) are distinct
+ * elements. All [N, T] arrays of a call (data, flags, bv and outputs) share the strides; boot
+ * stays [N], contiguous. Elements outside the (n, t) grid are neither read nor written.
+ * Sizes: N >= 0, 0 <= T <= 2^30, the largest element offset representable.
  * Workspace: at least rlcs_workspace_size_columns(N, T) bytes, zero-filled once, lets few
- * environments (N below about 64K) be split along T over several workgroups; without it
- * each group of 64 environments is scanned by one workgroup. Every other convention is the
- * row-major one.                                                                          */
-rlcs_status rlcs_gae_tm(const void* r, const void* v, const uint8_t* term, const uint8_t* trunc,
-                        const void* bv, const void* boot, float* adv, float* ret, int64_t N,
-                        int64_t T, int64_t ld, float gamma, float lambda, rlcs_dtype dtype,
-                        void* ws, size_t ws_bytes, rlcs_stream_t stream);
-rlcs_status rlcs_vtrace_tm(const void* r, const void* v, const void* log_rho, const uint8_t* term,
-                           const uint8_t* trunc, const void* bv, const void* boot, float* vs,
-                           float* pg, int64_t N, int64_t T, int64_t ld, float gamma,
-                           float rho_bar, float c_bar, rlcs_dtype dtype, void* ws,
-                           size_t ws_bytes, rlcs_stream_t stream);
-rlcs_status rlcs_retrace_tm(const void* r, const void* q, const void* eq, const void* log_rho,
-                            const uint8_t* term, const uint8_t* trunc, const void* bv,
-                            const void* boot, float* delta, float* q_ret, int64_t N, int64_t T,
-                            int64_t ld, float gamma, float lambda, float c_bar, rlcs_dtype dtype,
-                            void* ws, size_t ws_bytes, rlcs_stream_t stream);
-rlcs_status rlcs_td_lambda_tm(const void* r, const void* v, const uint8_t* term,
-                              const uint8_t* trunc, const void* bv, const void* boot, float* ret,
-                              int64_t N, int64_t T, int64_t ld, float gamma, float lambda,
-                              rlcs_dtype dtype, void* ws, size_t ws_bytes, rlcs_stream_t stream);
-rlcs_status rlcs_discounted_tm(const void* r, const uint8_t* term, const uint8_t* trunc,
-                               const void* bv, const void* boot, float* ret, int64_t N, int64_t T,
-                               int64_t ld, float gamma, rlcs_dtype dtype, void* ws,
-                               size_t ws_bytes, rlcs_stream_t stream);
-rlcs_status rlcs_elig_trace_tm(const void* x, const uint8_t* term, const uint8_t* trunc, float* z,
-                               int64_t N, int64_t T, int64_t ld, float gamma, float lambda,
-                               rlcs_dtype dtype, void* ws, size_t ws_bytes, rlcs_stream_t stream);
-rlcs_status rlcs_episodic_prefix_tm(const void* x, const uint8_t* term, const uint8_t* trunc,
-                                    float* c, int64_t N, int64_t T, int64_t ld,
-                                    rlcs_boundary boundary, rlcs_dtype dtype, void* ws,
-                                    size_t ws_bytes, rlcs_stream_t stream);
+ * environments (N below about 64K) be split along T over several workgroups; without it each
+ * group of 64 environments is scanned by one workgroup (the dense layout takes
+ * rlcs_workspace_size(N, T) instead). Every other convention is the row-major one.        */
+rlcs_status rlcs_gae_strided(const void* r, const void* v, const uint8_t* term,
+                             const uint8_t* trunc, const void* bv, const void* boot, float* adv,
+                             float* ret, int64_t N, int64_t T, int64_t stride_n, int64_t stride_t,
+                             float gamma, float lambda, rlcs_dtype dtype, void* ws,
+                             size_t ws_bytes, rlcs_stream_t stream);
+rlcs_status rlcs_vtrace_strided(const void* r, const void* v, const void* log_rho,
+                                const uint8_t* term, const uint8_t* trunc, const void* bv,
+                                const void* boot, float* vs, float* pg, int64_t N, int64_t T,
+                                int64_t stride_n, int64_t stride_t, float gamma, float rho_bar,
+                                float c_bar, rlcs_dtype dtype, void* ws, size_t ws_bytes,
+                                rlcs_stream_t stream);
+rlcs_status rlcs_retrace_strided(const void* r, const void* q, const void* eq, const void* log_rho,
+                                 const uint8_t* term, const uint8_t* trunc, const void* bv,
+                                 const void* boot, float* delta, float* q_ret, int64_t N,
+                                 int64_t T, int64_t stride_n, int64_t stride_t, float gamma,
+                                 float lambda, float c_bar, rlcs_dtype dtype, void* ws,
+                                 size_t ws_bytes, rlcs_stream_t stream);
+rlcs_status rlcs_td_lambda_strided(const void* r, const void* v, const uint8_t* term,
+                                   const uint8_t* trunc, const void* bv, const void* boot,
+                                   float* ret, int64_t N, int64_t T, int64_t stride_n,
+                                   int64_t stride_t, float gamma, float lambda, rlcs_dtype dtype,
+                                   void* ws, size_t ws_bytes, rlcs_stream_t stream);
+rlcs_status rlcs_discounted_strided(const void* r, const uint8_t* term, const uint8_t* trunc,
+                                    const void* bv, const void* boot, float* ret, int64_t N,
+                                    int64_t T, int64_t stride_n, int64_t stride_t, float gamma,
+                                    rlcs_dtype dtype, void* ws, size_t ws_bytes,
+                                    rlcs_stream_t stream);
+rlcs_status rlcs_elig_trace_strided(const void* x, const uint8_t* term, const uint8_t* trunc,
+                                    float* z, int64_t N, int64_t T, int64_t stride_n,
+                                    int64_t stride_t, float gamma, float lambda, rlcs_dtype dtype,
+                                    void* ws, size_t ws_bytes, rlcs_stream_t stream);
+rlcs_status rlcs_episodic_prefix_strided(const void* x, const uint8_t* term, const uint8_t* trunc,
+                                         float* c, int64_t N, int64_t T, int64_t stride_n,
+                                         int64_t stride_t, rlcs_boundary boundary,
+                                         rlcs_dtype dtype, void* ws, size_t ws_bytes,
+                                         rlcs_stream_t stream);
 
 /* Eligibility traces of feature vectors (Section 3.3.5: the trace of the gradient, or of the
  * feature vector under linear function approximation), forward:
@@ -272,14 +285,14 @@ rlcs_status rlcs_episodic_prefix_tm(const void* x, const uint8_t* term, const ui
  *   term, trunc  [N, T] as above (one flag per step, for every feature)
  *   z        [N, T, F] float32 out: traces
  * Sizes: N, F >= 0, 0 <= T <= 2^30, N*T*F representable; any of them 0 is a no-op.
- * Workspace: rlcs_workspace_size_columns(N * F, T) bytes, as for the time-major calls (used
+ * Workspace: rlcs_workspace_size_columns(N * F, T) bytes, as for the strided calls (used
  * when N*F is below about 64K).                                                           */
 rlcs_status rlcs_elig_trace_vec(const void* x, const uint8_t* term, const uint8_t* trunc,
                                 float* z, int64_t N, int64_t T, int64_t F, float gamma,
                                 float lambda, rlcs_dtype dtype, void* ws, size_t ws_bytes,
                                 rlcs_stream_t stream);
 
-/* Workspace bytes for the time-major calls (columns = N) and rlcs_elig_trace_vec
+/* Workspace bytes for the strided calls (columns = N) and rlcs_elig_trace_vec
  * (columns = N * F) over T steps: the fixed 65600-byte part plus 16 bytes per column per
  * 32-step tile; 0 for negative sizes or a size that overflows. */
 size_t rlcs_workspace_size_columns(int64_t columns, int64_t T);

@@ -23,8 +23,9 @@ __all__ = [
     "rlcs_gae", "rlcs_vtrace", "rlcs_retrace", "rlcs_retrace_full", "rlcs_td_lambda", "rlcs_discounted",
     "rlcs_elig_trace", "rlcs_episodic_prefix", "rlcs_affine_scan", "rlcs_workspace_size",
     "rlcs_version", "rlcs_set_variant_override", "make_workspace", "RlcsError",
-    "rlcs_gae_tm", "rlcs_vtrace_tm", "rlcs_retrace_tm", "rlcs_td_lambda_tm", "rlcs_discounted_tm",
-    "rlcs_elig_trace_tm", "rlcs_episodic_prefix_tm", "rlcs_elig_trace_vec",
+    "rlcs_gae_strided", "rlcs_vtrace_strided", "rlcs_retrace_strided", "rlcs_td_lambda_strided",
+    "rlcs_discounted_strided", "rlcs_elig_trace_strided", "rlcs_episodic_prefix_strided",
+    "rlcs_elig_trace_vec",
     "rlcs_workspace_size_columns", "make_workspace_columns", "rlcs_gae_masked",
     "rlcs_workspace_size_masked",
 ]
@@ -267,32 +268,44 @@ def rlcs_affine_scan(alpha, beta, carry=None, out=None, *, reverse: bool = True,
     return out
 
 
-# ---------------------------------------------------------------- time-major layouts
-# Every [N, T] tensor of the row-major functions becomes a [T, N] tensor (step t of
-# environment n at [t, n]) whose rows may be strided: stride (ld, 1) with ld >= N, the same
-# for every [T, N] tensor of the call. Outputs not given are allocated with that stride.
+# ---------------------------------------------------------------- strided layouts
+# Every [N, T] tensor of the row-major functions may be any 2-D view with strides
+# (stride_n, stride_t) in elements, the same for every [N, T] tensor of the call: a time-major
+# [T, N] buffer is passed as its transpose ``x.t()`` (strides (1, ld)), a view of the first T
+# steps of wider rows as is (strides (ld, 1)). Outputs not given are allocated with the inputs'
+# strides.
 
-def _prep_tm(x: torch.Tensor):
+def _strides(t: torch.Tensor):
+    """(stride_n, stride_t) of a 2-D view, with the stride of a size-1 dimension chosen so that
+    the dimensions nest (it never multiplies an index other than 0)."""
+    N, T = int(t.shape[0]), int(t.shape[1])
+    sn, st = int(t.stride(0)), int(t.stride(1))
+    if T == 1:
+        st = max(1, N * max(sn, 1))
+    if N == 1:
+        sn = max(1, T * max(st, 1))
+    return sn, st
+
+
+def _prep_strided(x: torch.Tensor):
     if not isinstance(x, torch.Tensor) or x.dim() != 2:
-        raise ValueError("data inputs must be 2-D [T, N] tensors")
+        raise ValueError("data inputs must be 2-D [N, T] tensors")
     if x.dtype not in _DTYPES:
         raise TypeError(f"data inputs must be float32 or bfloat16, got {x.dtype}")
     if x.device.type != "cuda":
         raise ValueError("tensors must be on a GPU")
-    T, N = int(x.shape[0]), int(x.shape[1])
-    ld = int(x.stride(0)) if T > 1 else N
-    if (N > 1 and x.stride(1) != 1) or ld < N:
-        raise ValueError("time-major tensors must have stride (ld, 1) with ld >= N")
-    return T, N, ld, x.dtype, x.device
+    N, T = int(x.shape[0]), int(x.shape[1])
+    sn, st = _strides(x)
+    return N, T, sn, st, x.dtype, x.device
 
 
-def _check_tm(name, t, T, N, ld, device, dtype=None, flags=False):
+def _check_strided(name, t, N, T, sn, st, device, dtype=None, flags=False):
     if t is None:
         return None
     if not isinstance(t, torch.Tensor):
         raise TypeError(f"{name} must be a torch.Tensor")
-    if tuple(t.shape) != (T, N):
-        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {(T, N)}")
+    if tuple(t.shape) != (N, T):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {(N, T)}")
     if flags:
         if t.dtype not in (torch.uint8, torch.bool):
             raise TypeError(f"{name} must be uint8 or bool, got {t.dtype}")
@@ -300,25 +313,25 @@ def _check_tm(name, t, T, N, ld, device, dtype=None, flags=False):
         raise TypeError(f"{name} has dtype {t.dtype}, expected {dtype}")
     if t.device != device:
         raise ValueError(f"{name} is on {t.device}, expected {device}")
-    if (N > 1 and t.stride(1) != 1) or (T > 1 and t.stride(0) != ld):
-        raise ValueError(f"{name} has strides {t.stride()}, expected ({ld}, 1) like the first input")
+    if _strides(t) != (sn, st):
+        raise ValueError(f"{name} has strides {t.stride()}, expected ({sn}, {st}) like the first input")
     return t
 
 
-def _out_tm(name, t, T, N, ld, device):
+def _out_strided(name, t, N, T, sn, st, device):
     if t is None:
-        return torch.empty((T, ld), dtype=torch.float32, device=device)[:, :N]
+        return torch.empty_strided((N, T), (sn, st), dtype=torch.float32, device=device)
     if t.dtype != torch.float32:
         raise ValueError(f"{name} must be float32")
-    return _check_tm(name, t, T, N, ld, device)
+    return _check_strided(name, t, N, T, sn, st, device)
 
 
-def _boot_tm(boot, N, dtype, device):
+def _boot_strided(boot, N, dtype, device):
     return _check_data("boot", boot, 1, N, dtype, device, shape=(N,))
 
 
 def make_workspace_columns(columns: int, T: int, device) -> torch.Tensor:
-    """Zero-filled workspace for time-major calls (columns = N) and rlcs_elig_trace_vec
+    """Zero-filled workspace for strided calls (columns = N) and rlcs_elig_trace_vec
     (columns = N * F) over T steps."""
     n = int(_native.load().rlcs_workspace_size_columns(int(columns), int(T)))
     return torch.zeros(max(n, 64), dtype=torch.uint8, device=device)
@@ -328,109 +341,116 @@ def rlcs_workspace_size_columns(columns: int, T: int) -> int:
     return int(_native.load().rlcs_workspace_size_columns(int(columns), int(T)))
 
 
-def rlcs_gae_tm(r, v, term=None, trunc=None, bv=None, boot=None, adv=None, ret=None, *,
-                gamma: float, lam: float, ws=None, want_ret: bool = True):
-    T, N, ld, dt, dev = _prep_tm(r)
-    _check_tm("v", v, T, N, ld, dev, dt); _check_tm("bv", bv, T, N, ld, dev, dt)
-    _check_tm("term", term, T, N, ld, dev, flags=True); _check_tm("trunc", trunc, T, N, ld, dev, flags=True)
-    _boot_tm(boot, N, dt, dev)
-    adv = _out_tm("adv", adv, T, N, ld, dev)
-    ret = _out_tm("ret", ret, T, N, ld, dev) if (want_ret or ret is not None) else None
+def rlcs_gae_strided(r, v, term=None, trunc=None, bv=None, boot=None, adv=None, ret=None, *,
+                     gamma: float, lam: float, ws=None, want_ret: bool = True):
+    N, T, sn, st, dt, dev = _prep_strided(r)
+    _check_strided("v", v, N, T, sn, st, dev, dt); _check_strided("bv", bv, N, T, sn, st, dev, dt)
+    _check_strided("term", term, N, T, sn, st, dev, flags=True)
+    _check_strided("trunc", trunc, N, T, sn, st, dev, flags=True)
+    _boot_strided(boot, N, dt, dev)
+    adv = _out_strided("adv", adv, N, T, sn, st, dev)
+    ret = _out_strided("ret", ret, N, T, sn, st, dev) if (want_ret or ret is not None) else None
     wp, wb = _ws(ws, dev)
     with torch.cuda.device(dev):
-        _call("rlcs_gae_tm", _ptr(r), _ptr(v), _ptr(term), _ptr(trunc), _ptr(bv), _ptr(boot),
-              _ptr(adv), _ptr(ret), N, T, ld, gamma, lam, _DTYPES[dt], wp, wb, _stream(dev))
+        _call("rlcs_gae_strided", _ptr(r), _ptr(v), _ptr(term), _ptr(trunc), _ptr(bv), _ptr(boot),
+              _ptr(adv), _ptr(ret), N, T, sn, st, gamma, lam, _DTYPES[dt], wp, wb, _stream(dev))
     return adv, ret
 
 
-def rlcs_vtrace_tm(r, v, log_rho, term=None, trunc=None, bv=None, boot=None, vs=None, pg=None, *,
-                   gamma: float, rho_bar: float = 1.0, c_bar: float = 1.0, ws=None,
-                   want_pg: bool = True):
-    T, N, ld, dt, dev = _prep_tm(r)
+def rlcs_vtrace_strided(r, v, log_rho, term=None, trunc=None, bv=None, boot=None, vs=None,
+                        pg=None, *, gamma: float, rho_bar: float = 1.0, c_bar: float = 1.0,
+                        ws=None, want_pg: bool = True):
+    N, T, sn, st, dt, dev = _prep_strided(r)
     for name, t in (("v", v), ("log_rho", log_rho), ("bv", bv)):
-        _check_tm(name, t, T, N, ld, dev, dt)
-    _check_tm("term", term, T, N, ld, dev, flags=True); _check_tm("trunc", trunc, T, N, ld, dev, flags=True)
-    _boot_tm(boot, N, dt, dev)
-    vs = _out_tm("vs", vs, T, N, ld, dev)
-    pg = _out_tm("pg", pg, T, N, ld, dev) if (want_pg or pg is not None) else None
+        _check_strided(name, t, N, T, sn, st, dev, dt)
+    _check_strided("term", term, N, T, sn, st, dev, flags=True)
+    _check_strided("trunc", trunc, N, T, sn, st, dev, flags=True)
+    _boot_strided(boot, N, dt, dev)
+    vs = _out_strided("vs", vs, N, T, sn, st, dev)
+    pg = _out_strided("pg", pg, N, T, sn, st, dev) if (want_pg or pg is not None) else None
     wp, wb = _ws(ws, dev)
     with torch.cuda.device(dev):
-        _call("rlcs_vtrace_tm", _ptr(r), _ptr(v), _ptr(log_rho), _ptr(term), _ptr(trunc),
-              _ptr(bv), _ptr(boot), _ptr(vs), _ptr(pg), N, T, ld, gamma, rho_bar, c_bar,
+        _call("rlcs_vtrace_strided", _ptr(r), _ptr(v), _ptr(log_rho), _ptr(term), _ptr(trunc),
+              _ptr(bv), _ptr(boot), _ptr(vs), _ptr(pg), N, T, sn, st, gamma, rho_bar, c_bar,
               _DTYPES[dt], wp, wb, _stream(dev))
     return vs, pg
 
 
-def rlcs_retrace_tm(r, q, eq, log_rho, term=None, trunc=None, bv=None, boot=None, delta=None,
-                    q_ret=None, *, gamma: float, lam: float, c_bar: float = 1.0, ws=None,
-                    want_q_ret: bool = True):
-    T, N, ld, dt, dev = _prep_tm(r)
+def rlcs_retrace_strided(r, q, eq, log_rho, term=None, trunc=None, bv=None, boot=None,
+                         delta=None, q_ret=None, *, gamma: float, lam: float, c_bar: float = 1.0,
+                         ws=None, want_q_ret: bool = True):
+    N, T, sn, st, dt, dev = _prep_strided(r)
     for name, t in (("q", q), ("eq", eq), ("log_rho", log_rho), ("bv", bv)):
-        _check_tm(name, t, T, N, ld, dev, dt)
-    _check_tm("term", term, T, N, ld, dev, flags=True); _check_tm("trunc", trunc, T, N, ld, dev, flags=True)
-    _boot_tm(boot, N, dt, dev)
-    delta = _out_tm("delta", delta, T, N, ld, dev)
-    q_ret = _out_tm("q_ret", q_ret, T, N, ld, dev) if (want_q_ret or q_ret is not None) else None
+        _check_strided(name, t, N, T, sn, st, dev, dt)
+    _check_strided("term", term, N, T, sn, st, dev, flags=True)
+    _check_strided("trunc", trunc, N, T, sn, st, dev, flags=True)
+    _boot_strided(boot, N, dt, dev)
+    delta = _out_strided("delta", delta, N, T, sn, st, dev)
+    q_ret = _out_strided("q_ret", q_ret, N, T, sn, st, dev) if (want_q_ret or q_ret is not None) else None
     wp, wb = _ws(ws, dev)
     with torch.cuda.device(dev):
-        _call("rlcs_retrace_tm", _ptr(r), _ptr(q), _ptr(eq), _ptr(log_rho), _ptr(term),
-              _ptr(trunc), _ptr(bv), _ptr(boot), _ptr(delta), _ptr(q_ret), N, T, ld, gamma, lam,
-              c_bar, _DTYPES[dt], wp, wb, _stream(dev))
+        _call("rlcs_retrace_strided", _ptr(r), _ptr(q), _ptr(eq), _ptr(log_rho), _ptr(term),
+              _ptr(trunc), _ptr(bv), _ptr(boot), _ptr(delta), _ptr(q_ret), N, T, sn, st, gamma,
+              lam, c_bar, _DTYPES[dt], wp, wb, _stream(dev))
     return delta, q_ret
 
 
-def rlcs_td_lambda_tm(r, v, term=None, trunc=None, bv=None, boot=None, ret=None, *, gamma: float,
-                      lam: float, ws=None) -> torch.Tensor:
-    T, N, ld, dt, dev = _prep_tm(r)
-    _check_tm("v", v, T, N, ld, dev, dt); _check_tm("bv", bv, T, N, ld, dev, dt)
-    _check_tm("term", term, T, N, ld, dev, flags=True); _check_tm("trunc", trunc, T, N, ld, dev, flags=True)
-    _boot_tm(boot, N, dt, dev)
-    ret = _out_tm("ret", ret, T, N, ld, dev)
+def rlcs_td_lambda_strided(r, v, term=None, trunc=None, bv=None, boot=None, ret=None, *,
+                           gamma: float, lam: float, ws=None) -> torch.Tensor:
+    N, T, sn, st, dt, dev = _prep_strided(r)
+    _check_strided("v", v, N, T, sn, st, dev, dt); _check_strided("bv", bv, N, T, sn, st, dev, dt)
+    _check_strided("term", term, N, T, sn, st, dev, flags=True)
+    _check_strided("trunc", trunc, N, T, sn, st, dev, flags=True)
+    _boot_strided(boot, N, dt, dev)
+    ret = _out_strided("ret", ret, N, T, sn, st, dev)
     wp, wb = _ws(ws, dev)
     with torch.cuda.device(dev):
-        _call("rlcs_td_lambda_tm", _ptr(r), _ptr(v), _ptr(term), _ptr(trunc), _ptr(bv),
-              _ptr(boot), _ptr(ret), N, T, ld, gamma, lam, _DTYPES[dt], wp, wb, _stream(dev))
+        _call("rlcs_td_lambda_strided", _ptr(r), _ptr(v), _ptr(term), _ptr(trunc), _ptr(bv),
+              _ptr(boot), _ptr(ret), N, T, sn, st, gamma, lam, _DTYPES[dt], wp, wb, _stream(dev))
     return ret
 
 
-def rlcs_discounted_tm(r, term=None, trunc=None, bv=None, boot=None, ret=None, *, gamma: float,
-                       ws=None) -> torch.Tensor:
-    T, N, ld, dt, dev = _prep_tm(r)
-    _check_tm("bv", bv, T, N, ld, dev, dt)
-    _check_tm("term", term, T, N, ld, dev, flags=True); _check_tm("trunc", trunc, T, N, ld, dev, flags=True)
-    _boot_tm(boot, N, dt, dev)
-    ret = _out_tm("ret", ret, T, N, ld, dev)
+def rlcs_discounted_strided(r, term=None, trunc=None, bv=None, boot=None, ret=None, *,
+                            gamma: float, ws=None) -> torch.Tensor:
+    N, T, sn, st, dt, dev = _prep_strided(r)
+    _check_strided("bv", bv, N, T, sn, st, dev, dt)
+    _check_strided("term", term, N, T, sn, st, dev, flags=True)
+    _check_strided("trunc", trunc, N, T, sn, st, dev, flags=True)
+    _boot_strided(boot, N, dt, dev)
+    ret = _out_strided("ret", ret, N, T, sn, st, dev)
     wp, wb = _ws(ws, dev)
     with torch.cuda.device(dev):
-        _call("rlcs_discounted_tm", _ptr(r), _ptr(term), _ptr(trunc), _ptr(bv), _ptr(boot),
-              _ptr(ret), N, T, ld, gamma, _DTYPES[dt], wp, wb, _stream(dev))
+        _call("rlcs_discounted_strided", _ptr(r), _ptr(term), _ptr(trunc), _ptr(bv), _ptr(boot),
+              _ptr(ret), N, T, sn, st, gamma, _DTYPES[dt], wp, wb, _stream(dev))
     return ret
 
 
-def rlcs_elig_trace_tm(x, term=None, trunc=None, z=None, *, gamma: float, lam: float,
-                       ws=None) -> torch.Tensor:
-    T, N, ld, dt, dev = _prep_tm(x)
-    _check_tm("term", term, T, N, ld, dev, flags=True); _check_tm("trunc", trunc, T, N, ld, dev, flags=True)
-    z = _out_tm("z", z, T, N, ld, dev)
+def rlcs_elig_trace_strided(x, term=None, trunc=None, z=None, *, gamma: float, lam: float,
+                            ws=None) -> torch.Tensor:
+    N, T, sn, st, dt, dev = _prep_strided(x)
+    _check_strided("term", term, N, T, sn, st, dev, flags=True)
+    _check_strided("trunc", trunc, N, T, sn, st, dev, flags=True)
+    z = _out_strided("z", z, N, T, sn, st, dev)
     wp, wb = _ws(ws, dev)
     with torch.cuda.device(dev):
-        _call("rlcs_elig_trace_tm", _ptr(x), _ptr(term), _ptr(trunc), _ptr(z), N, T, ld, gamma,
-              lam, _DTYPES[dt], wp, wb, _stream(dev))
+        _call("rlcs_elig_trace_strided", _ptr(x), _ptr(term), _ptr(trunc), _ptr(z), N, T, sn, st,
+              gamma, lam, _DTYPES[dt], wp, wb, _stream(dev))
     return z
 
 
-def rlcs_episodic_prefix_tm(x, term=None, trunc=None, c=None, *, boundary: str = "ends_at",
-                            ws=None) -> torch.Tensor:
-    T, N, ld, dt, dev = _prep_tm(x)
+def rlcs_episodic_prefix_strided(x, term=None, trunc=None, c=None, *, boundary: str = "ends_at",
+                                 ws=None) -> torch.Tensor:
+    N, T, sn, st, dt, dev = _prep_strided(x)
     if boundary not in ("ends_at", "starts_at"):
         raise ValueError(f"boundary must be 'ends_at' or 'starts_at', got {boundary!r}")
-    _check_tm("term", term, T, N, ld, dev, flags=True); _check_tm("trunc", trunc, T, N, ld, dev, flags=True)
-    c = _out_tm("c", c, T, N, ld, dev)
+    _check_strided("term", term, N, T, sn, st, dev, flags=True)
+    _check_strided("trunc", trunc, N, T, sn, st, dev, flags=True)
+    c = _out_strided("c", c, N, T, sn, st, dev)
     wp, wb = _ws(ws, dev)
     b = _native.RLCS_STARTS_AT if boundary == "starts_at" else _native.RLCS_ENDS_AT
     with torch.cuda.device(dev):
-        _call("rlcs_episodic_prefix_tm", _ptr(x), _ptr(term), _ptr(trunc), _ptr(c), N, T, ld, b,
-              _DTYPES[dt], wp, wb, _stream(dev))
+        _call("rlcs_episodic_prefix_strided", _ptr(x), _ptr(term), _ptr(trunc), _ptr(c), N, T, sn,
+              st, b, _DTYPES[dt], wp, wb, _stream(dev))
     return c
 
 

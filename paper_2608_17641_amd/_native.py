@@ -44,15 +44,19 @@ PROTOTYPES = {
     "rlcs_episodic_prefix": [_P, _P, _P, _P, _I64, _I64, _INT, _INT, _P, _SZ, _P],
     "rlcs_affine_scan": [_P, _P, _P, _P, _I64, _I64, _INT, _INT, _P, _SZ, _P],
     "rlcs_workspace_size": [_I64, _I64],
-    "rlcs_gae_tm": [_P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _F, _F, _INT, _P, _SZ, _P],
-    "rlcs_vtrace_tm": [_P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _F, _F, _F, _INT, _P,
-                       _SZ, _P],
-    "rlcs_retrace_tm": [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _F, _F, _F, _INT,
-                        _P, _SZ, _P],
-    "rlcs_td_lambda_tm": [_P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _F, _F, _INT, _P, _SZ, _P],
-    "rlcs_discounted_tm": [_P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _F, _INT, _P, _SZ, _P],
-    "rlcs_elig_trace_tm": [_P, _P, _P, _P, _I64, _I64, _I64, _F, _F, _INT, _P, _SZ, _P],
-    "rlcs_episodic_prefix_tm": [_P, _P, _P, _P, _I64, _I64, _I64, _INT, _INT, _P, _SZ, _P],
+    "rlcs_gae_strided": [_P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I64, _F, _F, _INT, _P,
+                         _SZ, _P],
+    "rlcs_vtrace_strided": [_P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I64, _F, _F, _F,
+                            _INT, _P, _SZ, _P],
+    "rlcs_retrace_strided": [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I64, _F, _F,
+                             _F, _INT, _P, _SZ, _P],
+    "rlcs_td_lambda_strided": [_P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I64, _F, _F, _INT, _P,
+                               _SZ, _P],
+    "rlcs_discounted_strided": [_P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I64, _F, _INT, _P, _SZ,
+                                _P],
+    "rlcs_elig_trace_strided": [_P, _P, _P, _P, _I64, _I64, _I64, _I64, _F, _F, _INT, _P, _SZ, _P],
+    "rlcs_episodic_prefix_strided": [_P, _P, _P, _P, _I64, _I64, _I64, _I64, _INT, _INT, _P, _SZ,
+                                     _P],
     "rlcs_elig_trace_vec": [_P, _P, _P, _P, _I64, _I64, _I64, _F, _F, _INT, _P, _SZ, _P],
     "rlcs_workspace_size_columns": [_I64, _I64],
     "rlcs_gae_masked": [_P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _F, _F, _INT, _F, _INT, _P,

@@ -80,21 +80,32 @@ rlcs_status col_dispatch(Args& a, const ColGeom& g, rlcs_dtype dtype, bool has_t
     return hipGetLastError() == hipSuccess ? RLCS_OK : RLCS_ERR_LAUNCH;
 }
 
-// Time-major [T, ld] geometry (ld >= N; 0 means N): column n is environment n, flags laid out
-// like the data. Checks sizes, dtype, ld and alignment; fills `g`.
-inline rlcs_status check_time_major(int64_t N, int64_t T, int64_t& ld, rlcs_dtype dtype,
-                                    std::initializer_list<const void*> data,
-                                    std::initializer_list<const void*> outs, ColGeom& g) {
+// Strided [N, T] geometry: element (n, t) of every [N, T] array of the call (data, flags,
+// continuation values, outputs) at n * stride_n + t * stride_t, both strides >= 1 and one
+// dimension nested in the other (stride_n >= T * stride_t, or stride_t >= N * stride_n), so
+// that distinct (n, t) are distinct elements. Column n is environment n (one column per batch
+// row), its flags laid out like its data. `dense`: the plain row-major layout.
+inline rlcs_status check_strided(int64_t N, int64_t T, int64_t sn, int64_t st, rlcs_dtype dtype,
+                                 std::initializer_list<const void*> data,
+                                 std::initializer_list<const void*> outs, ColGeom& g, bool& dense) {
     if (N < 0 || T < 0) return RLCS_ERR_INVALID_ARG;
     if (dtype != RLCS_F32 && dtype != RLCS_BF16) return RLCS_ERR_DTYPE;
-    if (ld == 0) ld = N;
-    if (ld < N || T > kMaxT || (T > 0 && ld > INT64_MAX / T)) return RLCS_ERR_INVALID_ARG;
+    if (sn < 1 || st < 1 || T > kMaxT) return RLCS_ERR_INVALID_ARG;
+    if (N > 0 && T > 0) {
+        if ((N - 1) > INT64_MAX / sn || (T - 1) > INT64_MAX / st) return RLCS_ERR_INVALID_ARG;
+        const int64_t en = (N - 1) * sn, et = (T - 1) * st;
+        if (en > INT64_MAX - et) return RLCS_ERR_INVALID_ARG;
+        const bool rows_outer = T <= sn / st;   // sn >= T * st
+        const bool steps_outer = N <= st / sn;  // st >= N * sn
+        if (!rows_outer && !steps_outer) return RLCS_ERR_INVALID_ARG;
+    }
     const size_t es = dtype_size(dtype);
     for (const void* p : data)
         if (p && !aligned(p, es)) return RLCS_ERR_INVALID_ARG;
     for (const void* p : outs)
         if (p && !aligned(p, 4)) return RLCS_ERR_INVALID_ARG;
-    g = ColGeom{N, N > 0 ? N : 1, ld, 0, 0, 0, 1};
+    g = ColGeom{N, 1, st, sn, 0, 0, 1};
+    dense = st == 1 && sn == T;
     return RLCS_OK;
 }
 

@@ -1,5 +1,5 @@
 // Column-scan entry points of the forward recurrences (Table 1; Sections 3.3.5-3.3.6):
-// time-major eligibility traces and prefix sums, eligibility traces of F-vectors, and the
+// strided eligibility traces and prefix sums, eligibility traces of F-vectors, and the
 // workspace size of the column scans.
 #include "rlcs_columns_dispatch.h"
 
@@ -8,38 +8,48 @@ using namespace rlcs::host;
 
 extern "C" {
 
-rlcs_status rlcs_elig_trace_tm(const void* x, const uint8_t* term, const uint8_t* trunc, float* z,
-                               int64_t N, int64_t T, int64_t ld, float gamma, float lambda,
-                               rlcs_dtype dtype, void* ws, size_t ws_bytes, rlcs_stream_t stream) {
+rlcs_status rlcs_elig_trace_strided(const void* x, const uint8_t* term, const uint8_t* trunc,
+                                    float* z, int64_t N, int64_t T, int64_t stride_n,
+                                    int64_t stride_t, float gamma, float lambda, rlcs_dtype dtype,
+                                    void* ws, size_t ws_bytes, rlcs_stream_t stream) {
     ColGeom g;
-    rlcs_status st = check_time_major(N, T, ld, dtype, {x}, {z}, g);
+    bool dense;
+    rlcs_status st = check_strided(N, T, stride_n, stride_t, dtype, {x}, {z}, g, dense);
     if (st != RLCS_OK) return st;
     if (!unit_interval(gamma) || !unit_interval(lambda)) return RLCS_ERR_INVALID_ARG;
     if (N == 0 || T == 0) return RLCS_OK;
     if (!x || !z) return RLCS_ERR_INVALID_ARG;
+    if (dense) return rlcs_elig_trace(x, term, trunc, z, N, T, gamma, lambda, dtype, ws, ws_bytes, stream);
     Args a = make_args(N, T, gamma, lambda, 1.f, 1.f);
     a.in[0] = x;
     a.term = term; a.trunc = trunc;
     a.out0 = z;
+    if (stride_t == 1) return dispatch_strided_rows<ForwardOp<true, false>>(a, stride_n, dtype, trunc != nullptr, stream);
     return col_dispatch<ForwardOp<true, false>>(a, g, dtype, trunc != nullptr, ws, ws_bytes, stream);
 }
 
-rlcs_status rlcs_episodic_prefix_tm(const void* x, const uint8_t* term, const uint8_t* trunc,
-                                    float* c, int64_t N, int64_t T, int64_t ld,
-                                    rlcs_boundary boundary, rlcs_dtype dtype, void* ws,
-                                    size_t ws_bytes, rlcs_stream_t stream) {
+rlcs_status rlcs_episodic_prefix_strided(const void* x, const uint8_t* term, const uint8_t* trunc,
+                                         float* c, int64_t N, int64_t T, int64_t stride_n,
+                                         int64_t stride_t, rlcs_boundary boundary,
+                                         rlcs_dtype dtype, void* ws, size_t ws_bytes,
+                                         rlcs_stream_t stream) {
     ColGeom g;
-    rlcs_status st = check_time_major(N, T, ld, dtype, {x}, {c}, g);
+    bool dense;
+    rlcs_status st = check_strided(N, T, stride_n, stride_t, dtype, {x}, {c}, g, dense);
     if (st != RLCS_OK) return st;
     if (boundary != RLCS_ENDS_AT && boundary != RLCS_STARTS_AT) return RLCS_ERR_INVALID_ARG;
     if (N == 0 || T == 0) return RLCS_OK;
     if (!x || !c) return RLCS_ERR_INVALID_ARG;
+    if (dense) return rlcs_episodic_prefix(x, term, trunc, c, N, T, boundary, dtype, ws, ws_bytes, stream);
     Args a = make_args(N, T, 1.f, 1.f, 1.f, 1.f);
     a.in[0] = x;
     a.term = term; a.trunc = trunc;
     a.out0 = c;
-    if (boundary == RLCS_STARTS_AT)
+    if (boundary == RLCS_STARTS_AT) {
+        if (stride_t == 1) return dispatch_strided_rows<ForwardOp<false, true>>(a, stride_n, dtype, trunc != nullptr, stream);
         return col_dispatch<ForwardOp<false, true>>(a, g, dtype, trunc != nullptr, ws, ws_bytes, stream);
+    }
+    if (stride_t == 1) return dispatch_strided_rows<ForwardOp<false, false>>(a, stride_n, dtype, trunc != nullptr, stream);
     return col_dispatch<ForwardOp<false, false>>(a, g, dtype, trunc != nullptr, ws, ws_bytes, stream);
 }
 

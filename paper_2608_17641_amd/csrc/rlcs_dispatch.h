@@ -186,11 +186,45 @@ rlcs_status dispatch(Args& a, rlcs_dtype dtype, bool has_trunc, void* ws, size_t
     return dispatch_dt<Op, float>(a, has_trunc, ws, ws_bytes, s);
 }
 
+// Rows with a row stride (period) above T: the rows kernel over the positions n * period + t,
+// element-wise (the steps t >= T of each period are skipped), whole rows per workgroup.
+template <class Op>
+rlcs_status dispatch_strided_rows(Args& a, int64_t period, rlcs_dtype dtype, bool has_trunc,
+                                  rlcs_stream_t stream) {
+    if (a.N == 0 || a.T == 0) return RLCS_OK;
+    if (period > kMaxT) return RLCS_ERR_INVALID_ARG;
+    a.period = period;
+    a.inv_period = 1.f / float(period);
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    auto run = [&](auto dt_tag) -> rlcs_status {
+        using DT = decltype(dt_tag);
+        constexpr int K = Width<DT>::K;
+        Plan p{};
+        p.split = false;
+        const int64_t E_small = int64_t(kSmallWaves) * kWave * K;
+        p.waves = (period <= E_small) ? kSmallWaves : kLargeWaves;
+        const int64_t E = int64_t(p.waves) * kWave * K;
+        const int64_t slack = (period % K == 0) ? 0 : K - 1;
+        p.rows_per_wg = (period <= E - slack) ? (E - slack) / period : 1;
+        if ((a.N + p.rows_per_wg - 1) / p.rows_per_wg > INT32_MAX) return RLCS_ERR_INVALID_ARG;
+        p.wave_local = 0;
+        p.lds_bytes = 0;
+        if constexpr (Op::kFlags) {
+            if (has_trunc) return launch<Op, DT, false, true>(a, p, s);
+        }
+        return launch<Op, DT, false, false>(a, p, s);
+    };
+    if (dtype == RLCS_BF16) return run(bf16_t{});
+    return run(float{});
+}
+
 inline Args make_args(int64_t N, int64_t T, float gamma, float lambda, float rho_bar, float c_bar) {
     Args a{};
     a.N = N;
     a.T = T;
     a.inv_T = T > 0 ? 1.f / float(T) : 0.f;
+    a.period = T;
+    a.inv_period = a.inv_T;
     a.p = Params{gamma, lambda, rho_bar, c_bar};
     return a;
 }

@@ -41,6 +41,11 @@ struct Args {
     Params p;
     int64_t N, T;
     float inv_T;           // 1 / T in fp32 (row bookkeeping)
+    // Positions of the rows kernel: row n's step t at n * period + t (period = T for dense
+    // rows; a row stride above T for strided rows, whose steps t >= T are not part of the
+    // call and are neither read nor written).
+    int64_t period;
+    float inv_period;
     void* ws;              // cross-workgroup carry records (split-row variant only)
 };
 

@@ -227,32 +227,37 @@ struct Chunk {
         for (int k = 0; k < K; ++k) B[k] = (k == ke_) ? rv : 0.f;
     }
 
-    // Step 1 for a chunk with steps outside [lo, hi): element-wise, masked.
+    // Step 1 for a chunk with steps outside [lo, hi), or rows with a period above T (their
+    // positions t >= T are skipped): element-wise, masked.
     template <class BaseFn, class PreFn>
     __device__ void load_masked(const Args& a, int64_t lo, int64_t hi, BaseFn&& base_of, int lane,
                                 float (&nraw)[Op::kNbrRaw], PreFn&& pre) {
-        const int64_t T = a.T;
+        const int64_t T = a.T, Pd = a.period;
         pre();
-        valid = 0;
+        uint32_t inrange = 0;
 #pragma unroll
         for (int k = 0; k < K; ++k)
-            if (p0 + k >= lo && p0 + k < hi) valid |= 1u << k;
+            if (p0 + k >= lo && p0 + k < hi) inrange |= 1u << k;
+        valid = 0;
         edge = 0;
 #pragma unroll
         for (int k = 0; k < K; ++k) B[k] = 0.f;
-        if (valid) {
-            const int64_t first = p0 + __builtin_ctz(valid);
+        if (inrange) {
+            const int64_t first = p0 + __builtin_ctz(inrange);
             int64_t row, t;
-            row_and_step(base_of(), first, T, a.inv_T, row, t);
+            row_and_step(base_of(), first, Pd, a.inv_period, row, t);
 #pragma unroll
             for (int k = 0; k < K; ++k) {
-                if (p0 + k < first || !bit(valid, k)) continue;
-                const bool e = kBack ? (t == T - 1) : (t == 0);
-                if (e) {
-                    edge |= 1u << k;
-                    if (Op::kRowValue && a.row_value) B[k] = load_one<DT>(a.row_value, row);
+                if (p0 + k < first || !bit(inrange, k)) continue;
+                if (t < T) {
+                    valid |= 1u << k;
+                    const bool e = kBack ? (t == T - 1) : (t == 0);
+                    if (e) {
+                        edge |= 1u << k;
+                        if (Op::kRowValue && a.row_value) B[k] = load_one<DT>(a.row_value, row);
+                    }
                 }
-                if (++t == T) { t = 0; ++row; }
+                if (++t == Pd) { t = 0; ++row; }
             }
         }
         term = 0; trunc = 0;
@@ -537,8 +542,8 @@ __global__ void __launch_bounds__(W * kWave) rows_kernel(Args a, int64_t rows_pe
     const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
     const int64_t row_lo = int64_t(blockIdx.x) * rows_per_wg;
     const int64_t row_hi = min(row_lo + rows_per_wg, a.N);
-    const int64_t lo = row_lo * a.T, hi = row_hi * a.T;
-    const bool can_full = VEC && a.T >= K;
+    const int64_t lo = row_lo * a.period, hi = row_hi * a.period;
+    const bool can_full = VEC && a.T >= K && a.period == a.T;
     float carry = 0.f;
     auto carry_of = [&]() { return carry; };
     extern __shared__ __align__(16) float s_dyn[];  // staged policies only (sized at launch)

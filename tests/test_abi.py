@@ -159,39 +159,42 @@ def test_column_workspace_size(lib):
     assert lib.rlcs_workspace_size_columns(2 ** 62, 2 ** 30) == 0  # overflows
 
 
-def gae_tm(lib, **kw):
+def gae_strided(lib, **kw):
     a = dict(r=FAKE, v=FAKE, term=None, trunc=None, bv=None, boot=None, adv=FAKE2, ret=None,
-             N=4, T=8, ld=0, gamma=0.99, lam=0.95, dtype=0, ws=None, ws_bytes=0, stream=None)
+             N=4, T=8, sn=1, st=4, gamma=0.99, lam=0.95, dtype=0, ws=None, ws_bytes=0, stream=None)
     a.update(kw)
-    return lib.rlcs_gae_tm(*a.values())
+    return lib.rlcs_gae_strided(*a.values())
 
 
-def test_time_major_validation(lib):
+def test_strided_validation(lib):
     from paper_2608_17641_amd import _native as n
-    assert gae_tm(lib, N=-1) == n.RLCS_ERR_INVALID_ARG
-    assert gae_tm(lib, T=-1) == n.RLCS_ERR_INVALID_ARG
-    assert gae_tm(lib, ld=3) == n.RLCS_ERR_INVALID_ARG       # ld < N
-    assert gae_tm(lib, ld=-5) == n.RLCS_ERR_INVALID_ARG
-    assert gae_tm(lib, T=2 ** 30 + 1) == n.RLCS_ERR_INVALID_ARG
-    assert gae_tm(lib, T=2 ** 30, ld=2 ** 40) == n.RLCS_ERR_INVALID_ARG  # T*ld overflows
-    assert gae_tm(lib, dtype=5) == n.RLCS_ERR_DTYPE
-    assert gae_tm(lib, r=None) == n.RLCS_ERR_INVALID_ARG
-    assert gae_tm(lib, trunc=FAKE) == n.RLCS_ERR_INVALID_ARG
-    assert gae_tm(lib, r=MISALIGNED) == n.RLCS_ERR_INVALID_ARG
-    assert gae_tm(lib, gamma=1.5) == n.RLCS_ERR_INVALID_ARG
-    assert gae_tm(lib, N=0) == n.RLCS_OK and gae_tm(lib, T=0) == n.RLCS_OK
-    assert lib.rlcs_vtrace_tm(FAKE, FAKE, FAKE, None, None, None, None, FAKE2, None, 4, 8, 0,
-                              0.99, 0.0, 1.0, 0, None, 0, None) == n.RLCS_ERR_INVALID_ARG
-    assert lib.rlcs_retrace_tm(FAKE, FAKE, None, FAKE, None, None, None, None, FAKE2, None, 4, 8,
-                               0, 0.99, 0.95, 1.0, 0, None, 0, None) == n.RLCS_ERR_INVALID_ARG
-    assert lib.rlcs_td_lambda_tm(FAKE, FAKE, None, None, None, None, FAKE2, 4, 8, 2, 0.99, 0.95,
-                                 0, None, 0, None) == n.RLCS_ERR_INVALID_ARG
-    assert lib.rlcs_discounted_tm(FAKE, None, FAKE, None, None, FAKE2, 4, 8, 0, 0.99, 0, None, 0,
-                                  None) == n.RLCS_ERR_INVALID_ARG
-    assert lib.rlcs_elig_trace_tm(FAKE, None, None, FAKE2, 4, 8, 0, 0.99, math.nan, 0, None, 0,
-                                  None) == n.RLCS_ERR_INVALID_ARG
-    assert lib.rlcs_episodic_prefix_tm(FAKE, None, None, FAKE2, 4, 8, 0, 9, 0, None, 0,
-                                       None) == n.RLCS_ERR_INVALID_ARG
+    assert gae_strided(lib, N=-1) == n.RLCS_ERR_INVALID_ARG
+    assert gae_strided(lib, T=-1) == n.RLCS_ERR_INVALID_ARG
+    assert gae_strided(lib, st=3) == n.RLCS_ERR_INVALID_ARG           # time-major ld < N
+    assert gae_strided(lib, sn=7, st=1) == n.RLCS_ERR_INVALID_ARG     # row stride < T
+    assert gae_strided(lib, sn=2, st=2) == n.RLCS_ERR_INVALID_ARG     # dimensions interleave
+    assert gae_strided(lib, sn=0) == n.RLCS_ERR_INVALID_ARG
+    assert gae_strided(lib, st=-4) == n.RLCS_ERR_INVALID_ARG
+    assert gae_strided(lib, T=2 ** 30 + 1) == n.RLCS_ERR_INVALID_ARG
+    assert gae_strided(lib, T=2 ** 30, st=2 ** 40) == n.RLCS_ERR_INVALID_ARG  # offsets overflow
+    assert gae_strided(lib, dtype=5) == n.RLCS_ERR_DTYPE
+    assert gae_strided(lib, r=None) == n.RLCS_ERR_INVALID_ARG
+    assert gae_strided(lib, trunc=FAKE) == n.RLCS_ERR_INVALID_ARG
+    assert gae_strided(lib, r=MISALIGNED) == n.RLCS_ERR_INVALID_ARG
+    assert gae_strided(lib, gamma=1.5) == n.RLCS_ERR_INVALID_ARG
+    assert gae_strided(lib, N=0) == n.RLCS_OK and gae_strided(lib, T=0) == n.RLCS_OK
+    assert lib.rlcs_vtrace_strided(FAKE, FAKE, FAKE, None, None, None, None, FAKE2, None, 4, 8, 8,
+                                   1, 0.99, 0.0, 1.0, 0, None, 0, None) == n.RLCS_ERR_INVALID_ARG
+    assert lib.rlcs_retrace_strided(FAKE, FAKE, None, FAKE, None, None, None, None, FAKE2, None, 4,
+                                    8, 1, 4, 0.99, 0.95, 1.0, 0, None, 0, None) == n.RLCS_ERR_INVALID_ARG
+    assert lib.rlcs_td_lambda_strided(FAKE, FAKE, None, None, None, None, FAKE2, 4, 8, 1, 2, 0.99,
+                                      0.95, 0, None, 0, None) == n.RLCS_ERR_INVALID_ARG
+    assert lib.rlcs_discounted_strided(FAKE, None, FAKE, None, None, FAKE2, 4, 8, 1, 4, 0.99, 0,
+                                       None, 0, None) == n.RLCS_ERR_INVALID_ARG
+    assert lib.rlcs_elig_trace_strided(FAKE, None, None, FAKE2, 4, 8, 1, 4, 0.99, math.nan, 0,
+                                       None, 0, None) == n.RLCS_ERR_INVALID_ARG
+    assert lib.rlcs_episodic_prefix_strided(FAKE, None, None, FAKE2, 4, 8, 1, 4, 9, 0, None, 0,
+                                            None) == n.RLCS_ERR_INVALID_ARG
 
 
 def test_elig_trace_vec_validation(lib):

@@ -46,30 +46,38 @@ TM_ESTIMATORS = ("gae", "vtrace", "retrace", "td_lambda", "discounted", "elig_tr
                  "prefix_ends", "prefix_starts")
 
 
-def run_tm(name, d, *, trunc=True, boot=True, ws=None):
+def run_strided(name, d, *, trunc=True, boot=True, ws=None):
+    """Estimator `name` on [N, T] views `d` of any layout, through the strided entry points."""
     tr = d["trunc"] if trunc else None
     bv = d["bv"] if trunc else None
     bt = d["boot"] if boot else None
     if name == "gae":
-        a, b = rl.rlcs_gae_tm(d["r"], d["v"], d["term"], tr, bv, bt, gamma=G, lam=L, ws=ws)
+        a, b = rl.rlcs_gae_strided(d["r"], d["v"], d["term"], tr, bv, bt, gamma=G, lam=L, ws=ws)
         return {"adv": a, "ret": b}
     if name == "vtrace":
-        a, b = rl.rlcs_vtrace_tm(d["r"], d["v"], d["log_rho"], d["term"], tr, bv, bt, gamma=G,
-                                 rho_bar=1.0, c_bar=0.9, ws=ws)
+        a, b = rl.rlcs_vtrace_strided(d["r"], d["v"], d["log_rho"], d["term"], tr, bv, bt, gamma=G,
+                                      rho_bar=1.0, c_bar=0.9, ws=ws)
         return {"vs": a, "pg": b}
     if name == "retrace":
-        a, b = rl.rlcs_retrace_tm(d["r"], d["q"], d["eq"], d["log_rho"], d["term"], tr, bv, bt,
-                                  gamma=G, lam=L, c_bar=1.0, ws=ws)
+        a, b = rl.rlcs_retrace_strided(d["r"], d["q"], d["eq"], d["log_rho"], d["term"], tr, bv, bt,
+                                       gamma=G, lam=L, c_bar=1.0, ws=ws)
         return {"delta": a, "q_ret": b}
     if name == "td_lambda":
-        return {"ret": rl.rlcs_td_lambda_tm(d["r"], d["v"], d["term"], tr, bv, bt, gamma=G, lam=L,
-                                            ws=ws)}
+        return {"ret": rl.rlcs_td_lambda_strided(d["r"], d["v"], d["term"], tr, bv, bt, gamma=G,
+                                                 lam=L, ws=ws)}
     if name == "discounted":
-        return {"ret": rl.rlcs_discounted_tm(d["r"], d["term"], tr, bv, bt, gamma=G, ws=ws)}
+        return {"ret": rl.rlcs_discounted_strided(d["r"], d["term"], tr, bv, bt, gamma=G, ws=ws)}
     if name == "elig_trace":
-        return {"z": rl.rlcs_elig_trace_tm(d["x"], d["term"], tr, gamma=G, lam=L, ws=ws)}
+        return {"z": rl.rlcs_elig_trace_strided(d["x"], d["term"], tr, gamma=G, lam=L, ws=ws)}
     b = "starts_at" if name == "prefix_starts" else "ends_at"
-    return {"c": rl.rlcs_episodic_prefix_tm(d["x"], d["term"], tr, boundary=b, ws=ws)}
+    return {"c": rl.rlcs_episodic_prefix_strided(d["x"], d["term"], tr, boundary=b, ws=ws)}
+
+
+def run_tm(name, d, *, trunc=True, boot=True, ws=None):
+    """Time-major [T, N] tensors in `d`: passed as their [N, T] transposes; outputs [T, N]."""
+    dt = {k: (v.t() if v.dim() == 2 else v) for k, v in d.items()}
+    out = run_strided(name, dt, trunc=trunc, boot=boot, ws=ws)
+    return {k: (None if v is None else v.t()) for k, v in out.items()}
 
 
 def ref_tm(name, ro, *, trunc=True, boot=True):
@@ -135,7 +143,7 @@ def test_time_major_bf16_plain_and_strided(v):
                 assert_parity(out, ref_tm(name, ro), TOL["bf16"], label=f"tm bf16 {name} ld={ld}")
                 if ld is not None:
                     for o in out.values():
-                        assert o.stride() == (ld, 1)
+                        assert o.stride() == (ld, 1)  # [T, N] view of [T, ld] storage
             for name in ("gae", "discounted", "elig_trace"):
                 out = run_tm(name, d, trunc=False, boot=False, ws=ws)
                 torch.cuda.synchronize()
@@ -150,8 +158,8 @@ def test_time_major_strided_padding_untouched():
     d = device_tm(ro, ld)
     adv_buf = torch.full((T, ld), -3.0, device=DEV)
     ret_buf = torch.full((T, ld), -4.0, device=DEV)
-    rl.rlcs_gae_tm(d["r"], d["v"], d["term"], d["trunc"], d["bv"], d["boot"], adv_buf[:, :N],
-                   ret_buf[:, :N], gamma=G, lam=L)
+    rl.rlcs_gae_strided(d["r"].t(), d["v"].t(), d["term"].t(), d["trunc"].t(), d["bv"].t(),
+                        d["boot"], adv_buf[:, :N].t(), ret_buf[:, :N].t(), gamma=G, lam=L)
     torch.cuda.synchronize()
     assert torch.all(adv_buf[:, N:] == -3.0) and torch.all(ret_buf[:, N:] == -4.0)
     assert_parity({"adv": adv_buf[:, :N], "ret": ret_buf[:, :N]}, ref_tm("gae", ro), TOL["f32"],
@@ -177,15 +185,15 @@ def test_time_major_deterministic_and_workspace_reuse():
     d = device_tm(ro)
     ws = rl.make_workspace_columns(4 * N, 2 * T, DEV)
     with variant(2):
-        a1, _ = rl.rlcs_gae_tm(d["r"], d["v"], d["term"], d["trunc"], d["bv"], d["boot"], gamma=G,
-                               lam=L, ws=ws)
+        a1, _ = rl.rlcs_gae_strided(d["r"].t(), d["v"].t(), d["term"].t(), d["trunc"].t(),
+                                    d["bv"].t(), d["boot"], gamma=G, lam=L, ws=ws)
         for T2, N2 in ((37, 3), (999, 200), (64, 64)):
             ro2 = workloads.make_rollout_time_major(T2, N2, seed=T2)
             out = run_tm("vtrace", device_tm(ro2), ws=ws)
             torch.cuda.synchronize()
             assert_parity(out, ref_tm("vtrace", ro2), TOL["f32"], label=f"reuse {T2}x{N2}")
-        a2, _ = rl.rlcs_gae_tm(d["r"], d["v"], d["term"], d["trunc"], d["bv"], d["boot"], gamma=G,
-                               lam=L, ws=ws)
+        a2, _ = rl.rlcs_gae_strided(d["r"].t(), d["v"].t(), d["term"].t(), d["trunc"].t(),
+                                    d["bv"].t(), d["boot"], gamma=G, lam=L, ws=ws)
         torch.cuda.synchronize()
     assert torch.equal(a1, a2)
     assert int(ws[8:12].view(torch.int32).item()) == 0
@@ -274,3 +282,40 @@ def test_workspace_shared_by_row_major_and_column_calls():
             torch.cuda.synchronize()
             assert_parity(out, oracle_run("elig_trace", ro4), TOL["f32"], label=f"row-major elig {rnd}")
     assert int(ws[8:12].view(torch.int32).item()) == 0
+
+
+def strided_rows(t, ld):
+    """`t` [N, T] copied into the first T steps of [N, ld] rows (a view with stride (ld, 1))."""
+    buf = torch.full((t.shape[0], ld), 5, dtype=t.dtype, device=t.device)
+    buf[:, : t.shape[1]] = t
+    return buf[:, : t.shape[1]]
+
+
+@pytest.mark.parametrize("v", [0, 1, 2])
+@pytest.mark.parametrize("N,T,ld", [(1, 1, 3), (9, 33, 40), (100, 256, 300), (5, 1000, 1001)])
+def test_strided_rows_every_estimator(N, T, ld, v):
+    """Row-major rows with a row stride above T (the first T steps of wider rows)."""
+    ro = workloads.make_rollout(N, T, seed=N + T, p_term=0.05, p_trunc=0.05)
+    d = {k: (strided_rows(to_device(a, DEV), ld) if a.ndim == 2 else to_device(a, DEV))
+         for k, a in ro.items()}
+    ws = rl.make_workspace_columns(N, T, DEV)
+    from cases import oracle_run
+    with variant(v):
+        for name in TM_ESTIMATORS:
+            out = run_strided(name, d, ws=ws)
+            torch.cuda.synchronize()
+            for o in out.values():
+                assert o.stride() == (ld, 1) or T == 1
+            assert_parity(out, oracle_run(name, ro, gamma=G, lam=L, c_bar=1.0 if name != "vtrace" else 0.9),
+                          TOL["f32"], label=f"strided rows {name} {N}x{T} ld={ld} v={v}")
+
+
+def test_strided_dense_layout_runs_the_row_major_path():
+    """stride (T, 1) is the plain row-major layout: same results as the row-major entry point,
+    bit for bit."""
+    ro = workloads.make_rollout(64, 300, seed=3)
+    d = {k: to_device(a, DEV) for k, a in ro.items()}
+    a1, r1 = rl.rlcs_gae_strided(d["r"], d["v"], d["term"], d["trunc"], d["bv"], d["boot"], gamma=G, lam=L)
+    a2, r2 = rl.rlcs_gae(d["r"], d["v"], d["term"], d["trunc"], d["bv"], d["boot"], gamma=G, lam=L)
+    torch.cuda.synchronize()
+    assert torch.equal(a1, a2) and torch.equal(r1, r2)
