@@ -105,14 +105,16 @@ rlcs_status launch(const Args& a, const Plan& p, hipStream_t stream) {
     return hipGetLastError() == hipSuccess ? RLCS_OK : RLCS_ERR_LAUNCH;
 }
 
-// LDS bytes of a staged policy's chunk with W waves: the staged slots plus the two
-// [steps, A] slices.
+// LDS bytes of a staged policy's chunk with W waves: the larger of the two [steps, A] slices and
+// the staged slots, which reuse the slices' bytes once they are reduced.
 template <class Op, typename DT>
 constexpr int64_t staged_lds_bytes(int W, int64_t A) {
     const int64_t E = int64_t(W) * kWave * Width<DT>::K;
     const int64_t per_block = 16 / int64_t(sizeof(DT));
     const int64_t cap = ((E + 1) * A + 3 * per_block) / per_block * per_block;  // see stage_chunk
-    return int64_t(sizeof(float)) * Op::kStaged * (E + 4) + 2 * cap * int64_t(sizeof(DT));
+    const int64_t slots = int64_t(sizeof(float)) * Op::kStaged * (E + 4);
+    const int64_t slices = 2 * cap * int64_t(sizeof(DT));
+    return slots > slices ? slots : slices;
 }
 
 template <class Op, typename DT>

@@ -412,8 +412,9 @@ __device__ __forceinline__ float run_chunk(C& c, const Args& a, int64_t chunk_lo
 // tid, tid + blockDim, ...) reduces its slices into the Op::kStaged staged slots. The caller
 // synchronises before the slots are read.
 //
-// Layout of `dyn` (16-byte aligned): kStaged slots of E + 4 floats, then the two slices as DT,
-// `cap` elements each (the size staged_lds_bytes on the host assumes). With 16-byte aligned
+// Layout of `dyn` (16-byte aligned): the two slices as DT, `cap` elements each, and, over the
+// same bytes once the slices are reduced, kStaged slots of E + 4 floats (the larger of the two is
+// the size staged_lds_bytes on the host assumes). With 16-byte aligned
 // tensors the 16-byte blocks covering a slice go straight from global memory to LDS
 // (global_load_lds_dwordx4: lane l of a wave fills the 16 bytes at the wave-uniform LDS
 // address plus 16*l), with no register round trip and every block of the chunk in flight at
@@ -424,7 +425,6 @@ template <class Op, typename DT, int E, int J>
 struct Stager {
     static constexpr int64_t kPerBlock = 16 / int64_t(sizeof(DT));
     static constexpr int kStride = E + 4;
-    static_assert((Op::kStaged * kStride * sizeof(float)) % 16 == 0, "slices must be 16-byte aligned");
     int32_t act[J];
     float mu[J];
     int64_t s_lo, s_hi;      // staged steps
@@ -467,7 +467,7 @@ struct Stager {
         el_copy = max(el_lo, (blk_lo + nfull) * kPerBlock);
         const u32x4* gq = reinterpret_cast<const u32x4*>(a.in[1]) + blk_lo;
         const u32x4* gp = reinterpret_cast<const u32x4*>(a.in[2]) + blk_lo;
-        u32x4* lq = reinterpret_cast<u32x4*>(dyn + Op::kStaged * kStride);
+        u32x4* lq = reinterpret_cast<u32x4*>(dyn);
         u32x4* lp = lq + cap(A) / kPerBlock;
         const int lane = tid & (kWave - 1);
         for (int64_t b0 = tid - lane; b0 < nfull; b0 += nt) {
@@ -481,7 +481,7 @@ struct Stager {
     __device__ __forceinline__ void commit(const Args& a, int64_t chunk_lo, float* dyn) {
         const int64_t A = a.A;
         const int nt = blockDim.x, tid = threadIdx.x;
-        DT* sq = reinterpret_cast<DT*>(dyn + Op::kStaged * kStride);
+        DT* sq = reinterpret_cast<DT*>(dyn);
         DT* sp = sq + cap(A);
         const DT* gq = reinterpret_cast<const DT*>(a.in[1]);
         const DT* gp = reinterpret_cast<const DT*>(a.in[2]);
@@ -504,18 +504,24 @@ struct Stager {
         __syncthreads();
         // rows are 16-byte aligned whole blocks in LDS when A is a multiple of a block
         const bool rows16 = a.stage_vec && A % kPerBlock == 0;
+        float v[J][Op::kStaged];
+#pragma unroll
+        for (int j = 0; j < J; ++j) {
+            const int64_t i = tid + int64_t(j) * nt;
+            const int64_t st = chunk_lo + i;
+#pragma unroll
+            for (int q = 0; q < Op::kStaged; ++q) v[j][q] = 0.f;
+            if (i <= E && st >= s_lo && st < s_hi)
+                Op::template reduce_step<DT>(sq + (st * A - e0), sp + (st * A - e0), A, rows16, act[j], mu[j], v[j]);
+        }
+        // the slots overlay the slices: every slice read is done before any slot is written
+        __syncthreads();
 #pragma unroll
         for (int j = 0; j < J; ++j) {
             const int64_t i = tid + int64_t(j) * nt;
             if (i > E) continue;
-            const int64_t st = chunk_lo + i;
-            float v[Op::kStaged];
 #pragma unroll
-            for (int q = 0; q < Op::kStaged; ++q) v[q] = 0.f;
-            if (st >= s_lo && st < s_hi)
-                Op::template reduce_step<DT>(sq + (st * A - e0), sp + (st * A - e0), A, rows16, act[j], mu[j], v);
-#pragma unroll
-            for (int q = 0; q < Op::kStaged; ++q) dyn[q * kStride + i] = v[q];
+            for (int q = 0; q < Op::kStaged; ++q) dyn[q * kStride + i] = v[j][q];
         }
     }
 };
