@@ -63,7 +63,12 @@ def parse():
                     help="print per-kernel durations of a rocprofv3 --kernel-trace run and exit")
     ap.add_argument("--profile-pass", action="store_true",
                     help="eager launches of the timed kernel plus a plain copy of known size, "
-                         "for rocprofv3 runs (no JSON line)")
+                         "for rocprofv3 runs (no JSON line); with --extra, of every workload")
+    ap.add_argument("--manifest", default="",
+                    help="with --extra --profile-pass: write the workload list (JSON) here")
+    ap.add_argument("--summarize-extra", nargs=4, metavar=("TRACE_DIR", "FETCH_DIR", "WRITE_DIR", "MANIFEST"),
+                    help="per-workload kernel durations and HBM traffic of three rocprofv3 runs of "
+                         "--extra --profile-pass (kernel trace, FETCH_SIZE, WRITE_SIZE) and exit")
     return ap.parse_args()
 
 
@@ -130,20 +135,35 @@ def _rocpd(path):
     return sqlite3.connect(dbs[0])
 
 
+def _is_copy(name):
+    return "copyBuffer" in name or "copy_kernel" in name
+
+
+def _calibration_kib(rows, counter):
+    """Mean counter value of the calibration copies of COPY_BYTES: the copy dispatches that end
+    a profile pass (rows are (dispatch_id, kernel name, value) in dispatch order)."""
+    tail = []
+    for _, name, val in reversed(rows):
+        if not _is_copy(name):
+            break
+        tail.append(val)
+    if not tail:
+        raise SystemExit(f"{counter}: no calibration copy at the end of the run")
+    return statistics.mean(tail)
+
+
 def summarize_counters(fetch_dir, write_dir):
     """Counter summary (FETCH_SIZE, WRITE_SIZE per dispatch of the timed kernel, each scaled by
     the same counter on a plain device copy of COPY_BYTES) in the committed format."""
     out = {}
     for counter, path in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
         cur = _rocpd(path).cursor()
-        rows = cur.execute("select kernel_name, value, grid_size from counters_collection "
-                           "where counter_name = ?", (counter,)).fetchall()
-        mine = [v for n, v, g in rows if KERNEL_TAG in n]
-        # the copy of COPY_BYTES is the largest copy dispatch in the run
-        copies = [(g, v) for n, v, g in rows if "copyBuffer" in n or "copy_kernel" in n]
-        if not mine or not copies:
-            raise SystemExit(f"{counter}: kernel or calibration copy not found in {path}")
-        copy_kib = max(copies)[1]
+        rows = cur.execute("select dispatch_id, kernel_name, value from counters_collection "
+                           "where counter_name = ? order by dispatch_id", (counter,)).fetchall()
+        mine = [v for _, n, v in rows if KERNEL_TAG in n]
+        if not mine:
+            raise SystemExit(f"{counter}: kernel not found in {path}")
+        copy_kib = _calibration_kib(rows, counter)
         out[counter] = (statistics.mean(mine), len(mine), copy_kib, (COPY_BYTES / 1024) / copy_kib)
     fetch, write = out["FETCH_SIZE"], out["WRITE_SIZE"]
     traffic = int(round((fetch[0] * fetch[3] + write[0] * write[3]) * 1024))
@@ -183,6 +203,71 @@ def summarize_trace(trace_dir):
         v.sort()
         print(f"{n[:70]:<70} {len(v):>6} {statistics.mean(v):>8.3f} {v[len(v) // 2]:>9.3f} "
               f"{v[0]:>7.3f} {v[-1]:>8.3f}")
+
+
+def _blocks(path, value_col):
+    """The library's dispatches of a --extra --profile-pass run, in launch order, between each
+    pair of markers: a list of [(kernel name, value)] per block. `value_col` is 'duration'
+    (kernel trace, ns) or a counter name (counter run, per dispatch)."""
+    cur = _rocpd(path).cursor()
+    if value_col == "duration":
+        rows = cur.execute("select dispatch_id, name, duration from kernels order by dispatch_id").fetchall()
+    else:
+        rows = cur.execute("select dispatch_id, kernel_name, value from counters_collection "
+                           "where counter_name = ? order by dispatch_id", (value_col,)).fetchall()
+    blocks, inside = [], False
+    for _, name, val in rows:
+        if MARKER_KERNEL in name:
+            inside = not inside
+            if inside:
+                blocks.append([])
+        elif "rlcs::" in name and inside:
+            blocks[-1].append((name, val))
+    if inside:
+        raise SystemExit(f"{path}: unmatched block marker")
+    return blocks, rows
+
+
+def _copy_scale(rows, counter):
+    return (COPY_BYTES / 1024) / _calibration_kib(rows, counter)
+
+
+def _short(name):
+    name = name.replace("rlcs::", "").replace("void ", "")
+    return name.split("(")[0][:44]
+
+
+def summarize_extra(trace_dir, fetch_dir, write_dir, manifest):
+    """Per workload: each library kernel's average duration (kernel trace) and its HBM bytes
+    per call (FETCH_SIZE and WRITE_SIZE, scaled by the same counters on a plain copy of
+    COPY_BYTES), against the dense algorithmic bytes."""
+    man = json.load(open(manifest))
+    trace, _ = _blocks(trace_dir, "duration")
+    fetch, frows = _blocks(fetch_dir, "FETCH_SIZE")
+    write, wrows = _blocks(write_dir, "WRITE_SIZE")
+    fs, ws = _copy_scale(frows, "FETCH_SIZE"), _copy_scale(wrows, "WRITE_SIZE")
+    for what, b in (("trace", trace), ("FETCH_SIZE", fetch), ("WRITE_SIZE", write)):
+        if len(b) != len(man):
+            raise SystemExit(f"{what}: {len(b)} marked blocks, manifest lists {len(man)}")
+    print(f"FETCH_SIZE_scale: {fs:.4f}\nWRITE_SIZE_scale: {ws:.4f}")
+    print(f"{'workload':<18} {'estimator':<16} {'kernel':<44} {'avg_us':>8} {'GB/s':>7} {'%peak':>6} "
+          f"{'traffic_B':>11} {'alg_B':>11} {'ratio':>6}")
+    for m, tb, fb, wb in zip(man, trace, fetch, write):
+        calls = m["calls"]
+        kinds = sorted({n for n, _ in tb}, key=[n for n, _ in tb].index)
+        per_call_us = sum(v for _, v in tb) / 1e3 / calls
+        traffic = (sum(v for _, v in fb) * fs + sum(v for _, v in wb) * ws) * 1024 / calls
+        for k in kinds:
+            d = [v / 1e3 for n, v in tb if n == k]
+            f = [v for n, v in fb if n == k]
+            w = [v for n, v in wb if n == k]
+            kt = (statistics.mean(f) * fs + statistics.mean(w) * ws) * 1024
+            print(f"{m['label']:<18} {m['name']:<16} {_short(k):<44} {statistics.mean(d):>8.3f} "
+                  f"{'':>7} {'':>6} {kt:>11.0f} {'':>11} {'':>6}")
+        gbs = m["bytes"] / (per_call_us * 1e-6) / 1e9
+        print(f"{m['label']:<18} {m['name']:<16} {'(per call)':<44} {per_call_us:>8.3f} {gbs:>7.0f} "
+              f"{100 * gbs / PEAK_HBM_GBS:>5.1f}% {traffic:>11.0f} {m['bytes']:>11} "
+              f"{traffic / m['bytes']:>6.3f}")
 
 
 def profile_pass(step, args, dev):
@@ -308,25 +393,8 @@ def run_extra(dev, only=""):
             if rel > (1e-3 if dt == "bf16" else 1e-5):
                 raise SystemExit(f"parity failure in {label} {name}: {rel}")
             nbytes = extra_bytes(name, n_, t_, eb, trunc, boot)
-            est_us = max(2.0, nbytes / 5e3)
-            K = int(max(20, min(2000, 20000 / est_us)))
-            for i in range(3):
-                call(name, sets[i % S], ws, gamma, lam, trunc, boot)
-            torch.cuda.synchronize()
-            graph = torch.cuda.CUDAGraph()
-            with torch.cuda.graph(graph):
-                for i in range(K):
-                    call(name, sets[i % S], ws, gamma, lam, trunc, boot)
-            graph.replay()
-            torch.cuda.synchronize()
-            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            a.record(); graph.replay(); b.record()
-            torch.cuda.synchronize()
-            us = a.elapsed_time(b) * 1e3 / K
-            gbs = nbytes / (us * 1e-6) / 1e9
-            print(f"{label:<18} {name:<16} {us:>9.3f} {gbs:>8.1f} {100 * gbs / PEAK_HBM_GBS:>5.1f}% "
-                  f"{n_ * t_ / (us * 1e-6) / 1e9:>9.1f} {S:>5} {rel:>11.2e}", file=sys.stderr, flush=True)
-            del graph
+            _measure(label, name, lambda d: call(name, d, ws, gamma, lam, trunc, boot), sets, nbytes,
+                     n_ * t_, rel)
         del sets, base, ws
         torch.cuda.empty_cache()
     for label, n_, t_, a_ in (("rf_4096x256x4", 4096, 256, 4), ("rf_512x4096x4", 512, 4096, 4),
@@ -385,23 +453,7 @@ def run_retrace_full(label, n_, t_, a_, dev):
         raise SystemExit(f"parity failure in {label}: {rel}")
     # r, Q and pi [A], action (4 B), mu, term, trunc, bv, two outputs; bootstrap per row
     nbytes = n_ * t_ * (4 + 8 * a_ + 4 + 4 + 1 + 1 + 4 + 8) + 4 * n_
-    K = int(max(20, min(2000, 20000 / max(2.0, nbytes / 5e3))))
-    for i in range(3):
-        call(sets[i % S])
-    torch.cuda.synchronize()
-    graph = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(graph):
-        for i in range(K):
-            call(sets[i % S])
-    graph.replay()
-    torch.cuda.synchronize()
-    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    a.record(); graph.replay(); b.record()
-    torch.cuda.synchronize()
-    us = a.elapsed_time(b) * 1e3 / K
-    gbs = nbytes / (us * 1e-6) / 1e9
-    print(f"{label:<18} {'retrace_full':<16} {us:>9.3f} {gbs:>8.1f} {100 * gbs / PEAK_HBM_GBS:>5.1f}% "
-          f"{n_ * t_ / (us * 1e-6) / 1e9:>9.1f} {S:>5} {rel:>11.2e}", file=sys.stderr, flush=True)
+    _measure(label, "retrace_full", call, sets, nbytes, n_ * t_, rel)
 
 
 def _rotated_sets(base, S, outs):
@@ -443,6 +495,32 @@ def _report(label, name, us, nbytes, steps, S, rel):
           f"{steps / (us * 1e-6) / 1e9:>9.1f} {S:>5} {rel:>11.2e}", file=sys.stderr, flush=True)
 
 
+# With --extra --profile-pass: eager launches per workload for rocprofv3 runs instead of graph
+# timing. Each workload's launches sit between two one-element int16 fills (a marker no other
+# step of the run launches), and `manifest` lists the workloads in launch order.
+_PROFILE = {"on": False, "calls": 20, "manifest": []}
+MARKER_KERNEL = "FillFunctor<short>"
+
+
+def _measure(label, name, call, sets, nbytes, steps, rel):
+    """Graph-time `call` over the rotated `sets` and print a table line, or, in a profile pass,
+    launch it eagerly after a block marker and record the workload in the manifest."""
+    import torch
+    if not _PROFILE["on"]:
+        _report(label, name, _graph_time(call, sets, nbytes), nbytes, steps, len(sets), rel)
+        return
+    dev = next(v for v in sets[0].values() if torch.is_tensor(v)).device
+    torch.cuda.synchronize()
+    torch.full((1,), 7, dtype=torch.int16, device=dev)
+    for i in range(_PROFILE["calls"]):
+        call(sets[i % len(sets)])
+    torch.full((1,), 7, dtype=torch.int16, device=dev)
+    torch.cuda.synchronize()
+    _PROFILE["manifest"].append({"label": label, "name": name, "calls": _PROFILE["calls"],
+                                 "bytes": int(nbytes), "steps": int(steps)})
+    print(f"profile pass: {label} {name} x{_PROFILE['calls']}", file=sys.stderr, flush=True)
+
+
 def run_time_major(label, t_, n_, dev):
     """GAE and V-Trace on a time-major [T, N] fp32 buffer with truncation: parity on sampled
     environments, then graph-timed. Same dense byte count as the row-major form."""
@@ -481,7 +559,7 @@ def run_time_major(label, t_, n_, dev):
         if rel > 1e-5:
             raise SystemExit(f"parity failure in {label} {name}: {rel}")
         nbytes = extra_bytes(name, n_, t_, 4, True, True)
-        _report(label, name + "_tm", _graph_time(call, sets, nbytes), nbytes, n_ * t_, S, rel)
+        _measure(label, name + "_tm", call, sets, nbytes, n_ * t_, rel)
 
 
 def run_strided_rows(label, n_, t_, ld, dev):
@@ -523,7 +601,7 @@ def run_strided_rows(label, n_, t_, ld, dev):
     if rel > 1e-5:
         raise SystemExit(f"parity failure in {label}: {rel}")
     nbytes = extra_bytes("gae", n_, t_, 4, True, True)
-    _report(label, "gae_strided", _graph_time(call, sets, nbytes), nbytes, n_ * t_, S, rel)
+    _measure(label, "gae_strided", call, sets, nbytes, n_ * t_, rel)
 
 
 def run_vector_trace(label, n_, t_, f_, dev):
@@ -553,7 +631,7 @@ def run_vector_trace(label, n_, t_, f_, dev):
     if rel > 1e-5:
         raise SystemExit(f"parity failure in {label}: {rel}")
     nbytes = n_ * t_ * (8 * f_ + 2)
-    _report(label, "elig_trace_vec", _graph_time(call, sets, nbytes), nbytes, n_ * t_ * f_, S, rel)
+    _measure(label, "elig_trace_vec", call, sets, nbytes, n_ * t_ * f_, rel)
 
 
 def run_masked(label, n_, t_, dev):
@@ -587,8 +665,7 @@ def run_masked(label, n_, t_, dev):
         rel = float(np.max(np.abs(got - r_))) / (1 + float(np.max(np.abs(r_))))
         if rel > 1e-5:
             raise SystemExit(f"parity failure in {label} norm={norm}: {rel}")
-        _report(label, "gae_masked" + ("_norm" if norm else ""), _graph_time(call, sets, nbytes),
-                nbytes, n_ * t_, S, rel)
+        _measure(label, "gae_masked" + ("_norm" if norm else ""), call, sets, nbytes, n_ * t_, rel)
 
 
 def main():
@@ -598,6 +675,9 @@ def main():
         return
     if args.summarize_trace:
         summarize_trace(args.summarize_trace)
+        return
+    if args.summarize_extra:
+        summarize_extra(*args.summarize_extra)
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); rows are independent, so "
@@ -614,7 +694,20 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     if args.extra:
+        if args.profile_pass:
+            _PROFILE["on"] = True
         run_extra(dev, args.only)
+        if args.profile_pass:
+            src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device=dev)
+            dst = torch.empty_like(src)
+            for _ in range(3):
+                dst.copy_(src)
+            torch.cuda.synchronize()
+            if args.manifest:
+                with open(args.manifest, "w") as f:
+                    json.dump(_PROFILE["manifest"], f, indent=0)
+            print(f"profile pass: {len(_PROFILE['manifest'])} workloads, 3 copies of {COPY_BYTES} B",
+                  flush=True)
         return
 
     ro = workloads.make_rollout(N, T, seed=0, p_term=0.02, p_trunc=0.01)

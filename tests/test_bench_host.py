@@ -1,0 +1,81 @@
+"""Host logic of bench.py: byte accounting and the rocprofv3 summaries (on small synthetic
+profiler databases with the columns rocprofv3 writes)."""
+import json
+import os
+import sqlite3
+
+import pytest
+
+import bench
+
+
+def _db(path, kernels=(), counters=()):
+    os.makedirs(path, exist_ok=True)
+    con = sqlite3.connect(os.path.join(path, "run_results.db"))
+    con.execute("create table kernels (dispatch_id integer, name text, start integer, "
+                "\"end\" integer, duration integer)")
+    con.execute("create table counters_collection (dispatch_id integer, kernel_name text, "
+                "counter_name text, value real, grid_size integer)")
+    for i, (n, d) in enumerate(kernels):
+        con.execute("insert into kernels values (?, ?, ?, ?, ?)", (i, n, 1000 * i, 1000 * i + d, d))
+    for i, (n, c, v, g) in enumerate(counters):
+        con.execute("insert into counters_collection values (?, ?, ?, ?, ?)", (i, n, c, v, g))
+    con.commit()
+    con.close()
+
+
+MARK = "void at::native::vectorized_elementwise_kernel<4, at::native::FillFunctor<short>>"
+GAE = "void rlcs::rows_kernel<rlcs::GaeOp, float, 4, 4, true, true>(rlcs::Args, long, int)"
+NORM = "void rlcs::masked_normalize_kernel(rlcs::MaskedArgs)"
+MASK = "void rlcs::masked_gae_kernel<float, 4, 4, true, false, true, true>(rlcs::MaskedArgs)"
+COPY = "__amd_rocclr_copyBuffer"
+OTHER = "void at::native::index_select_kernel<float>"
+
+
+def test_algorithmic_bytes_headline():
+    # r, v, bv fp32; term, trunc u8; adv, ret fp32 -> 22 B per step, plus a 4-byte bootstrap per row
+    assert bench.algorithmic_bytes(4096, 256) == 4096 * 256 * 22 + 4096 * 4
+    assert bench.algorithmic_bytes(8, 128, trunc=False) == 8 * 128 * 17 + 8 * 4
+    assert bench.extra_bytes("gae", 4096, 256, 4, True, True) == bench.algorithmic_bytes(4096, 256)
+    assert bench.extra_bytes("elig_trace", 10, 10, 2, True, True) == 100 * (2 + 1 + 1 + 4)
+
+
+def test_summarize_extra(tmp_path, capsys):
+    # two workloads: two GAE calls, then one whitened masked call (two kernels); a parity call and
+    # a torch kernel outside the markers must be ignored
+    seq = [(GAE, 999), (MARK, 1), (GAE, 5000), (OTHER, 7), (GAE, 7000), (MARK, 1),
+           (MASK, 999), (MARK, 1), (MASK, 3000), (NORM, 2000), (MARK, 1), (COPY, 9)]
+    _db(str(tmp_path / "t"), kernels=seq)
+    copy_kib = (bench.COPY_BYTES / 1024) / 2  # a counter that reads half the copy: scale 2
+    fvals = {GAE: 100.0, MASK: 40.0, NORM: 10.0, MARK: 0.0, OTHER: 1.0}
+    _db(str(tmp_path / "f"), counters=[(n, "FETCH_SIZE", fvals.get(n, copy_kib), 1) for n, _ in seq])
+    _db(str(tmp_path / "w"), counters=[(n, "WRITE_SIZE", fvals.get(n, bench.COPY_BYTES / 1024), 1)
+                                       for n, _ in seq])
+    man = [{"label": "a", "name": "gae", "calls": 2, "bytes": 4_000_000, "steps": 10},
+           {"label": "b", "name": "gae_masked_norm", "calls": 1, "bytes": 1_000_000, "steps": 10}]
+    mp = tmp_path / "m.json"
+    mp.write_text(json.dumps(man))
+    bench.summarize_extra(str(tmp_path / "t"), str(tmp_path / "f"), str(tmp_path / "w"), str(mp))
+    out = capsys.readouterr().out.splitlines()
+    assert "FETCH_SIZE_scale: 2.0000" in out and "WRITE_SIZE_scale: 1.0000" in out
+    per_call = [l.split() for l in out if "(per call)" in l]
+    assert len(per_call) == 2
+    # workload a: (5 + 7) / 2 = 6 us per call; traffic (2 * 100 + 100) KiB per call
+    assert per_call[0][0] == "a" and float(per_call[0][4]) == pytest.approx(6.0)
+    assert int(per_call[0][7]) == 300 * 1024
+    # workload b: both kernels of the call, 3 + 2 us; traffic (2 * 50 + 50) KiB
+    assert per_call[1][0] == "b" and float(per_call[1][4]) == pytest.approx(5.0)
+    assert int(per_call[1][7]) == 150 * 1024
+
+
+def test_summarize_extra_rejects_mismatch(tmp_path):
+    seq = [(MARK, 1), (GAE, 5000), (MARK, 1), (COPY, 9)]
+    for d, kind in (("t", None), ("f", "FETCH_SIZE"), ("w", "WRITE_SIZE")):
+        if kind is None:
+            _db(str(tmp_path / d), kernels=seq)
+        else:
+            _db(str(tmp_path / d), counters=[(n, kind, 1.0, 1) for n, _ in seq])
+    mp = tmp_path / "m.json"
+    mp.write_text(json.dumps([{"label": "a", "name": "x", "calls": 1, "bytes": 1, "steps": 1}] * 2))
+    with pytest.raises(SystemExit):
+        bench.summarize_extra(str(tmp_path / "t"), str(tmp_path / "f"), str(tmp_path / "w"), str(mp))
