@@ -234,7 +234,7 @@ def _copy_scale(rows, counter):
 
 def _short(name):
     name = name.replace("rlcs::", "").replace("void ", "")
-    return name.split("(")[0][:44]
+    return name.split("(")[0][:42]
 
 
 def summarize_extra(trace_dir, fetch_dir, write_dir, manifest):
@@ -257,15 +257,16 @@ def summarize_extra(trace_dir, fetch_dir, write_dir, manifest):
         kinds = sorted({n for n, _ in tb}, key=[n for n, _ in tb].index)
         per_call_us = sum(v for _, v in tb) / 1e3 / calls
         traffic = (sum(v for _, v in fb) * fs + sum(v for _, v in wb) * ws) * 1024 / calls
-        for k in kinds:
+        for k in kinds if len(kinds) > 1 else ():
             d = [v / 1e3 for n, v in tb if n == k]
             f = [v for n, v in fb if n == k]
             w = [v for n, v in wb if n == k]
             kt = (statistics.mean(f) * fs + statistics.mean(w) * ws) * 1024
-            print(f"{m['label']:<18} {m['name']:<16} {_short(k):<44} {statistics.mean(d):>8.3f} "
-                  f"{'':>7} {'':>6} {kt:>11.0f} {'':>11} {'':>6}")
+            print(f"{m['label']:<18} {m['name']:<16} {'- ' + _short(k):<44} {statistics.mean(d):>8.3f} "
+                  f"{'':>7} {'':>6} {kt:>11.0f}")
         gbs = m["bytes"] / (per_call_us * 1e-6) / 1e9
-        print(f"{m['label']:<18} {m['name']:<16} {'(per call)':<44} {per_call_us:>8.3f} {gbs:>7.0f} "
+        what = _short(kinds[0]) if len(kinds) == 1 else "(per call: the kernels above)"
+        print(f"{m['label']:<18} {m['name']:<16} {what:<44} {per_call_us:>8.3f} {gbs:>7.0f} "
               f"{100 * gbs / PEAK_HBM_GBS:>5.1f}% {traffic:>11.0f} {m['bytes']:>11} "
               f"{traffic / m['bytes']:>6.3f}")
 

@@ -58,14 +58,15 @@ def test_summarize_extra(tmp_path, capsys):
     bench.summarize_extra(str(tmp_path / "t"), str(tmp_path / "f"), str(tmp_path / "w"), str(mp))
     out = capsys.readouterr().out.splitlines()
     assert "FETCH_SIZE_scale: 2.0000" in out and "WRITE_SIZE_scale: 1.0000" in out
-    per_call = [l.split() for l in out if "(per call)" in l]
+    # per workload: label, estimator, kernel (several words), avg_us, GB/s, %peak, traffic, alg, ratio
+    per_call = [l.split() for l in out if l[:2] in ("a ", "b ") and l.split()[2] != "-"]
     assert len(per_call) == 2
     # workload a: (5 + 7) / 2 = 6 us per call; traffic (2 * 100 + 100) KiB per call
-    assert per_call[0][0] == "a" and float(per_call[0][4]) == pytest.approx(6.0)
-    assert int(per_call[0][7]) == 300 * 1024
+    assert per_call[0][0] == "a" and float(per_call[0][-6]) == pytest.approx(6.0)
+    assert int(per_call[0][-3]) == 300 * 1024
     # workload b: both kernels of the call, 3 + 2 us; traffic (2 * 50 + 50) KiB
-    assert per_call[1][0] == "b" and float(per_call[1][4]) == pytest.approx(5.0)
-    assert int(per_call[1][7]) == 150 * 1024
+    assert per_call[1][0] == "b" and float(per_call[1][-6]) == pytest.approx(5.0)
+    assert int(per_call[1][-3]) == 150 * 1024
 
 
 def test_summarize_extra_rejects_mismatch(tmp_path):
