@@ -209,8 +209,9 @@ size_t rlcs_workspace_size(int64_t N, int64_t T);
  *            unbiased variance over the steps that take part (var 0 with fewer than two),
  *            applied to every step. eps >= 0, finite.
  *   ws       required when normalize = 1: rlcs_workspace_size_masked(N, T) bytes, 64-byte
- *            aligned, zero-filled once before its first use (every call leaves it ready for
- *            the next; calls sharing it must be ordered on one stream); unused otherwise.
+ *            aligned, any contents (no clearing needed); calls sharing it must be ordered on
+ *            one stream. After the call its first 16 bytes hold the mean and 1/sqrt(var + eps)
+ *            as two doubles. Unused when normalize = 0.
  * Rows are never split across workgroups for this entry point.                             */
 rlcs_status rlcs_gae_masked(const void* r, const void* v, const uint8_t* mask,
                             const uint8_t* term, const uint8_t* trunc, const void* bv,

@@ -16,15 +16,14 @@
 // steps, a DPP wave scan composes lanes, LDS composes waves and carries chunks.
 //
 // Whitening: the scan kernel also reduces the advantages of the unmasked steps of each
-// workgroup to (count, mean, M2) in fp64 and publishes them; the workgroup that finishes last
-// (an atomic count of finished workgroups) merges all partials in a fixed order (Chan et al.'s
-// pairwise update) into the mean and 1/sqrt(var + eps), var the unbiased variance; a second
-// kernel rewrites the advantages. Every order is fixed, so results are reproducible bit for
-// bit. A partial is written at device scope and its write completes before its workgroup
-// counts itself finished, so the last workgroup, which reads the partials at device scope
-// after the count, sees every one of them. Finished workgroups are counted in two levels
-// (groups of kMomentGroup workgroups, each with its own counter line; the last of a group
-// counts the group) because atomics on one address serialise.
+// workgroup to fp64 sums (count, sum, sum of squares) and stores them as the workgroup's
+// partial. A second kernel rewrites the advantages: each of its workgroups first adds up all
+// partials itself, in one fixed order, so every workgroup derives the same mean and
+// 1/sqrt(var + eps) (var the unbiased variance) and results are reproducible bit for bit.
+// The kernel boundary orders the partials before their readers, so no atomics or fences are
+// needed. With more than kDirectPartials partials a small kernel in between first adds them
+// in blocks of kDirectPartials. fp64 sums of fp32 advantages lose accuracy in the variance only
+// when |mean| / std approaches 1e6, far past what fp32 advantages resolve anyway.
 #pragma once
 
 #include "rlcs_kernels.h"
@@ -85,31 +84,21 @@ __device__ __forceinline__ AW shift_up1(AW v, AW fill) {
     return AW{shift_up1(v.A, fill.A), shift_up1(v.W, fill.W)};
 }
 
+// fp64 sums of the advantages of the unmasked steps of one workgroup (or of a block of
+// partials): count, sum, sum of squares.
+struct alignas(32) Moments {
+    double n, s1, s2, pad;
+};
+
 struct MaskedArgs {
     Args a;              // in[0] r, in[1] v, in[2] bv; term, trunc; row_value = boot;
                          // out0 adv, out1 ret (optional)
     const uint8_t* mask; // [N, T], nonzero = the step takes part; null = every step does
-    // whitening only (workspace): stats = {mean, 1/sqrt(var + eps)}; the count of finished
-    // groups; per group, the count of its finished workgroups (one 64-byte line each; all
-    // counts zero between calls); one (count, mean, M2) partial per workgroup
-    double* stats;
-    uint32_t* groups_done;
-    uint32_t* group_counts;
-    double* partials;
-    float eps;
+    // whitening only (workspace): one partial per workgroup
+    Moments* partials;
 };
 
-constexpr int kMomentGroup = 32;  // workgroups per first-level finished count
-
-// Chan et al.'s merge of (n, mean, M2) summaries: b into a.
-__device__ __forceinline__ void merge_moments(double& n, double& mean, double& m2, double nb,
-                                              double mb, double m2b) {
-    if (nb == 0.0) return;
-    const double nn = n + nb, d = mb - mean;
-    mean += d * (nb / nn);
-    m2 += m2b + d * d * (n * nb / nn);
-    n = nn;
-}
+constexpr int kDirectPartials = 4096;  // partials one normalize workgroup adds up itself
 
 // Map of one step.
 __device__ __forceinline__ Tri masked_gae_step(const Params& P, bool in, bool te, bool tr, bool ed,
@@ -296,94 +285,81 @@ __global__ void __launch_bounds__(W * kWave) masked_gae_kernel(MaskedArgs ma, in
         chunk_hi = chunk_lo;
     }
     if constexpr (STATS) {
-        __shared__ int s_last;
         n = wave_sum(n);
         s1 = wave_sum(s1);
         s2 = wave_sum(s2);
         if (lane == 0) { s_stat[0][wave] = n; s_stat[1][wave] = s1; s_stat[2][wave] = s2; }
         __syncthreads();
         if (threadIdx.x == 0) {
-            double tn = 0.0, t1 = 0.0, t2 = 0.0;
-            for (int w = 0; w < W; ++w) { tn += s_stat[0][w]; t1 += s_stat[1][w]; t2 += s_stat[2][w]; }
-            const double mean = tn > 0.0 ? t1 / tn : 0.0;
-            const double m2 = tn > 0.0 ? fmax(t2 - t1 * mean, 0.0) : 0.0;
-            uint64_t* out = reinterpret_cast<uint64_t*>(ma.partials + 4 * int64_t(blockIdx.x));
-            st_relaxed(out, uint64_t(__double_as_longlong(tn)));
-            st_relaxed(out + 1, uint64_t(__double_as_longlong(mean)));
-            st_relaxed(out + 2, uint64_t(__double_as_longlong(m2)));
-            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the partial is written
-            const uint32_t G = gridDim.x, g = blockIdx.x / kMomentGroup;
-            const uint32_t n_groups = (G + kMomentGroup - 1) / kMomentGroup;
-            const uint32_t in_group = min(uint32_t(kMomentGroup), G - g * kMomentGroup);
-            uint32_t* gc = ma.group_counts + 16 * g;
-            bool last = false;
-            if (__hip_atomic_fetch_add(gc, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
-                in_group - 1) {
-                st_relaxed(gc, 0u);
-                last = __hip_atomic_fetch_add(ma.groups_done, 1u, __ATOMIC_RELAXED,
-                                              __HIP_MEMORY_SCOPE_AGENT) == n_groups - 1;
-                if (last) st_relaxed(ma.groups_done, 0u);
-            }
-            s_last = last ? 1 : 0;
-        }
-        __syncthreads();
-        if (s_last) {
-            // merge every partial: thread-serial over a fixed stride, then a fixed butterfly
-            // within each wave, then the waves in order
-            double cn = 0.0, cm = 0.0, c2 = 0.0;
-            const uint64_t* part = reinterpret_cast<const uint64_t*>(ma.partials);
-            constexpr int kBatch = 8;  // partials per thread in flight
-            const int64_t G = gridDim.x, step = int64_t(W) * kWave;
-            for (int64_t g0 = threadIdx.x; g0 < G; g0 += kBatch * step) {
-                uint64_t raw[kBatch][3];
-#pragma unroll
-                for (int u = 0; u < kBatch; ++u) {
-                    const int64_t g = g0 + u * step;
-                    if (g < G) {
-                        raw[u][0] = ld_relaxed(part + 4 * g);
-                        raw[u][1] = ld_relaxed(part + 4 * g + 1);
-                        raw[u][2] = ld_relaxed(part + 4 * g + 2);
-                    }
-                }
-#pragma unroll
-                for (int u = 0; u < kBatch; ++u) {
-                    if (g0 + u * step < G)
-                        merge_moments(cn, cm, c2, __longlong_as_double(int64_t(raw[u][0])),
-                                      __longlong_as_double(int64_t(raw[u][1])),
-                                      __longlong_as_double(int64_t(raw[u][2])));
-                }
-            }
-#pragma unroll
-            for (int o = 32; o >= 1; o >>= 1) {
-                const double nb = __shfl_xor(cn, o, kWave), mb = __shfl_xor(cm, o, kWave),
-                             m2b = __shfl_xor(c2, o, kWave);
-                merge_moments(cn, cm, c2, nb, mb, m2b);
-            }
-            __syncthreads();
-            if (lane == 0) { s_stat[0][wave] = cn; s_stat[1][wave] = cm; s_stat[2][wave] = c2; }
-            __syncthreads();
-            if (threadIdx.x == 0) {
-                double tn = 0.0, tm = 0.0, t2 = 0.0;
-                for (int w = 0; w < W; ++w) merge_moments(tn, tm, t2, s_stat[0][w], s_stat[1][w], s_stat[2][w]);
-                const double var = tn > 1.0 ? t2 / (tn - 1.0) : 0.0;
-                ma.stats[0] = tn > 0.0 ? tm : 0.0;
-                ma.stats[1] = 1.0 / sqrt(var + double(ma.eps));
-            }
+            Moments m{0.0, 0.0, 0.0, 0.0};
+            for (int w = 0; w < W; ++w) { m.n += s_stat[0][w]; m.s1 += s_stat[1][w]; m.s2 += s_stat[2][w]; }
+            ma.partials[blockIdx.x] = m;
         }
     }
 }
 
-// adv <- (adv - mean) * rstd over all `total` elements. Each thread rewrites kNormVec 16-byte
-// vectors (strided by the workgroup size, so that a wave's accesses are contiguous), all loads
-// issued before the first store; workgroup 0 also does the elements past the last vector. The
-// element-wise form is for advantages not 16-byte aligned.
+// Sum of partials [lo, hi) over a workgroup of kNormThreads threads, in one fixed order
+// (thread-serial over a stride of kNormThreads, a butterfly within each wave, then the waves in
+// order), returned to every thread. Every thread of the workgroup must call it.
 constexpr int kNormThreads = 256;
+
+__device__ __forceinline__ Moments sum_partials(const Moments* part, int64_t lo, int64_t hi) {
+    __shared__ double s_sum[3][kNormThreads / kWave];
+    double n = 0.0, s1 = 0.0, s2 = 0.0;
+    constexpr int kBatch = 4;  // partials per thread in flight
+    for (int64_t g0 = lo + threadIdx.x; g0 < hi; g0 += int64_t(kBatch) * kNormThreads) {
+        Moments m[kBatch];
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            const int64_t g = g0 + int64_t(u) * kNormThreads;
+            m[u] = g < hi ? part[g] : Moments{0.0, 0.0, 0.0, 0.0};
+        }
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) { n += m[u].n; s1 += m[u].s1; s2 += m[u].s2; }
+    }
+    n = wave_sum(n);
+    s1 = wave_sum(s1);
+    s2 = wave_sum(s2);
+    const int wave = threadIdx.x / kWave;
+    if ((threadIdx.x & (kWave - 1)) == 0) { s_sum[0][wave] = n; s_sum[1][wave] = s1; s_sum[2][wave] = s2; }
+    __syncthreads();
+    Moments t{0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+    for (int w = 0; w < kNormThreads / kWave; ++w) { t.n += s_sum[0][w]; t.s1 += s_sum[1][w]; t.s2 += s_sum[2][w]; }
+    return t;
+}
+
+// Second-level partials: workgroup j adds partials [j * kDirectPartials, (j + 1) * kDirectPartials).
+__global__ void __launch_bounds__(kNormThreads) masked_sum_partials_kernel(const Moments* part,
+                                                                           int64_t G, Moments* out) {
+    const int64_t lo = int64_t(blockIdx.x) * kDirectPartials;
+    const Moments t = sum_partials(part, lo, min(lo + kDirectPartials, G));
+    if (threadIdx.x == 0) out[blockIdx.x] = t;
+}
+
+// adv <- (adv - mean) * rstd over all `total` elements, mean and rstd from the sum of the G
+// partials. Each thread rewrites kNormVec 16-byte vectors (strided by the workgroup size, so
+// that a wave's accesses are contiguous), its loads issued before the partials are added up;
+// workgroup 0 also does the elements past the last vector and stores {mean, rstd} to `stats`.
+// The element-wise form is for advantages not 16-byte aligned.
 constexpr int kNormVec = 4;
 
+__device__ __forceinline__ void whitening(const Moments* part, int64_t G, float eps, double* stats,
+                                          float& mean, float& rstd) {
+    const Moments t = sum_partials(part, 0, G);
+    const double m = t.n > 0.0 ? t.s1 / t.n : 0.0;
+    const double var = t.n > 1.0 ? fmax(t.s2 - t.s1 * m, 0.0) / (t.n - 1.0) : 0.0;
+    const double r = 1.0 / sqrt(var + double(eps));
+    if (blockIdx.x == 0 && threadIdx.x == 0) { stats[0] = m; stats[1] = r; }
+    mean = float(m);
+    rstd = float(r);
+}
+
 __global__ void __launch_bounds__(kNormThreads) masked_normalize_kernel(float* adv, int64_t total,
-                                                                        const double* stats,
-                                                                        int vec) {
-    const float mean = float(stats[0]), rstd = float(stats[1]);
+                                                                        const Moments* part,
+                                                                        int64_t G, float eps,
+                                                                        double* stats, int vec) {
+    float mean, rstd;
     const int64_t base = int64_t(blockIdx.x) * kNormThreads * kNormVec + threadIdx.x;
     if (vec) {
         f32x4* p = reinterpret_cast<f32x4*>(adv);
@@ -394,6 +370,7 @@ __global__ void __launch_bounds__(kNormThreads) masked_normalize_kernel(float* a
             const int64_t i = base + int64_t(u) * kNormThreads;
             if (i < nv) x[u] = __builtin_nontemporal_load(p + i);
         }
+        whitening(part, G, eps, stats, mean, rstd);
 #pragma unroll
         for (int u = 0; u < kNormVec; ++u) {
             const int64_t i = base + int64_t(u) * kNormThreads;
@@ -412,6 +389,7 @@ __global__ void __launch_bounds__(kNormThreads) masked_normalize_kernel(float* a
             const int64_t i = first + int64_t(u) * kNormThreads;
             if (i < total) x[u] = adv[i];
         }
+        whitening(part, G, eps, stats, mean, rstd);
 #pragma unroll
         for (int u = 0; u < 4 * kNormVec; ++u) {
             const int64_t i = first + int64_t(u) * kNormThreads;

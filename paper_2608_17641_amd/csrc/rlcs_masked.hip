@@ -9,10 +9,12 @@ using namespace rlcs::host;
 namespace {
 
 // Bytes of the whitening workspace of an [N, T] call (at most one workgroup per row): 64 for
-// the statistics and the count of finished groups, a 64-byte count line per group of
-// kMomentGroup workgroups, then one 32-byte partial per workgroup.
-size_t masked_groups(int64_t N) { return size_t((N > 0 ? N : 1) + kMomentGroup - 1) / kMomentGroup; }
-size_t masked_ws_need(int64_t N) { return 64 + 64 * masked_groups(N) + 32 * size_t(N > 0 ? N : 1); }
+// the statistics {mean, rstd}, one 32-byte partial per workgroup (room for N), then one per
+// block of kDirectPartials partials.
+size_t masked_rows(int64_t N) { return size_t(N > 0 ? N : 1); }
+size_t masked_ws_need(int64_t N) {
+    return 64 + sizeof(Moments) * (masked_rows(N) + (masked_rows(N) + kDirectPartials - 1) / kDirectPartials);
+}
 
 template <typename DT, bool VEC, bool TR, bool HM, bool STATS>
 void launch_masked(const MaskedArgs& ma, int waves, int64_t groups, int64_t rows_per_wg,
@@ -47,12 +49,10 @@ rlcs_status run_masked(MaskedArgs& ma, bool normalize, float eps, void* ws, hipS
                (!ma.mask || aligned(ma.mask, K));
     const bool tr = a.trunc != nullptr, hm = ma.mask != nullptr;
     double* stats = reinterpret_cast<double*>(ws);
+    Moments* level2 = nullptr;
     if (normalize) {
-        ma.stats = stats;
-        ma.groups_done = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(ws) + 16);
-        ma.group_counts = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(ws) + 64);
-        ma.partials = reinterpret_cast<double*>(reinterpret_cast<char*>(ws) + 64 + 64 * masked_groups(N));
-        ma.eps = eps;
+        ma.partials = reinterpret_cast<Moments*>(reinterpret_cast<char*>(ws) + 64);
+        level2 = ma.partials + masked_rows(N);
     }
 #define RLCS_MASKED(V, TRV, HMV, ST) launch_masked<DT, V, TRV, HMV, ST>(ma, waves, groups, rows_per_wg, wave_local, s)
 #define RLCS_MASKED_ST(V, TRV, HMV) \
@@ -71,8 +71,17 @@ rlcs_status run_masked(MaskedArgs& ma, bool normalize, float eps, void* ws, hipS
         const int64_t per_wg = int64_t(kNormThreads) * kNormVec * 4;  // elements
         const int64_t grid = (total + per_wg - 1) / per_wg;
         if (grid > INT32_MAX) return RLCS_ERR_INVALID_ARG;
+        const Moments* part = ma.partials;
+        int64_t G = groups;
+        if (G > kDirectPartials) {
+            const int64_t blocks = (G + kDirectPartials - 1) / kDirectPartials;
+            hipLaunchKernelGGL(masked_sum_partials_kernel, dim3(unsigned(blocks)), dim3(kNormThreads),
+                               0, s, ma.partials, G, level2);
+            part = level2;
+            G = blocks;
+        }
         hipLaunchKernelGGL(masked_normalize_kernel, dim3(unsigned(grid)), dim3(kNormThreads), 0, s,
-                           a.out0, total, stats, aligned(a.out0, 16) ? 1 : 0);
+                           a.out0, total, part, G, eps, stats, aligned(a.out0, 16) ? 1 : 0);
     }
     return hipGetLastError() == hipSuccess ? RLCS_OK : RLCS_ERR_LAUNCH;
 }

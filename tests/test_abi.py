@@ -235,5 +235,7 @@ def test_gae_masked_validation(lib):
     assert call(normalize=1, ws=FAKE, ws_bytes=10) == n.RLCS_ERR_WORKSPACE
     assert call(lam=2.0) == n.RLCS_ERR_INVALID_ARG
     assert call(N=0) == n.RLCS_OK
-    assert lib.rlcs_workspace_size_masked(100, 7) == 64 + 64 * 4 + 32 * 100  # groups of 32
+    # statistics, one partial per row, one per block of 4096 partials
+    assert lib.rlcs_workspace_size_masked(100, 7) == 64 + 32 * 100 + 32
+    assert lib.rlcs_workspace_size_masked(4097, 7) == 64 + 32 * 4097 + 32 * 2
     assert lib.rlcs_workspace_size_masked(-1, 7) == 0

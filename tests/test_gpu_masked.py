@@ -97,8 +97,9 @@ def test_gae_masked_deterministic():
 
 
 def test_gae_masked_workspace_reuse():
-    """One zero-filled whitening workspace serves calls of several shapes in turn."""
-    ws = torch.zeros(rl.rlcs_workspace_size_masked(600, 1), dtype=torch.uint8, device=DEV)
+    """One whitening workspace, never cleared (filled with NaN bytes to start), serves calls of
+    several shapes in turn."""
+    ws = torch.full((rl.rlcs_workspace_size_masked(600, 1),), 255, dtype=torch.uint8, device=DEV)
     for N, T, seed in ((600, 40, 1), (7, 3000, 2), (600, 40, 1), (64, 1024, 3)):
         ro = workloads.make_multiturn(N, T, seed=seed, mean_action=20, mean_obs=30)
         d = {k: to_device(v, DEV) for k, v in ro.items()}
@@ -109,7 +110,21 @@ def test_gae_masked_workspace_reuse():
                                  gamma=1.0, lam=0.95)
         assert_parity({"adv": adv}, {"adv": oracle.normalize_advantages(a, ro["mask"], eps=1e-8)},
                       TOL["f32"], label=f"reuse {N}x{T}")
-    assert int(ws[16:20].view(torch.int32).item()) == 0
+        # the workspace's first 16 bytes hold the call's mean and 1/sqrt(var + eps), taken over
+        # the kernel's float32 advantages: float32 rounding against the oracle's fp64 ones
+        st = ws[:16].view(torch.float64).cpu().numpy()
+        sel = a[ro["mask"] != 0]
+        assert abs(st[0] - sel.mean()) <= 1e-6 * (1 + np.abs(sel).max())
+        assert st[1] == pytest.approx(1 / np.sqrt(sel.var(ddof=1) + 1e-8), rel=1e-5)
+
+
+@pytest.mark.parametrize("N,T", [(4500, 1024), (9000, 256)])
+def test_gae_masked_whitened_many_workgroups(N, T):
+    """More workgroups than one normalize workgroup adds up directly (4096): the partials are
+    first added in blocks."""
+    ro = workloads.make_multiturn(N, T, seed=N, mean_action=20, mean_obs=30)
+    out, ref = run(ro, ro["mask"], normalize=True, gamma=1.0, lam=0.95, trunc=False)
+    assert_parity(out, ref, TOL["f32"], label=f"whitened {N}x{T}")
 
 
 def test_gae_masked_unaligned_outputs_whitened():
