@@ -9,6 +9,7 @@
 #include <climits>
 #include <cstdint>
 #include <initializer_list>
+#include <type_traits>
 
 #include "rlcs.h"
 #include "rlcs_kernels.h"
@@ -74,9 +75,10 @@ struct Plan {
     int64_t rows_per_wg;  // rows kernel: rows per workgroup
     int wave_local;       // rows kernel: no carry crosses waves
     size_t lds_bytes;     // dynamic LDS (staged policies)
+    bool pad;             // rows kernel, vector path: lanes outside the range or in row gaps skip
 };
 
-template <class Op, typename DT, bool VEC, bool TR, int W>
+template <class Op, typename DT, bool VEC, bool TR, int W, bool PAD = false>
 void launch_w(const Args& a, const Plan& p, hipStream_t stream) {
     constexpr int K = Width<DT>::K;
     const dim3 block(W * kWave);
@@ -88,12 +90,19 @@ void launch_w(const Args& a, const Plan& p, hipStream_t stream) {
         }
     }
     const int64_t groups = (a.N + p.rows_per_wg - 1) / p.rows_per_wg;
-    hipLaunchKernelGGL((rows_kernel<Op, DT, K, W, VEC, TR>), dim3(unsigned(groups)), block,
+    hipLaunchKernelGGL((rows_kernel<Op, DT, K, W, VEC, TR, PAD>), dim3(unsigned(groups)), block,
                        p.lds_bytes, stream, a, p.rows_per_wg, p.wave_local);
 }
 
 template <class Op, typename DT, bool VEC, bool TR>
 rlcs_status launch(const Args& a, const Plan& p, hipStream_t stream) {
+    if constexpr (VEC && Op::kStaged == 0) {
+        if (p.pad && !p.split) {
+            if (p.waves == kSmallWaves) launch_w<Op, DT, true, TR, kSmallWaves, true>(a, p, stream);
+            else launch_w<Op, DT, true, TR, kLargeWaves, true>(a, p, stream);
+            return hipGetLastError() == hipSuccess ? RLCS_OK : RLCS_ERR_LAUNCH;
+        }
+    }
     if constexpr (Op::kStaged > 0) {
         if (p.waves == kStagedWaves) launch_w<Op, DT, VEC, TR, kStagedWaves>(a, p, stream);
         else launch_w<Op, DT, VEC, TR, kSmallWaves>(a, p, stream);
@@ -167,6 +176,9 @@ rlcs_status dispatch_dt(Args& a, bool has_trunc, void* ws, size_t ws_bytes, hipS
         if ((N + p.rows_per_wg - 1) / p.rows_per_wg > INT32_MAX) return RLCS_ERR_INVALID_ARG;
         // Rows never straddle waves when T divides a wave's span (and is a multiple of K).
         p.wave_local = (T % K == 0 && (int64_t(kWave) * K) % T == 0) ? 1 : 0;
+        // When a workgroup's rows do not fill its chunks exactly, lanes outside its range skip
+        // their steps so that every chunk still takes the vector path (needs T a multiple of K).
+        p.pad = vec && Op::kStaged == 0 && T % K == 0 && (p.rows_per_wg * T) % E != 0;
     }
 
     if constexpr (Op::kFlags) {
@@ -188,8 +200,9 @@ rlcs_status dispatch(Args& a, rlcs_dtype dtype, bool has_trunc, void* ws, size_t
     return dispatch_dt<Op, float>(a, has_trunc, ws, ws_bytes, s);
 }
 
-// Rows with a row stride (period) above T: the rows kernel over the positions n * period + t,
-// element-wise (the steps t >= T of each period are skipped), whole rows per workgroup.
+// Rows with a row stride (period) above T: the rows kernel over the positions n * period + t
+// (the steps t >= T of each period are skipped), whole rows per workgroup; vector loads and
+// stores when T and the period are multiples of K and the arrays aligned, else element-wise.
 template <class Op>
 rlcs_status dispatch_strided_rows(Args& a, int64_t period, rlcs_dtype dtype, bool has_trunc,
                                   rlcs_stream_t stream) {
@@ -211,10 +224,22 @@ rlcs_status dispatch_strided_rows(Args& a, int64_t period, rlcs_dtype dtype, boo
         if ((a.N + p.rows_per_wg - 1) / p.rows_per_wg > INT32_MAX) return RLCS_ERR_INVALID_ARG;
         p.wave_local = 0;
         p.lds_bytes = 0;
+        // Vector path when every lane's K steps lie in one row or in one gap: T and the row
+        // stride multiples of K, data and outputs 16-byte aligned, flags K-byte aligned.
+        bool vec = a.T % K == 0 && period % K == 0;
+        for (int i = 0; i < Op::kSlots; ++i)
+            if (Op::slot_used(i, has_trunc) && !aligned(a.in[i], 16)) vec = false;
+        if (!aligned(a.out0, 16) || (a.out1 && !aligned(a.out1, 16))) vec = false;
+        if (Op::kFlags && ((a.term && !aligned(a.term, K)) || (has_trunc && !aligned(a.trunc, K)))) vec = false;
+        p.pad = vec;
+        auto go = [&](auto tr_tag) -> rlcs_status {
+            constexpr bool TR = decltype(tr_tag)::value;
+            return vec ? launch<Op, DT, true, TR>(a, p, s) : launch<Op, DT, false, TR>(a, p, s);
+        };
         if constexpr (Op::kFlags) {
-            if (has_trunc) return launch<Op, DT, false, true>(a, p, s);
+            if (has_trunc) return go(std::true_type{});
         }
-        return launch<Op, DT, false, false>(a, p, s);
+        return go(std::false_type{});
     };
     if (dtype == RLCS_BF16) return run(bf16_t{});
     return run(float{});

@@ -115,8 +115,13 @@ __device__ __forceinline__ void row_and_step(const RowBase& b, int64_t p, int64_
 // branch-free path: one vector load per input, issued back to back, and at most one row edge
 // per lane, whose per-row value is loaded unconditionally from a clamped row index. Other
 // chunks (the ragged ends of a range) take the masked element-wise path.
-template <class Op, typename DT, int K, int W, bool VEC, bool TR>
+// PAD: rows lie `a.period` steps apart (period >= T, both multiples of K), so a lane's K steps
+// are either all inside one row or all in the gap after it. Lanes in a gap, and lanes outside
+// the workgroup's range [lo, hi) (a multiple of K at both ends), skip their steps (no loads, the
+// identity map, no stores), so every chunk takes the vector path.
+template <class Op, typename DT, int K, int W, bool VEC, bool TR, bool PAD = false>
 struct Chunk {
+    static_assert(!PAD || (VEC && Op::kStaged == 0), "padded rows: vector path, unstaged policies");
     static constexpr bool kBack = Op::kBackward;
     static constexpr int NS = Op::kSlots;
     static constexpr int NB = Op::kNbr > 0 ? Op::kNbr : 1;
@@ -166,9 +171,29 @@ struct Chunk {
     // after the flags, are in flight; they read the continuations unconditionally, since
     // choosing by the flags would wait for the copies.
     template <class BaseFn, class PreFn>
-    __device__ void load_full(const Args& a, BaseFn&& base_of, int lane, float (&nraw)[Op::kNbrRaw],
-                              PreFn&& pre) {
+    __device__ void load_full(const Args& a, int64_t lo, int64_t hi, BaseFn&& base_of, int lane,
+                              float (&nraw)[Op::kNbrRaw], PreFn&& pre) {
         const int64_t T = a.T;
+        int64_t row = 0, t = 0;
+        if constexpr (PAD) {
+            const bool inside = p0 >= lo && p0 < hi;
+            if (inside) row_and_step(base_of(), p0, a.period, a.inv_period, row, t);
+            if (!inside || t >= T) {  // outside the range, or in the gap between rows
+                valid = 0;
+                edge = 0;
+                ke_ = -1;
+                rv_raw_ = 0.f;
+                trunc = 0;
+#pragma unroll
+                for (int i = 0; i < (K + 3) / 4; ++i) { tw_[i] = 0u; rw_[i] = 0u; }
+#pragma unroll
+                for (int s = 0; s < NS; ++s)
+#pragma unroll
+                    for (int i = 0; i < kWords; ++i) w_[s][i] = 0u;
+                convert_full(a);
+                return;
+            }
+        }
         valid = kAll;
         // A missing optional array is read from in[0] instead (in bounds) and the value dropped.
         const uint8_t* fallback = reinterpret_cast<const uint8_t*>(a.in[0]);
@@ -180,8 +205,7 @@ struct Chunk {
             if (Op::slot_used(s, TR) && s != kTS) load_words<DT, K>(a.in[s], p0, w_[s]);
 
         // at most one row edge among the K steps (T >= K)
-        int64_t row, t;
-        row_and_step(base_of(), p0, T, a.inv_T, row, t);
+        if constexpr (!PAD) row_and_step(base_of(), p0, T, a.inv_T, row, t);
         ke_ = -1;
         int64_t row_e = row;
         if (kBack) {
@@ -290,7 +314,7 @@ struct Chunk {
         p0 = chunk_lo + sidx;
         stage = staged;
         float nraw[Op::kNbrRaw];
-        if (FULL) load_full(a, base_of, lane, nraw, pre);
+        if (FULL) load_full(a, lo, hi, base_of, lane, nraw, pre);
         else load_masked(a, lo, hi, base_of, lane, nraw, pre);
         mid();
         if constexpr (Op::kStaged > 0) {
@@ -317,7 +341,7 @@ struct Chunk {
         }
 
         Op::template build<K, TR>(a.p, d, term, trunc, edge, B, nb, al, be);
-        if (!FULL) {
+        if (!FULL || PAD) {
 #pragma unroll
             for (int k = 0; k < K; ++k)
                 if (!bit(valid, k)) { al[k] = 0.f; be[k] = 1.f; }
@@ -379,6 +403,7 @@ struct Chunk {
         }
         float o0[K], o1[K];
         Op::template finish<K, TR>(a.p, d, term, trunc, edge, B, nb, A, X, o0, o1);
+        if (PAD && FULL && !valid) return kBack ? A[0] : A[K - 1];  // a gap between rows
         store_k<K>(a.out0, p0, valid, FULL, o0);
         if (a.out1) store_k<K>(a.out1, p0, valid, FULL, o1);
         return kBack ? A[0] : A[K - 1];
@@ -537,9 +562,9 @@ struct NoStager {
 // aligned to multiples of K, starting from the carry source (the end for backward scans).
 // `wave_local`: every wave's span starts and ends on row edges (T divides 64*K and the chunk
 // is row aligned), so no carry crosses waves and step 5 is skipped.
-template <class Op, typename DT, int K, int W, bool VEC, bool TR>
+template <class Op, typename DT, int K, int W, bool VEC, bool TR, bool PAD = false>
 __global__ void __launch_bounds__(W * kWave) rows_kernel(Args a, int64_t rows_per_wg, int wave_local) {
-    using C = Chunk<Op, DT, K, W, VEC, TR>;
+    using C = Chunk<Op, DT, K, W, VEC, TR, PAD>;
     constexpr int64_t E = int64_t(W) * kWave * K;
     using S = std::conditional_t<(Op::kStaged > 0), Stager<Op, DT, int(E), K + 1>,
                                  NoStager<Op, DT, int(E), K + 1>>;
@@ -549,7 +574,7 @@ __global__ void __launch_bounds__(W * kWave) rows_kernel(Args a, int64_t rows_pe
     const int64_t row_lo = int64_t(blockIdx.x) * rows_per_wg;
     const int64_t row_hi = min(row_lo + rows_per_wg, a.N);
     const int64_t lo = row_lo * a.period, hi = row_hi * a.period;
-    const bool can_full = VEC && a.T >= K && a.period == a.T;
+    const bool can_full = VEC && a.T >= K && (PAD || a.period == a.T);
     float carry = 0.f;
     auto carry_of = [&]() { return carry; };
     extern __shared__ __align__(16) float s_dyn[];  // staged policies only (sized at launch)
@@ -564,7 +589,7 @@ __global__ void __launch_bounds__(W * kWave) rows_kernel(Args a, int64_t rows_pe
             auto pre = [&]() { sg.issue(a, chunk_lo, lo, s_dyn); };
             auto mid = [&]() { if constexpr (Op::kStaged > 0) { sg.commit(a, chunk_lo, s_dyn); __syncthreads(); } };
             C c;
-            const float first = (can_full && chunk_lo >= lo && chunk_hi <= hi)
+            const float first = (can_full && (PAD || (chunk_lo >= lo && chunk_hi <= hi)))
                 ? run_chunk<true>(c, a, chunk_lo, lo, hi, s_a, s_b, lane, wave, wave_local, base_of, carry_of, stage, pre, mid)
                 : run_chunk<false>(c, a, chunk_lo, lo, hi, s_a, s_b, lane, wave, wave_local, base_of, carry_of, stage, pre, mid);
             if (chunk_lo <= lo) break;
@@ -582,7 +607,7 @@ __global__ void __launch_bounds__(W * kWave) rows_kernel(Args a, int64_t rows_pe
             auto pre = [&]() { sg.issue(a, chunk_lo, lo, s_dyn); };
             auto mid = [&]() { if constexpr (Op::kStaged > 0) { sg.commit(a, chunk_lo, s_dyn); __syncthreads(); } };
             C c;
-            const float last = (can_full && chunk_lo >= lo && chunk_lo + E <= hi)
+            const float last = (can_full && (PAD || (chunk_lo >= lo && chunk_lo + E <= hi)))
                 ? run_chunk<true>(c, a, chunk_lo, lo, hi, s_a, s_b, lane, wave, wave_local, base_of, carry_of, stage, pre, mid)
                 : run_chunk<false>(c, a, chunk_lo, lo, hi, s_a, s_b, lane, wave, wave_local, base_of, carry_of, stage, pre, mid);
             if (chunk_lo + E >= hi) break;

@@ -310,6 +310,32 @@ def test_strided_rows_every_estimator(N, T, ld, v):
                           TOL["f32"], label=f"strided rows {name} {N}x{T} ld={ld} v={v}")
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("N,T,ld", [(100, 256, 320), (37, 64, 72), (6, 4096, 4160), (300, 8, 16),
+                                    (3, 2048, 2056)])
+def test_strided_rows_vector_path(N, T, ld, dtype):
+    """T and the row stride multiples of the vector width, aligned storage: the vector path of
+    the rows kernel, whose lanes in the gaps between rows skip their steps. Every estimator
+    against the oracle; the gaps of the outputs are never written."""
+    ro = workloads.make_rollout(N, T, seed=N * 7 + T, dtype=dtype, p_term=0.05, p_trunc=0.05)
+    d = {k: (strided_rows(to_device(a, DEV), ld) if a.ndim == 2 else to_device(a, DEV))
+         for k, a in ro.items()}
+    from cases import oracle_run
+    for name in TM_ESTIMATORS:
+        out = run_strided(name, d)
+        torch.cuda.synchronize()
+        assert_parity(out, oracle_run(name, ro, gamma=G, lam=L, c_bar=1.0 if name != "vtrace" else 0.9),
+                      TOL[dtype], label=f"strided rows {name} {N}x{T} ld={ld} {dtype}")
+    bufs = [torch.full((N, ld), -3.0, device=DEV) for _ in range(2)]
+    adv, ret = rl.rlcs_gae_strided(d["r"], d["v"], d["term"], d["trunc"], d["bv"], d["boot"],
+                                   bufs[0][:, :T], bufs[1][:, :T], gamma=G, lam=L)
+    torch.cuda.synchronize()
+    assert_parity({"adv": adv, "ret": ret}, oracle_run("gae", ro, gamma=G, lam=L),
+                  TOL[dtype], label=f"strided rows gae, given outputs {N}x{T} ld={ld} {dtype}")
+    for b in bufs:
+        assert bool((b[:, T:] == -3.0).all())
+
+
 def test_strided_dense_layout_runs_the_row_major_path():
     """stride (T, 1) is the plain row-major layout: same results as the row-major entry point,
     bit for bit."""

@@ -84,6 +84,19 @@ def test_odd_lengths_all_estimators(T, var):
             check(name, ro, ws=ws, gamma=0.97, lam=0.9, label=f"T={T} variant {var}")
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("T", [24, 96, 200, 1000, 3000, 5000, 8200])
+def test_vector_lengths_not_dividing_the_chunk(T, dtype):
+    """T a multiple of the vector width whose rows do not fill a workgroup's chunks exactly:
+    the vector path with the lanes outside the workgroup's rows skipped."""
+    N = 37
+    ws = rl.make_workspace(N, T, DEV)
+    with variant(1):
+        for i, name in enumerate(ESTIMATORS):
+            ro = make_inputs(name, N, T, seed=T * 10 + i, dtype=dtype, p_term=0.05, p_trunc=0.05)
+            check(name, ro, ws=ws, gamma=0.97, lam=0.9, label=f"T={T} {dtype}")
+
+
 @pytest.mark.parametrize("T", [3, 64, 129, 2050])
 @pytest.mark.parametrize("var", [1, 2])
 def test_odd_lengths_bf16(T, var):
