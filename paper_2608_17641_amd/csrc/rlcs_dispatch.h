@@ -176,9 +176,10 @@ rlcs_status dispatch_dt(Args& a, bool has_trunc, void* ws, size_t ws_bytes, hipS
         if ((N + p.rows_per_wg - 1) / p.rows_per_wg > INT32_MAX) return RLCS_ERR_INVALID_ARG;
         // Rows never straddle waves when T divides a wave's span (and is a multiple of K).
         p.wave_local = (T % K == 0 && (int64_t(kWave) * K) % T == 0) ? 1 : 0;
-        // When a workgroup's rows do not fill its chunks exactly, lanes outside its range skip
-        // their steps so that every chunk still takes the vector path (needs T a multiple of K).
-        p.pad = vec && Op::kStaged == 0 && T % K == 0 && (p.rows_per_wg * T) % E != 0;
+        // When a workgroup's rows do not fill its chunks exactly, every chunk still takes the
+        // vector path lane by lane: only the lanes at the ragged ends of the workgroup's range
+        // go element-wise.
+        p.pad = vec && Op::kStaged == 0 && T >= K && (T % K != 0 || (p.rows_per_wg * T) % E != 0);
     }
 
     if constexpr (Op::kFlags) {
@@ -202,7 +203,7 @@ rlcs_status dispatch(Args& a, rlcs_dtype dtype, bool has_trunc, void* ws, size_t
 
 // Rows with a row stride (period) above T: the rows kernel over the positions n * period + t
 // (the steps t >= T of each period are skipped), whole rows per workgroup; vector loads and
-// stores when T and the period are multiples of K and the arrays aligned, else element-wise.
+// stores where a lane's steps allow when the arrays are aligned, else element-wise.
 template <class Op>
 rlcs_status dispatch_strided_rows(Args& a, int64_t period, rlcs_dtype dtype, bool has_trunc,
                                   rlcs_stream_t stream) {
@@ -224,9 +225,9 @@ rlcs_status dispatch_strided_rows(Args& a, int64_t period, rlcs_dtype dtype, boo
         if ((a.N + p.rows_per_wg - 1) / p.rows_per_wg > INT32_MAX) return RLCS_ERR_INVALID_ARG;
         p.wave_local = 0;
         p.lds_bytes = 0;
-        // Vector path when every lane's K steps lie in one row or in one gap: T and the row
-        // stride multiples of K, data and outputs 16-byte aligned, flags K-byte aligned.
-        bool vec = a.T % K == 0 && period % K == 0;
+        // Vector path, lane by lane (lanes whose steps reach into a gap or past the range go
+        // element-wise): T >= K, data and outputs 16-byte aligned, flags K-byte aligned.
+        bool vec = a.T >= K;
         for (int i = 0; i < Op::kSlots; ++i)
             if (Op::slot_used(i, has_trunc) && !aligned(a.in[i], 16)) vec = false;
         if (!aligned(a.out0, 16) || (a.out1 && !aligned(a.out1, 16))) vec = false;

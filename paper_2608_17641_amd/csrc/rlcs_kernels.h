@@ -115,10 +115,13 @@ __device__ __forceinline__ void row_and_step(const RowBase& b, int64_t p, int64_
 // branch-free path: one vector load per input, issued back to back, and at most one row edge
 // per lane, whose per-row value is loaded unconditionally from a clamped row index. Other
 // chunks (the ragged ends of a range) take the masked element-wise path.
-// PAD: rows lie `a.period` steps apart (period >= T, both multiples of K), so a lane's K steps
-// are either all inside one row or all in the gap after it. Lanes in a gap, and lanes outside
-// the workgroup's range [lo, hi) (a multiple of K at both ends), skip their steps (no loads, the
-// identity map, no stores), so every chunk takes the vector path.
+// PAD: every chunk takes the vector path, lane by lane. Rows lie `a.period` steps apart
+// (period >= T; the steps t >= T of a period are a gap). A lane whose K steps are all in the
+// workgroup's range [lo, hi) and, with gaps, all among the first T steps of one row takes the
+// vector path; so does, without gaps, a lane at a ragged end of the range whose vector lies
+// inside the array (its steps outside the range are masked off: the identity map, no stores).
+// Any other lane (a vector that reaches into a gap or past the array, or one wholly outside
+// the range) takes the element-wise path for its steps in range, which may be none.
 template <class Op, typename DT, int K, int W, bool VEC, bool TR, bool PAD = false>
 struct Chunk {
     static_assert(!PAD || (VEC && Op::kStaged == 0), "padded rows: vector path, unstaged policies");
@@ -175,26 +178,30 @@ struct Chunk {
                               float (&nraw)[Op::kNbrRaw], PreFn&& pre) {
         const int64_t T = a.T;
         int64_t row = 0, t = 0;
+        uint32_t in_range = kAll;
         if constexpr (PAD) {
-            const bool inside = p0 >= lo && p0 < hi;
-            if (inside) row_and_step(base_of(), p0, a.period, a.inv_period, row, t);
-            if (!inside || t >= T) {  // outside the range, or in the gap between rows
-                valid = 0;
-                edge = 0;
-                ke_ = -1;
-                rv_raw_ = 0.f;
-                trunc = 0;
-#pragma unroll
-                for (int i = 0; i < (K + 3) / 4; ++i) { tw_[i] = 0u; rw_[i] = 0u; }
-#pragma unroll
-                for (int s = 0; s < NS; ++s)
-#pragma unroll
-                    for (int i = 0; i < kWords; ++i) w_[s][i] = 0u;
-                convert_full(a);
+            bool vector = p0 >= lo && p0 + K <= hi;
+            if (vector) {
+                row_and_step(base_of(), p0, a.period, a.inv_period, row, t);
+                if (a.period != T) vector = t + K <= T;
+            } else if (a.period == T && p0 + K > lo && p0 < hi && p0 >= 0 && p0 + K <= a.N * T) {
+                // a ragged end of a range without gaps, inside the array
+                vector = true;
+                if (p0 < lo) {
+                    in_range &= (kAll << uint32_t(lo - p0)) & kAll;
+                    const RowBase b = base_of();  // the row before the range's first one
+                    row_and_step(RowBase{b.pos - T, b.row - 1, b.t}, p0, T, a.inv_T, row, t);
+                } else {
+                    row_and_step(base_of(), p0, T, a.inv_T, row, t);
+                }
+                if (p0 + K > hi) in_range &= kAll >> uint32_t(p0 + K - hi);
+            }
+            if (!vector) {
+                load_masked(a, lo, hi, base_of, lane, nraw, pre);
                 return;
             }
         }
-        valid = kAll;
+        valid = in_range;
         // A missing optional array is read from in[0] instead (in bounds) and the value dropped.
         const uint8_t* fallback = reinterpret_cast<const uint8_t*>(a.in[0]);
         if (Op::kFlags && TR) load_flag_words<K>(a.trunc, p0, rw_);
@@ -403,9 +410,9 @@ struct Chunk {
         }
         float o0[K], o1[K];
         Op::template finish<K, TR>(a.p, d, term, trunc, edge, B, nb, A, X, o0, o1);
-        if (PAD && FULL && !valid) return kBack ? A[0] : A[K - 1];  // a gap between rows
-        store_k<K>(a.out0, p0, valid, FULL, o0);
-        if (a.out1) store_k<K>(a.out1, p0, valid, FULL, o1);
+        const bool vstore = FULL && (!PAD || valid == kAll);
+        store_k<K>(a.out0, p0, valid, vstore, o0);
+        if (a.out1) store_k<K>(a.out1, p0, valid, vstore, o1);
         return kBack ? A[0] : A[K - 1];
     }
 };

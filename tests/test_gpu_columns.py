@@ -312,10 +312,10 @@ def test_strided_rows_every_estimator(N, T, ld, v):
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("N,T,ld", [(100, 256, 320), (37, 64, 72), (6, 4096, 4160), (300, 8, 16),
-                                    (3, 2048, 2056)])
+                                    (3, 2048, 2056), (25, 33, 37), (9, 1001, 1003), (40, 100, 128)])
 def test_strided_rows_vector_path(N, T, ld, dtype):
-    """T and the row stride multiples of the vector width, aligned storage: the vector path of
-    the rows kernel, whose lanes in the gaps between rows skip their steps. Every estimator
+    """Aligned storage: the vector path of the rows kernel, lane by lane (lanes whose steps reach
+    into the gaps between rows go element-wise, lanes wholly in a gap skip). Every estimator
     against the oracle; the gaps of the outputs are never written."""
     ro = workloads.make_rollout(N, T, seed=N * 7 + T, dtype=dtype, p_term=0.05, p_trunc=0.05)
     d = {k: (strided_rows(to_device(a, DEV), ld) if a.ndim == 2 else to_device(a, DEV))
