@@ -125,11 +125,14 @@ struct MaskedChunk {
     Tri incl;
     int64_t p0;
 
-    // Steps of a chunk whose K steps are all in range, 16-byte aligned data and T >= K: vector
-    // loads, every one issued before the first use; at most one row edge.
-    __device__ __forceinline__ void load_full(const MaskedArgs& ma, const RowBase& base) {
+    // Vector loads of the lane's K steps (16-byte aligned data, T >= K, all K steps inside the
+    // array; `base` a row start at or before p0), every one issued before the first use; at most
+    // one row edge. `in_range` selects the steps that are the lane's: all, or those of a ragged
+    // end of the workgroup's range.
+    __device__ __forceinline__ void load_full(const MaskedArgs& ma, const RowBase& base,
+                                              uint32_t in_range) {
         const Args& a = ma.a;
-        valid = kAll;
+        valid = in_range;
         const uint8_t* fallback = reinterpret_cast<const uint8_t*>(a.in[0]);
         uint32_t tw[(K + 3) / 4], rw[(K + 3) / 4], mw[(K + 3) / 4];
         if (TR) load_flag_words<K>(a.trunc, p0, rw);
@@ -207,7 +210,8 @@ struct MaskedChunk {
     }
 
     // Outputs given Xw, the state entering the wave's span; returns the state at the lane's
-    // first step. Accumulates the advantages that take part into (n, sum, sumsq).
+    // first step. Accumulates the advantages that take part into (n, sum, sumsq). `full`: the
+    // lane's steps are vector-aligned (stored as vectors when all of them are the lane's).
     template <bool STATS>
     __device__ __forceinline__ AW finish(const Args& a, AW Xw, bool full, double& n, double& s1,
                                          double& s2) {
@@ -225,8 +229,9 @@ struct MaskedChunk {
                 s2 = fma(d, d, s2);
             }
         }
-        store_k<K>(a.out0, p0, valid, full, adv);
-        if (a.out1) store_k<K>(a.out1, p0, valid, full, ret);
+        const bool vstore = full && valid == kAll;
+        store_k<K>(a.out0, p0, valid, vstore, adv);
+        if (a.out1) store_k<K>(a.out1, p0, valid, vstore, ret);
         return x;
     }
 };
@@ -262,8 +267,30 @@ __global__ void __launch_bounds__(W * kWave) masked_gae_kernel(MaskedArgs ma, in
         MaskedChunk<DT, K, TR, HM> c;
         c.p0 = chunk_lo + (int64_t(wave) * kWave + (kWave - 1 - lane)) * K;
         const bool full = can_full && chunk_lo >= lo && chunk_hi <= hi;
-        if (full) c.load_full(ma, base);
-        else c.load_masked(ma, base, lo, hi);
+        if (full) {
+            c.load_full(ma, base, MaskedChunk<DT, K, TR, HM>::kAll);
+        } else if (can_full) {
+            // lane by lane: vector loads wherever the lane's K steps lie inside the array (the
+            // steps outside the range masked off), element-wise otherwise
+            constexpr uint32_t kAll = MaskedChunk<DT, K, TR, HM>::kAll;
+            const int64_t p = c.p0;
+            if (p >= lo && p + K <= hi) {
+                c.load_full(ma, base, kAll);
+            } else if (p + K > lo && p < hi && p >= 0 && p + K <= a.N * a.T) {
+                uint32_t m = kAll;
+                RowBase b = base;
+                if (p < lo) {
+                    m &= (kAll << uint32_t(lo - p)) & kAll;
+                    b = RowBase{base.pos - a.T, base.row - 1, base.t};  // the row before
+                }
+                if (p + K > hi) m &= kAll >> uint32_t(p + K - hi);
+                c.load_full(ma, b, m);
+            } else {
+                c.load_masked(ma, base, lo, hi);
+            }
+        } else {
+            c.load_masked(ma, base, lo, hi);
+        }
         const Tri incl = c.local(a.p, lane);
         Tri win = identity_tri();
         if (!wave_local) {
@@ -275,7 +302,7 @@ __global__ void __launch_bounds__(W * kWave) masked_gae_kernel(MaskedArgs ma, in
             for (int w = W - 1; w > wave; --w)
                 win = compose(Tri{s_m[0][w], s_m[1][w], s_m[2][w], s_m[3][w], s_m[4][w]}, win);
         }
-        const AW first = c.template finish<STATS>(a, apply(win, carry), full, n, s1, s2);
+        const AW first = c.template finish<STATS>(a, apply(win, carry), can_full, n, s1, s2);
         if (chunk_lo <= lo) break;
         // the next chunk (earlier in time) continues from the state at chunk_lo, held by lane
         // 63 of wave 0
