@@ -60,6 +60,10 @@ struct ColGeom {
 constexpr int kColK = 8;  // steps per lane
 constexpr int kColW = 4;  // waves per workgroup (time sub-spans of a chunk)
 constexpr int kColL = kColK * kColW;  // steps per chunk
+// Split columns: waves per workgroup of the one-tile-per-workgroup kernel, whose tiles are
+// twice as long as a whole-column walk's chunks (fewer tiles to chain, more steps in flight)
+constexpr int kColSplitW = 8;
+constexpr int kColSplitL = kColK * kColSplitW;
 
 // One lane's K steps of one column.
 template <class Op, typename DT, int K, bool TR>

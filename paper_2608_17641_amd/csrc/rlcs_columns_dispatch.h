@@ -14,13 +14,15 @@ namespace host {
 constexpr int64_t kColSerialBlocks = kWsSlots;
 
 inline int64_t col_tiles(int64_t T) { return (T + kColL - 1) / kColL; }
+inline int64_t col_split_tiles(int64_t T) { return (T + kColSplitL - 1) / kColSplitL; }
 
 // Whole-column walks of at least this many chunks overlap each chunk's loads with the scan of
 // the one before (shorter ones gain less than the unconditional continuation reads cost).
 constexpr int64_t kColPipeChunks = 8;
 
 // Workspace bytes of a split column call: header and block slots, then two records per column
-// per tile (0 if the size does not fit in size_t).
+// per 32-step span (a bound on the split tiles, which are longer; 0 if the size does not fit in
+// size_t).
 inline size_t col_ws_need(int64_t J, int64_t T) {
     const int64_t P = col_tiles(T);
     if (J <= 0 || P <= 0) return kWsRecordsOffset;
@@ -32,8 +34,9 @@ template <class Op, typename DT, bool TR>
 void col_launch(const Args& a, const ColGeom& g, bool split, int64_t blocks, hipStream_t s) {
     const dim3 block(kColW * kWave);
     if (split) {
-        hipLaunchKernelGGL((cols_tiles_kernel<Op, DT, kColK, kColW, TR>),
-                           dim3(unsigned(blocks * col_tiles(a.T))), block, 0, s, a, g, blocks);
+        hipLaunchKernelGGL((cols_tiles_kernel<Op, DT, kColK, kColSplitW, TR>),
+                           dim3(unsigned(blocks * col_split_tiles(a.T))), dim3(kColSplitW * kWave),
+                           0, s, a, g, blocks);
     } else if (col_tiles(a.T) >= kColPipeChunks) {
         hipLaunchKernelGGL((cols_rows_kernel<Op, DT, kColK, kColW, TR, true>), dim3(unsigned(blocks)),
                            block, 0, s, a, g);
@@ -62,6 +65,7 @@ rlcs_status col_dispatch(Args& a, const ColGeom& g, rlcs_dtype dtype, bool has_t
     } else {
         split = P > 1 && ws_ok && blocks < kColSerialBlocks;
     }
+    if (split && col_split_tiles(a.T) == 1) split = false;  // one tile: a whole-column walk
     if (split) {
         if (blocks * P > INT32_MAX) return RLCS_ERR_INVALID_ARG;
         a.ws = ws;
