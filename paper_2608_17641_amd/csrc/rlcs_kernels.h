@@ -180,11 +180,14 @@ struct Chunk {
         int64_t row = 0, t = 0;
         uint32_t in_range = kAll;
         if constexpr (PAD) {
-            bool vector = p0 >= lo && p0 + K <= hi;
-            if (vector) {
+            bool vector = false, skip = false;
+            if (p0 >= lo && p0 + K <= hi) {
                 row_and_step(base_of(), p0, a.period, a.inv_period, row, t);
-                if (a.period != T) vector = t + K <= T;
-            } else if (a.period == T && p0 + K > lo && p0 < hi && p0 >= 0 && p0 + K <= a.N * T) {
+                if (a.period == T || t + K <= T) vector = true;
+                else skip = t >= T && t + K <= a.period;  // wholly in a gap
+            } else if (p0 + K <= lo || p0 >= hi) {
+                skip = true;  // wholly outside the range
+            } else if (a.period == T && p0 >= 0 && p0 + K <= a.N * T) {
                 // a ragged end of a range without gaps, inside the array
                 vector = true;
                 if (p0 < lo) {
@@ -195,6 +198,21 @@ struct Chunk {
                     row_and_step(base_of(), p0, T, a.inv_T, row, t);
                 }
                 if (p0 + K > hi) in_range &= kAll >> uint32_t(p0 + K - hi);
+            }
+            if (skip) {  // no step to do: no loads, the identity map, no stores
+                valid = 0;
+                edge = 0;
+                ke_ = -1;
+                rv_raw_ = 0.f;
+                trunc = 0;
+#pragma unroll
+                for (int i = 0; i < (K + 3) / 4; ++i) { tw_[i] = 0u; rw_[i] = 0u; }
+#pragma unroll
+                for (int s = 0; s < NS; ++s)
+#pragma unroll
+                    for (int i = 0; i < kWords; ++i) w_[s][i] = 0u;
+                convert_full(a);
+                return;
             }
             if (!vector) {
                 load_masked(a, lo, hi, base_of, lane, nraw, pre);
