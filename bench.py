@@ -72,6 +72,31 @@ def parse():
     return ap.parse_args()
 
 
+def copy_reference(nbytes, sets, steps, dev):
+    """A plain device copy moving the same number of bytes per step as the timed kernel (half
+    read, half written), timed the same way: `steps` copies replayed from a HIP graph over
+    `sets` rotated buffer pairs (cold HBM). The ceiling a streaming kernel of this size meets."""
+    import torch
+    n = nbytes // 8  # float32 elements per buffer: n * 4 bytes read and n * 4 written
+    bufs = [(torch.ones(n, device=dev), torch.empty(n, device=dev)) for _ in range(sets)]
+    for i in range(3):
+        bufs[i % sets][1].copy_(bufs[i % sets][0])
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for i in range(steps):
+            src, dst = bufs[i % sets]
+            dst.copy_(src)
+    g.replay()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(); g.replay(); b.record()
+    torch.cuda.synchronize()
+    us = a.elapsed_time(b) * 1e3 / steps
+    del g, bufs
+    return us
+
+
 def cpu_baseline(ro, seconds):
     """The fp64 oracle on the same workload, single thread, repeated for about `seconds`."""
     import oracle
@@ -781,6 +806,10 @@ def main():
             ts.append(a.elapsed_time(b))
         trials.append(float(np.median(ts)))
     print(f"full-call (per-call events, min of 5 medians): {min(trials) * 1e3:.2f} us", file=sys.stderr)
+    copy_us = copy_reference(nbytes, S, args.steps, dev)
+    print(f"copy reference (same bytes, half read, half written, cold): {copy_us:.3f} us = "
+          f"{nbytes / copy_us / 1e3:.1f} GB/s; the kernel takes {per_step_s * 1e6 / copy_us:.3f}x its time",
+          file=sys.stderr)
 
     out = {
         "metric": METRIC,
@@ -803,6 +832,9 @@ def main():
         "roofline": {"bound": "hbm", "achieved": round(gbs, 2), "peak": PEAK_HBM_GBS,
                      "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
                      "traffic": recorded_traffic()},
+        "copy_reference": {"kernel": "torch copy_, algorithmic_bytes/2 read and written, cold",
+                           "us": round(copy_us, 3), "GB/s": round(nbytes / copy_us / 1e3, 1),
+                           "kernel_time_over_copy": round(per_step_s * 1e6 / copy_us, 3)},
     }
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(ro, args.cpu_seconds)
