@@ -126,17 +126,19 @@ def test_tree_scan_equals_sequential_oracle_exactly(T):
     """On dyadic inputs small enough that every partial result is exact, the log-depth scan
     by combine and the oracle's sequential recurrence agree bitwise, carry included."""
     rng = np.random.default_rng(T)
-    for _ in range(5):
-        a = rng.integers(-8, 9, size=T) / 4.0
-        b = rng.integers(0, 3, size=T) / 2.0  # 0, 0.5, 1: products stay dyadic
-        carry = float(rng.integers(-8, 9) / 4.0)
-        seq = oracle.affine_scan(a[None], b[None], np.array([carry]), reverse=True)[0]
-        tree = scan_algebra.scan_backward_by_combine(list(a), list(b), carry)
-        assert list(seq) == tree
+    # five rows in one call: each row is its own recurrence with its own carry
+    a = rng.integers(-8, 9, size=(5, T)) / 4.0
+    b = rng.integers(0, 3, size=(5, T)) / 2.0  # 0, 0.5, 1: products stay dyadic
+    carry = rng.integers(-8, 9, size=5) / 4.0
+    seq = oracle.affine_scan(a, b, carry, reverse=True)
+    fwd = oracle.affine_scan(a, b, carry, reverse=False)
+    for n in range(5):
+        tree = scan_algebra.scan_backward_by_combine(list(a[n]), list(b[n]), float(carry[n]))
+        assert list(seq[n]) == tree
         # forward mirror: reverse the arrays
-        fwd = oracle.affine_scan(a[None], b[None], np.array([carry]), reverse=False)[0]
-        tree_f = scan_algebra.scan_backward_by_combine(list(a[::-1]), list(b[::-1]), carry)[::-1]
-        assert list(fwd) == tree_f
+        tree_f = scan_algebra.scan_backward_by_combine(list(a[n][::-1]), list(b[n][::-1]),
+                                                       float(carry[n]))[::-1]
+        assert list(fwd[n]) == tree_f
 
 
 # ---------------------------------------------------------------- brute force, exhaustive
@@ -524,6 +526,7 @@ def test_retrace_full_brute_force(A):
     act = ro["actions"].copy()
     act[::7, ::3] = A + 2      # out of range: selects nothing
     act[1::9, 1::4] = -1
+    act[2::11, 2::5] = A       # the first index past the last action
     c_bar = 0.8
     dl, qr = oracle.retrace_full(ro["r"], ro["q3"], ro["pi3"], act, ro["mu"], ro["term"],
                                  ro["trunc"], ro["bv"], ro["boot"], gamma=G, lam=L, c_bar=c_bar)
@@ -765,3 +768,84 @@ def test_normalize_advantages_exact_moments():
     one = np.zeros_like(mask); one[3, 4] = 1
     out1 = oracle.normalize_advantages(adv, one, eps=eps)
     rtol_close(out1, (adv - adv[3, 4]) / math.sqrt(oracle.param(eps)))
+
+
+# ---------------------------------------------------------------- memory discipline
+
+def test_oracle_writes_only_its_outputs():
+    """Every oracle routine writes exactly its [N, T] outputs: called through the C ABI with
+    output buffers that carry 32 sentinel doubles before and after, the sentinels survive and
+    every output element is written."""
+    import ctypes
+    lib = oracle._load()
+    N, T, A, F, G = 3, 9, 4, 2, 32
+    rng = np.random.default_rng(5)
+    D, U8, I32 = ctypes.c_double, ctypes.c_uint8, ctypes.c_int32
+    keep = []
+
+    def data(*shape):
+        x = np.ascontiguousarray(rng.normal(size=shape))
+        keep.append(x)
+        return x.ctypes.data_as(ctypes.POINTER(D))
+
+    def flags(p):
+        f = np.ascontiguousarray((rng.random((N, T)) < p).astype(np.uint8))
+        keep.append(f)
+        return f.ctypes.data_as(ctypes.POINTER(U8))
+
+    def out(n):
+        buf = np.full(n + 2 * G, 12345.0)
+        buf[G:G + n] = np.nan
+        keep.append(buf)
+        return buf, buf[G:].ctypes.data_as(ctypes.POINTER(D))
+
+    def check(bufs, n):
+        for buf in bufs:
+            assert np.all(buf[:G] == 12345.0) and np.all(buf[G + n:] == 12345.0)
+            assert np.all(np.isfinite(buf[G:G + n]))
+
+    g, lam = 0.99, 0.95
+    nt = N * T
+    o1, p1 = out(nt); o2, p2 = out(nt)
+    lib.oracle_gae(data(N, T), data(N, T), flags(0.2), flags(0.2), data(N, T), data(N), p1, p2, N, T, g, lam)
+    check((o1, o2), nt)
+    o1, p1 = out(nt)
+    lib.oracle_td_lambda(data(N, T), data(N, T), flags(0.2), flags(0.2), data(N, T), data(N), p1, N, T, g, lam)
+    check((o1,), nt)
+    o1, p1 = out(nt)
+    lib.oracle_discounted(data(N, T), flags(0.2), flags(0.2), data(N, T), data(N), p1, N, T, g)
+    check((o1,), nt)
+    o1, p1 = out(nt); o2, p2 = out(nt)
+    lib.oracle_vtrace(data(N, T), data(N, T), data(N, T), flags(0.2), flags(0.2), data(N, T), data(N),
+                      p1, p2, N, T, g, 1.0, 1.0)
+    check((o1, o2), nt)
+    o1, p1 = out(nt); o2, p2 = out(nt)
+    lib.oracle_retrace(data(N, T), data(N, T), data(N, T), data(N, T), flags(0.2), flags(0.2), data(N, T),
+                       data(N), p1, p2, N, T, g, lam, 1.0)
+    check((o1, o2), nt)
+    acts = np.ascontiguousarray(rng.integers(-1, A + 1, size=(N, T)).astype(np.int32))
+    mu = np.ascontiguousarray(rng.uniform(0.1, 1.0, size=(N, T)))
+    keep += [acts, mu]
+    o1, p1 = out(nt); o2, p2 = out(nt)
+    lib.oracle_retrace_full(data(N, T), data(N, T, A), data(N, T, A), acts.ctypes.data_as(ctypes.POINTER(I32)),
+                            mu.ctypes.data_as(ctypes.POINTER(D)), flags(0.2), flags(0.2), data(N, T), data(N),
+                            p1, p2, N, T, A, g, lam, 1.0)
+    check((o1, o2), nt)
+    o1, p1 = out(nt)
+    lib.oracle_elig_trace(data(N, T), flags(0.2), flags(0.2), p1, N, T, g, lam)
+    check((o1,), nt)
+    o1, p1 = out(nt * F)
+    lib.oracle_elig_trace_vec(data(N, T, F), flags(0.2), flags(0.2), p1, N, T, F, g, lam)
+    check((o1,), nt * F)
+    o1, p1 = out(nt); o2, p2 = out(nt)
+    lib.oracle_gae_masked(data(N, T), data(N, T), flags(0.6), flags(0.2), flags(0.2), data(N, T), data(N),
+                          p1, p2, N, T, g, lam)
+    check((o1, o2), nt)
+    for starts_at in (0, 1):
+        o1, p1 = out(nt)
+        lib.oracle_episodic_prefix(data(N, T), flags(0.2), flags(0.2), p1, N, T, starts_at)
+        check((o1,), nt)
+    for reverse in (0, 1):
+        o1, p1 = out(nt)
+        lib.oracle_affine_scan(data(N, T), data(N, T), data(N), p1, N, T, reverse)
+        check((o1,), nt)
