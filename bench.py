@@ -14,7 +14,8 @@ Cold HBM: the timed steps rotate over enough independent input/output sets (well
 Prints one JSON line on stdout:
   value      effective bandwidth = algorithmic bytes / (timed time / K), GB/s
   roofline   the same figure against the 8 TB/s HBM peak
-  cpu_baseline  the fp64 oracle on the host, single thread, on a bounded sample
+  cpu_baseline  the fp64 oracle on the host, rows split over the host's cores (the single-thread
+                rate in its `sample`), each timed for about --cpu-seconds
 """
 from __future__ import annotations
 
@@ -98,26 +99,42 @@ def copy_reference(nbytes, sets, steps, dev):
 
 
 def cpu_baseline(ro, seconds):
-    """The fp64 oracle on the same workload, single thread, repeated for about `seconds`."""
+    """The fp64 oracle on the same workload, repeated for about `seconds` each way: on one
+    thread, and with the rows split over the host's cores (at most 16 threads; the oracle's C
+    calls release the GIL). Reported: the all-cores rate, the single-thread one in `sample`."""
+    import concurrent.futures as cf
     import oracle
     a = (ro["r"], ro["v"], ro["term"], ro["trunc"], ro["bv"], ro["boot"])
     oracle.gae(*a, gamma=GAMMA, lam=LAM)  # warm-up (also builds/loads the library)
-    reps, t0 = 0, time.perf_counter()
-    while True:
-        oracle.gae(*a, gamma=GAMMA, lam=LAM)
-        reps += 1
-        el = time.perf_counter() - t0
-        if el >= seconds:
-            break
-    per_call = el / reps
+
+    def timed(fn):
+        reps, t0 = 0, time.perf_counter()
+        while True:
+            fn()
+            reps += 1
+            el = time.perf_counter() - t0
+            if el >= seconds:
+                return el / reps, reps, el
+
+    one, reps1, el1 = timed(lambda: oracle.gae(*a, gamma=GAMMA, lam=LAM))
+    threads = max(1, min(16, len(os.sched_getaffinity(0))))
+    bounds = np.linspace(0, N, threads + 1).astype(int)
+    slices = [tuple(x[lo:hi] for x in a) for lo, hi in zip(bounds[:-1], bounds[1:])]
+    with cf.ThreadPoolExecutor(threads) as ex:
+        def all_rows():
+            list(ex.map(lambda sl: oracle.gae(*sl, gamma=GAMMA, lam=LAM), slices))
+        all_rows()
+        par, reps, el = timed(all_rows)
+    nbytes = algorithmic_bytes(N, T)
     return {
-        "value": round(algorithmic_bytes(N, T) / per_call / 1e9, 3),
+        "value": round(nbytes / par / 1e9, 3),
         "unit": "GB/s",
-        "cores": 1,
+        "cores": threads,
         "kind": "oracle",
-        "sample": f"GAE {N}x{T} fp32+trunc, full workload repeated {reps}x in {el:.1f} s "
-                  f"(fp64 sequential C, {per_call * 1e3:.1f} ms/call, "
-                  f"{N * T / per_call / 1e9:.4f} Gsteps/s)",
+        "sample": f"GAE {N}x{T} fp32+trunc, full workload: {threads} threads (rows split), "
+                  f"{reps}x in {el:.1f} s, {par * 1e3:.2f} ms/call, {N * T / par / 1e9:.3f} Gsteps/s; "
+                  f"1 thread: {reps1}x in {el1:.1f} s, {one * 1e3:.1f} ms/call, "
+                  f"{nbytes / one / 1e9:.3f} GB/s, {N * T / one / 1e9:.4f} Gsteps/s (fp64 sequential C)",
     }
 
 
