@@ -218,10 +218,11 @@ rlcs_status dispatch_strided_rows(Args& a, int64_t period, rlcs_dtype dtype, boo
         Plan p{};
         p.split = false;
         const int64_t E_small = int64_t(kSmallWaves) * kWave * K;
-        p.waves = (period <= E_small) ? kSmallWaves : kLargeWaves;
+        p.waves = (a.T <= E_small) ? kSmallWaves : kLargeWaves;
         const int64_t E = int64_t(p.waves) * kWave * K;
         const int64_t slack = (period % K == 0) ? 0 : K - 1;
-        p.rows_per_wg = (period <= E - slack) ? (E - slack) / period : 1;
+        // as many rows as fit in one chunk: the last one's gap is not part of the range
+        p.rows_per_wg = (a.T <= E - slack) ? (E - slack - a.T) / period + 1 : 1;
         if ((a.N + p.rows_per_wg - 1) / p.rows_per_wg > INT32_MAX) return RLCS_ERR_INVALID_ARG;
         p.wave_local = 0;
         p.lds_bytes = 0;

@@ -598,7 +598,8 @@ __global__ void __launch_bounds__(W * kWave) rows_kernel(Args a, int64_t rows_pe
     const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
     const int64_t row_lo = int64_t(blockIdx.x) * rows_per_wg;
     const int64_t row_hi = min(row_lo + rows_per_wg, a.N);
-    const int64_t lo = row_lo * a.period, hi = row_hi * a.period;
+    // the range ends at the last row's last step (rows lie `period` apart; its gap is not part)
+    const int64_t lo = row_lo * a.period, hi = (row_hi - 1) * a.period + a.T;
     const bool can_full = VEC && a.T >= K && (PAD || a.period == a.T);
     float carry = 0.f;
     auto carry_of = [&]() { return carry; };
