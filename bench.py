@@ -54,6 +54,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=200)
     ap.add_argument("--sets", type=int, default=32, help="rotated input/output sets (cold HBM)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-context", action="store_true",
+                    help="skip the context measurements (full-call timing, copy reference, warm "
+                         "figure): for kernel-trace runs, which then see only the cold timed path")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--extra", action="store_true",
                     help="time every estimator of every workload (table on stderr, no JSON line)")
@@ -810,8 +813,39 @@ def main():
     nbytes = algorithmic_bytes(N, T)
     gbs = nbytes / per_step_s / 1e9
 
-    # Context (stderr): full-call time of one eager call through the Python binding, the
-    # paper's protocol (per-call events, median of 50, min over 5 trials).
+    out = {
+        "metric": METRIC,
+        "value": round(gbs, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(total_ms / args.steps, 6),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"GAE {N}x{T} fp32, term+trunc, bootstrap, cold HBM ({S} rotated input/output sets)",
+                   "N": N, "T": T, "algorithmic_bytes": nbytes,
+                   "gsteps_per_s": round(N * T / per_step_s / 1e9, 2),
+                   "pct_of_peak": round(100 * gbs / PEAK_HBM_GBS, 2)},
+        "roofline": {"bound": "hbm", "achieved": round(gbs, 2), "peak": PEAK_HBM_GBS,
+                     "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
+                     "traffic": recorded_traffic()},
+    }
+    if not args.no_context:
+        out.update(context(step, nbytes, per_step_s, S, args, dev, start, end))
+    if not args.no_cpu:
+        out["cpu_baseline"] = cpu_baseline(ro, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+def context(step, nbytes, per_step_s, S, args, dev, start, end):
+    """Context figures next to the headline (also on stderr): the full-call time of one eager
+    call through the Python binding by the paper's protocol (per-call events, median of 50, min
+    over 5 trials), a plain copy of the same bytes, and the warm (cache-resident) step."""
+    import torch
     trials = []
     for _ in range(5):
         ts = []
@@ -840,37 +874,13 @@ def main():
     del wgraph
     print(f"warm (one set, Infinity-Cache resident): {warm_us:.3f} us = {nbytes / warm_us / 1e3:.1f} GB/s "
           f"effective", file=sys.stderr)
-
-    out = {
-        "metric": METRIC,
-        "value": round(gbs, 2),
-        "unit": "GB/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": round(total_ms / args.steps, 6),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "f32",
-        "data": "synthetic",
-        "config": {"workload": f"GAE {N}x{T} fp32, term+trunc, bootstrap, cold HBM "
-                               f"({S} rotated input/output sets)",
-                   "N": N, "T": T, "algorithmic_bytes": nbytes,
-                   "gsteps_per_s": round(N * T / per_step_s / 1e9, 2),
-                   "pct_of_peak": round(100 * gbs / PEAK_HBM_GBS, 2)},
-        "roofline": {"bound": "hbm", "achieved": round(gbs, 2), "peak": PEAK_HBM_GBS,
-                     "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
-                     "traffic": recorded_traffic()},
+    return {
         "copy_reference": {"kernel": "torch copy_, algorithmic_bytes/2 read and written, cold",
                            "us": round(copy_us, 3), "GB/s": round(nbytes / copy_us / 1e3, 1),
                            "kernel_time_over_copy": round(per_step_s * 1e6 / copy_us, 3)},
         "warm": {"what": "same steps on one input/output set, Infinity-Cache resident (context only)",
                  "us": round(warm_us, 3), "GB/s": round(nbytes / warm_us / 1e3, 1)},
     }
-    if not args.no_cpu:
-        out["cpu_baseline"] = cpu_baseline(ro, args.cpu_seconds)
-    print(json.dumps(out), flush=True)
 
 
 if __name__ == "__main__":
