@@ -405,6 +405,13 @@ def run_extra(dev, only=""):
     plan.append(("all7_4096x32", 4096, 32, "f32", dict(p_term=0.02, p_trunc=0.01), True, True, 0.99, 0.95, seven))
     plan.append(("4096x256", 4096, 256, "f32", dict(p_term=0.02, p_trunc=0.01), True, True, 0.99, 0.95, ("gae", "vtrace")))
     plan.append(("rlhf_64x4096", 64, 4096, "f32", None, False, False, 1.0, 0.95, ("gae", "td_lambda")))
+    # rows that do not fill a workgroup's chunks: the lane-by-lane vector path
+    plan.append(("ragged_4096x255", 4096, 255, "f32", dict(p_term=0.02, p_trunc=0.01), True, True, 0.99, 0.95,
+                 ("gae", "vtrace", "elig_trace")))
+    plan.append(("ragged_1024x1001", 1024, 1001, "f32", dict(p_term=0.02, p_trunc=0.01), True, True, 0.99, 0.95,
+                 ("gae",)))
+    plan.append(("ragged_bf16_16384x100", 16384, 100, "bf16", dict(p_term=0.005, p_trunc=0.005), True, True, 0.99,
+                 0.95, ("gae", "retrace")))
     for n_ in (16384, 65536):
         for t_ in (64, 512, 2048):
             plan.append((f"bf16_{n_}x{t_}", n_, t_, "bf16", dict(p_term=0.005, p_trunc=0.005), True, True, 0.99, 0.95, seven))
