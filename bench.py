@@ -216,10 +216,10 @@ def summarize_counters(fetch_dir, write_dir):
     lines = [
         f"# HBM traffic of {KERNEL_TAG}",
         f"# workload: GAE {N}x{T} fp32, term+trunc, bootstrap (bench.py --profile-pass)",
-        "commands (repo root, GPU box):",
-        "  rocprofv3 --pmc FETCH_SIZE -d gpurun_out/pmc_fetch -o run -- python bench.py --profile-pass --steps 200 --warmup 20",
-        "  rocprofv3 --pmc WRITE_SIZE -d gpurun_out/pmc_write -o run -- python bench.py --profile-pass --steps 200 --warmup 20",
-        "  python bench.py --summarize-counters gpurun_out/pmc_fetch gpurun_out/pmc_write",
+        "commands (repo root, on the MI355X host):",
+        "  rocprofv3 --pmc FETCH_SIZE -d prof/pmc_fetch -o run -- python bench.py --profile-pass --steps 200 --warmup 20",
+        "  rocprofv3 --pmc WRITE_SIZE -d prof/pmc_write -o run -- python bench.py --profile-pass --steps 200 --warmup 20",
+        "  python bench.py --summarize-counters prof/pmc_fetch prof/pmc_write",
         f"FETCH_SIZE_KiB_per_dispatch: {fetch[0]:.1f}",
         f"FETCH_SIZE_dispatches: {fetch[1]}",
         f"FETCH_SIZE_copy_KiB: {fetch[2]:.1f}",
@@ -734,7 +734,7 @@ def main():
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); rows are independent, so "
-              "a multi-GPU run would shard rows with no exchange and is not part of this build.",
+              "a multi-GPU run would shard rows with no exchange and is not implemented.",
               file=sys.stderr)
         sys.exit(2)
 
