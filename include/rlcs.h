@@ -294,8 +294,8 @@ rlcs_status rlcs_elig_trace_vec(const void* x, const uint8_t* term, const uint8_
                                 rlcs_stream_t stream);
 
 /* Workspace bytes for the strided calls (columns = N) and rlcs_elig_trace_vec
- * (columns = N * F) over T steps: the fixed 65600-byte part plus 16 bytes per column per
- * 32-step tile; 0 for negative sizes or a size that overflows. */
+ * (columns = N * F) over T steps: the fixed 65600-byte part plus 16 bytes per column per 32
+ * steps (rounded up); 0 for negative sizes or a size that overflows. */
 size_t rlcs_workspace_size_columns(int64_t columns, int64_t T);
 
 /* Static description of a status code. Never NULL. */

@@ -21,8 +21,8 @@
 //   5. take the value entering the chunk (previous chunk of the same workgroup, or the
 //      published maps of other workgroups' tiles) and finish the K steps; store.
 // cols_rows_kernel walks all of T in chunks (carry through LDS); cols_tiles_kernel gives each
-// chunk its own workgroup and carries between them with the workspace protocol of the split-row
-// kernel, per column: a tile publishes its 64 composed maps and composes the maps of the tiles
+// tile (kColSplitW waves, twice a walk's chunk) its own workgroup and carries between them with
+// the workspace protocol of the split-row kernel, per column: a tile publishes its 64 composed maps and composes the maps of the tiles
 // on its carry-source side, nearest first, until it meets beta = 0 (an episode or row edge).
 // Tiles only ever wait for tiles of their own column block, so each block has its own ticket
 // counter: tickets order the block's tiles from the carry source, and no counter is touched by

@@ -13,7 +13,9 @@
 //   7. the policy's epilogue and one vector store per output.
 //
 // rows kernel  : each workgroup owns whole rows and walks them chunk by chunk from the carry
-//                source, passing the carry between chunks in LDS. Needs no workspace.
+//                source, passing the carry between chunks in LDS. Needs no workspace. Rows
+//                may also lie a stride (`period`) apart; with PAD, chunks that the rows do not
+//                fill exactly still run vector loads, each lane deciding for itself (Chunk).
 // tiles kernel : each workgroup owns one chunk ("tile") of the flat array, wherever rows start
 //                or end. A tile whose edge step is not a row edge needs the carry from the
 //                tiles after it (backward) or before it (forward) in the same row: every tile
