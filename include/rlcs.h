@@ -25,7 +25,8 @@
  * Outputs    Must not overlap any input or each other. An output documented as optional may
  *            be NULL, in which case it is not written.
  * Alignment  Every pointer must be aligned to its element size. 16-byte aligned data pointers
- *            (and 4-byte aligned flag pointers) take the vectorised path; others a slower one.
+ *            (and flag pointers aligned to 4 bytes for float32, 8 for bfloat16) take the
+ *            vectorised path; others a slower one.
  * Sizes      N >= 0, 0 <= T <= 2^30, N*T representable. N == 0 or T == 0 is a no-op returning
  *            RLCS_OK.
  * Params     Discount gamma and trace parameter lambda must lie in [0, 1]; clipping
