@@ -80,3 +80,14 @@ def test_summarize_extra_rejects_mismatch(tmp_path):
     mp.write_text(json.dumps([{"label": "a", "name": "x", "calls": 1, "bytes": 1, "steps": 1}] * 2))
     with pytest.raises(SystemExit):
         bench.summarize_extra(str(tmp_path / "t"), str(tmp_path / "f"), str(tmp_path / "w"), str(mp))
+
+
+def test_bench_refuses_more_than_one_gpu():
+    """The bench measures one GPU: any other --gpus exits with status 2 and says why, before
+    touching a GPU."""
+    import subprocess
+    import sys
+    r = subprocess.run([sys.executable, os.path.join(os.path.dirname(bench.__file__), "bench.py"),
+                        "--gpus", "2"], capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr and r.stdout == ""
