@@ -1,0 +1,102 @@
+"""Seeded random GPU parity sweep: 160 cases drawn from one fixed seed, each one estimator on one
+shape, dtype, flag density, layout (row-major, strided rows, time-major) and kernel variant,
+against the fp64 oracle on the same inputs. The cases cover what hand-picked shapes can miss:
+odd sizes, rows that straddle vectors and workgroups, row strides and time-major strides of any
+residue, optional inputs present or not. Each case prints itself before it runs."""
+import numpy as np
+import pytest
+
+from cases import TOL, assert_parity, oracle_run, to_device
+import workloads
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+import paper_2608_17641_amd as rl  # noqa: E402
+
+DEV = torch.device("cuda:0")
+NAMES = ("gae", "vtrace", "retrace", "td_lambda", "discounted", "elig_trace", "prefix_ends",
+         "prefix_starts")
+OUT_KEYS = {"gae": ("adv", "ret"), "vtrace": ("vs", "pg"), "retrace": ("delta", "q_ret"),
+            "td_lambda": ("ret",), "discounted": ("ret",), "elig_trace": ("z",),
+            "prefix_ends": ("c",), "prefix_starts": ("c",)}
+
+
+def _cases(n=160):
+    rng = np.random.default_rng(20261202)
+    out = []
+    for i in range(n):
+        layout = ("rows", "strided", "tm")[rng.integers(0, 3)]
+        N = int(rng.choice([1, 2, 3, 7, 16, 33, 64, 100, 257, 600]))
+        T = int(rng.choice([1, 2, 3, 4, 5, 8, 31, 33, 64, 100, 255, 256, 257, 1000, 1025, 3000]))
+        pad = int(rng.integers(0, 40))
+        out.append(dict(i=i, name=NAMES[rng.integers(0, len(NAMES))], N=N, T=T,
+                        dtype=("f32", "bf16")[rng.integers(0, 2)], layout=layout, pad=pad,
+                        p=float(rng.choice([0.0, 0.005, 0.05, 0.3])), trunc=bool(rng.integers(0, 2)),
+                        boot=bool(rng.integers(0, 2)), variant=int(rng.integers(0, 3)),
+                        seed=int(rng.integers(0, 2 ** 31))))
+    return out
+
+
+def _view(t, layout, pad):
+    """An [N, T] view of `t` in the case's layout (a copy into fresh storage for strided ones)."""
+    if t.dim() != 2 or layout == "rows":
+        return t
+    N, T = t.shape
+    if layout == "strided":
+        buf = torch.full((N, T + pad), 3, dtype=t.dtype, device=t.device)
+        buf[:, :T] = t
+        return buf[:, :T]
+    buf = torch.full((T, N + pad), 3, dtype=t.dtype, device=t.device)
+    buf[:, :N] = t.t()
+    return buf[:, :N].t()
+
+
+def _run(name, d, trunc, boot, ws, strided):
+    tr = d["trunc"] if trunc else None
+    bv = d["bv"] if trunc else None
+    bt = d["boot"] if boot else None
+    sfx = "_strided" if strided else ""
+    f = lambda base: getattr(rl, "rlcs_" + base + sfx)
+    if name == "gae":
+        return f("gae")(d["r"], d["v"], d["term"], tr, bv, bt, gamma=0.97, lam=0.9, ws=ws)
+    if name == "vtrace":
+        return f("vtrace")(d["r"], d["v"], d["log_rho"], d["term"], tr, bv, bt, gamma=0.97,
+                           rho_bar=1.0, c_bar=0.9, ws=ws)
+    if name == "retrace":
+        return f("retrace")(d["r"], d["q"], d["eq"], d["log_rho"], d["term"], tr, bv, bt,
+                            gamma=0.97, lam=0.9, c_bar=1.0, ws=ws)
+    if name == "td_lambda":
+        return (f("td_lambda")(d["r"], d["v"], d["term"], tr, bv, bt, gamma=0.97, lam=0.9, ws=ws),)
+    if name == "discounted":
+        return (f("discounted")(d["r"], d["term"], tr, bv, bt, gamma=0.97, ws=ws),)
+    if name == "elig_trace":
+        return (f("elig_trace")(d["x"], d["term"], tr, gamma=0.97, lam=0.9, ws=ws),)
+    b = "starts_at" if name == "prefix_starts" else "ends_at"
+    return (f("episodic_prefix")(d["x"], d["term"], tr, boundary=b, ws=ws),)
+
+
+@pytest.mark.parametrize("case", _cases(), ids=lambda c: f"c{c['i']}")
+def test_random_case(case):
+    c = case
+    print(f"case {c}", flush=True)
+    ro = workloads.make_rollout(c["N"], c["T"], c["seed"], dtype=c["dtype"], p_term=c["p"],
+                                p_trunc=c["p"])
+    d = {k: _view(to_device(v, DEV), c["layout"], c["pad"]) for k, v in ro.items()}
+    strided = c["layout"] != "rows"
+    ws = (rl.make_workspace_columns(c["N"], c["T"], DEV) if strided
+          else rl.make_workspace(c["N"], c["T"], DEV))
+    rl.rlcs_set_variant_override(c["variant"])
+    try:
+        outs = _run(c["name"], d, c["trunc"], c["boot"], ws, strided)
+        torch.cuda.synchronize()
+    finally:
+        rl.rlcs_set_variant_override(0)
+    ref = oracle_run(c["name"], ro, trunc=c["trunc"], boot=c["boot"], gamma=0.97, lam=0.9,
+                     c_bar=0.9 if c["name"] == "vtrace" else 1.0)
+    got = {k: o for k, o in zip(OUT_KEYS[c["name"]], outs) if o is not None}
+    assert_parity(got, {k: ref[k] for k in got}, TOL[c["dtype"]], label=f"random case {c['i']}")
+    assert int(ws[8:12].view(torch.int32).item()) == 0
