@@ -29,18 +29,20 @@
 // every workgroup of the grid.
 //
 // Workspace of cols_tiles_kernel (the layout of rlcs_kernels.h, zero-filled once):
-//   header: `state` = call epoch << 32 | number of column blocks finished in this call, and the
-//     error flag;
-//   per-block slots: ticket counter (32 bits), finished tiles (32 bits), 64 bytes per block
-//     (at most kWsSlots blocks);
-//   records: two 64-bit words per column per tile, (tag << 32 | bits(a)), (tag << 32 | bits(b)),
-//     valid for the current call when tag = 2*epoch+1.
-// Every workgroup reads the epoch when it starts. The epoch only advances when the last tile of
-// the call finishes (the last tile of a block counts the block finished; the last block advances
-// the epoch and clears the count), so every workgroup of a call reads the same epoch and every
-// call on a workspace has its own, whatever the geometry of the calls before it. The last
-// drawer of a block resets its ticket counter and the last finisher its finished count, so the
-// next call on the same stream finds the workspace ready.
+//   per-block slots, 64 bytes per block (at most kWsSlots blocks): one 64-bit draw word,
+//     generation << 32 | tickets drawn in this call;
+//   records: two 64-bit words per column per tile at record p * J + j, (tag0 << 32 | bits(a)),
+//     (tag1 << 32 | bits(b)), valid for the current call when tag0 = 2*gen + 2 and
+//     tag1 = tag0 + J * kColTagMix.
+// A workgroup draws its ticket and its block's generation with one atomic add on the block's
+// draw word; the last drawer of a block stores (gen + 1, 0), so the next call on the same
+// stream finds the block ready with a new generation. Nothing else is counted: no workgroup
+// waits at its end, and the header's call state (used by the row kernels) is not touched.
+// Why a stale record can never pass for a current one: a record's address fixes its tile and
+// column once J is fixed, so a stale record with the current J (same tag1) was written by an
+// earlier call on the same block, whose generation was older; a stale record written under
+// another J has another tag1. The row kernels' tags are odd and tag0 is even, so one workspace
+// serves both kinds of call.
 #pragma once
 
 #include "rlcs_kernels.h"
@@ -324,10 +326,12 @@ __global__ void __launch_bounds__(W * kWave) cols_rows_kernel(Args a, ColGeom g)
 // beta = 0 (the column's edge tile always has one). Up to kColLookAhead records are read per
 // round. Bounded polls: on exhaustion the error flag is set and NaN returned.
 constexpr int kColLookAhead = 4;
+constexpr uint32_t kColGenMask = 0x3fffffffu;
+constexpr uint32_t kColTagMix = 0x9e3779b1u;  // odd: distinct J give distinct tag1
 
 template <bool kBack>
 __device__ float cols_gather(const uint64_t* rec, int64_t tile, int64_t P, int64_t J, int64_t j,
-                             uint32_t tag, WsHeader* hdr) {
+                             uint32_t tag0, uint32_t tag1, WsHeader* hdr) {
     Pair acc = identity_pair();
     int64_t dist = 1;
     for (;;) {
@@ -348,7 +352,7 @@ __device__ float cols_gather(const uint64_t* rec, int64_t tile, int64_t P, int64
             const bool inside = kBack ? (q < P) : (q >= 0);
             if (!inside) return acc.a;  // past the column's edge tile (not reached in practice)
             uint32_t polls = 0;
-            while (uint32_t(w0[i] >> 32) != tag || uint32_t(w1[i] >> 32) != tag) {
+            while (uint32_t(w0[i] >> 32) != tag0 || uint32_t(w1[i] >> 32) != tag1) {
                 if (++polls > kMaxPolls) {
                     st_relaxed(&hdr->error, 1u);
                     return __builtin_nanf("");
@@ -383,17 +387,19 @@ __global__ void __launch_bounds__(W * kWave) cols_tiles_kernel(Args a, ColGeom g
     const int64_t P = (T + L - 1) / L;
     const int64_t block = int64_t(blockIdx.x) % num_blocks;
 
-    uint32_t* slot = reinterpret_cast<uint32_t*>(slots + block * 64);
     if (threadIdx.x == 0) {
-        const uint32_t epoch = uint32_t(ld_relaxed(&hdr->state) >> 32);
-        const uint32_t ticket = __hip_atomic_fetch_add(slot, 1u, __ATOMIC_RELAXED,
-                                                       __HIP_MEMORY_SCOPE_AGENT);
-        if (ticket == uint32_t(P - 1)) st_relaxed(slot, 0u);
+        uint64_t* draw = reinterpret_cast<uint64_t*>(slots + block * 64);
+        const uint64_t old = __hip_atomic_fetch_add(draw, uint64_t(1), __ATOMIC_RELAXED,
+                                                    __HIP_MEMORY_SCOPE_AGENT);
+        const uint32_t ticket = uint32_t(old);
+        const uint32_t gen = uint32_t(old >> 32) & kColGenMask;
+        if (ticket == uint32_t(P - 1)) st_relaxed(draw, uint64_t((gen + 1u) & kColGenMask) << 32);
         s_ticket = ticket;
-        s_tag = 2u * epoch + 1u;
+        s_tag = 2u * gen + 2u;
     }
     __syncthreads();
-    const uint32_t tag = s_tag;
+    const uint32_t tag0 = s_tag;
+    const uint32_t tag1 = tag0 + uint32_t(g.J) * kColTagMix;
     const int64_t ticket = s_ticket;
     if (ticket >= P) {
         // Only possible if the workspace was not zero-filled before first use.
@@ -421,26 +427,13 @@ __global__ void __launch_bounds__(W * kWave) cols_tiles_kernel(Args a, ColGeom g
             } else {
                 for (int w = 0; w < W; ++w) tm = compose(Pair{s_a[w][lane], s_b[w][lane]}, tm);
             }
-            const uint64_t hi_tag = uint64_t(tag) << 32;
-            st_relaxed(rec + 2 * (p * g.J + cl.j), hi_tag | __float_as_uint(tm.a));
-            st_relaxed(rec + 2 * (p * g.J + cl.j) + 1, hi_tag | __float_as_uint(tm.b));
+            st_relaxed(rec + 2 * (p * g.J + cl.j), uint64_t(tag0) << 32 | __float_as_uint(tm.a));
+            st_relaxed(rec + 2 * (p * g.J + cl.j) + 1, uint64_t(tag1) << 32 | __float_as_uint(tm.b));
         }
-        s_carry[lane] = (need && cl.active) ? cols_gather<kBack>(rec, p, P, g.J, cl.j, tag, hdr) : 0.f;
+        s_carry[lane] = (need && cl.active) ? cols_gather<kBack>(rec, p, P, g.J, cl.j, tag0, tag1, hdr) : 0.f;
     }
     __syncthreads();
     c.finish(a, a.p, cl.base, g.st, apply(win, s_carry[lane]));
-    if (threadIdx.x == 0) {
-        // this tile is done with the epoch (its records and look-back are behind it)
-        const uint32_t done = __hip_atomic_fetch_add(slot + 1, 1u, __ATOMIC_RELAXED,
-                                                     __HIP_MEMORY_SCOPE_AGENT);
-        if (done == uint32_t(P - 1)) {
-            st_relaxed(slot + 1, 0u);
-            const uint64_t old = __hip_atomic_fetch_add(&hdr->state, uint64_t(1), __ATOMIC_RELAXED,
-                                                        __HIP_MEMORY_SCOPE_AGENT);
-            if (uint32_t(old) == uint32_t(num_blocks - 1))
-                st_relaxed(&hdr->state, uint64_t(((old >> 32) + 1u) & 0x7fffffffu) << 32);
-        }
-    }
 }
 
 }  // namespace rlcs
