@@ -38,7 +38,8 @@
  * Stream     `stream` is a hipStream_t (NULL = the default stream). Every call only enqueues
  *            work and returns; outputs are valid once the stream has reached that point.
  * Workspace  `ws` (optional) is device memory of at least rlcs_workspace_size(N, T) bytes.
- *            With it, rows much longer than a workgroup's tile are split over several
+ *            With it, calls of few long rows (under 256 rows longer than 4096 fp32 or 8192
+ *            bf16 steps, T a multiple of 4 or 8) split each row into tiles over several
  *            workgroups that pass carries to each other through `ws`, which fills the GPU
  *            when N is small. `ws` must be zero-filled once before its first use; every call
  *            leaves it ready for the next one. Calls sharing one `ws` must be ordered on one
@@ -185,10 +186,10 @@ rlcs_status rlcs_affine_scan(const void* alpha, const void* beta, const void* ca
                              void* ws, size_t ws_bytes, rlcs_stream_t stream);
 
 /* Bytes of workspace that let any entry point above split rows of an [N, T] call over
- * several workgroups: a fixed 65600-byte part plus 16 bytes per 4096-step tile (0 if the size
- * overflows). Every entry point of this header lays the workspace out the same way, so one
- * workspace at least as large as each call needs serves calls of every kind and shape,
- * row-major and time-major alike, as long as they are ordered on one stream. */
+ * several workgroups: a fixed 65600-byte part plus 16 bytes per row per 1024 steps, rounded up
+ * (0 if the size overflows). Every entry point of this header lays the workspace out the same
+ * way, so one workspace at least as large as each call needs serves calls of every kind and
+ * shape, row-major and time-major alike, as long as they are ordered on one stream. */
 size_t rlcs_workspace_size(int64_t N, int64_t T);
 
 /* GAE with observation-skip masking, for multi-turn and tool-use trajectories (the extension
@@ -306,7 +307,8 @@ const char* rlcs_status_string(rlcs_status status);
 int rlcs_version(void);
 
 /* Kernel-variant override, process-wide, for tests and benchmarks: 0 = automatic choice,
- * 1 = whole rows per workgroup, 2 = rows split across workgroups (needs the workspace).
+ * 1 = whole rows per workgroup, 2 = rows split across workgroups (needs the workspace; calls
+ * of more than 1024 rows, or columns in more than 1024 blocks of 64, still run whole).
  * Not thread-safe with concurrent calls. Returns RLCS_ERR_INVALID_ARG for other values. */
 rlcs_status rlcs_set_variant_override(int variant);
 

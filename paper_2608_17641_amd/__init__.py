@@ -12,6 +12,7 @@ GPU. ``ws`` is an optional zero-initialised uint8 workspace (see ``make_workspac
 """
 from __future__ import annotations
 
+import contextlib
 from typing import Optional, Tuple
 
 import torch
@@ -98,8 +99,23 @@ def _prep(x: torch.Tensor):
     return int(N), int(T), x.dtype, x.device
 
 
+_raw_stream = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+
+
 def _stream(device):
+    """The current HIP stream of `device` as a raw handle (the direct accessor when this
+    PyTorch has it: building a Stream object costs more than the kernel launch)."""
+    if _raw_stream is not None:
+        return _raw_stream(device.index)
     return torch.cuda.current_stream(device).cuda_stream
+
+
+_SAME_DEVICE = contextlib.nullcontext()
+
+
+def _on(device):
+    """Context that makes `device` current for the call (nothing to do when it already is)."""
+    return _SAME_DEVICE if device.index == torch.cuda.current_device() else torch.cuda.device(device)
 
 
 def _call(fn: str, *args):
@@ -135,7 +151,7 @@ def rlcs_gae(r, v, term=None, trunc=None, bv=None, boot=None, adv=None, ret=None
     adv = _out("adv", adv, N, T, dev)
     ret = _out("ret", ret, N, T, dev) if (want_ret or ret is not None) else None
     wp, wb = _ws(ws, dev)
-    with torch.cuda.device(dev):
+    with _on(dev):
         _call("rlcs_gae", _ptr(r), _ptr(v), _ptr(term), _ptr(trunc), _ptr(bv), _ptr(boot),
               _ptr(adv), _ptr(ret), N, T, gamma, lam, _DTYPES[dt], wp, wb, _stream(dev))
     return adv, ret
@@ -151,7 +167,7 @@ def rlcs_vtrace(r, v, log_rho, term=None, trunc=None, bv=None, boot=None, vs=Non
     vs = _out("vs", vs, N, T, dev)
     pg = _out("pg", pg, N, T, dev) if (want_pg or pg is not None) else None
     wp, wb = _ws(ws, dev)
-    with torch.cuda.device(dev):
+    with _on(dev):
         _call("rlcs_vtrace", _ptr(r), _ptr(v), _ptr(log_rho), _ptr(term), _ptr(trunc), _ptr(bv),
               _ptr(boot), _ptr(vs), _ptr(pg), N, T, gamma, rho_bar, c_bar, _DTYPES[dt], wp, wb,
               _stream(dev))
@@ -169,7 +185,7 @@ def rlcs_retrace(r, q, eq, log_rho, term=None, trunc=None, bv=None, boot=None, d
     delta = _out("delta", delta, N, T, dev)
     q_ret = _out("q_ret", q_ret, N, T, dev) if (want_q_ret or q_ret is not None) else None
     wp, wb = _ws(ws, dev)
-    with torch.cuda.device(dev):
+    with _on(dev):
         _call("rlcs_retrace", _ptr(r), _ptr(q), _ptr(eq), _ptr(log_rho), _ptr(term), _ptr(trunc),
               _ptr(bv), _ptr(boot), _ptr(delta), _ptr(q_ret), N, T, gamma, lam, c_bar,
               _DTYPES[dt], wp, wb, _stream(dev))
@@ -194,7 +210,7 @@ def rlcs_retrace_full(r, q, pi, actions, mu, term=None, trunc=None, bv=None, boo
     _check_flags("term", term, N, T, dev); _check_flags("trunc", trunc, N, T, dev)
     delta = _out("delta", delta, N, T, dev)
     q_ret = _out("q_ret", q_ret, N, T, dev) if (want_q_ret or q_ret is not None) else None
-    with torch.cuda.device(dev):
+    with _on(dev):
         _call("rlcs_retrace_full", _ptr(r), _ptr(q), _ptr(pi), _ptr(actions), _ptr(mu),
               _ptr(term), _ptr(trunc), _ptr(bv), _ptr(boot), _ptr(delta), _ptr(q_ret), N, T, A,
               gamma, lam, c_bar, _DTYPES[dt], None, 0, _stream(dev))
@@ -209,7 +225,7 @@ def rlcs_td_lambda(r, v, term=None, trunc=None, bv=None, boot=None, ret=None, *,
     _check_flags("term", term, N, T, dev); _check_flags("trunc", trunc, N, T, dev)
     ret = _out("ret", ret, N, T, dev)
     wp, wb = _ws(ws, dev)
-    with torch.cuda.device(dev):
+    with _on(dev):
         _call("rlcs_td_lambda", _ptr(r), _ptr(v), _ptr(term), _ptr(trunc), _ptr(bv), _ptr(boot),
               _ptr(ret), N, T, gamma, lam, _DTYPES[dt], wp, wb, _stream(dev))
     return ret
@@ -222,7 +238,7 @@ def rlcs_discounted(r, term=None, trunc=None, bv=None, boot=None, ret=None, *, g
     _check_flags("term", term, N, T, dev); _check_flags("trunc", trunc, N, T, dev)
     ret = _out("ret", ret, N, T, dev)
     wp, wb = _ws(ws, dev)
-    with torch.cuda.device(dev):
+    with _on(dev):
         _call("rlcs_discounted", _ptr(r), _ptr(term), _ptr(trunc), _ptr(bv), _ptr(boot), _ptr(ret),
               N, T, gamma, _DTYPES[dt], wp, wb, _stream(dev))
     return ret
@@ -234,7 +250,7 @@ def rlcs_elig_trace(x, term=None, trunc=None, z=None, *, gamma: float, lam: floa
     _check_flags("term", term, N, T, dev); _check_flags("trunc", trunc, N, T, dev)
     z = _out("z", z, N, T, dev)
     wp, wb = _ws(ws, dev)
-    with torch.cuda.device(dev):
+    with _on(dev):
         _call("rlcs_elig_trace", _ptr(x), _ptr(term), _ptr(trunc), _ptr(z), N, T, gamma, lam,
               _DTYPES[dt], wp, wb, _stream(dev))
     return z
@@ -249,7 +265,7 @@ def rlcs_episodic_prefix(x, term=None, trunc=None, c=None, *, boundary: str = "e
     c = _out("c", c, N, T, dev)
     wp, wb = _ws(ws, dev)
     b = _native.RLCS_STARTS_AT if boundary == "starts_at" else _native.RLCS_ENDS_AT
-    with torch.cuda.device(dev):
+    with _on(dev):
         _call("rlcs_episodic_prefix", _ptr(x), _ptr(term), _ptr(trunc), _ptr(c), N, T, b,
               _DTYPES[dt], wp, wb, _stream(dev))
     return c
@@ -262,7 +278,7 @@ def rlcs_affine_scan(alpha, beta, carry=None, out=None, *, reverse: bool = True,
     out = _out("out", out, N, T, dev)
     wp, wb = _ws(ws, dev)
     d = _native.RLCS_BACKWARD if reverse else _native.RLCS_FORWARD
-    with torch.cuda.device(dev):
+    with _on(dev):
         _call("rlcs_affine_scan", _ptr(alpha), _ptr(beta), _ptr(carry), _ptr(out), N, T, d,
               _DTYPES[dt], wp, wb, _stream(dev))
     return out
@@ -351,7 +367,7 @@ def rlcs_gae_strided(r, v, term=None, trunc=None, bv=None, boot=None, adv=None, 
     adv = _out_strided("adv", adv, N, T, sn, st, dev)
     ret = _out_strided("ret", ret, N, T, sn, st, dev) if (want_ret or ret is not None) else None
     wp, wb = _ws(ws, dev)
-    with torch.cuda.device(dev):
+    with _on(dev):
         _call("rlcs_gae_strided", _ptr(r), _ptr(v), _ptr(term), _ptr(trunc), _ptr(bv), _ptr(boot),
               _ptr(adv), _ptr(ret), N, T, sn, st, gamma, lam, _DTYPES[dt], wp, wb, _stream(dev))
     return adv, ret
@@ -369,7 +385,7 @@ def rlcs_vtrace_strided(r, v, log_rho, term=None, trunc=None, bv=None, boot=None
     vs = _out_strided("vs", vs, N, T, sn, st, dev)
     pg = _out_strided("pg", pg, N, T, sn, st, dev) if (want_pg or pg is not None) else None
     wp, wb = _ws(ws, dev)
-    with torch.cuda.device(dev):
+    with _on(dev):
         _call("rlcs_vtrace_strided", _ptr(r), _ptr(v), _ptr(log_rho), _ptr(term), _ptr(trunc),
               _ptr(bv), _ptr(boot), _ptr(vs), _ptr(pg), N, T, sn, st, gamma, rho_bar, c_bar,
               _DTYPES[dt], wp, wb, _stream(dev))
@@ -388,7 +404,7 @@ def rlcs_retrace_strided(r, q, eq, log_rho, term=None, trunc=None, bv=None, boot
     delta = _out_strided("delta", delta, N, T, sn, st, dev)
     q_ret = _out_strided("q_ret", q_ret, N, T, sn, st, dev) if (want_q_ret or q_ret is not None) else None
     wp, wb = _ws(ws, dev)
-    with torch.cuda.device(dev):
+    with _on(dev):
         _call("rlcs_retrace_strided", _ptr(r), _ptr(q), _ptr(eq), _ptr(log_rho), _ptr(term),
               _ptr(trunc), _ptr(bv), _ptr(boot), _ptr(delta), _ptr(q_ret), N, T, sn, st, gamma,
               lam, c_bar, _DTYPES[dt], wp, wb, _stream(dev))
@@ -404,7 +420,7 @@ def rlcs_td_lambda_strided(r, v, term=None, trunc=None, bv=None, boot=None, ret=
     _boot_strided(boot, N, dt, dev)
     ret = _out_strided("ret", ret, N, T, sn, st, dev)
     wp, wb = _ws(ws, dev)
-    with torch.cuda.device(dev):
+    with _on(dev):
         _call("rlcs_td_lambda_strided", _ptr(r), _ptr(v), _ptr(term), _ptr(trunc), _ptr(bv),
               _ptr(boot), _ptr(ret), N, T, sn, st, gamma, lam, _DTYPES[dt], wp, wb, _stream(dev))
     return ret
@@ -419,7 +435,7 @@ def rlcs_discounted_strided(r, term=None, trunc=None, bv=None, boot=None, ret=No
     _boot_strided(boot, N, dt, dev)
     ret = _out_strided("ret", ret, N, T, sn, st, dev)
     wp, wb = _ws(ws, dev)
-    with torch.cuda.device(dev):
+    with _on(dev):
         _call("rlcs_discounted_strided", _ptr(r), _ptr(term), _ptr(trunc), _ptr(bv), _ptr(boot),
               _ptr(ret), N, T, sn, st, gamma, _DTYPES[dt], wp, wb, _stream(dev))
     return ret
@@ -432,7 +448,7 @@ def rlcs_elig_trace_strided(x, term=None, trunc=None, z=None, *, gamma: float, l
     _check_strided("trunc", trunc, N, T, sn, st, dev, flags=True)
     z = _out_strided("z", z, N, T, sn, st, dev)
     wp, wb = _ws(ws, dev)
-    with torch.cuda.device(dev):
+    with _on(dev):
         _call("rlcs_elig_trace_strided", _ptr(x), _ptr(term), _ptr(trunc), _ptr(z), N, T, sn, st,
               gamma, lam, _DTYPES[dt], wp, wb, _stream(dev))
     return z
@@ -448,7 +464,7 @@ def rlcs_episodic_prefix_strided(x, term=None, trunc=None, c=None, *, boundary: 
     c = _out_strided("c", c, N, T, sn, st, dev)
     wp, wb = _ws(ws, dev)
     b = _native.RLCS_STARTS_AT if boundary == "starts_at" else _native.RLCS_ENDS_AT
-    with torch.cuda.device(dev):
+    with _on(dev):
         _call("rlcs_episodic_prefix_strided", _ptr(x), _ptr(term), _ptr(trunc), _ptr(c), N, T, sn,
               st, b, _DTYPES[dt], wp, wb, _stream(dev))
     return c
@@ -474,7 +490,7 @@ def rlcs_elig_trace_vec(x, term=None, trunc=None, z=None, *, gamma: float, lam: 
             or not z.is_contiguous():
         raise ValueError(f"z must be a contiguous float32 [N, T, F] tensor on {dev}")
     wp, wb = _ws(ws, dev)
-    with torch.cuda.device(dev):
+    with _on(dev):
         _call("rlcs_elig_trace_vec", _ptr(x), _ptr(term), _ptr(trunc), _ptr(z), N, T, F, gamma,
               lam, _DTYPES[x.dtype], wp, wb, _stream(dev))
     return z
@@ -502,7 +518,7 @@ def rlcs_gae_masked(r, v, mask=None, term=None, trunc=None, bv=None, boot=None, 
     if normalize and ws is None:
         ws = torch.empty(max(rlcs_workspace_size_masked(N, T), 64), dtype=torch.uint8, device=dev)
     wp, wb = _ws(ws, dev)
-    with torch.cuda.device(dev):
+    with _on(dev):
         _call("rlcs_gae_masked", _ptr(r), _ptr(v), _ptr(mask), _ptr(term), _ptr(trunc), _ptr(bv),
               _ptr(boot), _ptr(adv), _ptr(ret), N, T, gamma, lam, 1 if normalize else 0, eps,
               _DTYPES[dt], wp, wb, _stream(dev))

@@ -22,27 +22,15 @@
 //      published maps of other workgroups' tiles) and finish the K steps; store.
 // cols_rows_kernel walks all of T in chunks (carry through LDS); cols_tiles_kernel gives each
 // tile (kColSplitW waves, twice a walk's chunk) its own workgroup and carries between them with
-// the workspace protocol of the split-row kernel, per column: a tile publishes its 64 composed maps and composes the maps of the tiles
-// on its carry-source side, nearest first, until it meets beta = 0 (an episode or row edge).
-// Tiles only ever wait for tiles of their own column block, so each block has its own ticket
-// counter: tickets order the block's tiles from the carry source, and no counter is touched by
-// every workgroup of the grid.
+// the split-row kernel's workspace protocol, per column: a tile publishes its 64 composed maps
+// and composes the maps of the tiles on its carry-source side, nearest first, until it meets
+// beta = 0 (an episode or row edge). Tiles only ever wait for tiles of their own column block,
+// so each block has its own draw slot: its tickets order the block's tiles from the carry
+// source, and no counter is touched by every workgroup of the grid.
 //
-// Workspace of cols_tiles_kernel (the layout of rlcs_kernels.h, zero-filled once):
-//   per-block slots, 64 bytes per block (at most kWsSlots blocks): one 64-bit draw word,
-//     generation << 32 | tickets drawn in this call;
-//   records: two 64-bit words per column per tile at record p * J + j, (tag0 << 32 | bits(a)),
-//     (tag1 << 32 | bits(b)), valid for the current call when tag0 = 2*gen + 2 and
-//     tag1 = tag0 + J * kColTagMix.
-// A workgroup draws its ticket and its block's generation with one atomic add on the block's
-// draw word; the last drawer of a block stores (gen + 1, 0), so the next call on the same
-// stream finds the block ready with a new generation. Nothing else is counted: no workgroup
-// waits at its end, and the header's call state (used by the row kernels) is not touched.
-// Why a stale record can never pass for a current one: a record's address fixes its tile and
-// column once J is fixed, so a stale record with the current J (same tag1) was written by an
-// earlier call on the same block, whose generation was older; a stale record written under
-// another J has another tag1. The row kernels' tags are odd and tag0 is even, so one workspace
-// serves both kinds of call.
+// Workspace of cols_tiles_kernel: the split layout of rlcs_kernels.h (zero-filled once), with
+// one draw slot per 64-column block (at most kWsSlots blocks), records at index p * J + j for
+// tile p of column j, and even tags (tag0 = 2*gen + 2, tag1 = tag0 + J * kTagMix).
 #pragma once
 
 #include "rlcs_kernels.h"
@@ -326,8 +314,6 @@ __global__ void __launch_bounds__(W * kWave) cols_rows_kernel(Args a, ColGeom g)
 // beta = 0 (the column's edge tile always has one). Up to kColLookAhead records are read per
 // round. Bounded polls: on exhaustion the error flag is set and NaN returned.
 constexpr int kColLookAhead = 4;
-constexpr uint32_t kColGenMask = 0x3fffffffu;
-constexpr uint32_t kColTagMix = 0x9e3779b1u;  // odd: distinct J give distinct tag1
 
 template <bool kBack>
 __device__ float cols_gather(const uint64_t* rec, int64_t tile, int64_t P, int64_t J, int64_t j,
@@ -380,7 +366,6 @@ __global__ void __launch_bounds__(W * kWave) cols_tiles_kernel(Args a, ColGeom g
     __shared__ float s_carry[kWave];
     __shared__ uint32_t s_ticket, s_tag;
     WsHeader* hdr = reinterpret_cast<WsHeader*>(a.ws);
-    char* slots = reinterpret_cast<char*>(a.ws) + sizeof(WsHeader);
     uint64_t* rec = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(a.ws) + kWsRecordsOffset);
     const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
     const int64_t T = a.T;
@@ -388,18 +373,13 @@ __global__ void __launch_bounds__(W * kWave) cols_tiles_kernel(Args a, ColGeom g
     const int64_t block = int64_t(blockIdx.x) % num_blocks;
 
     if (threadIdx.x == 0) {
-        uint64_t* draw = reinterpret_cast<uint64_t*>(slots + block * 64);
-        const uint64_t old = __hip_atomic_fetch_add(draw, uint64_t(1), __ATOMIC_RELAXED,
-                                                    __HIP_MEMORY_SCOPE_AGENT);
-        const uint32_t ticket = uint32_t(old);
-        const uint32_t gen = uint32_t(old >> 32) & kColGenMask;
-        if (ticket == uint32_t(P - 1)) st_relaxed(draw, uint64_t((gen + 1u) & kColGenMask) << 32);
-        s_ticket = ticket;
+        uint32_t gen;
+        s_ticket = draw_ticket(draw_word(a.ws, block), P, gen);
         s_tag = 2u * gen + 2u;
     }
     __syncthreads();
     const uint32_t tag0 = s_tag;
-    const uint32_t tag1 = tag0 + uint32_t(g.J) * kColTagMix;
+    const uint32_t tag1 = tag0 + uint32_t(g.J) * kTagMix;
     const int64_t ticket = s_ticket;
     if (ticket >= P) {
         // Only possible if the workspace was not zero-filled before first use.

@@ -15,8 +15,10 @@ extern "C" {
 size_t rlcs_workspace_size(int64_t N, int64_t T) {
     if (N <= 0 || T <= 0) return kWsRecordsOffset;
     if (N > INT64_MAX / T) return 0;
-    const int64_t tiles = (N * T + kMinTile - 1) / kMinTile;
-    return kWsRecordsOffset + size_t(tiles) * kWsRecordBytes;
+    // N * (tiles per row) records, at most kMinTile steps per tile
+    const int64_t per_row = (T + kMinTile - 1) / kMinTile;
+    if (N > int64_t((SIZE_MAX - kWsRecordsOffset) / kWsRecordBytes) / per_row) return 0;
+    return kWsRecordsOffset + size_t(N * per_row) * kWsRecordBytes;
 }
 
 const char* rlcs_status_string(rlcs_status status) {

@@ -31,12 +31,18 @@ template <typename DT> struct Width;
 template <> struct Width<float> { static constexpr int K = 4; };
 template <> struct Width<bf16_t> { static constexpr int K = 8; };
 
-// Smallest tile of the split-row variant (float32), which sizes the workspace.
-constexpr int64_t kMinTile = int64_t(kLargeWaves) * kWave * Width<float>::K;
+// Smallest tile of the split-row variant (float32, 4 waves), which sizes the workspace.
+constexpr int64_t kMinTile = int64_t(kSmallWaves) * kWave * Width<float>::K;
 
-// Rows longer than one large workgroup's chunk are split across workgroups (when a workspace
-// is given) only if there are too few rows for whole-row workgroups to fill the GPU.
-constexpr int64_t kSplitBelowRows = 1024;
+// Rows longer than one large workgroup's chunk are split across workgroups (a workspace given,
+// T a multiple of K) when there are fewer than kSplitBelowRows of them. With more rows, or
+// shorter ones, whole-row workgroups are faster: a tile waiting for its neighbours' maps costs
+// more than the idle CUs (timed: 64 x 4096 fp32 GAE 3.9 us whole-row, 5.2 us split; 512 x 8192
+// the same either way; 16 x 16384 bf16 9.2 us whole-row, 6.4 us split).
+constexpr int64_t kSplitBelowRows = 256;
+// Split rows use 4-wave tiles, or 16-wave tiles when a row would have more than this many
+// 4-wave ones (all tiles of a row draw their tickets from one word).
+constexpr int64_t kMaxSmallTilesPerRow = 64;
 
 // Largest action axis of full-form Retrace (its [steps, A] slices are staged in LDS).
 constexpr int64_t kMaxActions = 28;
@@ -71,7 +77,7 @@ inline rlcs_status check_common(int64_t N, int64_t T, rlcs_dtype dtype,
 struct Plan {
     bool split;           // tiles kernel (rows split across workgroups) vs rows kernel
     int waves;            // waves per workgroup
-    int64_t num_tiles;    // tiles kernel: grid size
+    int64_t tiles_per_row;  // tiles kernel: tiles of each row (grid = N * tiles_per_row)
     int64_t rows_per_wg;  // rows kernel: rows per workgroup
     int wave_local;       // rows kernel: no carry crosses waves
     size_t lds_bytes;     // dynamic LDS (staged policies)
@@ -84,8 +90,9 @@ void launch_w(const Args& a, const Plan& p, hipStream_t stream) {
     const dim3 block(W * kWave);
     if constexpr (Op::kStaged == 0) {
         if (p.split) {
-            hipLaunchKernelGGL((tiles_kernel<Op, DT, K, W, VEC, TR>), dim3(unsigned(p.num_tiles)),
-                               block, 0, stream, a, p.num_tiles);
+            hipLaunchKernelGGL((tiles_kernel<Op, DT, K, W, VEC, TR>),
+                               dim3(unsigned(a.N * p.tiles_per_row)), block, 0, stream, a,
+                               p.tiles_per_row);
             return;
         }
     }
@@ -107,8 +114,7 @@ rlcs_status launch(const Args& a, const Plan& p, hipStream_t stream) {
         if (p.waves == kStagedWaves) launch_w<Op, DT, VEC, TR, kStagedWaves>(a, p, stream);
         else launch_w<Op, DT, VEC, TR, kSmallWaves>(a, p, stream);
     } else {
-        if (p.split) launch_w<Op, DT, VEC, TR, kLargeWaves>(a, p, stream);
-        else if (p.waves == kSmallWaves) launch_w<Op, DT, VEC, TR, kSmallWaves>(a, p, stream);
+        if (p.waves == kSmallWaves) launch_w<Op, DT, VEC, TR, kSmallWaves>(a, p, stream);
         else launch_w<Op, DT, VEC, TR, kLargeWaves>(a, p, stream);
     }
     return hipGetLastError() == hipSuccess ? RLCS_OK : RLCS_ERR_LAUNCH;
@@ -131,7 +137,7 @@ rlcs_status dispatch_dt(Args& a, bool has_trunc, void* ws, size_t ws_bytes, hipS
     constexpr int K = Width<DT>::K;
     constexpr int64_t E_small = int64_t(kSmallWaves) * kWave * K;
     constexpr int64_t E_large = int64_t(kLargeWaves) * kWave * K;
-    const int64_t N = a.N, T = a.T, total = N * T;
+    const int64_t N = a.N, T = a.T;
 
     // Vector path: 16-byte data and output vectors, K-byte flag vectors.
     bool vec = true;
@@ -141,9 +147,14 @@ rlcs_status dispatch_dt(Args& a, bool has_trunc, void* ws, size_t ws_bytes, hipS
     if (Op::kFlags && ((a.term && !aligned(a.term, K)) || (has_trunc && !aligned(a.trunc, K)))) vec = false;
 
     Plan p{};
-    p.num_tiles = (total + E_large - 1) / E_large;
-    const size_t ws_need = kWsRecordsOffset + size_t(p.num_tiles) * kWsRecordBytes;
-    const bool ws_ok = ws && ws_bytes >= ws_need && aligned(ws, 64) && p.num_tiles < int64_t(UINT32_MAX);
+    // Split rows: 4-wave tiles unless a row would have too many of them.
+    const int64_t P_small = (T + E_small - 1) / E_small;
+    const bool small_tiles = P_small <= kMaxSmallTilesPerRow;
+    p.tiles_per_row = small_tiles ? P_small : (T + E_large - 1) / E_large;
+    const bool slots_ok = N <= kWsSlots;  // one draw slot per row
+    const size_t ws_need = slots_ok ? kWsRecordsOffset + size_t(N * p.tiles_per_row) * kWsRecordBytes
+                                    : kWsRecordsOffset;
+    const bool ws_ok = ws && ws_bytes >= ws_need && aligned(ws, 64);
     const int forced = g_variant.load(std::memory_order_relaxed);
     if constexpr (Op::kStaged > 0) {
         // Staged policies keep whole rows in one workgroup (chunk loop for long rows).
@@ -155,17 +166,18 @@ rlcs_status dispatch_dt(Args& a, bool has_trunc, void* ws, size_t ws_bytes, hipS
     } else {
         if (forced == 2) {
             if (!ws_ok) return RLCS_ERR_WORKSPACE;
-            p.split = true;
+            p.split = slots_ok;  // more rows than draw slots: whole rows
         } else if (forced == 1) {
             p.split = false;
         } else {
-            p.split = T > E_large && ws_ok && N < kSplitBelowRows;
+            p.split = ws_ok && slots_ok && T % K == 0 && T > E_large && N < kSplitBelowRows;
         }
-        p.waves = p.split ? kLargeWaves : ((T <= E_small) ? kSmallWaves : kLargeWaves);
+        if (p.split) p.waves = small_tiles ? kSmallWaves : kLargeWaves;
+        else p.waves = (T <= E_small) ? kSmallWaves : kLargeWaves;
         p.lds_bytes = 0;
     }
     if (p.split) {
-        if (p.num_tiles > INT32_MAX) return RLCS_ERR_INVALID_ARG;
+        if (N * p.tiles_per_row > INT32_MAX) return RLCS_ERR_INVALID_ARG;
         a.ws = ws;
     } else {
         const int64_t E = int64_t(p.waves) * kWave * K;

@@ -16,15 +16,16 @@
 //                source, passing the carry between chunks in LDS. Needs no workspace. Rows
 //                may also lie a stride (`period`) apart; with PAD, chunks that the rows do not
 //                fill exactly still run vector loads, each lane deciding for itself (Chunk).
-// tiles kernel : each workgroup owns one chunk ("tile") of the flat array, wherever rows start
-//                or end. A tile whose edge step is not a row edge needs the carry from the
-//                tiles after it (backward) or before it (forward) in the same row: every tile
-//                publishes its composed map to the workspace as soon as step 5 is done, and a
-//                waiting tile composes its neighbours' maps, nearest first, until it meets a
-//                map with beta = 0 (an episode or row edge). Only maps are exchanged, never
-//                partial results, so the association order is fixed and results are
-//                reproducible bit for bit. Tile order comes from an atomic ticket, so a tile
-//                only ever waits for tiles that started before it.
+// tiles kernel : rows split into tiles of one chunk each (the last tile of a row may be
+//                shorter), one workgroup per tile. A tile whose carry-source edge is not the
+//                row's edge needs the carry from the tiles after it (backward) or before it
+//                (forward) in the same row: every tile publishes its composed map to the
+//                workspace as soon as step 5 is done, and a waiting tile composes its
+//                neighbours' maps, nearest first, until it meets a map with beta = 0 (an episode
+//                or row edge). Only maps are exchanged, never partial results, so the
+//                association order is fixed and results are reproducible bit for bit. Tile
+//                order within a row comes from the row's atomic ticket, so a tile only ever
+//                waits for tiles that started before it.
 #pragma once
 
 #include <type_traits>
@@ -35,27 +36,30 @@ namespace rlcs {
 
 // Workspace layout (zero-filled once by the caller), shared by the split kernels of every
 // entry point so that one workspace serves calls of any kind and shape:
-//   header (64 bytes): `state` (call epoch in the high half, a per-call counter in the low
-//   half) and an error flag;
-//   kWsSlotsBytes of per-block counters (column scans only);
-//   from kWsRecordsOffset, the records: two 64-bit words per tile (per column and tile for the
-//   column scans), (tag << 32 | bits(a)) and (tag << 32 | bits(b)).
-// Tiles kernel:
-// A record is valid for the current call when its tag equals 2*epoch+1. Each workgroup draws
-// its ticket and the call's epoch with one atomic add on the draw state; the workgroup that
-// draws the last ticket of a call stores (epoch + 1, 0), so stale records never match and the
-// next call on the same stream finds the state ready. Nothing but the draw touches the state,
-// so no fence is needed (records carry their own tag).
+//   header (64 bytes): a reserved word and an error flag;
+//   kWsSlots draw slots of 64 bytes, one per row (row tiles) or per 64-column block (column
+//   tiles), each holding one 64-bit draw word: generation << 32 | tickets drawn in this call;
+//   from kWsRecordsOffset, the records: two 64-bit words per tile, (tag0 << 32 | bits(a)) and
+//   (tag1 << 32 | bits(b)), at index p * n + i for tile p of row (column) i of the call's n.
+// A workgroup draws its ticket and its slot's generation with one relaxed atomic add; the last
+// drawer of a slot stores (gen + 1, 0), so the next call on the same stream finds the slot
+// ready with a new generation, and no workgroup counts anything at its end. A record is valid
+// for the current call when tag0 = 2*gen + 1 (row tiles; 2*gen + 2 for column tiles) and
+// tag1 = tag0 + n * kTagMix. A stale record can never pass for a current one: with the same n
+// its index fixes its tile and row (column), hence its slot, whose generation has moved on
+// since; under another n its tag1 differs; row and column tags differ in parity.
 struct WsHeader {
-    uint64_t state;  // epoch << 32 | ticket
+    uint64_t reserved;
     uint32_t error;  // set to 1 if a call found the workspace in an inconsistent state
     uint32_t pad[13];
 };
 static_assert(sizeof(WsHeader) == 64, "workspace header is 64 bytes");
 constexpr size_t kWsRecordBytes = 16;
-constexpr int64_t kWsSlots = 1024;  // column blocks a split column scan may have
+constexpr int64_t kWsSlots = 1024;  // rows or column blocks a split call may have
 constexpr size_t kWsSlotsBytes = size_t(kWsSlots) * 64;
 constexpr size_t kWsRecordsOffset = sizeof(WsHeader) + kWsSlotsBytes;
+constexpr uint32_t kGenMask = 0x3fffffffu;
+constexpr uint32_t kTagMix = 0x9e3779b1u;  // odd: distinct n give distinct tag1
 
 template <typename T>
 __device__ __forceinline__ T ld_relaxed(const T* p) {
@@ -66,17 +70,19 @@ __device__ __forceinline__ void st_relaxed(T* p, T v) {
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Ticket of a workgroup among the n_tiles workgroups of a call that share the draw state
-// `state`, and the call's record tag; drawn by one thread with a single relaxed atomic.
-__device__ __forceinline__ uint32_t draw_ticket(uint64_t* state, int64_t n_tiles, uint32_t& tag) {
-    const uint64_t old = __hip_atomic_fetch_add(state, uint64_t(1), __ATOMIC_RELAXED,
+// Ticket of a workgroup among the n_tiles workgroups of a call that draw from `word`, and the
+// slot's generation for this call; one relaxed atomic, by one thread.
+__device__ __forceinline__ uint32_t draw_ticket(uint64_t* word, int64_t n_tiles, uint32_t& gen) {
+    const uint64_t old = __hip_atomic_fetch_add(word, uint64_t(1), __ATOMIC_RELAXED,
                                                 __HIP_MEMORY_SCOPE_AGENT);
     const uint32_t ticket = uint32_t(old);
-    const uint32_t epoch = uint32_t(old >> 32);
-    if (ticket == uint32_t(n_tiles - 1))
-        st_relaxed(state, uint64_t((epoch + 1u) & 0x7fffffffu) << 32);
-    tag = 2u * epoch + 1u;
+    gen = uint32_t(old >> 32) & kGenMask;
+    if (ticket == uint32_t(n_tiles - 1)) st_relaxed(word, uint64_t((gen + 1u) & kGenMask) << 32);
     return ticket;
+}
+
+__device__ __forceinline__ uint64_t* draw_word(void* ws, int64_t slot) {
+    return reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) + sizeof(WsHeader) + slot * 64);
 }
 
 // Lane l of a wave owns the l-th group of K steps of the wave's span for forward scans and the
@@ -652,27 +658,27 @@ __global__ void __launch_bounds__(W * kWave) rows_kernel(Args a, int64_t rows_pe
 // and flags the workspace header instead of waiting forever.
 constexpr uint32_t kMaxPolls = 1u << 20;
 
-// Value entering tile `tile` from its carry-source side, composed from the published maps of
-// the neighbouring tiles of the same row, nearest outermost; run by one full wave. Lane l looks
-// at the tile 63-l places further (so the nearest tile sits in lane 63, outermost in the
-// prefix scan).
+// Value entering tile `tile` of a row from its carry-source side, composed from the published
+// maps of the row's other tiles (tile q's record at rec_row + q * rstride), nearest outermost;
+// run by one full wave. Lane l looks at the tile 63-l places further (so the nearest tile sits
+// in lane 63, outermost in the prefix scan).
 template <bool kBack>
-__device__ float gather_carry(const uint64_t* rec, int64_t tile, int64_t first_tile,
-                              int64_t last_tile, uint32_t tag, int lane, WsHeader* hdr) {
+__device__ float gather_carry(const uint64_t* rec_row, int64_t rstride, int64_t tile, int64_t P,
+                              uint32_t tag0, uint32_t tag1, int lane, WsHeader* hdr) {
     const int dist = kWave - 1 - lane;
     Pair acc = identity_pair();
     int64_t step = 1;
     for (;;) {
         const int64_t j = kBack ? tile + step + dist : tile - step - dist;
-        const bool inside = kBack ? (j <= last_tile) : (j >= first_tile);
+        const bool inside = kBack ? (j < P) : (j >= 0);
         Pair v = Pair{0.f, 0.f};  // past the row edge: nothing flows in
         bool ready = !inside;
         uint64_t prefix_mask, sever_mask;
         for (uint32_t polls = 0;; ++polls) {
             if (!ready) {
-                const uint64_t w0 = ld_relaxed(rec + 2 * j);
-                const uint64_t w1 = ld_relaxed(rec + 2 * j + 1);
-                if (uint32_t(w0 >> 32) == tag && uint32_t(w1 >> 32) == tag) {
+                const uint64_t w0 = ld_relaxed(rec_row + j * rstride);
+                const uint64_t w1 = ld_relaxed(rec_row + j * rstride + 1);
+                if (uint32_t(w0 >> 32) == tag0 && uint32_t(w1 >> 32) == tag1) {
                     ready = true;
                     v = Pair{__uint_as_float(uint32_t(w0)), __uint_as_float(uint32_t(w1))};
                 }
@@ -699,79 +705,67 @@ __device__ float gather_carry(const uint64_t* rec, int64_t tile, int64_t first_t
     }
 }
 
-// Tiles kernel: one workgroup per E-step tile of the flat array, split rows carried through
-// the workspace. Grid = number of tiles.
+// Tiles kernel: row n split into P tiles of E steps (the last one may be shorter), one
+// workgroup per tile, carries passed through the workspace. Workgroup g serves row g mod N and
+// takes its tile from that row's ticket, in carry-source order. Grid = N * P (N <= kWsSlots).
 template <class Op, typename DT, int K, int W, bool VEC, bool TR>
-__global__ void __launch_bounds__(W * kWave) tiles_kernel(Args a, int64_t num_tiles) {
+__global__ void __launch_bounds__(W * kWave) tiles_kernel(Args a, int64_t P) {
     using C = Chunk<Op, DT, K, W, VEC, TR>;
     constexpr bool kBack = Op::kBackward;
     constexpr int64_t E = int64_t(W) * kWave * K;
     __shared__ float s_a[W], s_b[W];
     __shared__ float s_carry;
-    __shared__ uint32_t s_ticket, s_tag;
+    __shared__ uint32_t s_ticket, s_gen;
     WsHeader* hdr = reinterpret_cast<WsHeader*>(a.ws);
     uint64_t* rec = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(a.ws) + kWsRecordsOffset);
     const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+    const int64_t N = a.N, T = a.T;
+    const int64_t row = int64_t(blockIdx.x) % N;
 
     if (threadIdx.x == 0) {
-        uint32_t tag;
-        s_ticket = draw_ticket(&hdr->state, num_tiles, tag);
-        s_tag = tag;
+        uint32_t gen;
+        s_ticket = draw_ticket(draw_word(a.ws, row), P, gen);
+        s_gen = gen;
     }
     __syncthreads();
-    const uint32_t tag = s_tag;
+    const uint32_t tag0 = 2u * s_gen + 1u;
+    const uint32_t tag1 = tag0 + uint32_t(N) * kTagMix;
     const int64_t ticket = s_ticket;
-    if (ticket >= num_tiles) {
+    if (ticket >= P) {
         // Only possible if the workspace was not zero-filled before first use.
         if (threadIdx.x == 0) st_relaxed(&hdr->error, 1u);
         return;
     }
-    const int64_t tile = kBack ? num_tiles - 1 - ticket : ticket;
-    const int64_t total = a.N * a.T;
-    const int64_t lo = tile * E, hi = min(lo + E, total);
+    const int64_t p = kBack ? P - 1 - ticket : ticket;
+    const int64_t lo = row * T + p * E, hi = min(lo + E, row * T + T);
 
     C c;
-    const bool full = VEC && a.T >= K && hi - lo == E;
-    // row and step of the tile's first position (uniform; evaluated after the loads are issued)
-    auto base_of = [&]() {
-        const int64_t r = lo / a.T;
-        return RowBase{lo, r, lo - r * a.T};
-    };
+    // whole 16-byte vectors: a full tile whose rows start on a vector boundary
+    const bool full = VEC && T % K == 0 && hi - lo == E;
+    auto base_of = [&]() { return RowBase{lo, row, p * E}; };
     static_assert(Op::kStaged == 0, "staged policies run on the rows kernel only");
     if (full) c.template local_scan<true>(a, lo, lo, hi, s_a, s_b, lane, wave, false, base_of, nullptr, Nop{}, Nop{});
     else c.template local_scan<false>(a, lo, lo, hi, s_a, s_b, lane, wave, false, base_of, nullptr, Nop{}, Nop{});
     __syncthreads();
     c.wave_prefix(s_a, s_b, wave);
 
-    // A tile is read by its neighbour on the output side iff the boundary between them is not
-    // a row edge; it needs its own carry iff its carry-source boundary is not a row edge.
-    const int64_t T = a.T;
-    const bool publish = kBack ? (lo % T != 0) : (hi % T != 0 && hi < total);
-    const bool need = kBack ? (hi % T != 0) : (lo % T != 0);
+    // A tile is read by its neighbour on the output side unless it holds the row's output-side
+    // edge; it needs a carry unless it holds the row's carry-source edge.
+    const bool publish = kBack ? (p > 0) : (p < P - 1);
+    const bool need = kBack ? (p < P - 1) : (p > 0);
     if (publish && threadIdx.x == 0) {
         const Pair m = C::chunk_map(s_a, s_b);
-        const uint64_t hi_tag = uint64_t(tag) << 32;
-        st_relaxed(rec + 2 * tile, hi_tag | __float_as_uint(m.a));
-        st_relaxed(rec + 2 * tile + 1, hi_tag | __float_as_uint(m.b));
+        st_relaxed(rec + 2 * (p * N + row), uint64_t(tag0) << 32 | __float_as_uint(m.a));
+        st_relaxed(rec + 2 * (p * N + row) + 1, uint64_t(tag1) << 32 | __float_as_uint(m.b));
     }
     if (need && wave == 0) {
-        // Tiles of the same row on the carry-source side.
-        int64_t first_tile = 0, last_tile = 0;
-        if (kBack) {
-            const int64_t row_end = (hi / T) * T + T - 1;  // hi is inside the row (need)
-            last_tile = row_end / E;
-        } else {
-            const int64_t row_start = (lo / T) * T;
-            first_tile = row_start / E;
-        }
-        const float v = gather_carry<kBack>(rec, tile, first_tile, last_tile, tag, lane, hdr);
+        const float v = gather_carry<kBack>(rec + 2 * row, 2 * N, p, P, tag0, tag1, lane, hdr);
         if (lane == 0) s_carry = v;
     }
     __syncthreads();
     const float carry = need ? s_carry : 0.f;
     if (full) c.template finish<true>(a, carry);
     else c.template finish<false>(a, carry);
-
 }
 
 }  // namespace rlcs

@@ -49,11 +49,14 @@ def test_status_strings_and_version(lib):
 
 
 def test_workspace_size(lib):
-    fixed = 64 + 1024 * 64  # header, per-block counter slots
+    fixed = 64 + 1024 * 64  # header, draw slots (one per row or column block)
     assert lib.rlcs_workspace_size(0, 5) == fixed
-    assert lib.rlcs_workspace_size(64, 4096) == fixed + 16 * (64 * 4096 // 4096)
-    assert lib.rlcs_workspace_size(1, 4097) == fixed + 16 * 2
+    # one 16-byte record per 1024-step tile of every row (the shortest split tile, float32)
+    assert lib.rlcs_workspace_size(64, 4096) == fixed + 16 * 64 * 4
+    assert lib.rlcs_workspace_size(1, 4097) == fixed + 16 * 5
+    assert lib.rlcs_workspace_size(5000, 3) == fixed + 16 * 5000
     assert lib.rlcs_workspace_size(-1, 5) == fixed
+    assert lib.rlcs_workspace_size(2 ** 40, 2 ** 23) == 0  # overflows
 
 
 FAKE = ctypes.c_void_p(0x10000)       # never dereferenced: every call below fails validation
