@@ -121,7 +121,9 @@ struct ColChunk {
             rv = (Op::kRowValue && a.row_value) ? load_one<DT>(a.row_value, active ? j : 0) : 0.f;
         } else {
             if constexpr (Op::kNbr > 0) {
-                const int64_t tp = max(t0 - 1, int64_t(0));
+                // the step before the lane's first one, clamped into the column (a lane past
+                // the column's end drops it)
+                const int64_t tp = min(max(t0 - 1, int64_t(0)), T - 1);
                 pt = (a.term ? a.term : fallback)[fbase + tp * fstep];
                 pr = TR ? a.trunc[fbase + tp * fstep] : uint8_t(0);
             }
@@ -292,6 +294,102 @@ __global__ void __launch_bounds__(W * kWave) cols_rows_kernel(Args a, ColGeom g)
     if constexpr (PIPE) {
         // software pipeline: chunk i+1's loads (continuation values included, so that nothing
         // waits for the flags) go out before chunk i is scanned
+        for (int64_t i = 0; i + 1 < P; ++i) {
+            ColChunk<Op, DT, K, TR> nxt;
+            nxt.template issue<true>(a, cl.active, cl.j, cl.base, g.st, cl.fbase, cl.fstep, t0_of(i + 1));
+            __builtin_amdgcn_sched_barrier(0);  // keep those loads ahead of this chunk's first wait
+            scan(c);
+            c = nxt;
+        }
+        scan(c);
+    } else {
+        for (int64_t i = 0;; ++i) {
+            scan(c);
+            if (i + 1 == P) break;
+            c.template issue<false>(a, cl.active, cl.j, cl.base, g.st, cl.fbase, cl.fstep, t0_of(i + 1));
+        }
+    }
+}
+
+// Narrow column groups, whole columns per workgroup, no workspace: a workgroup serves
+// kNarrowCols(DT) columns (64 bytes of a step: 16 float32 or 32 bfloat16 columns), so that a
+// few thousand columns already give every CU a workgroup without splitting columns in time.
+// Lane l of a wave owns column l mod C and the (l / C)-th of the wave's 64/C lane groups, which
+// take consecutive time spans of K steps, as the W waves of the workgroup do: one chunk is
+// (64/C)*W*K steps. Per chunk, a lane's K steps compose serially, the lane groups of a wave
+// scan by shuffles, the waves compose through LDS, and the carry passes to the next chunk
+// through LDS. Two column groups share a 128-byte line; they go to workgroups b and b+8, which
+// the dispatcher deals to the same XCD (its L2 then fetches the line once). Grid: one
+// workgroup per column group.
+template <typename DT>
+constexpr int narrow_cols() { return 64 / int(sizeof(DT)); }
+
+__device__ __forceinline__ int64_t narrow_group(int64_t b, int64_t groups) {
+    const int64_t paired = groups / 16 * 16;
+    if (b >= paired) return b;
+    return b / 16 * 16 + (b % 8) * 2 + (b / 8) % 2;
+}
+
+template <class Op, typename DT, int K, int W, bool TR, bool PIPE>
+__global__ void __launch_bounds__(W * kWave) cols_narrow_kernel(Args a, ColGeom g, int64_t groups) {
+    constexpr bool kBack = Op::kBackward;
+    constexpr int C = narrow_cols<DT>();
+    constexpr int G = kWave / C;  // lane groups per wave
+    constexpr int64_t L = int64_t(G) * W * K;
+    __shared__ float s_a[W][C], s_b[W][C];
+    __shared__ float s_carry[C];
+    const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+    const int col = lane % C, grp = lane / C;
+    ColLane cl;
+    cl.j = narrow_group(blockIdx.x, groups) * C + col;
+    cl.active = cl.j < g.J;
+    {
+        const int64_t jj = cl.active ? cl.j : 0;
+        const int64_t b = jj / g.C, c = jj - b * g.C;
+        cl.base = b * g.bstride + c;
+        cl.fbase = g.fcol ? cl.base : b * g.fbstride;
+        cl.fstep = g.fcol ? g.st : g.fst;
+    }
+    const int64_t T = a.T;
+    const int64_t P = (T + L - 1) / L;
+    const int span = wave * G + grp;  // the lane's K steps within the chunk, in time order
+    float carry = 0.f;
+    auto t0_of = [&](int64_t i) { return (kBack ? P - 1 - i : i) * L + int64_t(span) * K; };
+    auto scan = [&](ColChunk<Op, DT, K, TR>& c) {
+        c.template complete<PIPE>(a, cl.base, g.st);
+        const Pair m = c.local(a.p);
+        // lane groups of the wave: inclusive scan from the carry-source side, then the
+        // composition of the groups on this group's carry-source side
+        Pair incl = m;
+#pragma unroll
+        for (int d = 1; d < G; d <<= 1) {
+            const int src = kBack ? lane + d * C : lane - d * C;
+            const Pair o{__shfl(incl.a, src), __shfl(incl.b, src)};
+            if (kBack ? (grp + d < G) : (grp >= d)) incl = compose(incl, o);
+        }
+        const int nsrc = kBack ? lane + C : lane - C;
+        const Pair nxt{__shfl(incl.a, nsrc), __shfl(incl.b, nsrc)};
+        const Pair grp_in = (kBack ? (grp + 1 < G) : (grp > 0)) ? nxt : identity_pair();
+        if (grp == (kBack ? 0 : G - 1)) {  // this lane's incl is the whole wave's map
+            s_a[wave][col] = incl.a;
+            s_b[wave][col] = incl.b;
+        }
+        __syncthreads();
+        Pair win = identity_pair();
+        if (kBack) {
+            for (int w = W - 1; w > wave; --w) win = compose(Pair{s_a[w][col], s_b[w][col]}, win);
+        } else {
+            for (int w = 0; w < wave; ++w) win = compose(Pair{s_a[w][col], s_b[w][col]}, win);
+        }
+        const float X = apply(grp_in, apply(win, carry));
+        const float out_edge = c.finish(a, a.p, cl.base, g.st, X);
+        if (span == (kBack ? 0 : G * W - 1)) s_carry[col] = out_edge;
+        __syncthreads();
+        carry = s_carry[col];
+    };
+    ColChunk<Op, DT, K, TR> c;
+    c.template issue<PIPE>(a, cl.active, cl.j, cl.base, g.st, cl.fbase, cl.fstep, t0_of(0));
+    if constexpr (PIPE) {
         for (int64_t i = 0; i + 1 < P; ++i) {
             ColChunk<Op, DT, K, TR> nxt;
             nxt.template issue<true>(a, cl.active, cl.j, cl.base, g.st, cl.fbase, cl.fstep, t0_of(i + 1));

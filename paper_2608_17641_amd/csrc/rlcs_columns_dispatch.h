@@ -30,6 +30,46 @@ inline size_t col_ws_need(int64_t J, int64_t T) {
     return kWsRecordsOffset + size_t(P * J) * kWsRecordBytes;
 }
 
+// Narrow column groups (whole columns, no workspace) when the columns fit in one 16-wave chunk
+// (256 steps) and the groups give one or two workgroups per CU. Longer columns walk chunk
+// after chunk, one workgroup per CU, and the split tiles are faster there; with more groups
+// the 1024-thread workgroups queue behind each other. C harness, cold, time-major GAE, narrow
+// against split: 256 x 4096 6.84 us against 8.23; 128 x 8192 8.04 against 8.06; 256 x 16384
+// 19.6 against 17.7; 512 x 4096 15.0 against 11.5; 2048 x 4096 55.4 against 41.7.
+constexpr int64_t kNarrowMinGroups = 256;
+constexpr int64_t kNarrowMaxGroups = 512;
+// Narrow walks of at least this many chunks overlap each chunk's loads with the scan before.
+constexpr int64_t kNarrowPipeChunks = 4;
+
+template <typename DT>
+inline int64_t narrow_groups(int64_t J) { return (J + narrow_cols<DT>() - 1) / narrow_cols<DT>(); }
+
+// Steps of a 16-wave narrow chunk (the same for both dtypes).
+constexpr int64_t kNarrowChunk = int64_t(kWave / narrow_cols<float>()) * 16 * (narrow_cols<float>() / 4);
+static_assert(kNarrowChunk == int64_t(kWave / narrow_cols<bf16_t>()) * 16 * (narrow_cols<bf16_t>() / 4),
+              "narrow chunks hold the same number of steps in both dtypes");
+
+template <class Op, typename DT, bool TR>
+void narrow_launch(const Args& a, const ColGeom& g, hipStream_t s) {
+    constexpr int C = narrow_cols<DT>();
+    constexpr int K = C / 4;  // 4 float32 or 8 bfloat16 steps per lane: 16 steps per wave
+    constexpr int G = kWave / C;
+    const dim3 grid(unsigned(narrow_groups<DT>(g.J)));
+    if (a.T <= int64_t(G) * 4 * K) {  // one 4-wave chunk
+        hipLaunchKernelGGL((cols_narrow_kernel<Op, DT, K, 4, TR, false>), grid, dim3(4 * kWave), 0,
+                           s, a, g, int64_t(grid.x));
+        return;
+    }
+    const int64_t chunks = (a.T + int64_t(G) * 16 * K - 1) / (int64_t(G) * 16 * K);
+    if (chunks >= kNarrowPipeChunks) {
+        hipLaunchKernelGGL((cols_narrow_kernel<Op, DT, K, 16, TR, true>), grid, dim3(16 * kWave), 0,
+                           s, a, g, int64_t(grid.x));
+    } else {
+        hipLaunchKernelGGL((cols_narrow_kernel<Op, DT, K, 16, TR, false>), grid, dim3(16 * kWave), 0,
+                           s, a, g, int64_t(grid.x));
+    }
+}
+
 template <class Op, typename DT, bool TR>
 void col_launch(const Args& a, const ColGeom& g, bool split, int64_t blocks, hipStream_t s) {
     const dim3 block(kColW * kWave);
@@ -56,6 +96,21 @@ rlcs_status col_dispatch(Args& a, const ColGeom& g, rlcs_dtype dtype, bool has_t
     const bool ws_ok = ws && need > 0 && ws_bytes >= need && aligned(ws, 64) &&
                        blocks <= int64_t(UINT32_MAX) / P;
     const int forced = g_variant.load(std::memory_order_relaxed);
+    const int64_t ngroups = dtype == RLCS_BF16 ? narrow_groups<bf16_t>(g.J) : narrow_groups<float>(g.J);
+    if (forced == 3 || (forced == 0 && a.T <= kNarrowChunk && ngroups >= kNarrowMinGroups &&
+                        ngroups <= kNarrowMaxGroups)) {
+        if (ngroups > INT32_MAX) return RLCS_ERR_INVALID_ARG;
+        hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+        const bool tr = Op::kFlags && has_trunc;
+        if (dtype == RLCS_BF16) {
+            if (tr) narrow_launch<Op, bf16_t, true>(a, g, s);
+            else narrow_launch<Op, bf16_t, false>(a, g, s);
+        } else {
+            if (tr) narrow_launch<Op, float, true>(a, g, s);
+            else narrow_launch<Op, float, false>(a, g, s);
+        }
+        return hipGetLastError() == hipSuccess ? RLCS_OK : RLCS_ERR_LAUNCH;
+    }
     bool split;
     if (forced == 2) {
         if (!ws_ok) return RLCS_ERR_WORKSPACE;

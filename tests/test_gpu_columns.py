@@ -1,8 +1,8 @@
 """GPU parity of the column scans through the C ABI: the time-major [T, N] entry points of every
 estimator and the F-vector eligibility traces, against the fp64 oracle on the same seeded
-inputs, with both kernel variants (whole columns per workgroup, columns split over
-workgroups). Bar: max |gpu - oracle| <= tol * (1 + max |oracle|) per output, tol = 1e-5 for
-float32 inputs and 1e-3 for bfloat16 inputs."""
+inputs, under every kernel variant (64-column walks, columns split over workgroups, narrow
+column groups of 16 or 32 columns per workgroup). Bar: max |gpu - oracle| <= tol * (1 + max
+|oracle|) per output, tol = 1e-5 for float32 inputs and 1e-3 for bfloat16 inputs."""
 import contextlib
 
 import numpy as np
@@ -115,7 +115,7 @@ def device_tm(ro, ld=None):
     return d
 
 
-@pytest.mark.parametrize("v", [0, 1, 2])
+@pytest.mark.parametrize("v", [0, 1, 2, 3])
 @pytest.mark.parametrize("T,N", [(1, 1), (7, 3), (33, 64), (256, 100), (1000, 65), (4097, 5)])
 def test_time_major_every_estimator(T, N, v):
     ro = workloads.make_rollout_time_major(T, N, seed=T * 7 + N, p_term=0.05, p_trunc=0.05)
@@ -129,7 +129,7 @@ def test_time_major_every_estimator(T, N, v):
     assert int(ws[8:12].view(torch.int32).item()) == 0
 
 
-@pytest.mark.parametrize("v", [1, 2])
+@pytest.mark.parametrize("v", [1, 2, 3])
 def test_time_major_bf16_plain_and_strided(v):
     T, N = 300, 130
     ro = workloads.make_rollout_time_major(T, N, seed=3, dtype="bf16", p_term=0.03, p_trunc=0.03)
@@ -166,7 +166,7 @@ def test_time_major_strided_padding_untouched():
                   label="tm strided")
 
 
-@pytest.mark.parametrize("v", [1, 2])
+@pytest.mark.parametrize("v", [0, 1, 2, 3])
 def test_time_major_headline_shape(v):
     """GAE on the 4096-environment x 256-step workload stored time-major, whole."""
     T, N = 256, 4096
@@ -177,6 +177,24 @@ def test_time_major_headline_shape(v):
         out = run_tm("gae", d, ws=ws)
         torch.cuda.synchronize()
     assert_parity(out, ref_tm("gae", ro), TOL["f32"], label=f"tm 256x4096 v={v}")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("T,N,ld", [(1, 17, None), (64, 1000, None), (65, 1000, 1030), (300, 1000, None),
+                                    (1100, 4100, None), (2000, 530, 600), (5000, 4096, None)])
+def test_time_major_narrow_groups(T, N, ld, dtype):
+    """Narrow column groups (16 float32 or 32 bfloat16 columns per workgroup, whole columns):
+    group counts that are and are not multiples of 16 (the line-sharing pairs of workgroups
+    b and b+8, and the unpaired tail), one 4-wave chunk, 16-wave chunks walked with and without
+    the load pipeline, strided buffers. Forced here; the automatic choice (columns of at most
+    256 steps in at least 256 groups) runs in the headline-shape test."""
+    ro = workloads.make_rollout_time_major(T, N, seed=T + N, dtype=dtype, p_term=0.03, p_trunc=0.03)
+    d = device_tm(ro, ld)
+    with variant(3):
+        for name in (TM_ESTIMATORS if T * N <= 2_000_000 else ("gae", "elig_trace")):
+            out = run_tm(name, d)
+            torch.cuda.synchronize()
+            assert_parity(out, ref_tm(name, ro), TOL[dtype], label=f"narrow {name} T={T} N={N} {dtype}")
 
 
 def test_time_major_deterministic_and_workspace_reuse():
@@ -224,7 +242,7 @@ def run_vec(ro, *, trunc=True, ws=None):
     return z, ref
 
 
-@pytest.mark.parametrize("v", [0, 1, 2])
+@pytest.mark.parametrize("v", [0, 1, 2, 3])
 @pytest.mark.parametrize("N,T,F", [(1, 1, 1), (3, 7, 5), (64, 256, 16), (7, 1000, 33),
                                    (2, 4097, 3), (5, 40, 300), (1, 33, 64)])
 def test_elig_trace_vec_shapes(N, T, F, v):

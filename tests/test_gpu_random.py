@@ -36,7 +36,7 @@ def _cases(n=160):
         out.append(dict(i=i, name=NAMES[rng.integers(0, len(NAMES))], N=N, T=T,
                         dtype=("f32", "bf16")[rng.integers(0, 2)], layout=layout, pad=pad,
                         p=float(rng.choice([0.0, 0.005, 0.05, 0.3])), trunc=bool(rng.integers(0, 2)),
-                        boot=bool(rng.integers(0, 2)), variant=int(rng.integers(0, 3)),
+                        boot=bool(rng.integers(0, 2)), variant=int(rng.integers(0, 4)),
                         seed=int(rng.integers(0, 2 ** 31))))
     return out
 
