@@ -407,59 +407,148 @@ __global__ void __launch_bounds__(W * kWave) cols_narrow_kernel(Args a, ColGeom 
     }
 }
 
-// Look-back of one lane's column: the value entering tile `tile` from its carry-source side,
-// composed from the published maps of the column's tiles, nearest first, until a map with
-// beta = 0 (the column's edge tile always has one). Up to kColLookAhead records are read per
-// round. Bounded polls: on exhaustion the error flag is set and NaN returned.
+// Look-back over block aggregates, in ticket space (ticket 0 holds the column's carry-source
+// edge; a tile's carry comes from the tiles of lower tickets). Level-l block q of a column is
+// the tiles of tickets [q * 2^l, (q + 1) * 2^l); its map composes the maps of its two halves,
+// the upper half outermost, and is published by the block's last ticket, which finishes the
+// levels its ticket t closes (2^l divides t + 1) one after the other, each waiting for the lower
+// half's map. The value entering tile t composes, nearest first, the blocks of a fixed
+// decomposition of [0, t): from y = t down, a block [y - 2^l, y) with l the lesser of the
+// number of trailing zero bits of y and (steps taken - kColLiftAfter), so the first steps read
+// single tiles and later ones doubling blocks: O(log t) reads down to the edge. It stops at the
+// first block with beta = 0 (an episode edge; ticket 0 always holds one). The decomposition
+// depends only on t and every block composes in a fixed order, so results are bitwise
+// reproducible; a column without flags and gamma*lambda = 1 no longer reads all t maps.
+// Building the blocks makes some workgroups wait for chains of them, so the host asks for them
+// (`lift`) only when a look-back can be long: when the product of the betas of a run of tiles
+// cannot underflow to 0 within a few dozen tiles. Otherwise every block read is a single tile.
+// Records of level l start at block sum over l' < l of (P >> l'); a record is two 64-bit words
+// per column at index (offset + q) * J + j.
 constexpr int kColLookAhead = 4;
+constexpr int kColLiftAfter = 3;
 
-template <bool kBack>
-__device__ float cols_gather(const uint64_t* rec, int64_t tile, int64_t P, int64_t J, int64_t j,
+__device__ __forceinline__ int64_t col_level_offset(int64_t P, int l) {
+    int64_t off = 0;
+    for (int k = 0; k < l; ++k) off += P >> k;
+    return off;
+}
+
+__device__ __forceinline__ Pair col_wait_record(const uint64_t* r, uint32_t tag0, uint32_t tag1,
+                                                uint64_t w0, uint64_t w1, WsHeader* hdr, bool& ok) {
+    uint32_t polls = 0;
+    while (uint32_t(w0 >> 32) != tag0 || uint32_t(w1 >> 32) != tag1) {
+        if (++polls > kMaxPolls) {
+            st_relaxed(&hdr->error, 1u);
+            ok = false;
+            return Pair{__builtin_nanf(""), 0.f};
+        }
+        __builtin_amdgcn_s_sleep(1);
+        w0 = ld_relaxed(r);
+        w1 = ld_relaxed(r + 1);
+    }
+    return Pair{__uint_as_float(uint32_t(w0)), __uint_as_float(uint32_t(w1))};
+}
+
+// Value entering the tile of ticket t (t > 0) in column j. Bounded polls: on exhaustion the
+// error flag is set and NaN returned.
+template <bool LIFT>
+__device__ float cols_gather(const uint64_t* rec, int64_t t, int64_t P, int64_t J, int64_t j,
                              uint32_t tag0, uint32_t tag1, WsHeader* hdr) {
     Pair acc = identity_pair();
-    int64_t dist = 1;
-    for (;;) {
-        uint64_t w0[kColLookAhead], w1[kColLookAhead];
+    if constexpr (!LIFT) {
+        // single tiles only: tickets t-1, t-2, ..., kColLookAhead per round
+        for (int64_t d = 1;; d += kColLookAhead) {
+            uint64_t w0[kColLookAhead], w1[kColLookAhead];
 #pragma unroll
-        for (int i = 0; i < kColLookAhead; ++i) {
-            const int64_t q = kBack ? tile + dist + i : tile - dist - i;
-            const bool inside = kBack ? (q < P) : (q >= 0);
-            w0[i] = w1[i] = 0;
-            if (inside) {
-                w0[i] = ld_relaxed(rec + 2 * (q * J + j));
-                w1[i] = ld_relaxed(rec + 2 * (q * J + j) + 1);
+            for (int i = 0; i < kColLookAhead; ++i) {
+                const int64_t q = t - d - i;
+                w0[i] = w1[i] = 0;
+                if (q >= 0) {
+                    w0[i] = ld_relaxed(rec + 2 * (q * J + j));
+                    w1[i] = ld_relaxed(rec + 2 * (q * J + j) + 1);
+                }
+            }
+#pragma unroll
+            for (int i = 0; i < kColLookAhead; ++i) {
+                const int64_t q = t - d - i;
+                if (q < 0) return acc.a;  // past the edge tile (not reached: its beta is 0)
+                bool ok = true;
+                const Pair m = col_wait_record(rec + 2 * (q * J + j), tag0, tag1, w0[i], w1[i], hdr, ok);
+                if (!ok) return __builtin_nanf("");
+                acc = compose(acc, m);
+                if (m.b == 0.f) return acc.a;
+            }
+        }
+    }
+    int64_t y = t;
+    int step = 0;
+    while (y > 0) {
+        // the next kColLookAhead blocks of the decomposition, read together
+        const uint64_t* r[kColLookAhead];
+        uint64_t w0[kColLookAhead], w1[kColLookAhead];
+        int n = 0;
+        int64_t yy = y;
+#pragma unroll
+        for (int k = 0; k < kColLookAhead; ++k) {
+            r[k] = nullptr;
+            w0[k] = w1[k] = 0;
+            if (yy > 0) {
+                const int lim = max(step + k - kColLiftAfter, 0);
+                const int l = min(int(__builtin_ctzll(uint64_t(yy))), lim);
+                const int64_t q = (yy >> l) - 1;
+                r[k] = rec + 2 * ((col_level_offset(P, l) + q) * J + j);
+                w0[k] = ld_relaxed(r[k]);
+                w1[k] = ld_relaxed(r[k] + 1);
+                yy -= int64_t(1) << l;
+                n = k + 1;
             }
         }
 #pragma unroll
-        for (int i = 0; i < kColLookAhead; ++i) {
-            const int64_t q = kBack ? tile + dist + i : tile - dist - i;
-            const bool inside = kBack ? (q < P) : (q >= 0);
-            if (!inside) return acc.a;  // past the column's edge tile (not reached in practice)
-            uint32_t polls = 0;
-            while (uint32_t(w0[i] >> 32) != tag0 || uint32_t(w1[i] >> 32) != tag1) {
-                if (++polls > kMaxPolls) {
-                    st_relaxed(&hdr->error, 1u);
-                    return __builtin_nanf("");
-                }
-                __builtin_amdgcn_s_sleep(1);
-                w0[i] = ld_relaxed(rec + 2 * (q * J + j));
-                w1[i] = ld_relaxed(rec + 2 * (q * J + j) + 1);
-            }
-            const Pair m{__uint_as_float(uint32_t(w0[i])), __uint_as_float(uint32_t(w1[i]))};
+        for (int k = 0; k < kColLookAhead; ++k) {
+            if (k >= n) break;
+            bool ok = true;
+            const Pair m = col_wait_record(r[k], tag0, tag1, w0[k], w1[k], hdr, ok);
+            if (!ok) return __builtin_nanf("");
             acc = compose(acc, m);
             if (m.b == 0.f) return acc.a;
         }
-        dist += kColLookAhead;
+        y = yy;
+        step += n;
+    }
+    return acc.a;  // not reached: ticket 0's map has beta = 0
+}
+
+// Publishes the level-l maps that ticket t closes (block [t + 1 - 2^l, t + 1) for every l with
+// 2^l dividing t + 1), starting from `m`, the tile's own map; each waits for the map of the
+// block's lower half.
+__device__ void cols_publish_levels(uint64_t* rec, int64_t t, int64_t P, int64_t J, int64_t j,
+                                    Pair m, uint32_t tag0, uint32_t tag1, WsHeader* hdr) {
+    int64_t off_prev = 0;  // offset of level l - 1
+    for (int l = 1; l < 63 && ((t + 1) & ((int64_t(1) << l) - 1)) == 0; ++l) {
+        const int64_t q = ((t + 1) >> l) - 1;           // this block at level l
+        const int64_t lower = 2 * q;                     // its lower half at level l - 1
+        const uint64_t* r = rec + 2 * ((off_prev + lower) * J + j);
+        bool ok = true;
+        const Pair h = col_wait_record(r, tag0, tag1, ld_relaxed(r), ld_relaxed(r + 1), hdr, ok);
+        if (!ok) return;
+        m = compose(m, h);
+        const int64_t off = off_prev + (P >> (l - 1));
+        uint64_t* w = rec + 2 * ((off + q) * J + j);
+        st_relaxed(w, uint64_t(tag0) << 32 | __float_as_uint(m.a));
+        st_relaxed(w + 1, uint64_t(tag1) << 32 | __float_as_uint(m.b));
+        off_prev = off;
     }
 }
 
 // One chunk per workgroup. Workgroup g serves column block g mod num_blocks; its ticket among
 // that block's P workgroups orders the block's tiles from the carry source, so a tile only waits
-// for tiles of its block that drew earlier tickets. Grid: num_blocks * P workgroups.
-template <class Op, typename DT, int K, int W, bool TR>
+// for tiles of its block that drew earlier tickets. LIFT: publish and read block aggregates.
+// Grid: num_blocks * P workgroups.
+template <class Op, typename DT, int K, int W, bool TR, bool LIFT>
 __global__ void __launch_bounds__(W * kWave) cols_tiles_kernel(Args a, ColGeom g, int64_t num_blocks) {
     constexpr bool kBack = Op::kBackward;
     constexpr int64_t L = int64_t(W) * K;
+    static_assert(W >= 2, "wave 1 publishes the block aggregates while wave 0 looks back");
     __shared__ float s_a[W][kWave], s_b[W][kWave];
     __shared__ float s_carry[kWave];
     __shared__ uint32_t s_ticket, s_tag;
@@ -494,22 +583,27 @@ __global__ void __launch_bounds__(W * kWave) cols_tiles_kernel(Args a, ColGeom g
     s_b[wave][lane] = m.b;
     __syncthreads();
     const Pair win = cols_wave_in<kBack, W>(s_a, s_b, wave, lane);
-    const bool publish = kBack ? (p > 0) : (p < P - 1);
-    const bool need = kBack ? (p < P - 1) : (p > 0);
-    if (wave == 0) {
-        if (publish && cl.active) {
-            // the whole tile's map of this column
-            Pair tm = identity_pair();
-            if (kBack) {
-                for (int w = W - 1; w >= 0; --w) tm = compose(Pair{s_a[w][lane], s_b[w][lane]}, tm);
-            } else {
-                for (int w = 0; w < W; ++w) tm = compose(Pair{s_a[w][lane], s_b[w][lane]}, tm);
-            }
-            st_relaxed(rec + 2 * (p * g.J + cl.j), uint64_t(tag0) << 32 | __float_as_uint(tm.a));
-            st_relaxed(rec + 2 * (p * g.J + cl.j) + 1, uint64_t(tag1) << 32 | __float_as_uint(tm.b));
+    // In ticket space: a tile is read by higher tickets unless it is the last one, and needs a
+    // carry unless it holds the carry-source edge (ticket 0).
+    const bool publish = ticket < P - 1;
+    const bool need = ticket > 0;
+    if ((wave == 0 || (wave == 1 && LIFT)) && publish && cl.active) {
+        // the whole tile's map of this column
+        Pair tm = identity_pair();
+        if (kBack) {
+            for (int w = W - 1; w >= 0; --w) tm = compose(Pair{s_a[w][lane], s_b[w][lane]}, tm);
+        } else {
+            for (int w = 0; w < W; ++w) tm = compose(Pair{s_a[w][lane], s_b[w][lane]}, tm);
         }
-        s_carry[lane] = (need && cl.active) ? cols_gather<kBack>(rec, p, P, g.J, cl.j, tag0, tag1, hdr) : 0.f;
+        if (wave == 0) {
+            st_relaxed(rec + 2 * (ticket * g.J + cl.j), uint64_t(tag0) << 32 | __float_as_uint(tm.a));
+            st_relaxed(rec + 2 * (ticket * g.J + cl.j) + 1, uint64_t(tag1) << 32 | __float_as_uint(tm.b));
+        } else {
+            cols_publish_levels(rec, ticket, P, g.J, cl.j, tm, tag0, tag1, hdr);
+        }
     }
+    if (wave == 0)
+        s_carry[lane] = (need && cl.active) ? cols_gather<LIFT>(rec, ticket, P, g.J, cl.j, tag0, tag1, hdr) : 0.f;
     __syncthreads();
     c.finish(a, a.p, cl.base, g.st, apply(win, s_carry[lane]));
 }

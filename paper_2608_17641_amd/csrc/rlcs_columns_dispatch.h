@@ -2,6 +2,8 @@
 // the choice between whole columns per workgroup and split columns, and the launches.
 #pragma once
 
+#include <cmath>
+
 #include "rlcs_columns.h"
 #include "rlcs_dispatch.h"
 
@@ -70,13 +72,34 @@ void narrow_launch(const Args& a, const ColGeom& g, hipStream_t s) {
     }
 }
 
+// Split tiles publish block aggregates for long look-backs when a look-back may pass more than
+// this many tiles before the product of their betas underflows to 0.
+constexpr int64_t kColLiftTiles = 32;
+
+// Whether a look-back over P tiles of kColSplitL steps can be long: each step's beta is at most
+// gamma * lambda * max(1, c_bar) for every column scan, and a product of betas below about
+// 1.4e-45 is 0 in float32.
+inline bool col_lift(const Params& p, int64_t P) {
+    if (P <= kColLiftTiles) return false;
+    const double bmax = double(p.gamma) * double(p.lambda) * (p.c_bar > 1.f ? double(p.c_bar) : 1.0);
+    if (!(bmax < 1.0)) return true;
+    if (bmax <= 0.0) return false;
+    const double tiles = 104.0 / (double(kColSplitL) * -std::log(bmax)) + 1.0;
+    return tiles > double(kColLiftTiles);
+}
+
 template <class Op, typename DT, bool TR>
 void col_launch(const Args& a, const ColGeom& g, bool split, int64_t blocks, hipStream_t s) {
     const dim3 block(kColW * kWave);
     if (split) {
-        hipLaunchKernelGGL((cols_tiles_kernel<Op, DT, kColK, kColSplitW, TR>),
-                           dim3(unsigned(blocks * col_split_tiles(a.T))), dim3(kColSplitW * kWave),
-                           0, s, a, g, blocks);
+        const int64_t P = col_split_tiles(a.T);
+        const dim3 grid(unsigned(blocks * P)), tile_block(kColSplitW * kWave);
+        if (col_lift(a.p, P))
+            hipLaunchKernelGGL((cols_tiles_kernel<Op, DT, kColK, kColSplitW, TR, true>), grid,
+                               tile_block, 0, s, a, g, blocks);
+        else
+            hipLaunchKernelGGL((cols_tiles_kernel<Op, DT, kColK, kColSplitW, TR, false>), grid,
+                               tile_block, 0, s, a, g, blocks);
     } else if (col_tiles(a.T) >= kColPipeChunks) {
         hipLaunchKernelGGL((cols_rows_kernel<Op, DT, kColK, kColW, TR, true>), dim3(unsigned(blocks)),
                            block, 0, s, a, g);

@@ -230,6 +230,56 @@ def test_time_major_no_flags_long_lookback():
             assert_parity(out, ref_tm(name, ro, trunc=False), TOL["f32"], label=f"no flags {name}")
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_block_aggregates_with_rare_flags(dtype):
+    """Columns of 256 split tiles with gamma * lambda = 1 (c_bar = inf for V-Trace) and rare
+    flags (episodes of about 250 steps): look-backs run past their first tiles into block
+    aggregates, some of which hold an episode edge. Against the oracle, and bitwise run to run;
+    vector traces of 128 tiles the same way."""
+    T, N = 16384, 70
+    ro = workloads.make_rollout_time_major(T, N, seed=21, dtype=dtype, p_term=0.002, p_trunc=0.002)
+    d = {k: (v.t() if v.dim() == 2 else v) for k, v in device_tm(ro).items()}
+    ws = rl.make_workspace_columns(N, T, DEV)
+    tm = oracle.time_major
+    calls = {
+        "gae": (lambda: rl.rlcs_gae_strided(d["r"], d["v"], d["term"], d["trunc"], d["bv"], d["boot"],
+                                            gamma=1.0, lam=1.0, ws=ws),
+                lambda: tm(oracle.gae, ro["r"], ro["v"], ro["term"], ro["trunc"], ro["bv"], ro["boot"],
+                           gamma=1.0, lam=1.0)),
+        "vtrace": (lambda: rl.rlcs_vtrace_strided(d["r"], d["v"], d["log_rho"], d["term"], d["trunc"],
+                                                  d["bv"], d["boot"], gamma=1.0, rho_bar=1.0,
+                                                  c_bar=float("inf"), ws=ws),
+                   lambda: tm(oracle.vtrace, ro["r"], ro["v"], ro["log_rho"], ro["term"], ro["trunc"],
+                              ro["bv"], ro["boot"], gamma=1.0, rho_bar=1.0, c_bar=float("inf"))),
+        "elig_trace": (lambda: (rl.rlcs_elig_trace_strided(d["x"], d["term"], d["trunc"], gamma=1.0,
+                                                           lam=1.0, ws=ws),),
+                       lambda: (tm(oracle.elig_trace, ro["x"], ro["term"], ro["trunc"], gamma=1.0,
+                                   lam=1.0),)),
+        "prefix": (lambda: (rl.rlcs_episodic_prefix_strided(d["x"], d["term"], d["trunc"],
+                                                            boundary="ends_at", ws=ws),),
+                   lambda: (tm(oracle.episodic_prefix, ro["x"], ro["term"], ro["trunc"],
+                               boundary="ends_at"),)),
+    }
+    for name, (gpu, ref) in calls.items():
+        first = [o.clone() for o in gpu() if o is not None]
+        again = [o for o in gpu() if o is not None]
+        torch.cuda.synchronize()
+        for a, b in zip(first, again):
+            assert torch.equal(a, b), f"{name}: not bitwise reproducible"
+        expect = [r for r in ref() if r is not None]
+        assert_parity({str(i): o.t() for i, o in enumerate(first)},
+                      {str(i): r for i, r in enumerate(expect)}, TOL[dtype],
+                      label=f"block aggregates {name} {dtype}")
+    assert int(ws[8:12].view(torch.int32).item()) == 0
+    vr = workloads.make_vector_trace(2, 8192, 40, seed=22, p_term=0.002, p_trunc=0.002)
+    dv = {k: to_device(v, DEV) for k, v in vr.items()}
+    wsv = rl.make_workspace_columns(2 * 40, 8192, DEV)
+    z = rl.rlcs_elig_trace_vec(dv["x"], dv["term"], dv["trunc"], gamma=1.0, lam=1.0, ws=wsv)
+    torch.cuda.synchronize()
+    zr = oracle.elig_trace_vec(vr["x"], vr["term"], vr["trunc"], gamma=1.0, lam=1.0)
+    assert_parity({"z": z}, {"z": zr}, TOL["f32"], label="block aggregates vector traces")
+
+
 # ---------------------------------------------------------------- vector eligibility traces
 
 def run_vec(ro, *, trunc=True, ws=None):
