@@ -458,6 +458,8 @@ def run_extra(dev, only=""):
                           ("tm_64x65536", 64, 65536)):
         if label.startswith(only):
             run_time_major(label, t_, n_, dev)
+    if "tm_noflags_16384x64".startswith(only):
+        run_time_major("tm_noflags_16384x64", 16384, 64, dev, noflags=True)
     for label, n_, t_, ld in (("sr_4096x256_ld320", 4096, 256, 320), ("sr_64x4096_ld4160", 64, 4096, 4160)):
         if label.startswith(only):
             run_strided_rows(label, n_, t_, ld, dev)
@@ -574,14 +576,17 @@ def _measure(label, name, call, sets, nbytes, steps, rel):
     print(f"profile pass: {label} {name} x{_PROFILE['calls']}", file=sys.stderr, flush=True)
 
 
-def run_time_major(label, t_, n_, dev):
+def run_time_major(label, t_, n_, dev, noflags=False):
     """GAE and V-Trace on a time-major [T, N] fp32 buffer with truncation: parity on sampled
-    environments, then graph-timed. Same dense byte count as the row-major form."""
+    environments, then graph-timed. Same dense byte count as the row-major form. `noflags`: GAE
+    alone, a termination array with no flag set, no truncation, gamma = lambda = 1 (every
+    look-back runs to the column's edge)."""
     import torch
     import oracle
     import workloads
     import paper_2608_17641_amd as rl
-    ro = workloads.make_rollout_time_major(t_, n_, 0, p_term=0.02, p_trunc=0.01)
+    ro = workloads.make_rollout_time_major(t_, n_, 0, p_term=0.0 if noflags else 0.02,
+                                           p_trunc=0.0 if noflags else 0.01)
     base = {k: torch.from_numpy(np.ascontiguousarray(v)).to(dev) for k, v in ro.items()}
     set_bytes = sum(v.numel() * v.element_size() for v in base.values()) + 8 * n_ * t_
     S = max(1, min(32, -(-600_000_000 // set_bytes)))
@@ -589,8 +594,14 @@ def run_time_major(label, t_, n_, dev):
     ws = rl.make_workspace_columns(n_, t_, dev)
     cols = np.unique(np.concatenate([[0, n_ - 1], np.random.default_rng(1).integers(0, n_, 32)]))
     g = lambda k: np.ascontiguousarray(ro[k][:, cols]) if ro[k].ndim == 2 else ro[k][cols]
-    for name in ("gae", "vtrace"):
-        if name == "gae":
+    for name in (("gae",) if noflags else ("gae", "vtrace")):
+        if noflags:
+            call = lambda d: rl.rlcs_gae_strided(d["r"].t(), d["v"].t(), d["term"].t(), None, None,
+                                                 d["boot"], d["o0"].t(), d["o1"].t(), gamma=1.0,
+                                                 lam=1.0, ws=ws)
+            refs = oracle.time_major(oracle.gae, g("r"), g("v"), g("term"), None, None, g("boot"),
+                                     gamma=1.0, lam=1.0)
+        elif name == "gae":
             call = lambda d: rl.rlcs_gae_strided(d["r"].t(), d["v"].t(), d["term"].t(), d["trunc"].t(),
                                                  d["bv"].t(), d["boot"], d["o0"].t(), d["o1"].t(),
                                                  gamma=0.99, lam=0.95, ws=ws)
@@ -611,7 +622,7 @@ def run_time_major(label, t_, n_, dev):
             rel = max(rel, float(np.max(np.abs(got - r_))) / (1 + float(np.max(np.abs(r_)))))
         if rel > 1e-5:
             raise SystemExit(f"parity failure in {label} {name}: {rel}")
-        nbytes = extra_bytes(name, n_, t_, 4, True, True)
+        nbytes = extra_bytes(name, n_, t_, 4, not noflags, True)
         _measure(label, name + "_tm", call, sets, nbytes, n_ * t_, rel)
 
 

@@ -318,16 +318,17 @@ __global__ void __launch_bounds__(W * kWave) cols_rows_kernel(Args a, ColGeom g)
 // take consecutive time spans of K steps, as the W waves of the workgroup do: one chunk is
 // (64/C)*W*K steps. Per chunk, a lane's K steps compose serially, the lane groups of a wave
 // scan by shuffles, the waves compose through LDS, and the carry passes to the next chunk
-// through LDS. Two column groups share a 128-byte line; they go to workgroups b and b+8, which
-// the dispatcher deals to the same XCD (its L2 then fetches the line once). Grid: one
-// workgroup per column group.
+// through LDS. A 128-byte line of data spans two column groups and a line of flags eight
+// (float32; four for bfloat16). The dispatcher deals workgroup b to XCD b mod 8, so in every run
+// of 64 workgroups the eight of XCD x take groups 8x .. 8x+7: each line is fetched by one L2.
+// Grid: one workgroup per column group.
 template <typename DT>
 constexpr int narrow_cols() { return 64 / int(sizeof(DT)); }
 
 __device__ __forceinline__ int64_t narrow_group(int64_t b, int64_t groups) {
-    const int64_t paired = groups / 16 * 16;
-    if (b >= paired) return b;
-    return b / 16 * 16 + (b % 8) * 2 + (b / 8) % 2;
+    const int64_t dealt = groups / 64 * 64;
+    if (b >= dealt) return b;
+    return b / 64 * 64 + (b % 8) * 8 + (b / 8) % 8;
 }
 
 template <class Op, typename DT, int K, int W, bool TR, bool PIPE>

@@ -181,12 +181,13 @@ def test_time_major_headline_shape(v):
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("T,N,ld", [(1, 17, None), (64, 1000, None), (65, 1000, 1030), (300, 1000, None),
-                                    (1100, 4100, None), (2000, 530, 600), (5000, 4096, None)])
+                                    (64, 1600, 1700), (1100, 4100, None), (2000, 530, 600),
+                                    (5000, 4096, None)])
 def test_time_major_narrow_groups(T, N, ld, dtype):
     """Narrow column groups (16 float32 or 32 bfloat16 columns per workgroup, whole columns):
-    group counts that are and are not multiples of 16 (the line-sharing pairs of workgroups
-    b and b+8, and the unpaired tail), one 4-wave chunk, 16-wave chunks walked with and without
-    the load pipeline, strided buffers. Forced here; the automatic choice (columns of at most
+    group counts below, at and above multiples of 64 (runs of 64 workgroups deal eight
+    consecutive groups to each XCD; the rest keep their order), one 4-wave chunk, 16-wave chunks
+    walked with and without the load pipeline, strided buffers. Forced here; the automatic choice (columns of at most
     256 steps in at least 256 groups) runs in the headline-shape test."""
     ro = workloads.make_rollout_time_major(T, N, seed=T + N, dtype=dtype, p_term=0.03, p_trunc=0.03)
     d = device_tm(ro, ld)
