@@ -229,6 +229,15 @@ struct ColChunk {
     }
 };
 
+// Two 64-column blocks share a 128-byte line of flags; the dispatcher deals workgroup b to XCD
+// b mod 8, so in every run of 16 workgroups b and b+8 take blocks 2m and 2m+1 (one L2 fetches
+// the line).
+__device__ __forceinline__ int64_t paired_block(int64_t b, int64_t blocks) {
+    const int64_t dealt = blocks / 16 * 16;
+    if (b >= dealt) return b;
+    return b / 16 * 16 + (b % 8) * 2 + (b / 8) % 2;
+}
+
 // Per-lane column placement.
 struct ColLane {
     int64_t j, base, fbase, fstep;
@@ -271,7 +280,7 @@ __global__ void __launch_bounds__(W * kWave) cols_rows_kernel(Args a, ColGeom g)
     __shared__ float s_a[W][kWave], s_b[W][kWave];
     __shared__ float s_carry[kWave];
     const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
-    const ColLane cl = col_lane(g, blockIdx.x);
+    const ColLane cl = col_lane(g, paired_block(blockIdx.x, gridDim.x));
     const int64_t T = a.T;
     const int64_t P = (T + L - 1) / L;
     float carry = 0.f;
@@ -558,7 +567,8 @@ __global__ void __launch_bounds__(W * kWave) cols_tiles_kernel(Args a, ColGeom g
     const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
     const int64_t T = a.T;
     const int64_t P = (T + L - 1) / L;
-    const int64_t block = int64_t(blockIdx.x) % num_blocks;
+    const int64_t block = num_blocks % 8 == 0 ? paired_block(int64_t(blockIdx.x) % num_blocks, num_blocks)
+                                              : int64_t(blockIdx.x) % num_blocks;
 
     if (threadIdx.x == 0) {
         uint32_t gen;
