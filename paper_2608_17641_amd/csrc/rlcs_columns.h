@@ -45,6 +45,10 @@ struct ColGeom {
     int64_t fst;       // flags between consecutive steps (flags not per column)
     int64_t fbstride;  // flags between batch rows (flags not per column)
     int fcol;          // flags laid out like the data
+    // Outputs by non-temporal stores (the kernels' NT). They suit steps whose 64 columns fill
+    // whole 128-byte lines; where a batch row holds fewer (vector traces of F % 32 != 0) each
+    // partial line would go to memory as a whole one, and plain stores, merged in L2, write less.
+    int nt_store;
 };
 
 constexpr int kColK = 8;  // steps per lane
@@ -205,6 +209,7 @@ struct ColChunk {
 
     // Step 5 given X, the value entering the lane's steps from the carry-source side. Returns
     // the value of the lane's step nearest the output side.
+    template <bool NT>
     __device__ __forceinline__ float finish(const Args& a, const Params& P, int64_t base, int64_t st, float X) {
         float A[K];
         if (kBack) {
@@ -222,8 +227,13 @@ struct ColChunk {
         for (int k = 0; k < K; ++k) {
             if (!bit(valid, k)) continue;
             const int64_t e = base + (t0 + k) * st;
-            __builtin_nontemporal_store(o0[k], a.out0 + e);
-            if (a.out1) __builtin_nontemporal_store(o1[k], a.out1 + e);
+            if constexpr (NT) {
+                __builtin_nontemporal_store(o0[k], a.out0 + e);
+                if (a.out1) __builtin_nontemporal_store(o1[k], a.out1 + e);
+            } else {
+                a.out0[e] = o0[k];
+                if (a.out1) a.out1[e] = o1[k];
+            }
         }
         return kBack ? A[0] : A[K - 1];
     }
@@ -273,7 +283,7 @@ __device__ __forceinline__ Pair cols_wave_in(const float (*s_a)[kWave], const fl
 // output-side edge carried to the next chunk through LDS. PIPE (columns of several chunks):
 // the next chunk's loads are in flight while a chunk is scanned. Grid: ceil(J / 64)
 // workgroups.
-template <class Op, typename DT, int K, int W, bool TR, bool PIPE>
+template <class Op, typename DT, int K, int W, bool TR, bool PIPE, bool NT = true>
 __global__ void __launch_bounds__(W * kWave) cols_rows_kernel(Args a, ColGeom g) {
     constexpr bool kBack = Op::kBackward;
     constexpr int64_t L = int64_t(W) * K;
@@ -293,7 +303,7 @@ __global__ void __launch_bounds__(W * kWave) cols_rows_kernel(Args a, ColGeom g)
         s_b[wave][lane] = m.b;
         __syncthreads();
         const Pair win = cols_wave_in<kBack, W>(s_a, s_b, wave, lane);
-        const float out_edge = c.finish(a, a.p, cl.base, g.st, apply(win, carry));
+        const float out_edge = c.template finish<NT>(a, a.p, cl.base, g.st, apply(win, carry));
         if (wave == (kBack ? 0 : W - 1)) s_carry[lane] = out_edge;
         __syncthreads();
         carry = s_carry[lane];
@@ -340,7 +350,7 @@ __device__ __forceinline__ int64_t narrow_group(int64_t b, int64_t groups) {
     return b / 64 * 64 + (b % 8) * 8 + (b / 8) % 8;
 }
 
-template <class Op, typename DT, int K, int W, bool TR, bool PIPE>
+template <class Op, typename DT, int K, int W, bool TR, bool PIPE, bool NT = true>
 __global__ void __launch_bounds__(W * kWave) cols_narrow_kernel(Args a, ColGeom g, int64_t groups) {
     constexpr bool kBack = Op::kBackward;
     constexpr int C = narrow_cols<DT>();
@@ -392,7 +402,7 @@ __global__ void __launch_bounds__(W * kWave) cols_narrow_kernel(Args a, ColGeom 
             for (int w = 0; w < wave; ++w) win = compose(Pair{s_a[w][col], s_b[w][col]}, win);
         }
         const float X = apply(grp_in, apply(win, carry));
-        const float out_edge = c.finish(a, a.p, cl.base, g.st, X);
+        const float out_edge = c.template finish<NT>(a, a.p, cl.base, g.st, X);
         if (span == (kBack ? 0 : G * W - 1)) s_carry[col] = out_edge;
         __syncthreads();
         carry = s_carry[col];
@@ -554,7 +564,7 @@ __device__ void cols_publish_levels(uint64_t* rec, int64_t t, int64_t P, int64_t
 // that block's P workgroups orders the block's tiles from the carry source, so a tile only waits
 // for tiles of its block that drew earlier tickets. LIFT: publish and read block aggregates.
 // Grid: num_blocks * P workgroups.
-template <class Op, typename DT, int K, int W, bool TR, bool LIFT>
+template <class Op, typename DT, int K, int W, bool TR, bool LIFT, bool NT = true>
 __global__ void __launch_bounds__(W * kWave) cols_tiles_kernel(Args a, ColGeom g, int64_t num_blocks) {
     constexpr bool kBack = Op::kBackward;
     constexpr int64_t L = int64_t(W) * K;
@@ -616,7 +626,7 @@ __global__ void __launch_bounds__(W * kWave) cols_tiles_kernel(Args a, ColGeom g
     if (wave == 0)
         s_carry[lane] = (need && cl.active) ? cols_gather<LIFT>(rec, ticket, P, g.J, cl.j, tag0, tag1, hdr) : 0.f;
     __syncthreads();
-    c.finish(a, a.p, cl.base, g.st, apply(win, s_carry[lane]));
+    c.template finish<NT>(a, a.p, cl.base, g.st, apply(win, s_carry[lane]));
 }
 
 }  // namespace rlcs

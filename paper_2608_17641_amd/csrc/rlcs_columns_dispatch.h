@@ -3,6 +3,7 @@
 #pragma once
 
 #include <cmath>
+#include <type_traits>
 
 #include "rlcs_columns.h"
 #include "rlcs_dispatch.h"
@@ -51,23 +52,23 @@ constexpr int64_t kNarrowChunk = int64_t(kWave / narrow_cols<float>()) * 16 * (n
 static_assert(kNarrowChunk == int64_t(kWave / narrow_cols<bf16_t>()) * 16 * (narrow_cols<bf16_t>() / 4),
               "narrow chunks hold the same number of steps in both dtypes");
 
-template <class Op, typename DT, bool TR>
-void narrow_launch(const Args& a, const ColGeom& g, hipStream_t s) {
+template <class Op, typename DT, bool TR, bool NT>
+void narrow_launch_nt(const Args& a, const ColGeom& g, hipStream_t s) {
     constexpr int C = narrow_cols<DT>();
     constexpr int K = C / 4;  // 4 float32 or 8 bfloat16 steps per lane: 16 steps per wave
     constexpr int G = kWave / C;
     const dim3 grid(unsigned(narrow_groups<DT>(g.J)));
     if (a.T <= int64_t(G) * 4 * K) {  // one 4-wave chunk
-        hipLaunchKernelGGL((cols_narrow_kernel<Op, DT, K, 4, TR, false>), grid, dim3(4 * kWave), 0,
+        hipLaunchKernelGGL((cols_narrow_kernel<Op, DT, K, 4, TR, false, NT>), grid, dim3(4 * kWave), 0,
                            s, a, g, int64_t(grid.x));
         return;
     }
     const int64_t chunks = (a.T + int64_t(G) * 16 * K - 1) / (int64_t(G) * 16 * K);
     if (chunks >= kNarrowPipeChunks) {
-        hipLaunchKernelGGL((cols_narrow_kernel<Op, DT, K, 16, TR, true>), grid, dim3(16 * kWave), 0,
+        hipLaunchKernelGGL((cols_narrow_kernel<Op, DT, K, 16, TR, true, NT>), grid, dim3(16 * kWave), 0,
                            s, a, g, int64_t(grid.x));
     } else {
-        hipLaunchKernelGGL((cols_narrow_kernel<Op, DT, K, 16, TR, false>), grid, dim3(16 * kWave), 0,
+        hipLaunchKernelGGL((cols_narrow_kernel<Op, DT, K, 16, TR, false, NT>), grid, dim3(16 * kWave), 0,
                            s, a, g, int64_t(grid.x));
     }
 }
@@ -88,25 +89,46 @@ inline bool col_lift(const Params& p, int64_t P) {
     return tiles > double(kColLiftTiles);
 }
 
-template <class Op, typename DT, bool TR>
-void col_launch(const Args& a, const ColGeom& g, bool split, int64_t blocks, hipStream_t s) {
+template <class Op, typename DT, bool TR, bool NT>
+void col_launch_nt(const Args& a, const ColGeom& g, bool split, int64_t blocks, hipStream_t s) {
     const dim3 block(kColW * kWave);
     if (split) {
         const int64_t P = col_split_tiles(a.T);
         const dim3 grid(unsigned(blocks * P)), tile_block(kColSplitW * kWave);
         if (col_lift(a.p, P))
-            hipLaunchKernelGGL((cols_tiles_kernel<Op, DT, kColK, kColSplitW, TR, true>), grid,
+            hipLaunchKernelGGL((cols_tiles_kernel<Op, DT, kColK, kColSplitW, TR, true, NT>), grid,
                                tile_block, 0, s, a, g, blocks);
         else
-            hipLaunchKernelGGL((cols_tiles_kernel<Op, DT, kColK, kColSplitW, TR, false>), grid,
+            hipLaunchKernelGGL((cols_tiles_kernel<Op, DT, kColK, kColSplitW, TR, false, NT>), grid,
                                tile_block, 0, s, a, g, blocks);
     } else if (col_tiles(a.T) >= kColPipeChunks) {
-        hipLaunchKernelGGL((cols_rows_kernel<Op, DT, kColK, kColW, TR, true>), dim3(unsigned(blocks)),
+        hipLaunchKernelGGL((cols_rows_kernel<Op, DT, kColK, kColW, TR, true, NT>), dim3(unsigned(blocks)),
                            block, 0, s, a, g);
     } else {
-        hipLaunchKernelGGL((cols_rows_kernel<Op, DT, kColK, kColW, TR, false>), dim3(unsigned(blocks)),
+        hipLaunchKernelGGL((cols_rows_kernel<Op, DT, kColK, kColW, TR, false, NT>), dim3(unsigned(blocks)),
                            block, 0, s, a, g);
     }
+}
+
+// Plain-store kernels exist only for the eligibility-trace policy, the one that vector traces
+// (whose rows may hold fewer than 32 features) run on.
+template <class Op>
+constexpr bool kPlainStores = std::is_same<Op, ForwardOp<true, false>>::value;
+
+template <class Op, typename DT, bool TR>
+void narrow_launch(const Args& a, const ColGeom& g, hipStream_t s) {
+    if constexpr (kPlainStores<Op>) {
+        if (!g.nt_store) return narrow_launch_nt<Op, DT, TR, false>(a, g, s);
+    }
+    narrow_launch_nt<Op, DT, TR, true>(a, g, s);
+}
+
+template <class Op, typename DT, bool TR>
+void col_launch(const Args& a, const ColGeom& g, bool split, int64_t blocks, hipStream_t s) {
+    if constexpr (kPlainStores<Op>) {
+        if (!g.nt_store) return col_launch_nt<Op, DT, TR, false>(a, g, split, blocks, s);
+    }
+    col_launch_nt<Op, DT, TR, true>(a, g, split, blocks, s);
 }
 
 template <class Op>
@@ -186,7 +208,7 @@ inline rlcs_status check_strided(int64_t N, int64_t T, int64_t sn, int64_t st, r
         if (p && !aligned(p, es)) return RLCS_ERR_INVALID_ARG;
     for (const void* p : outs)
         if (p && !aligned(p, 4)) return RLCS_ERR_INVALID_ARG;
-    g = ColGeom{N, 1, st, sn, 0, 0, 1};
+    g = ColGeom{N, 1, st, sn, 0, 0, 1, 1};
     dense = st == 1 && sn == T;
     return RLCS_OK;
 }

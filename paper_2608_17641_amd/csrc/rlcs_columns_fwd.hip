@@ -69,8 +69,9 @@ rlcs_status rlcs_elig_trace_vec(const void* x, const uint8_t* term, const uint8_
     a.in[0] = x;
     a.term = term; a.trunc = trunc;
     a.out0 = z;
-    // column n*F + f: feature f of row n; flags one per step of a row
-    const ColGeom g{N * F, F, F, T * F, 1, T, 0};
+    // column n*F + f: feature f of row n; flags one per step of a row; non-temporal stores
+    // when a step's F outputs fill whole 128-byte lines
+    const ColGeom g{N * F, F, F, T * F, 1, T, 0, F % 32 == 0 ? 1 : 0};
     return col_dispatch<ForwardOp<true, false>>(a, g, dtype, trunc != nullptr, ws, ws_bytes, stream);
 }
 
