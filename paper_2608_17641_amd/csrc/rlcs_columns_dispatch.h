@@ -34,7 +34,9 @@ inline size_t col_ws_need(int64_t J, int64_t T) {
 }
 
 // Narrow column groups (whole columns, no workspace) when the columns fit in one 16-wave chunk
-// (256 steps) and the groups give one or two workgroups per CU. Longer columns walk chunk
+// (256 steps) and the groups give one or two workgroups per CU. Columns of at most 64 (128)
+// steps take 4-wave (8-wave) workgroups: 16 waves would leave half or more of them idle
+// (128 x 8192: 8.0 us with 16 waves, 6.6 with 8). Longer columns walk chunk
 // after chunk, one workgroup per CU, and the split tiles are faster there; with more groups
 // the 1024-thread workgroups queue behind each other. C harness, cold, time-major GAE, narrow
 // against split: 256 x 4096 6.84 us against 8.23; 128 x 8192 8.04 against 8.06; 256 x 16384
@@ -60,6 +62,11 @@ void narrow_launch_nt(const Args& a, const ColGeom& g, hipStream_t s) {
     const dim3 grid(unsigned(narrow_groups<DT>(g.J)));
     if (a.T <= int64_t(G) * 4 * K) {  // one 4-wave chunk
         hipLaunchKernelGGL((cols_narrow_kernel<Op, DT, K, 4, TR, false, NT>), grid, dim3(4 * kWave), 0,
+                           s, a, g, int64_t(grid.x));
+        return;
+    }
+    if (a.T <= int64_t(G) * 8 * K) {  // one 8-wave chunk
+        hipLaunchKernelGGL((cols_narrow_kernel<Op, DT, K, 8, TR, false, NT>), grid, dim3(8 * kWave), 0,
                            s, a, g, int64_t(grid.x));
         return;
     }
