@@ -20,17 +20,20 @@
 //   4. compose the maps of the waves on the carry-source side (LDS);
 //   5. take the value entering the chunk (previous chunk of the same workgroup, or the
 //      published maps of other workgroups' tiles) and finish the K steps; store.
-// cols_rows_kernel walks all of T in chunks (carry through LDS); cols_tiles_kernel gives each
-// tile (kColSplitW waves, twice a walk's chunk) its own workgroup and carries between them with
-// the split-row kernel's workspace protocol, per column: a tile publishes its 64 composed maps
-// and composes the maps of the tiles on its carry-source side, nearest first, until it meets
-// beta = 0 (an episode or row edge). Tiles only ever wait for tiles of their own column block,
-// so each block has its own draw slot: its tickets order the block's tiles from the carry
-// source, and no counter is touched by every workgroup of the grid.
+// cols_rows_kernel walks all of T in chunks (carry through LDS); cols_narrow_kernel does the
+// same for narrow groups of 16 or 32 columns, whose lane groups also split time (short columns,
+// a few thousand of them); cols_tiles_kernel gives each tile (kColSplitW waves, twice a walk's
+// chunk) its own workgroup and carries between them with the split-row kernel's workspace
+// protocol, per column: a tile publishes its 64 composed maps and composes the maps of the
+// tiles on its carry-source side, nearest first, until it meets beta = 0 (an episode or row
+// edge), over block aggregates when a look-back can be long. Tiles only ever wait for tiles of
+// their own column block, so each block has its own draw slot: its tickets order the block's
+// tiles from the carry source, and no counter is touched by every workgroup of the grid.
 //
 // Workspace of cols_tiles_kernel: the split layout of rlcs_kernels.h (zero-filled once), with
-// one draw slot per 64-column block (at most kWsSlots blocks), records at index p * J + j for
-// tile p of column j, and even tags (tag0 = 2*gen + 2, tag1 = tag0 + J * kTagMix).
+// one draw slot per 64-column block (at most kWsSlots blocks), records at index (offset of the
+// level + block) * J + j for column j (level 0: tile of ticket t at t * J + j), and even tags
+// (tag0 = 2*gen + 2, tag1 = tag0 + J * kTagMix).
 #pragma once
 
 #include "rlcs_kernels.h"

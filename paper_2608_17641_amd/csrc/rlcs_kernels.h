@@ -40,14 +40,15 @@ namespace rlcs {
 //   kWsSlots draw slots of 64 bytes, one per row (row tiles) or per 64-column block (column
 //   tiles), each holding one 64-bit draw word: generation << 32 | tickets drawn in this call;
 //   from kWsRecordsOffset, the records: two 64-bit words per tile, (tag0 << 32 | bits(a)) and
-//   (tag1 << 32 | bits(b)), at index p * n + i for tile p of row (column) i of the call's n.
+//   (tag1 << 32 | bits(b)), at index x * n + i for row (column) i of the call's n, with x the
+//   tile (rows) or the tile or block aggregate (columns, rlcs_columns.h).
 // A workgroup draws its ticket and its slot's generation with one relaxed atomic add; the last
 // drawer of a slot stores (gen + 1, 0), so the next call on the same stream finds the slot
 // ready with a new generation, and no workgroup counts anything at its end. A record is valid
 // for the current call when tag0 = 2*gen + 1 (row tiles; 2*gen + 2 for column tiles) and
 // tag1 = tag0 + n * kTagMix. A stale record can never pass for a current one: with the same n
-// its index fixes its tile and row (column), hence its slot, whose generation has moved on
-// since; under another n its tag1 differs; row and column tags differ in parity.
+// its index fixes its row (column), i = index mod n, hence its slot, whose generation has moved
+// on since; under another n its tag1 differs; row and column tags differ in parity.
 struct WsHeader {
     uint64_t reserved;
     uint32_t error;  // set to 1 if a call found the workspace in an inconsistent state
