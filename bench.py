@@ -142,7 +142,7 @@ def cpu_baseline(ro, seconds):
 
 
 COPY_BYTES = 64 << 20
-KERNEL_TAG = "rows_kernel<rlcs::GaeOp, float, 4, 4, true, true, false>"
+KERNEL_TAG = "rows_kernel<rlcs::GaeOp, float, 4, 1, true, true, false>"
 COUNTERS_FILE = os.path.join(ROOT, "profiles", "gae_4096x256_f32_counters.md")
 
 

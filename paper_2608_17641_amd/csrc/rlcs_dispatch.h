@@ -21,6 +21,14 @@ namespace host {
 // longer rows (one row, or a 16*64*K-step tile of one, per workgroup).
 constexpr int kSmallWaves = 4;
 constexpr int kLargeWaves = 16;
+// Rows of 32*K to 64*K steps (at most two rows per wave, whole rows per wave) run one-wave
+// workgroups for the policies where that measured faster (C harness, cold: 4096 x 256 fp32 GAE
+// 5.76 -> 5.68 us, eligibility traces 3.45 -> 3.38 us, bf16 GAE 16384 x 512 25.6 -> 25.1 us);
+// V-Trace, Retrace and TD(lambda) ran 2-7 % slower so and keep four-wave workgroups.
+template <class Op> struct OneWaveRows : std::false_type {};
+template <> struct OneWaveRows<GaeOp> : std::true_type {};
+template <bool D, bool S> struct OneWaveRows<ForwardOp<D, S>> : std::true_type {};
+
 // Staged policies (full-form Retrace) use 4 waves, or 1 when the action axis is too long for
 // a 4-wave chunk's slices to fit the LDS budget.
 constexpr int kStagedWaves = 1;
@@ -114,6 +122,12 @@ rlcs_status launch(const Args& a, const Plan& p, hipStream_t stream) {
         if (p.waves == kStagedWaves) launch_w<Op, DT, VEC, TR, kStagedWaves>(a, p, stream);
         else launch_w<Op, DT, VEC, TR, kSmallWaves>(a, p, stream);
     } else {
+        if constexpr (OneWaveRows<Op>::value) {
+            if (p.waves == 1) {
+                launch_w<Op, DT, VEC, TR, 1>(a, p, stream);
+                return hipGetLastError() == hipSuccess ? RLCS_OK : RLCS_ERR_LAUNCH;
+            }
+        }
         if (p.waves == kSmallWaves) launch_w<Op, DT, VEC, TR, kSmallWaves>(a, p, stream);
         else launch_w<Op, DT, VEC, TR, kLargeWaves>(a, p, stream);
     }
@@ -173,7 +187,10 @@ rlcs_status dispatch_dt(Args& a, bool has_trunc, void* ws, size_t ws_bytes, hipS
             p.split = ws_ok && slots_ok && T % K == 0 && T > E_large && N < kSplitBelowRows;
         }
         if (p.split) p.waves = small_tiles ? kSmallWaves : kLargeWaves;
-        else p.waves = (T <= E_small) ? kSmallWaves : kLargeWaves;
+        else if (T > E_small) p.waves = kLargeWaves;
+        else if (OneWaveRows<Op>::value && T % K == 0 && (int64_t(kWave) * K) % T == 0 && T >= 32 * K)
+            p.waves = 1;  // whole rows per wave, every chunk full
+        else p.waves = kSmallWaves;
         p.lds_bytes = 0;
     }
     if (p.split) {
