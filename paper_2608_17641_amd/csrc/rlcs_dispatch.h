@@ -29,10 +29,13 @@ template <class Op> struct OneWaveRows : std::false_type {};
 template <> struct OneWaveRows<GaeOp> : std::true_type {};
 template <bool D, bool S> struct OneWaveRows<ForwardOp<D, S>> : std::true_type {};
 
-// Staged policies (full-form Retrace) use 4 waves, or 1 when the action axis is too long for
-// a 4-wave chunk's slices to fit the LDS budget.
+// Staged policies (full-form Retrace) use 4 waves when a 4-wave chunk's slices fit in 64 KB of
+// LDS, else 2 waves when two 2-wave workgroups fit in a CU's 160 KB (80 KB each; 4096 x 256 x 18
+// fp32 49.6 -> 48.5 us against one wave), else 1 wave.
 constexpr int kStagedWaves = 1;
+constexpr int kStagedMidWaves = 2;
 constexpr int64_t kStagedLdsBudget = 64 * 1024;
+constexpr int64_t kStagedMidLdsBudget = 80 * 1024;
 
 // Steps per lane: one 16-byte vector of each input.
 template <typename DT> struct Width;
@@ -120,6 +123,7 @@ rlcs_status launch(const Args& a, const Plan& p, hipStream_t stream) {
     }
     if constexpr (Op::kStaged > 0) {
         if (p.waves == kStagedWaves) launch_w<Op, DT, VEC, TR, kStagedWaves>(a, p, stream);
+        else if (p.waves == kStagedMidWaves) launch_w<Op, DT, VEC, TR, kStagedMidWaves>(a, p, stream);
         else launch_w<Op, DT, VEC, TR, kSmallWaves>(a, p, stream);
     } else {
         if constexpr (OneWaveRows<Op>::value) {
@@ -174,6 +178,7 @@ rlcs_status dispatch_dt(Args& a, bool has_trunc, void* ws, size_t ws_bytes, hipS
         // Staged policies keep whole rows in one workgroup (chunk loop for long rows).
         p.split = false;
         if (staged_lds_bytes<Op, DT>(kSmallWaves, a.A) <= kStagedLdsBudget) p.waves = kSmallWaves;
+        else if (staged_lds_bytes<Op, DT>(kStagedMidWaves, a.A) <= kStagedMidLdsBudget) p.waves = kStagedMidWaves;
         else if (staged_lds_bytes<Op, DT>(kStagedWaves, a.A) <= kStagedLdsBudget) p.waves = kStagedWaves;
         else return RLCS_ERR_INVALID_ARG;
         p.lds_bytes = size_t(staged_lds_bytes<Op, DT>(p.waves, a.A));

@@ -20,7 +20,11 @@ template <typename DT, bool VEC, bool TR, bool HM, bool STATS>
 void launch_masked(const MaskedArgs& ma, int waves, int64_t groups, int64_t rows_per_wg,
                    int wave_local, hipStream_t s) {
     constexpr int K = Width<DT>::K;
-    if (waves == kSmallWaves)
+    if (waves == 1)
+        hipLaunchKernelGGL((masked_gae_kernel<DT, K, 1, VEC, TR, HM, STATS>),
+                           dim3(unsigned(groups)), dim3(kWave), 0, s, ma,
+                           rows_per_wg, wave_local);
+    else if (waves == kSmallWaves)
         hipLaunchKernelGGL((masked_gae_kernel<DT, K, kSmallWaves, VEC, TR, HM, STATS>),
                            dim3(unsigned(groups)), dim3(kSmallWaves * kWave), 0, s, ma,
                            rows_per_wg, wave_local);
@@ -36,7 +40,11 @@ rlcs_status run_masked(MaskedArgs& ma, bool normalize, float eps, void* ws, hipS
     const Args& a = ma.a;
     const int64_t N = a.N, T = a.T;
     constexpr int64_t E_small = int64_t(kSmallWaves) * kWave * K;
-    const int waves = (T <= E_small) ? kSmallWaves : kLargeWaves;
+    // Rows of 32*K to 64*K steps without whitening: one-wave workgroups, as for GAE (4096 x 256
+    // multi-turn 5.79 -> 5.54 us). With whitening they would quadruple the partials that every
+    // normalize workgroup adds up (12.4 -> 13.6 us), so those calls keep four waves.
+    const bool one_wave = !normalize && T % K == 0 && (int64_t(kWave) * K) % T == 0 && T >= 32 * K;
+    const int waves = (T <= E_small) ? (one_wave ? 1 : kSmallWaves) : kLargeWaves;
     const int64_t E = int64_t(waves) * kWave * K;
     const int64_t slack = (T % K == 0) ? 0 : K - 1;
     const int64_t rows_per_wg = (T <= E - slack) ? (E - slack) / T : 1;
