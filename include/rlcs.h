@@ -241,8 +241,10 @@ size_t rlcs_workspace_size_masked(int64_t N, int64_t T);
  * Workspace: at least rlcs_workspace_size_columns(N, T) bytes, zero-filled once, lets few
  * environments (N below about 64K) be split along T over several workgroups; without it each
  * group of 64 environments is scanned by one workgroup (the dense layout takes
- * rlcs_workspace_size(N, T) instead). Calls of at most 256 steps over 4096 to 8192 float32
- * (8192 to 16384 bfloat16) environments use none: each workgroup scans 16 (32) whole columns.
+ * rlcs_workspace_size(N, T) instead); calls that split into fewer than 256 tiles of 64
+ * columns by 64 steps split groups of 16 float32 (32 bfloat16) columns instead. Calls of at most 256 steps over 4096 to 8192
+ * float32 (8192 to 16384 bfloat16) environments use none: each workgroup scans 16 (32) whole
+ * columns.
  * Every other convention is the row-major one.                                             */
 rlcs_status rlcs_gae_strided(const void* r, const void* v, const uint8_t* term,
                              const uint8_t* trunc, const void* bv, const void* boot, float* adv,
@@ -312,7 +314,9 @@ int rlcs_version(void);
  * 1 = whole rows per workgroup, 2 = rows split across workgroups (needs the workspace; calls
  * of more than 1024 rows, or columns in more than 1024 blocks of 64, still run whole),
  * 3 = column scans in narrow groups (16 float32 or 32 bfloat16 columns per workgroup, whole
- * columns; row-major calls as with 0).
+ * columns; row-major calls as with 0), 4 = column scans in narrow groups split across
+ * workgroups along T (needs the workspace; at most 1024 groups and more than 64 steps, else
+ * as with 0; row-major calls as with 0).
  * Not thread-safe with concurrent calls. Returns RLCS_ERR_INVALID_ARG for other values. */
 rlcs_status rlcs_set_variant_override(int variant);
 

@@ -563,6 +563,11 @@ __device__ void cols_publish_levels(uint64_t* rec, int64_t t, int64_t P, int64_t
     }
 }
 
+// The n of a column call's tag1: the column count and which split kernel cut the columns into
+// blocks (0: 64-column blocks; 1, 2: narrow groups of 16 float32 or 32 bfloat16 columns), since a
+// column's draw slot depends on both. Distinct for every (J, kind) with J < 2^30.
+__device__ __forceinline__ uint32_t col_tag_n(int64_t J, int kind) { return uint32_t(J) * 4u + uint32_t(kind); }
+
 // One chunk per workgroup. Workgroup g serves column block g mod num_blocks; its ticket among
 // that block's P workgroups orders the block's tiles from the carry source, so a tile only waits
 // for tiles of its block that drew earlier tickets. LIFT: publish and read block aggregates.
@@ -590,7 +595,7 @@ __global__ void __launch_bounds__(W * kWave) cols_tiles_kernel(Args a, ColGeom g
     }
     __syncthreads();
     const uint32_t tag0 = s_tag;
-    const uint32_t tag1 = tag0 + uint32_t(g.J) * kTagMix;
+    const uint32_t tag1 = tag0 + col_tag_n(g.J, 0) * kTagMix;
     const int64_t ticket = s_ticket;
     if (ticket >= P) {
         // Only possible if the workspace was not zero-filled before first use.
@@ -630,6 +635,104 @@ __global__ void __launch_bounds__(W * kWave) cols_tiles_kernel(Args a, ColGeom g
         s_carry[lane] = (need && cl.active) ? cols_gather<LIFT>(rec, ticket, P, g.J, cl.j, tag0, tag1, hdr) : 0.f;
     __syncthreads();
     c.template finish<NT>(a, a.p, cl.base, g.st, apply(win, s_carry[lane]));
+}
+
+// Split tiles over narrow column groups (16 float32 or 32 bfloat16 columns per block, the lane
+// layout of cols_narrow_kernel): four (two) times the workgroups of 64-column tiles for calls of
+// few, long columns, with the same 64-step tiles, draw slots, records and look-back (per block
+// of C columns). Grid: num_blocks * P workgroups.
+template <class Op, typename DT, int K, int W, bool TR, bool LIFT, bool NT = true>
+__global__ void __launch_bounds__(W * kWave) cols_narrow_tiles_kernel(Args a, ColGeom g,
+                                                                      int64_t num_blocks) {
+    constexpr bool kBack = Op::kBackward;
+    constexpr int C = narrow_cols<DT>();
+    constexpr int G = kWave / C;
+    constexpr int64_t L = int64_t(G) * W * K;
+    static_assert(W >= 2, "wave 1 publishes the block aggregates while wave 0 looks back");
+    __shared__ float s_a[W][C], s_b[W][C];
+    __shared__ float s_carry[C];
+    __shared__ uint32_t s_ticket, s_tag;
+    WsHeader* hdr = reinterpret_cast<WsHeader*>(a.ws);
+    uint64_t* rec = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(a.ws) + kWsRecordsOffset);
+    const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+    const int col = lane % C, grp = lane / C;
+    const int64_t T = a.T;
+    const int64_t P = (T + L - 1) / L;
+    const int64_t block = int64_t(blockIdx.x) % num_blocks;
+
+    if (threadIdx.x == 0) {
+        uint32_t gen;
+        s_ticket = draw_ticket(draw_word(a.ws, block), P, gen);
+        s_tag = 2u * gen + 2u;
+    }
+    __syncthreads();
+    const uint32_t tag0 = s_tag;
+    const uint32_t tag1 = tag0 + col_tag_n(g.J, sizeof(DT) == 4 ? 1 : 2) * kTagMix;
+    const int64_t ticket = s_ticket;
+    if (ticket >= P) {
+        // Only possible if the workspace was not zero-filled before first use.
+        if (threadIdx.x == 0) st_relaxed(&hdr->error, 1u);
+        return;
+    }
+    const int64_t p = kBack ? P - 1 - ticket : ticket;
+    ColLane cl;
+    cl.j = block * C + col;
+    cl.active = cl.j < g.J;
+    {
+        const int64_t jj = cl.active ? cl.j : 0;
+        const int64_t b = jj / g.C, c = jj - b * g.C;
+        cl.base = b * g.bstride + c;
+        cl.fbase = g.fcol ? cl.base : b * g.fbstride;
+        cl.fstep = g.fcol ? g.st : g.fst;
+    }
+    const int span = wave * G + grp;  // the lane's K steps within the tile, in time order
+
+    ColChunk<Op, DT, K, TR> c;
+    c.load(a, cl.active, cl.j, cl.base, g.st, cl.fbase, cl.fstep, p * L + int64_t(span) * K);
+    const Pair m = c.local(a.p);
+    // lane groups of the wave (shuffles), then the waves (LDS), as in cols_narrow_kernel
+    Pair incl = m;
+#pragma unroll
+    for (int d = 1; d < G; d <<= 1) {
+        const int src = kBack ? lane + d * C : lane - d * C;
+        const Pair o{__shfl(incl.a, src), __shfl(incl.b, src)};
+        if (kBack ? (grp + d < G) : (grp >= d)) incl = compose(incl, o);
+    }
+    const int nsrc = kBack ? lane + C : lane - C;
+    const Pair nxt{__shfl(incl.a, nsrc), __shfl(incl.b, nsrc)};
+    const Pair grp_in = (kBack ? (grp + 1 < G) : (grp > 0)) ? nxt : identity_pair();
+    if (grp == (kBack ? 0 : G - 1)) {
+        s_a[wave][col] = incl.a;
+        s_b[wave][col] = incl.b;
+    }
+    __syncthreads();
+    Pair win = identity_pair();
+    if (kBack) {
+        for (int w = W - 1; w > wave; --w) win = compose(Pair{s_a[w][col], s_b[w][col]}, win);
+    } else {
+        for (int w = 0; w < wave; ++w) win = compose(Pair{s_a[w][col], s_b[w][col]}, win);
+    }
+    const bool publish = ticket < P - 1;
+    const bool need = ticket > 0;
+    if (grp == 0 && (wave == 0 || (wave == 1 && LIFT)) && publish && cl.active) {
+        // the whole tile's map of this column
+        Pair tm = identity_pair();
+        if (kBack) {
+            for (int w = W - 1; w >= 0; --w) tm = compose(Pair{s_a[w][col], s_b[w][col]}, tm);
+        } else {
+            for (int w = 0; w < W; ++w) tm = compose(Pair{s_a[w][col], s_b[w][col]}, tm);
+        }
+        if (wave == 0) {
+            st_relaxed(rec + 2 * (ticket * g.J + cl.j), uint64_t(tag0) << 32 | __float_as_uint(tm.a));
+            st_relaxed(rec + 2 * (ticket * g.J + cl.j) + 1, uint64_t(tag1) << 32 | __float_as_uint(tm.b));
+        } else {
+            cols_publish_levels(rec, ticket, P, g.J, cl.j, tm, tag0, tag1, hdr);
+        }
+    }
+    if (wave == 0 && grp == 0)
+        s_carry[col] = (need && cl.active) ? cols_gather<LIFT>(rec, ticket, P, g.J, cl.j, tag0, tag1, hdr) : 0.f;
+    __syncthreads();
+    c.template finish<NT>(a, a.p, cl.base, g.st, apply(grp_in, apply(win, s_carry[col])));
 }
 
 }  // namespace rlcs

@@ -43,6 +43,11 @@ inline size_t col_ws_need(int64_t J, int64_t T) {
 // 19.6 against 17.7; 512 x 4096 15.0 against 11.5; 2048 x 4096 55.4 against 41.7.
 constexpr int64_t kNarrowMinGroups = 256;
 constexpr int64_t kNarrowMaxGroups = 512;
+// Split calls whose 64-column tiles give fewer workgroups than this (one per CU) split narrow
+// groups instead, with four (two) times the workgroups: T x N = 4096 x 64 float32 takes 6.2 us
+// instead of 7.4, 2048 x 128 6.4 instead of 7.3; at 256 workgroups and more (16384 x 64,
+// 1024 x 1024, 4096 x 256) the 64-column tiles are 15-25% faster.
+constexpr int64_t kNarrowSplitBelowWgs = 256;
 // Narrow walks of at least this many chunks overlap each chunk's loads with the scan before.
 constexpr int64_t kNarrowPipeChunks = 4;
 
@@ -117,6 +122,25 @@ void col_launch_nt(const Args& a, const ColGeom& g, bool split, int64_t blocks, 
     }
 }
 
+// Split tiles over narrow column groups: the 64-step tiles of cols_tiles_kernel, a block being
+// one narrow group (4 waves x 4 lane groups x 4 float32 steps, or 4 x 2 x 8 bfloat16 steps).
+template <class Op, typename DT, bool TR, bool NT>
+void narrow_split_launch_nt(const Args& a, const ColGeom& g, int64_t nblocks, hipStream_t s) {
+    constexpr int C = narrow_cols<DT>();
+    constexpr int K = C / 4;
+    constexpr int G = kWave / C;
+    constexpr int W = kColSplitL / (G * K);
+    static_assert(G * W * K == kColSplitL, "narrow split tiles are as long as the 64-column ones");
+    const int64_t P = col_split_tiles(a.T);
+    const dim3 grid(unsigned(nblocks * P)), block(W * kWave);
+    if (col_lift(a.p, P))
+        hipLaunchKernelGGL((cols_narrow_tiles_kernel<Op, DT, K, W, TR, true, NT>), grid, block, 0, s,
+                           a, g, nblocks);
+    else
+        hipLaunchKernelGGL((cols_narrow_tiles_kernel<Op, DT, K, W, TR, false, NT>), grid, block, 0, s,
+                           a, g, nblocks);
+}
+
 // Plain-store kernels exist only for the eligibility-trace policy, the one that vector traces
 // (whose rows may hold fewer than 32 features) run on.
 template <class Op>
@@ -128,6 +152,14 @@ void narrow_launch(const Args& a, const ColGeom& g, hipStream_t s) {
         if (!g.nt_store) return narrow_launch_nt<Op, DT, TR, false>(a, g, s);
     }
     narrow_launch_nt<Op, DT, TR, true>(a, g, s);
+}
+
+template <class Op, typename DT, bool TR>
+void narrow_split_launch(const Args& a, const ColGeom& g, int64_t nblocks, hipStream_t s) {
+    if constexpr (kPlainStores<Op>) {
+        if (!g.nt_store) return narrow_split_launch_nt<Op, DT, TR, false>(a, g, nblocks, s);
+    }
+    narrow_split_launch_nt<Op, DT, TR, true>(a, g, nblocks, s);
 }
 
 template <class Op, typename DT, bool TR>
@@ -173,14 +205,31 @@ rlcs_status col_dispatch(Args& a, const ColGeom& g, rlcs_dtype dtype, bool has_t
         split = P > 1 && ws_ok && blocks < kColSerialBlocks;
     }
     if (split && col_split_tiles(a.T) == 1) split = false;  // one tile: a whole-column walk
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    const bool tr = Op::kFlags && has_trunc;
+    // Fewer split tiles than CUs: split the narrow groups instead. Forced by variant 4 whenever
+    // the workspace allows.
+    const bool nsplit_ok = ws_ok && ngroups <= kWsSlots && col_split_tiles(a.T) > 1;
+    if (forced == 4 && !ws_ok) return RLCS_ERR_WORKSPACE;
+    if (nsplit_ok && (forced == 4 ||
+                      (forced == 0 && split && blocks * col_split_tiles(a.T) < kNarrowSplitBelowWgs))) {
+        if (ngroups * col_split_tiles(a.T) > INT32_MAX) return RLCS_ERR_INVALID_ARG;
+        a.ws = ws;
+        if (dtype == RLCS_BF16) {
+            if (tr) narrow_split_launch<Op, bf16_t, true>(a, g, ngroups, s);
+            else narrow_split_launch<Op, bf16_t, false>(a, g, ngroups, s);
+        } else {
+            if (tr) narrow_split_launch<Op, float, true>(a, g, ngroups, s);
+            else narrow_split_launch<Op, float, false>(a, g, ngroups, s);
+        }
+        return hipGetLastError() == hipSuccess ? RLCS_OK : RLCS_ERR_LAUNCH;
+    }
     if (split) {
         if (blocks * P > INT32_MAX) return RLCS_ERR_INVALID_ARG;
         a.ws = ws;
     } else if (blocks > INT32_MAX) {
         return RLCS_ERR_INVALID_ARG;
     }
-    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    const bool tr = Op::kFlags && has_trunc;
     if (dtype == RLCS_BF16) {
         if (tr) col_launch<Op, bf16_t, true>(a, g, split, blocks, s);
         else col_launch<Op, bf16_t, false>(a, g, split, blocks, s);

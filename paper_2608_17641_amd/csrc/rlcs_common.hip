@@ -35,7 +35,7 @@ const char* rlcs_status_string(rlcs_status status) {
 int rlcs_version(void) { return 100; }
 
 rlcs_status rlcs_set_variant_override(int variant) {
-    if (variant < 0 || variant > 3) return RLCS_ERR_INVALID_ARG;
+    if (variant < 0 || variant > 4) return RLCS_ERR_INVALID_ARG;
     g_variant.store(variant, std::memory_order_relaxed);
     return RLCS_OK;
 }

@@ -146,8 +146,8 @@ def test_retrace_full_validation(lib):
 
 def test_variant_override_range(lib):
     from paper_2608_17641_amd import _native as n
-    assert lib.rlcs_set_variant_override(4) == n.RLCS_ERR_INVALID_ARG
-    assert lib.rlcs_set_variant_override(3) == n.RLCS_OK
+    assert lib.rlcs_set_variant_override(5) == n.RLCS_ERR_INVALID_ARG
+    assert lib.rlcs_set_variant_override(4) == n.RLCS_OK
     assert lib.rlcs_set_variant_override(-1) == n.RLCS_ERR_INVALID_ARG
     assert lib.rlcs_set_variant_override(0) == n.RLCS_OK
 

@@ -1,7 +1,7 @@
 """GPU parity of the column scans through the C ABI: the time-major [T, N] entry points of every
 estimator and the F-vector eligibility traces, against the fp64 oracle on the same seeded
 inputs, under every kernel variant (64-column walks, columns split over workgroups, narrow
-column groups of 16 or 32 columns per workgroup). Bar: max |gpu - oracle| <= tol * (1 + max
+column groups of 16 or 32 columns per workgroup, narrow groups split over workgroups). Bar: max |gpu - oracle| <= tol * (1 + max
 |oracle|) per output, tol = 1e-5 for float32 inputs and 1e-3 for bfloat16 inputs."""
 import contextlib
 
@@ -115,7 +115,7 @@ def device_tm(ro, ld=None):
     return d
 
 
-@pytest.mark.parametrize("v", [0, 1, 2, 3])
+@pytest.mark.parametrize("v", [0, 1, 2, 3, 4])
 @pytest.mark.parametrize("T,N", [(1, 1), (7, 3), (33, 64), (256, 100), (1000, 65), (4097, 5)])
 def test_time_major_every_estimator(T, N, v):
     ro = workloads.make_rollout_time_major(T, N, seed=T * 7 + N, p_term=0.05, p_trunc=0.05)
@@ -129,7 +129,7 @@ def test_time_major_every_estimator(T, N, v):
     assert int(ws[8:12].view(torch.int32).item()) == 0
 
 
-@pytest.mark.parametrize("v", [1, 2, 3])
+@pytest.mark.parametrize("v", [1, 2, 3, 4])
 def test_time_major_bf16_plain_and_strided(v):
     T, N = 300, 130
     ro = workloads.make_rollout_time_major(T, N, seed=3, dtype="bf16", p_term=0.03, p_trunc=0.03)
@@ -166,7 +166,7 @@ def test_time_major_strided_padding_untouched():
                   label="tm strided")
 
 
-@pytest.mark.parametrize("v", [0, 1, 2, 3])
+@pytest.mark.parametrize("v", [0, 1, 2, 3, 4])
 def test_time_major_headline_shape(v):
     """GAE on the 4096-environment x 256-step workload stored time-major, whole."""
     T, N = 256, 4096
@@ -231,12 +231,14 @@ def test_time_major_no_flags_long_lookback():
             assert_parity(out, ref_tm(name, ro, trunc=False), TOL["f32"], label=f"no flags {name}")
 
 
+@pytest.mark.parametrize("v", [0, 4])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_block_aggregates_with_rare_flags(dtype):
+def test_block_aggregates_with_rare_flags(dtype, v):
     """Columns of 256 split tiles with gamma * lambda = 1 (c_bar = inf for V-Trace) and rare
     flags (episodes of about 250 steps): look-backs run past their first tiles into block
     aggregates, some of which hold an episode edge. Against the oracle, and bitwise run to run;
-    vector traces of 128 tiles the same way."""
+    vector traces of 128 tiles the same way. Automatic choice (tiles of 64 columns) and split
+    narrow groups."""
     T, N = 16384, 70
     ro = workloads.make_rollout_time_major(T, N, seed=21, dtype=dtype, p_term=0.002, p_trunc=0.002)
     d = {k: (v.t() if v.dim() == 2 else v) for k, v in device_tm(ro).items()}
@@ -262,9 +264,10 @@ def test_block_aggregates_with_rare_flags(dtype):
                                boundary="ends_at"),)),
     }
     for name, (gpu, ref) in calls.items():
-        first = [o.clone() for o in gpu() if o is not None]
-        again = [o for o in gpu() if o is not None]
-        torch.cuda.synchronize()
+        with variant(v):
+            first = [o.clone() for o in gpu() if o is not None]
+            again = [o for o in gpu() if o is not None]
+            torch.cuda.synchronize()
         for a, b in zip(first, again):
             assert torch.equal(a, b), f"{name}: not bitwise reproducible"
         expect = [r for r in ref() if r is not None]
@@ -275,8 +278,9 @@ def test_block_aggregates_with_rare_flags(dtype):
     vr = workloads.make_vector_trace(2, 8192, 40, seed=22, p_term=0.002, p_trunc=0.002)
     dv = {k: to_device(v, DEV) for k, v in vr.items()}
     wsv = rl.make_workspace_columns(2 * 40, 8192, DEV)
-    z = rl.rlcs_elig_trace_vec(dv["x"], dv["term"], dv["trunc"], gamma=1.0, lam=1.0, ws=wsv)
-    torch.cuda.synchronize()
+    with variant(v):
+        z = rl.rlcs_elig_trace_vec(dv["x"], dv["term"], dv["trunc"], gamma=1.0, lam=1.0, ws=wsv)
+        torch.cuda.synchronize()
     zr = oracle.elig_trace_vec(vr["x"], vr["term"], vr["trunc"], gamma=1.0, lam=1.0)
     assert_parity({"z": z}, {"z": zr}, TOL["f32"], label="block aggregates vector traces")
 
@@ -293,7 +297,7 @@ def run_vec(ro, *, trunc=True, ws=None):
     return z, ref
 
 
-@pytest.mark.parametrize("v", [0, 1, 2, 3])
+@pytest.mark.parametrize("v", [0, 1, 2, 3, 4])
 @pytest.mark.parametrize("N,T,F", [(1, 1, 1), (3, 7, 5), (64, 256, 16), (7, 1000, 33),
                                    (2, 4097, 3), (5, 40, 300), (1, 33, 64)])
 def test_elig_trace_vec_shapes(N, T, F, v):
@@ -360,7 +364,7 @@ def strided_rows(t, ld):
     return buf[:, : t.shape[1]]
 
 
-@pytest.mark.parametrize("v", [0, 1, 2])
+@pytest.mark.parametrize("v", [0, 1, 2, 4])
 @pytest.mark.parametrize("N,T,ld", [(1, 1, 3), (9, 33, 40), (100, 256, 300), (5, 1000, 1001)])
 def test_strided_rows_every_estimator(N, T, ld, v):
     """Row-major rows with a row stride above T (the first T steps of wider rows)."""
@@ -414,3 +418,24 @@ def test_strided_dense_layout_runs_the_row_major_path():
     a2, r2 = rl.rlcs_gae(d["r"], d["v"], d["term"], d["trunc"], d["bv"], d["boot"], gamma=G, lam=L)
     torch.cuda.synchronize()
     assert torch.equal(a1, a2) and torch.equal(r1, r2)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("T,N,ld", [(4096, 64, None), (2048, 128, 136), (65, 16, None), (129, 1, 3),
+                                    (1000, 33, None), (8192, 48, 50)])
+def test_time_major_narrow_split_auto(T, N, ld, dtype):
+    """Few long columns (fewer than 256 tiles of 64 columns by 64 steps): the automatic choice
+    splits narrow groups along T. Against the oracle, and bitwise run to run."""
+    ro = workloads.make_rollout_time_major(T, N, seed=T + 3 * N, dtype=dtype, p_term=0.01,
+                                           p_trunc=0.01)
+    d = device_tm(ro, ld)
+    ws = rl.make_workspace_columns(N, T, DEV)
+    for name in TM_ESTIMATORS:
+        out = run_tm(name, d, ws=ws)
+        again = run_tm(name, d, ws=ws)
+        torch.cuda.synchronize()
+        for k in out:
+            if out[k] is not None:
+                assert torch.equal(out[k], again[k]), f"{name} {k}: not bitwise reproducible"
+        assert_parity(out, ref_tm(name, ro), TOL[dtype], label=f"narrow split {name} T={T} N={N}")
+    assert int(ws[8:12].view(torch.int32).item()) == 0

@@ -43,7 +43,7 @@ def _cases(n=int(os.environ.get("RLCS_RANDOM_CASES", "160")),
                         dtype=("f32", "bf16")[rng.integers(0, 2)], layout=layout, pad=pad,
                         p=float(rng.choice([0.0, 0.001, 0.005, 0.05, 0.3])),
                         trunc=bool(rng.integers(0, 2)), boot=bool(rng.integers(0, 2)),
-                        variant=int(rng.integers(0, 4)), seed=int(rng.integers(0, 2 ** 31))))
+                        variant=int(rng.integers(0, 5)), seed=int(rng.integers(0, 2 ** 31))))
     return out
 
 
