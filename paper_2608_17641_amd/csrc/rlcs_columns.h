@@ -638,9 +638,9 @@ __global__ void __launch_bounds__(W * kWave) cols_tiles_kernel(Args a, ColGeom g
 }
 
 // Split tiles over narrow column groups (16 float32 or 32 bfloat16 columns per block, the lane
-// layout of cols_narrow_kernel): four (two) times the workgroups of 64-column tiles for calls of
-// few, long columns, with the same 64-step tiles, draw slots, records and look-back (per block
-// of C columns). Grid: num_blocks * P workgroups.
+// layout of cols_narrow_kernel): up to four (two) times the workgroups of 64-column tiles for
+// calls of few, long columns, with the draw slots, records and look-back of cols_tiles_kernel
+// (per block of C columns); tiles of G * W * K steps. Grid: num_blocks * P workgroups.
 template <class Op, typename DT, int K, int W, bool TR, bool LIFT, bool NT = true>
 __global__ void __launch_bounds__(W * kWave) cols_narrow_tiles_kernel(Args a, ColGeom g,
                                                                       int64_t num_blocks) {
