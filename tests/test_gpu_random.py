@@ -1,4 +1,4 @@
-"""Seeded random GPU parity sweep: 160 cases drawn from one fixed seed, each one estimator on one
+"""Seeded random GPU parity sweep: 600 cases drawn from one fixed seed, each one estimator on one
 shape, dtype, flag density, layout (row-major, strided rows, time-major) and kernel variant,
 against the fp64 oracle on the same inputs. The cases cover what hand-picked shapes can miss:
 odd sizes, rows that straddle vectors and workgroups, row strides and time-major strides of any
@@ -28,7 +28,7 @@ OUT_KEYS = {"gae": ("adv", "ret"), "vtrace": ("vs", "pg"), "retrace": ("delta", 
             "prefix_ends": ("c",), "prefix_starts": ("c",)}
 
 
-def _cases(n=int(os.environ.get("RLCS_RANDOM_CASES", "160")),
+def _cases(n=int(os.environ.get("RLCS_RANDOM_CASES", "600")),
            seed=int(os.environ.get("RLCS_RANDOM_SEED", "20261202"))):
     rng = np.random.default_rng(seed)
     out = []
