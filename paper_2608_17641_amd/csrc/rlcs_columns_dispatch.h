@@ -20,8 +20,9 @@ inline int64_t col_tiles(int64_t T) { return (T + kColL - 1) / kColL; }
 inline int64_t col_split_tiles(int64_t T) { return (T + kColSplitL - 1) / kColSplitL; }
 
 // Whole-column walks of at least this many chunks overlap each chunk's loads with the scan of
-// the one before (shorter ones gain less than the unconditional continuation reads cost).
-constexpr int64_t kColPipeChunks = 8;
+// the one before (shorter ones gain less than the unconditional continuation reads cost; four
+// chunks gain 1-3%: vector traces 1 x 128 x 2^20 215 -> 208 us, time-major 128 x 32768).
+constexpr int64_t kColPipeChunks = 4;
 
 // Workspace bytes of a split column call: header and block slots, then two records per column
 // per 32-step span (a bound on the split tiles, which are longer; 0 if the size does not fit in
@@ -45,8 +46,10 @@ constexpr int64_t kNarrowMinGroups = 256;
 constexpr int64_t kNarrowMaxGroups = 512;
 // Split calls whose 64-column tiles give fewer workgroups than this (one per CU) split narrow
 // groups instead, with four (two) times the workgroups: T x N = 4096 x 64 float32 takes 6.2 us
-// instead of 7.4, 2048 x 128 6.4 instead of 7.3; at 256 workgroups and more (16384 x 64,
-// 1024 x 1024, 4096 x 256) the 64-column tiles are 15-25% faster.
+// instead of 7.4, 2048 x 128 6.4 instead of 7.3; at 256 workgroups and more (1024 x 1024,
+// 4096 x 256, 8192 x 128, 32768 x 64) the 64-column tiles are 10-25% faster. So do calls of
+// fewer than 64 columns, whose one 64-column block leaves lanes idle: 16384 x 32 7.4 us instead
+// of 10.1.
 constexpr int64_t kNarrowSplitBelowWgs = 256;
 // Narrow walks of at least this many chunks overlap each chunk's loads with the scan before.
 constexpr int64_t kNarrowPipeChunks = 4;
@@ -220,12 +223,13 @@ rlcs_status col_dispatch(Args& a, const ColGeom& g, rlcs_dtype dtype, bool has_t
     if (split && col_split_tiles(a.T) == 1) split = false;  // one tile: a whole-column walk
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     const bool tr = Op::kFlags && has_trunc;
-    // Fewer split tiles than CUs: split the narrow groups instead. Forced by variant 4 whenever
-    // the workspace allows.
+    // Fewer split tiles than CUs, or one partly filled 64-column block: split the narrow groups
+    // instead. Forced by variant 4 whenever the workspace allows.
     const bool nsplit_ok = ws_ok && ngroups <= kWsSlots && col_split_tiles(a.T) > 1;
+    const bool nsplit_auto =
+        split && (blocks * col_split_tiles(a.T) < kNarrowSplitBelowWgs || g.J < kWave);
     if (forced == 4 && !ws_ok) return RLCS_ERR_WORKSPACE;
-    if (nsplit_ok && (forced == 4 ||
-                      (forced == 0 && split && blocks * col_split_tiles(a.T) < kNarrowSplitBelowWgs))) {
+    if (nsplit_ok && (forced == 4 || (forced == 0 && nsplit_auto))) {
         if (ngroups * col_split_tiles(a.T) > INT32_MAX) return RLCS_ERR_INVALID_ARG;
         a.ws = ws;
         if (dtype == RLCS_BF16) {

@@ -422,10 +422,11 @@ def test_strided_dense_layout_runs_the_row_major_path():
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("T,N,ld", [(4096, 64, None), (2048, 128, 136), (65, 16, None), (129, 1, 3),
-                                    (1000, 33, None), (8192, 48, 50)])
+                                    (1000, 33, None), (8192, 48, 50), (20000, 32, None)])
 def test_time_major_narrow_split_auto(T, N, ld, dtype):
-    """Few long columns (fewer than 256 tiles of 64 columns by 64 steps): the automatic choice
-    splits narrow groups along T. Against the oracle, and bitwise run to run."""
+    """Few long columns (fewer than 256 tiles of 64 columns by 64 steps, or fewer than 64
+    columns): the automatic choice splits narrow groups along T (64- and 128-step tiles).
+    Against the oracle, and bitwise run to run."""
     ro = workloads.make_rollout_time_major(T, N, seed=T + 3 * N, dtype=dtype, p_term=0.01,
                                            p_trunc=0.01)
     d = device_tm(ro, ld)
