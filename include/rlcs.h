@@ -241,7 +241,8 @@ size_t rlcs_workspace_size_masked(int64_t N, int64_t T);
  * Workspace: at least rlcs_workspace_size_columns(N, T) bytes, zero-filled once, lets few
  * environments (N below about 64K) be split along T over several workgroups; without it each
  * group of 64 environments is scanned by one workgroup (the dense layout takes
- * rlcs_workspace_size(N, T) instead); calls of fewer than 64 environments, or that split into
+ * rlcs_workspace_size(N, T) instead; Retrace splits below about 16K environments); calls of
+ * fewer than 64 environments, or that split into
  * fewer than 256 tiles of 64 columns by 64 steps, split groups of 16 float32 (32 bfloat16)
  * columns instead. Calls of at most 256 steps over 4096 to 8192
  * float32 (8192 to 16384 bfloat16) environments use none: each workgroup scans 16 (32) whole

@@ -15,6 +15,11 @@ namespace host {
 // below it, columns longer than one chunk are split into one-chunk tiles when a workspace is
 // given. Never more than the workspace's per-block slots.
 constexpr int64_t kColSerialBlocks = kWsSlots;
+// Retrace from a quarter of that: its split tiles are eight waves of about 140 VGPRs, one
+// workgroup per CU, while its whole-column walks run four-wave workgroups, two or more per CU.
+// Time-major float32 T x N = 1024 x 32768 (512 blocks) 263 -> 195 us, 512 x 16384 (256 blocks)
+// 60.7 -> 43.3 us. The other estimators gain or lose a few percent either way there.
+constexpr int64_t kColSerialBlocksRetrace = kWsSlots / 4;
 
 inline int64_t col_tiles(int64_t T) { return (T + kColL - 1) / kColL; }
 inline int64_t col_split_tiles(int64_t T) { return (T + kColSplitL - 1) / kColSplitL; }
@@ -218,7 +223,8 @@ rlcs_status col_dispatch(Args& a, const ColGeom& g, rlcs_dtype dtype, bool has_t
     } else if (forced == 1) {
         split = false;
     } else {
-        split = P > 1 && ws_ok && blocks < kColSerialBlocks;
+        const int64_t serial = std::is_same_v<Op, RetraceOp> ? kColSerialBlocksRetrace : kColSerialBlocks;
+        split = P > 1 && ws_ok && blocks < serial;
     }
     if (split && col_split_tiles(a.T) == 1) split = false;  // one tile: a whole-column walk
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
