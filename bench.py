@@ -14,6 +14,8 @@ Cold HBM: the timed steps rotate over enough independent input/output sets (well
 Prints one JSON line on stdout:
   value      effective bandwidth = algorithmic bytes / (timed time / K), GB/s
   roofline   the same figure against the 8 TB/s HBM peak
+  copy_reference  a streaming kernel moving the same 22 B per step over the same sets, timed
+                the same way (the ceiling at this size), and the empty-launch floor
   cpu_baseline  the fp64 oracle on the host, rows split over the host's cores (the single-thread
                 rate in its `sample`), each timed for about --cpu-seconds
 """
@@ -47,6 +49,17 @@ def algorithmic_bytes(N, T, *, dtype_bytes=4, trunc=True, boot=True, outputs=2):
     return N * T * per + (N * dtype_bytes if boot else 0)
 
 
+def eager_steps(warmup, steps, sets):
+    """Eager calls before the graph is captured: at least `warmup`, and enough that every set the
+    timed steps touch (set i % sets for i < steps) has been written by an eager call."""
+    return max(warmup, min(steps, sets))
+
+
+def replay_check_set(steps, sets):
+    """The set whose advantages the first graph replay is compared with: the last one it writes."""
+    return (steps - 1) % sets
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -55,8 +68,9 @@ def parse():
     ap.add_argument("--sets", type=int, default=32, help="rotated input/output sets (cold HBM)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-context", action="store_true",
-                    help="skip the context measurements (full-call timing, copy reference, warm "
-                         "figure): for kernel-trace runs, which then see only the cold timed path")
+                    help="skip the full-call timing and the warm figure, which launch the GAE kernel "
+                         "outside the cold timed path: for kernel-trace runs (the copy reference, "
+                         "whose probe kernels are told apart by name, still runs)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--extra", action="store_true",
                     help="time every estimator of every workload (table on stderr, no JSON line)")
@@ -76,29 +90,76 @@ def parse():
     return ap.parse_args()
 
 
-def copy_reference(nbytes, sets, steps, dev):
-    """A plain device copy moving the same number of bytes per step as the timed kernel (half
-    read, half written), timed the same way: `steps` copies replayed from a HIP graph over
-    `sets` rotated buffer pairs (cold HBM). The ceiling a streaming kernel of this size meets."""
+def hold_stream(ms=2.0):
+    """Holds the current stream with a spin kernel of about `ms` milliseconds, so that the host
+    has enqueued the timing events and the whole replayed graph behind it before the start event
+    fires: the timed region then holds the K steps' GPU work and not the host's submission of
+    the graph (with K = 20, that submission is a sizeable part of K steps)."""
     import torch
-    n = nbytes // 8  # float32 elements per buffer: n * 4 bytes read and n * 4 written
-    bufs = [(torch.ones(n, device=dev), torch.empty(n, device=dev)) for _ in range(sets)]
-    for i in range(3):
-        bufs[i % sets][1].copy_(bufs[i % sets][0])
-    torch.cuda.synchronize()
+    torch.cuda._sleep(int(ms * 1e-3 * 2.4e9))
+
+
+def probe_lib():
+    """libprobe.so (built beside the library): the streaming reference kernel with GAE's byte
+    split and the empty launch."""
+    import ctypes
+    from paper_2608_17641_amd.build import PROBE_LIB
+    if not os.path.exists(PROBE_LIB):
+        raise RuntimeError(f"{PROBE_LIB} is missing: run __graft_entry__.build()")
+    lib = ctypes.CDLL(PROBE_LIB)
+    P = ctypes.c_void_p
+    lib.probe_stream_gae.argtypes = [P] * 7 + [ctypes.c_int64, ctypes.c_int, P]
+    lib.probe_stream_gae.restype = ctypes.c_int
+    lib.probe_empty.argtypes = [P]
+    lib.probe_empty.restype = ctypes.c_int
+    return lib
+
+
+def probe_stream_call(lib, s, threads):
+    """One streaming pass over set `s` (the GAE call's own buffers: r, v, bv, term, trunc read,
+    adv and ret written)."""
+    import torch
+    st = torch.cuda.current_stream().cuda_stream
+    rc = lib.probe_stream_gae(s["r"].data_ptr(), s["v"].data_ptr(), s["bv"].data_ptr(),
+                              s["term"].data_ptr(), s["trunc"].data_ptr(), s["adv"].data_ptr(),
+                              s["ret"].data_ptr(), s["r"].numel(), threads, st)
+    if rc != 0:
+        raise RuntimeError(f"probe_stream_gae returned {rc}")
+
+
+def _graph_replay_us(fn, steps):
+    """Mean microseconds per call of `steps` calls fn(i) replayed from one graph (the same
+    protocol as the timed GAE steps)."""
+    import torch
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g):
         for i in range(steps):
-            src, dst = bufs[i % sets]
-            dst.copy_(src)
+            fn(i)
     g.replay()
     torch.cuda.synchronize()
     a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    hold_stream()
     a.record(); g.replay(); b.record()
     torch.cuda.synchronize()
-    us = a.elapsed_time(b) * 1e3 / steps
-    del g, bufs
-    return us
+    del g
+    return a.elapsed_time(b) * 1e3 / steps
+
+
+def copy_reference(sets, steps):
+    """The streaming ceiling at this size: probe_stream_gae over the same rotated sets as the
+    GAE steps (22 B per step: the three data inputs and two flag arrays read, both outputs
+    written, densely), in 64- and 256-lane workgroups, timed like the GAE steps; and the
+    empty-launch floor of the same graph replay."""
+    lib = probe_lib()
+    S = len(sets)
+    for i in range(S):
+        probe_stream_call(lib, sets[i], 64)
+    out = {}
+    for threads in (64, 256):
+        out[threads] = _graph_replay_us(lambda i: probe_stream_call(lib, sets[i % S], threads), steps)
+    import torch
+    empty = _graph_replay_us(lambda i: lib.probe_empty(torch.cuda.current_stream().cuda_stream), steps)
+    return out, empty
 
 
 def cpu_baseline(ro, seconds):
@@ -538,6 +599,7 @@ def _graph_time(call, sets, nbytes):
     graph.replay()
     torch.cuda.synchronize()
     a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    hold_stream()
     a.record(); graph.replay(); b.record()
     torch.cuda.synchronize()
     del graph
@@ -805,10 +867,13 @@ def main():
         if err > 1e-5 * (1 + float(np.max(np.abs(ref)))):
             raise SystemExit(f"parity failure before timing: max err {err}")
 
-    for i in range(args.warmup):
+    # Eager warm-up writes every set that the graph will replay into, so that the replay can be
+    # compared with an eager result of the same set.
+    for i in range(eager_steps(args.warmup, args.steps, S)):
         step(i)
     torch.cuda.synchronize()
-    eager_adv = sets[(args.steps - 1) % S]["adv"].clone()
+    check_set = replay_check_set(args.steps, S)
+    eager_adv = sets[check_set]["adv"].clone()
 
     # The timed steps are replayed from a HIP graph so that host-side launch cost (Python,
     # ctypes) does not starve the GPU; each graph node is one rlcs_gae kernel launch.
@@ -818,10 +883,11 @@ def main():
             step(i)
     graph.replay()
     torch.cuda.synchronize()
-    if not torch.equal(sets[(args.steps - 1) % S]["adv"], eager_adv):
+    if not torch.equal(sets[check_set]["adv"], eager_adv):
         raise SystemExit("graph replay differs from the eager launch")
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
+    hold_stream()
     start.record()
     graph.replay()
     end.record()
@@ -852,17 +918,41 @@ def main():
                      "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
                      "traffic": recorded_traffic()},
     }
+    out.update(copy_context(nbytes, per_step_s, sets, args))
     if not args.no_context:
-        out.update(context(step, nbytes, per_step_s, S, args, dev, start, end))
+        out.update(context(step, nbytes, args, start, end))
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(ro, args.cpu_seconds)
     print(json.dumps(out), flush=True)
 
 
-def context(step, nbytes, per_step_s, S, args, dev, start, end):
+def copy_context(nbytes, per_step_s, sets, args):
+    """The streaming ceiling beside the headline (also on stderr): probe_stream_gae over the same
+    rotated sets, and the empty-launch floor. It launches only the probe kernels, so it also runs
+    in kernel-trace runs (--no-context), whose trace then holds the probe's durations."""
+    copies, empty_us = copy_reference(sets, args.steps)
+    copy_us = min(copies.values())
+    for threads, us in copies.items():
+        print(f"copy reference (probe_stream_gae, {threads}-lane workgroups, GAE's 22 B per step, "
+              f"cold): {us:.3f} us = {nbytes / us / 1e3:.1f} GB/s", file=sys.stderr)
+    print(f"the GAE step takes {per_step_s * 1e6 / copy_us:.3f}x the faster copy's time; empty "
+          f"launch {empty_us:.3f} us", file=sys.stderr)
+    return {
+        "copy_reference": {"kernel": "probe_stream_gae (libprobe.so): r, v, bv, term, trunc read "
+                                     "and adv, ret written densely, 22 B per step, non-temporal "
+                                     "16-byte vectors, same rotated sets, graph replay, cold",
+                           "us_64_lanes": round(copies[64], 3), "us_256_lanes": round(copies[256], 3),
+                           "us": round(copy_us, 3), "GB/s": round(nbytes / copy_us / 1e3, 1),
+                           "frac_of_peak": round(nbytes / copy_us / 1e3 / PEAK_HBM_GBS, 4),
+                           "kernel_time_over_copy": round(per_step_s * 1e6 / copy_us, 3),
+                           "empty_launch_us": round(empty_us, 3)},
+    }
+
+
+def context(step, nbytes, args, start, end):
     """Context figures next to the headline (also on stderr): the full-call time of one eager
     call through the Python binding by the paper's protocol (per-call events, median of 50, min
-    over 5 trials), a plain copy of the same bytes, and the warm (cache-resident) step."""
+    over 5 trials), and the warm (cache-resident) step."""
     import torch
     trials = []
     for _ in range(5):
@@ -874,11 +964,8 @@ def context(step, nbytes, per_step_s, S, args, dev, start, end):
             torch.cuda.synchronize()
             ts.append(a.elapsed_time(b))
         trials.append(float(np.median(ts)))
-    print(f"full-call (per-call events, min of 5 medians): {min(trials) * 1e3:.2f} us", file=sys.stderr)
-    copy_us = copy_reference(nbytes, S, args.steps, dev)
-    print(f"copy reference (same bytes, half read, half written, cold): {copy_us:.3f} us = "
-          f"{nbytes / copy_us / 1e3:.1f} GB/s; the kernel takes {per_step_s * 1e6 / copy_us:.3f}x its time",
-          file=sys.stderr)
+    full_us = min(trials) * 1e3
+    print(f"full-call (per-call events, min of 5 medians): {full_us:.2f} us", file=sys.stderr)
     # Warm (context only): every step on set 0, Infinity-Cache resident after the first.
     wgraph = torch.cuda.CUDAGraph()
     with torch.cuda.graph(wgraph):
@@ -886,6 +973,7 @@ def context(step, nbytes, per_step_s, S, args, dev, start, end):
             step(0)
     wgraph.replay()
     torch.cuda.synchronize()
+    hold_stream()
     start.record(); wgraph.replay(); end.record()
     torch.cuda.synchronize()
     warm_us = start.elapsed_time(end) * 1e3 / args.steps
@@ -893,13 +981,10 @@ def context(step, nbytes, per_step_s, S, args, dev, start, end):
     print(f"warm (one set, Infinity-Cache resident): {warm_us:.3f} us = {nbytes / warm_us / 1e3:.1f} GB/s "
           f"effective", file=sys.stderr)
     return {
-        "copy_reference": {"kernel": "torch copy_, algorithmic_bytes/2 read and written, cold",
-                           "us": round(copy_us, 3), "GB/s": round(nbytes / copy_us / 1e3, 1),
-                           "kernel_time_over_copy": round(per_step_s * 1e6 / copy_us, 3)},
+        "full_call_us": round(full_us, 2),
         "warm": {"what": "same steps on one input/output set, Infinity-Cache resident (context only)",
                  "us": round(warm_us, 3), "GB/s": round(nbytes / warm_us / 1e3, 1)},
     }
-
 
 if __name__ == "__main__":
     main()

@@ -45,8 +45,8 @@
  *            leaves it ready for the next one. Calls sharing one `ws` must be ordered on one
  *            stream. With ws == NULL (or ws_bytes too small) the library processes each row
  *            within one workgroup: same results up to rounding, less parallel.
- * Memory     The library allocates nothing and keeps no state between calls apart from the
- *            process-wide variant override below; it is safe to call from several threads.
+ * Memory     The library allocates nothing and keeps no state between calls; it is safe to
+ *            call from several threads.
  * Errors     Every argument is checked on the host before any HIP call; an error returns a
  *            status and enqueues nothing. RLCS_ERR_LAUNCH reports a failed kernel launch.
  */
@@ -312,15 +312,6 @@ const char* rlcs_status_string(rlcs_status status);
 /* Library version as major * 10000 + minor * 100 + patch. */
 int rlcs_version(void);
 
-/* Kernel-variant override, process-wide, for tests and benchmarks: 0 = automatic choice,
- * 1 = whole rows per workgroup, 2 = rows split across workgroups (needs the workspace; calls
- * of more than 1024 rows, or columns in more than 1024 blocks of 64, still run whole),
- * 3 = column scans in narrow groups (16 float32 or 32 bfloat16 columns per workgroup, whole
- * columns; row-major calls as with 0), 4 = column scans in narrow groups split across
- * workgroups along T (needs the workspace; at most 1024 groups and more than 64 steps, else
- * as with 0; row-major calls as with 0).
- * Not thread-safe with concurrent calls. Returns RLCS_ERR_INVALID_ARG for other values. */
-rlcs_status rlcs_set_variant_override(int variant);
 
 #ifdef __cplusplus
 }

@@ -124,7 +124,7 @@ void oracle_gae_masked(const double* r, const double* v, const uint8_t* mask,
     }
 }
 
-/* Vector eligibility traces, Table 1 and Section 3.3.4:
+/* TD(lambda) returns, Table 1 and Section 3.3.4:
  *   G_t = r_t + gamma * [(1 - lambda) V(s_{t+1}) + lambda G_{t+1}] inside an episode,
  *   with the successor value given by Section 3.2; a truncated step takes the continuation
  *   with the full gamma; a terminated step has no successor; the window carry is G_T = B, so

@@ -138,8 +138,9 @@ def rlcs_version() -> int:
     return int(_native.load().rlcs_version())
 
 
-def rlcs_set_variant_override(variant: int) -> None:
-    _call("rlcs_set_variant_override", int(variant))
+def testing_set_variant(variant: int) -> None:
+    """Test hook: force a kernel variant for this thread's later calls (0 = automatic)."""
+    _call("rlcs_testing_set_variant", int(variant))
 
 
 def rlcs_gae(r, v, term=None, trunc=None, bv=None, boot=None, adv=None, ret=None, *,

@@ -64,7 +64,7 @@ PROTOTYPES = {
     "rlcs_workspace_size_masked": [_I64, _I64],
     "rlcs_status_string": [_INT],
     "rlcs_version": [],
-    "rlcs_set_variant_override": [_INT],
+    "rlcs_testing_set_variant": [_INT],
 }
 RESTYPES = {"rlcs_workspace_size": _SZ, "rlcs_workspace_size_columns": _SZ,
             "rlcs_workspace_size_masked": _SZ,

@@ -4,7 +4,9 @@
 
 produces ``paper_2608_17641_amd/librlcs.so`` from the translation units ``csrc/rlcs_*.hip``
 (one per group of entry points, compiled in parallel; kernels in ``csrc/rlcs_*.h``) against
-the public header ``include/rlcs.h``.
+the public header ``include/rlcs.h``, and ``paper_2608_17641_amd/libprobe.so`` from
+``csrc/probe_stream.hip``: reference kernels that bench.py times beside the library (a streaming
+copy with GAE's byte split, an empty launch), not part of the library.
 """
 from __future__ import annotations
 
@@ -21,6 +23,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "librlcs.so")
+PROBE_LIB = os.path.join(PKG, "libprobe.so")
+PROBE_SOURCE = os.path.join(CSRC, "probe_stream.hip")
 SOURCES = sorted(glob.glob(os.path.join(CSRC, "rlcs_*.hip")))
 HEADERS = sorted(glob.glob(os.path.join(CSRC, "rlcs_*.h"))) + [os.path.join(INCLUDE, "rlcs.h")]
 
@@ -67,27 +71,30 @@ def _run(cmd):
 
 
 def build(force: bool = True, verbose: bool = False) -> str:
-    """Compile librlcs.so: always when force, else only if it does not exist yet."""
-    if not force and os.path.exists(LIB):
+    """Compile librlcs.so and libprobe.so: always when force, else only what does not exist
+    yet."""
+    if not force and os.path.exists(LIB) and os.path.exists(PROBE_LIB):
         return LIB
     with tempfile.TemporaryDirectory(prefix="rlcs_build_") as tmpdir:
         objs = [os.path.join(tmpdir, os.path.basename(src) + ".o") for src in SOURCES]
-        jobs = min(len(SOURCES), max(1, min(8, os.cpu_count() or 1)))
+        probe_obj = os.path.join(tmpdir, "probe_stream.o")
+        jobs = min(len(SOURCES) + 1, max(1, min(8, os.cpu_count() or 1)))
         with ThreadPoolExecutor(max_workers=jobs) as pool:
             results = list(pool.map(lambda so: (so[0], _run(compile_command(*so))),
-                                    zip(SOURCES, objs)))
+                                    list(zip(SOURCES, objs)) + [(PROBE_SOURCE, probe_obj)]))
         for src, (rc, err) in results:
             if rc != 0:
                 raise RuntimeError(f"hipcc failed on {src} ({rc}):\n{err}")
             if verbose and err.strip():
                 print(err, file=sys.stderr)
-        tmp = LIB + f".tmp{os.getpid()}"
-        rc, err = _run(link_command(objs, tmp))
-        if rc != 0:
-            if os.path.exists(tmp):
-                os.remove(tmp)
-            raise RuntimeError(f"link failed ({rc}):\n{err}")
-        os.replace(tmp, LIB)
+        for objects, out in ((objs, LIB), ([probe_obj], PROBE_LIB)):
+            tmp = out + f".tmp{os.getpid()}"
+            rc, err = _run(link_command(objects, tmp))
+            if rc != 0:
+                if os.path.exists(tmp):
+                    os.remove(tmp)
+                raise RuntimeError(f"link of {os.path.basename(out)} failed ({rc}):\n{err}")
+            os.replace(tmp, out)
     return LIB
 
 

@@ -597,6 +597,7 @@ __global__ void __launch_bounds__(W * kWave) cols_tiles_kernel(Args a, ColGeom g
     const uint32_t tag0 = s_tag;
     const uint32_t tag1 = tag0 + col_tag_n(g.J, 0) * kTagMix;
     const int64_t ticket = s_ticket;
+    if (wave == 0) advance_idle_slots(a.ws, num_blocks, (tag0 - 2u) / 2u, lane);
     if (ticket >= P) {
         // Only possible if the workspace was not zero-filled before first use.
         if (threadIdx.x == 0) st_relaxed(&hdr->error, 1u);
@@ -668,6 +669,7 @@ __global__ void __launch_bounds__(W * kWave) cols_narrow_tiles_kernel(Args a, Co
     __syncthreads();
     const uint32_t tag0 = s_tag;
     const uint32_t tag1 = tag0 + col_tag_n(g.J, sizeof(DT) == 4 ? 1 : 2) * kTagMix;
+    if (wave == 0) advance_idle_slots(a.ws, num_blocks, (tag0 - 2u) / 2u, lane);
     const int64_t ticket = s_ticket;
     if (ticket >= P) {
         // Only possible if the workspace was not zero-filled before first use.

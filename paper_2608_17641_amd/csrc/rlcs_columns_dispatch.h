@@ -200,7 +200,7 @@ rlcs_status col_dispatch(Args& a, const ColGeom& g, rlcs_dtype dtype, bool has_t
     const size_t need = col_ws_need(g.J, a.T);
     const bool ws_ok = ws && need > 0 && ws_bytes >= need && aligned(ws, 64) &&
                        blocks <= int64_t(UINT32_MAX) / P;
-    const int forced = g_variant.load(std::memory_order_relaxed);
+    const int forced = g_variant;
     const int64_t ngroups = dtype == RLCS_BF16 ? narrow_groups<bf16_t>(g.J) : narrow_groups<float>(g.J);
     if (forced == 3 || (forced == 0 && a.T <= kNarrowChunk && ngroups >= kNarrowMinGroups &&
                         ngroups <= kNarrowMaxGroups)) {

@@ -1,12 +1,14 @@
-// Entry points that launch nothing: workspace size, status strings, version, variant override.
+// Entry points that launch nothing: workspace size, status strings, version, and the test-only
+// variant override.
 #include "rlcs_dispatch.h"
+#include "rlcs_testing.h"
 
 using namespace rlcs;
 using namespace rlcs::host;
 
 namespace rlcs {
 namespace host {
-std::atomic<int> g_variant{0};
+thread_local int g_variant = 0;
 }  // namespace host
 }  // namespace rlcs
 
@@ -34,9 +36,9 @@ const char* rlcs_status_string(rlcs_status status) {
 
 int rlcs_version(void) { return 100; }
 
-rlcs_status rlcs_set_variant_override(int variant) {
+rlcs_status rlcs_testing_set_variant(int variant) {
     if (variant < 0 || variant > 4) return RLCS_ERR_INVALID_ARG;
-    g_variant.store(variant, std::memory_order_relaxed);
+    g_variant = variant;
     return RLCS_OK;
 }
 

@@ -61,8 +61,9 @@ constexpr int64_t kMaxActions = 28;
 // Longest supported row (the kernels keep offsets within a row range in 32 bits).
 constexpr int64_t kMaxT = int64_t(1) << 30;
 
-// Process-wide kernel-variant override (rlcs_set_variant_override); defined in rlcs_common.hip.
-extern std::atomic<int> g_variant;
+// Kernel-variant override of the calling thread (rlcs_testing_set_variant, a test-only entry
+// point); defined in rlcs_common.hip.
+extern thread_local int g_variant;
 
 inline bool aligned(const void* p, size_t a) { return reinterpret_cast<uintptr_t>(p) % a == 0; }
 inline bool unit_interval(float x) { return x >= 0.f && x <= 1.f; }  // false for NaN
@@ -173,7 +174,7 @@ rlcs_status dispatch_dt(Args& a, bool has_trunc, void* ws, size_t ws_bytes, hipS
     const size_t ws_need = slots_ok ? kWsRecordsOffset + size_t(N * p.tiles_per_row) * kWsRecordBytes
                                     : kWsRecordsOffset;
     const bool ws_ok = ws && ws_bytes >= ws_need && aligned(ws, 64);
-    const int forced = g_variant.load(std::memory_order_relaxed);
+    const int forced = g_variant;
     if constexpr (Op::kStaged > 0) {
         // Staged policies keep whole rows in one workgroup (chunk loop for long rows).
         p.split = false;

@@ -44,11 +44,17 @@ namespace rlcs {
 //   tile (rows) or the tile or block aggregate (columns, rlcs_columns.h).
 // A workgroup draws its ticket and its slot's generation with one relaxed atomic add; the last
 // drawer of a slot stores (gen + 1, 0), so the next call on the same stream finds the slot
-// ready with a new generation, and no workgroup counts anything at its end. A record is valid
-// for the current call when tag0 = 2*gen + 1 (row tiles; 2*gen + 2 for column tiles) and
-// tag1 = tag0 + n * kTagMix. A stale record can never pass for a current one: with the same n
-// its index fixes its row (column), i = index mod n, hence its slot, whose generation has moved
-// on since; under another n its tag1 differs; row and column tags differ in parity.
+// ready with a new generation, and no workgroup counts anything at its end. The slots a call
+// does not draw from are moved on to gen + 1 as well (advance_idle_slots), so every slot always
+// holds the same generation: the number of split calls made on the workspace, which names one
+// call of its whole history (modulo 2^30). A record word is valid for the current call when its
+// tag is the call's: tag0 = 2*gen + 1 (row tiles; 2*gen + 2 for column tiles) on the word of
+// a, tag1 = tag0 + n * kTagMix on the word of b. Each word is checked on its own, so each tag
+// must name the call by itself: a reader may load one word before the writer's store and the
+// other after it, and a stale word whose tag matched the current call's would then pair with a
+// current one. With per-slot generations that could happen (a word of another call, of another
+// n, written when its slot stood at the generation the reader's slot stands at now); with the
+// generation shared by all slots, no earlier call wrote a word with either current tag.
 struct WsHeader {
     uint64_t reserved;
     uint32_t error;  // set to 1 if a call found the workspace in an inconsistent state
@@ -84,6 +90,17 @@ __device__ __forceinline__ uint32_t draw_ticket(uint64_t* word, int64_t n_tiles,
 
 __device__ __forceinline__ uint64_t* draw_word(void* ws, int64_t slot) {
     return reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) + sizeof(WsHeader) + slot * 64);
+}
+
+// Moves the slots from `used` on, which no workgroup of this call draws from, to generation
+// gen + 1, the generation the last drawer of each used slot leaves behind: run by every lane of
+// one wave per workgroup, once the workgroup's own draw has returned `gen` (all slots stand at
+// the same generation). The slots are spread over the grid, a few stores per workgroup.
+__device__ __forceinline__ void advance_idle_slots(void* ws, int64_t used, uint32_t gen, int lane) {
+    const uint64_t next = uint64_t((gen + 1u) & kGenMask) << 32;
+    for (int64_t s = used + int64_t(blockIdx.x) * kWave + lane; s < kWsSlots;
+         s += int64_t(gridDim.x) * kWave)
+        st_relaxed(draw_word(ws, s), next);
 }
 
 // Lane l of a wave owns the l-th group of K steps of the wave's span for forward scans and the
@@ -732,6 +749,7 @@ __global__ void __launch_bounds__(W * kWave) tiles_kernel(Args a, int64_t P) {
     const uint32_t tag0 = 2u * s_gen + 1u;
     const uint32_t tag1 = tag0 + uint32_t(N) * kTagMix;
     const int64_t ticket = s_ticket;
+    if (wave == 0) advance_idle_slots(a.ws, N, s_gen, lane);
     if (ticket >= P) {
         // Only possible if the workspace was not zero-filled before first use.
         if (threadIdx.x == 0) st_relaxed(&hdr->error, 1u);

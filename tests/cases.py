@@ -138,5 +138,19 @@ def assert_parity(gpu: dict, ref: dict, tol: float, label=""):
         assert np.all(np.isfinite(g)), f"{label} {k}: non-finite GPU output"
         err, scale = max_err(g, r)
         worst[k] = err / scale
-        assert err <= tol * scale, f"{label} {k}: max err {err:.3e} > {tol:g} * {scale:.3f}"
+        assert err <= tol * scale, (f"{label} {k}: max err {err:.3e} > {tol:g} * {scale:.3f}; "
+                                    + mismatch_report(g, r, tol * scale))
     return worst
+
+
+def mismatch_report(g: np.ndarray, r: np.ndarray, bound: float, show: int = 12) -> str:
+    """Where a failed comparison differs: how many elements exceed the bound, the first ones
+    (index, GPU value, oracle value), and the byte span they cover in a float32 output."""
+    bad = np.argwhere(np.abs(np.asarray(g, np.float64) - r) > bound)
+    if bad.size == 0:
+        return "no element above the bound"
+    flat = np.ravel_multi_index(bad.T, r.shape)
+    first = ", ".join(f"{tuple(int(x) for x in i)}: {float(g[tuple(i)]):.6g} vs {float(r[tuple(i)]):.6g}"
+                      for i in bad[:show])
+    return (f"{len(bad)} of {r.size} elements differ, flat float32 byte offsets "
+            f"{4 * int(flat.min())}..{4 * int(flat.max()) + 3}; first: {first}")

@@ -145,11 +145,12 @@ def test_retrace_full_validation(lib):
 
 
 def test_variant_override_range(lib):
+    """The test-only variant hook (not in the public header) checks its range."""
     from paper_2608_17641_amd import _native as n
-    assert lib.rlcs_set_variant_override(5) == n.RLCS_ERR_INVALID_ARG
-    assert lib.rlcs_set_variant_override(4) == n.RLCS_OK
-    assert lib.rlcs_set_variant_override(-1) == n.RLCS_ERR_INVALID_ARG
-    assert lib.rlcs_set_variant_override(0) == n.RLCS_OK
+    assert lib.rlcs_testing_set_variant(5) == n.RLCS_ERR_INVALID_ARG
+    assert lib.rlcs_testing_set_variant(4) == n.RLCS_OK
+    assert lib.rlcs_testing_set_variant(-1) == n.RLCS_ERR_INVALID_ARG
+    assert lib.rlcs_testing_set_variant(0) == n.RLCS_OK
 
 
 def test_column_workspace_size(lib):

@@ -26,11 +26,11 @@ G, L = 0.99, 0.95
 
 @contextlib.contextmanager
 def variant(v):
-    rl.rlcs_set_variant_override(v)
+    rl.testing_set_variant(v)
     try:
         yield
     finally:
-        rl.rlcs_set_variant_override(0)
+        rl.testing_set_variant(0)
 
 
 def strided(t, ld):

@@ -23,11 +23,11 @@ DEV = torch.device("cuda:0")
 
 @contextlib.contextmanager
 def variant(v):
-    rl.rlcs_set_variant_override(v)
+    rl.testing_set_variant(v)
     try:
         yield
     finally:
-        rl.rlcs_set_variant_override(0)
+        rl.testing_set_variant(0)
 
 
 def check(name, ro, *, trunc=True, boot=True, ws=None, label="", **params):

@@ -95,12 +95,12 @@ def test_random_case(case):
     strided = c["layout"] != "rows"
     ws = (rl.make_workspace_columns(c["N"], c["T"], DEV) if strided
           else rl.make_workspace(c["N"], c["T"], DEV))
-    rl.rlcs_set_variant_override(c["variant"])
+    rl.testing_set_variant(c["variant"])
     try:
         outs = _run(c["name"], d, c["trunc"], c["boot"], ws, strided)
         torch.cuda.synchronize()
     finally:
-        rl.rlcs_set_variant_override(0)
+        rl.testing_set_variant(0)
     ref = oracle_run(c["name"], ro, trunc=c["trunc"], boot=c["boot"], gamma=0.97, lam=0.9,
                      c_bar=0.9 if c["name"] == "vtrace" else 1.0)
     got = {k: o for k, o in zip(OUT_KEYS[c["name"]], outs) if o is not None}
