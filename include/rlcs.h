@@ -225,6 +225,27 @@ rlcs_status rlcs_gae_masked(const void* r, const void* v, const uint8_t* mask,
  * sizes). */
 size_t rlcs_workspace_size_masked(int64_t N, int64_t T);
 
+/* rlcs_gae_masked without a workspace argument, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc). Same
+ * arguments, results and kernels as rlcs_gae_masked; whitening (normalize = 1) uses a
+ * workspace built into the library instead of `ws`: a static device array of 2 MiB per GPU,
+ * held until the process ends, enough for N <= 65536 rows. The call itself allocates nothing
+ * (no hipMalloc, no allocating library routine).
+ *   N > 65536  RLCS_ERR_WORKSPACE, checked first (also with normalize = 0), before any HIP
+ *              call; the other checks are rlcs_gae_masked's.
+ *   The array's device address is looked up on the first call on each device (that device
+ *   current); if the lookup fails the call returns RLCS_ERR_LAUNCH and enqueues nothing.
+ * Every call on one GPU shares that GPU's array and nothing in it needs clearing (each call
+ * writes what it reads back). Calls that can overlap on one GPU (other streams, other
+ * threads, other graph replays running at the same time) race on the array and must not
+ * whiten at once; calls ordered on one stream are safe. The mean and 1/sqrt(var + eps) of the
+ * last call are not returned (use rlcs_gae_masked with a workspace for them). */
+rlcs_status rlcs_gae_masked_noalloc(const void* r, const void* v, const uint8_t* mask,
+                                    const uint8_t* term, const uint8_t* trunc, const void* bv,
+                                    const void* boot, float* adv, float* ret, int64_t N, int64_t T,
+                                    float gamma, float lambda, int normalize, float eps,
+                                    rlcs_dtype dtype, rlcs_stream_t stream);
+
 /* ---------------------------------------------------------------------------------------
  * Strided layouts. The entry points below compute exactly what their row-major namesakes
  * compute, for [N, T] arrays laid out with element (n, t) at n * stride_n + t * stride_t:

@@ -524,3 +524,22 @@ def rlcs_gae_masked(r, v, mask=None, term=None, trunc=None, bv=None, boot=None, 
               _ptr(boot), _ptr(adv), _ptr(ret), N, T, gamma, lam, 1 if normalize else 0, eps,
               _DTYPES[dt], wp, wb, _stream(dev))
     return adv, ret
+
+
+def rlcs_gae_masked_noalloc(r, v, mask=None, term=None, trunc=None, bv=None, boot=None, adv=None,
+                            ret=None, *, gamma: float, lam: float, normalize: bool = False,
+                            eps: float = 1e-8, want_ret: bool = True):
+    """rlcs_gae_masked with the library's built-in whitening workspace (N <= 65536): the C call
+    allocates nothing. Pass `adv` (and `ret`) to keep this wrapper from allocating them."""
+    N, T, dt, dev = _prep(r)
+    _check_data("v", v, N, T, dt, dev); _check_data("bv", bv, N, T, dt, dev)
+    _check_data("boot", boot, N, T, dt, dev, shape=(N,))
+    _check_flags("mask", mask, N, T, dev)
+    _check_flags("term", term, N, T, dev); _check_flags("trunc", trunc, N, T, dev)
+    adv = _out("adv", adv, N, T, dev)
+    ret = _out("ret", ret, N, T, dev) if (want_ret or ret is not None) else None
+    with _on(dev):
+        _call("rlcs_gae_masked_noalloc", _ptr(r), _ptr(v), _ptr(mask), _ptr(term), _ptr(trunc),
+              _ptr(bv), _ptr(boot), _ptr(adv), _ptr(ret), N, T, gamma, lam, 1 if normalize else 0,
+              eps, _DTYPES[dt], _stream(dev))
+    return adv, ret

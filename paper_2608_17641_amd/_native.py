@@ -62,6 +62,8 @@ PROTOTYPES = {
     "rlcs_gae_masked": [_P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _F, _F, _INT, _F, _INT, _P,
                         _SZ, _P],
     "rlcs_workspace_size_masked": [_I64, _I64],
+    "rlcs_gae_masked_noalloc": [_P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _F, _F, _INT, _F,
+                                _INT, _P],
     "rlcs_status_string": [_INT],
     "rlcs_version": [],
     "rlcs_testing_set_variant": [_INT],

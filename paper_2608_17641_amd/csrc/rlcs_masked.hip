@@ -1,5 +1,7 @@
 // GAE with observation-skip masking and optional advantage whitening (Section 9.3; Table 1 and
 // Section 3.3.1 for the unmasked steps).
+#include <mutex>
+
 #include "rlcs_dispatch.h"
 #include "rlcs_masked.h"
 
@@ -11,8 +13,8 @@ namespace {
 // Bytes of the whitening workspace of an [N, T] call (at most one workgroup per row): 64 for
 // the statistics {mean, rstd}, one 32-byte partial per workgroup (room for N), then one per
 // block of kDirectPartials partials.
-size_t masked_rows(int64_t N) { return size_t(N > 0 ? N : 1); }
-size_t masked_ws_need(int64_t N) {
+constexpr size_t masked_rows(int64_t N) { return size_t(N > 0 ? N : 1); }
+constexpr size_t masked_ws_need(int64_t N) {
     return 64 + sizeof(Moments) * (masked_rows(N) + (masked_rows(N) + kDirectPartials - 1) / kDirectPartials);
 }
 
@@ -94,33 +96,101 @@ rlcs_status run_masked(MaskedArgs& ma, bool normalize, float eps, void* ws, hipS
     return hipGetLastError() == hipSuccess ? RLCS_OK : RLCS_ERR_LAUNCH;
 }
 
+// The whitening workspace of rlcs_gae_masked_noalloc: a static device array sized for calls of
+// up to kNoAllocMaxRows rows (2 MiB), one copy per GPU, held until the process ends. Host code
+// never uses the array's name as an address: the device address comes from
+// hipGetSymbolAddress, once per device, and every call on a device shares that device's copy.
+constexpr int64_t kNoAllocMaxRows = 65536;
+constexpr size_t kNoAllocScratchBytes = masked_ws_need(kNoAllocMaxRows);
+static_assert(kNoAllocScratchBytes % 64 == 0, "the scratch holds whole 64-byte units");
+
+constexpr int kMaxDevices = 64;
+
 }  // namespace
 
-extern "C" {
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
 
-rlcs_status rlcs_gae_masked(const void* r, const void* v, const uint8_t* mask,
-                            const uint8_t* term, const uint8_t* trunc, const void* bv,
-                            const void* boot, float* adv, float* ret, int64_t N, int64_t T,
-                            float gamma, float lambda, int normalize, float eps,
-                            rlcs_dtype dtype, void* ws, size_t ws_bytes, rlcs_stream_t stream) {
-    rlcs_status st = check_common(N, T, dtype, {r, v, bv, boot}, {adv, ret});
+namespace {
+
+// Device address of `scratch` on the current device (nullptr if it cannot be had), looked up
+// with that device current on its first use and kept per device.
+void* scratch_address() {
+    static std::mutex mu;
+    static void* addr[kMaxDevices] = {};
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!addr[dev]) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess) return nullptr;
+        addr[dev] = p;
+    }
+    return addr[dev];
+}
+
+// Argument checks of the masked entry points (host only, before any HIP call).
+rlcs_status check_masked(const void* r, const void* v, const uint8_t* trunc, const void* bv,
+                         const void* boot, const float* adv, const float* ret, int64_t N, int64_t T,
+                         float gamma, float lambda, int normalize, float eps, rlcs_dtype dtype) {
+    const rlcs_status st = check_common(N, T, dtype, {r, v, bv, boot}, {adv, ret});
     if (st != RLCS_OK) return st;
     if (!unit_interval(gamma) || !unit_interval(lambda)) return RLCS_ERR_INVALID_ARG;
     if (normalize != 0 && normalize != 1) return RLCS_ERR_INVALID_ARG;
     if (normalize && !(eps >= 0.f && eps < INFINITY)) return RLCS_ERR_INVALID_ARG;
     if (N == 0 || T == 0) return RLCS_OK;
     if (!r || !v || !adv || (trunc && !bv)) return RLCS_ERR_INVALID_ARG;
-    if (normalize && (!ws || ws_bytes < masked_ws_need(N) || !aligned(ws, 64)))
-        return RLCS_ERR_WORKSPACE;
+    return RLCS_OK;
+}
+
+// A checked, non-empty call (ws: the whitening workspace when normalize).
+rlcs_status masked_call(const void* r, const void* v, const uint8_t* mask, const uint8_t* term,
+                        const uint8_t* trunc, const void* bv, const void* boot, float* adv,
+                        float* ret, int64_t N, int64_t T, float gamma, float lambda, bool normalize,
+                        float eps, rlcs_dtype dtype, void* ws, hipStream_t s) {
     MaskedArgs ma{};
     ma.a = make_args(N, T, gamma, lambda, 1.f, 1.f);
     ma.a.in[0] = r; ma.a.in[1] = v; ma.a.in[2] = bv;
     ma.a.term = term; ma.a.trunc = trunc; ma.a.row_value = boot;
     ma.a.out0 = adv; ma.a.out1 = ret;
     ma.mask = mask;
-    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    if (dtype == RLCS_BF16) return run_masked<bf16_t>(ma, normalize != 0, eps, ws, s);
-    return run_masked<float>(ma, normalize != 0, eps, ws, s);
+    if (dtype == RLCS_BF16) return run_masked<bf16_t>(ma, normalize, eps, ws, s);
+    return run_masked<float>(ma, normalize, eps, ws, s);
+}
+
+}  // namespace
+
+extern "C" {
+
+rlcs_status rlcs_gae_masked_noalloc(const void* r, const void* v, const uint8_t* mask,
+                                    const uint8_t* term, const uint8_t* trunc, const void* bv,
+                                    const void* boot, float* adv, float* ret, int64_t N, int64_t T,
+                                    float gamma, float lambda, int normalize, float eps,
+                                    rlcs_dtype dtype, rlcs_stream_t stream) {
+    if (N > kNoAllocMaxRows) return RLCS_ERR_WORKSPACE;
+    const rlcs_status st = check_masked(r, v, trunc, bv, boot, adv, ret, N, T, gamma, lambda,
+                                        normalize, eps, dtype);
+    if (st != RLCS_OK || N == 0 || T == 0) return st;
+    void* ws = nullptr;
+    if (normalize) {
+        ws = scratch_address();
+        if (!ws) return RLCS_ERR_LAUNCH;
+    }
+    return masked_call(r, v, mask, term, trunc, bv, boot, adv, ret, N, T, gamma, lambda,
+                       normalize != 0, eps, dtype, ws, reinterpret_cast<hipStream_t>(stream));
+}
+
+rlcs_status rlcs_gae_masked(const void* r, const void* v, const uint8_t* mask,
+                            const uint8_t* term, const uint8_t* trunc, const void* bv,
+                            const void* boot, float* adv, float* ret, int64_t N, int64_t T,
+                            float gamma, float lambda, int normalize, float eps,
+                            rlcs_dtype dtype, void* ws, size_t ws_bytes, rlcs_stream_t stream) {
+    const rlcs_status st = check_masked(r, v, trunc, bv, boot, adv, ret, N, T, gamma, lambda,
+                                        normalize, eps, dtype);
+    if (st != RLCS_OK || N == 0 || T == 0) return st;
+    if (normalize && (!ws || ws_bytes < masked_ws_need(N) || !aligned(ws, 64)))
+        return RLCS_ERR_WORKSPACE;
+    return masked_call(r, v, mask, term, trunc, bv, boot, adv, ret, N, T, gamma, lambda,
+                       normalize != 0, eps, dtype, ws, reinterpret_cast<hipStream_t>(stream));
 }
 
 size_t rlcs_workspace_size_masked(int64_t N, int64_t T) {

@@ -244,3 +244,19 @@ def test_gae_masked_validation(lib):
     assert lib.rlcs_workspace_size_masked(100, 7) == 64 + 32 * 100 + 32
     assert lib.rlcs_workspace_size_masked(4097, 7) == 64 + 32 * 4097 + 32 * 2
     assert lib.rlcs_workspace_size_masked(-1, 7) == 0
+
+
+def test_noalloc_rejects_more_rows_than_its_workspace(lib):
+    """rlcs_gae_masked_noalloc refuses calls of more rows than its built-in workspace holds,
+    with or without whitening, before any HIP call."""
+    from paper_2608_17641_amd import _native as n
+    for norm in (0, 1):
+        assert lib.rlcs_gae_masked_noalloc(FAKE, FAKE, None, None, None, None, None, FAKE2, None,
+                                           65537, 4, 0.99, 0.95, norm, 1e-8, n.RLCS_F32,
+                                           None) == n.RLCS_ERR_WORKSPACE
+    # the argument checks of rlcs_gae_masked still apply below the limit
+    assert lib.rlcs_gae_masked_noalloc(FAKE, FAKE, None, None, None, None, None, FAKE2, None,
+                                       8, 4, 1.5, 0.95, 1, 1e-8, n.RLCS_F32,
+                                       None) == n.RLCS_ERR_INVALID_ARG
+    assert lib.rlcs_gae_masked_noalloc(FAKE, FAKE, None, None, None, None, None, FAKE2, None,
+                                       8, 4, 0.99, 0.95, 1, 1e-8, 7, None) == n.RLCS_ERR_DTYPE
