@@ -94,6 +94,7 @@ struct Plan {
     int wave_local;       // rows kernel: no carry crosses waves
     size_t lds_bytes;     // dynamic LDS (staged policies)
     bool pad;             // rows kernel, vector path: lanes outside the range or in row gaps skip
+    int wave_rows_log2T;  // >= 0: wave_rows_kernel (rows tile a wave exactly; T = 2^log2T)
 };
 
 template <class Op, typename DT, bool VEC, bool TR, int W, bool PAD = false>
@@ -115,6 +116,15 @@ void launch_w(const Args& a, const Plan& p, hipStream_t stream) {
 
 template <class Op, typename DT, bool VEC, bool TR>
 rlcs_status launch(const Args& a, const Plan& p, hipStream_t stream) {
+    if constexpr (VEC && Op::kStaged == 0) {
+        if (p.wave_rows_log2T >= 0) {
+            constexpr int64_t span = int64_t(kWave) * Width<DT>::K;
+            const int64_t groups = (a.N * a.T + span - 1) / span;
+            hipLaunchKernelGGL((wave_rows_kernel<Op, DT, Width<DT>::K, TR>), dim3(unsigned(groups)),
+                               dim3(kWave), 0, stream, a, p.wave_rows_log2T);
+            return hipGetLastError() == hipSuccess ? RLCS_OK : RLCS_ERR_LAUNCH;
+        }
+    }
     if constexpr (VEC && Op::kStaged == 0) {
         if (p.pad && !p.split) {
             if (p.waves == kSmallWaves) launch_w<Op, DT, true, TR, kSmallWaves, true>(a, p, stream);
@@ -199,6 +209,14 @@ rlcs_status dispatch_dt(Args& a, bool has_trunc, void* ws, size_t ws_bytes, hipS
         else p.waves = kSmallWaves;
         p.lds_bytes = 0;
     }
+    p.wave_rows_log2T = -1;
+    if (Op::kStaged == 0 && !p.split && vec && T >= K && T <= int64_t(kWave) * K && (T & (T - 1)) == 0) {
+        // rows tile a wave exactly: the wave-rows kernel
+        if ((N * T + int64_t(kWave) * K - 1) / (int64_t(kWave) * K) > INT32_MAX) return RLCS_ERR_INVALID_ARG;
+        int l = 0;
+        while ((int64_t(1) << l) < T) ++l;
+        p.wave_rows_log2T = l;
+    }
     if (p.split) {
         if (N * p.tiles_per_row > INT32_MAX) return RLCS_ERR_INVALID_ARG;
         a.ws = ws;
@@ -261,6 +279,7 @@ rlcs_status dispatch_strided_rows(Args& a, int64_t period, rlcs_dtype dtype, boo
         if ((a.N + p.rows_per_wg - 1) / p.rows_per_wg > INT32_MAX) return RLCS_ERR_INVALID_ARG;
         p.wave_local = 0;
         p.lds_bytes = 0;
+        p.wave_rows_log2T = -1;
         // Vector path, lane by lane (lanes whose steps reach into a gap or past the range go
         // element-wise): T >= K, data and outputs 16-byte aligned, flags K-byte aligned.
         bool vec = a.T >= K;

@@ -671,6 +671,117 @@ __global__ void __launch_bounds__(W * kWave) rows_kernel(Args a, int64_t rows_pe
     }
 }
 
+// Rows that tile a wave exactly: T a power of two with K <= T <= 64*K, dense rows, every array
+// aligned for the vector path. One wave per workgroup; wave g owns steps [g*64*K, (g+1)*64*K)
+// of the flat [N*T] array, lane l the l-th group of K steps (the (63-l)-th backward), so every
+// row lies inside one wave and its edge step inside one lane. A lane's row and step are a
+// shift and a mask of its position, and the step after (before) the lane's last (first) one
+// is either in lane l-1 or across the row's edge, so no neighbour is read from memory and
+// nothing crosses waves: per lane, the flag words, the data vectors and the per-row value are
+// issued back to back, the continuation vector follows only where a step is truncated, then
+// Table 1's coefficients, the lane's serial map, the DPP wave scan and the stores. Lanes past
+// the array's end (its last wave may be partial; N*T is a multiple of K) load step 0 of row
+// 0 and store nothing. Grid: ceil(N*T / (64*K)) workgroups of one wave.
+template <class Op, typename DT, int K, bool TR>
+__global__ void __launch_bounds__(kWave) wave_rows_kernel(Args a, int log2T) {
+    static_assert(Op::kStaged == 0, "staged policies run on the rows kernel");
+    constexpr bool kBack = Op::kBackward;
+    constexpr int NS = Op::kSlots;
+    constexpr int NB = Op::kNbr > 0 ? Op::kNbr : 1;
+    constexpr int kWords = K * int(sizeof(DT)) / 4;
+    constexpr int kTS = TR ? Op::kTruncSlot : -1;
+    const int lane = threadIdx.x;
+    const int64_t T = a.T;
+    const int64_t p0 = int64_t(blockIdx.x) * (kWave * K) + int64_t(lane_group<kBack>(lane)) * K;
+    const bool live = p0 < a.N * T;
+    const int64_t pc = live ? p0 : 0;
+    const uint8_t* fallback = reinterpret_cast<const uint8_t*>(a.in[0]);
+
+    uint32_t tw[(K + 3) / 4], rw[(K + 3) / 4];
+    uint32_t w[NS][kWords];
+    if (Op::kFlags && TR) load_flag_words<K>(a.trunc, pc, rw);
+    if (Op::kFlags) load_flag_words<K>(a.term ? a.term : fallback, pc, tw);
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+        if (Op::slot_used(s, TR) && s != kTS) load_words<DT, K>(a.in[s], pc, w[s]);
+    const int64_t row = pc >> log2T;
+    const int64_t t = pc & (T - 1);
+    const bool has_rv = Op::kRowValue && a.row_value;
+    const float rv = load_one<DT>(has_rv ? a.row_value : a.in[0], row);
+    // the row's edge step, if among the lane's K steps (T is a multiple of K)
+    const int ke = kBack ? (t + K == T ? K - 1 : -1) : (t == 0 ? 0 : -1);
+    const uint32_t edge = ke >= 0 ? (1u << ke) : 0u;
+    const uint32_t trunc = (Op::kFlags && TR) ? flag_mask<K>(rw) : 0u;
+    if constexpr (kTS >= 0) {
+        if (trunc) load_words<DT, K>(a.in[kTS], pc, w[kTS]);
+        else {
+#pragma unroll
+            for (int i = 0; i < kWords; ++i) w[kTS][i] = 0u;
+        }
+    }
+    float d[NS][K];
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+        if (Op::slot_used(s, TR)) unpack_words<DT, K>(w[s], d[s]);
+        else {
+#pragma unroll
+            for (int k = 0; k < K; ++k) d[s][k] = 0.f;
+        }
+    }
+    const uint32_t term = (Op::kFlags && a.term) ? flag_mask<K>(tw) : 0u;
+    float B[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) B[k] = (k == ke && has_rv) ? rv : 0.f;
+
+    // neighbour on the carry-source side: lane l-1 (across a row edge it is not used)
+    float nb[NB];
+    if constexpr (Op::kNbr > 0) {
+        float own[NB];
+        Op::template nbr_export<K>(a.p, d, term | trunc, own);
+#pragma unroll
+        for (int i = 0; i < NB; ++i) nb[i] = shift_up1(own[i], 0.f);
+    } else {
+#pragma unroll
+        for (int i = 0; i < NB; ++i) nb[i] = 0.f;
+    }
+    float al[K], be[K];
+    Op::template build<K, TR>(a.p, d, term, trunc, edge, B, nb, al, be);
+    if (!live) {
+#pragma unroll
+        for (int k = 0; k < K; ++k) { al[k] = 0.f; be[k] = 1.f; }
+    }
+    Pair agg;
+    if (kBack) {
+        agg = Pair{al[K - 1], be[K - 1]};
+#pragma unroll
+        for (int k = K - 2; k >= 0; --k) agg = compose(Pair{al[k], be[k]}, agg);
+    } else {
+        agg = Pair{al[0], be[0]};
+#pragma unroll
+        for (int k = 1; k < K; ++k) agg = compose(Pair{al[k], be[k]}, agg);
+    }
+    const Pair incl = wave_scan_inclusive(agg, lane);
+    // value entering this lane: the value leaving lane l-1 (nothing enters lane 0, whose
+    // carry-source side is a row edge)
+    const float X = shift_up1(incl.a, 0.f);
+    float A[K];
+    if (kBack) {
+        float nxt = X;
+#pragma unroll
+        for (int k = K - 1; k >= 0; --k) { A[k] = fmaf(be[k], nxt, al[k]); nxt = A[k]; }
+    } else {
+        float prv = X;
+#pragma unroll
+        for (int k = 0; k < K; ++k) { A[k] = fmaf(be[k], prv, al[k]); prv = A[k]; }
+    }
+    float o0[K], o1[K];
+    Op::template finish<K, TR>(a.p, d, term, trunc, edge, B, nb, A, X, o0, o1);
+    if (live) {
+        store_k<K>(a.out0, p0, 0u, true, o0);
+        if (a.out1) store_k<K>(a.out1, p0, 0u, true, o1);
+    }
+}
+
 // Polls of one record before a waiting tile gives up (about a second). Reached only when the
 // workspace was not zero-filled before first use; the tile then continues with a NaN carry
 // and flags the workspace header instead of waiting forever.

@@ -108,6 +108,24 @@ def test_odd_lengths_bf16(T, var):
             check(name, ro, ws=ws, gamma=0.97, lam=0.9, label=f"bf16 T={T} variant {var}")
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("T", [4, 8, 16, 32, 64, 128, 256, 512])
+def test_rows_tiling_a_wave(T, dtype):
+    """Power-of-two rows of K to 64*K steps (K = 4 float32, 8 bfloat16 steps per lane): the
+    wave-rows kernel, whole rows per wave. Row counts that leave the last wave partial, one
+    row, and many rows; with and without truncation and bootstrap."""
+    K = 4 if dtype == "f32" else 8
+    if T < K or T > 64 * K:
+        pytest.skip("not a wave-rows shape for this dtype")
+    for N in (1, 3, 1000 // T + 1, 4099):
+        for i, name in enumerate(ESTIMATORS):
+            ro = make_inputs(name, N, T, seed=N * 7 + T + i, dtype=dtype, p_term=0.05, p_trunc=0.05)
+            check(name, ro, gamma=0.97, lam=0.9, label=f"{N}x{T} {dtype}")
+            if name in ("gae", "vtrace", "td_lambda"):
+                check(name, ro, trunc=False, boot=False, gamma=0.97, lam=0.9,
+                      label=f"{N}x{T} {dtype} plain")
+
+
 @pytest.mark.parametrize("N,T", [(1, 1), (1, 4096), (1, 1 << 20), (3, 100_000), (5000, 3)])
 @pytest.mark.parametrize("var", [0, 1, 2])
 def test_extreme_shapes(N, T, var):
