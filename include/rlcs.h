@@ -211,10 +211,14 @@ size_t rlcs_workspace_size(int64_t N, int64_t T);
  *            unbiased variance over the steps that take part (var 0 with fewer than two),
  *            applied to every step. eps >= 0, finite.
  *   ws       required when normalize = 1: rlcs_workspace_size_masked(N, T) bytes, 64-byte
- *            aligned, any contents (no clearing needed); calls sharing it must be ordered on
- *            one stream. After the call its first 16 bytes hold the mean and 1/sqrt(var + eps)
- *            as two doubles. Unused when normalize = 0.
- * Rows are never split across workgroups for this entry point.                             */
+ *            aligned, zero-filled once before its first use (every call leaves it ready for
+ *            the next); calls sharing it must be ordered on one stream. After the call its
+ *            first 16 bytes hold the mean and 1/sqrt(var + eps) as two doubles. Unused when
+ *            normalize = 0.
+ * Rows are never split across workgroups for this entry point. A whitened call whose rows fit
+ * in one workgroup's chunk (T <= 4096 float32 / 8192 bfloat16 steps) and whose workgroups
+ * are all resident on the GPU at once runs as one kernel that reads and writes every array
+ * once; otherwise a second kernel rewrites the advantages.                                  */
 rlcs_status rlcs_gae_masked(const void* r, const void* v, const uint8_t* mask,
                             const uint8_t* term, const uint8_t* trunc, const void* bv,
                             const void* boot, float* adv, float* ret, int64_t N, int64_t T,
@@ -228,18 +232,19 @@ size_t rlcs_workspace_size_masked(int64_t N, int64_t T);
 /* rlcs_gae_masked without a workspace argument, for callers that cannot allocate device memory
  * (code under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc). Same
  * arguments, results and kernels as rlcs_gae_masked; whitening (normalize = 1) uses a
- * workspace built into the library instead of `ws`: a static device array of 2 MiB per GPU,
- * held until the process ends, enough for N <= 65536 rows. The call itself allocates nothing
+ * workspace built into the library instead of `ws`: a static device array of 2.2 MiB per
+ * GPU, held until the process ends, enough for N <= 65536 rows. The call itself allocates nothing
  * (no hipMalloc, no allocating library routine).
  *   N > 65536  RLCS_ERR_WORKSPACE, checked first (also with normalize = 0), before any HIP
  *              call; the other checks are rlcs_gae_masked's.
  *   The array's device address is looked up on the first call on each device (that device
  *   current); if the lookup fails the call returns RLCS_ERR_LAUNCH and enqueues nothing.
- * Every call on one GPU shares that GPU's array and nothing in it needs clearing (each call
- * writes what it reads back). Calls that can overlap on one GPU (other streams, other
- * threads, other graph replays running at the same time) race on the array and must not
- * whiten at once; calls ordered on one stream are safe. The mean and 1/sqrt(var + eps) of the
- * last call are not returned (use rlcs_gae_masked with a workspace for them). */
+ * Every call on one GPU shares that GPU's array, which starts zero-filled when the library is
+ * loaded on that device; every call leaves it ready for the next, so nothing needs clearing.
+ * Calls that can overlap on one GPU (other streams, other threads, other graph replays
+ * running at the same time) race on the array and must not whiten at once; calls ordered on
+ * one stream are safe. The mean and 1/sqrt(var + eps) of the last call are not returned (use
+ * rlcs_gae_masked with a workspace for them). */
 rlcs_status rlcs_gae_masked_noalloc(const void* r, const void* v, const uint8_t* mask,
                                     const uint8_t* term, const uint8_t* trunc, const void* bv,
                                     const void* boot, float* adv, float* ret, int64_t N, int64_t T,

@@ -507,8 +507,9 @@ def rlcs_gae_masked(r, v, mask=None, term=None, trunc=None, bv=None, boot=None, 
                     ret=None, *, gamma: float, lam: float, normalize: bool = False,
                     eps: float = 1e-8, ws=None, want_ret: bool = True):
     """GAE with observation-skip masking (mask nonzero = the step takes part), optionally with
-    the advantages whitened over the steps that take part. A workspace for whitening is
-    allocated when none is given (its contents never need clearing)."""
+    the advantages whitened over the steps that take part. A zero-filled workspace for
+    whitening is allocated when none is given (a workspace passed in must have been zero-filled
+    before its first use)."""
     N, T, dt, dev = _prep(r)
     _check_data("v", v, N, T, dt, dev); _check_data("bv", bv, N, T, dt, dev)
     _check_data("boot", boot, N, T, dt, dev, shape=(N,))
@@ -517,7 +518,7 @@ def rlcs_gae_masked(r, v, mask=None, term=None, trunc=None, bv=None, boot=None, 
     adv = _out("adv", adv, N, T, dev)
     ret = _out("ret", ret, N, T, dev) if (want_ret or ret is not None) else None
     if normalize and ws is None:
-        ws = torch.empty(max(rlcs_workspace_size_masked(N, T), 64), dtype=torch.uint8, device=dev)
+        ws = torch.zeros(max(rlcs_workspace_size_masked(N, T), 64), dtype=torch.uint8, device=dev)
     wp, wb = _ws(ws, dev)
     with _on(dev):
         _call("rlcs_gae_masked", _ptr(r), _ptr(v), _ptr(mask), _ptr(term), _ptr(trunc), _ptr(bv),

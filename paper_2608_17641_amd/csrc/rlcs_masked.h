@@ -212,11 +212,13 @@ struct MaskedChunk {
     // Outputs given Xw, the state entering the wave's span; returns the state at the lane's
     // first step. Accumulates the advantages that take part into (n, sum, sumsq). `full`: the
     // lane's steps are vector-aligned (stored as vectors when all of them are the lane's).
-    template <bool STATS>
+    float adv[K];  // the lane's advantages (kept for the fused whitening)
+
+    template <bool STATS, bool STORE_ADV = true>
     __device__ __forceinline__ AW finish(const Args& a, AW Xw, bool full, double& n, double& s1,
                                          double& s2) {
         AW x = shift_up1(apply(incl, Xw), Xw);
-        float adv[K], ret[K];
+        float ret[K];
 #pragma unroll
         for (int k = K - 1; k >= 0; --k) {
             x = apply(m[k], x);
@@ -230,7 +232,7 @@ struct MaskedChunk {
             }
         }
         const bool vstore = full && valid == kAll;
-        store_k<K>(a.out0, p0, valid, vstore, adv);
+        if (STORE_ADV) store_k<K>(a.out0, p0, valid, vstore, adv);
         if (a.out1) store_k<K>(a.out1, p0, valid, vstore, ret);
         return x;
     }
@@ -261,6 +263,42 @@ __device__ __forceinline__ double wave_sum(double x) {
     return (read_lane_f64(x, 15) + read_lane_f64(x, 31)) + (read_lane_f64(x, 47) + read_lane_f64(x, 63));
 }
 
+// Step 1 of one chunk [chunk_lo, chunk_hi) of a workgroup's range [lo, hi) (lane l of wave w
+// owns the (63-l)-th group of K steps of the wave's span).
+template <typename DT, int K, bool TR, bool HM>
+__device__ __forceinline__ void masked_chunk_load(MaskedChunk<DT, K, TR, HM>& c, const MaskedArgs& ma,
+                                                  const RowBase& base, int64_t lo, int64_t hi,
+                                                  int64_t chunk_lo, int64_t chunk_hi, bool can_full,
+                                                  int lane, int wave) {
+    const Args& a = ma.a;
+    c.p0 = chunk_lo + (int64_t(wave) * kWave + (kWave - 1 - lane)) * K;
+    const bool full = can_full && chunk_lo >= lo && chunk_hi <= hi;
+    if (full) {
+        c.load_full(ma, base, MaskedChunk<DT, K, TR, HM>::kAll);
+    } else if (can_full) {
+        // lane by lane: vector loads wherever the lane's K steps lie inside the array (the
+        // steps outside the range masked off), element-wise otherwise
+        constexpr uint32_t kAll = MaskedChunk<DT, K, TR, HM>::kAll;
+        const int64_t p = c.p0;
+        if (p >= lo && p + K <= hi) {
+            c.load_full(ma, base, kAll);
+        } else if (p + K > lo && p < hi && p >= 0 && p + K <= a.N * a.T) {
+            uint32_t m = kAll;
+            RowBase b = base;
+            if (p < lo) {
+                m &= (kAll << uint32_t(lo - p)) & kAll;
+                b = RowBase{base.pos - a.T, base.row - 1, base.t};  // the row before
+            }
+            if (p + K > hi) m &= kAll >> uint32_t(p + K - hi);
+            c.load_full(ma, b, m);
+        } else {
+            c.load_masked(ma, base, lo, hi);
+        }
+    } else {
+        c.load_masked(ma, base, lo, hi);
+    }
+}
+
 // Rows kernel for masked GAE: workgroup g owns rows [g*R, g*R + R) and walks them in chunks of
 // E = W*64*K steps from the end. `wave_local`: every row lies within one wave's span, so no
 // carry crosses waves.
@@ -284,32 +322,7 @@ __global__ void __launch_bounds__(W * kWave) masked_gae_kernel(MaskedArgs ma, in
     for (;;) {
         const int64_t chunk_lo = chunk_hi - E;
         MaskedChunk<DT, K, TR, HM> c;
-        c.p0 = chunk_lo + (int64_t(wave) * kWave + (kWave - 1 - lane)) * K;
-        const bool full = can_full && chunk_lo >= lo && chunk_hi <= hi;
-        if (full) {
-            c.load_full(ma, base, MaskedChunk<DT, K, TR, HM>::kAll);
-        } else if (can_full) {
-            // lane by lane: vector loads wherever the lane's K steps lie inside the array (the
-            // steps outside the range masked off), element-wise otherwise
-            constexpr uint32_t kAll = MaskedChunk<DT, K, TR, HM>::kAll;
-            const int64_t p = c.p0;
-            if (p >= lo && p + K <= hi) {
-                c.load_full(ma, base, kAll);
-            } else if (p + K > lo && p < hi && p >= 0 && p + K <= a.N * a.T) {
-                uint32_t m = kAll;
-                RowBase b = base;
-                if (p < lo) {
-                    m &= (kAll << uint32_t(lo - p)) & kAll;
-                    b = RowBase{base.pos - a.T, base.row - 1, base.t};  // the row before
-                }
-                if (p + K > hi) m &= kAll >> uint32_t(p + K - hi);
-                c.load_full(ma, b, m);
-            } else {
-                c.load_masked(ma, base, lo, hi);
-            }
-        } else {
-            c.load_masked(ma, base, lo, hi);
-        }
+        masked_chunk_load(c, ma, base, lo, hi, chunk_lo, chunk_hi, can_full, lane, wave);
         const Tri incl = c.local(a.p, lane);
         Tri win = identity_tri();
         if (!wave_local) {
@@ -442,6 +455,185 @@ __global__ void __launch_bounds__(kNormThreads) masked_normalize_kernel(float* a
             if (i < total) adv[i] = (x[u] - mean) * rstd;
         }
     }
+}
+
+// ---------------------------------------------------------------- whitening in one pass
+// When every workgroup of a whitened call is resident on the GPU at once and holds one chunk,
+// the call runs as one kernel: each workgroup computes its advantages, stores the returns,
+// keeps the advantages in registers and publishes its fp64 moments; workgroup 0 adds them all
+// up (one record per lane, at most one per lane of its W waves) into the mean and
+// 1/sqrt(var + eps) and publishes them in kStatsCopies copies; every other workgroup waits for
+// its copy; then each whitens its advantages and stores them, once. Two round trips through
+// memory follow the last moments. The sums run in one fixed order, so results are
+// reproducible bit for bit. Every wait is for a workgroup that is already resident (the host
+// launches this form only when the whole grid fits on the GPU at once), and no atomic
+// read-modify-write is used (a counter that every workgroup increments serializes them, about
+// 17 ns each). A waiting workgroup polls one record with one lane, with pauses that grow, so
+// that the waiting workgroups do not flood memory while others still stream their data (every
+// workgroup polling every record it needs slowed whole calls several times over).
+//
+// Workspace of the whitening (zero-filled once before its first use; every call leaves it
+// ready for the next):
+//   [0, 16)    mean and 1/sqrt(var + eps) of the last call, two doubles (for the caller);
+//   [16, 24)   generation: the number of one-pass calls made on the workspace (mod 2^31);
+//              workgroup 0 advances it once every moment of its call is in, hence after every
+//              workgroup of the call has read it;
+//   kMaskedFusedOff: one tagged moments record (six words) per workgroup, kFusedMaxGroups;
+//   kMaskedStatsOff: kStatsCopies copies of the tagged statistics record (four words), one per
+//              128-byte line;
+//   kMaskedTwoPassOff: the partials of the two-pass form (Moments, 32 bytes each).
+// A tagged word holds a 32-bit half of a double in its low half and the tag 2*gen + 1 of its
+// call in the high half; a reader takes a double only when both of its words carry the
+// current tag, so no word of another call (or of the two-pass partials, which live apart)
+// passes for a current one. Polls are bounded (the loads may see a write late); on exhaustion
+// the statistics are NaN.
+constexpr int64_t kFusedMaxGroups = 1024;
+constexpr int kStatsCopies = 64;
+constexpr size_t kMaskedGenOff = 16;
+constexpr size_t kMaskedFusedOff = 64;
+constexpr size_t kMaskedStatsOff = (kMaskedFusedOff + 48 * size_t(kFusedMaxGroups) + 127) / 128 * 128;
+constexpr size_t kMaskedTwoPassOff = kMaskedStatsOff + 128 * size_t(kStatsCopies);
+
+__device__ __forceinline__ void put_tagged(uint64_t* w, double v, uint32_t tag) {
+    const uint64_t u = uint64_t(__double_as_longlong(v));
+    st_relaxed(w, uint64_t(tag) << 32 | (u & 0xffffffffu));
+    st_relaxed(w + 1, uint64_t(tag) << 32 | (u >> 32));
+}
+
+// Doubles v[0 .. M) from the tagged words w[0 .. 2M) once every word carries `tag`: all words
+// are loaded at once and reloaded until they do, after a pause that doubles from `pause`
+// to about 500 cycles (NaN after kMaxPolls rounds).
+template <int M>
+__device__ __forceinline__ void get_tagged(const uint64_t* w, uint32_t tag, double (&v)[M], int pause) {
+    uint64_t x[2 * M];
+#pragma unroll
+    for (int i = 0; i < 2 * M; ++i) x[i] = ld_relaxed(w + i);
+    for (uint32_t polls = 0;; ++polls) {
+        bool ok = true;
+#pragma unroll
+        for (int i = 0; i < 2 * M; ++i) ok = ok && uint32_t(x[i] >> 32) == tag;
+        if (ok) break;
+        if (polls >= kMaxPolls) {
+#pragma unroll
+            for (int i = 0; i < M; ++i) v[i] = __builtin_nan("");
+            return;
+        }
+        for (int i = 0; i < pause; ++i) __builtin_amdgcn_s_sleep(2);
+        pause = min(2 * pause, 4);
+#pragma unroll
+        for (int i = 0; i < 2 * M; ++i)
+            if (uint32_t(x[i] >> 32) != tag) x[i] = ld_relaxed(w + i);
+    }
+#pragma unroll
+    for (int i = 0; i < M; ++i)
+        v[i] = __longlong_as_double(int64_t((x[2 * i + 1] << 32) | (x[2 * i] & 0xffffffffu)));
+}
+
+// One-pass whitened masked GAE: workgroup g owns rows [g*R, g*R + R), which fit in one chunk;
+// every workgroup of the grid (G <= W * 64 <= kFusedMaxGroups of them) is resident at once.
+// `ws`: the whitening workspace.
+template <typename DT, int K, int W, bool VEC, bool TR, bool HM>
+__global__ void __launch_bounds__(W * kWave) masked_gae_fused_kernel(MaskedArgs ma, int64_t rows_per_wg,
+                                                                     int wave_local, float eps,
+                                                                     char* ws) {
+    static_assert(int64_t(W) * kWave <= kFusedMaxGroups, "one moments record per lane of workgroup 0");
+    const Args& a = ma.a;
+    constexpr int64_t E = int64_t(W) * kWave * K;
+    __shared__ float s_m[5][W];
+    __shared__ double s_stat[3][W];
+    __shared__ uint32_t s_tag;
+    __shared__ float s_mean, s_rstd;
+    const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+    const int64_t G = gridDim.x, g = blockIdx.x;
+    const int64_t row_lo = g * rows_per_wg;
+    const int64_t row_hi = min(row_lo + rows_per_wg, a.N);
+    const int64_t lo = row_lo * a.T, hi = row_hi * a.T;
+    const bool can_full = VEC && a.T >= K;
+    const RowBase base{lo, row_lo, 0};
+    const int64_t chunk_hi = (hi + K - 1) / K * K;
+    const int64_t chunk_lo = chunk_hi - E;  // <= lo: the rows fit in one chunk
+    uint64_t* gen_word = reinterpret_cast<uint64_t*>(ws + kMaskedGenOff);
+    uint64_t* rec = reinterpret_cast<uint64_t*>(ws + kMaskedFusedOff);
+    uint64_t* stats_rec = reinterpret_cast<uint64_t*>(ws + kMaskedStatsOff);
+    // the generation cannot move before this workgroup's moments are in
+    if (threadIdx.x == 0) s_tag = 2u * (uint32_t(ld_relaxed(gen_word)) & 0x7fffffffu) + 1u;
+
+    MaskedChunk<DT, K, TR, HM> c;
+    masked_chunk_load(c, ma, base, lo, hi, chunk_lo, chunk_hi, can_full, lane, wave);
+    const Tri incl = c.local(a.p, lane);
+    Tri win = identity_tri();
+    if (!wave_local) {
+        if (lane == kWave - 1) {
+            s_m[0][wave] = incl.p; s_m[1][wave] = incl.q; s_m[2][wave] = incl.s;
+            s_m[3][wave] = incl.ca; s_m[4][wave] = incl.cw;
+        }
+        __syncthreads();
+        for (int w = W - 1; w > wave; --w)
+            win = compose(Tri{s_m[0][w], s_m[1][w], s_m[2][w], s_m[3][w], s_m[4][w]}, win);
+    }
+    double n = 0.0, s1 = 0.0, s2 = 0.0;
+    c.template finish<true, false>(a, apply(win, AW{0.f, 0.f}), can_full, n, s1, s2);
+
+    // this workgroup's moments
+    n = wave_sum(n);
+    s1 = wave_sum(s1);
+    s2 = wave_sum(s2);
+    if (lane == 0) { s_stat[0][wave] = n; s_stat[1][wave] = s1; s_stat[2][wave] = s2; }
+    __syncthreads();
+    const uint32_t tag = s_tag;
+    if (g != 0) {
+        if (threadIdx.x == 0) {
+            Moments m{0.0, 0.0, 0.0, 0.0};
+            for (int w = 0; w < W; ++w) { m.n += s_stat[0][w]; m.s1 += s_stat[1][w]; m.s2 += s_stat[2][w]; }
+            uint64_t* mine = rec + 6 * g;
+            put_tagged(mine, m.n, tag);
+            put_tagged(mine + 2, m.s1, tag);
+            put_tagged(mine + 4, m.s2, tag);
+            double v[2];
+            get_tagged<2>(stats_rec + 16 * (g % kStatsCopies), tag, v, 2);
+            s_mean = float(v[0]);
+            s_rstd = float(v[1]);
+        }
+    } else {
+        // workgroup 0: every workgroup's moments (its own from LDS), one per lane
+        double v[3] = {0.0, 0.0, 0.0};
+        if (threadIdx.x == 0) {
+            for (int w = 0; w < W; ++w) { v[0] += s_stat[0][w]; v[1] += s_stat[1][w]; v[2] += s_stat[2][w]; }
+        } else if (threadIdx.x < G) {
+            get_tagged<3>(rec + 6 * int64_t(threadIdx.x), tag, v, 1);
+        }
+        __syncthreads();  // every lane of workgroup 0 has read s_stat
+        v[0] = wave_sum(v[0]);
+        v[1] = wave_sum(v[1]);
+        v[2] = wave_sum(v[2]);
+        if (lane == 0) { s_stat[0][wave] = v[0]; s_stat[1][wave] = v[1]; s_stat[2][wave] = v[2]; }
+        __syncthreads();
+        if (wave == 0) {
+            Moments t{0.0, 0.0, 0.0, 0.0};
+            for (int w = 0; w < W; ++w) { t.n += s_stat[0][w]; t.s1 += s_stat[1][w]; t.s2 += s_stat[2][w]; }
+            const double m = t.n > 0.0 ? t.s1 / t.n : 0.0;
+            const double var = t.n > 1.0 ? fmax(t.s2 - t.s1 * m, 0.0) / (t.n - 1.0) : 0.0;
+            const double r = 1.0 / sqrt(var + double(eps));
+            uint64_t* copy = stats_rec + 16 * lane;  // one 128-byte line per copy
+            put_tagged(copy, m, tag);
+            put_tagged(copy + 2, r, tag);
+            if (lane == 0) {
+                // every moment of the call is in, so every workgroup has read the generation
+                double* stats = reinterpret_cast<double*>(ws);
+                stats[0] = m;
+                stats[1] = r;
+                st_relaxed(gen_word, uint64_t(((tag - 1u) / 2u + 1u) & 0x7fffffffu));
+                s_mean = float(m);
+                s_rstd = float(r);
+            }
+        }
+    }
+    __syncthreads();
+    const float mean = s_mean, rstd = s_rstd;
+    float y[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) y[k] = (c.adv[k] - mean) * rstd;
+    store_k<K>(a.out0, c.p0, c.valid, can_full && c.valid == MaskedChunk<DT, K, TR, HM>::kAll, y);
 }
 
 }  // namespace rlcs

@@ -10,12 +10,24 @@ using namespace rlcs::host;
 
 namespace {
 
-// Bytes of the whitening workspace of an [N, T] call (at most one workgroup per row): 64 for
-// the statistics {mean, rstd}, one 32-byte partial per workgroup (room for N), then one per
-// block of kDirectPartials partials.
+// Bytes of the whitening workspace of an [N, T] call (at most one workgroup per row): the
+// 64-byte header (statistics, arrival word, statistics record), the one-pass form's moments
+// records (kFusedMaxGroups of 48 bytes), then the two-pass form's partials: one 32-byte
+// partial per workgroup (room for N), then one per block of kDirectPartials partials.
 constexpr size_t masked_rows(int64_t N) { return size_t(N > 0 ? N : 1); }
 constexpr size_t masked_ws_need(int64_t N) {
-    return 64 + sizeof(Moments) * (masked_rows(N) + (masked_rows(N) + kDirectPartials - 1) / kDirectPartials);
+    return kMaskedTwoPassOff +
+           sizeof(Moments) * (masked_rows(N) + (masked_rows(N) + kDirectPartials - 1) / kDirectPartials);
+}
+
+// Workgroups of `kernel` (with `threads` lanes) that the current device holds at once, or 0.
+template <class Kernel>
+int64_t resident_groups(Kernel kernel, int threads) {
+    int dev = 0, cus = 0, per_cu = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0) != hipSuccess) return 0;
+    return int64_t(cus) * per_cu;
 }
 
 template <typename DT, bool VEC, bool TR, bool HM, bool STATS>
@@ -34,6 +46,20 @@ void launch_masked(const MaskedArgs& ma, int waves, int64_t groups, int64_t rows
         hipLaunchKernelGGL((masked_gae_kernel<DT, K, kLargeWaves, VEC, TR, HM, STATS>),
                            dim3(unsigned(groups)), dim3(kLargeWaves * kWave), 0, s, ma,
                            rows_per_wg, wave_local);
+}
+
+// The one-pass whitened call (16-wave workgroups) when its grid is resident at once; false
+// when it is not (the caller then runs the two-pass form).
+template <typename DT, bool VEC, bool TR, bool HM>
+bool launch_fused(const MaskedArgs& ma, int64_t groups, int64_t rows_per_wg, int wave_local,
+                  float eps, void* ws, hipStream_t s) {
+    constexpr int K = Width<DT>::K;
+    constexpr int W = kLargeWaves;
+    const auto kernel = masked_gae_fused_kernel<DT, K, W, VEC, TR, HM>;
+    if (groups > int64_t(W) * kWave || groups > resident_groups(kernel, W * kWave)) return false;
+    hipLaunchKernelGGL(kernel, dim3(unsigned(groups)), dim3(W * kWave), 0, s, ma, rows_per_wg,
+                       wave_local, eps, static_cast<char*>(ws));
+    return true;
 }
 
 template <typename DT>
@@ -58,10 +84,29 @@ rlcs_status run_masked(MaskedArgs& ma, bool normalize, float eps, void* ws, hipS
                (!a.term || aligned(a.term, K)) && (!a.trunc || aligned(a.trunc, K)) &&
                (!ma.mask || aligned(ma.mask, K));
     const bool tr = a.trunc != nullptr, hm = ma.mask != nullptr;
+    constexpr int64_t E_large = int64_t(kLargeWaves) * kWave * K;
+    if (normalize && T <= E_large - slack && g_variant != 1) {
+        // every row in one 16-wave chunk: the one-pass form when the grid is resident at once
+        const int64_t rows16 = (E_large - slack) / T;
+        const int64_t groups16 = (N + rows16 - 1) / rows16;
+        bool fused = false;
+#define RLCS_FUSED(V, TRV, HMV) fused = launch_fused<DT, V, TRV, HMV>(ma, groups16, rows16, wave_local, eps, ws, s)
+#define RLCS_FUSED_HM(V, TRV) \
+    if (hm) { RLCS_FUSED(V, TRV, true); } else { RLCS_FUSED(V, TRV, false); }
+#define RLCS_FUSED_TR(V) \
+    if (tr) { RLCS_FUSED_HM(V, true); } else { RLCS_FUSED_HM(V, false); }
+        if (groups16 <= kFusedMaxGroups) {
+            if (vec) { RLCS_FUSED_TR(true); } else { RLCS_FUSED_TR(false); }
+        }
+#undef RLCS_FUSED_TR
+#undef RLCS_FUSED_HM
+#undef RLCS_FUSED
+        if (fused) return hipGetLastError() == hipSuccess ? RLCS_OK : RLCS_ERR_LAUNCH;
+    }
     double* stats = reinterpret_cast<double*>(ws);
     Moments* level2 = nullptr;
     if (normalize) {
-        ma.partials = reinterpret_cast<Moments*>(reinterpret_cast<char*>(ws) + 64);
+        ma.partials = reinterpret_cast<Moments*>(reinterpret_cast<char*>(ws) + kMaskedTwoPassOff);
         level2 = ma.partials + masked_rows(N);
     }
 #define RLCS_MASKED(V, TRV, HMV, ST) launch_masked<DT, V, TRV, HMV, ST>(ma, waves, groups, rows_per_wg, wave_local, s)
@@ -97,7 +142,8 @@ rlcs_status run_masked(MaskedArgs& ma, bool normalize, float eps, void* ws, hipS
 }
 
 // The whitening workspace of rlcs_gae_masked_noalloc: a static device array sized for calls of
-// up to kNoAllocMaxRows rows (2 MiB), one copy per GPU, held until the process ends. Host code
+// up to kNoAllocMaxRows rows (2.2 MiB), zero-filled when the library's code is loaded on a
+// device (static storage), one copy per GPU, held until the process ends. Host code
 // never uses the array's name as an address: the device address comes from
 // hipGetSymbolAddress, once per device, and every call on a device shares that device's copy.
 constexpr int64_t kNoAllocMaxRows = 65536;

@@ -9,8 +9,9 @@ extern "C" {
 
 /* Forces a kernel variant for the calls made afterwards FROM THE CALLING THREAD (the setting is
  * thread-local, so it never affects other threads' calls): 0 = automatic choice, 1 = whole rows
- * per workgroup, 2 = rows split across workgroups (needs the workspace; calls of more than 1024
- * rows, or columns in more than 1024 blocks of 64, still run whole), 3 = column scans in narrow
+ * per workgroup (and, for whitened masked GAE, the two-pass whitening), 2 = rows split across
+ * workgroups (needs the workspace; calls of more than 1024 rows, or columns in more than 1024
+ * blocks of 64, still run whole), 3 = column scans in narrow
  * groups (16 float32 or 32 bfloat16 columns per workgroup, whole columns; row-major calls as
  * with 0), 4 = column scans in narrow groups split across workgroups along T (needs the
  * workspace; at most 1024 groups and more than 64 steps, else as with 0; row-major calls as

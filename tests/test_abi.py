@@ -240,9 +240,11 @@ def test_gae_masked_validation(lib):
     assert call(normalize=1, ws=FAKE, ws_bytes=10) == n.RLCS_ERR_WORKSPACE
     assert call(lam=2.0) == n.RLCS_ERR_INVALID_ARG
     assert call(N=0) == n.RLCS_OK
-    # statistics, one partial per row, one per block of 4096 partials
-    assert lib.rlcs_workspace_size_masked(100, 7) == 64 + 32 * 100 + 32
-    assert lib.rlcs_workspace_size_masked(4097, 7) == 64 + 32 * 4097 + 32 * 2
+    # header, 1024 one-pass moments records of 48 bytes, 64 copies of the statistics on their
+    # own 128-byte lines, then the two-pass partials: one per row and one per block of 4096
+    fixed = (64 + 48 * 1024 + 127) // 128 * 128 + 128 * 64
+    assert lib.rlcs_workspace_size_masked(100, 7) == fixed + 32 * 100 + 32
+    assert lib.rlcs_workspace_size_masked(4097, 7) == fixed + 32 * 4097 + 32 * 2
     assert lib.rlcs_workspace_size_masked(-1, 7) == 0
 
 

@@ -26,7 +26,7 @@ def test_graph_replays_equal_eager():
     rf = {k: to_device(v, DEV) for k, v in workloads.make_retrace_full(256, 129, 5, seed=4).items()}
     ws_rows = rl.make_workspace(64, 8192, DEV)
     ws_cols = rl.make_workspace_columns(256, 1024, DEV)
-    ws_mask = torch.empty(rl.rlcs_workspace_size_masked(64, 2048), dtype=torch.uint8, device=DEV)
+    ws_mask = torch.zeros(rl.rlcs_workspace_size_masked(64, 2048), dtype=torch.uint8, device=DEV)
 
     def outputs():
         return [torch.empty((64, 8192), device=DEV), torch.empty((64, 8192), device=DEV),

@@ -2,6 +2,8 @@
 through the C ABI, against the fp64 oracle on the same seeded inputs. Bar: max |gpu - oracle|
 <= tol * (1 + max |oracle|) per output, tol = 1e-5 for float32 inputs and 1e-3 for bfloat16
 inputs (whitened outputs included: the oracle whitens its own fp64 advantages)."""
+import contextlib
+
 import numpy as np
 import pytest
 
@@ -19,6 +21,15 @@ import paper_2608_17641_amd as rl  # noqa: E402
 
 DEV = torch.device("cuda:0")
 G, L = 0.99, 0.95
+
+
+@contextlib.contextmanager
+def variant(v):
+    rl.testing_set_variant(v)
+    try:
+        yield
+    finally:
+        rl.testing_set_variant(0)
 
 
 def run(ro, mask, *, trunc=True, boot=True, normalize=False, eps=1e-8, gamma=G, lam=L):
@@ -97,25 +108,47 @@ def test_gae_masked_deterministic():
 
 
 def test_gae_masked_workspace_reuse():
-    """One whitening workspace, never cleared (filled with NaN bytes to start), serves calls of
-    several shapes in turn."""
+    """One whitening workspace serves calls of several shapes in turn, one-pass and two-pass.
+    Only its 64-byte header is zero-filled; every record and partial starts as 0xff bytes."""
     ws = torch.full((rl.rlcs_workspace_size_masked(600, 1),), 255, dtype=torch.uint8, device=DEV)
-    for N, T, seed in ((600, 40, 1), (7, 3000, 2), (600, 40, 1), (64, 1024, 3)):
+    ws[:64] = 0
+    for N, T, seed, var in ((600, 40, 1, 0), (7, 3000, 2, 0), (600, 40, 1, 1), (600, 40, 1, 0),
+                            (64, 1024, 3, 1), (64, 1024, 3, 0)):
         ro = workloads.make_multiturn(N, T, seed=seed, mean_action=20, mean_obs=30)
         d = {k: to_device(v, DEV) for k, v in ro.items()}
-        adv, _ = rl.rlcs_gae_masked(d["r"], d["v"], d["mask"], d["term"], None, None, d["boot"],
-                                    gamma=1.0, lam=0.95, normalize=True, ws=ws)
+        with variant(var):
+            adv, _ = rl.rlcs_gae_masked(d["r"], d["v"], d["mask"], d["term"], None, None,
+                                        d["boot"], gamma=1.0, lam=0.95, normalize=True, ws=ws)
         torch.cuda.synchronize()
         a, _ = oracle.gae_masked(ro["r"], ro["v"], ro["mask"], ro["term"], None, None, ro["boot"],
                                  gamma=1.0, lam=0.95)
         assert_parity({"adv": adv}, {"adv": oracle.normalize_advantages(a, ro["mask"], eps=1e-8)},
-                      TOL["f32"], label=f"reuse {N}x{T}")
+                      TOL["f32"], label=f"reuse {N}x{T} variant {var}")
         # the workspace's first 16 bytes hold the call's mean and 1/sqrt(var + eps), taken over
         # the kernel's float32 advantages: float32 rounding against the oracle's fp64 ones
         st = ws[:16].view(torch.float64).cpu().numpy()
         sel = a[ro["mask"] != 0]
         assert abs(st[0] - sel.mean()) <= 1e-6 * (1 + np.abs(sel).max())
         assert st[1] == pytest.approx(1 / np.sqrt(sel.var(ddof=1) + 1e-8), rel=1e-5)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("N,T", [(4096, 256), (64, 4096), (1000, 33), (3, 8192), (513, 1)])
+def test_gae_masked_one_pass_and_two_pass_whitening(N, T, dtype):
+    """Whitening in one kernel (every workgroup resident, advantages held in registers) and in
+    two (a second kernel rewrites them), each against the oracle. Where every row lies within
+    one wave the two forms scan each row alike, and the returns agree bit for bit."""
+    ro = workloads.make_rollout(N, T, seed=N + 3 * T, dtype=dtype, p_term=0.03, p_trunc=0.03)
+    mask = (np.random.default_rng(N + T).random((N, T)) < 0.7).astype(np.uint8)
+    rets = []
+    for var in (0, 1):
+        with variant(var):
+            out, ref = run(ro, mask, normalize=True)
+        assert_parity(out, ref, TOL[dtype], label=f"{N}x{T} {dtype} variant {var}")
+        rets.append(out["ret"])
+    K = 4 if dtype == "f32" else 8
+    if T % K == 0 and (64 * K) % T == 0:
+        assert torch.equal(rets[0], rets[1])
 
 
 @pytest.mark.parametrize("N,T", [(4500, 1024), (9000, 256)])

@@ -37,7 +37,7 @@ def _both(d, m, N, T, normalize):
     print(f"rlcs_gae_masked_noalloc N={N} T={T} normalize={normalize}", flush=True)
     rl.rlcs_gae_masked_noalloc(d["r"], d["v"], m, d["term"], d["trunc"], d["bv"], d["boot"], a0, r0,
                                gamma=G, lam=L, normalize=normalize)
-    ws = torch.empty(rl.rlcs_workspace_size_masked(N, T), dtype=torch.uint8, device=DEV)
+    ws = torch.zeros(rl.rlcs_workspace_size_masked(N, T), dtype=torch.uint8, device=DEV)
     a1, r1 = rl.rlcs_gae_masked(d["r"], d["v"], m, d["term"], d["trunc"], d["bv"], d["boot"],
                                 gamma=G, lam=L, normalize=normalize, ws=ws)
     torch.cuda.synchronize()
