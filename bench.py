@@ -512,7 +512,8 @@ def run_extra(dev, only=""):
         del sets, base, ws
         torch.cuda.empty_cache()
     for label, n_, t_, a_ in (("rf_4096x256x4", 4096, 256, 4), ("rf_512x4096x4", 512, 4096, 4),
-                              ("rf_4096x256x18", 4096, 256, 18)):
+                              ("rf_4096x256x18", 4096, 256, 18), ("rf_4096x256x64", 4096, 256, 64),
+                              ("rf_1024x256x256", 1024, 256, 256)):
         if label.startswith(only):
             run_retrace_full(label, n_, t_, a_, dev)
     for label, t_, n_ in (("tm_256x4096", 256, 4096), ("tm_4096x64", 4096, 64),

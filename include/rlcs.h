@@ -128,14 +128,19 @@ rlcs_status rlcs_retrace(const void* r, const void* q, const void* eq, const voi
  *   c_t = lambda * min(c_bar, rho_t),  c_T = 0,
  * and then scanned exactly as rlcs_retrace does.
  *   q, pi    [N, T, A] Q-values and target-policy probabilities, dtype, contiguous
- *   actions  [N, T] int32 taken actions; an action outside [0, A) selects nothing (its Q and
- *            pi are taken as 0)
+ *   actions  [N, T] int32 taken actions. An action outside [0, A) is a caller error the
+ *            kernel cannot return: that step takes Q(s_t, a_t) = pi(a_t|s_t) = 0 (so rho_t = 0),
+ *            and if `ws` is given the call sets its error word (below) to 2
  *   mu       [N, T] behaviour-policy probability of the taken action, dtype (nonzero)
  *   bv, boot E_pi Q of the true successor of a truncated step / of s_T, as for rlcs_retrace
  *   delta, q_ret  as for rlcs_retrace
- *   A        number of actions, 1 <= A <= 28 (each workgroup stages its rows' [steps, A]
- *            slices in LDS)
- * Rows are never split across workgroups for this entry point; ws is unused.               */
+ *   A        number of actions, A >= 1. Each workgroup stages its chunk's [steps, A] slices
+ *            of q and pi in LDS: whole for A <= 28, in slices of the action axis otherwise
+ *            (28 float32 / 24 bfloat16 actions at a time).
+ *   ws       optional, at least 64 bytes, 64-byte aligned, zero-filled by the caller: the int32
+ *            at byte 8 becomes 2 when a call meets an out-of-range action, and stays so until
+ *            the caller clears it. Unused otherwise; NULL = no report.
+ * Rows are never split across workgroups for this entry point.                             */
 rlcs_status rlcs_retrace_full(const void* r, const void* q, const void* pi,
                               const int32_t* actions, const void* mu, const uint8_t* term,
                               const uint8_t* trunc, const void* bv, const void* boot,

@@ -23,12 +23,12 @@ from ._native import RlcsError
 __all__ = [
     "rlcs_gae", "rlcs_vtrace", "rlcs_retrace", "rlcs_retrace_full", "rlcs_td_lambda", "rlcs_discounted",
     "rlcs_elig_trace", "rlcs_episodic_prefix", "rlcs_affine_scan", "rlcs_workspace_size",
-    "rlcs_version", "rlcs_set_variant_override", "make_workspace", "RlcsError",
+    "rlcs_version", "testing_set_variant", "make_workspace", "RlcsError",
     "rlcs_gae_strided", "rlcs_vtrace_strided", "rlcs_retrace_strided", "rlcs_td_lambda_strided",
     "rlcs_discounted_strided", "rlcs_elig_trace_strided", "rlcs_episodic_prefix_strided",
     "rlcs_elig_trace_vec",
     "rlcs_workspace_size_columns", "make_workspace_columns", "rlcs_gae_masked",
-    "rlcs_workspace_size_masked",
+    "rlcs_workspace_size_masked", "rlcs_gae_masked_noalloc",
 ]
 
 _DTYPES = {torch.float32: _native.RLCS_F32, torch.bfloat16: _native.RLCS_BF16}
@@ -195,8 +195,10 @@ def rlcs_retrace(r, q, eq, log_rho, term=None, trunc=None, bv=None, boot=None, d
 
 def rlcs_retrace_full(r, q, pi, actions, mu, term=None, trunc=None, bv=None, boot=None,
                       delta=None, q_ret=None, *, gamma: float, lam: float, c_bar: float = 1.0,
-                      want_q_ret: bool = True):
-    """Full-form Retrace: q, pi [N, T, A] (data dtype), actions int32 [N, T], mu [N, T]."""
+                      want_q_ret: bool = True, ws=None):
+    """Full-form Retrace: q, pi [N, T, A] (data dtype), actions int32 [N, T], mu [N, T]. With a
+    zero-filled `ws` of at least 64 bytes, a call that meets an action outside [0, A) sets the
+    int32 at byte 8 of `ws` to 2 (the step takes Q and pi as 0)."""
     N, T, dt, dev = _prep(r)
     if not isinstance(q, torch.Tensor) or q.dim() != 3 or tuple(q.shape[:2]) != (N, T):
         raise ValueError("q must be a [N, T, A] tensor")
@@ -214,7 +216,7 @@ def rlcs_retrace_full(r, q, pi, actions, mu, term=None, trunc=None, bv=None, boo
     with _on(dev):
         _call("rlcs_retrace_full", _ptr(r), _ptr(q), _ptr(pi), _ptr(actions), _ptr(mu),
               _ptr(term), _ptr(trunc), _ptr(bv), _ptr(boot), _ptr(delta), _ptr(q_ret), N, T, A,
-              gamma, lam, c_bar, _DTYPES[dt], None, 0, _stream(dev))
+              gamma, lam, c_bar, _DTYPES[dt], *_ws(ws, dev), _stream(dev))
     return delta, q_ret
 
 

@@ -55,7 +55,8 @@ constexpr int64_t kSplitBelowRows = 256;
 // 4-wave ones (all tiles of a row draw their tickets from one word).
 constexpr int64_t kMaxSmallTilesPerRow = 64;
 
-// Largest action axis of full-form Retrace (its [steps, A] slices are staged in LDS).
+// Largest action axis of full-form Retrace whose chunk's whole [steps, A] slices are staged in
+// LDS; longer axes are staged in slices of sliced_width actions.
 constexpr int64_t kMaxActions = 28;
 
 // Longest supported row (the kernels keep offsets within a row range in 32 bits).
@@ -132,7 +133,9 @@ rlcs_status launch(const Args& a, const Plan& p, hipStream_t stream) {
             return hipGetLastError() == hipSuccess ? RLCS_OK : RLCS_ERR_LAUNCH;
         }
     }
-    if constexpr (Op::kStaged > 0) {
+    if constexpr (Op::kStaged > 0 && Op::kSliced) {
+        launch_w<Op, DT, VEC, TR, kStagedWaves>(a, p, stream);
+    } else if constexpr (Op::kStaged > 0) {
         if (p.waves == kStagedWaves) launch_w<Op, DT, VEC, TR, kStagedWaves>(a, p, stream);
         else if (p.waves == kStagedMidWaves) launch_w<Op, DT, VEC, TR, kStagedMidWaves>(a, p, stream);
         else launch_w<Op, DT, VEC, TR, kSmallWaves>(a, p, stream);
@@ -161,6 +164,29 @@ constexpr int64_t staged_lds_bytes(int W, int64_t A) {
     return slots > slices ? slots : slices;
 }
 
+// Sliced staging (long action axes), W waves: LDS elements of one array's slab of As actions
+// (SlicedStager::cap), the widest slice (a multiple of 16 bytes of DT) whose two slabs fit in
+// `budget` bytes, and the LDS bytes of a chunk (slabs or slots, which overlay them).
+template <typename DT>
+constexpr int64_t sliced_cap(int W, int64_t As) {
+    const int64_t E = int64_t(W) * kWave * Width<DT>::K, per_block = 16 / int64_t(sizeof(DT));
+    return ((E + 1) * As + per_block - 1) / per_block * per_block;
+}
+template <typename DT>
+constexpr int64_t sliced_width(int W, int64_t budget) {
+    const int64_t per_block = 16 / int64_t(sizeof(DT));
+    int64_t As = per_block;
+    while (2 * sliced_cap<DT>(W, As + per_block) * int64_t(sizeof(DT)) <= budget) As += per_block;
+    return As;
+}
+template <class Op, typename DT>
+constexpr int64_t sliced_lds_bytes(int W, int64_t As) {
+    const int64_t E = int64_t(W) * kWave * Width<DT>::K;
+    const int64_t slots = int64_t(sizeof(float)) * Op::kStaged * (E + 4);
+    const int64_t slabs = 2 * sliced_cap<DT>(W, As) * int64_t(sizeof(DT));
+    return slots > slabs ? slots : slabs;
+}
+
 template <class Op, typename DT>
 rlcs_status dispatch_dt(Args& a, bool has_trunc, void* ws, size_t ws_bytes, hipStream_t stream) {
     constexpr int K = Width<DT>::K;
@@ -185,7 +211,13 @@ rlcs_status dispatch_dt(Args& a, bool has_trunc, void* ws, size_t ws_bytes, hipS
                                     : kWsRecordsOffset;
     const bool ws_ok = ws && ws_bytes >= ws_need && aligned(ws, 64);
     const int forced = g_variant;
-    if constexpr (Op::kStaged > 0) {
+    if constexpr (Op::kStaged > 0 && Op::kSliced) {
+        // Long action axes: one-wave workgroups, the widest slice that fits the LDS budget.
+        p.split = false;
+        p.waves = kStagedWaves;
+        a.A_slice = sliced_width<DT>(kStagedWaves, kStagedLdsBudget);
+        p.lds_bytes = size_t(sliced_lds_bytes<Op, DT>(kStagedWaves, a.A_slice));
+    } else if constexpr (Op::kStaged > 0) {
         // Staged policies keep whole rows in one workgroup (chunk loop for long rows).
         p.split = false;
         if (staged_lds_bytes<Op, DT>(kSmallWaves, a.A) <= kStagedLdsBudget) p.waves = kSmallWaves;

@@ -32,6 +32,7 @@ struct Args {
     const void* in[5];     // data inputs, meaning fixed by the policy
     const int32_t* actions;  // full-form Retrace: taken actions [N, T]
     int64_t A;             // full-form Retrace: number of actions
+    int64_t A_slice;       // full-form Retrace, long action axes: actions staged at a time
     int stage_vec;         // full-form Retrace: Q and pi are 16-byte aligned
     const uint8_t* term;   // [N, T] or null
     const uint8_t* trunc;  // [N, T] or null
@@ -52,6 +53,7 @@ struct Args {
 // Defaults shared by the policies: no inputs staged through LDS.
 struct OpBase {
     static constexpr int kStaged = 0;
+    static constexpr bool kSliced = false;  // staged policies: action axis taken in slices
     static constexpr int staged_index(int) { return -1; }
 };
 
@@ -272,6 +274,34 @@ struct RetraceFullOp : OpBase {
         v[1] = e;
         v[2] = pa / mu;
     }
+    // One slice of a step's rows, actions [a0, a0 + aw) (row pointers at action a0): adds
+    // pi * Q over the slice to `e`, in action order, and takes Q and pi of the taken action if
+    // it lies in the slice. Rows of whole 16-byte blocks are read one block at a time.
+    template <typename DT>
+    __device__ __forceinline__ static void accumulate_slice(const DT* q_row, const DT* pi_row, int64_t a0,
+                                                            int64_t aw, int32_t act, float& e, float& qa,
+                                                            float& pa) {
+        constexpr int kPer = 16 / int(sizeof(DT));
+        if (aw % kPer == 0) {
+            for (int64_t b = 0; b < aw / kPer; ++b) {
+                const u32x4 bq = *reinterpret_cast<const u32x4*>(q_row + b * kPer);
+                const u32x4 bp = *reinterpret_cast<const u32x4*>(pi_row + b * kPer);
+#pragma unroll
+                for (int u = 0; u < kPer; ++u) {
+                    const float qk = word_elem<DT>(bq[u * 4 / kPer], u);
+                    const float pk = word_elem<DT>(bp[u * 4 / kPer], u);
+                    e = fmaf(pk, qk, e);
+                    if (a0 + b * kPer + u == act) { qa = qk; pa = pk; }
+                }
+            }
+        } else {
+            for (int64_t k = 0; k < aw; ++k) {
+                const float qk = widen(q_row[k]), pk = widen(pi_row[k]);
+                e = fmaf(pk, qk, e);
+                if (a0 + k == act) { qa = qk; pa = pk; }
+            }
+        }
+    }
     __device__ static void nbr_from_stage(const Params& P, const float* stage, int stride, int i,
                                           float (&nb)[kNbr]) {
         nb[0] = stage[1 * stride + i];
@@ -304,6 +334,12 @@ struct RetraceFullOp : OpBase {
 #pragma unroll
         for (int k = 0; k < K; ++k) { o0[k] = A[k]; o1[k] = d[1][k] + A[k]; }
     }
+};
+
+// Full-form Retrace with the action axis staged in slices (axes too long for a chunk's whole
+// [steps, A] slices in LDS).
+struct RetraceFullSlicedOp : RetraceFullOp {
+    static constexpr bool kSliced = true;
 };
 
 // ---------------------------------------------------------------- TD(lambda) (Section 3.3.4)

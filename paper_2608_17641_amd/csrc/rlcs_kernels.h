@@ -88,6 +88,12 @@ __device__ __forceinline__ uint32_t draw_ticket(uint64_t* word, int64_t n_tiles,
     return ticket;
 }
 
+// Marks, in the workspace header's error word, a full-form Retrace call that met an action
+// outside [0, A) (value 2; the call takes that step's Q and pi as 0).
+__device__ __forceinline__ void report_bad_action(void* ws) {
+    st_relaxed(&reinterpret_cast<WsHeader*>(ws)->error, 2u);
+}
+
 __device__ __forceinline__ uint64_t* draw_word(void* ws, int64_t slot) {
     return reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) + sizeof(WsHeader) + slot * 64);
 }
@@ -581,15 +587,19 @@ struct Stager {
         // rows are 16-byte aligned whole blocks in LDS when A is a multiple of a block
         const bool rows16 = a.stage_vec && A % kPerBlock == 0;
         float v[J][Op::kStaged];
+        bool bad = false;
 #pragma unroll
         for (int j = 0; j < J; ++j) {
             const int64_t i = tid + int64_t(j) * nt;
             const int64_t st = chunk_lo + i;
 #pragma unroll
             for (int q = 0; q < Op::kStaged; ++q) v[j][q] = 0.f;
-            if (i <= E && st >= s_lo && st < s_hi)
+            if (i <= E && st >= s_lo && st < s_hi) {
                 Op::template reduce_step<DT>(sq + (st * A - e0), sp + (st * A - e0), A, rows16, act[j], mu[j], v[j]);
+                bad = bad || act[j] < 0 || act[j] >= A;
+            }
         }
+        if (bad && a.ws) report_bad_action(a.ws);
         // the slots overlay the slices: every slice read is done before any slot is written
         __syncthreads();
 #pragma unroll
@@ -599,6 +609,127 @@ struct Stager {
 #pragma unroll
             for (int q = 0; q < Op::kStaged; ++q) dyn[q * kStride + i] = v[j][q];
         }
+    }
+};
+
+// Staging for action axes too long for a chunk's whole [steps, A] slices in LDS: the axis is
+// taken in slices of a.A_slice actions (a multiple of 16 bytes of DT). For each slice, the
+// [staged steps, slice] blocks of Q and pi go to LDS (row stride = the slice's width: by
+// global_load_lds_dwordx4 when every row segment is whole aligned 16-byte blocks, element-wise
+// otherwise), and the owner thread of each step adds the slice's terms to its running sums:
+// E_pi Q over the actions in order (the same sequence of fused multiply-adds as one slice
+// holding the whole axis), and Q and pi of the taken action when it lies in the slice. A
+// barrier separates each slice's reads from the next slice's copies, and the last reads from
+// the slots, which overlay the slices as in Stager. The first slice is issued with the chunk's
+// other loads; the others follow one at a time.
+template <class Op, typename DT, int E, int J>
+struct SlicedStager {
+    static constexpr int64_t kPerBlock = 16 / int64_t(sizeof(DT));
+    static constexpr int kStride = E + 4;
+    int32_t act[J];
+    float mu[J];
+    float qa[J], ex[J], pa[J];
+    int64_t s_lo, s_hi;
+
+    // LDS elements of one array's slab of `As` actions (rounded up to whole 16-byte blocks).
+    __device__ static int64_t cap(int64_t As) {
+        return (int64_t(E + 1) * As + kPerBlock - 1) / kPerBlock * kPerBlock;
+    }
+
+    __device__ __forceinline__ void copy_slice(const Args& a, int64_t a0, int64_t aw, float* dyn) {
+        const int64_t A = a.A, rows = s_hi - s_lo;
+        const int nt = blockDim.x, tid = threadIdx.x;
+        DT* sq = reinterpret_cast<DT*>(dyn);
+        DT* sp = sq + cap(a.A_slice);
+        if (a.stage_vec && A % kPerBlock == 0 && aw % kPerBlock == 0) {
+            // a0 is a multiple of the slice width, itself a multiple of kPerBlock
+            const int64_t bpr = aw / kPerBlock, nblk = rows * bpr;
+            const u32x4* gq = reinterpret_cast<const u32x4*>(a.in[1]);
+            const u32x4* gp = reinterpret_cast<const u32x4*>(a.in[2]);
+            u32x4* lq = reinterpret_cast<u32x4*>(sq);
+            u32x4* lp = reinterpret_cast<u32x4*>(sp);
+            const int lane = tid & (kWave - 1);
+            for (int64_t b0 = tid - lane; b0 < nblk; b0 += nt) {
+                const int64_t b = b0 + lane;
+                if (b < nblk) {
+                    const int64_t row = b / bpr, cb = b - row * bpr;
+                    const int64_t g = ((s_lo + row) * A + a0) / kPerBlock + cb;
+                    __builtin_amdgcn_global_load_lds(gq + g, (__attribute__((address_space(3))) void*)(lq + b0), 16, 0, 0);
+                    __builtin_amdgcn_global_load_lds(gp + g, (__attribute__((address_space(3))) void*)(lp + b0), 16, 0, 0);
+                }
+            }
+        } else {
+            const DT* gq = reinterpret_cast<const DT*>(a.in[1]);
+            const DT* gp = reinterpret_cast<const DT*>(a.in[2]);
+            for (int64_t row = tid / aw, c = tid % aw; row < rows;) {
+                const int64_t g = (s_lo + row) * A + a0 + c;
+                sq[row * aw + c] = gq[g];
+                sp[row * aw + c] = gp[g];
+                c += nt;
+                row += c / aw;
+                c %= aw;
+            }
+        }
+    }
+
+    __device__ __forceinline__ void issue(const Args& a, int64_t chunk_lo, int64_t lo, float* dyn) {
+        const int64_t total = a.N * a.T;
+        const int nt = blockDim.x, tid = threadIdx.x;
+        s_lo = max(chunk_lo, lo);
+        s_hi = max(min(chunk_lo + E + 1, total), s_lo);
+#pragma unroll
+        for (int j = 0; j < J; ++j) {
+            const int64_t i = tid + int64_t(j) * nt;  // stage index
+            const int64_t st = chunk_lo + i;
+            const bool ok = i <= E && st >= s_lo && st < s_hi;
+            const int64_t sc = ok ? st : s_lo;
+            const int32_t act_raw = a.actions[sc];
+            const float mu_raw = load_one<DT>(a.in[3], sc);
+            act[j] = ok ? act_raw : -1;
+            mu[j] = ok ? mu_raw : 1.f;
+            qa[j] = ex[j] = pa[j] = 0.f;
+        }
+        copy_slice(a, 0, min(a.A_slice, a.A), dyn);
+    }
+
+    __device__ __forceinline__ void commit(const Args& a, int64_t chunk_lo, float* dyn) {
+        const int64_t A = a.A, As = a.A_slice;
+        const int nt = blockDim.x, tid = threadIdx.x;
+        const DT* sq = reinterpret_cast<const DT*>(dyn);
+        const DT* sp = sq + cap(As);
+        for (int64_t a0 = 0;;) {
+            const int64_t aw = min(As, A - a0);
+            // the LDS copies of this wave have landed; then every wave's have
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            __syncthreads();
+#pragma unroll
+            for (int j = 0; j < J; ++j) {
+                const int64_t i = tid + int64_t(j) * nt;
+                const int64_t st = chunk_lo + i;
+                if (i <= E && st >= s_lo && st < s_hi)
+                    Op::template accumulate_slice<DT>(sq + (st - s_lo) * aw, sp + (st - s_lo) * aw, a0, aw,
+                                                      act[j], ex[j], qa[j], pa[j]);
+            }
+            a0 += aw;
+            if (a0 >= A) break;
+            __syncthreads();  // every read of this slice is done before the next one lands
+            copy_slice(a, a0, min(As, A - a0), dyn);
+        }
+        // the slots overlay the slices: every slice read is done before any slot is written
+        __syncthreads();
+        bool bad = false;
+#pragma unroll
+        for (int j = 0; j < J; ++j) {
+            const int64_t i = tid + int64_t(j) * nt;
+            if (i > E) continue;
+            const int64_t st = chunk_lo + i;
+            const bool in = st >= s_lo && st < s_hi;
+            bad = bad || (in && (act[j] < 0 || act[j] >= A));
+            float v[Op::kStaged] = {in ? qa[j] : 0.f, in ? ex[j] : 0.f, in ? pa[j] / mu[j] : 0.f};
+#pragma unroll
+            for (int q = 0; q < Op::kStaged; ++q) dyn[q * kStride + i] = v[q];
+        }
+        if (bad && a.ws) report_bad_action(a.ws);
     }
 };
 
@@ -617,7 +748,9 @@ template <class Op, typename DT, int K, int W, bool VEC, bool TR, bool PAD = fal
 __global__ void __launch_bounds__(W * kWave) rows_kernel(Args a, int64_t rows_per_wg, int wave_local) {
     using C = Chunk<Op, DT, K, W, VEC, TR, PAD>;
     constexpr int64_t E = int64_t(W) * kWave * K;
-    using S = std::conditional_t<(Op::kStaged > 0), Stager<Op, DT, int(E), K + 1>,
+    using S = std::conditional_t<(Op::kStaged > 0),
+                                 std::conditional_t<Op::kSliced, SlicedStager<Op, DT, int(E), K + 1>,
+                                                    Stager<Op, DT, int(E), K + 1>>,
                                  NoStager<Op, DT, int(E), K + 1>>;
     __shared__ float s_a[W], s_b[W];
     __shared__ float s_carry;

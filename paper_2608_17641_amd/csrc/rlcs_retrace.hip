@@ -32,7 +32,7 @@ rlcs_status rlcs_retrace_full(const void* r, const void* q, const void* pi,
     rlcs_status st = check_common(N, T, dtype, {r, q, pi, mu, bv, boot}, {delta, q_ret});
     if (st != RLCS_OK) return st;
     if (!unit_interval(gamma) || !unit_interval(lambda) || !positive(c_bar)) return RLCS_ERR_INVALID_ARG;
-    if (A < 1 || A > kMaxActions) return RLCS_ERR_INVALID_ARG;
+    if (A < 1 || A > INT32_MAX) return RLCS_ERR_INVALID_ARG;
     if (N == 0 || T == 0) return RLCS_OK;
     if (N * T > INT64_MAX / A) return RLCS_ERR_INVALID_ARG;
     if (!r || !q || !pi || !actions || !mu || !delta || (trunc && !bv)) return RLCS_ERR_INVALID_ARG;
@@ -43,7 +43,11 @@ rlcs_status rlcs_retrace_full(const void* r, const void* q, const void* pi,
     a.stage_vec = (aligned(q, 16) && aligned(pi, 16)) ? 1 : 0;
     a.term = term; a.trunc = trunc; a.row_value = boot;
     a.out0 = delta; a.out1 = q_ret;
-    return dispatch<RetraceFullOp>(a, dtype, trunc != nullptr, ws, ws_bytes, stream);
+    // a workspace, if given, receives the out-of-range-action report in its error word
+    a.ws = (ws && ws_bytes >= sizeof(WsHeader) && aligned(ws, 64)) ? ws : nullptr;
+    if (A > kMaxActions)
+        return dispatch<RetraceFullSlicedOp>(a, dtype, trunc != nullptr, nullptr, 0, stream);
+    return dispatch<RetraceFullOp>(a, dtype, trunc != nullptr, nullptr, 0, stream);
 }
 
 }  // extern "C"

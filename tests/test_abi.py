@@ -135,7 +135,9 @@ def test_retrace_full_validation(lib):
         a.update(kw)
         return lib.rlcs_retrace_full(*a.values())
     assert rf(A=0) == n.RLCS_ERR_INVALID_ARG
-    assert rf(A=29) == n.RLCS_ERR_INVALID_ARG
+    assert rf(A=-5) == n.RLCS_ERR_INVALID_ARG
+    assert rf(A=2 ** 31) == n.RLCS_ERR_INVALID_ARG  # actions are int32
+    assert rf(N=2 ** 31, T=2 ** 20, A=2 ** 20) == n.RLCS_ERR_INVALID_ARG  # N*T*A overflows
     assert rf(act=None) == n.RLCS_ERR_INVALID_ARG
     assert rf(mu=None) == n.RLCS_ERR_INVALID_ARG
     assert rf(pi=None) == n.RLCS_ERR_INVALID_ARG

@@ -303,6 +303,45 @@ def test_retrace_full_shapes(A, T):
     assert_parity(out, ref, 1e-5, label=f"retrace_full A={A} T={T}")
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("A", [29, 30, 64, 100, 256])
+@pytest.mark.parametrize("T", [1, 33, 4097])
+def test_retrace_full_long_action_axes(A, T, dtype):
+    """More actions than a chunk's whole slices hold in LDS: the action axis staged in slices
+    (28 float32 / 24 bfloat16 actions at a time; A = 30 and 100 leave a partial last slice,
+    and an odd count of bfloat16 actions per row splits 16-byte blocks between rows)."""
+    N = 5 if T > 1000 else 23
+    ro = workloads.make_retrace_full(N, T, A, seed=A * 31 + T, dtype=dtype, p_term=0.05, p_trunc=0.05)
+    out, ref = _retrace_full_run(ro, c_bar=0.9)
+    assert_parity(out, ref, TOL[dtype], label=f"retrace_full A={A} T={T} {dtype}")
+
+
+@pytest.mark.parametrize("A", [5, 64])
+def test_retrace_full_reports_out_of_range_actions(A):
+    """An action outside [0, A) takes Q and pi as 0 at its step (as the oracle does) and sets
+    the workspace's error word to 2; a call without such actions leaves it at 0."""
+    ro = workloads.make_retrace_full(64, 100, A, seed=79 + A, p_term=0.05, p_trunc=0.05)
+    d = device_inputs(ro, DEV)
+    ws = torch.zeros(64, dtype=torch.uint8, device=DEV)
+    rl.rlcs_retrace_full(d["r"], d["q3"], d["pi3"], d["actions"], d["mu"], d["term"], d["trunc"],
+                         d["bv"], d["boot"], gamma=0.97, lam=0.9, ws=ws)
+    torch.cuda.synchronize()
+    assert int(ws[8:12].view(torch.int32).item()) == 0
+    act = ro["actions"].copy()
+    act[::3, ::7] = A
+    act[1::5, 2::9] = -3
+    d["actions"] = torch.from_numpy(act).to(DEV)
+    dl, qr = rl.rlcs_retrace_full(d["r"], d["q3"], d["pi3"], d["actions"], d["mu"], d["term"],
+                                  d["trunc"], d["bv"], d["boot"], gamma=0.97, lam=0.9, ws=ws)
+    torch.cuda.synchronize()
+    assert int(ws[8:12].view(torch.int32).item()) == 2
+    import oracle
+    rd, rq = oracle.retrace_full(ro["r"], ro["q3"], ro["pi3"], act, ro["mu"], ro["term"],
+                                 ro["trunc"], ro["bv"], ro["boot"], gamma=0.97, lam=0.9)
+    assert_parity({"delta": dl, "q_ret": qr}, {"delta": rd, "q_ret": rq}, 1e-5,
+                  label=f"out-of-range actions A={A}")
+
+
 @pytest.mark.parametrize("A", [4, 8, 18, 24])
 def test_retrace_full_bf16_and_plain(A):
     ro = workloads.make_retrace_full(300, 129, A, seed=A, dtype="bf16", p_term=0.05, p_trunc=0.05)
@@ -321,7 +360,7 @@ def _misaligned(t):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("A", [3, 4, 18])
+@pytest.mark.parametrize("A", [3, 4, 18, 40])
 def test_retrace_full_unaligned_slices(A, dtype):
     """Q and pi not 16-byte aligned: the slices are staged element-wise."""
     ro = workloads.make_retrace_full(37, 301, A, seed=5 + A, dtype=dtype, p_term=0.05, p_trunc=0.05)
