@@ -174,12 +174,26 @@ struct Chunk {
     Pair incl;     // lanes 0..lane of this wave composed (lane 0 innermost)
     Pair wave_in;  // waves between this wave and the chunk's carry-source edge
 
+    // Forward policies with a neighbour (the done flag of the step before), full chunks of
+    // several waves: lane 0 of a wave after the first does not read that flag from memory (a
+    // 128-byte line that the wave before streams past L2 as well). It builds its first step
+    // as if no flag cut it, every wave stores its last step's done flag in LDS with its map,
+    // and after the barrier a wave whose predecessor's last step is done scales the beta of
+    // its first step, of every lane's inclusive map and of its wave map by 0: the innermost
+    // beta only ever multiplies the beta part of a composition, so this equals building
+    // with it (bit for bit). `defer_chunk_`: the chunk defers; `defer_`: this wave does.
+    // Four-wave chunks only: with sixteen waves it made one-row-per-workgroup calls slower
+    // (eligibility traces 1024 x 4096 fp32 9.9 -> 12.8 us, 256 x 8192 6.6 -> 7.2), unexplained.
+    static constexpr bool kCanDefer = !kBack && Op::kNbr > 0 && Op::kStaged == 0 && !PAD && W == 4;
+    bool defer_chunk_ = false, defer_ = false;
+
     // Whether lane 0 must read the carry-source neighbour of its edge step from memory: only
     // if that step is in range and not a row edge (then the neighbour is in the same row,
-    // hence inside the array).
+    // hence inside the array), and the wave does not take it from LDS later.
     __device__ bool needs_nbr(int lane) const {
         const int ke = kBack ? K - 1 : 0;
-        return Op::kNbr > 0 && Op::kStaged == 0 && lane == 0 && bit(valid, ke) && !bit(edge, ke);
+        return Op::kNbr > 0 && Op::kStaged == 0 && lane == 0 && bit(valid, ke) && !bit(edge, ke) &&
+               !(kCanDefer && defer_);
     }
 
     // Staged slot s (Op::staged_index(s) >= 0) of the lane's K steps, from LDS.
@@ -366,7 +380,12 @@ struct Chunk {
     template <bool FULL, class BaseFn, class PreFn, class MidFn>
     __device__ void local_scan(const Args& a, int64_t chunk_lo, int64_t lo, int64_t hi,
                                float* s_a, float* s_b, int lane, int wave, bool wave_local,
-                               BaseFn&& base_of, const float* staged, PreFn&& pre, MidFn&& mid) {
+                               BaseFn&& base_of, const float* staged, PreFn&& pre, MidFn&& mid,
+                               float* s_d = nullptr) {
+        if constexpr (kCanDefer) {
+            defer_chunk_ = FULL && s_d != nullptr && !wave_local;
+            defer_ = defer_chunk_ && wave > 0;
+        }
         sidx = (wave * kWave + lane_group<kBack>(lane)) * K;
         p0 = chunk_lo + sidx;
         stage = staged;
@@ -416,16 +435,36 @@ struct Chunk {
             for (int k = 1; k < K; ++k) agg = compose(Pair{al[k], be[k]}, agg);
         }
         incl = wave_scan_inclusive(agg, lane);
-        if (!wave_local && lane == kWave - 1) { s_a[wave] = incl.a; s_b[wave] = incl.b; }
+        if (!wave_local && lane == kWave - 1) {
+            s_a[wave] = incl.a;
+            s_b[wave] = incl.b;
+            if constexpr (kCanDefer) {
+                if (defer_chunk_) s_d[wave] = bit(term | trunc, K - 1) ? 1.f : 0.f;
+            }
+        }
     }
 
-    // Step 5 (after the barrier): maps of the waves on this wave's carry-source side.
-    __device__ void wave_prefix(const float* s_a, const float* s_b, int wave) {
+    // Step 5 (after the barrier): maps of the waves on this wave's carry-source side (and, for
+    // a deferring chunk, the cut of each wave's first step by the flag before it).
+    __device__ void wave_prefix(const float* s_a, const float* s_b, int wave, const float* s_d = nullptr) {
         Pair acc = identity_pair();
         if (kBack) {
             for (int j = W - 1; j > wave; --j) acc = compose(Pair{s_a[j], s_b[j]}, acc);
         } else {
-            for (int j = 0; j < wave; ++j) acc = compose(Pair{s_a[j], s_b[j]}, acc);
+            // bit j: wave j's last step is done (one LDS read per lane, then scalar bit tests)
+            uint64_t done = 0;
+            if (kCanDefer && defer_chunk_) {
+                const int l = threadIdx.x & (kWave - 1);
+                done = __ballot(l < W && s_d[l < W ? l : 0] != 0.f);
+            }
+            for (int j = 0; j < wave; ++j) {
+                const bool cut = kCanDefer && j > 0 && ((done >> (j - 1)) & 1u);
+                acc = compose(Pair{s_a[j], cut ? 0.f : s_b[j]}, acc);
+            }
+            if (kCanDefer && defer_ && ((done >> (wave - 1)) & 1u)) {
+                incl.b = 0.f;
+                if ((threadIdx.x & (kWave - 1)) == 0) be[0] = 0.f;  // lane 0: the wave's first step
+            }
         }
         wave_in = acc;
     }
@@ -471,17 +510,17 @@ struct Chunk {
 // `carry_of`, the value entering the chunk; then the carry application and stores.
 template <bool FULL, class C, class BaseFn, class CarryFn, class PreFn, class MidFn>
 __device__ __forceinline__ float run_chunk(C& c, const Args& a, int64_t chunk_lo, int64_t lo,
-                                           int64_t hi, float* s_a, float* s_b, int lane,
-                                           int wave, bool wave_local, BaseFn&& base_of,
+                                           int64_t hi, float* s_a, float* s_b, float* s_d,
+                                           int lane, int wave, bool wave_local, BaseFn&& base_of,
                                            CarryFn&& carry_of, const float* staged, PreFn&& pre,
                                            MidFn&& mid) {
     c.template local_scan<FULL>(a, chunk_lo, lo, hi, s_a, s_b, lane, wave, wave_local, base_of,
-                                staged, pre, mid);
+                                staged, pre, mid, s_d);
     if (wave_local) {
         c.wave_in = identity_pair();
     } else {
         __syncthreads();
-        c.wave_prefix(s_a, s_b, wave);
+        c.wave_prefix(s_a, s_b, wave, s_d);
     }
     return c.template finish<FULL>(a, carry_of());
 }
@@ -753,6 +792,7 @@ __global__ void __launch_bounds__(W * kWave) rows_kernel(Args a, int64_t rows_pe
                                                     Stager<Op, DT, int(E), K + 1>>,
                                  NoStager<Op, DT, int(E), K + 1>>;
     __shared__ float s_a[W], s_b[W];
+    __shared__ float s_d[C::kCanDefer ? W : 1];
     __shared__ float s_carry;
     const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
     const int64_t row_lo = int64_t(blockIdx.x) * rows_per_wg;
@@ -775,8 +815,8 @@ __global__ void __launch_bounds__(W * kWave) rows_kernel(Args a, int64_t rows_pe
             auto mid = [&]() { if constexpr (Op::kStaged > 0) { sg.commit(a, chunk_lo, s_dyn); __syncthreads(); } };
             C c;
             const float first = (can_full && (PAD || (chunk_lo >= lo && chunk_hi <= hi)))
-                ? run_chunk<true>(c, a, chunk_lo, lo, hi, s_a, s_b, lane, wave, wave_local, base_of, carry_of, stage, pre, mid)
-                : run_chunk<false>(c, a, chunk_lo, lo, hi, s_a, s_b, lane, wave, wave_local, base_of, carry_of, stage, pre, mid);
+                ? run_chunk<true>(c, a, chunk_lo, lo, hi, s_a, s_b, s_d, lane, wave, wave_local, base_of, carry_of, stage, pre, mid)
+                : run_chunk<false>(c, a, chunk_lo, lo, hi, s_a, s_b, s_d, lane, wave, wave_local, base_of, carry_of, stage, pre, mid);
             if (chunk_lo <= lo) break;
             // the next chunk (earlier in time) continues from A at chunk_lo, held by lane 63 of
             // wave 0
@@ -793,8 +833,8 @@ __global__ void __launch_bounds__(W * kWave) rows_kernel(Args a, int64_t rows_pe
             auto mid = [&]() { if constexpr (Op::kStaged > 0) { sg.commit(a, chunk_lo, s_dyn); __syncthreads(); } };
             C c;
             const float last = (can_full && (PAD || (chunk_lo >= lo && chunk_lo + E <= hi)))
-                ? run_chunk<true>(c, a, chunk_lo, lo, hi, s_a, s_b, lane, wave, wave_local, base_of, carry_of, stage, pre, mid)
-                : run_chunk<false>(c, a, chunk_lo, lo, hi, s_a, s_b, lane, wave, wave_local, base_of, carry_of, stage, pre, mid);
+                ? run_chunk<true>(c, a, chunk_lo, lo, hi, s_a, s_b, s_d, lane, wave, wave_local, base_of, carry_of, stage, pre, mid)
+                : run_chunk<false>(c, a, chunk_lo, lo, hi, s_a, s_b, s_d, lane, wave, wave_local, base_of, carry_of, stage, pre, mid);
             if (chunk_lo + E >= hi) break;
             if (threadIdx.x == W * kWave - 1) s_carry = last;
             __syncthreads();
