@@ -517,7 +517,7 @@ def run_extra(dev, only=""):
         if label.startswith(only):
             run_retrace_full(label, n_, t_, a_, dev)
     for label, t_, n_ in (("tm_256x4096", 256, 4096), ("tm_4096x64", 4096, 64),
-                          ("tm_64x65536", 64, 65536)):
+                          ("tm_2048x128", 2048, 128), ("tm_64x65536", 64, 65536)):
         if label.startswith(only):
             run_time_major(label, t_, n_, dev)
     if "tm_noflags_16384x64".startswith(only):

@@ -642,9 +642,17 @@ __global__ void __launch_bounds__(W * kWave) cols_tiles_kernel(Args a, ColGeom g
 // layout of cols_narrow_kernel): up to four (two) times the workgroups of 64-column tiles for
 // calls of few, long columns, with the draw slots, records and look-back of cols_tiles_kernel
 // (per block of C columns); tiles of G * W * K steps. Grid: num_blocks * P workgroups.
+// With `dealt` set (the dispatcher sets it only when the whole grid is resident at once and P
+// is a multiple of 8), the tiles are dealt statically instead of drawn: workgroup b runs on XCD
+// x = b mod 8, and its r = b / 8 serves block r mod num_blocks at tile x * P/8 + r / num_blocks,
+// so each XCD takes a contiguous eighth of the tiles of every block. The blocks of one tile,
+// which share lines of data (two float32 blocks) and of flags (all the blocks of a flag row),
+// then run on one XCD, and each line is fetched by one L2; drawn in arrival order, they run on
+// different XCDs. A static order needs every workgroup resident, as a tile waits on the one
+// before it.
 template <class Op, typename DT, int K, int W, bool TR, bool LIFT, bool NT = true>
 __global__ void __launch_bounds__(W * kWave) cols_narrow_tiles_kernel(Args a, ColGeom g,
-                                                                      int64_t num_blocks) {
+                                                                      int64_t num_blocks, int dealt) {
     constexpr bool kBack = Op::kBackward;
     constexpr int C = narrow_cols<DT>();
     constexpr int G = kWave / C;
@@ -659,10 +667,11 @@ __global__ void __launch_bounds__(W * kWave) cols_narrow_tiles_kernel(Args a, Co
     const int col = lane % C, grp = lane / C;
     const int64_t T = a.T;
     const int64_t P = (T + L - 1) / L;
-    const int64_t block = int64_t(blockIdx.x) % num_blocks;
+    const int64_t r = int64_t(blockIdx.x) / 8;
+    const int64_t block = dealt ? r % num_blocks : int64_t(blockIdx.x) % num_blocks;
 
     if (threadIdx.x == 0) {
-        uint32_t gen;
+        uint32_t gen;  // dealt tiles draw too: the P-th draw moves the slot to the next generation
         s_ticket = draw_ticket(draw_word(a.ws, block), P, gen);
         s_tag = 2u * gen + 2u;
     }
@@ -670,12 +679,12 @@ __global__ void __launch_bounds__(W * kWave) cols_narrow_tiles_kernel(Args a, Co
     const uint32_t tag0 = s_tag;
     const uint32_t tag1 = tag0 + col_tag_n(g.J, sizeof(DT) == 4 ? 1 : 2) * kTagMix;
     if (wave == 0) advance_idle_slots(a.ws, num_blocks, (tag0 - 2u) / 2u, lane);
-    const int64_t ticket = s_ticket;
-    if (ticket >= P) {
+    if (s_ticket >= P) {
         // Only possible if the workspace was not zero-filled before first use.
         if (threadIdx.x == 0) st_relaxed(&hdr->error, 1u);
         return;
     }
+    const int64_t ticket = dealt ? int64_t(blockIdx.x % 8) * (P / 8) + r / num_blocks : int64_t(s_ticket);
     const int64_t p = kBack ? P - 1 - ticket : ticket;
     ColLane cl;
     cl.j = block * C + col;

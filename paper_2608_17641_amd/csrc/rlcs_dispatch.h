@@ -17,6 +17,16 @@
 namespace rlcs {
 namespace host {
 
+// Workgroups of `kernel` (with `threads` lanes) that the current device holds at once, or 0.
+template <class Kernel>
+int64_t resident_groups(Kernel kernel, int threads) {
+    int dev = 0, cus = 0, per_cu = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0) != hipSuccess) return 0;
+    return int64_t(cus) * per_cu;
+}
+
 // Waves per workgroup: 4 for rows of up to 4*64*K steps (several rows per workgroup), 16 for
 // longer rows (one row, or a 16*64*K-step tile of one, per workgroup).
 constexpr int kSmallWaves = 4;

@@ -20,16 +20,6 @@ constexpr size_t masked_ws_need(int64_t N) {
            sizeof(Moments) * (masked_rows(N) + (masked_rows(N) + kDirectPartials - 1) / kDirectPartials);
 }
 
-// Workgroups of `kernel` (with `threads` lanes) that the current device holds at once, or 0.
-template <class Kernel>
-int64_t resident_groups(Kernel kernel, int threads) {
-    int dev = 0, cus = 0, per_cu = 0;
-    if (hipGetDevice(&dev) != hipSuccess) return 0;
-    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0) != hipSuccess) return 0;
-    return int64_t(cus) * per_cu;
-}
-
 template <typename DT, bool VEC, bool TR, bool HM, bool STATS>
 void launch_masked(const MaskedArgs& ma, int waves, int64_t groups, int64_t rows_per_wg,
                    int wave_local, hipStream_t s) {

@@ -13,9 +13,9 @@ extern "C" {
  * workgroups (needs the workspace; calls of more than 1024 rows, or columns in more than 1024
  * blocks of 64, still run whole), 3 = column scans in narrow
  * groups (16 float32 or 32 bfloat16 columns per workgroup, whole columns; row-major calls as
- * with 0), 4 = column scans in narrow groups split across workgroups along T (needs the
- * workspace; at most 1024 groups and more than 64 steps, else as with 0; row-major calls as
- * with 0). Returns RLCS_ERR_INVALID_ARG for other values. */
+ * with 0), 4 = column scans in narrow groups split across workgroups along T, the tiles drawn
+ * in arrival order (needs the workspace; at most 1024 groups and more than 64 steps, else as
+ * with 0; row-major calls as with 0). Returns RLCS_ERR_INVALID_ARG for other values. */
 rlcs_status rlcs_testing_set_variant(int variant);
 
 #ifdef __cplusplus

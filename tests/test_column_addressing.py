@@ -213,6 +213,11 @@ def emulate_narrow_tiles(g, T, backward, esz, TL):
     lane, wave = np.arange(WAVE, dtype=I), np.arange(W, dtype=I)
     col, grp = lane % C, lane // C
     span = wave[:, None] * G + grp[None, :]
+    if P % 8 == 0:  # static dealing: workgroup b -> (block, ticket), onto every pair once
+        b = np.arange(groups * P, dtype=I)
+        r = b // 8
+        pairs = (r % groups) * P + ((b % 8) * (P // 8) + r // groups)
+        assert np.array_equal(np.sort(pairs), np.arange(groups * P, dtype=I))
     ticket = np.arange(P, dtype=I)
     p = (P - 1 - ticket) if backward else ticket
     for b0 in range(0, groups, 16):

@@ -285,6 +285,28 @@ def test_block_aggregates_with_rare_flags(dtype, v):
     assert_parity({"z": z}, {"z": zr}, TOL["f32"], label="block aggregates vector traces")
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("T,N", [(4096, 128), (1024, 64), (1024, 40), (8192, 64), (512, 7)])
+def test_narrow_split_dealt_tiles(T, N, dtype):
+    """Split narrow groups with the tiles dealt statically to XCDs, the automatic choice for these
+    shapes in float32 (a grid resident at once, a multiple of 8 tiles per group, 128-step tiles
+    or at most 16 tiles; ragged groups): every estimator against the oracle, and bitwise against
+    the same tiles drawn in arrival order (variant 4)."""
+    ro = workloads.make_rollout_time_major(T, N, seed=T + 3 * N, dtype=dtype, p_term=0.01,
+                                           p_trunc=0.01)
+    d = device_tm(ro)
+    ws = rl.make_workspace_columns(N, T, DEV)
+    for name in TM_ESTIMATORS:
+        dealt = {k: o.clone() for k, o in run_tm(name, d, ws=ws).items()}
+        with variant(4):
+            drawn = run_tm(name, d, ws=ws)
+        torch.cuda.synchronize()
+        for k in dealt:
+            assert torch.equal(dealt[k], drawn[k]), f"{name} {k}: dealt and drawn tiles differ"
+        assert_parity(dealt, ref_tm(name, ro), TOL[dtype], label=f"dealt {name} T={T} N={N} {dtype}")
+    assert int(ws[8:12].view(torch.int32).item()) == 0
+
+
 # ---------------------------------------------------------------- vector eligibility traces
 
 def run_vec(ro, *, trunc=True, ws=None):
