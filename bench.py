@@ -50,13 +50,13 @@ def algorithmic_bytes(N, T, *, dtype_bytes=4, trunc=True, boot=True, outputs=2):
 
 
 def eager_steps(warmup, steps, sets):
-    """Eager calls before the graph is captured: at least `warmup`, and enough that every set the
+    """Eager calls before the timed steps: at least `warmup`, and enough that every set the
     timed steps touch (set i % sets for i < steps) has been written by an eager call."""
     return max(warmup, min(steps, sets))
 
 
 def replay_check_set(steps, sets):
-    """The set whose advantages the first graph replay is compared with: the last one it writes."""
+    """The set whose advantages the timed steps are compared with: the last one they write."""
     return (steps - 1) % sets
 
 
@@ -92,9 +92,9 @@ def parse():
 
 def hold_stream(ms=2.0):
     """Holds the current stream with a spin kernel of about `ms` milliseconds, so that the host
-    has enqueued the timing events and the whole replayed graph behind it before the start event
-    fires: the timed region then holds the K steps' GPU work and not the host's submission of
-    the graph (with K = 20, that submission is a sizeable part of K steps)."""
+    has enqueued the timing events and every timed launch (or the replayed graph) behind it
+    before the start event fires: the timed region then holds the K steps' GPU work and not the
+    host's submission of them."""
     import torch
     torch.cuda._sleep(int(ms * 1e-3 * 2.4e9))
 
@@ -127,38 +127,67 @@ def probe_stream_call(lib, s, threads):
         raise RuntimeError(f"probe_stream_gae returned {rc}")
 
 
-def _graph_replay_us(fn, steps):
-    """Mean microseconds per call of `steps` calls fn(i) replayed from one graph (the same
-    protocol as the timed GAE steps)."""
+# Up to this many steps the timed calls are launched eagerly behind the spin; more are replayed
+# from one HIP graph. Measured on the GAE step (us per step, min-max of three; graph / eager):
+# K = 20: 5.65-6.14 / 5.54-5.58; K = 200: 5.25-5.28 / 5.47-5.50; K = 2000: 5.24 / 5.49. A graph
+# replay starts with about 8-12 us of fixed cost, which 20 steps do not amortise; an eager
+# launch costs about 0.25 us more per kernel than a graph node.
+EAGER_MAX_STEPS = 50
+
+
+def timing_protocol(steps):
+    """How `steps` timed calls are issued: 'eager' or 'graph'."""
+    return "eager" if steps <= EAGER_MAX_STEPS else "graph"
+
+
+def time_steps(fn, steps, start=None, end=None):
+    """Milliseconds for exactly `steps` calls fn(0) .. fn(steps - 1) on the current stream,
+    between two events recorded behind a spin kernel (see hold_stream): launched eagerly for
+    few steps, replayed from one HIP graph (captured and replayed once beforehand) for more."""
     import torch
-    g = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(g):
+    start = start or torch.cuda.Event(enable_timing=True)
+    end = end or torch.cuda.Event(enable_timing=True)
+    graph = None
+    if timing_protocol(steps) == "graph":
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            for i in range(steps):
+                fn(i)
+        graph.replay()
+    torch.cuda.synchronize()
+    # the spin outlasts the host's submission of every eager call (a Python call takes ~12 us)
+    hold_stream(2.0 + 0.05 * steps if graph is None else 2.0)
+    start.record()
+    if graph is None:
         for i in range(steps):
             fn(i)
-    g.replay()
+    else:
+        graph.replay()
+    end.record()
     torch.cuda.synchronize()
-    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    hold_stream()
-    a.record(); g.replay(); b.record()
-    torch.cuda.synchronize()
-    del g
-    return a.elapsed_time(b) * 1e3 / steps
+    del graph
+    return start.elapsed_time(end)
+
+
+def _per_step_us(fn, steps):
+    """Mean microseconds per call of `steps` calls timed as the GAE steps are."""
+    return time_steps(fn, steps) * 1e3 / steps
 
 
 def copy_reference(sets, steps):
     """The streaming ceiling at this size: probe_stream_gae over the same rotated sets as the
     GAE steps (22 B per step: the three data inputs and two flag arrays read, both outputs
     written, densely), in 64- and 256-lane workgroups, timed like the GAE steps; and the
-    empty-launch floor of the same graph replay."""
+    empty-launch floor, issued like the timed GAE steps."""
     lib = probe_lib()
     S = len(sets)
     for i in range(S):
         probe_stream_call(lib, sets[i], 64)
     out = {}
     for threads in (64, 256):
-        out[threads] = _graph_replay_us(lambda i: probe_stream_call(lib, sets[i % S], threads), steps)
+        out[threads] = _per_step_us(lambda i: probe_stream_call(lib, sets[i % S], threads), steps)
     import torch
-    empty = _graph_replay_us(lambda i: lib.probe_empty(torch.cuda.current_stream().cuda_stream), steps)
+    empty = _per_step_us(lambda i: lib.probe_empty(torch.cuda.current_stream().cuda_stream), steps)
     return out, empty
 
 
@@ -203,7 +232,7 @@ def cpu_baseline(ro, seconds):
 
 
 COPY_BYTES = 64 << 20
-KERNEL_TAG = "rows_kernel<rlcs::GaeOp, float, 4, 1, true, true, false>"
+KERNEL_TAG = "wave_rows_kernel<rlcs::GaeOp, float, 4, true>"
 COUNTERS_FILE = os.path.join(ROOT, "profiles", "gae_4096x256_f32_counters.md")
 
 
@@ -868,32 +897,21 @@ def main():
         if err > 1e-5 * (1 + float(np.max(np.abs(ref)))):
             raise SystemExit(f"parity failure before timing: max err {err}")
 
-    # Eager warm-up writes every set that the graph will replay into, so that the replay can be
-    # compared with an eager result of the same set.
+    # Eager warm-up writes every set that the timed steps write into, so that their result can
+    # be compared with an eager result of the same set.
     for i in range(eager_steps(args.warmup, args.steps, S)):
         step(i)
     torch.cuda.synchronize()
     check_set = replay_check_set(args.steps, S)
     eager_adv = sets[check_set]["adv"].clone()
 
-    # The timed steps are replayed from a HIP graph so that host-side launch cost (Python,
-    # ctypes) does not starve the GPU; each graph node is one rlcs_gae kernel launch.
-    graph = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(graph):
-        for i in range(args.steps):
-            step(i)
-    graph.replay()
-    torch.cuda.synchronize()
-    if not torch.equal(sets[check_set]["adv"], eager_adv):
-        raise SystemExit("graph replay differs from the eager launch")
+    # The timed steps: eager launches behind a spin kernel for few steps, a HIP graph replay for
+    # more (so that host-side launch cost, Python and ctypes, does not starve the GPU); each
+    # step is one rlcs_gae kernel launch either way.
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    hold_stream()
-    start.record()
-    graph.replay()
-    end.record()
-    torch.cuda.synchronize()
-    total_ms = start.elapsed_time(end)
+    total_ms = time_steps(step, args.steps, start, end)
+    if not torch.equal(sets[check_set]["adv"], eager_adv):
+        raise SystemExit("the timed steps' result differs from the eager launch")
     per_step_s = total_ms / 1e3 / args.steps
     nbytes = algorithmic_bytes(N, T)
     gbs = nbytes / per_step_s / 1e9
@@ -911,6 +929,9 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
+        "timing": f"{timing_protocol(args.steps)}: " + ("eager launches queued behind a spin kernel"
+                  if timing_protocol(args.steps) == "eager" else "one HIP graph replay") +
+                  ", HIP events on the launch stream around exactly K steps",
         "config": {"workload": f"GAE {N}x{T} fp32, term+trunc, bootstrap, cold HBM ({S} rotated input/output sets)",
                    "N": N, "T": T, "algorithmic_bytes": nbytes,
                    "gsteps_per_s": round(N * T / per_step_s / 1e9, 2),
@@ -941,7 +962,7 @@ def copy_context(nbytes, per_step_s, sets, args):
     return {
         "copy_reference": {"kernel": "probe_stream_gae (libprobe.so): r, v, bv, term, trunc read "
                                      "and adv, ret written densely, 22 B per step, non-temporal "
-                                     "16-byte vectors, same rotated sets, graph replay, cold",
+                                     "16-byte vectors, same rotated sets, timed like the GAE steps, cold",
                            "us_64_lanes": round(copies[64], 3), "us_256_lanes": round(copies[256], 3),
                            "us": round(copy_us, 3), "GB/s": round(nbytes / copy_us / 1e3, 1),
                            "frac_of_peak": round(nbytes / copy_us / 1e3 / PEAK_HBM_GBS, 4),
@@ -968,17 +989,7 @@ def context(step, nbytes, args, start, end):
     full_us = min(trials) * 1e3
     print(f"full-call (per-call events, min of 5 medians): {full_us:.2f} us", file=sys.stderr)
     # Warm (context only): every step on set 0, Infinity-Cache resident after the first.
-    wgraph = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(wgraph):
-        for _ in range(args.steps):
-            step(0)
-    wgraph.replay()
-    torch.cuda.synchronize()
-    hold_stream()
-    start.record(); wgraph.replay(); end.record()
-    torch.cuda.synchronize()
-    warm_us = start.elapsed_time(end) * 1e3 / args.steps
-    del wgraph
+    warm_us = time_steps(lambda i: step(0), args.steps, start, end) * 1e3 / args.steps
     print(f"warm (one set, Infinity-Cache resident): {warm_us:.3f} us = {nbytes / warm_us / 1e3:.1f} GB/s "
           f"effective", file=sys.stderr)
     return {

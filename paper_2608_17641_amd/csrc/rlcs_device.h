@@ -44,33 +44,35 @@ __device__ __forceinline__ Pair read_lane(Pair v, int lane) {
                 __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v.b), lane))};
 }
 
+// One Kogge-Stone step of the wave scan folded into two DPP-modified VALU operations: a lane
+// whose DPP source lane exists (and is written by the row mask) composes its map with the
+// source's map, the source inner: a += b * a_src, then b *= b_src. With bound_ctrl off, a lane
+// whose source does not exist is not written and keeps its map, as composing with the identity
+// would leave it. Each DPP read of a register a VALU operation wrote just before needs two wait
+// states, hence the s_nop 1 ahead of each.
+#define RLCS_DPP_STEP(v, CTRL)                                                             \
+    asm volatile("s_nop 1\n\tv_fmac_f32_dpp %0, %0, %1 " CTRL " bank_mask:0xf\n\t"        \
+                 "s_nop 1\n\tv_mul_f32_dpp %1, %1, %1 " CTRL " bank_mask:0xf"               \
+                 : "+v"(v.a), "+v"(v.b))
+
 // Inclusive prefix scan of per-lane maps over the 64 lanes (lane l ends with lanes 0..l
-// composed, lane 0 innermost). Kogge-Stone inside each row of 16 lanes with DPP row shifts
-// (4 steps), then the three row totals are read into scalars and composed onto the rows
-// after them. No LDS traffic; the same tree as the Hillis-Steele trace of Appendix A inside a
-// row.
+// composed, lane 0 innermost): Kogge-Stone inside each row of 16 lanes with DPP row shifts
+// (4 steps, the tree of the Hillis-Steele trace of Appendix A), then two row broadcasts carry
+// the row totals onto the rows after them. Twelve VALU operations, no LDS, no lane reads;
+// moving the source maps into registers first (with the identity where a source is missing)
+// and reading the row totals into scalars took 39.
 __device__ __forceinline__ Pair wave_scan_inclusive(Pair v, int lane) {
-#define RLCS_ROW_STEP(S)                                                                 \
-    {                                                                                    \
-        const Pair o{dpp_move<kDppRowShr + S>(0.f, v.a), dpp_move<kDppRowShr + S>(1.f, v.b)}; \
-        v = compose(v, o);                                                               \
-    }
-    RLCS_ROW_STEP(1)
-    RLCS_ROW_STEP(2)
-    RLCS_ROW_STEP(4)
-    RLCS_ROW_STEP(8)
-#undef RLCS_ROW_STEP
-    const Pair t0 = read_lane(v, 15), t1 = read_lane(v, 31), t2 = read_lane(v, 47);
-    const Pair p1 = t0;
-    const Pair p2 = compose(t1, p1);
-    const Pair p3 = compose(t2, p2);
-    const int row = lane >> 4;
-    if (row > 0) {
-        const Pair p = (row == 1) ? p1 : ((row == 2) ? p2 : p3);
-        v = compose(v, p);
-    }
+    (void)lane;
+    RLCS_DPP_STEP(v, "row_shr:1 row_mask:0xf");
+    RLCS_DPP_STEP(v, "row_shr:2 row_mask:0xf");
+    RLCS_DPP_STEP(v, "row_shr:4 row_mask:0xf");
+    RLCS_DPP_STEP(v, "row_shr:8 row_mask:0xf");
+    // rows 1 and 3 take lane 15 of the row before; then rows 2 and 3 take lane 31
+    RLCS_DPP_STEP(v, "row_bcast:15 row_mask:0xa");
+    RLCS_DPP_STEP(v, "row_bcast:31 row_mask:0xc");
     return v;
 }
+#undef RLCS_DPP_STEP
 
 // ------------------------------------------------------------------ element loads / stores
 

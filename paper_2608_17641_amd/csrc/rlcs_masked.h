@@ -49,13 +49,6 @@ __device__ __forceinline__ AW apply(const Tri& m, AW x) {
     return AW{fmaf(m.p, x.A, fmaf(m.q, x.W, m.ca)), fmaf(m.s, x.W, m.cw)};
 }
 
-template <int S>
-__device__ __forceinline__ Tri tri_row_shr(const Tri& v) {
-    return Tri{dpp_move<kDppRowShr + S>(1.f, v.p), dpp_move<kDppRowShr + S>(0.f, v.q),
-               dpp_move<kDppRowShr + S>(1.f, v.s), dpp_move<kDppRowShr + S>(0.f, v.ca),
-               dpp_move<kDppRowShr + S>(0.f, v.cw)};
-}
-
 __device__ __forceinline__ float readlane_f(float v, int lane) {
     return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
 }
@@ -65,19 +58,38 @@ __device__ __forceinline__ Tri read_lane(const Tri& v, int lane) {
                readlane_f(v.ca, lane), readlane_f(v.cw, lane)};
 }
 
-// Inclusive prefix scan of per-lane maps over the 64 lanes, as wave_scan_inclusive for pairs.
+// One Kogge-Stone step on triangular maps with DPP-modified VALU operations, as for pairs
+// (wave_scan_inclusive in the device header): a lane whose DPP source exists composes its map
+// (outer) with the source's map (inner); the others are not written and keep theirs. Every
+// component of the source is read before the source lane overwrites it, so q and ca are first
+// copied: q' = q s_src + p q_src, ca' = ca + q cw_src + p ca_src, cw' = cw + s cw_src,
+// s' = s s_src, p' = p p_src, in that order.
+#define RLCS_TRI_DPP_STEP(v, CTRL)                                                            \
+    {                                                                                         \
+        float tq = v.q, tca = v.ca;                                                           \
+        asm volatile("s_nop 1\n\tv_mul_f32_dpp %1, %2, %1 " CTRL " bank_mask:0xf\n\t"         \
+                     "s_nop 1\n\tv_fmac_f32_dpp %1, %5, %0 " CTRL " bank_mask:0xf\n\t"        \
+                     "s_nop 1\n\tv_fmac_f32_dpp %3, %4, %5 " CTRL " bank_mask:0xf\n\t"        \
+                     "s_nop 1\n\tv_fmac_f32_dpp %3, %6, %0 " CTRL " bank_mask:0xf\n\t"        \
+                     "s_nop 1\n\tv_fmac_f32_dpp %4, %4, %2 " CTRL " bank_mask:0xf\n\t"        \
+                     "s_nop 1\n\tv_mul_f32_dpp %2, %2, %2 " CTRL " bank_mask:0xf\n\t"         \
+                     "s_nop 1\n\tv_mul_f32_dpp %0, %0, %0 " CTRL " bank_mask:0xf"               \
+                     : "+v"(v.p), "+v"(v.q), "+v"(v.s), "+v"(v.ca), "+v"(v.cw), "+v"(tq), "+v"(tca)); \
+    }
+
+// Inclusive prefix scan of per-lane maps over the 64 lanes, as wave_scan_inclusive for pairs:
+// four row shifts, then the row broadcasts of lanes 15 and 31.
 __device__ __forceinline__ Tri wave_scan_inclusive(Tri v, int lane) {
-    v = compose(v, tri_row_shr<1>(v));
-    v = compose(v, tri_row_shr<2>(v));
-    v = compose(v, tri_row_shr<4>(v));
-    v = compose(v, tri_row_shr<8>(v));
-    const Tri t0 = read_lane(v, 15), t1 = read_lane(v, 31), t2 = read_lane(v, 47);
-    const Tri p2 = compose(t1, t0);
-    const Tri p3 = compose(t2, p2);
-    const int row = lane >> 4;
-    if (row > 0) v = compose(v, (row == 1) ? t0 : ((row == 2) ? p2 : p3));
+    (void)lane;
+    RLCS_TRI_DPP_STEP(v, "row_shr:1 row_mask:0xf")
+    RLCS_TRI_DPP_STEP(v, "row_shr:2 row_mask:0xf")
+    RLCS_TRI_DPP_STEP(v, "row_shr:4 row_mask:0xf")
+    RLCS_TRI_DPP_STEP(v, "row_shr:8 row_mask:0xf")
+    RLCS_TRI_DPP_STEP(v, "row_bcast:15 row_mask:0xa")
+    RLCS_TRI_DPP_STEP(v, "row_bcast:31 row_mask:0xc")
     return v;
 }
+#undef RLCS_TRI_DPP_STEP
 
 // Value of lane l-1 (lane 0 receives `fill`).
 __device__ __forceinline__ AW shift_up1(AW v, AW fill) {

@@ -96,10 +96,19 @@ def test_bench_refuses_more_than_one_gpu():
 @pytest.mark.parametrize("steps,warmup,sets", [(20, 5, 32), (2000, 200, 32), (1, 0, 32), (5, 100, 32),
                                                (64, 5, 32), (33, 0, 32), (7, 3, 1)])
 def test_replay_check_set_was_written_eagerly(steps, warmup, sets):
-    """The graph replay is compared with the eager result of the same set: that set must be one
-    the eager calls before capture wrote (the driver's --steps 20 --warmup 5 among them)."""
+    """The timed steps' result is compared with the eager result of the same set: that set must be
+    one the eager calls before timing wrote (the driver's --steps 20 --warmup 5 among them)."""
     eager = {i % sets for i in range(bench.eager_steps(warmup, steps, sets))}
     replayed = {i % sets for i in range(steps)}
     assert replayed <= eager
     assert bench.replay_check_set(steps, sets) in eager
     assert bench.eager_steps(warmup, steps, sets) >= warmup
+
+
+def test_timing_protocol():
+    """Few timed steps are launched eagerly behind the spin (a graph replay's fixed start-up cost
+    is not amortised by them), many are replayed from one graph."""
+    assert bench.timing_protocol(20) == "eager"
+    assert bench.timing_protocol(bench.EAGER_MAX_STEPS) == "eager"
+    assert bench.timing_protocol(bench.EAGER_MAX_STEPS + 1) == "graph"
+    assert bench.timing_protocol(2000) == "graph"

@@ -30,6 +30,7 @@ def test_bench_driver_command():
         assert key in out, key
     assert out["n_gpus"] == 1 and out["steps"] == 20 and out["warmup"] == 5
     assert out["dtype"] == "f32" and out["unit"] == "GB/s" and out["higher_is_better"] is True
+    assert out["timing"].startswith("eager")
     assert out["config"]["workload"].startswith("GAE 4096x256 fp32")
     assert out["config"]["N"] == 4096 and out["config"]["T"] == 256
     rf = out["roofline"]
