@@ -75,6 +75,9 @@ def parse():
     ap.add_argument("--extra", action="store_true",
                     help="time every estimator of every workload (table on stderr, no JSON line)")
     ap.add_argument("--only", default="", help="with --extra: only workloads whose label starts so")
+    ap.add_argument("--variant", type=int, default=0,
+                    help="with --extra: force a kernel variant through the library's test hook "
+                         "(rlcs_testing_set_variant; 1 = whole rows and two-pass whitening)")
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="print the counter summary of two rocprofv3 --pmc runs and exit")
     ap.add_argument("--summarize-trace", metavar="TRACE_DIR",
@@ -852,6 +855,8 @@ def main():
     if args.extra:
         if args.profile_pass:
             _PROFILE["on"] = True
+        if args.variant:
+            rl.testing_set_variant(args.variant)
         run_extra(dev, args.only)
         if args.profile_pass:
             src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device=dev)

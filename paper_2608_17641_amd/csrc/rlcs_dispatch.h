@@ -46,6 +46,9 @@ constexpr int kStagedWaves = 1;
 constexpr int kStagedMidWaves = 2;
 constexpr int64_t kStagedLdsBudget = 64 * 1024;
 constexpr int64_t kStagedMidLdsBudget = 80 * 1024;
+// LDS of a sliced chunk (long action axes, one wave): room for slices of one whole 128-byte line
+// of float32 actions (two slabs of 257 x 32 elements, 65.8 KB), two workgroups per CU.
+constexpr int64_t kSlicedLdsBudget = 80 * 1024;
 
 // Steps per lane: one 16-byte vector of each input.
 template <typename DT> struct Width;
@@ -184,8 +187,15 @@ constexpr int64_t sliced_cap(int W, int64_t As) {
 }
 template <typename DT>
 constexpr int64_t sliced_width(int W, int64_t budget) {
+    // whole 128-byte lines of actions when one fits: a slice that ends inside a line leaves the
+    // rest of that line to the next slice, which fetched it again from HBM (float32, A = 64 and
+    // 256: 1.96 and 1.99 times the algorithmic bytes with 28-action slices)
+    const int64_t per_line = 128 / int64_t(sizeof(DT));
+    int64_t As = 0;
+    while (2 * sliced_cap<DT>(W, As + per_line) * int64_t(sizeof(DT)) <= budget) As += per_line;
+    if (As > 0) return As;
     const int64_t per_block = 16 / int64_t(sizeof(DT));
-    int64_t As = per_block;
+    As = per_block;
     while (2 * sliced_cap<DT>(W, As + per_block) * int64_t(sizeof(DT)) <= budget) As += per_block;
     return As;
 }
@@ -225,7 +235,7 @@ rlcs_status dispatch_dt(Args& a, bool has_trunc, void* ws, size_t ws_bytes, hipS
         // Long action axes: one-wave workgroups, the widest slice that fits the LDS budget.
         p.split = false;
         p.waves = kStagedWaves;
-        a.A_slice = sliced_width<DT>(kStagedWaves, kStagedLdsBudget);
+        a.A_slice = sliced_width<DT>(kStagedWaves, kSlicedLdsBudget);
         p.lds_bytes = size_t(sliced_lds_bytes<Op, DT>(kStagedWaves, a.A_slice));
     } else if constexpr (Op::kStaged > 0) {
         // Staged policies keep whole rows in one workgroup (chunk loop for long rows).

@@ -652,8 +652,9 @@ struct Stager {
 };
 
 // Staging for action axes too long for a chunk's whole [steps, A] slices in LDS: the axis is
-// taken in slices of a.A_slice actions (a multiple of 16 bytes of DT). For each slice, the
-// [staged steps, slice] blocks of Q and pi go to LDS (row stride = the slice's width: by
+// taken in slices of a.A_slice actions (whole 128-byte lines of DT where one fits, else a
+// multiple of 16 bytes). For each slice, the [staged steps, slice] blocks of Q and pi go to
+// LDS (row stride = the slice's width: by
 // global_load_lds_dwordx4 when every row segment is whole aligned 16-byte blocks, element-wise
 // otherwise), and the owner thread of each step adds the slice's terms to its running sums:
 // E_pi Q over the actions in order (the same sequence of fused multiply-adds as one slice
