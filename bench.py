@@ -2,6 +2,7 @@
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu]
     python bench.py --extra                      # every workload, table on stderr
+    python bench.py --probe-sweep                # streaming probe launch shapes beside the GAE step
 
 Workload: GAE over a 4096 x 256 float32 rollout buffer with termination and truncation flags,
 truncation continuations and per-row bootstraps (seeded synthetic data). One step is one call
@@ -75,6 +76,9 @@ def parse():
     ap.add_argument("--extra", action="store_true",
                     help="time every estimator of every workload (table on stderr, no JSON line)")
     ap.add_argument("--only", default="", help="with --extra: only workloads whose label starts so")
+    ap.add_argument("--probe-sweep", action="store_true",
+                    help="time the streaming probe in several launch shapes beside the GAE step on "
+                         "the headline sets (a table on stdout) and exit")
     ap.add_argument("--variant", type=int, default=0,
                     help="with --extra: force a kernel variant through the library's test hook "
                          "(rlcs_testing_set_variant; 1 = whole rows and two-pass whitening)")
@@ -115,6 +119,9 @@ def probe_lib():
     lib.probe_stream_gae.restype = ctypes.c_int
     lib.probe_empty.argtypes = [P]
     lib.probe_empty.restype = ctypes.c_int
+    lib.probe_stream_gae_shape.argtypes = [P] * 7 + [ctypes.c_int64, ctypes.c_int, ctypes.c_int,
+                                                     ctypes.c_int64, ctypes.c_int, P]
+    lib.probe_stream_gae_shape.restype = ctypes.c_int
     return lib
 
 
@@ -192,6 +199,55 @@ def copy_reference(sets, steps):
     import torch
     empty = _per_step_us(lambda i: lib.probe_empty(torch.cuda.current_stream().cuda_stream), steps)
     return out, empty
+
+
+# Launch shapes of the streaming probe timed by --probe-sweep: (label, lanes per workgroup,
+# vectors per lane, persistent grid size or 0, dependent continuation loads).
+PROBE_SHAPES = [
+    ("64 lanes, 1 vector/lane", 64, 1, 0, 0),
+    ("64 lanes, 1 vector/lane, dependent bv", 64, 1, 0, 1),
+    ("256 lanes, 1 vector/lane", 256, 1, 0, 0),
+    ("256 lanes, 1 vector/lane, dependent bv", 256, 1, 0, 1),
+    ("64 lanes, 2 vectors/lane", 64, 2, 0, 0),
+    ("64 lanes, 2 vectors/lane, dependent bv", 64, 2, 0, 1),
+    ("64 lanes, 4 vectors/lane", 64, 4, 0, 0),
+    ("256 lanes, 2 vectors/lane", 256, 2, 0, 0),
+    ("persistent 1024 x 64 lanes", 64, 1, 1024, 0),
+    ("persistent 2048 x 64 lanes", 64, 1, 2048, 0),
+    ("persistent 512 x 256 lanes", 256, 1, 512, 0),
+    ("persistent 1024 x 256 lanes", 256, 1, 1024, 0),
+]
+
+
+def probe_sweep(step, sets, steps):
+    """The GAE step, the streaming probe in every PROBE_SHAPES launch shape, and the empty launch,
+    each timed like the headline (`steps` calls over the rotated sets, cold); GB/s counts GAE's
+    algorithmic bytes for every row."""
+    import torch
+    lib = probe_lib()
+    S = len(sets)
+    nbytes = algorithmic_bytes(N, T)
+    rows = [("rlcs_gae", _per_step_us(step, steps))]
+    for label, threads, per_lane, groups, dep in PROBE_SHAPES:
+        def call(i, threads=threads, per_lane=per_lane, groups=groups, dep=dep):
+            s = sets[i % S]
+            rc = lib.probe_stream_gae_shape(s["r"].data_ptr(), s["v"].data_ptr(), s["bv"].data_ptr(),
+                                            s["term"].data_ptr(), s["trunc"].data_ptr(),
+                                            s["adv"].data_ptr(), s["ret"].data_ptr(), s["r"].numel(),
+                                            threads, per_lane, groups, dep,
+                                            torch.cuda.current_stream().cuda_stream)
+            if rc != 0:
+                raise RuntimeError(f"probe_stream_gae_shape returned {rc}")
+        for i in range(S):
+            call(i)
+        rows.append((f"probe: {label}", _per_step_us(call, steps)))
+    rows.append(("empty launch", _per_step_us(
+        lambda i: lib.probe_empty(torch.cuda.current_stream().cuda_stream), steps)))
+    print(f"# GAE {N}x{T} fp32 sets, {steps} steps per row ({timing_protocol(steps)}), cold; "
+          f"GB/s = {nbytes} B / time")
+    for label, us in rows:
+        print(f"{label:<48} {us:8.3f} us {nbytes / us / 1e3:8.1f} GB/s {100 * nbytes / us / 1e3 / PEAK_HBM_GBS:6.1f} %",
+              flush=True)
 
 
 def cpu_baseline(ro, seconds):
@@ -892,6 +948,11 @@ def main():
 
     if args.profile_pass:
         profile_pass(step, args, dev)
+        return
+    if args.probe_sweep:
+        for i in range(S):
+            step(i)
+        probe_sweep(step, sets, args.steps)
         return
 
     # parity of the timed configuration before timing

@@ -112,3 +112,22 @@ def test_timing_protocol():
     assert bench.timing_protocol(bench.EAGER_MAX_STEPS) == "eager"
     assert bench.timing_protocol(bench.EAGER_MAX_STEPS + 1) == "graph"
     assert bench.timing_protocol(2000) == "graph"
+
+
+def test_probe_library_rejects_bad_shapes():
+    """The streaming probe's argument checks run before any HIP call (no GPU needed): every
+    combination outside the supported shapes returns 1."""
+    import ctypes
+    import os
+    from paper_2608_17641_amd.build import PROBE_LIB
+    if not os.path.exists(PROBE_LIB):
+        pytest.skip("libprobe.so not built")
+    lib = bench.probe_lib()
+    fake = [ctypes.c_void_p(0x10000 * (k + 1)) for k in range(7)]  # 16-byte aligned, never dereferenced
+    n = 4096
+    for threads, per_lane, groups, dep in ((128, 1, 0, 0), (64, 3, 0, 0), (64, 2, 512, 0),
+                                           (64, 1, 512, 1), (64, 1, -1, 0), (64, 1, 0, 2)):
+        assert lib.probe_stream_gae_shape(*fake, n, threads, per_lane, groups, dep, None) == 1
+    assert lib.probe_stream_gae_shape(*fake, 4098, 64, 1, 0, 0, None) == 1   # not whole vectors
+    assert lib.probe_stream_gae_shape(None, *fake[1:], n, 64, 1, 0, 0, None) == 1
+    assert lib.probe_stream_gae_shape(*fake, 0, 64, 1, 0, 0, None) == 0      # nothing to stream
