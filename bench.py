@@ -296,12 +296,12 @@ COUNTERS_FILE = os.path.join(ROOT, "profiles", "gae_4096x256_f32_counters.md")
 
 
 def kernel_source_hash():
-    """sha256 over the HIP sources of the library (kernels and launch code) and the build script
-    that holds the compiler flags."""
+    """sha256 over the HIP sources of the library (kernels and launch code; not the measurement
+    probe built beside it) and the build script that holds the compiler flags."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2608_17641_amd", "csrc")
     for name in sorted(os.listdir(csrc)):
-        if name.endswith((".h", ".hip")):
+        if name.startswith("rlcs_") and name.endswith((".h", ".hip")):
             with open(os.path.join(csrc, name), "rb") as f:
                 h.update(name.encode() + b"\0" + f.read())
     with open(os.path.join(ROOT, "paper_2608_17641_amd", "build.py"), "rb") as f:
