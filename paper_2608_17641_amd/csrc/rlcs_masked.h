@@ -532,9 +532,10 @@ __device__ __forceinline__ void get_tagged(const uint64_t* w, uint32_t tag, doub
         }
         for (int i = 0; i < pause; ++i) __builtin_amdgcn_s_sleep(2);
         pause = min(2 * pause, 4);
+        // every word again, all loads in flight together: a word that already carried the tag
+        // carries it still (each word of a record is written once per call)
 #pragma unroll
-        for (int i = 0; i < 2 * M; ++i)
-            if (uint32_t(x[i] >> 32) != tag) x[i] = ld_relaxed(w + i);
+        for (int i = 0; i < 2 * M; ++i) x[i] = ld_relaxed(w + i);
     }
 #pragma unroll
     for (int i = 0; i < M; ++i)
