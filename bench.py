@@ -291,7 +291,7 @@ def cpu_baseline(ro, seconds):
 
 
 COPY_BYTES = 64 << 20
-KERNEL_TAG = "wave_rows_kernel<rlcs::GaeOp, float, 4, true>"
+KERNEL_TAG = "wave_rows_kernel<rlcs::GaeOp, float, 4, true, 4>"
 COUNTERS_FILE = os.path.join(ROOT, "profiles", "gae_4096x256_f32_counters.md")
 
 

@@ -855,18 +855,20 @@ __global__ void __launch_bounds__(W * kWave) rows_kernel(Args a, int64_t rows_pe
 // issued back to back, the continuation vector follows only where a step is truncated, then
 // Table 1's coefficients, the lane's serial map, the DPP wave scan and the stores. Lanes past
 // the array's end (its last wave may be partial; N*T is a multiple of K) load step 0 of row
-// 0 and store nothing. Grid: ceil(N*T / (64*K)) workgroups of one wave.
-template <class Op, typename DT, int K, bool TR>
-__global__ void __launch_bounds__(kWave) wave_rows_kernel(Args a, int log2T) {
+// 0 and store nothing. The WPG waves of a workgroup take consecutive wave spans, each on its
+// own (no LDS, no barrier). Grid: ceil(N*T / (64*K*WPG)) workgroups of WPG waves.
+template <class Op, typename DT, int K, bool TR, int WPG = 1>
+__global__ void __launch_bounds__(WPG * kWave) wave_rows_kernel(Args a, int log2T) {
     static_assert(Op::kStaged == 0, "staged policies run on the rows kernel");
     constexpr bool kBack = Op::kBackward;
     constexpr int NS = Op::kSlots;
     constexpr int NB = Op::kNbr > 0 ? Op::kNbr : 1;
     constexpr int kWords = K * int(sizeof(DT)) / 4;
     constexpr int kTS = TR ? Op::kTruncSlot : -1;
-    const int lane = threadIdx.x;
+    const int lane = threadIdx.x & (kWave - 1);
     const int64_t T = a.T;
-    const int64_t p0 = int64_t(blockIdx.x) * (kWave * K) + int64_t(lane_group<kBack>(lane)) * K;
+    const int64_t p0 = (int64_t(blockIdx.x) * WPG + threadIdx.x / kWave) * (kWave * K) +
+                       int64_t(lane_group<kBack>(lane)) * K;
     const bool live = p0 < a.N * T;
     const int64_t pc = live ? p0 : 0;
     const uint8_t* fallback = reinterpret_cast<const uint8_t*>(a.in[0]);
