@@ -36,13 +36,15 @@ constexpr int kLargeWaves = 16;
 // 5.76 -> 5.68 us, eligibility traces 3.45 -> 3.38 us, bf16 GAE 16384 x 512 25.6 -> 25.1 us);
 // V-Trace, Retrace and TD(lambda) ran 2-7 % slower so and keep four-wave workgroups.
 // Wave-rows calls of float32 GAE with truncation take workgroups of four waves (each wave still
-// on its own) up to this many steps, one wave per workgroup beyond. Measured (C harness, cold,
-// one-wave against four-wave workgroups): 4096 x 256 5.21 -> 4.78 us, 8192 x 128 5.20 -> 4.85,
-// 16384 x 64 5.23 -> 4.91, 4096 x 128 3.55 -> 3.49, 2048 x 256 3.53 -> 3.49, 1024 x 256 3.00 ->
-// 2.92, 512 x 256 2.57 -> 2.59; above 2^20 steps four waves lose 4-8 % (6144 x 256 6.17 -> 6.68,
-// 16384 x 256 14.6 -> 15.3), and so they do without truncation (4096 x 256 4.29 -> 4.46), for
-// bfloat16 (16384 x 64 4.69 -> 4.92) and for V-Trace (4096 x 256 6.03 -> 6.16). Two waves per
-// workgroup lost everywhere, eight gained less than four.
+// on its own) from 2^18 to 2^20 steps (1024 to 4096 waves), one wave per workgroup otherwise.
+// Measured (C harness, cold, one-wave against four-wave workgroups): 4096 x 256 5.21 -> 4.78 us,
+// 8192 x 128 5.20 -> 4.85, 16384 x 64 5.23 -> 4.91, 4096 x 128 3.55 -> 3.49, 2048 x 256 3.53 ->
+// 3.49, 1024 x 256 3.00 -> 2.92; with fewer waves the four-wave grid leaves CUs idle (512 x 256
+// 2.57 -> 2.59, 4096 x 32 2.59 -> 2.70); above 2^20 steps four waves lose 4-8 % (6144 x 256 6.17
+// -> 6.68, 16384 x 256 14.6 -> 15.3), and so they do without truncation (4096 x 256 4.29 ->
+// 4.46), for bfloat16 (16384 x 64 4.69 -> 4.92) and for V-Trace (4096 x 256 6.03 -> 6.16). Two
+// waves per workgroup lost everywhere, eight gained less than four.
+constexpr int64_t kWaveRowsQuadMinSteps = int64_t(1) << 18;
 constexpr int64_t kWaveRowsQuadSteps = int64_t(1) << 20;
 template <class Op, typename DT, bool TR> struct WaveRowsQuads : std::false_type {};
 template <> struct WaveRowsQuads<GaeOp, float, true> : std::true_type {};
@@ -147,7 +149,7 @@ rlcs_status launch(const Args& a, const Plan& p, hipStream_t stream) {
             constexpr int64_t span = int64_t(kWave) * Width<DT>::K;
             const int64_t waves = (a.N * a.T + span - 1) / span;
             if constexpr (WaveRowsQuads<Op, DT, TR>::value) {
-                if (a.N * a.T <= kWaveRowsQuadSteps) {
+                if (a.N * a.T >= kWaveRowsQuadMinSteps && a.N * a.T <= kWaveRowsQuadSteps) {
                     hipLaunchKernelGGL((wave_rows_kernel<Op, DT, Width<DT>::K, TR, 4>),
                                        dim3(unsigned((waves + 3) / 4)), dim3(4 * kWave), 0, stream, a,
                                        p.wave_rows_log2T);
