@@ -556,6 +556,7 @@ def run_extra(dev, only=""):
     seven = tuple(EXTRA_EST)
     plan.append(("all7_4096x32", 4096, 32, "f32", dict(p_term=0.02, p_trunc=0.01), True, True, 0.99, 0.95, seven))
     plan.append(("4096x256", 4096, 256, "f32", dict(p_term=0.02, p_trunc=0.01), True, True, 0.99, 0.95, ("gae", "vtrace")))
+    plan.append(("4096x256_plain", 4096, 256, "f32", dict(p_term=0.02, p_trunc=0.0), False, True, 0.99, 0.95, ("gae",)))
     plan.append(("rlhf_64x4096", 64, 4096, "f32", None, False, False, 1.0, 0.95, ("gae", "td_lambda")))
     # rows that do not fill a workgroup's chunks: the lane-by-lane vector path
     plan.append(("ragged_4096x255", 4096, 255, "f32", dict(p_term=0.02, p_trunc=0.01), True, True, 0.99, 0.95,
