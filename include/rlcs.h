@@ -136,7 +136,7 @@ rlcs_status rlcs_retrace(const void* r, const void* q, const void* eq, const voi
  *   delta, q_ret  as for rlcs_retrace
  *   A        number of actions, A >= 1. Each workgroup stages its chunk's [steps, A] slices
  *            of q and pi in LDS: whole for A <= 28, in slices of the action axis otherwise
- *            (28 float32 / 24 bfloat16 actions at a time).
+ *            (32 actions at a time: one 128-byte line of float32, half a line of bfloat16).
  *   ws       optional, at least 64 bytes, 64-byte aligned, zero-filled by the caller: the int32
  *            at byte 8 becomes 2 when a call meets an out-of-range action, and stays so until
  *            the caller clears it. Unused otherwise; NULL = no report.

@@ -304,12 +304,13 @@ def test_retrace_full_shapes(A, T):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("A", [29, 30, 64, 100, 256])
+@pytest.mark.parametrize("A", [29, 30, 33, 64, 100, 256])
 @pytest.mark.parametrize("T", [1, 33, 4097])
 def test_retrace_full_long_action_axes(A, T, dtype):
     """More actions than a chunk's whole slices hold in LDS: the action axis staged in slices
-    (28 float32 / 24 bfloat16 actions at a time; A = 30 and 100 leave a partial last slice,
-    and an odd count of bfloat16 actions per row splits 16-byte blocks between rows)."""
+    of 32 actions (one slice at A = 29 and 30; A = 33 and 100 leave a partial last slice, 64
+    and 256 whole ones; an odd count of bfloat16 actions per row splits 16-byte blocks between
+    rows)."""
     N = 5 if T > 1000 else 23
     ro = workloads.make_retrace_full(N, T, A, seed=A * 31 + T, dtype=dtype, p_term=0.05, p_trunc=0.05)
     out, ref = _retrace_full_run(ro, c_bar=0.9)
