@@ -97,15 +97,6 @@ def parse():
     return ap.parse_args()
 
 
-def hold_stream(ms=2.0):
-    """Holds the current stream with a spin kernel of about `ms` milliseconds, so that the host
-    has enqueued the timing events and every timed launch (or the replayed graph) behind it
-    before the start event fires: the timed region then holds the K steps' GPU work and not the
-    host's submission of them."""
-    import torch
-    torch.cuda._sleep(int(ms * 1e-3 * 2.4e9))
-
-
 def probe_lib():
     """libprobe.so (built beside the library): the streaming reference kernel with GAE's byte
     split and the empty launch."""
@@ -137,12 +128,26 @@ def probe_stream_call(lib, s, threads):
         raise RuntimeError(f"probe_stream_gae returned {rc}")
 
 
-# Up to this many steps the timed calls are launched eagerly behind the spin; more are replayed
-# from one HIP graph. Measured on the GAE step (us per step, min-max of three; graph / eager):
-# K = 20: 5.65-6.14 / 5.54-5.58; K = 200: 5.25-5.28 / 5.47-5.50; K = 2000: 5.24 / 5.49. A graph
-# replay starts with about 8-12 us of fixed cost, which 20 steps do not amortise; an eager
-# launch costs about 0.25 us more per kernel than a graph node.
+# Up to this many steps the timed calls are launched eagerly; more are replayed from one HIP
+# graph. Either way they queue behind the hold below, on a stream of their own. Measured on the
+# GAE step behind the hold (us per step, median of six; eager / graph): K = 20: 5.23 / 5.27;
+# K = 2000 graph 4.78. Twenty steps pay about 9 us of fixed cost at the two events either way.
 EAGER_MAX_STEPS = 50
+
+# Untimed calls replayed from a graph right before the timed ones. They keep the GPU streaming
+# the same work (as the other steps of a training loop keep it busy) while the host queues the
+# timed calls, so that the timed calls neither wait for the host nor start on clocks that fell
+# while the GPU idled: behind a 2-3 ms spin kernel instead, the first timed 2000-step replay of
+# a process took 5.09-5.18 us per step and the later ones 4.78-4.88. A multiple of the number of
+# rotated sets, so the first timed call's set was last touched a whole rotation earlier, as in
+# the steady state of the timed calls themselves.
+HOLD_CALLS = 2048
+
+
+def hold_calls(sets):
+    """Untimed calls before the timed ones: HOLD_CALLS rounded up to a multiple of `sets`."""
+    sets = max(1, int(sets))
+    return sets * -(-HOLD_CALLS // sets)
 
 
 def timing_protocol(steps):
@@ -150,13 +155,18 @@ def timing_protocol(steps):
     return "eager" if steps <= EAGER_MAX_STEPS else "graph"
 
 
-def time_steps(fn, steps, start=None, end=None):
+def time_steps(fn, steps, start=None, end=None, sets=1):
     """Milliseconds for exactly `steps` calls fn(0) .. fn(steps - 1) on the current stream,
-    between two events recorded behind a spin kernel (see hold_stream): launched eagerly for
-    few steps, replayed from one HIP graph (captured and replayed once beforehand) for more."""
+    between two events. The timed calls queue behind hold_calls(sets) untimed calls fn(0) ..
+    replayed from a graph (fn(i) uses rotated set i % sets); they are launched eagerly for few
+    steps, and replayed from one HIP graph (captured and replayed once beforehand) for more."""
     import torch
     start = start or torch.cuda.Event(enable_timing=True)
     end = end or torch.cuda.Event(enable_timing=True)
+    hold = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(hold):
+        for i in range(hold_calls(sets)):
+            fn(i)
     graph = None
     if timing_protocol(steps) == "graph":
         graph = torch.cuda.CUDAGraph()
@@ -164,9 +174,9 @@ def time_steps(fn, steps, start=None, end=None):
             for i in range(steps):
                 fn(i)
         graph.replay()
+    hold.replay()
     torch.cuda.synchronize()
-    # the spin outlasts the host's submission of every eager call (a Python call takes ~12 us)
-    hold_stream(2.0 + 0.05 * steps if graph is None else 2.0)
+    hold.replay()
     start.record()
     if graph is None:
         for i in range(steps):
@@ -175,13 +185,13 @@ def time_steps(fn, steps, start=None, end=None):
         graph.replay()
     end.record()
     torch.cuda.synchronize()
-    del graph
+    del graph, hold
     return start.elapsed_time(end)
 
 
-def _per_step_us(fn, steps):
+def _per_step_us(fn, steps, sets=1):
     """Mean microseconds per call of `steps` calls timed as the GAE steps are."""
-    return time_steps(fn, steps) * 1e3 / steps
+    return time_steps(fn, steps, sets=sets) * 1e3 / steps
 
 
 def copy_reference(sets, steps):
@@ -195,7 +205,7 @@ def copy_reference(sets, steps):
         probe_stream_call(lib, sets[i], 64)
     out = {}
     for threads in (64, 256):
-        out[threads] = _per_step_us(lambda i: probe_stream_call(lib, sets[i % S], threads), steps)
+        out[threads] = _per_step_us(lambda i: probe_stream_call(lib, sets[i % S], threads), steps, S)
     import torch
     empty = _per_step_us(lambda i: lib.probe_empty(torch.cuda.current_stream().cuda_stream), steps)
     return out, empty
@@ -227,7 +237,7 @@ def probe_sweep(step, sets, steps):
     lib = probe_lib()
     S = len(sets)
     nbytes = algorithmic_bytes(N, T)
-    rows = [("rlcs_gae", _per_step_us(step, steps))]
+    rows = [("rlcs_gae", _per_step_us(step, steps, S))]
     for label, threads, per_lane, groups, dep in PROBE_SHAPES:
         def call(i, threads=threads, per_lane=per_lane, groups=groups, dep=dep):
             s = sets[i % S]
@@ -240,7 +250,7 @@ def probe_sweep(step, sets, steps):
                 raise RuntimeError(f"probe_stream_gae_shape returned {rc}")
         for i in range(S):
             call(i)
-        rows.append((f"probe: {label}", _per_step_us(call, steps)))
+        rows.append((f"probe: {label}", _per_step_us(call, steps, S)))
     rows.append(("empty launch", _per_step_us(
         lambda i: lib.probe_empty(torch.cuda.current_stream().cuda_stream), steps)))
     print(f"# GAE {N}x{T} fp32 sets, {steps} steps per row ({timing_protocol(steps)}), cold; "
@@ -678,10 +688,12 @@ def _rotated_sets(base, S, outs):
 
 
 def _graph_time(call, sets, nbytes):
-    """Mean microseconds per call over K graph-replayed calls cycling through `sets`."""
+    """Mean microseconds per call over K graph-replayed calls cycling through `sets` (K a
+    multiple of their number), timed behind an untimed replay of the same graph."""
     import torch
     S = len(sets)
     K = int(max(20, min(2000, 20000 / max(2.0, nbytes / 5e3))))
+    K = S * -(-K // S)
     for i in range(3):
         call(sets[i % S])
     torch.cuda.synchronize()
@@ -692,7 +704,7 @@ def _graph_time(call, sets, nbytes):
     graph.replay()
     torch.cuda.synchronize()
     a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    hold_stream()
+    graph.replay()
     a.record(); graph.replay(); b.record()
     torch.cuda.synchronize()
     del graph
@@ -912,6 +924,9 @@ def main():
     build(force=False)  # only if nothing is built yet
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    # Everything below runs on a stream of its own (default priority), as a caller's training
+    # loop would; on the null stream the same eager GAE steps took 0.1-0.2 us more each.
+    torch.cuda.set_stream(torch.cuda.Stream(dev))
     if args.extra:
         if args.profile_pass:
             _PROFILE["on"] = True
@@ -975,11 +990,12 @@ def main():
     check_set = replay_check_set(args.steps, S)
     eager_adv = sets[check_set]["adv"].clone()
 
-    # The timed steps: eager launches behind a spin kernel for few steps, a HIP graph replay for
-    # more (so that host-side launch cost, Python and ctypes, does not starve the GPU); each
-    # step is one rlcs_gae kernel launch either way.
+    # The timed steps: eager launches for few steps, a HIP graph replay for more, queued behind
+    # untimed steps that keep the GPU busy until the first timed one (so that host-side launch
+    # cost, Python and ctypes, does not starve the GPU); each step is one rlcs_gae kernel launch
+    # either way.
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    total_ms = time_steps(step, args.steps, start, end)
+    total_ms = time_steps(step, args.steps, start, end, sets=S)
     if not torch.equal(sets[check_set]["adv"], eager_adv):
         raise SystemExit("the timed steps' result differs from the eager launch")
     per_step_s = total_ms / 1e3 / args.steps
@@ -999,9 +1015,10 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "timing": f"{timing_protocol(args.steps)}: " + ("eager launches queued behind a spin kernel"
+        "timing": f"{timing_protocol(args.steps)}: " + ("eager launches"
                   if timing_protocol(args.steps) == "eager" else "one HIP graph replay") +
-                  ", HIP events on the launch stream around exactly K steps",
+                  f" on a stream of their own, queued behind {hold_calls(S)} untimed steps (one "
+                  "graph replay); HIP events on that stream around exactly K steps",
         "config": {"workload": f"GAE {N}x{T} fp32, term+trunc, bootstrap, cold HBM ({S} rotated input/output sets)",
                    "N": N, "T": T, "algorithmic_bytes": nbytes,
                    "gsteps_per_s": round(N * T / per_step_s / 1e9, 2),

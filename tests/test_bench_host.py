@@ -106,12 +106,21 @@ def test_replay_check_set_was_written_eagerly(steps, warmup, sets):
 
 
 def test_timing_protocol():
-    """Few timed steps are launched eagerly behind the spin (a graph replay's fixed start-up cost
-    is not amortised by them), many are replayed from one graph."""
+    """Few timed steps are launched eagerly, many are replayed from one graph."""
     assert bench.timing_protocol(20) == "eager"
     assert bench.timing_protocol(bench.EAGER_MAX_STEPS) == "eager"
     assert bench.timing_protocol(bench.EAGER_MAX_STEPS + 1) == "graph"
     assert bench.timing_protocol(2000) == "graph"
+
+
+@pytest.mark.parametrize("sets", [1, 3, 7, 20, 32, 33, 5000])
+def test_hold_ends_a_whole_rotation(sets):
+    """The untimed calls before the timed ones number at least HOLD_CALLS and a whole number of
+    rotations, so the first timed call (set 0) follows the hold's call on the last set, and its
+    own set was last touched a full rotation before."""
+    h = bench.hold_calls(sets)
+    assert h >= bench.HOLD_CALLS and h % sets == 0 and h - sets < max(bench.HOLD_CALLS, sets)
+    assert (h - 1) % sets == sets - 1
 
 
 def test_probe_library_rejects_bad_shapes():
