@@ -687,13 +687,20 @@ def _rotated_sets(base, S, outs):
     return sets
 
 
+def extra_calls(nbytes, sets):
+    """Timed calls per --extra row: about 8 GB of algorithmic bytes (a few ms at these rates, so
+    that the fixed cost at the two events, about 9 us, stays near 1 %), at least 20 and at most
+    2000 calls, rounded up to a whole number of rotations over `sets`."""
+    k = int(max(20, min(2000, -(-8e9 // max(1, nbytes)))))
+    return sets * -(-k // sets)
+
+
 def _graph_time(call, sets, nbytes):
-    """Mean microseconds per call over K graph-replayed calls cycling through `sets` (K a
-    multiple of their number), timed behind an untimed replay of the same graph."""
+    """Mean microseconds per call over extra_calls() graph-replayed calls cycling through
+    `sets`, timed behind an untimed replay of the same graph."""
     import torch
     S = len(sets)
-    K = int(max(20, min(2000, 20000 / max(2.0, nbytes / 5e3))))
-    K = S * -(-K // S)
+    K = extra_calls(nbytes, S)
     for i in range(3):
         call(sets[i % S])
     torch.cuda.synchronize()

@@ -140,3 +140,13 @@ def test_probe_library_rejects_bad_shapes():
     assert lib.probe_stream_gae_shape(*fake, 4098, 64, 1, 0, 0, None) == 1   # not whole vectors
     assert lib.probe_stream_gae_shape(None, *fake[1:], n, 64, 1, 0, 0, None) == 1
     assert lib.probe_stream_gae_shape(*fake, 0, 64, 1, 0, 0, None) == 0      # nothing to stream
+
+
+@pytest.mark.parametrize("nbytes,sets", [(17440, 32), (2899968, 32), (23085056, 16),
+                                         (2147614720, 1), (10**12, 3)])
+def test_extra_calls(nbytes, sets):
+    """Every --extra row times 20 to 2000 calls (more only to end on a whole rotation), a whole
+    number of rotations over its sets, and at least about 8 GB unless capped at 2000."""
+    k = bench.extra_calls(nbytes, sets)
+    assert k % sets == 0 and 20 <= k < 2000 + sets
+    assert k >= 2000 or k * nbytes >= 8e9
