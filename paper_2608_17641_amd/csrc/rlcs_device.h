@@ -218,4 +218,34 @@ __device__ __forceinline__ void store_k(float* base, int64_t p0, uint32_t valid,
     }
 }
 
+// Lanes of one wave exchanging values through LDS: every LDS write of the wave before the call
+// is seen by every LDS read after it (a wave's LDS instructions run in issue order; the fences
+// keep the compiler from moving LDS accesses across the call).
+__device__ __forceinline__ void wave_lds_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Eight outputs per lane (K = 8: bf16 inputs) where the wave's outputs are the 512 consecutive
+// ones [base, base + 512) and lane l holds group g of them. As two 16-byte stores per lane,
+// each store instruction of the wave would cover every other 16 bytes of its 2 KB, and
+// non-temporal stores of such half lines reach HBM as whole lines (6-11 % of the lines written
+// twice). Through the wave's 2 KB LDS `slot` lane l stores 16-byte pieces l and 64 + l instead,
+// so that each store instruction covers 1 KB of whole 128-byte lines. Pieces at or past `limit`
+// (a multiple of 8) are not stored. Every lane of the wave takes part; `out + base` is 16-byte
+// aligned.
+__device__ __forceinline__ void store8_lines(float* out, int64_t base, int64_t limit, int g,
+                                             int lane, const float (&v)[8], f32x4* slot) {
+    wave_lds_sync();  // the slot's previous readers are done
+    slot[2 * g] = f32x4{v[0], v[1], v[2], v[3]};
+    slot[2 * g + 1] = f32x4{v[4], v[5], v[6], v[7]};
+    wave_lds_sync();
+    const f32x4 x0 = slot[lane], x1 = slot[kWave + lane];
+    const int64_t p = base + 4 * int64_t(lane);
+    if (p < limit) __builtin_nontemporal_store(x0, reinterpret_cast<f32x4*>(out + p));
+    if (p + 4 * kWave < limit)
+        __builtin_nontemporal_store(x1, reinterpret_cast<f32x4*>(out + p + 4 * kWave));
+}
+
 }  // namespace rlcs

@@ -171,6 +171,10 @@ struct Chunk {
     int64_t p0;
     int sidx;            // p0 - chunk_lo: the lane's first step within the chunk
     const float* stage;  // staged slots (policies with kStaged > 0)
+    // Eight outputs per lane in full, unpadded chunks of unstaged policies: the wave's outputs
+    // are 512 consecutive ones, stored as whole lines through the wave's LDS slot.
+    static constexpr bool kLineStores = K == 8 && !PAD && Op::kStaged == 0;
+    f32x4* oslot = nullptr;
     Pair incl;     // lanes 0..lane of this wave composed (lane 0 innermost)
     Pair wave_in;  // waves between this wave and the chunk's carry-source edge
 
@@ -499,9 +503,17 @@ struct Chunk {
         }
         float o0[K], o1[K];
         Op::template finish<K, TR>(a.p, d, term, trunc, edge, B, nb, A, X, o0, o1);
-        const bool vstore = FULL && (!PAD || valid == kAll);
-        store_k<K>(a.out0, p0, valid, vstore, o0);
-        if (a.out1) store_k<K>(a.out1, p0, valid, vstore, o1);
+        if constexpr (kLineStores && FULL) {
+            const int lane = threadIdx.x & (kWave - 1);
+            const int g = sidx / K - (threadIdx.x / kWave) * kWave;  // the lane's group
+            const int64_t base = p0 - int64_t(g) * K;
+            store8_lines(a.out0, base, base + kWave * K, g, lane, o0, oslot);
+            if (a.out1) store8_lines(a.out1, base, base + kWave * K, g, lane, o1, oslot);
+        } else {
+            const bool vstore = FULL && (!PAD || valid == kAll);
+            store_k<K>(a.out0, p0, valid, vstore, o0);
+            if (a.out1) store_k<K>(a.out1, p0, valid, vstore, o1);
+        }
         return kBack ? A[0] : A[K - 1];
     }
 };
@@ -795,6 +807,7 @@ __global__ void __launch_bounds__(W * kWave) rows_kernel(Args a, int64_t rows_pe
     __shared__ float s_a[W], s_b[W];
     __shared__ float s_d[C::kCanDefer ? W : 1];
     __shared__ float s_carry;
+    __shared__ f32x4 s_out[C::kLineStores ? W : 1][C::kLineStores ? 2 * kWave : 1];
     const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
     const int64_t row_lo = int64_t(blockIdx.x) * rows_per_wg;
     const int64_t row_hi = min(row_lo + rows_per_wg, a.N);
@@ -815,6 +828,7 @@ __global__ void __launch_bounds__(W * kWave) rows_kernel(Args a, int64_t rows_pe
             auto pre = [&]() { sg.issue(a, chunk_lo, lo, s_dyn); };
             auto mid = [&]() { if constexpr (Op::kStaged > 0) { sg.commit(a, chunk_lo, s_dyn); __syncthreads(); } };
             C c;
+            c.oslot = s_out[C::kLineStores ? wave : 0];
             const float first = (can_full && (PAD || (chunk_lo >= lo && chunk_hi <= hi)))
                 ? run_chunk<true>(c, a, chunk_lo, lo, hi, s_a, s_b, s_d, lane, wave, wave_local, base_of, carry_of, stage, pre, mid)
                 : run_chunk<false>(c, a, chunk_lo, lo, hi, s_a, s_b, s_d, lane, wave, wave_local, base_of, carry_of, stage, pre, mid);
@@ -833,6 +847,7 @@ __global__ void __launch_bounds__(W * kWave) rows_kernel(Args a, int64_t rows_pe
             auto pre = [&]() { sg.issue(a, chunk_lo, lo, s_dyn); };
             auto mid = [&]() { if constexpr (Op::kStaged > 0) { sg.commit(a, chunk_lo, s_dyn); __syncthreads(); } };
             C c;
+            c.oslot = s_out[C::kLineStores ? wave : 0];
             const float last = (can_full && (PAD || (chunk_lo >= lo && chunk_lo + E <= hi)))
                 ? run_chunk<true>(c, a, chunk_lo, lo, hi, s_a, s_b, s_d, lane, wave, wave_local, base_of, carry_of, stage, pre, mid)
                 : run_chunk<false>(c, a, chunk_lo, lo, hi, s_a, s_b, s_d, lane, wave, wave_local, base_of, carry_of, stage, pre, mid);
@@ -952,7 +967,15 @@ __global__ void __launch_bounds__(WPG * kWave) wave_rows_kernel(Args a, int log2
     }
     float o0[K], o1[K];
     Op::template finish<K, TR>(a.p, d, term, trunc, edge, B, nb, A, X, o0, o1);
-    if (live) {
+    if constexpr (K == 8) {
+        // the wave's outputs are [base, base + 512): whole-line stores through LDS
+        __shared__ f32x4 s_out[WPG][2 * kWave];
+        f32x4* slot = s_out[threadIdx.x / kWave];
+        const int g = lane_group<kBack>(lane);
+        const int64_t base = p0 - int64_t(g) * K, limit = a.N * T;
+        store8_lines(a.out0, base, limit, g, lane, o0, slot);
+        if (a.out1) store8_lines(a.out1, base, limit, g, lane, o1, slot);
+    } else if (live) {
         store_k<K>(a.out0, p0, 0u, true, o0);
         if (a.out1) store_k<K>(a.out1, p0, 0u, true, o1);
     }
@@ -1021,6 +1044,7 @@ __global__ void __launch_bounds__(W * kWave) tiles_kernel(Args a, int64_t P) {
     __shared__ float s_a[W], s_b[W];
     __shared__ float s_carry;
     __shared__ uint32_t s_ticket, s_gen;
+    __shared__ f32x4 s_out[C::kLineStores ? W : 1][C::kLineStores ? 2 * kWave : 1];
     WsHeader* hdr = reinterpret_cast<WsHeader*>(a.ws);
     uint64_t* rec = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(a.ws) + kWsRecordsOffset);
     const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
@@ -1046,6 +1070,7 @@ __global__ void __launch_bounds__(W * kWave) tiles_kernel(Args a, int64_t P) {
     const int64_t lo = row * T + p * E, hi = min(lo + E, row * T + T);
 
     C c;
+    c.oslot = s_out[C::kLineStores ? wave : 0];
     // whole 16-byte vectors: a full tile whose rows start on a vector boundary
     const bool full = VEC && T % K == 0 && hi - lo == E;
     auto base_of = [&]() { return RowBase{lo, row, p * E}; };
