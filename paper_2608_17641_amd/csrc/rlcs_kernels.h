@@ -171,9 +171,9 @@ struct Chunk {
     int64_t p0;
     int sidx;            // p0 - chunk_lo: the lane's first step within the chunk
     const float* stage;  // staged slots (policies with kStaged > 0)
-    // Eight outputs per lane in full, unpadded chunks of unstaged policies: the wave's outputs
-    // are 512 consecutive ones, stored as whole lines through the wave's LDS slot.
-    static constexpr bool kLineStores = K == 8 && !PAD && Op::kStaged == 0;
+    // Eight outputs per lane, unstaged policies: a wave of a full chunk whose lanes all store
+    // whole vectors holds 512 consecutive outputs, stored as whole lines through its LDS slot.
+    static constexpr bool kLineStores = K == 8 && Op::kStaged == 0;
     f32x4* oslot = nullptr;
     Pair incl;     // lanes 0..lane of this wave composed (lane 0 innermost)
     Pair wave_in;  // waves between this wave and the chunk's carry-source edge
@@ -503,17 +503,19 @@ struct Chunk {
         }
         float o0[K], o1[K];
         Op::template finish<K, TR>(a.p, d, term, trunc, edge, B, nb, A, X, o0, o1);
+        const bool vstore = FULL && (!PAD || valid == kAll);
         if constexpr (kLineStores && FULL) {
-            const int lane = threadIdx.x & (kWave - 1);
-            const int g = sidx / K - (threadIdx.x / kWave) * kWave;  // the lane's group
-            const int64_t base = p0 - int64_t(g) * K;
-            store8_lines(a.out0, base, base + kWave * K, g, lane, o0, oslot);
-            if (a.out1) store8_lines(a.out1, base, base + kWave * K, g, lane, o1, oslot);
-        } else {
-            const bool vstore = FULL && (!PAD || valid == kAll);
-            store_k<K>(a.out0, p0, valid, vstore, o0);
-            if (a.out1) store_k<K>(a.out1, p0, valid, vstore, o1);
+            if (__all(vstore)) {
+                const int lane = threadIdx.x & (kWave - 1);
+                const int g = sidx / K - (threadIdx.x / kWave) * kWave;  // the lane's group
+                const int64_t base = p0 - int64_t(g) * K;
+                store8_lines(a.out0, base, base + kWave * K, g, lane, o0, oslot);
+                if (a.out1) store8_lines(a.out1, base, base + kWave * K, g, lane, o1, oslot);
+                return kBack ? A[0] : A[K - 1];
+            }
         }
+        store_k<K>(a.out0, p0, valid, vstore, o0);
+        if (a.out1) store_k<K>(a.out1, p0, valid, vstore, o1);
         return kBack ? A[0] : A[K - 1];
     }
 };

@@ -225,6 +225,24 @@ struct MaskedChunk {
     // first step. Accumulates the advantages that take part into (n, sum, sumsq). `full`: the
     // lane's steps are vector-aligned (stored as vectors when all of them are the lane's).
     float adv[K];  // the lane's advantages (kept for the fused whitening)
+    // K = 8: the wave's LDS slot for whole-line stores. A wave whose lanes all store whole
+    // vectors holds 512 consecutive outputs (lane l the group 63 - l of them).
+    f32x4* oslot = nullptr;
+
+    // Stores the lane's K outputs `v` to `out`: whole lines through the wave's slot when every
+    // lane of the wave stores whole vectors (K = 8), else per lane.
+    __device__ __forceinline__ void store(float* out, bool vstore, const float (&v)[K]) {
+        if constexpr (K == 8) {
+            if (__all(vstore)) {
+                const int lane = threadIdx.x & (kWave - 1);
+                const int g = kWave - 1 - lane;
+                const int64_t base = p0 - int64_t(g) * K;
+                store8_lines(out, base, base + kWave * K, g, lane, v, oslot);
+                return;
+            }
+        }
+        store_k<K>(out, p0, valid, vstore, v);
+    }
 
     template <bool STATS, bool STORE_ADV = true>
     __device__ __forceinline__ AW finish(const Args& a, AW Xw, bool full, double& n, double& s1,
@@ -244,8 +262,8 @@ struct MaskedChunk {
             }
         }
         const bool vstore = full && valid == kAll;
-        if (STORE_ADV) store_k<K>(a.out0, p0, valid, vstore, adv);
-        if (a.out1) store_k<K>(a.out1, p0, valid, vstore, ret);
+        if (STORE_ADV) store(a.out0, vstore, adv);
+        if (a.out1) store(a.out1, vstore, ret);
         return x;
     }
 };
@@ -322,6 +340,7 @@ __global__ void __launch_bounds__(W * kWave) masked_gae_kernel(MaskedArgs ma, in
     __shared__ float s_m[5][W];
     __shared__ float s_cA, s_cW;
     __shared__ double s_stat[3][W];
+    __shared__ f32x4 s_out[K == 8 ? W : 1][K == 8 ? 2 * kWave : 1];
     const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
     const int64_t row_lo = int64_t(blockIdx.x) * rows_per_wg;
     const int64_t row_hi = min(row_lo + rows_per_wg, a.N);
@@ -334,6 +353,7 @@ __global__ void __launch_bounds__(W * kWave) masked_gae_kernel(MaskedArgs ma, in
     for (;;) {
         const int64_t chunk_lo = chunk_hi - E;
         MaskedChunk<DT, K, TR, HM> c;
+        c.oslot = s_out[K == 8 ? wave : 0];
         masked_chunk_load(c, ma, base, lo, hi, chunk_lo, chunk_hi, can_full, lane, wave);
         const Tri incl = c.local(a.p, lane);
         Tri win = identity_tri();
@@ -556,6 +576,7 @@ __global__ void __launch_bounds__(W * kWave) masked_gae_fused_kernel(MaskedArgs 
     __shared__ double s_stat[3][W];
     __shared__ uint32_t s_tag;
     __shared__ float s_mean, s_rstd;
+    __shared__ f32x4 s_out[K == 8 ? W : 1][K == 8 ? 2 * kWave : 1];
     const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
     const int64_t G = gridDim.x, g = blockIdx.x;
     const int64_t row_lo = g * rows_per_wg;
@@ -572,6 +593,7 @@ __global__ void __launch_bounds__(W * kWave) masked_gae_fused_kernel(MaskedArgs 
     if (threadIdx.x == 0) s_tag = 2u * (uint32_t(ld_relaxed(gen_word)) & 0x7fffffffu) + 1u;
 
     MaskedChunk<DT, K, TR, HM> c;
+    c.oslot = s_out[K == 8 ? wave : 0];
     masked_chunk_load(c, ma, base, lo, hi, chunk_lo, chunk_hi, can_full, lane, wave);
     const Tri incl = c.local(a.p, lane);
     Tri win = identity_tri();
@@ -646,7 +668,7 @@ __global__ void __launch_bounds__(W * kWave) masked_gae_fused_kernel(MaskedArgs 
     float y[K];
 #pragma unroll
     for (int k = 0; k < K; ++k) y[k] = (c.adv[k] - mean) * rstd;
-    store_k<K>(a.out0, c.p0, c.valid, can_full && c.valid == MaskedChunk<DT, K, TR, HM>::kAll, y);
+    c.store(a.out0, can_full && c.valid == MaskedChunk<DT, K, TR, HM>::kAll, y);
 }
 
 }  // namespace rlcs
