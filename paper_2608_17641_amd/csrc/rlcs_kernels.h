@@ -229,12 +229,17 @@ struct Chunk {
         const int64_t T = a.T;
         int64_t row = 0, t = 0;
         uint32_t in_range = kAll;
+        bool deferred = false;  // row and step found once the loads are out
         if constexpr (PAD) {
             bool vector = false, skip = false;
             if (p0 >= lo && p0 + K <= hi) {
-                row_and_step(base_of(), p0, a.period, a.inv_period, row, t);
-                if (a.period == T || t + K <= T) vector = true;
-                else skip = t >= T && t + K <= a.period;  // wholly in a gap
+                if (a.period == T) {
+                    vector = deferred = true;  // no gaps: a lane in range takes the vector path
+                } else {
+                    row_and_step(base_of(), p0, a.period, a.inv_period, row, t);
+                    if (t + K <= T) vector = true;
+                    else skip = t >= T && t + K <= a.period;  // wholly in a gap
+                }
             } else if (p0 + K <= lo || p0 >= hi) {
                 skip = true;  // wholly outside the range
             } else if (a.period == T && p0 >= 0 && p0 + K <= a.N * T) {
@@ -281,6 +286,7 @@ struct Chunk {
 
         // at most one row edge among the K steps (T >= K)
         if constexpr (!PAD) row_and_step(base_of(), p0, T, a.inv_T, row, t);
+        else if (deferred) row_and_step(base_of(), p0, T, a.inv_T, row, t);
         ke_ = -1;
         int64_t row_e = row;
         if (kBack) {
