@@ -568,7 +568,14 @@ def run_extra(dev, only=""):
     plan.append(("4096x256", 4096, 256, "f32", dict(p_term=0.02, p_trunc=0.01), True, True, 0.99, 0.95, ("gae", "vtrace")))
     plan.append(("4096x256_plain", 4096, 256, "f32", dict(p_term=0.02, p_trunc=0.0), False, True, 0.99, 0.95, ("gae",)))
     plan.append(("rlhf_64x4096", 64, 4096, "f32", None, False, False, 1.0, 0.95, ("gae", "td_lambda")))
-    # rows that do not fill a workgroup's chunks: the lane-by-lane vector path
+    # dense rows of a multiple of the vector width that do not tile a wave: the flat rows kernel
+    plan.append(("flat_4096x200", 4096, 200, "f32", dict(p_term=0.02, p_trunc=0.01), True, True, 0.99, 0.95,
+                 ("gae", "vtrace", "elig_trace")))
+    plan.append(("flat_4096x1000", 4096, 1000, "f32", dict(p_term=0.02, p_trunc=0.01), True, True, 0.99, 0.95,
+                 ("gae", "td_lambda")))
+    plan.append(("flat_bf16_16384x200", 16384, 200, "bf16", dict(p_term=0.005, p_trunc=0.005), True, True, 0.99,
+                 0.95, ("gae", "retrace")))
+    # rows of a length that is not a multiple of the vector width: the lane-by-lane vector path
     plan.append(("ragged_4096x255", 4096, 255, "f32", dict(p_term=0.02, p_trunc=0.01), True, True, 0.99, 0.95,
                  ("gae", "vtrace", "elig_trace")))
     plan.append(("ragged_1024x1001", 1024, 1001, "f32", dict(p_term=0.02, p_trunc=0.01), True, True, 0.99, 0.95,

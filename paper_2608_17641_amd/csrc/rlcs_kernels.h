@@ -989,6 +989,151 @@ __global__ void __launch_bounds__(WPG * kWave) wave_rows_kernel(Args a, int log2
     }
 }
 
+// Dense rows of a multiple of K steps, K < T <= W*64*K: workgroup g owns rows [g*R, g*R + R),
+// R = floor(W*64*K / T), one contiguous, vector-aligned range [lo, hi); its W*64 lanes take
+// consecutive groups of K steps from lo (the (63-l)-th group of each wave backward), the lanes
+// past hi idle and loading nothing. Rows may straddle waves but not workgroups: each wave scans
+// its lanes as wave_rows_kernel does, the waves compose through LDS once, and lane 0 of a wave
+// reads its carry-source neighbour from memory with its other loads (it lies in the next or
+// previous wave's span unless a row edge comes first). A lane's row and step come from its
+// offset q in the range by a multiply and a shift: floor(q * magic / 2^22) = floor(q / T) for
+// q < W*64*K <= 2048 and T < 2048, magic = ceil(2^22 / T), since q * (magic - 2^22 / T) / 2^22 <
+// 1 / 2048. No chunk loop, no element-wise path. Grid: ceil(N / R) workgroups.
+template <class Op, typename DT, int K, bool TR, int W>
+__global__ void __launch_bounds__(W * kWave) flat_rows_kernel(Args a, int R, uint32_t magic) {
+    static_assert(Op::kStaged == 0, "staged policies run on the rows kernel");
+    constexpr bool kBack = Op::kBackward;
+    constexpr int NS = Op::kSlots;
+    constexpr int NB = Op::kNbr > 0 ? Op::kNbr : 1;
+    constexpr int kWords = K * int(sizeof(DT)) / 4;
+    constexpr int kTS = TR ? Op::kTruncSlot : -1;
+    __shared__ float s_a[W], s_b[W];
+    const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+    const int64_t T = a.T;
+    const int64_t row0 = int64_t(blockIdx.x) * R;
+    const int64_t lo = row0 * T;
+    const int64_t hi = min(row0 + R, a.N) * T;
+    const int g = lane_group<kBack>(lane);
+    const int q = (wave * kWave + g) * K;  // the lane's offset in the range
+    const int64_t p0 = lo + q;
+    const bool live = p0 < hi;
+    const int64_t pc = live ? p0 : 0;
+    const uint8_t* fallback = reinterpret_cast<const uint8_t*>(a.in[0]);
+
+    // Idle lanes load nothing: all of them reading one clamped address would pile every
+    // workgroup's idle loads onto a single line.
+    uint32_t tw[(K + 3) / 4] = {}, rw[(K + 3) / 4] = {};
+    uint32_t w[NS][kWords] = {};
+    float nraw[Op::kNbrRaw] = {};
+    if (live) {
+        if (Op::kFlags && TR) load_flag_words<K>(a.trunc, pc, rw);
+        if (Op::kFlags) load_flag_words<K>(a.term ? a.term : fallback, pc, tw);
+#pragma unroll
+        for (int s = 0; s < NS; ++s)
+            if (Op::slot_used(s, TR) && s != kTS) load_words<DT, K>(a.in[s], pc, w[s]);
+        // lane 0: the step past its carry-source edge, from memory (used unless a row edge
+        // comes first; an address outside the range is replaced by the lane's own)
+        if constexpr (Op::kNbr > 0) {
+            const int64_t pn = kBack ? p0 + K : p0 - 1;
+            const bool in = kBack ? pn < hi : pn >= lo;
+            if (lane == 0) Op::template nbr_load_raw<DT>(a, in ? pn : pc, nraw);
+        }
+    }
+    const int r_in = int((uint32_t(q) * magic) >> 22);
+    const int64_t row = live ? row0 + r_in : 0;
+    const int64_t t = live ? int64_t(q - r_in * int(T)) : 0;
+    const bool has_rv = Op::kRowValue && a.row_value;
+    const float rv = (has_rv && live) ? load_one<DT>(a.row_value, row) : 0.f;
+    // the row's edge step, if among the lane's K steps (T is a multiple of K)
+    const int ke = kBack ? (t + K == T ? K - 1 : -1) : (t == 0 ? 0 : -1);
+    const uint32_t edge = ke >= 0 ? (1u << ke) : 0u;
+    const uint32_t trunc = (Op::kFlags && TR) ? flag_mask<K>(rw) : 0u;
+    if constexpr (kTS >= 0) {
+        if (trunc) load_words<DT, K>(a.in[kTS], pc, w[kTS]);
+        else {
+#pragma unroll
+            for (int i = 0; i < kWords; ++i) w[kTS][i] = 0u;
+        }
+    }
+    float d[NS][K];
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+        if (Op::slot_used(s, TR)) unpack_words<DT, K>(w[s], d[s]);
+        else {
+#pragma unroll
+            for (int k = 0; k < K; ++k) d[s][k] = 0.f;
+        }
+    }
+    const uint32_t term = (Op::kFlags && a.term) ? flag_mask<K>(tw) : 0u;
+    float B[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) B[k] = (k == ke && has_rv) ? rv : 0.f;
+
+    // neighbour on the carry-source side: lane l-1, or for lane 0 the step read from memory
+    float nb[NB];
+    if constexpr (Op::kNbr > 0) {
+        float own[NB];
+        Op::template nbr_export<K>(a.p, d, term | trunc, own);
+#pragma unroll
+        for (int i = 0; i < NB; ++i) nb[i] = shift_up1(own[i], 0.f);
+        if (lane == 0 && live && !(edge & (kBack ? (1u << (K - 1)) : 1u))) Op::nbr_fix(a, nraw, nb);
+    } else {
+#pragma unroll
+        for (int i = 0; i < NB; ++i) nb[i] = 0.f;
+    }
+    float al[K], be[K];
+    Op::template build<K, TR>(a.p, d, term, trunc, edge, B, nb, al, be);
+    if (!live) {
+#pragma unroll
+        for (int k = 0; k < K; ++k) { al[k] = 0.f; be[k] = 1.f; }
+    }
+    Pair agg;
+    if (kBack) {
+        agg = Pair{al[K - 1], be[K - 1]};
+#pragma unroll
+        for (int k = K - 2; k >= 0; --k) agg = compose(Pair{al[k], be[k]}, agg);
+    } else {
+        agg = Pair{al[0], be[0]};
+#pragma unroll
+        for (int k = 1; k < K; ++k) agg = compose(Pair{al[k], be[k]}, agg);
+    }
+    const Pair incl = wave_scan_inclusive(agg, lane);
+    // the waves on this wave's carry-source side, composed (the range's carry-source end is a
+    // row edge, so nothing enters the range)
+    if (lane == kWave - 1) { s_a[wave] = incl.a; s_b[wave] = incl.b; }
+    __syncthreads();
+    Pair win = identity_pair();
+    if (kBack) {
+        for (int j = W - 1; j > wave; --j) win = compose(Pair{s_a[j], s_b[j]}, win);
+    } else {
+        for (int j = 0; j < wave; ++j) win = compose(Pair{s_a[j], s_b[j]}, win);
+    }
+    const float Xw = win.a;
+    const float X = shift_up1(apply(incl, Xw), Xw);
+    float A[K];
+    if (kBack) {
+        float nxt = X;
+#pragma unroll
+        for (int k = K - 1; k >= 0; --k) { A[k] = fmaf(be[k], nxt, al[k]); nxt = A[k]; }
+    } else {
+        float prv = X;
+#pragma unroll
+        for (int k = 0; k < K; ++k) { A[k] = fmaf(be[k], prv, al[k]); prv = A[k]; }
+    }
+    float o0[K], o1[K];
+    Op::template finish<K, TR>(a.p, d, term, trunc, edge, B, nb, A, X, o0, o1);
+    if constexpr (K == 8) {
+        // the wave's outputs are [base, base + 512) up to hi: stores of 16-byte pieces in order
+        __shared__ f32x4 s_out[W][2 * kWave];
+        const int64_t base = lo + int64_t(wave) * kWave * K;
+        store8_lines(a.out0, base, hi, g, lane, o0, s_out[wave]);
+        if (a.out1) store8_lines(a.out1, base, hi, g, lane, o1, s_out[wave]);
+    } else if (live) {
+        store_k<K>(a.out0, p0, 0u, true, o0);
+        if (a.out1) store_k<K>(a.out1, p0, 0u, true, o1);
+    }
+}
+
 // Polls of one record before a waiting tile gives up (about a second). Reached only when the
 // workspace was not zero-filled before first use; the tile then continues with a NaN carry
 // and flags the workspace header instead of waiting forever.
