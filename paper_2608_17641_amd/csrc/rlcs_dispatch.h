@@ -293,18 +293,26 @@ rlcs_status dispatch_dt(Args& a, bool has_trunc, void* ws, size_t ws_bytes, hipS
     }
     p.wave_rows_log2T = -1;
     p.flat_R = 0;
-    // Dense rows of a multiple of K steps, up to one four-wave chunk (float32) or one wave
-    // (bfloat16), except powers of two that tile a wave: the flat rows kernel. Measured against
+    // Dense rows up to one four-wave chunk (float32) or one wave (bfloat16), except powers of
+    // two that tile a wave: the flat rows kernel. Measured against
     // the rows kernel (C harness, cold): GAE 4096x192 fp32 5.05 -> 4.62 us, 4096x252 5.97 -> 5.22,
     // 4096x500 10.04 -> 8.68, 4096x1000 16.59 -> 15.48, 4096x1024 16.13 -> 15.54; bf16 16384x200
     // 12.83 -> 11.14, 16384x504 24.98 -> 23.16; longer bf16 rows were within 2.5 % either way
     // (16384x1000 45.4 -> 44.2, 16384x2048 82.3 -> 83.4) and keep the rows kernel.
+    // Rows whose length is not a multiple of K take it as well when a workgroup's rows can start
+    // and end on vector boundaries (R a multiple of K / gcd(T, K), N*T a multiple of K).
     const int64_t flat_max = sizeof(DT) == 4 ? E_small : int64_t(kWave) * K;
-    if (Op::kStaged == 0 && !p.split && vec && T > K && T <= flat_max && T % K == 0 &&
+    if (Op::kStaged == 0 && !p.split && vec && T > K && T <= flat_max && (N * T) % K == 0 &&
         !((T & (T - 1)) == 0 && T <= int64_t(kWave) * K)) {
-        p.flat_R = int(E_small / T);
-        p.flat_magic = uint32_t(((int64_t(1) << 22) + T - 1) / T);
-        if ((N + p.flat_R - 1) / p.flat_R > INT32_MAX) return RLCS_ERR_INVALID_ARG;
+        int64_t gcd = K, b = T % K;
+        while (b) { const int64_t r = gcd % b; gcd = b; b = r; }
+        const int64_t step = K / gcd;  // rows per vector-aligned range
+        const int64_t R = E_small / T / step * step;
+        if (R > 0) {
+            p.flat_R = int(R);
+            p.flat_magic = uint32_t(((int64_t(1) << 22) + T - 1) / T);
+            if ((N + R - 1) / R > INT32_MAX) return RLCS_ERR_INVALID_ARG;
+        }
     }
     if (Op::kStaged == 0 && !p.split && vec && T >= K && T <= int64_t(kWave) * K && (T & (T - 1)) == 0) {
         // rows tile a wave exactly: the wave-rows kernel

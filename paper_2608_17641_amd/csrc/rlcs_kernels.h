@@ -989,8 +989,9 @@ __global__ void __launch_bounds__(WPG * kWave) wave_rows_kernel(Args a, int log2
     }
 }
 
-// Dense rows of a multiple of K steps, K < T <= W*64*K: workgroup g owns rows [g*R, g*R + R),
-// R = floor(W*64*K / T), one contiguous, vector-aligned range [lo, hi); its W*64 lanes take
+// Dense rows, K < T <= W*64*K: workgroup g owns rows [g*R, g*R + R), R*T <= W*64*K and a
+// multiple of K (and N*T a multiple of K), one contiguous, vector-aligned range [lo, hi); a row
+// edge may fall inside a lane's K steps when T is not a multiple of K. Its W*64 lanes take
 // consecutive groups of K steps from lo (the (63-l)-th group of each wave backward), the lanes
 // past hi idle and loading nothing. Rows may straddle waves but not workgroups: each wave scans
 // its lanes as wave_rows_kernel does, the waves compose through LDS once, and lane 0 of a wave
@@ -1042,11 +1043,22 @@ __global__ void __launch_bounds__(W * kWave) flat_rows_kernel(Args a, int R, uin
     const int r_in = int((uint32_t(q) * magic) >> 22);
     const int64_t row = live ? row0 + r_in : 0;
     const int64_t t = live ? int64_t(q - r_in * int(T)) : 0;
+    // the row edge among the lane's K steps, if any (at most one: T >= K): backward the last
+    // step of the lane's first row, forward the first step of a row (the next one when the
+    // lane starts inside a row)
+    int ke = -1;
+    if (kBack) {
+        if (t + K >= T) ke = int(T - 1 - t);
+    } else {
+        if (t == 0) ke = 0;
+        else if (t + K > T) ke = int(T - t);
+    }
+    const uint32_t edge = (live && ke >= 0) ? (1u << ke) : 0u;
+    // the per-row value belongs to the edge's row: forward, a row starting inside the lane is
+    // the next one (it lies in the range, so it exists)
+    const int64_t row_e = (!kBack && ke > 0) ? row + 1 : row;
     const bool has_rv = Op::kRowValue && a.row_value;
-    const float rv = (has_rv && live) ? load_one<DT>(a.row_value, row) : 0.f;
-    // the row's edge step, if among the lane's K steps (T is a multiple of K)
-    const int ke = kBack ? (t + K == T ? K - 1 : -1) : (t == 0 ? 0 : -1);
-    const uint32_t edge = ke >= 0 ? (1u << ke) : 0u;
+    const float rv = (has_rv && live) ? load_one<DT>(a.row_value, row_e) : 0.f;
     const uint32_t trunc = (Op::kFlags && TR) ? flag_mask<K>(rw) : 0u;
     if constexpr (kTS >= 0) {
         if (trunc) load_words<DT, K>(a.in[kTS], pc, w[kTS]);

@@ -1,15 +1,18 @@
 """CPU emulation of flat_rows_kernel's lane geometry (csrc/rlcs_kernels.h; plan in
-csrc/rlcs_dispatch.h), restated from the kernel. For dense rows of T steps, T a multiple of K,
-K < T <= 256*K (float32, K = 4) or 64*K (bfloat16, K = 8), and not a power of two of at most 64*K
-steps: workgroup g owns rows [g*R, g*R + R), R = floor(256*K / T),
+csrc/rlcs_dispatch.h), restated from the kernel. For dense rows of T steps, K < T <= 256*K
+(float32, K = 4) or 64*K (bfloat16, K = 8), not a power of two of at most 64*K steps, N*T a
+multiple of K: workgroup g owns rows [g*R, g*R + R), R the most whole rows in 256*K steps that is
+a multiple of K / gcd(T, K),
 the range [lo, hi) = [g*R*T, min(g*R + R, N)*T); lane l of wave w holds the K steps at offset
 q = (64*w + g(l))*K (g(l) = 63 - l backward, l forward), live when lo + q < hi; its row is
 g*R + floor(q * magic / 2^22), magic = ceil(2^22 / T), and its step q - T*floor(q / T).
-Checked: the multiply-shift division is exact for every (K, T, q) the kernel sees; the live lanes
-cover every (row, step group) exactly once, each in one row; the neighbour a live lane takes (lane
-l-1 through the wave shift, or lane 0's read at p0 + K backward / p0 - 1 forward) is the adjacent
-step of the same row whenever the lane's edge step is not a row edge, and lane 0's read address
-lies inside the range then; and the bf16 whole-line stores of each wave ([lo + 512*w, ...) up to
+Checked: the multiply-shift division is exact for every (K, T, q) the kernel sees; every range
+starts and ends on a vector boundary and the live lanes cover every step exactly once; a lane
+holds at most one row edge, where the kernel's edge computation puts it, and the per-row
+value it reads is that edge step's row's; the neighbour a live
+lane takes (lane l-1 through the wave shift, or lane 0's read at p0 + K backward / p0 - 1
+forward) is the adjacent step whenever the lane's carry-source edge step is not a row edge, and
+lane 0's read address lies inside the range then; and the bf16 whole-line stores of each wave ([lo + 512*w, ...) up to
 hi) cover exactly the live lanes' outputs. Nothing here runs on a GPU."""
 import pytest
 
@@ -24,12 +27,21 @@ def flat_max(K):
     return W * WAVE * K if K == 4 else WAVE * K
 
 
-def is_flat(T, K):
-    return T % K == 0 and K < T <= flat_max(K) and not ((T & (T - 1)) == 0 and T <= WAVE * K)
+def rows_per_group(T, K):
+    """R as the dispatcher picks it: the most whole rows that fit W*64*K steps, a multiple of
+    K / gcd(T, K) so that the range starts and ends on vector boundaries (0: not taken)."""
+    from math import gcd
+    step = K // gcd(T, K)
+    return W * WAVE * K // T // step * step
+
+
+def is_flat(T, K, N=None):
+    return (K < T <= flat_max(K) and not ((T & (T - 1)) == 0 and T <= WAVE * K)
+            and rows_per_group(T, K) > 0 and (N is None or (N * T) % K == 0))
 
 
 def flat_shapes(K):
-    return [T for T in range(2 * K, flat_max(K) + 1, K) if is_flat(T, K)]
+    return [T for T in range(K + 1, flat_max(K) + 1) if is_flat(T, K)]
 
 
 @pytest.mark.parametrize("K", [4, 8])
@@ -42,7 +54,7 @@ def test_multiply_shift_division_is_exact(K):
 
 
 def lanes(N, T, K, backward):
-    R = W * WAVE * K // T
+    R = rows_per_group(T, K)
     for wg in range(-(-N // R)):
         row0 = wg * R
         lo, hi = row0 * T, min(row0 + R, N) * T
@@ -62,9 +74,10 @@ def lanes(N, T, K, backward):
 @pytest.mark.parametrize("N,T", [(1, 12), (7, 20), (5, 24), (33, 40), (100, 96), (13, 136),
                                  (9, 192), (64, 200), (3, 240), (17, 252), (11, 264), (4, 504),
                                  (50, 100), (5, 300), (7, 500), (6, 512), (3, 1000), (5, 1020),
-                                 (4, 1024)])
+                                 (4, 1024), (8, 255), (16, 255), (12, 129), (8, 100), (16, 101),
+                                 (8, 251), (4, 1001), (8, 33), (32, 9)])
 def test_flat_lanes_cover_rows_and_neighbours(N, T, K, backward):
-    if not is_flat(T, K):
+    if not is_flat(T, K, N):
         pytest.skip("not a flat-rows shape for this K")
     L = list(lanes(N, T, K, backward))
     seen = set()
@@ -72,26 +85,37 @@ def test_flat_lanes_cover_rows_and_neighbours(N, T, K, backward):
     for x in L:
         if not x["live"]:
             continue
-        row, t = x["row"], x["t"]
-        assert 0 <= row < N and t % K == 0 and t + K <= T
-        assert x["p0"] == row * T + t
-        assert (row, t) not in seen
-        seen.add((row, t))
+        assert x["lo"] % K == 0 and x["hi"] % K == 0  # whole, aligned vectors
+        p0 = x["p0"]
+        assert p0 == x["row"] * T + x["t"] and 0 <= x["t"] < T
+        for k in range(K):  # each step once
+            assert p0 + k not in seen
+            seen.add(p0 + k)
         where[(x["wg"], x["wave"], x["lane"])] = x
-    assert seen == {(n, t) for n in range(N) for t in range(0, T, K)}
+    assert seen == set(range(N * T))
     for (wg, wave, lane), x in where.items():
-        row, t = x["row"], x["t"]
-        at_edge = (t + K == T) if backward else (t == 0)
-        if at_edge:
+        t = x["t"]
+        # at most one row edge in the lane (T >= K); the lane's carry-source edge step is a row
+        # edge exactly when the kernel's edge bit sits there
+        edges = [k for k in range(K) if (t + k) % T == (T - 1 if backward else 0)]
+        assert len(edges) <= 1
+        if backward:
+            ke = T - 1 - t if t + K >= T else -1
+        else:
+            ke = 0 if t == 0 else (T - t if t + K > T else -1)
+        assert edges == ([ke] if ke >= 0 else [])
+        if ke >= 0:  # the per-row value read for the edge belongs to the edge step's row
+            row_e = x["row"] + 1 if (not backward and ke > 0) else x["row"]
+            assert (x["p0"] + ke) // T == row_e
+        if ke == (K - 1 if backward else 0):
             continue
-        want = (row, t + K) if backward else (row, t - K)
+        want = x["p0"] + K if backward else x["p0"] - K  # the adjacent group's first step
         if lane > 0:  # the wave shift: lane l-1 of the same wave
             y = where.get((wg, wave, lane - 1))
-            assert y is not None and (y["row"], y["t"]) == want
-        else:         # lane 0 reads the step from memory
+            assert y is not None and y["p0"] == want
+        else:         # lane 0 reads the step from memory, inside the range
             pn = x["p0"] + K if backward else x["p0"] - 1
             assert x["lo"] <= pn < x["hi"]
-            assert pn == (want[0] * T + want[1] if backward else want[0] * T + want[1] + K - 1)
     if K == 8:  # whole-line stores per wave cover exactly the live outputs
         for wg in {x["wg"] for x in L}:
             for wave in range(W):

@@ -148,6 +148,23 @@ def test_rows_flat(T, dtype):
                       label=f"{N}x{T} {dtype} plain")
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("T", [5, 9, 33, 100, 101, 129, 250, 251, 255, 257, 300, 499, 1001, 1023])
+def test_rows_flat_ragged(T, dtype):
+    """Rows whose length is not a multiple of K: the flat rows kernel where a workgroup's rows
+    start and end on vector boundaries (a row edge inside a lane's K steps), the lane-by-lane
+    rows kernel where they cannot (N*T not a multiple of K, or rows too long): both against the
+    oracle, with and without truncation and bootstrap."""
+    K = 4 if dtype == "f32" else 8
+    for N in (K, 3 * K, 4 * K + 1, 1000 * K):
+        for i, name in enumerate(ESTIMATORS):
+            ro = make_inputs(name, N, T, seed=N * 17 + T + i, dtype=dtype, p_term=0.05, p_trunc=0.05)
+            check(name, ro, gamma=0.97, lam=0.9, label=f"{N}x{T} {dtype}")
+            if name in ("gae", "vtrace", "td_lambda"):
+                check(name, ro, trunc=False, boot=False, gamma=0.97, lam=0.9,
+                      label=f"{N}x{T} {dtype} plain")
+
+
 @pytest.mark.parametrize("N,T", [(1, 1), (1, 4096), (1, 1 << 20), (3, 100_000), (5000, 3)])
 @pytest.mark.parametrize("var", [0, 1, 2])
 def test_extreme_shapes(N, T, var):
