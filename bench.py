@@ -128,11 +128,77 @@ def probe_stream_call(lib, s, threads):
         raise RuntimeError(f"probe_stream_gae returned {rc}")
 
 
+# The events around a timed region are created with hipEventDisableSystemFence: they serve for
+# timing only, so recording them skips the system-scope cache write-back and invalidation that a
+# default event performs (the host synchronizes with the device by itself after the end event,
+# outside the timed region). Measured on the 20 eager GAE steps behind the hold (us per step,
+# medians of six): 5.27 with default events, 5.11 with these; at 2000 steps 4.85 either way.
+HIP_EVENT_DISABLE_SYSTEM_FENCE = 0x20000000
+_HIP = {}
+
+
+def hip_runtime():
+    """The HIP runtime that PyTorch loaded (ctypes), found among the process's mapped files so
+    that no second copy of the runtime is loaded."""
+    if "lib" not in _HIP:
+        import ctypes
+        import torch
+        torch.cuda.init()
+        with open("/proc/self/maps") as f:
+            paths = {ln.split()[-1] for ln in f if "libamdhip64" in ln.split()[-1]}
+        if len(paths) != 1:
+            raise RuntimeError(f"expected one mapped HIP runtime, found {sorted(paths)}")
+        lib = ctypes.CDLL(paths.pop())
+        P = ctypes.c_void_p
+        lib.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(P), ctypes.c_uint]
+        lib.hipEventRecord.argtypes = [P, P]
+        lib.hipEventSynchronize.argtypes = [P]
+        lib.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), P, P]
+        lib.hipEventDestroy.argtypes = [P]
+        _HIP["lib"] = lib
+    return _HIP["lib"]
+
+
+class TimingEvent:
+    """A HIP event for timing only (hipEventDisableSystemFence), recorded on PyTorch's current
+    stream; record() and elapsed_time() as torch.cuda.Event's."""
+
+    def __init__(self):
+        import ctypes
+        self._lib = hip_runtime()
+        self._ev = ctypes.c_void_p()
+        rc = self._lib.hipEventCreateWithFlags(ctypes.byref(self._ev), HIP_EVENT_DISABLE_SYSTEM_FENCE)
+        if rc != 0:
+            raise RuntimeError(f"hipEventCreateWithFlags returned {rc}")
+
+    def record(self):
+        import ctypes
+        import torch
+        rc = self._lib.hipEventRecord(self._ev, ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+        if rc != 0:
+            raise RuntimeError(f"hipEventRecord returned {rc}")
+
+    def elapsed_time(self, end):
+        """Milliseconds from this event to `end` (waits for `end`)."""
+        import ctypes
+        rc = self._lib.hipEventSynchronize(end._ev)
+        ms = ctypes.c_float()
+        rc = rc or self._lib.hipEventElapsedTime(ctypes.byref(ms), self._ev, end._ev)
+        if rc != 0:
+            raise RuntimeError(f"hipEventElapsedTime returned {rc}")
+        return ms.value
+
+    def __del__(self):
+        if getattr(self, "_ev", None) and self._ev.value:
+            self._lib.hipEventDestroy(self._ev)
+
+
 # Up to this many steps the timed calls are launched eagerly; more are replayed from one HIP
-# graph. Either way they queue behind the hold below, on a stream of their own. Measured on the
-# GAE step behind the hold (us per step, median of six; eager / graph): K = 20: 5.23 / 5.27;
-# K = 2000 graph 4.78. Twenty steps pay about 9 us of fixed cost at the two events either way.
-EAGER_MAX_STEPS = 50
+# graph. Either way they queue behind the hold below, on a stream of their own. An eager launch
+# costs about 0.3 us more on the GPU than a graph node, and a graph about 7.5 us once at its
+# start. Measured on the GAE step behind the hold with the timing events above (us per step,
+# medians of six; eager / graph): K = 20: 5.17 / 5.27; K = 50: 5.17 / 5.01; K = 2000 graph 4.87.
+EAGER_MAX_STEPS = 25
 
 # Untimed calls replayed from a graph right before the timed ones. They keep the GPU streaming
 # the same work (as the other steps of a training loop keep it busy) while the host queues the
@@ -161,8 +227,8 @@ def time_steps(fn, steps, start=None, end=None, sets=1):
     replayed from a graph (fn(i) uses rotated set i % sets); they are launched eagerly for few
     steps, and replayed from one HIP graph (captured and replayed once beforehand) for more."""
     import torch
-    start = start or torch.cuda.Event(enable_timing=True)
-    end = end or torch.cuda.Event(enable_timing=True)
+    start = start or TimingEvent()
+    end = end or TimingEvent()
     hold = torch.cuda.CUDAGraph()
     with torch.cuda.graph(hold):
         for i in range(hold_calls(sets)):
@@ -717,7 +783,7 @@ def _graph_time(call, sets, nbytes):
             call(sets[i % S])
     graph.replay()
     torch.cuda.synchronize()
-    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a, b = TimingEvent(), TimingEvent()
     graph.replay()
     a.record(); graph.replay(); b.record()
     torch.cuda.synchronize()
@@ -1008,7 +1074,7 @@ def main():
     # untimed steps that keep the GPU busy until the first timed one (so that host-side launch
     # cost, Python and ctypes, does not starve the GPU); each step is one rlcs_gae kernel launch
     # either way.
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start, end = TimingEvent(), TimingEvent()
     total_ms = time_steps(step, args.steps, start, end, sets=S)
     if not torch.equal(sets[check_set]["adv"], eager_adv):
         raise SystemExit("the timed steps' result differs from the eager launch")
@@ -1032,7 +1098,8 @@ def main():
         "timing": f"{timing_protocol(args.steps)}: " + ("eager launches"
                   if timing_protocol(args.steps) == "eager" else "one HIP graph replay") +
                   f" on a stream of their own, queued behind {hold_calls(S)} untimed steps (one "
-                  "graph replay); HIP events on that stream around exactly K steps",
+                  "graph replay); HIP events for timing only (hipEventDisableSystemFence) on that stream "
+                  "around exactly K steps",
         "config": {"workload": f"GAE {N}x{T} fp32, term+trunc, bootstrap, cold HBM ({S} rotated input/output sets)",
                    "N": N, "T": T, "algorithmic_bytes": nbytes,
                    "gsteps_per_s": round(N * T / per_step_s / 1e9, 2),
