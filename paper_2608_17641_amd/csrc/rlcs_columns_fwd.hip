@@ -2,6 +2,7 @@
 // strided eligibility traces and prefix sums, eligibility traces of F-vectors, and the
 // workspace size of the column scans.
 #include "rlcs_columns_dispatch.h"
+#include "rlcs_vec.h"
 
 using namespace rlcs;
 using namespace rlcs::host;
@@ -69,6 +70,17 @@ rlcs_status rlcs_elig_trace_vec(const void* x, const uint8_t* term, const uint8_
     a.in[0] = x;
     a.term = term; a.trunc = trunc;
     a.out0 = z;
+    // Rows of vectors when they fit the row kernel (not under a forced column variant).
+    if (g_variant == 0 && aligned(x, 16) && aligned(z, 16)) {
+        const int wf = T % 4 == 0 && (!term || aligned(term, 4)) && (!trunc || aligned(trunc, 4));
+        hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+        bool done;
+        if (dtype == RLCS_BF16)
+            done = trunc ? vec_rows_launch<bf16_t, true>(a, F, wf, s) : vec_rows_launch<bf16_t, false>(a, F, wf, s);
+        else
+            done = trunc ? vec_rows_launch<float, true>(a, F, wf, s) : vec_rows_launch<float, false>(a, F, wf, s);
+        if (done) return hipGetLastError() == hipSuccess ? RLCS_OK : RLCS_ERR_LAUNCH;
+    }
     // column n*F + f: feature f of row n; flags one per step of a row; non-temporal stores
     // when a step's F outputs fill whole 128-byte lines
     const ColGeom g{N * F, F, F, T * F, 1, T, 0, F % 32 == 0 ? 1 : 0};

@@ -1,0 +1,249 @@
+// Eligibility traces of F-vectors along rows (Section 3.3.5): z_t = beta_t z_{t-1} + x_t for
+// x_t, z_t in R^F, beta_t = gamma lambda except 0 at a row's first step and after a step that
+// ends an episode, one beta per step shared by all F features.
+//
+// For F a multiple of the 16-byte vector width V (4 float32 or 8 bfloat16 features) with
+// L = F / V lanes per step a power of two up to 64, one workgroup of W waves scans one row of
+// the [N, T, F] input. Lane l of wave w holds features [V (l mod L), V (l mod L) + V) of the
+// kVecSteps = 4 consecutive steps from t0 = (w S + l / L) * 4, S = 64 / L step groups side by
+// side in a wave. The wave's inputs and outputs, S * 4 consecutive steps of the row, are
+// contiguous: where a step is under 128 bytes (L < 8), each wave loads its inputs as whole 1 KB
+// runs into its LDS slot, from which each lane takes one 16-byte vector per step (read straight
+// from memory, half a line per step at F = 16 float32: 4096 x 256 x 16 30.8 us against 27.0
+// staged; at F = 64 direct loads of whole lines 26.2 us against 27.2 staged). A lane's map
+// over its steps is V offsets and one shared factor; a wave scans its step groups by shuffles
+// across lanes L apart (log2 S rounds), the waves compose once through LDS (wave w's total maps
+// at [w][F] offsets and [w] factors) and each lane finishes its steps. The outputs pass back
+// through the slot so that each store instruction writes 1 KB of whole lines (pieces past the
+// row end are neither loaded nor stored). Flags: one 4-byte word per lane and array when
+// `word_flags` (T a multiple of 4, aligned flag arrays), otherwise one byte per step; lanes also
+// read the flags of the step before t0. Grid: N workgroups of W * 64 lanes.
+#pragma once
+
+#include "rlcs_dispatch.h"
+
+namespace rlcs {
+
+constexpr int kVecSteps = 4;
+
+// Bytes of dynamic LDS for a workgroup of W waves: W output slots of 64 * 4 * V floats, then
+// W * F offsets and W factors.
+template <typename DT>
+constexpr size_t vec_rows_lds(int W, int64_t F) {
+    constexpr int V = 16 / int(sizeof(DT));
+    return size_t(W) * kWave * kVecSteps * V * 4 + size_t(W) * size_t(F) * 4 + size_t(W) * 4;
+}
+
+template <typename DT, bool TR, int L>
+__global__ void __launch_bounds__(16 * kWave) vec_rows_kernel(Args a, int word_flags) {
+    constexpr int V = 16 / int(sizeof(DT));
+    constexpr int F = L * V;
+    constexpr int S = kWave / L;
+    constexpr int KS = kVecSteps;
+    constexpr int kPieces = kWave * KS * V / 4;  // 16-byte output pieces of one wave
+    extern __shared__ f32x4 s_vec[];
+    const int W = int(blockDim.x) / kWave;
+    const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+    const int fg = lane % L, sg = lane / L;
+    const int64_t T = a.T;
+    const int64_t frow = int64_t(blockIdx.x) * T;  // the row's first flag
+    const int64_t xrow = frow * F;                 // the row's first feature value
+    const int64_t t0 = (int64_t(wave) * S + sg) * KS;
+    float* s_off = reinterpret_cast<float*>(s_vec + W * kPieces);
+    float* s_fac = s_off + W * F;
+    const float decay = a.p.gamma * a.p.lambda;
+
+    // loads, all issued before the first use: the lane's inputs, then its flags and those of the
+    // step before t0. Steps of fewer than 128 bytes (L < 8) are staged: the wave loads its span,
+    // S * KS consecutive steps of the row, as whole 1 KB runs (16-byte piece i * 64 + lane, up to
+    // the row end) into its slot, and each lane takes its pieces from there; longer steps are
+    // whole lines already and each lane loads its own vectors.
+    constexpr bool kStaged = L < 8;
+    f32x4* slot = s_vec + wave * kPieces;
+    const int64_t wbase = xrow + int64_t(wave) * S * KS * F;  // the wave's first element
+    const int64_t limit = xrow + T * F;                       // the row's end
+    const DT* x = static_cast<const DT*>(a.in[0]);
+    int nv = 0;  // the lane's steps inside the row
+    if (t0 < T) nv = int(min(int64_t(KS), T - t0));
+    u32x4 raw[KS];
+#pragma unroll
+    for (int i = 0; i < KS; ++i) {
+        const int64_t p = kStaged ? wbase + int64_t(i * kWave + lane) * V : xrow + (t0 + i) * F + fg * V;
+        if (kStaged ? p < limit : i < nv)
+            raw[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(x + p));
+    }
+    uint32_t done = 0;  // bit k: step t0 + k ends an episode
+    bool cut0 = true;   // nothing enters step t0 (the row start, or an episode ended before it)
+    if (t0 < T) {
+        if (word_flags) {
+            uint32_t tw[1] = {0u}, rw[1] = {0u};
+            if (a.term) load_flag_words<4>(a.term, frow + t0, tw);
+            if (TR) load_flag_words<4>(a.trunc, frow + t0, rw);
+            done = flag_mask<4>(tw) | flag_mask<4>(rw);
+        } else {
+#pragma unroll
+            for (int k = 0; k < KS; ++k) {
+                if (k < nv) {
+                    const bool d = (a.term && a.term[frow + t0 + k]) || (TR && a.trunc[frow + t0 + k]);
+                    done |= d ? (1u << k) : 0u;
+                }
+            }
+        }
+        if (t0 > 0) cut0 = (a.term && a.term[frow + t0 - 1]) || (TR && a.trunc[frow + t0 - 1]);
+    }
+    if constexpr (kStaged) {
+#pragma unroll
+        for (int i = 0; i < KS; ++i) {
+            const int64_t p = wbase + int64_t(i * kWave + lane) * V;
+            if (p < limit) reinterpret_cast<u32x4*>(slot)[i * kWave + lane] = raw[i];
+        }
+        // the lane's vectors: step k's features at piece (sg * KS + k) * L + fg of the span
+        wave_lds_sync();
+#pragma unroll
+        for (int k = 0; k < KS; ++k) raw[k] = reinterpret_cast<const u32x4*>(slot)[(sg * KS + k) * L + fg];
+    }
+    float xv[KS][V];
+#pragma unroll
+    for (int k = 0; k < KS; ++k) {
+        const uint32_t w[4] = {raw[k].x, raw[k].y, raw[k].z, raw[k].w};
+        if (k < nv) {
+            unpack_words<DT, V>(w, xv[k]);
+        } else {
+#pragma unroll
+            for (int v = 0; v < V; ++v) xv[k][v] = 0.f;
+        }
+    }
+
+    // the lane's map over its steps: A_out = off + fac * A_in (steps past the row end are the
+    // identity; they follow every step of the row)
+    float be[KS];
+#pragma unroll
+    for (int k = 0; k < KS; ++k) {
+        const bool cut = k == 0 ? cut0 : bit(done, k - 1);
+        be[k] = k < nv ? (cut ? 0.f : decay) : 1.f;
+    }
+    float off[V];
+    float fac = be[0];
+#pragma unroll
+    for (int v = 0; v < V; ++v) off[v] = xv[0][v];
+#pragma unroll
+    for (int k = 1; k < KS; ++k) {
+#pragma unroll
+        for (int v = 0; v < V; ++v) off[v] = fmaf(be[k], off[v], xv[k][v]);
+        fac *= be[k];
+    }
+
+    // the wave's step groups: inclusive scan over lanes L apart, then the map of the groups
+    // before this lane's
+    float eo[V], ef = 1.f;
+#pragma unroll
+    for (int v = 0; v < V; ++v) eo[v] = 0.f;
+    if constexpr (S > 1) {
+#pragma unroll
+        for (int d = 1; d < S; d <<= 1) {
+            float po[V];
+#pragma unroll
+            for (int v = 0; v < V; ++v) po[v] = __shfl_up(off[v], d * L);
+            const float pf = __shfl_up(fac, d * L);
+            if (sg >= d) {
+#pragma unroll
+                for (int v = 0; v < V; ++v) off[v] = fmaf(fac, po[v], off[v]);
+                fac *= pf;
+            }
+        }
+        float po[V];
+#pragma unroll
+        for (int v = 0; v < V; ++v) po[v] = __shfl_up(off[v], L);
+        const float pf = __shfl_up(fac, L);
+        if (sg > 0) {
+#pragma unroll
+            for (int v = 0; v < V; ++v) eo[v] = po[v];
+            ef = pf;
+        }
+    }
+
+    // the waves before this one, composed from the row start
+    if (sg == S - 1) {
+#pragma unroll
+        for (int v = 0; v < V; ++v) s_off[wave * F + fg * V + v] = off[v];
+        if (fg == 0) s_fac[wave] = fac;
+    }
+    __syncthreads();
+    float X[V];
+#pragma unroll
+    for (int v = 0; v < V; ++v) X[v] = 0.f;
+    for (int j = 0; j < wave; ++j) {
+        const float f = s_fac[j];
+#pragma unroll
+        for (int v = 0; v < V; ++v) X[v] = fmaf(f, X[v], s_off[j * F + fg * V + v]);
+    }
+#pragma unroll
+    for (int v = 0; v < V; ++v) X[v] = fmaf(ef, X[v], eo[v]);
+
+    // the lane's steps, into the wave's slot (every lane of the wave has read its inputs from
+    // it): step k's features at float offset (sg * KS + k) * F + fg * V of the wave's outputs
+    wave_lds_sync();
+#pragma unroll
+    for (int k = 0; k < KS; ++k) {
+#pragma unroll
+        for (int v = 0; v < V; ++v) X[v] = fmaf(be[k], X[v], xv[k][v]);
+        const int piece = ((sg * KS + k) * F + fg * V) / 4;
+#pragma unroll
+        for (int i = 0; i < V / 4; ++i)
+            slot[piece + i] = f32x4{X[4 * i], X[4 * i + 1], X[4 * i + 2], X[4 * i + 3]};
+    }
+    wave_lds_sync();
+#pragma unroll
+    for (int i = 0; i < kPieces / kWave; ++i) {
+        const int pc = i * kWave + lane;
+        const int64_t p = wbase + 4 * int64_t(pc);
+        if (p < limit) __builtin_nontemporal_store(slot[pc], reinterpret_cast<f32x4*>(a.out0 + p));
+    }
+}
+
+namespace host {
+
+// Fewest rows that take the row kernel: its grid is one workgroup per row, and with fewer rows
+// the column scans, which also split time, fill the GPU better.
+constexpr int64_t kVecRowsMinRows = 256;
+// Dynamic LDS of one workgroup at most (the waves of a row are capped by it).
+constexpr size_t kVecRowsMaxLds = 64 * 1024;
+
+template <typename DT, bool TR, int L>
+void vec_rows_launch_l(const Args& a, int W, int word_flags, hipStream_t s) {
+    hipLaunchKernelGGL((vec_rows_kernel<DT, TR, L>), dim3(unsigned(a.N)), dim3(unsigned(W * kWave)),
+                       vec_rows_lds<DT>(W, int64_t(L) * (16 / int(sizeof(DT)))), s, a, word_flags);
+}
+
+// Launches the row kernel for a call of F features per step if it fits one (F a multiple of
+// the vector width with a power-of-two number of vectors up to 64, the row's steps within the
+// waves of 64 KB of LDS and more than half a wave's steps, at least kVecRowsMinRows rows; x
+// and z 16-byte aligned, checked by the caller) and returns whether it did.
+template <typename DT, bool TR>
+bool vec_rows_launch(const Args& a, int64_t F, int word_flags, hipStream_t s) {
+    constexpr int V = 16 / int(sizeof(DT));
+    if (F % V != 0) return false;
+    const int64_t L = F / V;
+    if (L > kWave || (L & (L - 1)) != 0) return false;
+    if (a.N < kVecRowsMinRows || a.N > INT32_MAX) return false;
+    const int64_t per_wave = (kWave / L) * kVecSteps;
+    int W = 1;
+    while (W < 16 && int64_t(W) * per_wave < a.T) W *= 2;
+    if (int64_t(W) * per_wave < a.T || vec_rows_lds<DT>(W, F) > kVecRowsMaxLds) return false;
+    // rows of at most half a wave's steps leave half its lanes idle: the column scans then win
+    // (16384 x 32 x 16 float32: 19.7 us here against 18.8)
+    if (2 * a.T <= per_wave) return false;
+    switch (L) {
+        case 1: vec_rows_launch_l<DT, TR, 1>(a, W, word_flags, s); break;
+        case 2: vec_rows_launch_l<DT, TR, 2>(a, W, word_flags, s); break;
+        case 4: vec_rows_launch_l<DT, TR, 4>(a, W, word_flags, s); break;
+        case 8: vec_rows_launch_l<DT, TR, 8>(a, W, word_flags, s); break;
+        case 16: vec_rows_launch_l<DT, TR, 16>(a, W, word_flags, s); break;
+        case 32: vec_rows_launch_l<DT, TR, 32>(a, W, word_flags, s); break;
+        default: vec_rows_launch_l<DT, TR, 64>(a, W, word_flags, s); break;
+    }
+    return true;
+}
+
+}  // namespace host
+}  // namespace rlcs

@@ -341,6 +341,29 @@ def test_elig_trace_vec_bf16_and_large():
     assert_parity({"z": z}, {"z": ref}, TOL["f32"], label="vec 4096x64x16")
 
 
+@pytest.mark.parametrize("N,T,F,dtype", [
+    (256, 2048, 4, "f32"), (257, 1999, 4, "f32"), (300, 65, 8, "f32"), (256, 511, 16, "f32"),
+    (256, 512, 16, "f32"), (260, 65, 16, "f32"), (256, 255, 32, "f32"), (256, 33, 64, "f32"),
+    (256, 64, 128, "f32"), (256, 31, 256, "f32"), (256, 32, 256, "f32"), (1000, 100, 16, "f32"),
+    (256, 1024, 8, "bf16"), (256, 257, 16, "bf16"), (256, 63, 64, "bf16"), (256, 16, 512, "bf16"),
+    (256, 5, 512, "bf16")])
+def test_elig_trace_vec_rows(N, T, F, dtype):
+    """Shapes the row kernel of vector traces takes (F a multiple of the vector width with a
+    power-of-two number of vectors, at least 256 rows, every wave count it uses, T a multiple
+    of 4 or not): with and without truncation, and with no flags at all."""
+    ro = workloads.make_vector_trace(N, T, F, seed=N + T + F, dtype=dtype, p_term=0.04,
+                                     p_trunc=0.04)
+    z, ref = run_vec(ro)
+    assert_parity({"z": z}, {"z": ref}, TOL[dtype], label=f"vec rows {N}x{T}x{F} {dtype}")
+    z, ref = run_vec(ro, trunc=False)
+    assert_parity({"z": z}, {"z": ref}, TOL[dtype], label=f"vec rows plain {N}x{T}x{F} {dtype}")
+    d = to_device(ro["x"], DEV)
+    z = rl.rlcs_elig_trace_vec(d, None, None, gamma=G, lam=L)
+    torch.cuda.synchronize()
+    ref = oracle.elig_trace_vec(ro["x"], None, None, gamma=G, lam=L)
+    assert_parity({"z": z}, {"z": ref}, TOL[dtype], label=f"vec rows no flags {N}x{T}x{F} {dtype}")
+
+
 def test_elig_trace_vec_one_feature_matches_scalar_entry_point():
     """F = 1 and the scalar row-major trace compute the same recurrence on the same data."""
     ro = workloads.make_vector_trace(33, 500, 1, seed=8)
