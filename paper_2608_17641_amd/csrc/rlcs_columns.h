@@ -180,7 +180,8 @@ struct ColChunk {
         if constexpr (kBack) {
             if (have_nbr && valid) Op::nbr_fix(a, nraw, nb);
         } else if constexpr (Op::kNbr > 0) {
-            nb[0] = (t0 > 0 && (pt || (TR && pr))) ? 1.f : 0.f;
+            // a missing termination array was read from the data instead: its byte is dropped
+            nb[0] = (t0 > 0 && ((a.term && pt) || (TR && pr))) ? 1.f : 0.f;
         }
     }
 

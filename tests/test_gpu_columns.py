@@ -307,6 +307,39 @@ def test_narrow_split_dealt_tiles(T, N, dtype):
     assert int(ws[8:12].view(torch.int32).item()) == 0
 
 
+@pytest.mark.parametrize("v", [0, 1, 2, 3, 4])
+@pytest.mark.parametrize("trunc", [False, True])
+def test_forward_column_scans_without_termination_array(v, trunc):
+    """Forward column scans given no termination array (truncation given or not): a kernel reads
+    a missing flag array from the data input instead and must drop what it reads there, also for
+    the previous step's flag that a lane takes from memory (once read as a flag, a data byte cut
+    the carry at every lane boundary). Time-major eligibility traces and prefix sums, and vector
+    traces on the column scans."""
+    T, N = 1000, 65
+    ro = workloads.make_rollout_time_major(T, N, seed=41, p_term=0.05, p_trunc=0.05)
+    d = device_tm(ro)
+    ws = rl.make_workspace_columns(N, T, DEV)
+    tr_d = d["trunc"].t() if trunc else None
+    tr_o = ro["trunc"] if trunc else None
+    with variant(v):
+        z = rl.rlcs_elig_trace_strided(d["x"].t(), None, tr_d, gamma=G, lam=L, ws=ws)
+        c = rl.rlcs_episodic_prefix_strided(d["x"].t(), None, tr_d, boundary="ends_at", ws=ws)
+        torch.cuda.synchronize()
+    zr = oracle.time_major(oracle.elig_trace, ro["x"], None, tr_o, gamma=G, lam=L)
+    cr = oracle.time_major(oracle.episodic_prefix, ro["x"], None, tr_o, boundary="ends_at")
+    assert_parity({"z": z.t()}, {"z": zr}, TOL["f32"], label=f"time-major elig, no term, v={v}")
+    assert_parity({"c": c.t()}, {"c": cr}, TOL["f32"], label=f"time-major prefix, no term, v={v}")
+    rv = workloads.make_vector_trace(300, 605, 4, seed=42, p_term=0.05, p_trunc=0.05)
+    wsv = rl.make_workspace_columns(300 * 4, 605, DEV)
+    with variant(v):
+        zv = rl.rlcs_elig_trace_vec(to_device(rv["x"], DEV), None,
+                                    to_device(rv["trunc"], DEV) if trunc else None,
+                                    gamma=G, lam=L, ws=wsv)
+        torch.cuda.synchronize()
+    zvr = oracle.elig_trace_vec(rv["x"], None, rv["trunc"] if trunc else None, gamma=G, lam=L)
+    assert_parity({"z": zv}, {"z": zvr}, TOL["f32"], label=f"vector traces, no term, v={v}")
+
+
 # ---------------------------------------------------------------- vector eligibility traces
 
 def run_vec(ro, *, trunc=True, ws=None):

@@ -2,8 +2,9 @@
 shape, dtype, flag density, layout (row-major, strided rows, time-major) and kernel variant,
 against the fp64 oracle on the same inputs. The cases cover what hand-picked shapes can miss:
 odd sizes, rows that straddle vectors and workgroups, row strides and time-major strides of any
-residue, optional inputs present or not. Each case prints itself before it runs.
-RLCS_RANDOM_CASES and RLCS_RANDOM_SEED (environment) draw a longer or another sweep."""
+residue, optional inputs (the termination array among them) present or not. A second sweep of 200 cases does the same for
+eligibility traces of F-vectors. Each case prints itself before it runs. RLCS_RANDOM_CASES,
+RLCS_RANDOM_VEC_CASES and RLCS_RANDOM_SEED (environment) draw longer or other sweeps."""
 import os
 
 import numpy as np
@@ -44,6 +45,9 @@ def _cases(n=int(os.environ.get("RLCS_RANDOM_CASES", "600")),
                         p=float(rng.choice([0.0, 0.001, 0.005, 0.05, 0.3])),
                         trunc=bool(rng.integers(0, 2)), boot=bool(rng.integers(0, 2)),
                         variant=int(rng.integers(0, 5)), seed=int(rng.integers(0, 2 ** 31))))
+        # one case in four has no termination array; taken from the case's seed, so that the
+        # draws of every other field stay as they were
+        out[-1]["term"] = out[-1]["seed"] % 4 != 0
     return out
 
 
@@ -68,21 +72,21 @@ def _run(name, d, trunc, boot, ws, strided):
     sfx = "_strided" if strided else ""
     f = lambda base: getattr(rl, "rlcs_" + base + sfx)
     if name == "gae":
-        return f("gae")(d["r"], d["v"], d["term"], tr, bv, bt, gamma=0.97, lam=0.9, ws=ws)
+        return f("gae")(d["r"], d["v"], d.get("term"), tr, bv, bt, gamma=0.97, lam=0.9, ws=ws)
     if name == "vtrace":
-        return f("vtrace")(d["r"], d["v"], d["log_rho"], d["term"], tr, bv, bt, gamma=0.97,
+        return f("vtrace")(d["r"], d["v"], d["log_rho"], d.get("term"), tr, bv, bt, gamma=0.97,
                            rho_bar=1.0, c_bar=0.9, ws=ws)
     if name == "retrace":
-        return f("retrace")(d["r"], d["q"], d["eq"], d["log_rho"], d["term"], tr, bv, bt,
+        return f("retrace")(d["r"], d["q"], d["eq"], d["log_rho"], d.get("term"), tr, bv, bt,
                             gamma=0.97, lam=0.9, c_bar=1.0, ws=ws)
     if name == "td_lambda":
-        return (f("td_lambda")(d["r"], d["v"], d["term"], tr, bv, bt, gamma=0.97, lam=0.9, ws=ws),)
+        return (f("td_lambda")(d["r"], d["v"], d.get("term"), tr, bv, bt, gamma=0.97, lam=0.9, ws=ws),)
     if name == "discounted":
-        return (f("discounted")(d["r"], d["term"], tr, bv, bt, gamma=0.97, ws=ws),)
+        return (f("discounted")(d["r"], d.get("term"), tr, bv, bt, gamma=0.97, ws=ws),)
     if name == "elig_trace":
-        return (f("elig_trace")(d["x"], d["term"], tr, gamma=0.97, lam=0.9, ws=ws),)
+        return (f("elig_trace")(d["x"], d.get("term"), tr, gamma=0.97, lam=0.9, ws=ws),)
     b = "starts_at" if name == "prefix_starts" else "ends_at"
-    return (f("episodic_prefix")(d["x"], d["term"], tr, boundary=b, ws=ws),)
+    return (f("episodic_prefix")(d["x"], d.get("term"), tr, boundary=b, ws=ws),)
 
 
 @pytest.mark.parametrize("case", _cases(), ids=lambda c: f"c{c['i']}")
@@ -91,6 +95,8 @@ def test_random_case(case):
     print(f"case {c}", flush=True)
     ro = workloads.make_rollout(c["N"], c["T"], c["seed"], dtype=c["dtype"], p_term=c["p"],
                                 p_trunc=c["p"])
+    if not c["term"]:
+        del ro["term"]
     d = {k: _view(to_device(v, DEV), c["layout"], c["pad"]) for k, v in ro.items()}
     strided = c["layout"] != "rows"
     ws = (rl.make_workspace_columns(c["N"], c["T"], DEV) if strided
@@ -105,4 +111,57 @@ def test_random_case(case):
                      c_bar=0.9 if c["name"] == "vtrace" else 1.0)
     got = {k: o for k, o in zip(OUT_KEYS[c["name"]], outs) if o is not None}
     assert_parity(got, {k: ref[k] for k in got}, TOL[c["dtype"]], label=f"random case {c['i']}")
+    assert int(ws[8:12].view(torch.int32).item()) == 0
+
+
+def _vec_cases(n=int(os.environ.get("RLCS_RANDOM_VEC_CASES", "200")),
+               seed=int(os.environ.get("RLCS_RANDOM_SEED", "20261202")) + 1):
+    """Vector eligibility traces: most cases shaped for the row kernel (at least 256 rows, F a
+    multiple of the vector width with a power-of-two number of vectors, T between half a wave's
+    steps and the most its waves hold), the rest any shape, under any variant."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for i in range(n):
+        dtype = ("f32", "bf16")[rng.integers(0, 2)]
+        if rng.random() < 0.7:
+            V = 4 if dtype == "f32" else 8
+            N = int(rng.choice([256, 257, 300, 513]))
+            F = V * int(rng.choice([1, 2, 4, 8, 16, 32, 64]))
+            per_wave = 64 // (F // V) * 4
+            most = per_wave * (8 if dtype == "f32" else 4)
+            T = int(rng.integers(per_wave // 2 + 1, most + 1))
+            variant = int(rng.choice([0, 0, 0, 0, 1, 3]))
+        else:
+            N = int(rng.choice([1, 7, 64, 255, 600]))
+            F = int(rng.choice([1, 3, 12, 16, 24, 40]))
+            T = int(rng.choice([1, 2, 3, 5, 31, 33, 64, 100, 129, 257, 1000, 2049]))
+            variant = int(rng.integers(0, 5))
+        T = max(1, min(T, 8_000_000 // (N * F)))  # at most 8M elements a case
+        out.append(dict(i=i, N=N, T=T, F=F, dtype=dtype, p=float(rng.choice([0.0, 0.005, 0.05, 0.3])),
+                        term=bool(rng.integers(0, 4) > 0), trunc=bool(rng.integers(0, 2)),
+                        variant=variant, seed=int(rng.integers(0, 2 ** 31))))
+    return out
+
+
+@pytest.mark.parametrize("case", _vec_cases(), ids=lambda c: f"v{c['i']}")
+def test_random_vec_case(case):
+    import oracle
+    c = case
+    print(f"case {c}", flush=True)
+    ro = workloads.make_vector_trace(c["N"], c["T"], c["F"], seed=c["seed"], dtype=c["dtype"],
+                                     p_term=c["p"], p_trunc=c["p"])
+    term = ro["term"] if c["term"] else None
+    trunc = ro["trunc"] if c["trunc"] else None
+    ws = rl.make_workspace_columns(c["N"] * c["F"], c["T"], DEV)
+    rl.testing_set_variant(c["variant"])
+    try:
+        z = rl.rlcs_elig_trace_vec(to_device(ro["x"], DEV),
+                                   None if term is None else to_device(term, DEV),
+                                   None if trunc is None else to_device(trunc, DEV),
+                                   gamma=0.97, lam=0.9, ws=ws)
+        torch.cuda.synchronize()
+    finally:
+        rl.testing_set_variant(0)
+    ref = oracle.elig_trace_vec(ro["x"], term, trunc, gamma=0.97, lam=0.9)
+    assert_parity({"z": z}, {"z": ref}, TOL[c["dtype"]], label=f"random vec case {c['i']}")
     assert int(ws[8:12].view(torch.int32).item()) == 0
