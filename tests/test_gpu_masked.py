@@ -32,16 +32,18 @@ def variant(v):
         rl.testing_set_variant(0)
 
 
-def run(ro, mask, *, trunc=True, boot=True, normalize=False, eps=1e-8, gamma=G, lam=L):
+def run(ro, mask, *, trunc=True, boot=True, normalize=False, eps=1e-8, gamma=G, lam=L, term=True):
     d = {k: to_device(v, DEV) for k, v in ro.items()}
+    te = d["term"] if term else None
     m = None if mask is None else to_device(mask, DEV)
     tr = d["trunc"] if trunc else None
     bv = d["bv"] if trunc else None
     bt = d["boot"] if boot else None
-    adv, ret = rl.rlcs_gae_masked(d["r"], d["v"], m, d["term"], tr, bv, bt, gamma=gamma, lam=lam,
+    adv, ret = rl.rlcs_gae_masked(d["r"], d["v"], m, te, tr, bv, bt, gamma=gamma, lam=lam,
                                   normalize=normalize, eps=eps)
     torch.cuda.synchronize()
-    a, r = oracle.gae_masked(ro["r"], ro["v"], mask, ro["term"], ro["trunc"] if trunc else None,
+    a, r = oracle.gae_masked(ro["r"], ro["v"], mask, ro["term"] if term else None,
+                             ro["trunc"] if trunc else None,
                              ro["bv"] if trunc else None, ro["boot"] if boot else None, gamma=gamma,
                              lam=lam)
     if normalize:
@@ -62,6 +64,11 @@ def test_gae_masked_random_masks(N, T, dtype):
     assert_parity(out, ref, TOL[dtype], label=f"unmasked {N}x{T} {dtype}")
     out, ref = run(ro, mask, trunc=False, boot=False)
     assert_parity(out, ref, TOL[dtype], label=f"masked plain {N}x{T} {dtype}")
+    for norm in (False, True):  # no termination array (with truncation, then without)
+        out, ref = run(ro, mask, term=False, normalize=norm)
+        assert_parity(out, ref, TOL[dtype], label=f"masked no term {N}x{T} {dtype} norm={norm}")
+    out, ref = run(ro, mask, term=False, trunc=False)
+    assert_parity(out, ref, TOL[dtype], label=f"masked no flags {N}x{T} {dtype}")
 
 
 def test_gae_masked_equals_gae_without_mask():
