@@ -317,17 +317,19 @@ def test_workspace_reused_across_shapes():
 
 # ------------------------------------------------------------------ full-form Retrace
 
-def _retrace_full_run(ro, *, trunc=True, boot=True, gamma=0.99, lam=0.95, c_bar=1.0, act=None):
+def _retrace_full_run(ro, *, trunc=True, boot=True, gamma=0.99, lam=0.95, c_bar=1.0, act=None,
+                      term=True):
     d = device_inputs(ro, DEV)
     if act is not None:
         d["actions"] = torch.from_numpy(act).to(DEV)
-    dl, qr = rl.rlcs_retrace_full(d["r"], d["q3"], d["pi3"], d["actions"], d["mu"], d["term"],
+    dl, qr = rl.rlcs_retrace_full(d["r"], d["q3"], d["pi3"], d["actions"], d["mu"],
+                                  d["term"] if term else None,
                                   d["trunc"] if trunc else None, d["bv"] if trunc else None,
                                   d["boot"] if boot else None, gamma=gamma, lam=lam, c_bar=c_bar)
     torch.cuda.synchronize()
     import oracle
     a = ro["actions"] if act is None else act
-    rd, rq = oracle.retrace_full(ro["r"], ro["q3"], ro["pi3"], a, ro["mu"], ro["term"],
+    rd, rq = oracle.retrace_full(ro["r"], ro["q3"], ro["pi3"], a, ro["mu"], ro["term"] if term else None,
                                  ro["trunc"] if trunc else None, ro["bv"] if trunc else None,
                                  ro["boot"] if boot else None, gamma=gamma, lam=lam, c_bar=c_bar)
     return {"delta": dl, "q_ret": qr}, {"delta": rd, "q_ret": rq}
@@ -340,6 +342,8 @@ def test_retrace_full_shapes(A, T):
     ro = workloads.make_retrace_full(N, T, A, seed=A * 1000 + T, p_term=0.05, p_trunc=0.05)
     out, ref = _retrace_full_run(ro, c_bar=0.9)
     assert_parity(out, ref, 1e-5, label=f"retrace_full A={A} T={T}")
+    out, ref = _retrace_full_run(ro, c_bar=0.9, term=False)
+    assert_parity(out, ref, 1e-5, label=f"retrace_full no term A={A} T={T}")
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
