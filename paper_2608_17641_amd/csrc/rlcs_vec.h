@@ -3,21 +3,23 @@
 // ends an episode, one beta per step shared by all F features.
 //
 // For F a multiple of the 16-byte vector width V (4 float32 or 8 bfloat16 features) with
-// L = F / V lanes per step a power of two up to 64, one workgroup of W waves scans one row of
-// the [N, T, F] input. Lane l of wave w holds features [V (l mod L), V (l mod L) + V) of the
-// kVecSteps = 4 consecutive steps from t0 = (w S + l / L) * 4, S = 64 / L step groups side by
-// side in a wave. The wave's inputs and outputs, S * 4 consecutive steps of the row, are
-// contiguous: where a step is under 128 bytes (L < 8), each wave loads its inputs as whole 1 KB
-// runs into its LDS slot, from which each lane takes one 16-byte vector per step (read straight
-// from memory, half a line per step at F = 16 float32: 4096 x 256 x 16 30.8 us against 27.0
-// staged; at F = 64 direct loads of whole lines 26.2 us against 27.2 staged). A lane's map
-// over its steps is V offsets and one shared factor; a wave scans its step groups by shuffles
-// across lanes L apart (log2 S rounds), the waves compose once through LDS (wave w's total maps
-// at [w][F] offsets and [w] factors) and each lane finishes its steps. The outputs pass back
-// through the slot so that each store instruction writes 1 KB of whole lines (pieces past the
-// row end are neither loaded nor stored). Flags: one 4-byte word per lane and array when
-// `word_flags` (T a multiple of 4, aligned flag arrays), otherwise one byte per step; lanes also
-// read the flags of the step before t0. Grid: N workgroups of W * 64 lanes.
+// L = F / V lanes per step a power of two up to 64, one workgroup of W waves scans R whole rows
+// of the [N, T, F] input as one range of R * T steps (contiguous in memory; the beta = 0 of each
+// row's first step keeps rows apart, so the scan needs no other boundary). Lane l of wave w
+// holds features [V (l mod L), V (l mod L) + V) of the kVecSteps = 4 consecutive steps from
+// t0 = (w S + l / L) * 4 of the range, S = 64 / L step groups side by side in a wave. The wave's
+// inputs and outputs, S * 4 consecutive steps, are contiguous: where a step is under 128 bytes
+// (L < 8), each wave loads its inputs as whole 1 KB runs into its LDS slot, from which each lane
+// takes one 16-byte vector per step (read straight from memory, half a line per step at F = 16
+// float32: 4096 x 256 x 16 30.8 us against 27.0 staged; at F = 64 direct loads of whole lines
+// 26.2 us against 27.2 staged). A lane's map over its steps is V offsets and one shared factor;
+// a wave scans its step groups by shuffles across lanes L apart (log2 S rounds), the waves
+// compose once through LDS (wave w's total maps at [w][F] offsets and [w] factors) and each lane
+// finishes its steps. The outputs pass back through the slot so that each store instruction
+// writes 1 KB of whole lines (pieces past the range's end are neither loaded nor stored). Flags:
+// one 4-byte word per lane and array when `word_flags` (T a multiple of 4, aligned flag arrays),
+// otherwise one byte per step; lanes also read the flags of the step before t0. Grid:
+// ceil(N / R) workgroups of W * 64 lanes.
 #pragma once
 
 #include "rlcs_dispatch.h"
@@ -35,7 +37,7 @@ constexpr size_t vec_rows_lds(int W, int64_t F) {
 }
 
 template <typename DT, bool TR, int L>
-__global__ void __launch_bounds__(16 * kWave) vec_rows_kernel(Args a, int word_flags) {
+__global__ void __launch_bounds__(16 * kWave) vec_rows_kernel(Args a, int R, int word_flags) {
     constexpr int V = 16 / int(sizeof(DT));
     constexpr int F = L * V;
     constexpr int S = kWave / L;
@@ -45,26 +47,30 @@ __global__ void __launch_bounds__(16 * kWave) vec_rows_kernel(Args a, int word_f
     const int W = int(blockDim.x) / kWave;
     const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
     const int fg = lane % L, sg = lane / L;
+    // the workgroup's rows [row0, row0 + R) as one range of E steps (a row's first step has
+    // beta = 0, so the scan needs no other row boundary)
     const int64_t T = a.T;
-    const int64_t frow = int64_t(blockIdx.x) * T;  // the row's first flag
-    const int64_t xrow = frow * F;                 // the row's first feature value
-    const int64_t t0 = (int64_t(wave) * S + sg) * KS;
+    const int64_t row0 = int64_t(blockIdx.x) * R;
+    const int64_t E = (min(row0 + R, a.N) - row0) * T;
+    const int64_t frow = row0 * T;  // the range's first flag
+    const int64_t xrow = frow * F;  // the range's first feature value
+    const int t0 = (wave * S + sg) * KS;  // the lane's first step in the range
     float* s_off = reinterpret_cast<float*>(s_vec + W * kPieces);
     float* s_fac = s_off + W * F;
     const float decay = a.p.gamma * a.p.lambda;
 
     // loads, all issued before the first use: the lane's inputs, then its flags and those of the
     // step before t0. Steps of fewer than 128 bytes (L < 8) are staged: the wave loads its span,
-    // S * KS consecutive steps of the row, as whole 1 KB runs (16-byte piece i * 64 + lane, up to
-    // the row end) into its slot, and each lane takes its pieces from there; longer steps are
-    // whole lines already and each lane loads its own vectors.
+    // S * KS consecutive steps of the range, as whole 1 KB runs (16-byte piece i * 64 + lane, up
+    // to the range's end) into its slot, and each lane takes its pieces from there; longer steps
+    // are whole lines already and each lane loads its own vectors.
     constexpr bool kStaged = L < 8;
     f32x4* slot = s_vec + wave * kPieces;
     const int64_t wbase = xrow + int64_t(wave) * S * KS * F;  // the wave's first element
-    const int64_t limit = xrow + T * F;                       // the row's end
+    const int64_t limit = xrow + E * F;                       // the range's end
     const DT* x = static_cast<const DT*>(a.in[0]);
-    int nv = 0;  // the lane's steps inside the row
-    if (t0 < T) nv = int(min(int64_t(KS), T - t0));
+    int nv = 0;  // the lane's steps inside the range
+    if (t0 < E) nv = int(min(int64_t(KS), E - t0));
     u32x4 raw[KS];
 #pragma unroll
     for (int i = 0; i < KS; ++i) {
@@ -73,8 +79,9 @@ __global__ void __launch_bounds__(16 * kWave) vec_rows_kernel(Args a, int word_f
             raw[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(x + p));
     }
     uint32_t done = 0;  // bit k: step t0 + k ends an episode
-    bool cut0 = true;   // nothing enters step t0 (the row start, or an episode ended before it)
-    if (t0 < T) {
+    bool cut0 = true;   // nothing enters step t0 (a row start, or an episode ended before it)
+    const int r0 = t0 % int(T);  // step t0's place in its row
+    if (t0 < E) {
         if (word_flags) {
             uint32_t tw[1] = {0u}, rw[1] = {0u};
             if (a.term) load_flag_words<4>(a.term, frow + t0, tw);
@@ -89,7 +96,7 @@ __global__ void __launch_bounds__(16 * kWave) vec_rows_kernel(Args a, int word_f
                 }
             }
         }
-        if (t0 > 0) cut0 = (a.term && a.term[frow + t0 - 1]) || (TR && a.trunc[frow + t0 - 1]);
+        if (r0 > 0) cut0 = (a.term && a.term[frow + t0 - 1]) || (TR && a.trunc[frow + t0 - 1]);
     }
     if constexpr (kStaged) {
 #pragma unroll
@@ -117,10 +124,12 @@ __global__ void __launch_bounds__(16 * kWave) vec_rows_kernel(Args a, int word_f
     // the lane's map over its steps: A_out = off + fac * A_in (steps past the row end are the
     // identity; they follow every step of the row)
     float be[KS];
+    int r = r0;  // step t0 + k's place in its row
 #pragma unroll
     for (int k = 0; k < KS; ++k) {
-        const bool cut = k == 0 ? cut0 : bit(done, k - 1);
+        const bool cut = k == 0 ? cut0 : (r == 0 || bit(done, k - 1));
         be[k] = k < nv ? (cut ? 0.f : decay) : 1.f;
+        r = r + 1 == int(T) ? 0 : r + 1;
     }
     float off[V];
     float fac = be[0];
@@ -203,44 +212,44 @@ __global__ void __launch_bounds__(16 * kWave) vec_rows_kernel(Args a, int word_f
 
 namespace host {
 
-// Fewest rows that take the row kernel: its grid is one workgroup per row, and with fewer rows
-// the column scans, which also split time, fill the GPU better.
-constexpr int64_t kVecRowsMinRows = 256;
+// Fewest workgroups of the row kernel: with fewer, the column scans, which also split time, fill
+// the GPU better.
+constexpr int64_t kVecRowsMinGroups = 256;
 // Dynamic LDS of one workgroup at most (the waves of a row are capped by it).
 constexpr size_t kVecRowsMaxLds = 64 * 1024;
 
 template <typename DT, bool TR, int L>
-void vec_rows_launch_l(const Args& a, int W, int word_flags, hipStream_t s) {
-    hipLaunchKernelGGL((vec_rows_kernel<DT, TR, L>), dim3(unsigned(a.N)), dim3(unsigned(W * kWave)),
-                       vec_rows_lds<DT>(W, int64_t(L) * (16 / int(sizeof(DT)))), s, a, word_flags);
+void vec_rows_launch_l(const Args& a, int64_t groups, int W, int R, int word_flags, hipStream_t s) {
+    hipLaunchKernelGGL((vec_rows_kernel<DT, TR, L>), dim3(unsigned(groups)), dim3(unsigned(W * kWave)),
+                       vec_rows_lds<DT>(W, int64_t(L) * (16 / int(sizeof(DT)))), s, a, R, word_flags);
 }
 
 // Launches the row kernel for a call of F features per step if it fits one (F a multiple of
-// the vector width with a power-of-two number of vectors up to 64, the row's steps within the
-// waves of 64 KB of LDS and more than half a wave's steps, at least kVecRowsMinRows rows; x
-// and z 16-byte aligned, checked by the caller) and returns whether it did.
+// the vector width with a power-of-two number of vectors up to 64, a row's steps within the
+// waves of 64 KB of LDS, at least kVecRowsMinGroups workgroups; x and z 16-byte aligned,
+// checked by the caller) and returns whether it did. W is the fewest waves (a power of two)
+// that hold a row, and a workgroup takes R = W * (steps per wave) / T whole rows.
 template <typename DT, bool TR>
 bool vec_rows_launch(const Args& a, int64_t F, int word_flags, hipStream_t s) {
     constexpr int V = 16 / int(sizeof(DT));
     if (F % V != 0) return false;
     const int64_t L = F / V;
     if (L > kWave || (L & (L - 1)) != 0) return false;
-    if (a.N < kVecRowsMinRows || a.N > INT32_MAX) return false;
     const int64_t per_wave = (kWave / L) * kVecSteps;
     int W = 1;
     while (W < 16 && int64_t(W) * per_wave < a.T) W *= 2;
     if (int64_t(W) * per_wave < a.T || vec_rows_lds<DT>(W, F) > kVecRowsMaxLds) return false;
-    // rows of at most half a wave's steps leave half its lanes idle: the column scans then win
-    // (16384 x 32 x 16 float32: 19.7 us here against 18.8)
-    if (2 * a.T <= per_wave) return false;
+    const int R = int(int64_t(W) * per_wave / a.T);
+    const int64_t groups = (a.N + R - 1) / R;
+    if (groups < kVecRowsMinGroups || groups > INT32_MAX) return false;
     switch (L) {
-        case 1: vec_rows_launch_l<DT, TR, 1>(a, W, word_flags, s); break;
-        case 2: vec_rows_launch_l<DT, TR, 2>(a, W, word_flags, s); break;
-        case 4: vec_rows_launch_l<DT, TR, 4>(a, W, word_flags, s); break;
-        case 8: vec_rows_launch_l<DT, TR, 8>(a, W, word_flags, s); break;
-        case 16: vec_rows_launch_l<DT, TR, 16>(a, W, word_flags, s); break;
-        case 32: vec_rows_launch_l<DT, TR, 32>(a, W, word_flags, s); break;
-        default: vec_rows_launch_l<DT, TR, 64>(a, W, word_flags, s); break;
+        case 1: vec_rows_launch_l<DT, TR, 1>(a, groups, W, R, word_flags, s); break;
+        case 2: vec_rows_launch_l<DT, TR, 2>(a, groups, W, R, word_flags, s); break;
+        case 4: vec_rows_launch_l<DT, TR, 4>(a, groups, W, R, word_flags, s); break;
+        case 8: vec_rows_launch_l<DT, TR, 8>(a, groups, W, R, word_flags, s); break;
+        case 16: vec_rows_launch_l<DT, TR, 16>(a, groups, W, R, word_flags, s); break;
+        case 32: vec_rows_launch_l<DT, TR, 32>(a, groups, W, R, word_flags, s); break;
+        default: vec_rows_launch_l<DT, TR, 64>(a, groups, W, R, word_flags, s); break;
     }
     return true;
 }

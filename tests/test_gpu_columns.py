@@ -379,11 +379,16 @@ def test_elig_trace_vec_bf16_and_large():
     (256, 512, 16, "f32"), (260, 65, 16, "f32"), (256, 255, 32, "f32"), (256, 33, 64, "f32"),
     (256, 64, 128, "f32"), (256, 31, 256, "f32"), (256, 32, 256, "f32"), (1000, 100, 16, "f32"),
     (256, 1024, 8, "bf16"), (256, 257, 16, "bf16"), (256, 63, 64, "bf16"), (256, 16, 512, "bf16"),
-    (256, 5, 512, "bf16")])
+    (256, 5, 512, "bf16"),
+    # short rows, several to a workgroup (the last one partly filled)
+    (601, 32, 16, "f32"), (3100, 5, 16, "f32"), (33000, 1, 8, "f32"), (600, 7, 64, "f32"),
+    (257, 33, 16, "f32"), (5001, 13, 4, "f32"), (300, 3, 512, "bf16"), (33001, 2, 8, "bf16"),
+    (1000, 9, 32, "bf16")])
 def test_elig_trace_vec_rows(N, T, F, dtype):
     """Shapes the row kernel of vector traces takes (F a multiple of the vector width with a
-    power-of-two number of vectors, at least 256 rows, every wave count it uses, T a multiple
-    of 4 or not): with and without truncation, and with no flags at all."""
+    power-of-two number of vectors, at least 256 workgroups, every wave count it uses, one row
+    or several short ones to a workgroup, T a multiple of 4 or not): with and without
+    truncation, and with no flags at all."""
     ro = workloads.make_vector_trace(N, T, F, seed=N + T + F, dtype=dtype, p_term=0.04,
                                      p_trunc=0.04)
     z, ref = run_vec(ro)

@@ -116,20 +116,24 @@ def test_random_case(case):
 
 def _vec_cases(n=int(os.environ.get("RLCS_RANDOM_VEC_CASES", "200")),
                seed=int(os.environ.get("RLCS_RANDOM_SEED", "20261202")) + 1):
-    """Vector eligibility traces: most cases shaped for the row kernel (at least 256 rows, F a
-    multiple of the vector width with a power-of-two number of vectors, T between half a wave's
-    steps and the most its waves hold), the rest any shape, under any variant."""
+    """Vector eligibility traces: most cases shaped for the row kernel (F a multiple of the vector
+    width with a power-of-two number of vectors, T up to the most its waves hold, enough rows for
+    256 workgroups or more), the rest any shape, under any variant."""
     rng = np.random.default_rng(seed)
     out = []
     for i in range(n):
         dtype = ("f32", "bf16")[rng.integers(0, 2)]
         if rng.random() < 0.7:
             V = 4 if dtype == "f32" else 8
-            N = int(rng.choice([256, 257, 300, 513]))
             F = V * int(rng.choice([1, 2, 4, 8, 16, 32, 64]))
             per_wave = 64 // (F // V) * 4
             most = per_wave * (8 if dtype == "f32" else 4)
-            T = int(rng.integers(per_wave // 2 + 1, most + 1))
+            if rng.random() < 0.4:  # at most a wave's steps: several rows to a workgroup
+                T = int(rng.integers(1, per_wave + 1))
+            else:
+                T = int(rng.integers(per_wave // 2 + 1, most + 1))
+            rows = max(1, per_wave // T)  # about the rows of a one-wave workgroup
+            N = int(rng.choice([256, 257, 300, 513])) * rows + int(rng.integers(0, rows))
             variant = int(rng.choice([0, 0, 0, 0, 1, 3]))
         else:
             N = int(rng.choice([1, 7, 64, 255, 600]))
