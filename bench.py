@@ -700,8 +700,8 @@ def run_extra(dev, only=""):
     for label, n_, t_, ld in (("sr_4096x256_ld320", 4096, 256, 320), ("sr_64x4096_ld4160", 64, 4096, 4160)):
         if label.startswith(only):
             run_strided_rows(label, n_, t_, ld, dev)
-    for label, n_, t_, f_ in (("vec_4096x256x16", 4096, 256, 16), ("vec_64x1024x256", 64, 1024, 256),
-                              ("vec_1x128x1M", 1, 128, 1 << 20)):
+    for label, n_, t_, f_ in (("vec_4096x256x16", 4096, 256, 16), ("vec_65536x8x16", 65536, 8, 16),
+                              ("vec_64x1024x256", 64, 1024, 256), ("vec_1x128x1M", 1, 128, 1 << 20)):
         if label.startswith(only):
             run_vector_trace(label, n_, t_, f_, dev)
     for label, n_, t_ in (("mt_64x4096", 64, 4096), ("mt_4096x256", 4096, 256),
