@@ -325,8 +325,11 @@ rlcs_status rlcs_episodic_prefix_strided(const void* x, const uint8_t* term, con
  *   term, trunc  [N, T] as above (one flag per step, for every feature)
  *   z        [N, T, F] float32 out: traces
  * Sizes: N, F >= 0, 0 <= T <= 2^30, N*T*F representable; any of them 0 is a no-op.
- * Workspace: rlcs_workspace_size_columns(N * F, T) bytes, as for the strided calls (used
- * when N*F is below about 64K).                                                           */
+ * Calls whose F is a multiple of the 16-byte vector width (4 float32 or 8 bfloat16 features)
+ * with a power-of-two number of vectors up to 64, short enough rows (F = 16 float32: up to 512
+ * steps) and enough of them for 256 workgroups run along rows, x and z 16-byte aligned; the
+ * others scan the N*F feature columns. Workspace: rlcs_workspace_size_columns(N * F, T) bytes,
+ * as for the strided calls (used by the column scans when N*F is below about 64K).        */
 rlcs_status rlcs_elig_trace_vec(const void* x, const uint8_t* term, const uint8_t* trunc,
                                 float* z, int64_t N, int64_t T, int64_t F, float gamma,
                                 float lambda, rlcs_dtype dtype, void* ws, size_t ws_bytes,
