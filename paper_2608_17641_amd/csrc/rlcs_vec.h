@@ -215,8 +215,9 @@ namespace host {
 // Fewest workgroups of the row kernel: with fewer, the column scans, which also split time, fill
 // the GPU better.
 constexpr int64_t kVecRowsMinGroups = 256;
-// Dynamic LDS of one workgroup at most (the waves of a row are capped by it).
-constexpr size_t kVecRowsMaxLds = 64 * 1024;
+// Dynamic LDS of one workgroup at most (the waves of a row are capped by it): what one CU of
+// the MI355X holds, 160 KB.
+constexpr size_t kVecRowsMaxLds = 160 * 1024;
 
 template <typename DT, bool TR, int L>
 void vec_rows_launch_l(const Args& a, int64_t groups, int W, int R, int word_flags, hipStream_t s) {
@@ -225,8 +226,8 @@ void vec_rows_launch_l(const Args& a, int64_t groups, int W, int R, int word_fla
 }
 
 // Launches the row kernel for a call of F features per step if it fits one (F a multiple of
-// the vector width with a power-of-two number of vectors up to 64, a row's steps within the
-// waves of 64 KB of LDS, at least kVecRowsMinGroups workgroups; x and z 16-byte aligned,
+// the vector width with a power-of-two number of vectors up to 64, a row's steps within 16
+// waves whose LDS fits one CU, at least kVecRowsMinGroups workgroups; x and z 16-byte aligned,
 // checked by the caller) and returns whether it did. W is the fewest waves (a power of two)
 // that hold a row, and a workgroup takes R = W * (steps per wave) / T whole rows.
 template <typename DT, bool TR>

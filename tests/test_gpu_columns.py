@@ -383,7 +383,10 @@ def test_elig_trace_vec_bf16_and_large():
     # short rows, several to a workgroup (the last one partly filled)
     (601, 32, 16, "f32"), (3100, 5, 16, "f32"), (33000, 1, 8, "f32"), (600, 7, 64, "f32"),
     (257, 33, 16, "f32"), (5001, 13, 4, "f32"), (300, 3, 512, "bf16"), (33001, 2, 8, "bf16"),
-    (1000, 9, 32, "bf16")])
+    (1000, 9, 32, "bf16"),
+    # 8 and 16 waves to a row (LDS beyond 64 KB)
+    (256, 1024, 16, "f32"), (256, 777, 16, "f32"), (256, 4096, 4, "f32"), (256, 64, 256, "f32"),
+    (256, 2048, 8, "bf16"), (256, 1000, 16, "bf16")])
 def test_elig_trace_vec_rows(N, T, F, dtype):
     """Shapes the row kernel of vector traces takes (F a multiple of the vector width with a
     power-of-two number of vectors, at least 256 workgroups, every wave count it uses, one row

@@ -127,7 +127,7 @@ def _vec_cases(n=int(os.environ.get("RLCS_RANDOM_VEC_CASES", "200")),
             V = 4 if dtype == "f32" else 8
             F = V * int(rng.choice([1, 2, 4, 8, 16, 32, 64]))
             per_wave = 64 // (F // V) * 4
-            most = per_wave * (8 if dtype == "f32" else 4)
+            most = per_wave * 16
             if rng.random() < 0.4:  # at most a wave's steps: several rows to a workgroup
                 T = int(rng.integers(1, per_wave + 1))
             else:

@@ -15,7 +15,7 @@ in float64, the last workgroup's partial range included. Nothing here runs on a 
 import numpy as np
 import pytest
 
-WAVE, KS, MAX_LDS, MIN_GROUPS = 64, 4, 64 * 1024, 256
+WAVE, KS, MAX_LDS, MIN_GROUPS = 64, 4, 160 * 1024, 256
 
 
 def lds_bytes(W, F, V):
@@ -41,7 +41,8 @@ def plan(T, F, V, N=1 << 20):
     return L, S, W, R
 
 
-SHAPES = [(2048, 4, 4), (1999, 4, 4), (65, 8, 4), (1, 8, 4), (3, 16, 4), (511, 16, 4),
+SHAPES = [(4096, 4, 4), (2048, 4, 4), (1999, 4, 4), (1024, 16, 4), (777, 16, 4), (2048, 8, 8),
+          (1000, 16, 8), (64, 256, 4), (65, 8, 4), (1, 8, 4), (3, 16, 4), (511, 16, 4),
           (512, 16, 4), (65, 16, 4), (32, 16, 4), (255, 32, 4), (33, 64, 4), (5, 64, 4),
           (64, 128, 4), (31, 256, 4), (32, 256, 4), (100, 16, 4), (256, 16, 4), (1024, 8, 8),
           (257, 16, 8), (63, 64, 8), (16, 512, 8), (5, 512, 8), (2, 512, 8), (7, 8, 8)]
@@ -63,7 +64,8 @@ def test_plan_declines():
     assert plan(256, 16, 4, N=255) is None  # too few workgroups
     assert plan(32, 16, 4, N=510) is None  # two rows a workgroup: 256 workgroups need 511 rows
     assert plan(32, 16, 4, N=511) is not None
-    assert plan(513, 16, 4) is None        # needs 16 waves: over the LDS bound
+    assert plan(1025, 16, 4) is None       # needs 32 waves
+    assert plan(4096, 4, 4) is not None and plan(4097, 4, 4) is None
     assert plan(65, 256, 4) is None        # L = 64: 4 steps per wave, 16 waves too many
     assert plan(256, 1024, 8) is None      # L = 128
 
