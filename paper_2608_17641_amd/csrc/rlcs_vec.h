@@ -36,8 +36,16 @@ constexpr size_t vec_rows_lds(int W, int64_t F) {
     return size_t(W) * kWave * kVecSteps * V * 4 + size_t(W) * size_t(F) * 4 + size_t(W) * 4;
 }
 
+// Eight waves per SIMD for float32 inputs with L > 1 (the compiler keeps the kernel within 64
+// VGPRs, no spills; left to itself it took 74-82 and ran 5 waves): fp32 4096 x 256 x 16
+// 26.5 -> 25.7 us, 65536 x 8 x 16 15.4 -> 13.0, 2048 x 1024 x 16 64.8 -> 58.7, 1024 x 2048 x 8
+// 35.5 -> 31.9. bfloat16 inputs and L = 1 stay unconstrained: held to 64 VGPRs they spill.
+template <typename DT, int L>
+constexpr int vec_rows_waves_per_eu() { return sizeof(DT) == 4 && L > 1 ? 8 : 1; }
+
 template <typename DT, bool TR, int L>
-__global__ void __launch_bounds__(16 * kWave) vec_rows_kernel(Args a, int R, int word_flags) {
+__global__ void __launch_bounds__(16 * kWave) __attribute__((amdgpu_waves_per_eu(vec_rows_waves_per_eu<DT, L>())))
+vec_rows_kernel(Args a, int R, int word_flags) {
     constexpr int V = 16 / int(sizeof(DT));
     constexpr int F = L * V;
     constexpr int S = kWave / L;
