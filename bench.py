@@ -641,9 +641,12 @@ def run_extra(dev, only=""):
                  ("gae", "td_lambda")))
     plan.append(("flat_bf16_16384x200", 16384, 200, "bf16", dict(p_term=0.005, p_trunc=0.005), True, True, 0.99,
                  0.95, ("gae", "retrace")))
-    # rows of a length that is not a multiple of the vector width: the lane-by-lane vector path
+    # rows of a length that is not a multiple of the vector width: the flat rows kernel (four or
+    # sixteen waves) where a workgroup's rows can start and end on vector boundaries
     plan.append(("ragged_4096x255", 4096, 255, "f32", dict(p_term=0.02, p_trunc=0.01), True, True, 0.99, 0.95,
                  ("gae", "vtrace", "elig_trace")))
+    plan.append(("ragged_4096x499", 4096, 499, "f32", dict(p_term=0.02, p_trunc=0.01), True, True, 0.99, 0.95,
+                 ("gae", "vtrace")))
     plan.append(("ragged_1024x1001", 1024, 1001, "f32", dict(p_term=0.02, p_trunc=0.01), True, True, 0.99, 0.95,
                  ("gae",)))
     plan.append(("ragged_bf16_16384x100", 16384, 100, "bf16", dict(p_term=0.005, p_trunc=0.005), True, True, 0.99,

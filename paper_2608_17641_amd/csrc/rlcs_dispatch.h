@@ -124,7 +124,8 @@ struct Plan {
     bool pad;             // rows kernel, vector path: lanes outside the range or in row gaps skip
     int wave_rows_log2T;  // >= 0: wave_rows_kernel (rows tile a wave exactly; T = 2^log2T)
     int flat_R;           // > 0: flat_rows_kernel with this many whole rows per workgroup
-    uint32_t flat_magic;  // ceil(2^22 / T): a lane's row in its range by multiply-shift
+    int flat_W;           // its waves per workgroup (4, or 16 for float32 rows)
+    uint32_t flat_magic;  // ceil(2^flat_shift(flat_W) / T): a lane's row by multiply-shift
 };
 
 template <class Op, typename DT, bool VEC, bool TR, int W, bool PAD = false>
@@ -148,9 +149,16 @@ template <class Op, typename DT, bool VEC, bool TR>
 rlcs_status launch(const Args& a, const Plan& p, hipStream_t stream) {
     if constexpr (VEC && Op::kStaged == 0) {
         if (p.flat_R > 0) {
-            hipLaunchKernelGGL((flat_rows_kernel<Op, DT, Width<DT>::K, TR, kSmallWaves>),
-                               dim3(unsigned((a.N + p.flat_R - 1) / p.flat_R)), dim3(kSmallWaves * kWave),
-                               0, stream, a, p.flat_R, p.flat_magic);
+            const dim3 grid(unsigned((a.N + p.flat_R - 1) / p.flat_R));
+            if constexpr (sizeof(DT) == 4) {
+                if (p.flat_W == kLargeWaves) {
+                    hipLaunchKernelGGL((flat_rows_kernel<Op, DT, Width<DT>::K, TR, kLargeWaves>), grid,
+                                       dim3(kLargeWaves * kWave), 0, stream, a, p.flat_R, p.flat_magic);
+                    return hipGetLastError() == hipSuccess ? RLCS_OK : RLCS_ERR_LAUNCH;
+                }
+            }
+            hipLaunchKernelGGL((flat_rows_kernel<Op, DT, Width<DT>::K, TR, kSmallWaves>), grid,
+                               dim3(kSmallWaves * kWave), 0, stream, a, p.flat_R, p.flat_magic);
             return hipGetLastError() == hipSuccess ? RLCS_OK : RLCS_ERR_LAUNCH;
         }
         if (p.wave_rows_log2T >= 0) {
@@ -293,6 +301,7 @@ rlcs_status dispatch_dt(Args& a, bool has_trunc, void* ws, size_t ws_bytes, hipS
     }
     p.wave_rows_log2T = -1;
     p.flat_R = 0;
+    p.flat_W = kSmallWaves;
     // Dense rows up to one four-wave chunk (float32) or one wave (bfloat16), except powers of
     // two that tile a wave: the flat rows kernel. Measured against
     // the rows kernel (C harness, cold): GAE 4096x192 fp32 5.05 -> 4.62 us, 4096x252 5.97 -> 5.22,
@@ -307,10 +316,19 @@ rlcs_status dispatch_dt(Args& a, bool has_trunc, void* ws, size_t ws_bytes, hipS
         int64_t gcd = K, b = T % K;
         while (b) { const int64_t r = gcd % b; gcd = b; b = r; }
         const int64_t step = K / gcd;  // rows per vector-aligned range
-        const int64_t R = E_small / T / step * step;
-        if (R > 0) {
+        int64_t R = E_small / T / step * step;
+        int W = kSmallWaves;
+        // float32 rows too long for `step` of them in four waves (T not a multiple of K, more
+        // than 256 steps): sixteen waves hold 4096 steps
+        if (R == 0 && sizeof(DT) == 4) {
+            R = E_large / T / step * step;
+            W = kLargeWaves;
+        }
+        const int64_t magic = ((int64_t(1) << flat_shift(W)) + T - 1) / T;
+        if (R > 0 && (int64_t(W) * kWave * K - 1) * magic < (int64_t(1) << 32)) {
             p.flat_R = int(R);
-            p.flat_magic = uint32_t(((int64_t(1) << 22) + T - 1) / T);
+            p.flat_W = W;
+            p.flat_magic = uint32_t(magic);
             if ((N + R - 1) / R > INT32_MAX) return RLCS_ERR_INVALID_ARG;
         }
     }
@@ -385,6 +403,7 @@ rlcs_status dispatch_strided_rows(Args& a, int64_t period, rlcs_dtype dtype, boo
         p.lds_bytes = 0;
         p.wave_rows_log2T = -1;
         p.flat_R = 0;
+        p.flat_W = kSmallWaves;
         // Vector path, lane by lane (lanes whose steps reach into a gap or past the range go
         // element-wise): T >= K, data and outputs 16-byte aligned, flags K-byte aligned.
         bool vec = a.T >= K;

@@ -997,9 +997,14 @@ __global__ void __launch_bounds__(WPG * kWave) wave_rows_kernel(Args a, int log2
 // its lanes as wave_rows_kernel does, the waves compose through LDS once, and lane 0 of a wave
 // reads its carry-source neighbour from memory with its other loads (it lies in the next or
 // previous wave's span unless a row edge comes first). A lane's row and step come from its
-// offset q in the range by a multiply and a shift: floor(q * magic / 2^22) = floor(q / T) for
-// q < W*64*K <= 2048 and T < 2048, magic = ceil(2^22 / T), since q * (magic - 2^22 / T) / 2^22 <
-// 1 / 2048. No chunk loop, no element-wise path. Grid: ceil(N / R) workgroups.
+// offset q in the range by a multiply and a shift: floor(q * magic / 2^s) = floor(q / T) with
+// magic = ceil(2^s / T), since q * (magic - 2^s / T) / 2^s < 1 / T whenever q * T < 2^s:
+// s = flat_shift(W), 22 for four waves (q < 1024 fp32 or 2048 bf16 steps, T below 2048) and
+// 26 for sixteen (q < 4096 fp32 steps, T up to 1024), with q * magic below 2^32 (the host
+// takes sixteen waves only for rows of more than 256 steps). No chunk loop, no element-wise
+// path. Grid: ceil(N / R) workgroups.
+constexpr int flat_shift(int W) { return W > 4 ? 26 : 22; }
+
 template <class Op, typename DT, int K, bool TR, int W>
 __global__ void __launch_bounds__(W * kWave) flat_rows_kernel(Args a, int R, uint32_t magic) {
     static_assert(Op::kStaged == 0, "staged policies run on the rows kernel");
@@ -1040,7 +1045,7 @@ __global__ void __launch_bounds__(W * kWave) flat_rows_kernel(Args a, int R, uin
             if (lane == 0) Op::template nbr_load_raw<DT>(a, in ? pn : pc, nraw);
         }
     }
-    const int r_in = int((uint32_t(q) * magic) >> 22);
+    const int r_in = int((uint32_t(q) * magic) >> flat_shift(W));
     const int64_t row = live ? row0 + r_in : 0;
     const int64_t t = live ? int64_t(q - r_in * int(T)) : 0;
     // the row edge among the lane's K steps, if any (at most one: T >= K): backward the last

@@ -1,38 +1,55 @@
 """CPU emulation of flat_rows_kernel's lane geometry (csrc/rlcs_kernels.h; plan in
 csrc/rlcs_dispatch.h), restated from the kernel. For dense rows of T steps, K < T <= 256*K
 (float32, K = 4) or 64*K (bfloat16, K = 8), not a power of two of at most 64*K steps, N*T a
-multiple of K: workgroup g owns rows [g*R, g*R + R), R the most whole rows in 256*K steps that is
-a multiple of K / gcd(T, K),
-the range [lo, hi) = [g*R*T, min(g*R + R, N)*T); lane l of wave w holds the K steps at offset
-q = (64*w + g(l))*K (g(l) = 63 - l backward, l forward), live when lo + q < hi; its row is
-g*R + floor(q * magic / 2^22), magic = ceil(2^22 / T), and its step q - T*floor(q / T).
-Checked: the multiply-shift division is exact for every (K, T, q) the kernel sees; every range
-starts and ends on a vector boundary and the live lanes cover every step exactly once; a lane
-holds at most one row edge, where the kernel's edge computation puts it, and the per-row
-value it reads is that edge step's row's; the neighbour a live
-lane takes (lane l-1 through the wave shift, or lane 0's read at p0 + K backward / p0 - 1
-forward) is the adjacent step whenever the lane's carry-source edge step is not a row edge, and
-lane 0's read address lies inside the range then; and the bf16 whole-line stores of each wave ([lo + 512*w, ...) up to
-hi) cover exactly the live lanes' outputs. Nothing here runs on a GPU."""
+multiple of K: workgroup g of W waves owns rows [g*R, g*R + R), R the most whole rows in W*64*K
+steps that is a multiple of K / gcd(T, K) (W = 4, or 16 for float32 rows of which no such R fits
+four waves), the range [lo, hi) = [g*R*T, min(g*R + R, N)*T); lane l of wave w holds the K steps
+at offset q = (64*w + g(l))*K (g(l) = 63 - l backward, l forward), live when lo + q < hi; its row
+is g*R + floor(q * magic / 2^s), magic = ceil(2^s / T) with s = 22 for four waves and 26 for
+sixteen, and its step q - T*floor(q / T). Checked: the multiply-shift division is exact and its
+32-bit product does not overflow for every (K, T, q) the kernel sees; sixteen waves are taken
+only where four hold no aligned range; every range starts and ends on a vector boundary and the
+live lanes cover every step exactly once; a lane holds at most one row edge, where the kernel's
+edge computation puts it, and the per-row value it reads is that edge step's row's; the
+neighbour a live lane takes (lane l-1 through the wave shift, or lane 0's read at p0 + K
+backward / p0 - 1 forward) is the adjacent step whenever the lane's carry-source edge step is
+not a row edge, and lane 0's read address lies inside the range then; and the bf16 whole-line
+stores of each wave ([lo + 512*w, ...) up to hi) cover exactly the live lanes' outputs. Nothing
+here runs on a GPU."""
 import pytest
 
-WAVE, W = 64, 4
+WAVE = 64
 
 
-def magic(T):
-    return ((1 << 22) + T - 1) // T
+def shift(W):
+    return 26 if W > 4 else 22
+
+
+def magic(T, W=4):
+    return ((1 << shift(W)) + T - 1) // T
 
 
 def flat_max(K):
-    return W * WAVE * K if K == 4 else WAVE * K
+    return 4 * WAVE * K if K == 4 else WAVE * K
+
+
+def plan(T, K):
+    """(W, R) as the dispatcher picks them: R the most whole rows that fit W*64*K steps, a
+    multiple of K / gcd(T, K) so that the range starts and ends on vector boundaries; four waves,
+    or sixteen for float32 rows of which no such R fits four; (4, 0): not taken."""
+    from math import gcd
+    step = K // gcd(T, K)
+    R = 4 * WAVE * K // T // step * step
+    W = 4
+    if R == 0 and K == 4:
+        R, W = 16 * WAVE * K // T // step * step, 16
+    if R > 0 and (W * WAVE * K - 1) * magic(T, W) >= 1 << 32:
+        R = 0
+    return W, R
 
 
 def rows_per_group(T, K):
-    """R as the dispatcher picks it: the most whole rows that fit W*64*K steps, a multiple of
-    K / gcd(T, K) so that the range starts and ends on vector boundaries (0: not taken)."""
-    from math import gcd
-    step = K // gcd(T, K)
-    return W * WAVE * K // T // step * step
+    return plan(T, K)[1]
 
 
 def is_flat(T, K, N=None):
@@ -47,14 +64,24 @@ def flat_shapes(K):
 @pytest.mark.parametrize("K", [4, 8])
 def test_multiply_shift_division_is_exact(K):
     for T in flat_shapes(K):
-        m = magic(T)
+        W = plan(T, K)[0]
+        m = magic(T, W)
         for q in range(0, W * WAVE * K):
-            assert (q * m) >> 22 == q // T, (K, T, q)
+            assert (q * m) >> shift(W) == q // T, (K, T, q)
         assert (W * WAVE * K - 1) * m < 2 ** 32  # no overflow of the 32-bit product
 
 
+def test_sixteen_waves_only_where_four_hold_no_aligned_range():
+    for T in flat_shapes(4):
+        W, R = plan(T, 4)
+        if W == 16:
+            assert T > 256 and T % 4 != 0 and 4 * WAVE * 4 // T // (4 // __import__("math").gcd(T, 4)) == 0
+    assert plan(1001, 4) == (16, 4) and plan(499, 4) == (16, 8) and plan(1023, 4) == (16, 4)
+    assert plan(255, 4) == (4, 4) and plan(250, 4)[0] == 4
+
+
 def lanes(N, T, K, backward):
-    R = rows_per_group(T, K)
+    W, R = plan(T, K)
     for wg in range(-(-N // R)):
         row0 = wg * R
         lo, hi = row0 * T, min(row0 + R, N) * T
@@ -64,14 +91,15 @@ def lanes(N, T, K, backward):
                 q = (wave * WAVE + g) * K
                 p0 = lo + q
                 live = p0 < hi
-                r_in = (q * magic(T)) >> 22
+                r_in = (q * magic(T, W)) >> shift(W)
                 yield dict(wg=wg, wave=wave, lane=lane, g=g, lo=lo, hi=hi, p0=p0, live=live,
                            row=row0 + r_in, t=q - r_in * T)
 
 
 @pytest.mark.parametrize("K", [4, 8])
 @pytest.mark.parametrize("backward", [False, True])
-@pytest.mark.parametrize("N,T", [(1, 12), (7, 20), (5, 24), (33, 40), (100, 96), (13, 136),
+@pytest.mark.parametrize("N,T", [(8, 1001), (12, 499), (8, 1023), (4, 1001), (16, 259), (6, 514),
+                                 (1, 12), (7, 20), (5, 24), (33, 40), (100, 96), (13, 136),
                                  (9, 192), (64, 200), (3, 240), (17, 252), (11, 264), (4, 504),
                                  (50, 100), (5, 300), (7, 500), (6, 512), (3, 1000), (5, 1020),
                                  (4, 1024), (8, 255), (16, 255), (12, 129), (8, 100), (16, 101),
@@ -79,6 +107,7 @@ def lanes(N, T, K, backward):
 def test_flat_lanes_cover_rows_and_neighbours(N, T, K, backward):
     if not is_flat(T, K, N):
         pytest.skip("not a flat-rows shape for this K")
+    W = plan(T, K)[0]
     L = list(lanes(N, T, K, backward))
     seen = set()
     where = {}

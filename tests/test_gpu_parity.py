@@ -149,7 +149,8 @@ def test_rows_flat(T, dtype):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("T", [5, 9, 33, 100, 101, 129, 250, 251, 255, 257, 300, 499, 1001, 1023])
+@pytest.mark.parametrize("T", [5, 9, 33, 100, 101, 129, 250, 251, 255, 257, 300, 499, 514, 771, 1001,
+                               1022, 1023])
 def test_rows_flat_ragged(T, dtype):
     """Rows whose length is not a multiple of K: the flat rows kernel where a workgroup's rows
     start and end on vector boundaries (a row edge inside a lane's K steps), the lane-by-lane
