@@ -302,7 +302,7 @@ rlcs_status dispatch_dt(Args& a, bool has_trunc, void* ws, size_t ws_bytes, hipS
     p.wave_rows_log2T = -1;
     p.flat_R = 0;
     p.flat_W = kSmallWaves;
-    // Dense rows up to one four-wave chunk (float32) or one wave (bfloat16), except powers of
+    // Dense rows up to one sixteen-wave chunk (float32) or one wave (bfloat16), except powers of
     // two that tile a wave: the flat rows kernel. Measured against
     // the rows kernel (C harness, cold): GAE 4096x192 fp32 5.05 -> 4.62 us, 4096x252 5.97 -> 5.22,
     // 4096x500 10.04 -> 8.68, 4096x1000 16.59 -> 15.48, 4096x1024 16.13 -> 15.54; bf16 16384x200
@@ -310,7 +310,12 @@ rlcs_status dispatch_dt(Args& a, bool has_trunc, void* ws, size_t ws_bytes, hipS
     // (16384x1000 45.4 -> 44.2, 16384x2048 82.3 -> 83.4) and keep the rows kernel.
     // Rows whose length is not a multiple of K take it as well when a workgroup's rows can start
     // and end on vector boundaries (R a multiple of K / gcd(T, K), N*T a multiple of K).
-    const int64_t flat_max = sizeof(DT) == 4 ? E_small : int64_t(kWave) * K;
+    // float32 rows up to one sixteen-wave chunk (4096 steps) take it too, in sixteen-wave
+    // ranges where four waves hold none, in place of one sixteen-wave rows-kernel workgroup per
+    // row (same protocol, GAE): 4096x2000 36.2 -> 29.9 us, 2048x3000 32.7 -> 24.7, 1024x4096
+    // 19.6 -> 17.1, 4096x1500 33.0 -> 24.7, 2048x2048 19.7 -> 17.0, 8192x1100 44.1 -> 34.0;
+    // 64x4096 even (4.45 -> 4.43).
+    const int64_t flat_max = sizeof(DT) == 4 ? E_large : int64_t(kWave) * K;
     if (Op::kStaged == 0 && !p.split && vec && T > K && T <= flat_max && (N * T) % K == 0 &&
         !((T & (T - 1)) == 0 && T <= int64_t(kWave) * K)) {
         int64_t gcd = K, b = T % K;
@@ -318,8 +323,8 @@ rlcs_status dispatch_dt(Args& a, bool has_trunc, void* ws, size_t ws_bytes, hipS
         const int64_t step = K / gcd;  // rows per vector-aligned range
         int64_t R = E_small / T / step * step;
         int W = kSmallWaves;
-        // float32 rows too long for `step` of them in four waves (T not a multiple of K, more
-        // than 256 steps): sixteen waves hold 4096 steps
+        // float32 rows too long for `step` of them in four waves (more than 1024 steps, or more
+        // than 256 that are not a multiple of K): sixteen waves hold 4096 steps
         if (R == 0 && sizeof(DT) == 4) {
             R = E_large / T / step * step;
             W = kLargeWaves;

@@ -1000,7 +1000,7 @@ __global__ void __launch_bounds__(WPG * kWave) wave_rows_kernel(Args a, int log2
 // offset q in the range by a multiply and a shift: floor(q * magic / 2^s) = floor(q / T) with
 // magic = ceil(2^s / T), since q * (magic - 2^s / T) / 2^s < 1 / T whenever q * T < 2^s:
 // s = flat_shift(W), 22 for four waves (q < 1024 fp32 or 2048 bf16 steps, T below 2048) and
-// 26 for sixteen (q < 4096 fp32 steps, T up to 1024), with q * magic below 2^32 (the host
+// 26 for sixteen (q < 4096 fp32 steps, T up to 4096), with q * magic below 2^32 (the host
 // takes sixteen waves only for rows of more than 256 steps). No chunk loop, no element-wise
 // path. Grid: ceil(N / R) workgroups.
 constexpr int flat_shift(int W) { return W > 4 ? 26 : 22; }

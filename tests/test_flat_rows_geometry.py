@@ -1,9 +1,10 @@
 """CPU emulation of flat_rows_kernel's lane geometry (csrc/rlcs_kernels.h; plan in
-csrc/rlcs_dispatch.h), restated from the kernel. For dense rows of T steps, K < T <= 256*K
+csrc/rlcs_dispatch.h), restated from the kernel. For dense rows of T steps, K < T <= 1024*K
 (float32, K = 4) or 64*K (bfloat16, K = 8), not a power of two of at most 64*K steps, N*T a
 multiple of K: workgroup g of W waves owns rows [g*R, g*R + R), R the most whole rows in W*64*K
 steps that is a multiple of K / gcd(T, K) (W = 4, or 16 for float32 rows of which no such R fits
-four waves), the range [lo, hi) = [g*R*T, min(g*R + R, N)*T); lane l of wave w holds the K steps
+four waves: rows of more than 1024 steps, or more than 256 not a multiple of K), the range
+[lo, hi) = [g*R*T, min(g*R + R, N)*T); lane l of wave w holds the K steps
 at offset q = (64*w + g(l))*K (g(l) = 63 - l backward, l forward), live when lo + q < hi; its row
 is g*R + floor(q * magic / 2^s), magic = ceil(2^s / T) with s = 22 for four waves and 26 for
 sixteen, and its step q - T*floor(q / T). Checked: the multiply-shift division is exact and its
@@ -30,7 +31,7 @@ def magic(T, W=4):
 
 
 def flat_max(K):
-    return 4 * WAVE * K if K == 4 else WAVE * K
+    return 16 * WAVE * K if K == 4 else WAVE * K
 
 
 def plan(T, K):
@@ -75,7 +76,7 @@ def test_sixteen_waves_only_where_four_hold_no_aligned_range():
     for T in flat_shapes(4):
         W, R = plan(T, 4)
         if W == 16:
-            assert T > 256 and T % 4 != 0 and 4 * WAVE * 4 // T // (4 // __import__("math").gcd(T, 4)) == 0
+            assert T > 256 and 4 * WAVE * 4 // T // (4 // __import__("math").gcd(T, 4)) == 0
     assert plan(1001, 4) == (16, 4) and plan(499, 4) == (16, 8) and plan(1023, 4) == (16, 4)
     assert plan(255, 4) == (4, 4) and plan(250, 4)[0] == 4
 
@@ -99,6 +100,7 @@ def lanes(N, T, K, backward):
 @pytest.mark.parametrize("K", [4, 8])
 @pytest.mark.parametrize("backward", [False, True])
 @pytest.mark.parametrize("N,T", [(8, 1001), (12, 499), (8, 1023), (4, 1001), (16, 259), (6, 514),
+                                 (5, 2000), (3, 3000), (2, 4096), (7, 1100), (4, 1500), (9, 2048),
                                  (1, 12), (7, 20), (5, 24), (33, 40), (100, 96), (13, 136),
                                  (9, 192), (64, 200), (3, 240), (17, 252), (11, 264), (4, 504),
                                  (50, 100), (5, 300), (7, 500), (6, 512), (3, 1000), (5, 1020),

@@ -128,18 +128,20 @@ def test_rows_tiling_a_wave(T, dtype):
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("T", [8, 12, 20, 24, 36, 40, 72, 100, 132, 136, 192, 200, 240, 252, 264,
-                               300, 384, 500, 504, 512, 600, 1000, 1020, 1024])
+                               300, 384, 500, 504, 512, 600, 1000, 1020, 1024, 1028, 1100, 1500,
+                               2000, 2048, 3000, 4092, 4096])
 def test_rows_flat(T, dtype):
-    """Dense rows of a multiple of K steps, at most one four-wave chunk (float32) or one wave
+    """Dense rows of a multiple of K steps, at most one sixteen-wave chunk (float32) or one wave
     (bfloat16), except powers of two that tile a wave: the flat rows kernel, floor(256*K / T)
-    whole rows per four-wave workgroup, rows straddling waves. Row counts that leave the last
+    whole rows per four-wave workgroup, or floor(1024*K / T) per sixteen-wave one for float32
+    rows of more than 1024 steps, rows straddling waves. Row counts that leave the last
     workgroup partial, one row, and many rows; with and without truncation and bootstrap."""
     K = 4 if dtype == "f32" else 8
-    flat_max = 256 * K if dtype == "f32" else 64 * K
+    flat_max = 1024 * K if dtype == "f32" else 64 * K
     if T % K or T <= K or T > flat_max or ((T & (T - 1)) == 0 and T <= 64 * K):
         pytest.skip("not a flat-rows shape for this dtype")
-    R = 256 * K // T
-    for N in (1, R + 1, 3 * R - 1, 4099):
+    R = 256 * K // T or 1024 * K // T
+    for N in (1, R + 1, 3 * R - 1, 4099 if T <= 256 * K else 601):
         for i, name in enumerate(ESTIMATORS):
             ro = make_inputs(name, N, T, seed=N * 13 + T + i, dtype=dtype, p_term=0.05, p_trunc=0.05)
             check(name, ro, gamma=0.97, lam=0.9, label=f"{N}x{T} {dtype}")
